@@ -1,0 +1,295 @@
+"""A page-level model of the shared KV store, in plain Python.
+
+TEST INFRASTRUCTURE ONLY (see the package docstring).
+
+What the paper fixes
+--------------------
+* The auxiliary thread runs on the *shared* context: it does not duplicate the
+  KV cache of the conversation; its only extra storage is its own transient
+  tokens, discarded when it finishes (§3.4 "Storage Costs"; Algorithm 1,
+  Phase 2 ``C_aux <- C + p``).
+* ``clear_kv(Delta_ids)`` removes the tokens of the named tool responses from
+  the cache after the main thread's turn has finished (Algorithm 1, Phase 1;
+  §3.1 step 4 "Synchronization").
+* The context grows by appends: the main thread's response R and the tool
+  output O (Algorithm 1, Phase 3).
+
+Readings adopted where the paper is silent (also listed in the design notes)
+-------------------------------------------------------------------------
+* Storage is paged: P tokens per page; a sequence (main thread or auxiliary
+  branch) is a list of page ids, a length and a position counter.
+* Page allocation takes the lowest free page id first; an operation that needs
+  several pages takes them one at a time, in the order they appear in the
+  sequence's page list.
+* Fork at F: the child aliases the parent's first F // P pages (refcount + 1,
+  no copy).  If F % P != 0 the child gets one new page holding a copy of slots
+  [0, F % P) of the parent's page F // P.  The child's position counter is the
+  parent's if F equals the parent's length, otherwise the position of the
+  parent's token F.  The child inherits the cursor spans that end at or before F.
+* Eviction is out of place: with f the first evicted index and fp = f // P,
+  pages [0, fp) are kept as they are; ceil(L'/P) - fp new pages are allocated
+  (before any old page is released) and filled with the kept tokens
+  [fp*P, L') gathered from the old pages; then every old page from fp on
+  loses one reference and is freed at zero.  Pages still referenced by another
+  live branch survive, so evicting one branch never changes what another
+  branch attends to.
+* Positions are carried, never recomputed: a kept token keeps its position and
+  new tokens continue from the counter.
+* Validation happens before any change: a failing call leaves the model as it
+  was.  Error kinds: Invalid, NoPages, UnknownSeq, UnknownCursor, SpanError.
+* Sequence handles are small integers, lowest free handle first.
+"""
+
+from __future__ import annotations
+
+import heapq
+import math
+
+import numpy as np
+
+from . import evict as _evict
+
+
+class OracleError(Exception):
+    code = 0
+
+
+class Invalid(OracleError):
+    code = 1
+
+
+class NoPages(OracleError):
+    code = 2
+
+
+class UnknownSeq(OracleError):
+    code = 3
+
+
+class UnknownCursor(OracleError):
+    code = 4
+
+
+class SpanError(OracleError):
+    code = 5
+
+
+class Seq:
+    __slots__ = ("pages", "length", "next_pos", "pos", "spans", "parent")
+
+    def __init__(self):
+        self.pages = []
+        self.length = 0
+        self.next_pos = 0
+        self.pos = []  # logical position of each token
+        self.spans = {}  # cursor id -> (start, end), current coordinates
+        self.parent = -1
+
+
+class PageModel:
+    """Page allocator, refcounts and sequences; optionally the K/V/pos data.
+
+    With ``with_data`` the physical pools are held as float64 arrays
+    K, V: [num_pages, P, NL, Hkv, D] and pos: [num_pages, P].
+    """
+
+    def __init__(self, num_pages, page_size, max_seqs, max_pages_per_seq,
+                 layers=1, kv_heads=1, head_dim=1, with_data=False):
+        self.num_pages = int(num_pages)
+        self.P = int(page_size)
+        self.max_seqs = int(max_seqs)
+        self.max_pages_per_seq = int(max_pages_per_seq)
+        self.layers, self.kv_heads, self.head_dim = layers, kv_heads, head_dim
+        self.refcount = np.zeros(self.num_pages, dtype=np.int64)
+        self._free = list(range(self.num_pages))
+        heapq.heapify(self._free)
+        self.seqs = {}
+        self.peak_pages = 0
+        self.with_data = with_data
+        if with_data:
+            shape = (self.num_pages, self.P, layers, kv_heads, head_dim)
+            self.K = np.zeros(shape)
+            self.V = np.zeros(shape)
+            self.POS = np.zeros((self.num_pages, self.P), dtype=np.int64)
+
+    # -- allocator ---------------------------------------------------------
+    def free_pages(self):
+        return len(self._free)
+
+    def live_pages(self):
+        return self.num_pages - len(self._free)
+
+    def _alloc(self):
+        page = heapq.heappop(self._free)
+        assert self.refcount[page] == 0
+        self.refcount[page] = 1
+        self.peak_pages = max(self.peak_pages, self.live_pages())
+        return page
+
+    def _unref(self, page):
+        self.refcount[page] -= 1
+        assert self.refcount[page] >= 0
+        if self.refcount[page] == 0:
+            heapq.heappush(self._free, page)
+            return 1
+        return 0
+
+    def _seq(self, h):
+        if h not in self.seqs:
+            raise UnknownSeq(f"unknown sequence {h}")
+        return self.seqs[h]
+
+    # -- sequences ---------------------------------------------------------
+    def seq_create(self):
+        for h in range(self.max_seqs):
+            if h not in self.seqs:
+                self.seqs[h] = Seq()
+                return h
+        raise Invalid("no free sequence handle")
+
+    def append(self, h, n, k_new=None, v_new=None):
+        """Append n tokens.  k_new, v_new: [NL, n, Hkv, D] (with data)."""
+        seq = self._seq(h)
+        if n < 0:
+            raise Invalid("negative token count")
+        new_len = seq.length + n
+        want = math.ceil(new_len / self.P)
+        if want > self.max_pages_per_seq:
+            raise Invalid("sequence would exceed its page-list capacity")
+        if want - len(seq.pages) > self.free_pages():
+            raise NoPages("not enough free pages")
+        if seq.length % self.P:
+            assert self.refcount[seq.pages[-1]] == 1, "partial tail page must be private"
+        for i in range(n):
+            if seq.length % self.P == 0:
+                seq.pages.append(self._alloc())
+            page, slot = seq.pages[seq.length // self.P], seq.length % self.P
+            if self.with_data:
+                self.K[page, slot] = np.asarray(k_new, dtype=np.float64)[:, i]
+                self.V[page, slot] = np.asarray(v_new, dtype=np.float64)[:, i]
+                self.POS[page, slot] = seq.next_pos
+            seq.pos.append(seq.next_pos)
+            seq.next_pos += 1
+            seq.length += 1
+
+    def span_mark(self, h, cursor, start, end):
+        """Register cursor ``cursor`` as the tokens [start, end) of sequence h."""
+        seq = self._seq(h)
+        if cursor < 0 or cursor in seq.spans:
+            raise Invalid("cursor id negative or already registered")
+        if not (0 <= start <= end <= seq.length):
+            raise SpanError("span outside the sequence")
+        if end > start:
+            for s, e in seq.spans.values():
+                if e > s and s < end and start < e:
+                    raise SpanError("span overlaps a registered span")
+        seq.spans[cursor] = (int(start), int(end))
+
+    def fork(self, parent, fork_len):
+        """Open an auxiliary branch on the first ``fork_len`` tokens."""
+        par = self._seq(parent)
+        if not (0 <= fork_len <= par.length):
+            raise Invalid("fork point outside the parent")
+        if len(self.seqs) >= self.max_seqs:
+            raise Invalid("no free sequence handle")
+        tail = fork_len % self.P
+        if tail and self.free_pages() < 1:
+            raise NoPages("no page for the fork's tail copy")
+        child_h = self.seq_create()
+        child = self.seqs[child_h]
+        full = fork_len // self.P
+        for page in par.pages[:full]:
+            self.refcount[page] += 1
+        child.pages = list(par.pages[:full])
+        if tail:
+            page = self._alloc()
+            src = par.pages[full]
+            if self.with_data:
+                self.K[page, :tail] = self.K[src, :tail]
+                self.V[page, :tail] = self.V[src, :tail]
+                self.POS[page, :tail] = self.POS[src, :tail]
+            child.pages.append(page)
+        child.length = fork_len
+        child.pos = list(par.pos[:fork_len])
+        child.next_pos = par.next_pos if fork_len == par.length else par.pos[fork_len]
+        child.spans = {c: se for c, se in par.spans.items() if se[1] <= fork_len}
+        child.parent = parent
+        return child_h
+
+    def release(self, h):
+        """Drop a branch: every page loses one reference."""
+        seq = self._seq(h)
+        freed = sum(self._unref(p) for p in seq.pages)
+        del self.seqs[h]
+        return freed
+
+    def evict(self, h, cursor_ids):
+        """``clear_kv``: remove the tokens of ``cursor_ids`` from sequence h."""
+        seq = self._seq(h)
+        ids = list(dict.fromkeys(int(c) for c in cursor_ids))
+        for c in ids:
+            if c not in seq.spans:
+                raise UnknownCursor(f"cursor {c} not registered")
+        spans = sorted(seq.spans[c] for c in ids if seq.spans[c][1] > seq.spans[c][0])
+        stats = dict(tokens_removed=0, tokens_moved=0, pages_allocated=0,
+                     pages_freed=0, first_evicted=seq.length)
+        if not spans:
+            for c in ids:
+                del seq.spans[c]
+            return stats
+        keep, _dst, src_of, new_len, first = _evict.plan(seq.length, spans)
+        fp = first // self.P
+        n_new = math.ceil(new_len / self.P) - fp
+        if n_new > self.free_pages():
+            raise NoPages("not enough free pages for the compacted tail")
+        new_pages = [self._alloc() for _ in range(n_new)]
+        if self.with_data:
+            for j in range(fp * self.P, new_len):
+                src = int(src_of[j])
+                sp, ss = seq.pages[src // self.P], src % self.P
+                dp, ds = new_pages[j // self.P - fp], j % self.P
+                self.K[dp, ds] = self.K[sp, ss]
+                self.V[dp, ds] = self.V[sp, ss]
+                self.POS[dp, ds] = self.POS[sp, ss]
+        freed = sum(self._unref(p) for p in seq.pages[fp:])
+        seq.pages = seq.pages[:fp] + new_pages
+        seq.pos = [p for p, k in zip(seq.pos, keep) if k]
+        old_len = seq.length
+        seq.length = new_len
+        for c in ids:
+            del seq.spans[c]
+        seq.spans = {c: _evict.shift_span(s, e, spans) for c, (s, e) in seq.spans.items()}
+        stats.update(tokens_removed=old_len - new_len,
+                     tokens_moved=new_len - fp * self.P,
+                     pages_allocated=n_new, pages_freed=freed, first_evicted=first)
+        return stats
+
+    # -- inspection --------------------------------------------------------
+    def page_table(self, h):
+        return list(self._seq(h).pages)
+
+    def info(self, h):
+        seq = self._seq(h)
+        return dict(length=seq.length, next_pos=seq.next_pos, n_pages=len(seq.pages),
+                    parent=seq.parent, n_spans=len(seq.spans))
+
+    def spans(self, h):
+        return dict(self._seq(h).spans)
+
+    def view(self, h):
+        """Logical view of sequence h: (K [L, NL, Hkv, D], V, pos [L]).
+
+        Without data only pos is returned (K and V are None)."""
+        seq = self._seq(h)
+        if not self.with_data:
+            return None, None, np.asarray(seq.pos, dtype=np.int64)
+        idx_p = [seq.pages[i // self.P] for i in range(seq.length)]
+        idx_s = [i % self.P for i in range(seq.length)]
+        k = self.K[idx_p, idx_s] if seq.length else np.zeros((0,) + self.K.shape[2:])
+        v = self.V[idx_p, idx_s] if seq.length else np.zeros((0,) + self.V.shape[2:])
+        pos = self.POS[idx_p, idx_s] if seq.length else np.zeros(0, dtype=np.int64)
+        return k, v, pos
+
+    def stats(self):
+        return dict(live_pages=self.live_pages(), peak_pages=self.peak_pages,
+                    free_pages=self.free_pages(), live_seqs=len(self.seqs))

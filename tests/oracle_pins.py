@@ -1,0 +1,491 @@
+"""Checks that pin the oracle to facts other than itself.
+
+Each ``check_*`` raises AssertionError when the oracle (as currently bound in
+the ``oracle`` package) breaks a fact fixed by the mathematics or by the
+paper's statement of the method:
+
+* closed forms (uniform weights, two keys, a single key),
+* invariants (weights sum to one, key-permutation invariance),
+* an independent library routine (``torch.softmax`` in float64),
+* brute force over tiny inputs (every subset of spans; a naive list model of
+  the context for append / fork / evict / release),
+* hand-worked page tables under the stated allocation convention.
+
+``test_oracle_pins.py`` runs them on the oracle as written;
+``test_oracle_mutants.py`` plants plausible mistakes in the oracle and shows
+each is caught by at least one check.
+"""
+
+from __future__ import annotations
+
+import copy
+import itertools
+import math
+
+import numpy as np
+import torch
+
+from oracle import attention as att
+from oracle import evict as ev
+from oracle import pages as pg
+
+
+def _rand_qkv(rng, hq, hkv, d, n):
+    q = rng.standard_normal((hq, d))
+    k = rng.standard_normal((n, hkv, d))
+    v = rng.standard_normal((n, hkv, d))
+    return q, k, v
+
+
+# --------------------------------------------------------------------------
+# attention
+# --------------------------------------------------------------------------
+def check_weights_sum_to_one(seed=1):
+    rng = np.random.default_rng(seed)
+    for hq, hkv, d, n in [(4, 1, 16, 37), (8, 2, 8, 5), (2, 2, 32, 300)]:
+        q, k, v = _rand_qkv(rng, hq, hkv, d, n)
+        p = att.weights(q, k, 1 / math.sqrt(d), hq // hkv)
+        assert np.all(p >= 0)
+        assert np.max(np.abs(p.sum(axis=1) - 1.0)) <= 1e-12
+        ones = np.ones_like(v)
+        out = att.attention(q, k, ones, 1 / math.sqrt(d), hq // hkv)
+        assert np.max(np.abs(out - 1.0)) <= 1e-14
+
+
+def check_single_key_returns_v(seed=2):
+    rng = np.random.default_rng(seed)
+    for hq, hkv, d in [(4, 1, 64), (8, 2, 8), (1, 1, 3)]:
+        q, k, v = _rand_qkv(rng, hq, hkv, d, 1)
+        out = att.attention(q, k, v, 0.37, hq // hkv)
+        for h in range(hq):
+            assert np.array_equal(out[h], v[0, h // (hq // hkv)])
+
+
+def check_textbook_softmax(seed=3):
+    """Equal to torch.softmax(scale q K^T) V in float64, K/V expanded per
+    query head with repeat_interleave (consecutive heads share a KV head)."""
+    rng = np.random.default_rng(seed)
+    for hq, hkv, d, n, scale in [(4, 1, 64, 50, 1 / 8), (8, 2, 8, 17, 0.5),
+                                 (6, 3, 16, 64, 1.7), (2, 2, 4, 1, 1.0),
+                                 (32, 8, 128, 40, 1 / math.sqrt(128))]:
+        q, k, v = _rand_qkv(rng, hq, hkv, d, n)
+        g = hq // hkv
+        out = att.attention(q, k, v, scale, g)
+        kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        qt = torch.from_numpy(q)[:, None, :]
+        logits = scale * torch.bmm(qt, kt.transpose(1, 2).contiguous())
+        ref = torch.bmm(torch.softmax(logits, dim=-1), vt)[:, 0, :].numpy()
+        assert np.max(np.abs(out - ref)) <= 1e-12, np.max(np.abs(out - ref))
+
+
+def check_uniform_closed_form(seed=4):
+    """q = 0 gives equal scores, so the output is the mean of the values."""
+    rng = np.random.default_rng(seed)
+    q, k, v = _rand_qkv(rng, 4, 2, 8, 9)
+    out = att.attention(np.zeros_like(q), k, v, 0.3, 2)
+    for h in range(4):
+        assert np.max(np.abs(out[h] - v[:, h // 2].mean(axis=0))) <= 1e-14
+
+
+def check_two_key_closed_form():
+    """Two keys with scores a, b: weight of the first is 1 / (1 + e^(b - a))."""
+    d = 2
+    q = np.array([[1.0, 0.0]])
+    k = np.array([[[2.0, 5.0]], [[-1.0, 3.0]]])
+    v = np.array([[[1.0, 0.0]], [[0.0, 1.0]]])
+    scale = 0.5
+    a, b = scale * 2.0, scale * -1.0
+    w1 = 1.0 / (1.0 + math.exp(b - a))
+    out = att.attention(q, k, v, scale, 1)
+    assert abs(out[0, 0] - w1) <= 1e-15 and abs(out[0, 1] - (1 - w1)) <= 1e-15
+    assert d == out.shape[1]
+
+
+def check_permutation_invariance(seed=5):
+    rng = np.random.default_rng(seed)
+    q, k, v = _rand_qkv(rng, 8, 2, 16, 33)
+    perm = rng.permutation(33)
+    a = att.attention(q, k, v, 0.25, 4)
+    b = att.attention(q, k[perm], v[perm], 0.25, 4)
+    assert np.max(np.abs(a - b)) <= 1e-13
+
+
+def check_masked_semantics(seed=6):
+    """Masking keys equals dropping them (general inputs, to round-off), and a
+    fully masked head returns zeros."""
+    rng = np.random.default_rng(seed)
+    q, k, v = _rand_qkv(rng, 4, 1, 8, 20)
+    mask = rng.integers(0, 2, 20).astype(np.uint8)
+    mask[3] = 1
+    a = att.masked_attention(q, k, v, mask, 0.4, 4)
+    keep = mask.astype(bool)
+    b = att.attention(q, k[keep], v[keep], 0.4, 4)
+    assert np.max(np.abs(a - b)) <= 1e-14
+    z = att.masked_attention(q, k, v, np.zeros(20, np.uint8), 0.4, 4)
+    assert np.array_equal(z, np.zeros_like(z))
+
+
+def check_merge_identity(seed=7):
+    """Partials of any partition of the keys merge to direct attention; empty
+    parts are ignored."""
+    rng = np.random.default_rng(seed)
+    for trial in range(12):
+        hq, hkv, d, n = [(4, 1, 8, 40), (8, 2, 16, 23), (2, 1, 4, 3)][trial % 3]
+        q, k, v = _rand_qkv(rng, hq, hkv, d, n)
+        g = hq // hkv
+        direct = att.attention(q, k, v, 0.6, g)
+        labels = rng.integers(0, 5, n)
+        parts = []
+        for s in range(6):  # part 5 is always empty
+            sel = labels == s
+            parts.append(att.partial(q, k[sel], v[sel], 0.6, g))
+        merged = att.merge(parts)
+        assert np.max(np.abs(merged - direct)) <= 1e-13
+    empty = att.partial(q, k[:0], v[:0], 0.6, g)
+    assert np.all(empty[0] == -np.inf) and np.all(empty[1] == 0)
+    assert np.array_equal(att.merge([empty, empty]), np.zeros((hq, d)))
+
+
+# --------------------------------------------------------------------------
+# eviction index arithmetic
+# --------------------------------------------------------------------------
+def check_scan_and_inverse(seed=8):
+    rng = np.random.default_rng(seed)
+    for n in [0, 1, 2, 17, 100]:
+        for _ in range(5):
+            spans = []
+            cut = sorted(rng.integers(0, n + 1, 6).tolist())
+            for i in range(0, 6, 2):
+                spans.append((cut[i], cut[i + 1]))
+            keep = ev.keep_mask(n, spans)
+            inside = [any(s <= i < e for s, e in spans) for i in range(n)]
+            assert keep.tolist() == [0 if x else 1 for x in inside]
+            dst = ev.exclusive_scan(keep)
+            want = [0] + list(itertools.accumulate(keep.tolist()))[:-1] if n else []
+            assert dst.tolist() == want
+            src_of = ev.inverse_map(keep, dst)
+            assert src_of.tolist() == np.flatnonzero(keep).tolist()
+            _, _, _, n_kept, first = ev.plan(n, spans)
+            assert n_kept == int(keep.sum()) == len(src_of)
+            assert first == (inside.index(True) if any(inside) else n)
+
+
+def check_span_shift(seed=9):
+    rng = np.random.default_rng(seed)
+    for _ in range(50):
+        n = 40
+        cuts = sorted(rng.choice(np.arange(n + 1), 8, replace=False).tolist())
+        spans = [(cuts[i], cuts[i + 1]) for i in range(0, 8, 2)]
+        gone = [spans[i] for i in range(4) if rng.random() < 0.5]
+        stay = [s for s in spans if s not in gone]
+        tokens = [i for i in range(n) if not any(s <= i < e for s, e in gone)]
+        for s, e in stay:
+            ns, ne = ev.shift_span(s, e, gone)
+            assert tokens[ns:ne] == list(range(s, e))
+
+
+# --------------------------------------------------------------------------
+# page model
+# --------------------------------------------------------------------------
+class ListModel:
+    """Naive context model: each sequence is a Python list of token records
+    (K row, V row, position); fork copies a prefix, evict filters."""
+
+    def __init__(self):
+        self.seqs = {}
+        self.next_pos = {}
+        self.spans = {}
+
+    def create(self, h):
+        self.seqs[h], self.next_pos[h], self.spans[h] = [], 0, {}
+
+    def append(self, h, k_new, v_new):
+        for i in range(k_new.shape[1]):
+            self.seqs[h].append((k_new[:, i].copy(), v_new[:, i].copy(), self.next_pos[h]))
+            self.next_pos[h] += 1
+
+    def fork(self, parent, f, child):
+        self.seqs[child] = list(self.seqs[parent][:f])
+        par = self.seqs[parent]
+        self.next_pos[child] = self.next_pos[parent] if f == len(par) else par[f][2]
+        self.spans[child] = {c: se for c, se in self.spans[parent].items() if se[1] <= f}
+
+    def evict(self, h, cursors):
+        gone = set()
+        for c in cursors:
+            s, e = self.spans[h][c]
+            gone.update(range(s, e))
+        old = self.seqs[h]
+        # a span's new coordinates: count the surviving tokens before each end
+        survivors_before = np.cumsum([0] + [0 if i in gone else 1 for i in range(len(old))])
+        self.spans[h] = {c: (int(survivors_before[s]), int(survivors_before[e]))
+                         for c, (s, e) in self.spans[h].items() if c not in cursors}
+        self.seqs[h] = [t for i, t in enumerate(old) if i not in gone]
+
+    def view(self, h):
+        toks = self.seqs[h]
+        if not toks:
+            return None
+        return (np.stack([t[0] for t in toks]), np.stack([t[1] for t in toks]),
+                np.array([t[2] for t in toks]))
+
+
+def _state(model):
+    return copy.deepcopy((model.refcount.tolist(), sorted(model._free),
+                          {h: (s.pages, s.length, s.next_pos, s.pos, s.spans, s.parent)
+                           for h, s in model.seqs.items()}, model.peak_pages))
+
+
+def check_against_list_model(seed=10, n_ops=60):
+    """Random op sequences: the page model's logical views equal a naive list
+    model's, for page sizes 1, 2, 4 and 16."""
+    rng = np.random.default_rng(seed)
+    nl, hkv, d = 2, 2, 3
+    for page in [1, 2, 4, 16]:
+        model = pg.PageModel(num_pages=400, page_size=page, max_seqs=6,
+                             max_pages_per_seq=400, layers=nl, kv_heads=hkv,
+                             head_dim=d, with_data=True)
+        ref = ListModel()
+        next_cursor = 0
+        h0 = model.seq_create()
+        ref.create(h0)
+        for _ in range(n_ops):
+            live = sorted(model.seqs)
+            op = rng.choice(["append", "append", "mark", "fork", "evict", "release"])
+            h = int(rng.choice(live))
+            if op == "append":
+                n = int(rng.integers(0, 2 * page + 3))
+                k = rng.standard_normal((nl, n, hkv, d))
+                v = rng.standard_normal((nl, n, hkv, d))
+                model.append(h, n, k, v)
+                ref.append(h, k, v)
+            elif op == "mark":
+                length = model.info(h)["length"]
+                s = int(rng.integers(0, length + 1))
+                e = int(rng.integers(s, length + 1))
+                try:
+                    model.span_mark(h, next_cursor, s, e)
+                    ref.spans[h][next_cursor] = (s, e)
+                except pg.SpanError:
+                    pass
+                next_cursor += 1
+            elif op == "fork" and len(live) < 6:
+                f = int(rng.integers(0, model.info(h)["length"] + 1))
+                c = model.fork(h, f)
+                ref.fork(h, f, c)
+            elif op == "evict":
+                cur = list(model.spans(h))
+                pick = [c for c in cur if rng.random() < 0.5]
+                model.evict(h, pick)
+                ref.evict(h, pick)
+            elif op == "release" and len(live) > 1:
+                model.release(h)
+                del ref.seqs[h]
+            for hh in model.seqs:
+                k, v, pos = model.view(hh)
+                want = ref.view(hh)
+                if want is None:
+                    assert model.info(hh)["length"] == 0
+                    continue
+                assert np.array_equal(k, want[0]) and np.array_equal(v, want[1])
+                assert np.array_equal(pos, want[2])
+                assert model.spans(hh) == ref.spans[hh]
+                assert model.info(hh)["next_pos"] == ref.next_pos[hh]
+        # every page referenced exactly as often as it appears in page lists
+        counts = np.zeros(model.num_pages, dtype=np.int64)
+        for hh in model.seqs:
+            for p in model.page_table(hh):
+                counts[p] += 1
+        assert np.array_equal(counts, model.refcount)
+        for h in list(model.seqs):
+            model.release(h)
+        assert model.live_pages() == 0
+
+
+def check_hand_worked_page_tables():
+    """Page ids under lowest-free-first allocation, worked by hand (P = 4)."""
+    m = pg.PageModel(num_pages=16, page_size=4, max_seqs=4, max_pages_per_seq=16)
+    a = m.seq_create()
+    assert a == 0
+    m.append(a, 10)                      # tokens 0..9 -> pages 0, 1, 2
+    assert m.page_table(a) == [0, 1, 2]
+    b = m.fork(a, 8)                     # aligned: aliases pages 0, 1
+    assert b == 1 and m.page_table(b) == [0, 1]
+    assert m.refcount[:3].tolist() == [2, 2, 1] and m.live_pages() == 3
+    c = m.fork(a, 6)                     # 6 = 1 page + 2 tokens: copy into page 3
+    assert c == 2 and m.page_table(c) == [0, 3]
+    m.append(b, 3)                       # b: 8 -> 11, new page 4
+    assert m.page_table(b) == [0, 1, 4]
+    m.span_mark(a, 7, 1, 6)              # evict [1, 6): f = 1, fp = 0
+    st = m.evict(a, [7])                 # L' = 5 -> 2 new pages: 5, 6
+    assert m.page_table(a) == [5, 6]
+    assert st == dict(tokens_removed=5, tokens_moved=5, pages_allocated=2,
+                      pages_freed=1, first_evicted=1)  # page 2 was a's alone
+    assert m.view(a)[2].tolist() == [0, 6, 7, 8, 9]
+    assert m.refcount[:7].tolist() == [2, 1, 0, 1, 1, 1, 1]
+    m.release(c)                         # page 0 -> 1 ref, page 3 freed
+    m.append(a, 4)                       # a: 5 -> 9: slot 1..3 of page 6, then page 2
+    assert m.page_table(a) == [5, 6, 2]
+    assert m.view(a)[2].tolist() == [0, 6, 7, 8, 9, 10, 11, 12, 13]
+    assert m.peak_pages == 7
+
+
+def check_fork_is_zero_copy_and_release_restores():
+    m = pg.PageModel(num_pages=64, page_size=16, max_seqs=4, max_pages_per_seq=64)
+    a = m.seq_create()
+    m.append(a, 160)
+    before = m.refcount.copy(), m.live_pages()
+    b = m.fork(a, 160)
+    assert m.live_pages() == before[1]          # aligned: no page
+    c = m.fork(a, 150)
+    assert m.live_pages() == before[1] + 1      # one tail page
+    m.release(b)
+    m.release(c)
+    assert np.array_equal(m.refcount, before[0]) and m.live_pages() == before[1]
+
+
+def check_all_keep_eviction_is_identity(seed=11):
+    rng = np.random.default_rng(seed)
+    m = pg.PageModel(num_pages=32, page_size=4, max_seqs=4, max_pages_per_seq=32,
+                     layers=1, kv_heads=1, head_dim=2, with_data=True)
+    a = m.seq_create()
+    m.append(a, 23, rng.standard_normal((1, 23, 1, 2)), rng.standard_normal((1, 23, 1, 2)))
+    m.span_mark(a, 1, 5, 5)
+    m.span_mark(a, 2, 9, 9)
+    m.span_mark(a, 3, 10, 14)
+    snap = _state(m), m.K.copy(), m.V.copy(), m.POS.copy(), m.stats()
+    for cursors in ([], [1], [2, 2]):
+        st = m.evict(a, cursors)
+        assert st["tokens_removed"] == 0 and st["tokens_moved"] == 0
+        assert st["pages_allocated"] == 0 and st["pages_freed"] == 0
+        assert m.page_table(a) == snap[0][2][a][0]
+        assert np.array_equal(m.K, snap[1]) and np.array_equal(m.V, snap[2])
+        assert np.array_equal(m.POS, snap[3]) and m.stats() == snap[4]
+    assert set(m.spans(a)) == {3}
+
+
+def check_positions_carried(seed=12):
+    rng = np.random.default_rng(seed)
+    m = pg.PageModel(num_pages=200, page_size=16, max_seqs=2, max_pages_per_seq=200)
+    a = m.seq_create()
+    m.append(a, 500)
+    cursor = 0
+    for _ in range(6):
+        length = m.info(a)["length"]
+        before = m.view(a)[2]
+        cuts = sorted(rng.choice(np.arange(length + 1), 6, replace=False).tolist())
+        spans = [(cuts[i], cuts[i + 1]) for i in range(0, 6, 2)]
+        ids = []
+        for s, e in spans:
+            m.span_mark(a, cursor, s, e)
+            ids.append(cursor)
+            cursor += 1
+        keep = ev.keep_mask(length, spans)
+        m.evict(a, ids)
+        after = m.view(a)[2]
+        assert np.array_equal(after, before[keep.astype(bool)])
+        assert np.all(np.diff(after) > 0)
+        m.append(a, 20)
+        assert m.view(a)[2][-1] == 500 + 20 * (_ + 1) - 1
+
+
+def check_evict_parent_leaves_child(seed=13):
+    rng = np.random.default_rng(seed)
+    m = pg.PageModel(num_pages=64, page_size=4, max_seqs=4, max_pages_per_seq=64,
+                     layers=1, kv_heads=1, head_dim=2, with_data=True)
+    a = m.seq_create()
+    m.append(a, 30, rng.standard_normal((1, 30, 1, 2)), rng.standard_normal((1, 30, 1, 2)))
+    b = m.fork(a, 26)
+    m.append(b, 5, rng.standard_normal((1, 5, 1, 2)), rng.standard_normal((1, 5, 1, 2)))
+    child_view = [x.copy() for x in m.view(b)]
+    m.span_mark(a, 0, 3, 20)             # straddles nothing, shared pages
+    m.span_mark(a, 1, 24, 28)            # straddles the fork point 26
+    m.evict(a, [0, 1])
+    for x, y in zip(child_view, m.view(b)):
+        assert np.array_equal(x, y)
+
+
+def check_errors_leave_state_unchanged():
+    m = pg.PageModel(num_pages=6, page_size=4, max_seqs=2, max_pages_per_seq=8)
+    a = m.seq_create()
+    m.append(a, 14)                      # 4 pages
+    m.span_mark(a, 0, 0, 3)
+    m.span_mark(a, 1, 8, 14)
+    cases = [
+        (lambda: m.append(a, 11), pg.NoPages),     # needs 3 more pages, 2 free
+        (lambda: m.append(a, 19), pg.Invalid),     # beyond 8 pages per sequence
+        (lambda: m.append(9, 1), pg.UnknownSeq),
+        (lambda: m.span_mark(a, 2, 2, 5), pg.SpanError),
+        (lambda: m.span_mark(a, 0, 4, 5), pg.Invalid),
+        (lambda: m.span_mark(a, 3, 10, 15), pg.SpanError),
+        (lambda: m.evict(a, [0, 5]), pg.UnknownCursor),
+        (lambda: m.fork(a, 15), pg.Invalid),
+        (lambda: m.release(7), pg.UnknownSeq),
+    ]
+    for fn, kind in cases:
+        snap = _state(m)
+        try:
+            fn()
+        except pg.OracleError as err:
+            assert type(err) is kind, (type(err), kind)
+        else:
+            raise AssertionError(f"expected {kind.__name__}")
+        assert _state(m) == snap
+    b = m.fork(a, 13)                    # takes the 5th page (tail copy)
+    assert m.free_pages() == 1
+    snap = _state(m)
+    try:
+        m.evict(a, [1])                  # needs ceil(8/4) - 2 = 0 pages: fine
+    except pg.OracleError:
+        raise AssertionError("evicting the tail needs no page")
+    assert _state(m) != snap
+    del b
+
+
+def check_masked_equals_compacted(page_sizes=(1, 2, 4, 16), seed=14, n_tokens=40):
+    """The paper's train/serve equivalence: attention over the compacted cache
+    is bit-identical to masked attention over the full cache, for every subset
+    of up to 6 spans."""
+    rng = np.random.default_rng(seed)
+    heads = [(1, 1), (4, 1), (8, 2)]
+    for page in page_sizes:
+        for hq, hkv in heads:
+            for d in (8, 64):
+                base = pg.PageModel(num_pages=3 * n_tokens, page_size=page, max_seqs=2,
+                                    max_pages_per_seq=n_tokens, layers=1, kv_heads=hkv,
+                                    head_dim=d, with_data=True)
+                a = base.seq_create()
+                n = n_tokens
+                base.append(a, n, rng.standard_normal((1, n, hkv, d)),
+                            rng.standard_normal((1, n, hkv, d)))
+                cuts = sorted(rng.choice(np.arange(n + 1), 12, replace=False).tolist())
+                spans = [(cuts[i], cuts[i + 1]) for i in range(0, 12, 2)]
+                for c, (s, e) in enumerate(spans):
+                    base.span_mark(a, c, s, e)
+                q = rng.standard_normal((hq, d))
+                k_full, v_full, pos_full = base.view(a)
+                scale = 1 / math.sqrt(d)
+                for r in range(len(spans) + 1):
+                    for subset in itertools.combinations(range(len(spans)), r):
+                        m = copy.deepcopy(base)
+                        m.evict(a, list(subset))
+                        keep = ev.keep_mask(n, [spans[c] for c in subset])
+                        k, v, pos = m.view(a)
+                        assert np.array_equal(pos, pos_full[keep.astype(bool)])
+                        got = att.attention(q, k[:, 0], v[:, 0], scale, hq // hkv)
+                        want = att.masked_attention(q, k_full[:, 0], v_full[:, 0],
+                                                    keep, scale, hq // hkv)
+                        assert np.array_equal(got, want)
+
+
+ALL_CHECKS = [
+    check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
+    check_uniform_closed_form, check_two_key_closed_form,
+    check_permutation_invariance, check_masked_semantics, check_merge_identity,
+    check_scan_and_inverse, check_span_shift, check_against_list_model,
+    check_hand_worked_page_tables, check_fork_is_zero_copy_and_release_restores,
+    check_all_keep_eviction_is_identity, check_positions_carried,
+    check_evict_parent_leaves_child, check_errors_leave_state_unchanged,
+    check_masked_equals_compacted,
+]

@@ -1,0 +1,166 @@
+"""Plant plausible mistakes in the oracle (on the CPU) and show the pins see them.
+
+Each mutant replaces one oracle function with a subtly wrong version; the test
+passes when at least one pin check fails on the mutated oracle.
+"""
+
+import heapq
+import math
+
+import numpy as np
+import pytest
+
+from oracle import attention as att
+from oracle import evict as ev
+from oracle import pages as pg
+from tests import oracle_pins as pins
+
+
+def _scores_gqa_modulo(q, k, scale, group, mask=None):
+    q = np.asarray(q, np.float64)
+    k = np.asarray(k, np.float64)
+    hkv = k.shape[1]
+    s = np.stack([scale * np.cumsum(k[:, h % hkv, :] * q[h], axis=1)[:, -1]
+                  if k.shape[0] else np.zeros(0) for h in range(q.shape[0])])
+    if mask is not None:
+        s[:, ~np.asarray(mask).astype(bool)] = -np.inf
+    return s
+
+
+_orig_scores = att.scores
+_orig_partial = att.partial
+
+
+def _scores_no_scale(q, k, scale, group, mask=None):
+    return _orig_scores(q, k, 1.0, group, mask)
+
+
+def _scores_sign(q, k, scale, group, mask=None):
+    return _orig_scores(q, k, -scale, group, mask)
+
+
+def _partial_k_as_v(q, k, v, scale, group, mask=None):
+    return _orig_partial(q, k, k, scale, group, mask)
+
+
+def _attention_unnormalised(q, k, v, scale, group, mask=None):
+    m, l, acc = _orig_partial(q, k, v, scale, group, mask)
+    return acc
+
+
+def _merge_no_rescale(parts):
+    accs = sum(np.asarray(p[2]) for p in parts)
+    ls = sum(np.asarray(p[1]) for p in parts)
+    out = np.zeros_like(accs)
+    live = ls > 0
+    out[live] = accs[live] / ls[live][:, None]
+    return out
+
+
+def _scan_inclusive(keep):
+    return np.cumsum(np.asarray(keep, dtype=np.int64))
+
+
+def _keep_mask_end_inclusive(length, spans):
+    keep = np.ones(int(length), dtype=np.uint8)
+    for s, e in spans:
+        keep[s:e + 1] = 0
+    return keep
+
+
+def _shift_span_wrong(start, end, evicted):
+    before = sum(e - s for s, e in evicted if s <= start)
+    return start - before, end - before + (1 if evicted else 0)
+
+
+def _alloc_highest(self):
+    page = max(self._free)
+    self._free.remove(page)
+    heapq.heapify(self._free)
+    self.refcount[page] = 1
+    self.peak_pages = max(self.peak_pages, self.live_pages())
+    return page
+
+
+_orig_fork = pg.PageModel.fork
+_orig_evict = pg.PageModel.evict
+
+
+def _fork_copies(self, parent, fork_len):
+    child = _orig_fork(self, parent, fork_len)
+    # a copying fork: take one fresh page per aliased page
+    seq = self.seqs[child]
+    for i, page in enumerate(list(seq.pages[: fork_len // self.P])):
+        fresh = self._alloc()
+        if self.with_data:
+            self.K[fresh], self.V[fresh], self.POS[fresh] = self.K[page], self.V[page], self.POS[page]
+        self._unref(page)
+        seq.pages[i] = fresh
+    return child
+
+
+def _fork_next_pos_parent(self, parent, fork_len):
+    child = _orig_fork(self, parent, fork_len)
+    self.seqs[child].next_pos = self.seqs[parent].next_pos
+    return child
+
+
+def _evict_recompute_pos(self, h, cursor_ids):
+    stats = _orig_evict(self, h, cursor_ids)
+    seq = self.seqs[h]
+    seq.pos = list(range(seq.length))
+    if self.with_data:
+        for i in range(seq.length):
+            self.POS[seq.pages[i // self.P], i % self.P] = i
+    return stats
+
+
+def _evict_keeps_old_refs(self, h, cursor_ids):
+    seq = self.seqs[h]
+    old = list(seq.pages)
+    stats = _orig_evict(self, h, cursor_ids)
+    if stats["tokens_removed"]:
+        fp = stats["first_evicted"] // self.P
+        for page in old[fp:]:  # leak: take the references back
+            if self.refcount[page] == 0:
+                self._free.remove(page)
+                heapq.heapify(self._free)
+            self.refcount[page] += 1
+    return stats
+
+
+MUTANTS = {
+    "gqa_head_modulo": (att, "scores", _scores_gqa_modulo),
+    "missing_scale": (att, "scores", _scores_no_scale),
+    "score_sign": (att, "scores", _scores_sign),
+    "k_used_as_v": (att, "partial", _partial_k_as_v),
+    "unnormalised_output": (att, "attention", _attention_unnormalised),
+    "merge_without_rescale": (att, "merge", _merge_no_rescale),
+    "inclusive_scan": (ev, "exclusive_scan", _scan_inclusive),
+    "span_end_inclusive": (ev, "keep_mask", _keep_mask_end_inclusive),
+    "span_shift_wrong": (ev, "shift_span", _shift_span_wrong),
+    "alloc_highest_first": (pg.PageModel, "_alloc", _alloc_highest),
+    "fork_copies_pages": (pg.PageModel, "fork", _fork_copies),
+    "fork_next_pos_from_parent": (pg.PageModel, "fork", _fork_next_pos_parent),
+    "evict_recomputes_positions": (pg.PageModel, "evict", _evict_recompute_pos),
+    "evict_leaks_old_pages": (pg.PageModel, "evict", _evict_keeps_old_refs),
+}
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name, monkeypatch):
+    owner, attr, fn = MUTANTS[name]
+    monkeypatch.setattr(owner, attr, fn)
+    failed = []
+    for check in pins.ALL_CHECKS:
+        try:
+            check()
+        except Exception as err:  # noqa: BLE001 - any failure counts as caught
+            failed.append((check.__name__, type(err).__name__))
+    assert failed, f"mutant {name} passed every pin"
+
+
+def test_pins_green_without_mutation():
+    for check in pins.ALL_CHECKS:
+        check()
+    assert math.isfinite(1.0)
