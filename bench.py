@@ -1,0 +1,315 @@
+#!/usr/bin/env python3
+"""Benchmark of the SideQuest KV hot path on one MI355X.
+
+Workload (the step that is timed): one decode step of 8 concurrent agent
+tasks at 128K context, each a main thread plus a forked auxiliary thread that
+shares all but the last pages of the main thread's cache (16 queries; 32
+query heads, 8 KV heads, head size 128, bf16 K/V).  A step appends the new
+token of every sequence (sq_append_batch) and runs decode attention over the
+shared paged cache (sq_decode_attn, AUTO mode: the shared prefix of each
+main/auxiliary pair is read once by the multi-query MFMA tile).
+
+value  = decode K/V bytes the method must read per step (shared pages once)
+         / measured step time, in GB/s (inputs resident in HBM).
+Also reported: tokens/s, the per-sequence modes, span eviction (64K context,
+65% of tokens in whole tool spans removed) in GB/s, the dominant kernel's
+roofline (HIP events on the library's stream), and the CPU oracle timed on a
+bounded sample of the same workload.
+
+Prints ONE JSON line on stdout; progress goes to stderr.
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "decode-attn HBM GB/s (% of 8 TB/s) + tokens/s at 128K ctx; evict GB/s"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse_args():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--tasks", type=int, default=8)
+    ap.add_argument("--ctx", type=int, default=131072)
+    ap.add_argument("--legs", default="decode,modes,evict,cpu",
+                    help="comma list of: decode, modes, evict, cpu")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    return ap.parse_args()
+
+
+def kernel_sha():
+    h = hashlib.sha256()
+    for f in ("decode_kernels.hip", "kv_kernels.hip", "sq_kernels.hpp"):
+        with open(os.path.join(ROOT, "paper_2602_22603_amd", "csrc", f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()[:16]
+
+
+def read_traffic(name):
+    """HBM bytes per launch from a committed rocprofv3 counter summary, if it
+    was taken on the current kernel sources."""
+    path = os.path.join(ROOT, "profiles", name)
+    if not os.path.exists(path):
+        return None
+    vals = {}
+    with open(path) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_sources_sha") != kernel_sha():
+        return None
+    try:
+        return float(vals["hbm_bytes_per_launch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def build_shared(sq, torch, wl, tasks, ctx, extra_tokens):
+    w = wl.shared128k(n_tasks=tasks, main_len=ctx, fork_at=ctx - 256, aux_private=512)
+    pages_task = ctx // 16 + w.aux_private // 16 + 2 * (extra_tokens // 16 + 2)
+    store = sq.Store(1, 32, 8, 128, num_pages=tasks * pages_task + 64, max_seqs=2 * tasks + 4,
+                     max_pages_per_seq=ctx // 16 + extra_tokens // 16 + 64)
+    seqs, sample = [], None
+    for t in range(tasks):
+        k = wl.device_normal_bf16((1, ctx, 8, 128), w.seed * 1000 + 4 * t, "cuda")
+        v = wl.device_normal_bf16((1, ctx, 8, 128), w.seed * 1000 + 4 * t + 1, "cuda")
+        ka = wl.device_normal_bf16((1, w.aux_private, 8, 128), w.seed * 1000 + 4 * t + 2, "cuda")
+        va = wl.device_normal_bf16((1, w.aux_private, 8, 128), w.seed * 1000 + 4 * t + 3, "cuda")
+        main = store.seq_create()
+        store.append(main, k[:, : w.fork_at], v[:, : w.fork_at])
+        aux = store.fork(main, w.fork_at)
+        store.append(main, k[:, w.fork_at:], v[:, w.fork_at:])
+        store.append(aux, ka, va)
+        seqs += [main, aux]
+        if t == 0:
+            sample = (k, v)
+        torch.cuda.synchronize()
+        del ka, va
+        if t:
+            del k, v
+    return store, seqs, sample, w
+
+
+def time_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
+    """Warm up, then time `steps` decode steps (append + attention)."""
+    n = len(seqs)
+    for i in range(warmup):
+        store.append_batch(seqs, kb[i], vb[i])
+        store.decode(0, seqs, qs[i], out=out, mode=mode)
+    torch.cuda.synchronize()
+    store.profile_enable(True)
+    store.profile_read()
+    st0 = store.stats()
+    plan = store.plan_info(seqs, mode)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(warmup, warmup + steps):
+        store.append_batch(seqs, kb[i], vb[i])
+        store.decode(0, seqs, qs[i], out=out, mode=mode)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = store.profile_read()
+    store.profile_enable(False)
+    st1 = store.stats()
+    ms = (t1 - t0) * 1e3 / steps
+    kv_bytes = (st1["decode_kv_bytes"] - st0["decode_kv_bytes"]) / steps
+    logical = (st1["decode_kv_bytes_logical"] - st0["decode_kv_bytes_logical"]) / steps
+    return dict(ms_per_step=ms, kv_bytes_per_step=kv_bytes, kv_bytes_logical_per_step=logical,
+                gbps=kv_bytes / (ms * 1e-3) / 1e9, tokens_per_s=n / (ms * 1e-3), prof=prof,
+                plan=plan)
+
+
+def evict_leg(sq, torch, wl, reps=8):
+    w = wl.compaction64k()
+    L = w.length
+    store = sq.Store(1, 32, 8, 128, num_pages=2 * (L // 16) + 64, max_seqs=4,
+                     max_pages_per_seq=L // 16 + 32)
+    k = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000, "cuda")
+    v = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000 + 1, "cuda")
+    base = store.seq_create()
+    store.append(base, k, v)
+    del k, v
+    for c, (s, e) in enumerate(w.spans):
+        store.span_mark(base, c, s, e)
+    torch.cuda.synchronize()
+    walls, stats = [], None
+    store.profile_enable(True)
+    for r in range(reps + 2):
+        f = store.fork(base, L)  # aligned: aliases every page of the base
+        torch.cuda.synchronize()
+        if r == 2:
+            store.profile_read()
+        t0 = time.perf_counter()
+        stats = store.evict(f, w.evict_ids)
+        torch.cuda.synchronize()
+        if r >= 2:
+            walls.append(time.perf_counter() - t0)
+        if r < reps + 1:
+            store.release(f)
+    prof = store.profile_read()
+    store.profile_enable(False)
+    gather_ms = prof["evict_gather_ms"] / max(1, prof["evict_gather_launches"])
+    scan_ms = prof["evict_scan_ms"] / max(1, prof["evict_scan_launches"])
+    moved = 2 * stats["bytes_moved"]  # read + write
+    # decode on the compacted cache vs the full cache (batch 1)
+    q = wl.device_normal_bf16((1, 32, 128), 77, "cuda")
+    out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
+    res = {}
+    for name, seq in (("compacted", f), ("full", base)):
+        for _ in range(3):
+            store.decode(0, [seq], q, out=out)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(32):
+            store.decode(0, [seq], q, out=out)
+        torch.cuda.synchronize()
+        res[name] = (time.perf_counter() - t0) * 1e3 / 32
+    info = dict(
+        workload=f"64K tokens, 40 tool + 40 reasoning spans, evict >= 65% (got "
+                 f"{stats['tokens_removed'] / L:.3f})",
+        tokens_removed=stats["tokens_removed"], tokens_moved=stats["tokens_moved"],
+        bytes_read_plus_written=moved, gather_ms=gather_ms, scan_ms=scan_ms,
+        evict_gbps=moved / (gather_ms * 1e-3) / 1e9,
+        evict_gbps_wall=moved / (sorted(walls)[len(walls) // 2]) / 1e9,
+        evict_wall_ms_median=sorted(walls)[len(walls) // 2] * 1e3,
+        decode_ms_compacted=res["compacted"], decode_ms_full=res["full"])
+    store.close()
+    return info
+
+
+def cpu_leg(sample, wl, budget_s):
+    import numpy as np
+    from oracle import attention as oatt
+    k, v = sample
+    ctx = k.shape[1]
+    rng = np.random.default_rng([2602, 2, 7])
+    q = wl.bf16_value(wl.normal_bf16(rng, (32, 128)))
+    done, t_total, heads = 0, 0.0, 0
+    for g in range(8):
+        kf = wl.torch_bf16_to_f64(k[0, :, g: g + 1])
+        vf = wl.torch_bf16_to_f64(v[0, :, g: g + 1])
+        t0 = time.perf_counter()
+        oatt.attention(q[4 * g: 4 * g + 4], kf, vf, 1 / math.sqrt(128), 4)
+        t_total += time.perf_counter() - t0
+        heads += 1
+        done += ctx * 512
+        if t_total >= budget_s:
+            break
+    return dict(value=done / t_total / 1e9, unit="GB/s", cores=1, kind="oracle",
+                sample=f"main thread of task 0: {ctx} tokens x {heads} of 8 KV heads (4 query "
+                       f"heads each), float64 NumPy oracle, {t_total:.1f} s")
+
+
+def main():
+    args = parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); this build has no "
+              "multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2602_22603_amd import sq
+    from paper_2602_22603_amd import workload as wl
+    sq.lib()
+    legs = set(args.legs.split(","))
+    torch.cuda.set_device(0)
+    total = args.warmup + args.steps
+    n_modes = 3 if "modes" in legs else 0
+    extra = total * (1 + n_modes) + 16
+    log(f"building {args.tasks} tasks at {args.ctx} tokens ...")
+    store, seqs, sample, w = build_shared(sq, torch, wl, args.tasks, args.ctx, extra)
+    B = len(seqs)
+    kb = [wl.device_normal_bf16((1, B, 8, 128), 500 + 3 * i, "cuda") for i in range(total)]
+    vb = [wl.device_normal_bf16((1, B, 8, 128), 501 + 3 * i, "cuda") for i in range(total)]
+    qs = [wl.device_normal_bf16((B, 32, 128), 502 + 3 * i, "cuda") for i in range(total)]
+    out = torch.empty((B, 32, 128), dtype=torch.float32, device="cuda")
+
+    log("timing decode steps (AUTO) ...")
+    main_res = time_steps(sq, torch, store, seqs, sq.ATTN_AUTO, args.steps, args.warmup,
+                          kb, vb, qs, out)
+    prof, plan = main_res["prof"], main_res["plan"]
+    if plan["n_items_mfma"]:
+        kname, kms, kn, kbytes = ("k_decode_mfma", prof["decode_mfma_ms"],
+                                  prof["decode_mfma_launches"], plan["kv_bytes_mfma"])
+    else:
+        kname, kms, kn, kbytes = ("k_decode_valu", prof["decode_valu_ms"],
+                                  prof["decode_valu_launches"], plan["kv_bytes_valu"])
+    kavg = kms / max(1, kn)
+    achieved = kbytes / (kavg * 1e-3) / 1e9
+    traffic = read_traffic("decode_mfma_shared128k_traffic.txt")
+    roofline = dict(bound="hbm", kernel=kname, achieved=round(achieved, 1), peak=HBM_PEAK_GBPS,
+                    unit="GB/s", frac=round(achieved / HBM_PEAK_GBPS, 4), traffic=traffic,
+                    algorithmic_bytes_per_launch=kbytes, avg_launch_ms=round(kavg, 5),
+                    merge_avg_ms=round(prof["decode_merge_ms"] / max(1, prof["decode_merge_launches"]), 5),
+                    append_avg_ms=round(prof["append_ms"] / max(1, prof["append_launches"]), 5))
+    modes = {}
+    if "modes" in legs:
+        for name, m in (("stream_valu", sq.ATTN_STREAM), ("per_sequence_mfma", sq.ATTN_MFMA),
+                        ("shared_prefix", sq.ATTN_SHARED_PREFIX)):
+            log(f"timing mode {name} ...")
+            r = time_steps(sq, torch, store, seqs, m, args.steps, args.warmup, kb, vb, qs, out)
+            modes[name] = dict(ms_per_step=round(r["ms_per_step"], 4),
+                               gbps_unique_bytes=round(r["gbps"], 1),
+                               gbps_logical_bytes=round(r["kv_bytes_logical_per_step"] /
+                                                        (r["ms_per_step"] * 1e-3) / 1e9, 1),
+                               tokens_per_s=round(r["tokens_per_s"], 1))
+    store.close()
+    del kb, vb, qs
+    torch.cuda.empty_cache()
+    evict = None
+    if "evict" in legs:
+        log("eviction leg (64K compaction) ...")
+        evict = evict_leg(sq, torch, wl)
+    cpu = None
+    if "cpu" in legs:
+        log("oracle CPU baseline ...")
+        cpu = cpu_leg(sample, wl, args.cpu_seconds)
+    res = {
+        "metric": METRIC,
+        "value": round(main_res["gbps"], 1),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(main_res["ms_per_step"], 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"{args.tasks} tasks x (main {args.ctx} + forked aux "
+                               f"{args.ctx - 256}+512) tokens, 16-query decode step "
+                               f"(append + attention), 1 layer, 32q/8kv heads, head_dim 128, "
+                               f"page 16, AUTO mode",
+                   "global_batch": B, "seq_len": args.ctx, "parallelism": "single GPU"},
+        "frac_of_hbm_peak": round(main_res["gbps"] / HBM_PEAK_GBPS, 4),
+        "tokens_per_s": round(main_res["tokens_per_s"], 1),
+        "kv_bytes_per_step": main_res["kv_bytes_per_step"],
+        "kv_bytes_logical_per_step": main_res["kv_bytes_logical_per_step"],
+        "roofline": roofline,
+        "modes": modes,
+        "evict": evict,
+        "cpu_baseline": cpu,
+        "kernel_sources_sha": kernel_sha(),
+    }
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,303 @@
+/*
+ * sq.h - C ABI of libsq, the SideQuest KV-cache hot path for MI355X (gfx950).
+ *
+ * SideQuest (arXiv 2602.22603) lets a reasoning model fork an auxiliary
+ * thread on its own shared context; the auxiliary thread names stale tool
+ * responses ("cursors") and, once the main thread's turn has finished, their
+ * tokens are cleared from the KV cache (Algorithm 1; §3.1).  This library
+ * holds that KV cache and runs the data-parallel work under it:
+ *
+ *   - a paged KV store in which an auxiliary branch aliases the main thread's
+ *     pages without copying them (sq_fork; storage claim of §3.4),
+ *   - span eviction, clear_kv(Delta_ids) of Algorithm 1 Phase 1: keep-mask ->
+ *     exclusive prefix sum -> page-level gather into fresh pages, kept keys
+ *     keeping their original positions (sq_evict_spans),
+ *   - decode-step attention of a batch of main and auxiliary queries over the
+ *     shared, compacted cache: GQA split-K flash decoding plus a cross-split
+ *     merge, and a multi-query MFMA tile for a prefix that several queries
+ *     share (sq_decode_attn; the memory-bound step of §1 and §3.4, whose
+ *     shared-prefix optimisation §3.4 points to).
+ *
+ * Conventions for every call
+ * --------------------------
+ *  - Every call returns an sq_status.  All validation happens before any
+ *    change: a call that fails with SQ_ERR_INVALID, SQ_ERR_NO_PAGES,
+ *    SQ_ERR_UNKNOWN_SEQ, SQ_ERR_UNKNOWN_CURSOR or SQ_ERR_SPAN changes nothing.
+ *    SQ_ERR_HIP means a HIP call failed after validation; the device state of
+ *    the store is then undefined and the store should be destroyed.
+ *    sq_last_error() gives a thread-local message for the last failure.
+ *  - Device buffers (pools, workspace, q, out, new K/V) are allocated and
+ *    owned by the caller and must outlive the store or the call.  The library
+ *    owns host metadata only; it never allocates device memory.  In device
+ *    mode it allocates one pinned host staging buffer at sq_store_create.
+ *  - Host metadata changes when a call returns; device work is enqueued on
+ *    the given HIP stream (a hipStream_t passed as void*; NULL = the null
+ *    stream).  All device work of one store must go to ONE stream, in call
+ *    order: stream order is what makes an eviction issued after a decode read
+ *    the old pages after that decode has read them (§3.1, step 4), and what
+ *    lets a released page be reused safely.
+ *  - A store is not thread-safe.
+ *
+ * Data layout in HBM (caller-allocated, sizes from sq_pool_bytes)
+ * ---------------------------------------------------------------
+ *   K pool  bf16  [NL][num_pages][Hkv][P][D]   token-major rows of D values
+ *   V pool  bf16  [NL][num_pages][Hkv][D][P]   page-transposed: the P tokens
+ *                                               of one channel are contiguous
+ *   pos     int32 [num_pages][P]               position of each cached token
+ * P (page_size) is 16 in device mode; D (head_dim) is 64 or 128; the query
+ * group G = Hq / Hkv is 1, 2, 4 or 8.  Query head h reads KV head h / G.
+ */
+#ifndef SQ_H
+#define SQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SQ_ABI_VERSION 1
+
+typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
+typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
+
+typedef enum {
+  SQ_OK = 0,
+  SQ_ERR_INVALID = 1,        /* bad argument, capacity or configuration */
+  SQ_ERR_NO_PAGES = 2,       /* the page pool cannot hold the result */
+  SQ_ERR_UNKNOWN_SEQ = 3,    /* handle not live */
+  SQ_ERR_UNKNOWN_CURSOR = 4, /* cursor not registered on the sequence */
+  SQ_ERR_SPAN = 5,           /* span outside the sequence or overlapping */
+  SQ_ERR_HIP = 6             /* a HIP runtime call failed */
+} sq_status;
+
+/* sq_store_config.flags */
+#define SQ_STORE_METADATA_ONLY 1u /* host bookkeeping only: no pools, no
+                                     workspace, no HIP calls; any page size;
+                                     sq_decode_attn is rejected */
+
+/* sq_decode_attn modes */
+#define SQ_ATTN_AUTO 0          /* shared-prefix tiles where queries share
+                                   pages, per-sequence tiles elsewhere */
+#define SQ_ATTN_STREAM 1        /* per-sequence VALU split-K kernel */
+#define SQ_ATTN_SHARED_PREFIX 2 /* shared prefixes on the MFMA multi-query
+                                   tile, suffixes on the VALU kernel */
+#define SQ_ATTN_MFMA 3          /* per-sequence, MFMA tile (no grouping) */
+
+/* Limits. */
+#define SQ_MAX_BATCH 64           /* sequences per sq_decode_attn / append_batch */
+#define SQ_MAX_EVICT_SPANS 16384  /* distinct cursors per sq_evict_spans call */
+
+typedef struct {
+  int32_t num_layers;        /* NL >= 1 */
+  int32_t num_q_heads;       /* Hq, a multiple of num_kv_heads */
+  int32_t num_kv_heads;      /* Hkv >= 1 */
+  int32_t head_dim;          /* D: 64 or 128 (device mode) */
+  int32_t page_size;         /* P: 16 (device mode) */
+  int32_t num_pages;         /* physical pages in the pools */
+  int32_t max_seqs;          /* live sequence handles at once */
+  int32_t max_pages_per_seq; /* longest page list of one sequence */
+  void *k_pool;              /* device, see layout above (device mode) */
+  void *v_pool;              /* device */
+  int32_t *pos_pool;         /* device */
+  void *workspace;           /* device scratch of sq_workspace_bytes() bytes */
+  uint64_t workspace_bytes;
+  uint32_t flags;            /* SQ_STORE_* */
+} sq_store_config;
+
+typedef struct {
+  int64_t length;   /* tokens in the sequence */
+  int64_t next_pos; /* position the next appended token gets */
+  int32_t n_pages;  /* entries in its page list */
+  int32_t parent;   /* handle it was forked from, -1 if none */
+  int32_t n_spans;  /* registered cursor spans */
+  int32_t reserved;
+} sq_seq_desc;
+
+typedef struct {
+  int64_t tokens_removed;  /* L - L' */
+  int64_t tokens_moved;    /* kept tokens gathered into new pages: L' - P*floor(f/P) */
+  int64_t bytes_moved;     /* bytes written by the gather: tokens_moved * (NL*Hkv*D*2*2 + 4);
+                              the gather reads as many */
+  int64_t pages_allocated; /* fresh pages taken for the compacted tail */
+  int64_t pages_freed;     /* old pages whose last reference went away */
+  int64_t first_evicted;   /* f, the first evicted index (L if none) */
+} sq_evict_stats;
+
+typedef struct {
+  int64_t live_pages, peak_pages, free_pages, live_seqs;
+  int64_t append_tokens;                     /* tokens appended so far */
+  int64_t fork_calls, fork_tail_copies;      /* forks; forks that copied a tail page */
+  int64_t evict_calls, evict_tokens_removed, evict_tokens_moved, evict_bytes_moved;
+  int64_t decode_calls;
+  int64_t decode_kv_bytes;    /* K/V bytes decode must read, shared prefixes once */
+  int64_t decode_kv_bytes_logical; /* same with every query's own tokens counted */
+} sq_stats;
+
+typedef struct {
+  int32_t n_segments;       /* (page range, query rows) work units */
+  int32_t n_groups;         /* shared-prefix groups (>= 2 sequences) */
+  int32_t n_items_valu;     /* work items of the VALU split kernel */
+  int32_t n_items_mfma;     /* work items of the MFMA tile kernel */
+  int32_t chunk_pages;      /* pages per work item */
+  int32_t reserved;
+  int64_t kv_bytes;         /* K/V bytes the call reads, shared pages once */
+  int64_t kv_bytes_logical; /* K/V bytes with every sequence's pages counted */
+  int64_t kv_bytes_valu;    /* part of kv_bytes read by the VALU kernel */
+  int64_t kv_bytes_mfma;    /* part of kv_bytes read by the MFMA kernel */
+  int64_t io_bytes;         /* q, out and page-id bytes */
+} sq_plan_info;
+
+typedef struct {
+  /* Sums of kernel durations (ms) measured with HIP events recorded on the
+     store's stream around each launch, over the calls made since profiling
+     was enabled or last read. */
+  double decode_valu_ms, decode_mfma_ms, decode_merge_ms;
+  double evict_scan_ms, evict_gather_ms, append_ms;
+  int64_t decode_valu_launches, decode_mfma_launches, decode_merge_launches;
+  int64_t evict_scan_launches, evict_gather_launches, append_launches;
+} sq_profile;
+
+/* ---- store -------------------------------------------------------------
+ * The paged KV store shared by the main thread and its auxiliary branches
+ * (§3.4, "Storage Costs": the branch does not duplicate the cache). */
+
+/* Bytes of device workspace a store with this configuration needs.
+ * Returns 0 for an invalid configuration. */
+uint64_t sq_workspace_bytes(const sq_store_config *cfg);
+
+/* Bytes of the K pool (which = 0), V pool (1) or position pool (2).
+ * Returns 0 for an invalid configuration or which. */
+uint64_t sq_pool_bytes(const sq_store_config *cfg, int32_t which);
+
+/* Create a store over caller-owned pools.  *out receives the handle.
+ * SQ_ERR_INVALID: bad shape, capacity, missing buffer or workspace too small. */
+sq_status sq_store_create(const sq_store_config *cfg, sq_store **out);
+
+/* Destroy a store (host metadata only; does not touch the caller's buffers).
+ * Waits for the store's last enqueued work before freeing its staging buffer. */
+sq_status sq_store_destroy(sq_store *store);
+
+/* New empty sequence (the context C <- [Q] of Algorithm 1 starts here).
+ * Handles are the lowest free integers.  SQ_ERR_INVALID when max_seqs are live. */
+sq_status sq_seq_create(sq_store *store, sq_seq *out);
+
+/* ---- growth (Algorithm 1, Phase 3: C <- C + R, C <- C + O) --------------
+ * Append n tokens to seq.  k_new, v_new: device bf16 [NL][n][Hkv][D].
+ * Pages are taken lowest free id first, in page-list order; token i gets
+ * position next_pos + i.  SQ_ERR_NO_PAGES if the pool is short,
+ * SQ_ERR_INVALID if the page list would exceed max_pages_per_seq. */
+sq_status sq_append(sq_store *store, sq_seq seq, int32_t n, const void *k_new,
+                    const void *v_new, void *stream);
+
+/* Append one token to each of `batch` distinct sequences (a decode step).
+ * k_new, v_new: device bf16 [NL][batch][Hkv][D].  Pages are taken in batch
+ * order.  SQ_ERR_INVALID for a repeated sequence or batch > SQ_MAX_BATCH. */
+sq_status sq_append_batch(sq_store *store, const sq_seq *seqs, int32_t batch,
+                          const void *k_new, const void *v_new, void *stream);
+
+/* Register cursor `cursor` (a tool call and its response, §3 footnote on
+ * "tool response"; the [Cursor n] indexing of §4.2) as the tokens
+ * [start, end) of seq, in its current coordinates.  Empty spans are allowed.
+ * SQ_ERR_INVALID: cursor < 0 or already registered on seq.
+ * SQ_ERR_SPAN: outside [0, length] or overlapping a non-empty registered span. */
+sq_status sq_span_mark(sq_store *store, sq_seq seq, int32_t cursor, int64_t start,
+                       int64_t end);
+
+/* ---- auxiliary thread (Algorithm 1, Phase 2: C_aux <- C + p) ------------
+ * Fork a branch on the first fork_len tokens of parent.  The child aliases
+ * the parent's first fork_len/P pages (refcount + 1, nothing copied, §3.4).
+ * If fork_len % P != 0 the child gets one new page with a copy of the first
+ * fork_len % P slots of the parent's page fork_len/P.  The child's next
+ * position is the parent's if fork_len == parent length, else the position of
+ * the parent's token fork_len.  The child inherits the cursor spans that end
+ * at or before fork_len.  SQ_ERR_INVALID: fork_len outside [0, length] or no
+ * free handle; SQ_ERR_NO_PAGES: no page for the tail copy. */
+sq_status sq_fork(sq_store *store, sq_seq parent, int64_t fork_len, sq_seq *child,
+                  void *stream);
+
+/* Drop a branch when its thread finishes (§3.4: its transient tokens are
+ * discarded; Algorithm 1 Phase 1 sets S_thread <- None).  Every page loses one
+ * reference; pages reaching zero return to the pool.  Host-only. */
+sq_status sq_release(sq_store *store, sq_seq seq);
+
+/* ---- eviction (Algorithm 1, Phase 1: C.clear_kv(Delta_ids)) --------------
+ * Remove from seq the tokens of the n cursors in cursor_ids (host array).
+ * Duplicates are ignored.  With L tokens, keep[i] = 0 inside an evicted span,
+ * dst = exclusive prefix sum of keep, L' = sum keep and src_of[dst[i]] = i.
+ * With f the first evicted index, pages [0, f/P) stay; ceil(L'/P) - f/P fresh
+ * pages (lowest ids, taken before any old page is released) receive the kept
+ * tokens [P*floor(f/P), L') from the old pages: K, V of every layer and head
+ * and their positions, which are carried unchanged.  Then every old page
+ * from f/P on loses one reference.  Pages another live branch still holds
+ * survive, so other branches keep attending to what they saw.  Remaining
+ * spans shift left by the evicted tokens before them.  Evicting only empty
+ * spans (or none) only unregisters the cursors.  Issue it after the main
+ * thread's turn (§3.1 step 4).  stats may be NULL.
+ * SQ_ERR_UNKNOWN_CURSOR: a cursor is not registered on seq;
+ * SQ_ERR_NO_PAGES: the pool cannot hold the compacted tail;
+ * SQ_ERR_INVALID: n < 0 or n > SQ_MAX_EVICT_SPANS. */
+sq_status sq_evict_spans(sq_store *store, sq_seq seq, const int32_t *cursor_ids,
+                         int32_t n, void *stream, sq_evict_stats *stats);
+
+/* ---- decode attention (the memory-bound decode step of §1 / §3.4) --------
+ * One decode step of layer `layer` for `batch` sequences (main threads and
+ * auxiliary branches together, §3.1 "Parallel Execution"):
+ *   out[b][h] = sum_i softmax_i(scale * q[b][h] . K[i][h/G]) * V[i][h/G]
+ * over all length(seqs[b]) cached tokens of seqs[b] (the caller appends the
+ * current token first).  q: device bf16 [batch][Hq][D]; out: device fp32
+ * [batch][Hq][D].  An empty sequence gives zeros.  mode: SQ_ATTN_*.  Pages
+ * that several queries share as a common prefix are read once per group in
+ * AUTO and SHARED_PREFIX modes (§3.4 cites shared-prefix kernels for this).
+ * SQ_ERR_INVALID: batch outside [1, SQ_MAX_BATCH], bad layer or mode,
+ * metadata-only store. */
+sq_status sq_decode_attn(sq_store *store, int32_t layer, const sq_seq *seqs, int32_t batch,
+                         const void *q, float *out, float scale, int32_t mode, void *stream);
+
+/* Host-only description of the work sq_decode_attn would do for this batch. */
+sq_status sq_decode_plan_info(sq_store *store, const sq_seq *seqs, int32_t batch,
+                              int32_t mode, sq_plan_info *out);
+
+/* ---- introspection -------------------------------------------------------*/
+sq_status sq_seq_info(sq_store *store, sq_seq seq, sq_seq_desc *out);
+
+/* Host copy of seq's page list: up to cap ids into out; *n = its length. */
+sq_status sq_page_table(sq_store *store, sq_seq seq, int32_t *out, int32_t cap, int32_t *n);
+
+/* Host copy of the positions of seq's tokens (the library's host record):
+ * up to cap values into out; *n = length. */
+sq_status sq_positions(sq_store *store, sq_seq seq, int64_t *out, int64_t cap, int64_t *n);
+
+/* Registered spans of seq, ordered by cursor id: up to cap entries. */
+sq_status sq_seq_spans(sq_store *store, sq_seq seq, int32_t *cursors, int64_t *starts,
+                       int64_t *ends, int32_t cap, int32_t *n);
+
+/* Refcount of every page: up to cap values into out (host array). */
+sq_status sq_refcounts(sq_store *store, int32_t *out, int32_t cap);
+
+sq_status sq_stats_get(sq_store *store, sq_stats *out);
+
+/* Device keep / dst / src_of arrays of the last eviction that removed tokens,
+ * copied to host buffers of cap entries (synchronises the store's stream).
+ * *n_tokens = L before that eviction, *n_kept = L'.  SQ_ERR_INVALID if no
+ * such eviction happened or cap < L. */
+sq_status sq_debug_last_evict(sq_store *store, uint8_t *keep, int32_t *dst, int32_t *src_of,
+                              int64_t cap, int64_t *n_tokens, int64_t *n_kept);
+
+/* Kernel timing with HIP events on the store's stream (off by default). */
+sq_status sq_profile_enable(sq_store *store, int32_t on);
+/* Synchronises the recorded events, returns the sums and resets them. */
+sq_status sq_profile_read(sq_store *store, sq_profile *out);
+
+/* Message for the last failed call on this thread ("" if none). */
+const char *sq_last_error(void);
+
+/* SQ_ABI_VERSION of the loaded library. */
+int32_t sq_abi_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SQ_H */

@@ -1,0 +1,370 @@
+// kv_kernels.hip - gfx950 kernels that write and move KV-cache pages:
+//   append (Algorithm 1, Phase 3: the context grows by the response R and the
+//   tool output O), the fork's tail-page copy (Phase 2, C_aux <- C + p), and
+//   span eviction clear_kv (Phase 1): keep-mask -> exclusive prefix sum ->
+//   inverse map -> page-level gather into fresh pages.
+//
+// Layouts (elements are bf16 stored as uint16_t):
+//   K pool [NL][NP][Hkv][P][D]   one 16-token page of one head is P*D
+//                                 contiguous values, token-major
+//   V pool [NL][NP][Hkv][D][P]   the same page stored channel-major: the P
+//                                 tokens of one channel are contiguous
+//   pos    [NP][P]               int32 position of each cached token
+// The page size is 16 throughout.
+#include "sq_kernels.hpp"
+
+namespace sq {
+namespace {
+
+constexpr int P = kPage;
+
+__device__ inline const uint16_t *k_chunk(const Pools &p, int layer, int page, int head) {
+  return p.k + layer * p.layer_stride + (int64_t)page * p.page_stride + head * p.head_stride;
+}
+__device__ inline const uint16_t *v_chunk(const Pools &p, int layer, int page, int head) {
+  return p.v + layer * p.layer_stride + (int64_t)page * p.page_stride + head * p.head_stride;
+}
+__device__ inline uint16_t *k_chunk_w(const Pools &p, int layer, int page, int head) {
+  return p.k + layer * p.layer_stride + (int64_t)page * p.page_stride + head * p.head_stride;
+}
+__device__ inline uint16_t *v_chunk_w(const Pools &p, int layer, int page, int head) {
+  return p.v + layer * p.layer_stride + (int64_t)page * p.page_stride + head * p.head_stride;
+}
+
+// ---------------------------------------------------------------------------
+// Append: one block per (page touched, layer * Hkv + head).  New tokens come
+// token-major [NL][n_total][Hkv][D]; K rows are copied as 16-byte units, V is
+// transposed through LDS when a whole page is written and scattered per
+// element when only some slots of a page are (the other slots of that page
+// already hold earlier tokens of the sequence).
+template <int D>
+__global__ __launch_bounds__(256) void k_append(Pools p, AppendArgs a,
+                                                const uint16_t *__restrict__ kn,
+                                                const uint16_t *__restrict__ vn) {
+  constexpr int U = D / 8; // 16-byte units per row
+  __shared__ uint16_t tile[P][D + 8];
+  const int pi = blockIdx.x;
+  const int lh = blockIdx.y;
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  const int page = a.page_ids[pi];
+  const int s_begin = pi == 0 ? a.slot0 : 0;
+  const int t_begin = pi == 0 ? 0 : pi * P - a.slot0; // launch-local token of s_begin
+  int s_end = s_begin + (a.n_tok - t_begin);
+  if (s_end > P) s_end = P;
+  const int ns = s_end - s_begin;
+  const int64_t tok_stride = (int64_t)p.hkv * D;
+  const int64_t src0 = ((int64_t)layer * a.n_total + a.tok0 + t_begin) * tok_stride + head * D;
+
+  uint16_t *kd = k_chunk_w(p, layer, page, head);
+  for (int idx = threadIdx.x; idx < ns * U; idx += blockDim.x) {
+    const int j = idx / U, u = idx % U;
+    const uint4 val = *(reinterpret_cast<const uint4 *>(kn + src0 + j * tok_stride) + u);
+    *(reinterpret_cast<uint4 *>(kd + (s_begin + j) * D) + u) = val;
+  }
+
+  uint16_t *vd = v_chunk_w(p, layer, page, head);
+  if (ns == P) {
+    for (int idx = threadIdx.x; idx < P * U; idx += blockDim.x) {
+      const int j = idx / U, u = idx % U;
+      const uint4 val = *(reinterpret_cast<const uint4 *>(vn + src0 + j * tok_stride) + u);
+      *reinterpret_cast<uint4 *>(&tile[j][u * 8]) = val;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < D * 2; idx += blockDim.x) {
+      const int d = idx >> 1, h = idx & 1;
+      uint32_t w[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = (uint32_t)tile[h * 8 + 2 * e][d] | ((uint32_t)tile[h * 8 + 2 * e + 1][d] << 16);
+      *reinterpret_cast<uint4 *>(vd + d * P + h * 8) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < ns * D; idx += blockDim.x) {
+      const int j = idx % ns, d = idx / ns;
+      vd[d * P + s_begin + j] = vn[src0 + j * tok_stride + d];
+    }
+  }
+
+  if (lh == 0) {
+    for (int j = threadIdx.x; j < ns; j += blockDim.x)
+      p.pos[(int64_t)page * P + s_begin + j] = a.pos0 + t_begin + j;
+    if (threadIdx.x == 0 && pi >= a.new_from) a.pt_row[a.pt_first + pi] = page;
+  }
+}
+
+// One token for each of n sequences: block (b, layer * Hkv + head).
+template <int D>
+__global__ __launch_bounds__(64) void k_append_batch(Pools p, AppendBatchArgs a,
+                                                     const uint16_t *__restrict__ kn,
+                                                     const uint16_t *__restrict__ vn) {
+  constexpr int U = D / 8;
+  const int b = blockIdx.x;
+  const int lh = blockIdx.y;
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  const int page = a.page[b];
+  const int slot = a.slot[b];
+  const int64_t src = (((int64_t)layer * a.n + b) * p.hkv + head) * D;
+  uint16_t *kd = k_chunk_w(p, layer, page, head) + slot * D;
+  for (int u = threadIdx.x; u < U; u += blockDim.x)
+    *(reinterpret_cast<uint4 *>(kd) + u) = *(reinterpret_cast<const uint4 *>(kn + src) + u);
+  uint16_t *vd = v_chunk_w(p, layer, page, head) + slot;
+  for (int d = threadIdx.x; d < D; d += blockDim.x) vd[d * P] = vn[src + d];
+  if (lh == 0 && threadIdx.x == 0) {
+    p.pos[(int64_t)page * P + slot] = a.pos[b];
+    if (a.pt_index[b] >= 0) a.pt[a.pt_index[b]] = page;
+  }
+}
+
+// dst[i] = src[i] for i < n, then dst[n] = tail_value when tail_value >= 0.
+__global__ __launch_bounds__(256) void k_copy_i32(int32_t *dst, const int32_t *src, int32_t n,
+                                                  int32_t tail_value) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = src[i];
+  if (i == n && tail_value >= 0) dst[n] = tail_value;
+}
+
+// Whole-page copy (every layer and head, K, V and pos): the fork's tail page.
+template <int D>
+__global__ __launch_bounds__(256) void k_copy_page(Pools p, int32_t src_page, int32_t dst_page) {
+  constexpr int U = P * D / 8;
+  const int lh = blockIdx.x;
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  const uint4 *ks = reinterpret_cast<const uint4 *>(k_chunk(p, layer, src_page, head));
+  const uint4 *vs = reinterpret_cast<const uint4 *>(v_chunk(p, layer, src_page, head));
+  uint4 *kd = reinterpret_cast<uint4 *>(k_chunk_w(p, layer, dst_page, head));
+  uint4 *vd = reinterpret_cast<uint4 *>(v_chunk_w(p, layer, dst_page, head));
+  for (int u = threadIdx.x; u < U; u += blockDim.x) {
+    kd[u] = ks[u];
+    vd[u] = vs[u];
+  }
+  if (lh == 0 && threadIdx.x < P)
+    p.pos[(int64_t)dst_page * P + threadIdx.x] = p.pos[(int64_t)src_page * P + threadIdx.x];
+}
+
+// ---------------------------------------------------------------------------
+// Eviction scan.  keep[i] = 0 iff token i lies in one of the sorted, disjoint,
+// non-empty spans; dst = exclusive prefix sum of keep; src_of[dst[i]] = i.
+// Three passes over blocks of kScanBlock tokens: count, scan of the block
+// counts, then the in-block scan that writes dst and src_of.
+constexpr int kPerThread = kScanBlock / kScanThreads; // 8
+
+__device__ inline int span_search(const int32_t *spans, int n_spans, int i) {
+  // index of the last span whose start <= i, or -1
+  int lo = 0, hi = n_spans - 1, ans = -1;
+  while (lo <= hi) {
+    const int mid = (lo + hi) >> 1;
+    if (spans[2 * mid] <= i) {
+      ans = mid;
+      lo = mid + 1;
+    } else {
+      hi = mid - 1;
+    }
+  }
+  return ans;
+}
+
+__device__ inline int block_sum(int v, int *red) {
+  // 256 threads = 4 waves
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  const int w = threadIdx.x >> 6;
+  if ((threadIdx.x & 63) == 0) red[w] = v;
+  __syncthreads();
+  const int total = red[0] + red[1] + red[2] + red[3];
+  __syncthreads();
+  return total;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_evict_count(EvictArgs a) {
+  __shared__ int red[4];
+  const int base = blockIdx.x * kScanBlock + threadIdx.x * kPerThread;
+  int cnt = 0;
+  if (base < a.n_tokens) {
+    int s = span_search(a.spans, a.n_spans, base);
+    for (int e = 0; e < kPerThread; ++e) {
+      const int i = base + e;
+      if (i >= a.n_tokens) break;
+      while (s + 1 < a.n_spans && a.spans[2 * (s + 1)] <= i) ++s;
+      const bool inside = s >= 0 && i < a.spans[2 * s + 1];
+      a.keep[i] = inside ? 0 : 1;
+      cnt += inside ? 0 : 1;
+    }
+  }
+  const int total = block_sum(cnt, red);
+  if (threadIdx.x == 0) a.blocks[blockIdx.x] = total;
+}
+
+// Exclusive scan of n block counts in place; blocks[n] = total.  One block.
+__global__ __launch_bounds__(1024) void k_evict_scan_blocks(int32_t *blocks, int32_t n) {
+  __shared__ int buf[1024];
+  int carry = 0;
+  for (int base = 0; base < n; base += 1024) {
+    const int i = base + threadIdx.x;
+    const int v = i < n ? blocks[i] : 0;
+    buf[threadIdx.x] = v;
+    __syncthreads();
+    for (int o = 1; o < 1024; o <<= 1) {
+      const int t = threadIdx.x >= o ? buf[threadIdx.x - o] : 0;
+      __syncthreads();
+      buf[threadIdx.x] += t;
+      __syncthreads();
+    }
+    if (i < n) blocks[i] = carry + buf[threadIdx.x] - v;
+    const int chunk_total = buf[1023];
+    __syncthreads();
+    carry += chunk_total;
+  }
+  if (threadIdx.x == 0) blocks[n] = carry;
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_evict_finalize(EvictArgs a) {
+  __shared__ int buf[kScanThreads];
+  const int base = blockIdx.x * kScanBlock + threadIdx.x * kPerThread;
+  uint8_t kv[kPerThread];
+  int cnt = 0;
+#pragma unroll
+  for (int e = 0; e < kPerThread; ++e) {
+    const int i = base + e;
+    kv[e] = i < a.n_tokens ? a.keep[i] : 0;
+    cnt += kv[e];
+  }
+  buf[threadIdx.x] = cnt;
+  __syncthreads();
+  for (int o = 1; o < kScanThreads; o <<= 1) {
+    const int t = threadIdx.x >= o ? buf[threadIdx.x - o] : 0;
+    __syncthreads();
+    buf[threadIdx.x] += t;
+    __syncthreads();
+  }
+  int run = a.blocks[blockIdx.x] + buf[threadIdx.x] - cnt;
+#pragma unroll
+  for (int e = 0; e < kPerThread; ++e) {
+    const int i = base + e;
+    if (i >= a.n_tokens) break;
+    a.dst[i] = run;
+    if (kv[e]) a.src_of[run] = i;
+    run += kv[e];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Gather: block (fresh page pi, layer * Hkv + head) fills destination page
+// fp + pi with the kept tokens (fp + pi) * P + j, j < P, j below L'.  Each
+// comes from token src_of[t] of the old pages (old_ids, from page fp on).
+// Old and fresh pages are distinct, so nothing is read after being written.
+template <int D>
+__global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
+  constexpr int U = D / 8;
+  __shared__ int spage[P];
+  __shared__ int sslot[P];
+  __shared__ int nvalid;
+  const int pi = blockIdx.x;
+  const int lh = blockIdx.y;
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  const int dst_page = a.new_ids[pi];
+  const int t0 = (a.fp + pi) * P;
+  if (threadIdx.x < P) {
+    const int t = t0 + threadIdx.x;
+    if (t < a.new_len) {
+      const int src = a.src_of[t];
+      spage[threadIdx.x] = a.old_ids[src / P - a.fp];
+      sslot[threadIdx.x] = src % P;
+    }
+  }
+  if (threadIdx.x == 0) nvalid = min(P, a.new_len - t0);
+  __syncthreads();
+  const int nv = nvalid;
+
+  uint16_t *kd = k_chunk_w(p, layer, dst_page, head);
+  for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) {
+    const int j = idx / U, u = idx % U;
+    const uint4 *ks = reinterpret_cast<const uint4 *>(k_chunk(p, layer, spage[j], head) +
+                                                      sslot[j] * D);
+    *(reinterpret_cast<uint4 *>(kd + j * D) + u) = ks[u];
+  }
+  uint16_t *vd = v_chunk_w(p, layer, dst_page, head);
+  for (int idx = threadIdx.x; idx < D * P; idx += blockDim.x) {
+    const int j = idx % P, d = idx / P;
+    if (j < nv) vd[d * P + j] = v_chunk(p, layer, spage[j], head)[d * P + sslot[j]];
+  }
+  if (lh == 0) {
+    if (threadIdx.x < nv)
+      p.pos[(int64_t)dst_page * P + threadIdx.x] =
+          p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
+    if (threadIdx.x == 0) a.pt_row[a.fp + pi] = dst_page;
+  }
+}
+
+} // namespace
+
+// ---------------------------------------------------------------------------
+hipError_t launch_append(const Pools &p, const AppendArgs &a, const void *k_new,
+                         const void *v_new, hipStream_t s) {
+  dim3 grid(a.n_pages, p.nl * p.hkv);
+  const auto *kn = static_cast<const uint16_t *>(k_new);
+  const auto *vn = static_cast<const uint16_t *>(v_new);
+  if (p.d == 128)
+    hipLaunchKernelGGL(k_append<128>, grid, dim3(256), 0, s, p, a, kn, vn);
+  else
+    hipLaunchKernelGGL(k_append<64>, grid, dim3(256), 0, s, p, a, kn, vn);
+  return hipGetLastError();
+}
+
+hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const void *k_new,
+                               const void *v_new, hipStream_t s) {
+  dim3 grid(a.n, p.nl * p.hkv);
+  const auto *kn = static_cast<const uint16_t *>(k_new);
+  const auto *vn = static_cast<const uint16_t *>(v_new);
+  if (p.d == 128)
+    hipLaunchKernelGGL(k_append_batch<128>, grid, dim3(64), 0, s, p, a, kn, vn);
+  else
+    hipLaunchKernelGGL(k_append_batch<64>, grid, dim3(64), 0, s, p, a, kn, vn);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t tail_index,
+                           int32_t tail_value, hipStream_t s) {
+  (void)tail_index;
+  const int total = n + 1;
+  hipLaunchKernelGGL(k_copy_i32, dim3((total + 255) / 256), dim3(256), 0, s, dst, src, n,
+                     tail_value);
+  return hipGetLastError();
+}
+
+hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s) {
+  if (p.d == 128)
+    hipLaunchKernelGGL(k_copy_page<128>, dim3(p.nl * p.hkv), dim3(256), 0, s, p, src_page,
+                       dst_page);
+  else
+    hipLaunchKernelGGL(k_copy_page<64>, dim3(p.nl * p.hkv), dim3(256), 0, s, p, src_page,
+                       dst_page);
+  return hipGetLastError();
+}
+
+hipError_t launch_evict_scan(const EvictArgs &a, hipStream_t s) {
+  const int nblk = (a.n_tokens + kScanBlock - 1) / kScanBlock;
+  if (nblk == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_evict_count, dim3(nblk), dim3(kScanThreads), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_evict_scan_blocks, dim3(1), dim3(1024), 0, s, a.blocks, nblk);
+  e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(k_evict_finalize, dim3(nblk), dim3(kScanThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s) {
+  if (a.n_new == 0) return hipSuccess;
+  dim3 grid(a.n_new, p.nl * p.hkv);
+  if (p.d == 128)
+    hipLaunchKernelGGL(k_evict_gather<128>, grid, dim3(256), 0, s, p, a);
+  else
+    hipLaunchKernelGGL(k_evict_gather<64>, grid, dim3(256), 0, s, p, a);
+  return hipGetLastError();
+}
+
+} // namespace sq

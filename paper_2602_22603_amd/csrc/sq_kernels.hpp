@@ -1,0 +1,149 @@
+// sq_kernels.hpp - kernel-argument structs and launchers shared by the host
+// library (store.cpp) and the gfx950 kernels (kv_kernels.hip,
+// decode_kernels.hip).  Everything here is internal to libsq.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace sq {
+
+constexpr int kPage = 16;            // tokens per page in device mode
+constexpr int kMaxAppendPages = 240; // pages one append launch may touch
+constexpr int kMaxBatch = 64;        // queries per decode call
+constexpr int kMaxSegs = 128;        // (page range, query rows) units per decode
+constexpr int kMaxMembers = 4;       // sequences stacked in one MFMA tile
+constexpr int kRows = 16;            // query rows per partial slot (MFMA N)
+constexpr int kMaxItems = 8192;      // partial slots in the workspace
+constexpr int kScanBlock = 2048;     // tokens per block of the eviction scan
+constexpr int kScanThreads = 256;
+
+// Device pools and shapes.  K: [NL][NP][Hkv][P][D]; V: [NL][NP][Hkv][D][P];
+// pos: [NP][P].  Element strides are in bf16 units.
+struct Pools {
+  uint16_t *k;
+  uint16_t *v;
+  int32_t *pos;
+  int32_t nl, hkv, d, np;
+  int64_t layer_stride; // NP * Hkv * P * D
+  int64_t page_stride;  // Hkv * P * D
+  int64_t head_stride;  // P * D
+};
+
+// ---- append ---------------------------------------------------------------
+// Tokens [tok0, tok0 + n_tok) of an append of n_total tokens, landing in
+// pages page_ids[0..n_pages) starting at slot slot0 of the first page.
+struct AppendArgs {
+  int32_t n_tok;
+  int32_t n_total;
+  int32_t tok0;
+  int32_t slot0;
+  int32_t pos0;      // position of token tok0
+  int32_t n_pages;
+  int32_t pt_first;  // page-list index of page_ids[0]
+  int32_t new_from;  // page_ids[i] with i >= new_from are new: write them to the mirror
+  int32_t *pt_row;   // device page-table row of the sequence
+  int32_t page_ids[kMaxAppendPages];
+};
+
+// One token for each of n sequences.
+struct AppendBatchArgs {
+  int32_t n;
+  int32_t page[kMaxBatch];
+  int32_t slot[kMaxBatch];
+  int32_t pos[kMaxBatch];
+  int32_t pt_index[kMaxBatch]; // row * max_pages + index, or -1 if the page is not new
+  int32_t *pt;                 // device page-table mirror base
+};
+
+// ---- eviction -------------------------------------------------------------
+struct EvictArgs {
+  int32_t n_tokens;    // L
+  int32_t n_spans;
+  const int32_t *spans; // [n_spans][2] sorted, disjoint, non-empty, device
+  uint8_t *keep;       // [L]
+  int32_t *dst;        // [L]
+  int32_t *src_of;     // [L']
+  int32_t *blocks;     // [ceil(L / kScanBlock) + 1]
+};
+
+struct GatherArgs {
+  int32_t fp;          // first affected page index
+  int32_t n_new;       // fresh pages
+  int32_t new_len;     // L'
+  const int32_t *src_of;
+  const int32_t *old_ids; // old page ids from page index fp on, device
+  const int32_t *new_ids; // fresh page ids, device
+  int32_t *pt_row;        // device page-table row
+};
+
+// ---- decode ---------------------------------------------------------------
+// A segment: `ntok` tokens read from page-table row `row` starting at page
+// index `page0`, attended by `nmem` query sequences (batch indices packed as
+// bytes in `mem`).  Its work items are item0 + g * nchunk + c for KV head g
+// and chunk c, each chunk `chunk_pages` pages long.
+struct Seg {
+  int32_t row;
+  int32_t page0;
+  int32_t ntok;
+  int32_t item0;
+  int32_t nchunk;
+  int32_t nmem;
+  uint32_t mem; // byte j = batch index of member j
+};
+
+struct DecodeArgs {
+  const uint16_t *q;   // [B][Hq][D] bf16
+  const uint16_t *k;   // K pool at this layer
+  const uint16_t *v;   // V pool at this layer
+  const int32_t *pt;   // page-table mirror base
+  float *part_m;       // [kMaxItems][kRows]  (log2 domain)
+  float *part_l;       // [kMaxItems][kRows]
+  float *part_acc;     // [kMaxItems][kRows][D]
+  int64_t page_stride; // Hkv * P * D elements
+  int32_t max_pages;   // page-table row pitch
+  int32_t hq;
+  int32_t chunk_pages;
+  int32_t n_segs;
+  int32_t item_begin;  // global index of this launch's first item
+  int32_t n_items;
+  float scale_log2;    // scale * log2(e)
+  Seg segs[kMaxSegs];
+};
+
+struct MergeArgs {
+  float *out;  // [B][Hq][D]
+  const float *part_m;
+  const float *part_l;
+  const float *part_acc;
+  int32_t hq;
+  int32_t group; // G
+  // per batch entry: up to two (item base, chunks, member) triples
+  int32_t n_src[kMaxBatch];
+  int32_t item_base[kMaxBatch][2];
+  int32_t nchunk[kMaxBatch][2];
+  int32_t member[kMaxBatch][2];
+};
+
+// Kernel arguments are passed by value; keep each well under 4 KiB.
+static_assert(sizeof(AppendArgs) < 4096, "append kernel arguments too large");
+static_assert(sizeof(AppendBatchArgs) < 4096, "append-batch kernel arguments too large");
+static_assert(sizeof(DecodeArgs) < 4096, "decode kernel arguments too large");
+static_assert(sizeof(MergeArgs) < 4096, "merge kernel arguments too large");
+
+// ---- launchers (return the launch status) ------------------------------------
+hipError_t launch_append(const Pools &p, const AppendArgs &a, const void *k_new,
+                         const void *v_new, hipStream_t s);
+hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const void *k_new,
+                               const void *v_new, hipStream_t s);
+hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t tail_index,
+                           int32_t tail_value, hipStream_t s);
+hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s);
+hipError_t launch_evict_scan(const EvictArgs &a, hipStream_t s);
+hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);
+hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
+hipError_t launch_decode_mfma(int d, int group, const DecodeArgs &a, hipStream_t s);
+hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s);
+
+} // namespace sq

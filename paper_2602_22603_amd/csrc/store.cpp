@@ -1,0 +1,1147 @@
+// store.cpp - host side of libsq: the paged KV store's metadata (page
+// allocator, refcounts, per-sequence page lists, positions and cursor spans),
+// planning of every device operation, and the extern "C" ABI of include/sq.h.
+//
+// The model follows SideQuest's statement of the problem (arXiv 2602.22603):
+// a context that grows by appends (Algorithm 1, Phase 3), a forked auxiliary
+// branch that shares the context's storage (Phase 2; §3.4 "Storage Costs"),
+// and clear_kv over cursor ids applied between main-thread turns (Phase 1;
+// §3.1 steps 3-4).  Conventions the paper leaves open:
+//   * pages are taken lowest free id first, one at a time in page-list order;
+//   * eviction is out of place: the kept tail from page floor(f/P) on is
+//     gathered into fresh pages taken before any old page is released;
+//   * positions are carried through eviction, never recomputed;
+//   * every call validates everything before it changes anything.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <map>
+#include <string>
+#include <vector>
+
+#include "../../include/sq.h"
+#include "sq_kernels.hpp"
+
+namespace {
+
+thread_local std::string g_err;
+
+sq_status fail(sq_status st, const char *fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+sq_status hip_fail(hipError_t e, const char *what) {
+  return fail(SQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+constexpr uint64_t kAlign = 256;
+uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+struct Layout {
+  uint64_t pt, keep, dst, src, blocks, upload, part_m, part_l, part_acc, total;
+  uint64_t upload_elems;
+};
+
+Layout layout_of(const sq_store_config &c) {
+  Layout L{};
+  const uint64_t max_tok = (uint64_t)c.max_pages_per_seq * c.page_size;
+  uint64_t off = 0;
+  auto take = [&](uint64_t bytes) {
+    const uint64_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  };
+  L.pt = take((uint64_t)c.max_seqs * c.max_pages_per_seq * 4);
+  L.keep = take(max_tok);
+  L.dst = take(max_tok * 4);
+  L.src = take(max_tok * 4);
+  L.blocks = take((max_tok / sq::kScanBlock + 2) * 4);
+  L.upload_elems = 2ull * SQ_MAX_EVICT_SPANS + 2ull * c.max_pages_per_seq;
+  L.upload = take(L.upload_elems * 4);
+  L.part_m = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
+  L.part_l = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
+  L.part_acc = take((uint64_t)sq::kMaxItems * sq::kRows * c.head_dim * 4);
+  L.total = off;
+  return L;
+}
+
+bool shape_ok(const sq_store_config *c, bool device, std::string *why) {
+  auto bad = [&](const char *m) {
+    if (why) *why = m;
+    return false;
+  };
+  if (!c) return bad("null configuration");
+  if (c->num_layers < 1 || c->num_kv_heads < 1 || c->num_q_heads < 1 || c->head_dim < 1 ||
+      c->page_size < 1 || c->num_pages < 1 || c->max_seqs < 1 || c->max_pages_per_seq < 1)
+    return bad("every size must be positive");
+  if (c->num_q_heads % c->num_kv_heads) return bad("num_q_heads must be a multiple of num_kv_heads");
+  if ((int64_t)c->max_pages_per_seq * c->page_size > (int64_t)INT32_MAX / 2)
+    return bad("max_pages_per_seq * page_size too large");
+  if (device) {
+    const int grp = c->num_q_heads / c->num_kv_heads;
+    if (c->page_size != sq::kPage) return bad("device mode needs page_size 16");
+    if (c->head_dim != 64 && c->head_dim != 128) return bad("device mode needs head_dim 64 or 128");
+    if (grp != 1 && grp != 2 && grp != 4 && grp != 8) return bad("num_q_heads / num_kv_heads must be 1, 2, 4 or 8");
+    if (c->max_seqs > 255) return bad("device mode supports at most 255 sequences");
+  }
+  return true;
+}
+
+struct PosRun {
+  int64_t idx0; // first logical index
+  int64_t pos0; // its position
+  int64_t n;
+};
+
+struct Seq {
+  bool live = false;
+  std::vector<int32_t> pages;
+  int64_t length = 0;
+  int64_t next_pos = 0;
+  std::vector<PosRun> runs;                             // positions of tokens
+  std::map<int32_t, std::pair<int64_t, int64_t>> spans; // cursor -> [start, end)
+  std::map<int64_t, int64_t> nonempty;                  // start -> end of non-empty spans
+  int32_t parent = -1;
+};
+
+enum ProfKind { kProfValu, kProfMfma, kProfMerge, kProfScan, kProfGather, kProfAppend, kProfKinds };
+
+struct ProfPair {
+  hipEvent_t a, b;
+  int kind;
+};
+
+int64_t pos_at(const Seq &s, int64_t i) {
+  // runs are ordered by idx0 and cover [0, length)
+  size_t lo = 0, hi = s.runs.size();
+  while (hi - lo > 1) {
+    const size_t mid = (lo + hi) / 2;
+    if (s.runs[mid].idx0 <= i) lo = mid;
+    else hi = mid;
+  }
+  return s.runs[lo].pos0 + (i - s.runs[lo].idx0);
+}
+
+void runs_append(Seq &s, int64_t n) {
+  if (n <= 0) return;
+  if (!s.runs.empty()) {
+    PosRun &r = s.runs.back();
+    if (r.idx0 + r.n == s.length && r.pos0 + r.n == s.next_pos) {
+      r.n += n;
+      return;
+    }
+  }
+  s.runs.push_back({s.length, s.next_pos, n});
+}
+
+std::vector<PosRun> runs_truncate(const std::vector<PosRun> &runs, int64_t f) {
+  std::vector<PosRun> out;
+  for (const PosRun &r : runs) {
+    if (r.idx0 >= f) break;
+    PosRun c = r;
+    if (c.idx0 + c.n > f) c.n = f - c.idx0;
+    out.push_back(c);
+  }
+  return out;
+}
+
+// Tokens evicted before index x, for sorted disjoint spans with prefix sums.
+int64_t evicted_before(const std::vector<std::pair<int64_t, int64_t>> &sp,
+                       const std::vector<int64_t> &prefix, int64_t x) {
+  // number of spans with start < x
+  size_t lo = 0, hi = sp.size();
+  while (lo < hi) {
+    const size_t mid = (lo + hi) / 2;
+    if (sp[mid].first < x) lo = mid + 1;
+    else hi = mid;
+  }
+  if (lo == 0) return 0;
+  const size_t k = lo - 1; // last span starting before x
+  return prefix[k] + (std::min(sp[k].second, x) - sp[k].first);
+}
+
+} // namespace
+
+struct sq_store {
+  sq_store_config cfg{};
+  bool device = false;
+  int P = 16, G = 1, D = 128;
+  std::vector<int32_t> refcount;
+  std::vector<uint64_t> freebits;
+  int32_t free_hint = 0;
+  int64_t n_free = 0;
+  std::vector<Seq> seqs;
+  sq_stats st{};
+  int64_t peak_pages = 0;
+
+  // device
+  sq::Pools pools{};
+  Layout lay{};
+  int32_t *pt_dev = nullptr;
+  uint8_t *ev_keep = nullptr;
+  int32_t *ev_dst = nullptr, *ev_src = nullptr, *ev_blocks = nullptr, *ev_upload = nullptr;
+  float *part_m = nullptr, *part_l = nullptr, *part_acc = nullptr;
+  int32_t *staging = nullptr;
+  hipEvent_t staging_ev = nullptr;
+  bool staging_pending = false;
+  hipStream_t last_stream = nullptr;
+  bool have_last_evict = false;
+  int64_t last_evict_L = 0, last_evict_Lp = 0;
+
+  // tuning
+  int target_items = 4096;
+  bool auto_single_mfma = true;
+
+  // profiling
+  bool prof_on = false;
+  std::vector<ProfPair> prof_pending;
+  std::vector<hipEvent_t> ev_pool;
+  double prof_ms[kProfKinds] = {};
+  int64_t prof_n[kProfKinds] = {};
+
+  // ---- allocator ----
+  int64_t live_pages() const { return (int64_t)cfg.num_pages - n_free; }
+
+  int32_t alloc_page() {
+    const int32_t nw = (int32_t)freebits.size();
+    for (int32_t w = free_hint / 64; w < nw; ++w) {
+      if (freebits[w]) {
+        const int bit = __builtin_ctzll(freebits[w]);
+        const int32_t id = w * 64 + bit;
+        freebits[w] &= ~(1ull << bit);
+        free_hint = id + 1;
+        --n_free;
+        refcount[id] = 1;
+        peak_pages = std::max(peak_pages, live_pages());
+        return id;
+      }
+    }
+    return -1; // callers check n_free first
+  }
+
+  void unref(int32_t id, int64_t *freed) {
+    if (--refcount[id] == 0) {
+      freebits[id / 64] |= 1ull << (id % 64);
+      if (id < free_hint) free_hint = id;
+      ++n_free;
+      if (freed) ++*freed;
+    }
+  }
+
+  Seq *get(sq_seq h) {
+    if (h < 0 || h >= (int32_t)seqs.size() || !seqs[h].live) return nullptr;
+    return &seqs[h];
+  }
+
+  int32_t *pt_row(sq_seq h) { return pt_dev + (int64_t)h * cfg.max_pages_per_seq; }
+
+  // ---- profiling ----
+  hipEvent_t take_event() {
+    if (!ev_pool.empty()) {
+      hipEvent_t e = ev_pool.back();
+      ev_pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  bool prof_begin(hipStream_t s, ProfPair *pp, int kind) {
+    if (!prof_on) return false;
+    pp->a = take_event();
+    pp->b = take_event();
+    pp->kind = kind;
+    if (!pp->a || !pp->b) return false;
+    (void)hipEventRecord(pp->a, s);
+    return true;
+  }
+  void prof_end(hipStream_t s, ProfPair *pp, bool active) {
+    if (!active) return;
+    (void)hipEventRecord(pp->b, s);
+    prof_pending.push_back(*pp);
+  }
+};
+
+namespace {
+
+sq_status check_stream_store(sq_store *s) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  return SQ_OK;
+}
+
+bool aligned16(const void *p) { return ((uintptr_t)p & 15u) == 0; }
+
+// Upload host int32 data to the workspace through the pinned staging buffer,
+// in stream order.  The staging buffer is reused only after the copy that
+// last read it has completed.
+sq_status upload(sq_store *s, int32_t *dev_dst, const int32_t *src, size_t n, hipStream_t strm) {
+  if (n == 0) return SQ_OK;
+  if (s->staging_pending) {
+    hipError_t e = hipEventSynchronize(s->staging_ev);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(staging)");
+    s->staging_pending = false;
+  }
+  std::memcpy(s->staging, src, n * 4);
+  hipError_t e = hipMemcpyAsync(dev_dst, s->staging, n * 4, hipMemcpyHostToDevice, strm);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(upload)");
+  e = hipEventRecord(s->staging_ev, strm);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord(staging)");
+  s->staging_pending = true;
+  return SQ_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Decode planning.
+struct PlanSeg {
+  sq::Seg seg;
+  bool mfma;
+  int32_t members[sq::kMaxMembers];
+};
+
+struct Plan {
+  std::vector<PlanSeg> segs;
+  int n_groups = 0;
+  int chunk_pages = 1;
+  int n_items_valu = 0, n_items_mfma = 0;
+  int64_t kv_bytes = 0, kv_bytes_logical = 0, io_bytes = 0;
+  int64_t kv_bytes_valu = 0, kv_bytes_mfma = 0;
+};
+
+sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode, Plan *plan) {
+  const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
+  const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
+  std::vector<int> group_of(batch, -1);
+  std::vector<std::vector<int>> groups;
+  std::vector<int64_t> npre;
+  const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
+  if (grouping) {
+    // Sequences whose page lists start with the same physical page share a
+    // prefix (the auxiliary branch aliases the main thread's pages).  Group
+    // them, at most max_mem per group, in batch order.
+    std::vector<std::pair<int32_t, int>> open; // (first page, group index)
+    for (int b = 0; b < batch; ++b) {
+      const Seq &q = s->seqs[seqs[b]];
+      if (q.length < s->P) continue; // no full page to share
+      const int32_t first = q.pages[0];
+      int gi = -1;
+      for (auto &o : open)
+        if (o.first == first && (int)groups[o.second].size() < max_mem) {
+          gi = o.second;
+          break;
+        }
+      if (gi < 0) {
+        gi = (int)groups.size();
+        groups.push_back({});
+        open.push_back({first, gi});
+      }
+      groups[gi].push_back(b);
+      group_of[b] = gi;
+    }
+    npre.assign(groups.size(), 0);
+    for (size_t gi = 0; gi < groups.size(); ++gi) {
+      auto &mem = groups[gi];
+      if (mem.size() < 2) {
+        for (int b : mem) group_of[b] = -1;
+        continue;
+      }
+      const Seq &lead = s->seqs[seqs[mem[0]]];
+      int64_t lcp = lead.length / s->P;
+      for (size_t j = 1; j < mem.size(); ++j) {
+        const Seq &o = s->seqs[seqs[mem[j]]];
+        int64_t k = 0;
+        const int64_t lim = std::min<int64_t>(lcp, o.length / s->P);
+        while (k < lim && o.pages[k] == lead.pages[k]) ++k;
+        lcp = k;
+      }
+      npre[gi] = lcp;
+      if (lcp == 0)
+        for (int b : mem) group_of[b] = -1;
+    }
+  }
+
+  auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
+                     const std::vector<int> &members) {
+    PlanSeg ps{};
+    ps.seg.row = row;
+    ps.seg.page0 = page0;
+    ps.seg.ntok = (int32_t)ntok;
+    ps.seg.nmem = (int32_t)members.size();
+    ps.seg.mem = 0;
+    for (size_t j = 0; j < members.size(); ++j) {
+      ps.seg.mem |= (uint32_t)members[j] << (8 * j);
+      ps.members[j] = members[j];
+    }
+    ps.mfma = mfma;
+    plan->segs.push_back(ps);
+  };
+
+  const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma);
+  std::vector<bool> done(groups.size(), false);
+  for (int b = 0; b < batch; ++b) {
+    const Seq &q = s->seqs[seqs[b]];
+    plan->kv_bytes_logical += q.length * tok_bytes;
+    const int gi = group_of[b];
+    if (gi >= 0 && !done[gi]) {
+      done[gi] = true;
+      ++plan->n_groups;
+      const int lead = groups[gi][0];
+      add_seg(seqs[lead], 0, npre[gi] * s->P, true, groups[gi]);
+    }
+    const int64_t start_page = gi >= 0 ? npre[gi] : 0;
+    const int64_t rest = q.length - start_page * s->P;
+    if (rest > 0) add_seg(seqs[b], (int32_t)start_page, rest, single_mfma, {b});
+  }
+
+  // chunking: roughly target_items work items over all segments
+  int64_t work = 0;
+  for (auto &ps : plan->segs) work += (ps.seg.ntok + s->P - 1) / s->P;
+  work *= s->cfg.num_kv_heads;
+  int64_t chunk = std::max<int64_t>(1, (work + s->target_items - 1) / s->target_items);
+  for (;;) {
+    int64_t items = 0;
+    for (auto &ps : plan->segs)
+      items += ((ps.seg.ntok + s->P - 1) / s->P + chunk - 1) / chunk * s->cfg.num_kv_heads;
+    if (items <= sq::kMaxItems) break;
+    chunk = chunk * 2;
+  }
+  plan->chunk_pages = (int)chunk;
+  // items: VALU segments first, then MFMA segments
+  int32_t item = 0;
+  for (int pass = 0; pass < 2; ++pass) {
+    for (auto &ps : plan->segs) {
+      if (ps.mfma != (pass == 1)) continue;
+      const int64_t np = (ps.seg.ntok + s->P - 1) / s->P;
+      ps.seg.nchunk = (int32_t)((np + chunk - 1) / chunk);
+      ps.seg.item0 = item;
+      item += ps.seg.nchunk * s->cfg.num_kv_heads;
+      if (pass == 0) plan->n_items_valu += ps.seg.nchunk * s->cfg.num_kv_heads;
+      else plan->n_items_mfma += ps.seg.nchunk * s->cfg.num_kv_heads;
+      plan->kv_bytes += (int64_t)ps.seg.ntok * tok_bytes;
+      (pass == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += (int64_t)ps.seg.ntok * tok_bytes;
+      plan->io_bytes += np * 4;
+    }
+  }
+  plan->io_bytes += (int64_t)batch * s->cfg.num_q_heads * s->cfg.head_dim * (2 + 4);
+  if ((int)plan->segs.size() > sq::kMaxSegs)
+    return fail(SQ_ERR_INVALID, "decode batch needs %d segments (max %d)", (int)plan->segs.size(),
+                sq::kMaxSegs);
+  return SQ_OK;
+}
+
+} // namespace
+
+// ===========================================================================
+extern "C" {
+
+int32_t sq_abi_version(void) { return SQ_ABI_VERSION; }
+
+const char *sq_last_error(void) { return g_err.c_str(); }
+
+uint64_t sq_workspace_bytes(const sq_store_config *cfg) {
+  if (!shape_ok(cfg, !(cfg && (cfg->flags & SQ_STORE_METADATA_ONLY)), nullptr)) return 0;
+  if (cfg->flags & SQ_STORE_METADATA_ONLY) return 0;
+  return layout_of(*cfg).total;
+}
+
+uint64_t sq_pool_bytes(const sq_store_config *cfg, int32_t which) {
+  if (!shape_ok(cfg, false, nullptr)) return 0;
+  const uint64_t kv = (uint64_t)cfg->num_layers * cfg->num_pages * cfg->num_kv_heads *
+                      cfg->page_size * cfg->head_dim * 2;
+  if (which == 0 || which == 1) return kv;
+  if (which == 2) return (uint64_t)cfg->num_pages * cfg->page_size * 4;
+  return 0;
+}
+
+sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
+  if (!out) return fail(SQ_ERR_INVALID, "null output pointer");
+  const bool device = cfg && !(cfg->flags & SQ_STORE_METADATA_ONLY);
+  std::string why;
+  if (!shape_ok(cfg, device, &why)) return fail(SQ_ERR_INVALID, "bad configuration: %s", why.c_str());
+  Layout lay{};
+  if (device) {
+    if (!cfg->k_pool || !cfg->v_pool || !cfg->pos_pool || !cfg->workspace)
+      return fail(SQ_ERR_INVALID, "device mode needs k_pool, v_pool, pos_pool and workspace");
+    if (((uintptr_t)cfg->k_pool | (uintptr_t)cfg->v_pool | (uintptr_t)cfg->pos_pool |
+         (uintptr_t)cfg->workspace) & 255u)
+      return fail(SQ_ERR_INVALID, "pools and workspace must be 256-byte aligned");
+    lay = layout_of(*cfg);
+    if (cfg->workspace_bytes < lay.total)
+      return fail(SQ_ERR_INVALID, "workspace too small: %llu < %llu bytes",
+                  (unsigned long long)cfg->workspace_bytes, (unsigned long long)lay.total);
+  }
+  sq_store *s = new sq_store();
+  s->cfg = *cfg;
+  s->device = device;
+  s->P = cfg->page_size;
+  s->G = cfg->num_q_heads / cfg->num_kv_heads;
+  s->D = cfg->head_dim;
+  s->refcount.assign(cfg->num_pages, 0);
+  s->freebits.assign((cfg->num_pages + 63) / 64, 0);
+  for (int32_t i = 0; i < cfg->num_pages; ++i) s->freebits[i / 64] |= 1ull << (i % 64);
+  s->n_free = cfg->num_pages;
+  s->seqs.resize(cfg->max_seqs);
+  if (const char *e = std::getenv("SQ_TARGET_ITEMS")) {
+    const int v = std::atoi(e);
+    if (v >= 1) s->target_items = v;
+  }
+  if (const char *e = std::getenv("SQ_AUTO_SINGLE")) s->auto_single_mfma = std::strcmp(e, "valu") != 0;
+  if (device) {
+    s->lay = lay;
+    char *ws = static_cast<char *>(cfg->workspace);
+    s->pt_dev = reinterpret_cast<int32_t *>(ws + lay.pt);
+    s->ev_keep = reinterpret_cast<uint8_t *>(ws + lay.keep);
+    s->ev_dst = reinterpret_cast<int32_t *>(ws + lay.dst);
+    s->ev_src = reinterpret_cast<int32_t *>(ws + lay.src);
+    s->ev_blocks = reinterpret_cast<int32_t *>(ws + lay.blocks);
+    s->ev_upload = reinterpret_cast<int32_t *>(ws + lay.upload);
+    s->part_m = reinterpret_cast<float *>(ws + lay.part_m);
+    s->part_l = reinterpret_cast<float *>(ws + lay.part_l);
+    s->part_acc = reinterpret_cast<float *>(ws + lay.part_acc);
+    sq::Pools &p = s->pools;
+    p.k = static_cast<uint16_t *>(cfg->k_pool);
+    p.v = static_cast<uint16_t *>(cfg->v_pool);
+    p.pos = cfg->pos_pool;
+    p.nl = cfg->num_layers;
+    p.hkv = cfg->num_kv_heads;
+    p.d = cfg->head_dim;
+    p.np = cfg->num_pages;
+    p.head_stride = (int64_t)s->P * s->D;
+    p.page_stride = p.head_stride * cfg->num_kv_heads;
+    p.layer_stride = p.page_stride * cfg->num_pages;
+    void *host = nullptr;
+    hipError_t e = hipHostMalloc(&host, lay.upload_elems * 4, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      delete s;
+      return hip_fail(e, "hipHostMalloc(staging)");
+    }
+    s->staging = static_cast<int32_t *>(host);
+    e = hipEventCreateWithFlags(&s->staging_ev, hipEventDisableTiming);
+    if (e != hipSuccess) {
+      (void)hipHostFree(host);
+      delete s;
+      return hip_fail(e, "hipEventCreate");
+    }
+  }
+  *out = s;
+  return SQ_OK;
+}
+
+sq_status sq_store_destroy(sq_store *s) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  if (s->device) {
+    if (s->staging_pending) (void)hipEventSynchronize(s->staging_ev);
+    for (auto &pp : s->prof_pending) {
+      (void)hipEventSynchronize(pp.b);
+      (void)hipEventDestroy(pp.a);
+      (void)hipEventDestroy(pp.b);
+    }
+    for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
+    if (s->staging_ev) (void)hipEventDestroy(s->staging_ev);
+    if (s->staging) (void)hipHostFree(s->staging);
+  }
+  delete s;
+  return SQ_OK;
+}
+
+sq_status sq_seq_create(sq_store *s, sq_seq *out) {
+  if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
+  for (int32_t h = 0; h < s->cfg.max_seqs; ++h) {
+    if (!s->seqs[h].live) {
+      s->seqs[h] = Seq();
+      s->seqs[h].live = true;
+      ++s->st.live_seqs;
+      *out = h;
+      return SQ_OK;
+    }
+  }
+  return fail(SQ_ERR_INVALID, "all %d sequence handles are live", s->cfg.max_seqs);
+}
+
+sq_status sq_append(sq_store *s, sq_seq h, int32_t n, const void *k_new, const void *v_new,
+                    void *stream) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  if (n < 0) return fail(SQ_ERR_INVALID, "negative token count");
+  if (n == 0) return SQ_OK;
+  const int64_t new_len = q->length + n;
+  const int64_t want = (new_len + s->P - 1) / s->P;
+  if (want > s->cfg.max_pages_per_seq)
+    return fail(SQ_ERR_INVALID, "sequence %d would need %lld pages (max %d)", h, (long long)want,
+                s->cfg.max_pages_per_seq);
+  if (want - (int64_t)q->pages.size() > s->n_free)
+    return fail(SQ_ERR_NO_PAGES, "append needs %lld pages, %lld free",
+                (long long)(want - (int64_t)q->pages.size()), (long long)s->n_free);
+  if (s->device) {
+    if (!k_new || !v_new) return fail(SQ_ERR_INVALID, "null K/V");
+    if (!aligned16(k_new) || !aligned16(v_new)) return fail(SQ_ERR_INVALID, "K/V must be 16-byte aligned");
+    if (q->next_pos + n > INT32_MAX) return fail(SQ_ERR_INVALID, "positions exceed int32");
+  }
+  const int64_t old_len = q->length;
+  const int32_t old_np = (int32_t)q->pages.size();
+  while ((int64_t)q->pages.size() < want) q->pages.push_back(s->alloc_page());
+  runs_append(*q, n);
+  const int64_t pos0 = q->next_pos;
+  q->length = new_len;
+  q->next_pos += n;
+  s->st.append_tokens += n;
+  if (!s->device) return SQ_OK;
+
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  // launches of at most kMaxAppendPages pages each
+  int64_t t = 0;
+  while (t < n) {
+    const int64_t gidx = old_len + t; // global token index
+    const int32_t first_page = (int32_t)(gidx / s->P);
+    const int32_t slot0 = (int32_t)(gidx % s->P);
+    const int64_t room = (int64_t)sq::kMaxAppendPages * s->P - slot0;
+    const int64_t cnt = std::min<int64_t>(room, n - t);
+    sq::AppendArgs a{};
+    a.n_tok = (int32_t)cnt;
+    a.n_total = n;
+    a.tok0 = (int32_t)t;
+    a.slot0 = slot0;
+    a.pos0 = (int32_t)(pos0 + t);
+    a.n_pages = (int32_t)((slot0 + cnt + s->P - 1) / s->P);
+    a.pt_first = first_page;
+    a.new_from = std::max(0, old_np - first_page);
+    a.pt_row = s->pt_row(h);
+    for (int i = 0; i < a.n_pages; ++i) a.page_ids[i] = q->pages[first_page + i];
+    ProfPair pp;
+    const bool on = s->prof_begin(strm, &pp, kProfAppend);
+    hipError_t e = sq::launch_append(s->pools, a, k_new, v_new, strm);
+    s->prof_end(strm, &pp, on);
+    if (e != hipSuccess) return hip_fail(e, "append kernel");
+    t += cnt;
+  }
+  return SQ_OK;
+}
+
+sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const void *k_new,
+                          const void *v_new, void *stream) {
+  if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
+  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
+  int64_t need = 0;
+  for (int b = 0; b < batch; ++b) {
+    Seq *q = s->get(seqs[b]);
+    if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
+    for (int c = 0; c < b; ++c)
+      if (seqs[c] == seqs[b]) return fail(SQ_ERR_INVALID, "sequence %d repeated in the batch", seqs[b]);
+    if (q->length % s->P == 0) {
+      if (q->length / s->P + 1 > s->cfg.max_pages_per_seq)
+        return fail(SQ_ERR_INVALID, "sequence %d is at its page-list capacity", seqs[b]);
+      ++need;
+    }
+    if (s->device && q->next_pos + 1 > INT32_MAX) return fail(SQ_ERR_INVALID, "positions exceed int32");
+  }
+  if (need > s->n_free) return fail(SQ_ERR_NO_PAGES, "append needs %lld pages, %lld free",
+                                    (long long)need, (long long)s->n_free);
+  if (s->device) {
+    if (!k_new || !v_new) return fail(SQ_ERR_INVALID, "null K/V");
+    if (!aligned16(k_new) || !aligned16(v_new)) return fail(SQ_ERR_INVALID, "K/V must be 16-byte aligned");
+  }
+  sq::AppendBatchArgs a{};
+  a.n = batch;
+  a.pt = s->pt_dev;
+  for (int b = 0; b < batch; ++b) {
+    Seq &q = s->seqs[seqs[b]];
+    a.pt_index[b] = -1;
+    if (q.length % s->P == 0) {
+      q.pages.push_back(s->alloc_page());
+      a.pt_index[b] = seqs[b] * s->cfg.max_pages_per_seq + (int32_t)q.pages.size() - 1;
+    }
+    a.page[b] = q.pages[q.length / s->P];
+    a.slot[b] = (int32_t)(q.length % s->P);
+    a.pos[b] = (int32_t)q.next_pos;
+    runs_append(q, 1);
+    q.length += 1;
+    q.next_pos += 1;
+  }
+  s->st.append_tokens += batch;
+  if (!s->device) return SQ_OK;
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  ProfPair pp;
+  const bool on = s->prof_begin(strm, &pp, kProfAppend);
+  hipError_t e = sq::launch_append_batch(s->pools, a, k_new, v_new, strm);
+  s->prof_end(strm, &pp, on);
+  if (e != hipSuccess) return hip_fail(e, "append_batch kernel");
+  return SQ_OK;
+}
+
+sq_status sq_span_mark(sq_store *s, sq_seq h, int32_t cursor, int64_t start, int64_t end) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  if (cursor < 0 || q->spans.count(cursor))
+    return fail(SQ_ERR_INVALID, "cursor %d negative or already registered", cursor);
+  if (!(0 <= start && start <= end && end <= q->length))
+    return fail(SQ_ERR_SPAN, "span [%lld, %lld) outside [0, %lld]", (long long)start,
+                (long long)end, (long long)q->length);
+  if (end > start) {
+    auto it = q->nonempty.lower_bound(start);
+    if (it != q->nonempty.end() && it->first < end)
+      return fail(SQ_ERR_SPAN, "span overlaps [%lld, %lld)", (long long)it->first, (long long)it->second);
+    if (it != q->nonempty.begin()) {
+      --it;
+      if (it->second > start)
+        return fail(SQ_ERR_SPAN, "span overlaps [%lld, %lld)", (long long)it->first, (long long)it->second);
+    }
+    q->nonempty[start] = end;
+  }
+  q->spans[cursor] = {start, end};
+  return SQ_OK;
+}
+
+sq_status sq_fork(sq_store *s, sq_seq parent, int64_t fork_len, sq_seq *child, void *stream) {
+  if (!s || !child) return fail(SQ_ERR_INVALID, "null argument");
+  Seq *par = s->get(parent);
+  if (!par) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", parent);
+  if (!(0 <= fork_len && fork_len <= par->length))
+    return fail(SQ_ERR_INVALID, "fork point %lld outside [0, %lld]", (long long)fork_len,
+                (long long)par->length);
+  int32_t h = -1;
+  for (int32_t i = 0; i < s->cfg.max_seqs; ++i)
+    if (!s->seqs[i].live) {
+      h = i;
+      break;
+    }
+  if (h < 0) return fail(SQ_ERR_INVALID, "all %d sequence handles are live", s->cfg.max_seqs);
+  const int64_t full = fork_len / s->P;
+  const int64_t tail = fork_len % s->P;
+  if (tail && s->n_free < 1) return fail(SQ_ERR_NO_PAGES, "no page for the fork's tail copy");
+
+  Seq c;
+  c.live = true;
+  c.pages.assign(par->pages.begin(), par->pages.begin() + full);
+  for (int32_t p : c.pages) ++s->refcount[p];
+  int32_t tail_page = -1;
+  if (tail) {
+    tail_page = s->alloc_page();
+    c.pages.push_back(tail_page);
+  }
+  c.length = fork_len;
+  c.runs = runs_truncate(par->runs, fork_len);
+  c.next_pos = fork_len == par->length ? par->next_pos : pos_at(*par, fork_len);
+  for (auto &kv : par->spans)
+    if (kv.second.second <= fork_len) {
+      c.spans[kv.first] = kv.second;
+      if (kv.second.second > kv.second.first) c.nonempty[kv.second.first] = kv.second.second;
+    }
+  c.parent = parent;
+  const int32_t src_tail_page = tail ? par->pages[full] : -1;
+  s->seqs[h] = std::move(c);
+  ++s->st.live_seqs;
+  ++s->st.fork_calls;
+  if (tail) ++s->st.fork_tail_copies;
+  *child = h;
+  if (!s->device) return SQ_OK;
+
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  hipError_t e = sq::launch_copy_i32(s->pt_row(h), s->pt_row(parent), (int32_t)full, -1,
+                                     tail_page, strm);
+  if (e != hipSuccess) return hip_fail(e, "fork page-table copy");
+  if (tail) {
+    e = sq::launch_copy_page(s->pools, src_tail_page, tail_page, strm);
+    if (e != hipSuccess) return hip_fail(e, "fork tail copy");
+  }
+  return SQ_OK;
+}
+
+sq_status sq_release(sq_store *s, sq_seq h) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  for (int32_t p : q->pages) s->unref(p, nullptr);
+  *q = Seq();
+  --s->st.live_seqs;
+  return SQ_OK;
+}
+
+sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32_t n,
+                         void *stream, sq_evict_stats *stats) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  if (n < 0 || n > SQ_MAX_EVICT_SPANS)
+    return fail(SQ_ERR_INVALID, "cursor count %d outside [0, %d]", n, SQ_MAX_EVICT_SPANS);
+  if (n > 0 && !cursor_ids) return fail(SQ_ERR_INVALID, "null cursor list");
+  std::vector<int32_t> ids(cursor_ids, cursor_ids + n);
+  std::sort(ids.begin(), ids.end());
+  ids.erase(std::unique(ids.begin(), ids.end()), ids.end());
+  for (int32_t c : ids)
+    if (!q->spans.count(c)) return fail(SQ_ERR_UNKNOWN_CURSOR, "cursor %d not registered on sequence %d", c, h);
+  std::vector<std::pair<int64_t, int64_t>> sp;
+  for (int32_t c : ids) {
+    auto se = q->spans[c];
+    if (se.second > se.first) sp.push_back(se);
+  }
+  std::sort(sp.begin(), sp.end());
+  sq_evict_stats es{};
+  es.first_evicted = q->length;
+  const int64_t L = q->length;
+  if (sp.empty()) {
+    for (int32_t c : ids) q->spans.erase(c);
+    if (stats) *stats = es;
+    return SQ_OK;
+  }
+  int64_t removed = 0;
+  std::vector<int64_t> prefix(sp.size());
+  for (size_t i = 0; i < sp.size(); ++i) {
+    prefix[i] = removed;
+    removed += sp[i].second - sp[i].first;
+  }
+  const int64_t Lp = L - removed;
+  const int64_t f = sp[0].first;
+  const int64_t fp = f / s->P;
+  const int64_t new_np = (Lp + s->P - 1) / s->P;
+  const int64_t n_new = new_np - fp;
+  if (n_new > s->n_free)
+    return fail(SQ_ERR_NO_PAGES, "eviction needs %lld fresh pages, %lld free", (long long)n_new,
+                (long long)s->n_free);
+
+  // ---- commit: allocate, gather, release ----
+  std::vector<int32_t> new_ids(n_new);
+  for (int64_t i = 0; i < n_new; ++i) new_ids[i] = s->alloc_page();
+  std::vector<int32_t> old_tail(q->pages.begin() + fp, q->pages.end());
+
+  if (s->device) {
+    hipStream_t strm = static_cast<hipStream_t>(stream);
+    s->last_stream = strm;
+    // upload: spans [2 * nsp] | old page ids from fp [n_old] | new page ids [n_new]
+    std::vector<int32_t> up;
+    up.reserve(2 * sp.size() + old_tail.size() + new_ids.size());
+    for (auto &x : sp) {
+      up.push_back((int32_t)x.first);
+      up.push_back((int32_t)x.second);
+    }
+    const size_t off_old = up.size();
+    up.insert(up.end(), old_tail.begin(), old_tail.end());
+    const size_t off_new = up.size();
+    up.insert(up.end(), new_ids.begin(), new_ids.end());
+    sq_status us = upload(s, s->ev_upload, up.data(), up.size(), strm);
+    if (us != SQ_OK) return us;
+    sq::EvictArgs ea{};
+    ea.n_tokens = (int32_t)L;
+    ea.n_spans = (int32_t)sp.size();
+    ea.spans = s->ev_upload;
+    ea.keep = s->ev_keep;
+    ea.dst = s->ev_dst;
+    ea.src_of = s->ev_src;
+    ea.blocks = s->ev_blocks;
+    ProfPair pp;
+    bool on = s->prof_begin(strm, &pp, kProfScan);
+    hipError_t e = sq::launch_evict_scan(ea, strm);
+    s->prof_end(strm, &pp, on);
+    if (e != hipSuccess) return hip_fail(e, "eviction scan");
+    sq::GatherArgs ga{};
+    ga.fp = (int32_t)fp;
+    ga.n_new = (int32_t)n_new;
+    ga.new_len = (int32_t)Lp;
+    ga.src_of = s->ev_src;
+    ga.old_ids = s->ev_upload + off_old;
+    ga.new_ids = s->ev_upload + off_new;
+    ga.pt_row = s->pt_row(h);
+    on = s->prof_begin(strm, &pp, kProfGather);
+    e = sq::launch_evict_gather(s->pools, ga, strm);
+    s->prof_end(strm, &pp, on);
+    if (e != hipSuccess) return hip_fail(e, "eviction gather");
+    s->have_last_evict = true;
+    s->last_evict_L = L;
+    s->last_evict_Lp = Lp;
+  }
+
+  int64_t freed = 0;
+  for (int32_t p : old_tail) s->unref(p, &freed);
+  q->pages.resize(fp);
+  q->pages.insert(q->pages.end(), new_ids.begin(), new_ids.end());
+  // positions: drop the evicted index ranges, re-index the rest
+  {
+    std::vector<PosRun> out;
+    size_t k = 0;
+    for (const PosRun &r : q->runs) {
+      int64_t i = r.idx0;
+      const int64_t iend = r.idx0 + r.n;
+      while (i < iend) {
+        while (k < sp.size() && sp[k].second <= i) ++k;
+        int64_t stop = iend;
+        if (k < sp.size()) {
+          if (sp[k].first <= i) { // inside an evicted span: skip it
+            i = std::min(iend, sp[k].second);
+            continue;
+          }
+          stop = std::min(stop, sp[k].first);
+        }
+        const int64_t ni = i - evicted_before(sp, prefix, i);
+        const int64_t np = r.pos0 + (i - r.idx0);
+        if (!out.empty() && out.back().idx0 + out.back().n == ni &&
+            out.back().pos0 + out.back().n == np)
+          out.back().n += stop - i;
+        else
+          out.push_back({ni, np, stop - i});
+        i = stop;
+      }
+    }
+    q->runs = std::move(out);
+  }
+  q->length = Lp;
+  for (int32_t c : ids) q->spans.erase(c);
+  q->nonempty.clear();
+  for (auto &kv : q->spans) {
+    auto &se = kv.second;
+    const int64_t ns = se.first - evicted_before(sp, prefix, se.first);
+    const int64_t ne = se.second - evicted_before(sp, prefix, se.second);
+    se = {ns, ne};
+    if (ne > ns) q->nonempty[ns] = ne;
+  }
+  const int64_t moved = Lp - fp * s->P;
+  const int64_t per_tok = (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2 + 4;
+  es.tokens_removed = removed;
+  es.tokens_moved = moved;
+  es.bytes_moved = moved * per_tok;
+  es.pages_allocated = n_new;
+  es.pages_freed = freed;
+  es.first_evicted = f;
+  ++s->st.evict_calls;
+  s->st.evict_tokens_removed += removed;
+  s->st.evict_tokens_moved += moved;
+  s->st.evict_bytes_moved += es.bytes_moved;
+  if (stats) *stats = es;
+  return SQ_OK;
+}
+
+sq_status sq_decode_plan_info(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,
+                              sq_plan_info *out) {
+  if (!s || !seqs || !out) return fail(SQ_ERR_INVALID, "null argument");
+  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
+  if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
+  for (int b = 0; b < batch; ++b)
+    if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
+  Plan plan;
+  sq_status r = build_plan(s, seqs, batch, mode, &plan);
+  if (r != SQ_OK) return r;
+  *out = sq_plan_info{};
+  out->n_segments = (int32_t)plan.segs.size();
+  out->n_groups = plan.n_groups;
+  out->n_items_valu = plan.n_items_valu;
+  out->n_items_mfma = plan.n_items_mfma;
+  out->chunk_pages = plan.chunk_pages;
+  out->kv_bytes = plan.kv_bytes;
+  out->kv_bytes_logical = plan.kv_bytes_logical;
+  out->kv_bytes_valu = plan.kv_bytes_valu;
+  out->kv_bytes_mfma = plan.kv_bytes_mfma;
+  out->io_bytes = plan.io_bytes;
+  return SQ_OK;
+}
+
+sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
+                         const void *q, float *out, float scale, int32_t mode, void *stream) {
+  if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
+  if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
+  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
+  if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
+  if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
+  if (!q || !out || !aligned16(q) || !aligned16(out))
+    return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
+  for (int b = 0; b < batch; ++b)
+    if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
+  Plan plan;
+  sq_status r = build_plan(s, seqs, batch, mode, &plan);
+  if (r != SQ_OK) return r;
+
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  sq::DecodeArgs base{};
+  base.q = static_cast<const uint16_t *>(q);
+  base.k = s->pools.k + layer * s->pools.layer_stride;
+  base.v = s->pools.v + layer * s->pools.layer_stride;
+  base.pt = s->pt_dev;
+  base.part_m = s->part_m;
+  base.part_l = s->part_l;
+  base.part_acc = s->part_acc;
+  base.page_stride = s->pools.page_stride;
+  base.max_pages = s->cfg.max_pages_per_seq;
+  base.hq = s->cfg.num_q_heads;
+  base.chunk_pages = plan.chunk_pages;
+  base.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  sq::MergeArgs ma{};
+  ma.out = out;
+  ma.part_m = s->part_m;
+  ma.part_l = s->part_l;
+  ma.part_acc = s->part_acc;
+  ma.hq = s->cfg.num_q_heads;
+  ma.group = s->G;
+  for (const PlanSeg &ps : plan.segs)
+    for (int j = 0; j < ps.seg.nmem; ++j) {
+      const int b = ps.members[j];
+      const int e = ma.n_src[b]++;
+      ma.item_base[b][e] = ps.seg.item0;
+      ma.nchunk[b][e] = ps.seg.nchunk;
+      ma.member[b][e] = j;
+    }
+  for (int pass = 0; pass < 2; ++pass) {
+    sq::DecodeArgs a = base;
+    a.n_segs = 0;
+    for (const PlanSeg &ps : plan.segs)
+      if (ps.mfma == (pass == 1)) a.segs[a.n_segs++] = ps.seg;
+    a.item_begin = pass == 0 ? 0 : plan.n_items_valu;
+    a.n_items = pass == 0 ? plan.n_items_valu : plan.n_items_mfma;
+    if (a.n_items == 0) continue;
+    ProfPair pp;
+    const bool on = s->prof_begin(strm, &pp, pass == 0 ? kProfValu : kProfMfma);
+    hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, a, strm)
+                             : sq::launch_decode_mfma(s->D, s->G, a, strm);
+    s->prof_end(strm, &pp, on);
+    if (e != hipSuccess) return hip_fail(e, "decode kernel");
+  }
+  ProfPair pp;
+  const bool on = s->prof_begin(strm, &pp, kProfMerge);
+  hipError_t e = sq::launch_decode_merge(s->D, batch, ma, strm);
+  s->prof_end(strm, &pp, on);
+  if (e != hipSuccess) return hip_fail(e, "decode merge");
+  ++s->st.decode_calls;
+  s->st.decode_kv_bytes += plan.kv_bytes;
+  s->st.decode_kv_bytes_logical += plan.kv_bytes_logical;
+  return SQ_OK;
+}
+
+sq_status sq_seq_info(sq_store *s, sq_seq h, sq_seq_desc *out) {
+  if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  *out = sq_seq_desc{};
+  out->length = q->length;
+  out->next_pos = q->next_pos;
+  out->n_pages = (int32_t)q->pages.size();
+  out->parent = q->parent;
+  out->n_spans = (int32_t)q->spans.size();
+  return SQ_OK;
+}
+
+sq_status sq_page_table(sq_store *s, sq_seq h, int32_t *out, int32_t cap, int32_t *n) {
+  if (!s || !n) return fail(SQ_ERR_INVALID, "null argument");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  *n = (int32_t)q->pages.size();
+  for (int32_t i = 0; i < std::min(cap, *n); ++i) out[i] = q->pages[i];
+  return SQ_OK;
+}
+
+sq_status sq_positions(sq_store *s, sq_seq h, int64_t *out, int64_t cap, int64_t *n) {
+  if (!s || !n) return fail(SQ_ERR_INVALID, "null argument");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  *n = q->length;
+  int64_t i = 0;
+  for (const PosRun &r : q->runs)
+    for (int64_t j = 0; j < r.n && i < cap; ++j, ++i) out[i] = r.pos0 + j;
+  return SQ_OK;
+}
+
+sq_status sq_seq_spans(sq_store *s, sq_seq h, int32_t *cursors, int64_t *starts, int64_t *ends,
+                       int32_t cap, int32_t *n) {
+  if (!s || !n) return fail(SQ_ERR_INVALID, "null argument");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  *n = (int32_t)q->spans.size();
+  int32_t i = 0;
+  for (auto &kv : q->spans) {
+    if (i >= cap) break;
+    cursors[i] = kv.first;
+    starts[i] = kv.second.first;
+    ends[i] = kv.second.second;
+    ++i;
+  }
+  return SQ_OK;
+}
+
+sq_status sq_refcounts(sq_store *s, int32_t *out, int32_t cap) {
+  if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
+  for (int32_t i = 0; i < std::min(cap, s->cfg.num_pages); ++i) out[i] = s->refcount[i];
+  return SQ_OK;
+}
+
+sq_status sq_stats_get(sq_store *s, sq_stats *out) {
+  if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
+  *out = s->st;
+  out->live_pages = s->live_pages();
+  out->peak_pages = s->peak_pages;
+  out->free_pages = s->n_free;
+  return SQ_OK;
+}
+
+sq_status sq_debug_last_evict(sq_store *s, uint8_t *keep, int32_t *dst, int32_t *src_of,
+                              int64_t cap, int64_t *n_tokens, int64_t *n_kept) {
+  if (!s || !keep || !dst || !src_of || !n_tokens || !n_kept) return fail(SQ_ERR_INVALID, "null argument");
+  if (!s->device || !s->have_last_evict) return fail(SQ_ERR_INVALID, "no eviction has moved tokens yet");
+  if (cap < s->last_evict_L) return fail(SQ_ERR_INVALID, "cap %lld < %lld tokens", (long long)cap,
+                                         (long long)s->last_evict_L);
+  hipStream_t strm = s->last_stream;
+  hipError_t e = hipMemcpyAsync(keep, s->ev_keep, s->last_evict_L, hipMemcpyDeviceToHost, strm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(dst, s->ev_dst, s->last_evict_L * 4, hipMemcpyDeviceToHost, strm);
+  if (e == hipSuccess)
+    e = hipMemcpyAsync(src_of, s->ev_src, s->last_evict_Lp * 4, hipMemcpyDeviceToHost, strm);
+  if (e == hipSuccess) e = hipStreamSynchronize(strm);
+  if (e != hipSuccess) return hip_fail(e, "debug copy");
+  *n_tokens = s->last_evict_L;
+  *n_kept = s->last_evict_Lp;
+  return SQ_OK;
+}
+
+sq_status sq_profile_enable(sq_store *s, int32_t on) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  if (!s->device && on) return fail(SQ_ERR_INVALID, "metadata-only store has no kernels to time");
+  s->prof_on = on != 0;
+  return SQ_OK;
+}
+
+sq_status sq_profile_read(sq_store *s, sq_profile *out) {
+  if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
+  for (auto &pp : s->prof_pending) {
+    hipError_t e = hipEventSynchronize(pp.b);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(profile)");
+    float ms = 0.f;
+    e = hipEventElapsedTime(&ms, pp.a, pp.b);
+    if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    s->prof_ms[pp.kind] += ms;
+    s->prof_n[pp.kind] += 1;
+    s->ev_pool.push_back(pp.a);
+    s->ev_pool.push_back(pp.b);
+  }
+  s->prof_pending.clear();
+  *out = sq_profile{};
+  out->decode_valu_ms = s->prof_ms[kProfValu];
+  out->decode_mfma_ms = s->prof_ms[kProfMfma];
+  out->decode_merge_ms = s->prof_ms[kProfMerge];
+  out->evict_scan_ms = s->prof_ms[kProfScan];
+  out->evict_gather_ms = s->prof_ms[kProfGather];
+  out->append_ms = s->prof_ms[kProfAppend];
+  out->decode_valu_launches = s->prof_n[kProfValu];
+  out->decode_mfma_launches = s->prof_n[kProfMfma];
+  out->decode_merge_launches = s->prof_n[kProfMerge];
+  out->evict_scan_launches = s->prof_n[kProfScan];
+  out->evict_gather_launches = s->prof_n[kProfGather];
+  out->append_launches = s->prof_n[kProfAppend];
+  for (int k = 0; k < kProfKinds; ++k) {
+    s->prof_ms[k] = 0;
+    s->prof_n[k] = 0;
+  }
+  return SQ_OK;
+}
+
+} // extern "C"

@@ -1,0 +1,260 @@
+"""Host logic of libsq against the oracle's page model (CPU only).
+
+A metadata-only store runs every bookkeeping step of the library (allocator,
+refcounts, page lists, positions, spans, eviction planning, decode planning)
+without a GPU; page tables, refcounts, positions and spans must match the
+oracle bit for bit, and failing calls must fail the same way and change
+nothing.
+"""
+
+import math
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import pages as pg
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def sq():
+    from paper_2602_22603_amd import build_lib, sq as sqmod
+    if not os.path.exists(sqmod.LIB_PATH):
+        build_lib.build()
+    sqmod.lib()
+    return sqmod
+
+
+ERR_KIND = {1: pg.Invalid, 2: pg.NoPages, 3: pg.UnknownSeq, 4: pg.UnknownCursor, 5: pg.SpanError}
+
+
+def test_library_exports_every_declared_symbol(sq):
+    header = open(os.path.join(ROOT, "include", "sq.h")).read()
+    declared = set(re.findall(r"^\s*(?:[\w\s\*]+?)\b(sq_\w+)\s*\(", header, flags=re.M))
+    declared -= {"sq_store", "sq_seq"}
+    assert len(declared) >= 20
+    lib = sq.lib()
+    for name in sorted(declared):
+        assert hasattr(lib, name), name
+    assert declared == set(sq.EXPORTED)
+    assert lib.sq_abi_version() == 1
+
+
+def _store(sq, num_pages, page, max_seqs, max_pages):
+    return sq.Store(num_layers=2, num_q_heads=4, num_kv_heads=2, head_dim=8,
+                    num_pages=num_pages, max_seqs=max_seqs, max_pages_per_seq=max_pages,
+                    page_size=page, metadata_only=True)
+
+
+def _compare(store, model):
+    assert store.refcounts().tolist() == model.refcount.tolist()
+    st = store.stats()
+    ms = model.stats()
+    assert (st["live_pages"], st["peak_pages"], st["free_pages"], st["live_seqs"]) == (
+        ms["live_pages"], ms["peak_pages"], ms["free_pages"], ms["live_seqs"])
+    for h in model.seqs:
+        assert store.page_table(h) == model.page_table(h)
+        info = store.seq_info(h)
+        want = model.info(h)
+        for k in ("length", "next_pos", "n_pages", "parent", "n_spans"):
+            assert info[k] == want[k], (k, info[k], want[k])
+        assert store.positions(h).tolist() == model.view(h)[2].tolist()
+        assert store.spans(h) == model.spans(h)
+
+
+def _both(store, model, sq, fn_store, fn_model):
+    """Run one op on both; same outcome (value or error kind)."""
+    try:
+        want = fn_model()
+        err_m = None
+    except pg.OracleError as e:
+        want, err_m = None, type(e)
+    try:
+        got = fn_store()
+        err_s = None
+    except sq.SqError as e:
+        got, err_s = None, ERR_KIND[e.code]
+    assert err_s == err_m, (err_s, err_m)
+    return got, want
+
+
+@pytest.mark.parametrize("page", [1, 2, 4, 16])
+@pytest.mark.parametrize("seed", [0, 1])
+def test_random_ops_match_oracle(sq, page, seed):
+    rng = np.random.default_rng(100 + seed * 7 + page)
+    num_pages, max_seqs, max_pages = 300 // page + 40, 5, 400 // page + 8
+    store = _store(sq, num_pages, page, max_seqs, max_pages)
+    model = pg.PageModel(num_pages, page, max_seqs, max_pages)
+    cursor = 0
+    h0, _ = _both(store, model, sq, store.seq_create, model.seq_create)
+    for _ in range(250):
+        live = sorted(model.seqs)
+        h = int(rng.choice(live)) if live else 0
+        op = rng.choice(["append", "append", "mark", "mark", "fork", "evict", "release",
+                         "bad"])
+        if op == "append":
+            n = int(rng.integers(0, 3 * page + 5))
+            _both(store, model, sq, lambda: store.append(h, n=n), lambda: model.append(h, n))
+        elif op == "mark":
+            length = model.info(h)["length"]
+            s = int(rng.integers(0, length + 1))
+            e = int(rng.integers(s, min(length, s + 40) + 1))
+            c = cursor if rng.random() < 0.9 else int(rng.integers(0, cursor + 1))
+            _both(store, model, sq, lambda: store.span_mark(h, c, s, e),
+                  lambda: model.span_mark(h, c, s, e))
+            cursor += 1
+        elif op == "fork":
+            f = int(rng.integers(0, model.info(h)["length"] + 2))
+            _both(store, model, sq, lambda: store.fork(h, f), lambda: model.fork(h, f))
+        elif op == "evict":
+            cur = list(model.spans(h))
+            pick = [c for c in cur if rng.random() < 0.4]
+            if rng.random() < 0.1:
+                pick.append(10_000 + cursor)  # unknown cursor
+            pick += pick[:1]                   # a duplicate
+            got, want = _both(store, model, sq, lambda: store.evict(h, pick),
+                              lambda: model.evict(h, pick))
+            if want is not None:
+                for k in want:
+                    assert got[k] == want[k], (k, got, want)
+        elif op == "release" and len(live) > 1:
+            _both(store, model, sq, lambda: store.release(h), lambda: model.release(h))
+        elif op == "bad":
+            _both(store, model, sq, lambda: store.release(99), lambda: model.release(99))
+        _compare(store, model)
+    for h in list(model.seqs):
+        store.release(h)
+        model.release(h)
+    _compare(store, model)
+    assert store.stats()["live_pages"] == 0
+
+
+def test_hand_worked_page_tables(sq):
+    s = _store(sq, 16, 4, 4, 16)
+    a = s.seq_create()
+    s.append(a, n=10)
+    assert s.page_table(a) == [0, 1, 2]
+    b = s.fork(a, 8)
+    c = s.fork(a, 6)
+    assert (b, c) == (1, 2) and s.page_table(b) == [0, 1] and s.page_table(c) == [0, 3]
+    s.append(b, n=3)
+    s.span_mark(a, 7, 1, 6)
+    st = s.evict(a, [7])
+    assert s.page_table(a) == [5, 6]
+    assert (st["tokens_removed"], st["tokens_moved"], st["pages_allocated"],
+            st["pages_freed"], st["first_evicted"]) == (5, 5, 2, 1, 1)
+    assert st["bytes_moved"] == 5 * (2 * 2 * 8 * 2 * 2 + 4)
+    s.release(c)
+    s.append(a, n=4)
+    assert s.page_table(a) == [5, 6, 2]
+    assert s.positions(a).tolist() == [0, 6, 7, 8, 9, 10, 11, 12, 13]
+    assert s.stats()["peak_pages"] == 7
+
+
+def test_error_paths_leave_state_unchanged(sq):
+    s = _store(sq, 6, 4, 2, 8)
+    m = pg.PageModel(6, 4, 2, 8)
+    a = s.seq_create()
+    m.seq_create()
+    s.append(a, n=14)
+    m.append(a, 14)
+    for c, (x, y) in enumerate([(0, 3), (8, 14)]):
+        s.span_mark(a, c, x, y)
+        m.span_mark(a, c, x, y)
+    cases = [
+        (lambda: s.append(a, n=11), lambda: m.append(a, 11)),
+        (lambda: s.append(a, n=19), lambda: m.append(a, 19)),
+        (lambda: s.append(9, n=1), lambda: m.append(9, 1)),
+        (lambda: s.append(a, n=-1), lambda: m.append(a, -1)),
+        (lambda: s.span_mark(a, 2, 2, 5), lambda: m.span_mark(a, 2, 2, 5)),
+        (lambda: s.span_mark(a, 0, 4, 5), lambda: m.span_mark(a, 0, 4, 5)),
+        (lambda: s.span_mark(a, 3, 10, 15), lambda: m.span_mark(a, 3, 10, 15)),
+        (lambda: s.span_mark(a, -1, 4, 5), lambda: m.span_mark(a, -1, 4, 5)),
+        (lambda: s.evict(a, [0, 5]), lambda: m.evict(a, [0, 5])),
+        (lambda: s.fork(a, 15), lambda: m.fork(a, 15)),
+        (lambda: s.fork(a, -1), lambda: m.fork(a, -1)),
+        (lambda: s.release(7), lambda: m.release(7)),
+    ]
+    for fs, fm in cases:
+        before = (s.page_table(a), s.refcounts().tolist(), s.spans(a), s.stats())
+        _both(s, m, sq, fs, fm)
+        assert before == (s.page_table(a), s.refcounts().tolist(), s.spans(a), s.stats())
+    # pool exhaustion for an eviction: fill the pool, then ask for fresh pages
+    b = s.fork(a, 13)
+    m.fork(a, 13)
+    s.append(b, n=4)
+    m.append(b, 4)
+    _compare(s, m)
+    assert s.stats()["free_pages"] == 0
+    s.span_mark(a, 9, 4, 6)
+    m.span_mark(a, 9, 4, 6)
+    before = (s.page_table(a), s.refcounts().tolist(), s.spans(a))
+    with pytest.raises(sq.SqError) as ei:
+        s.evict(a, [9])
+    assert ei.value.code == sq.ERR_NO_PAGES
+    with pytest.raises(pg.NoPages):
+        m.evict(a, [9])
+    assert before == (s.page_table(a), s.refcounts().tolist(), s.spans(a))
+
+
+def test_invalid_configurations(sq):
+    with pytest.raises(sq.SqError):
+        sq.Store(1, 3, 2, 8, 16, 2, 4, page_size=4, metadata_only=True)  # 3 % 2
+    with pytest.raises(sq.SqError):
+        sq.Store(1, 4, 1, 8, 0, 2, 4, page_size=4, metadata_only=True)
+    cfg = sq.StoreConfig(1, 4, 1, 96, 16, 64, 2, 8)  # head_dim 96: no device kernels
+    assert sq.lib().sq_workspace_bytes(cfg) == 0
+    cfg = sq.StoreConfig(1, 4, 1, 64, 8, 64, 2, 8)   # page size 8: device needs 16
+    assert sq.lib().sq_workspace_bytes(cfg) == 0
+    cfg = sq.StoreConfig(1, 4, 1, 64, 16, 64, 2, 8)
+    assert sq.lib().sq_workspace_bytes(cfg) > 0
+
+
+def test_decode_plan_shared_prefix_bytes(sq):
+    """Eight tasks at 128K: main + auxiliary share their first 8176 pages; the
+    shared-prefix plan reads each shared page once."""
+    tasks, main_len, fork_at, aux = 8, 131072, 130816, 512
+    per_task_pages = main_len // 16 + aux // 16
+    s = sq.Store(1, 32, 8, 128, num_pages=tasks * per_task_pages + 64, max_seqs=32,
+                 max_pages_per_seq=main_len // 16 + 64, page_size=16, metadata_only=True)
+    batch = []
+    for _ in range(tasks):
+        m = s.seq_create()
+        s.append(m, n=fork_at)
+        a = s.fork(m, fork_at)
+        s.append(m, n=main_len - fork_at)
+        s.append(a, n=aux)
+        batch += [m, a]
+    tok = 8 * 128 * 2 * 2
+    info = s.plan_info(batch, sq.ATTN_AUTO)
+    assert info["n_groups"] == tasks
+    assert info["kv_bytes"] == tasks * (main_len + aux) * tok == 4_311_744_512
+    assert info["kv_bytes_logical"] == tasks * (main_len + fork_at + aux) * tok == 8_598_323_200
+    stream = s.plan_info(batch, sq.ATTN_STREAM)
+    assert stream["n_groups"] == 0 and stream["n_items_mfma"] == 0
+    assert stream["kv_bytes"] == stream["kv_bytes_logical"] == info["kv_bytes_logical"]
+    assert info["n_items_valu"] + info["n_items_mfma"] <= 16384
+    mf = s.plan_info(batch, sq.ATTN_MFMA)
+    assert mf["n_items_valu"] == 0 and mf["kv_bytes"] == info["kv_bytes_logical"]
+    assert math.isclose(info["kv_bytes"] / info["kv_bytes_logical"], 0.5014, rel_tol=1e-3)
+
+
+def test_decode_plan_after_eviction(sq):
+    """After the main thread evicts, main and auxiliary share only the pages
+    before the first evicted one."""
+    s = sq.Store(1, 32, 8, 128, num_pages=400, max_seqs=4, max_pages_per_seq=200,
+                 page_size=16, metadata_only=True)
+    m = s.seq_create()
+    s.append(m, n=1000)
+    a = s.fork(m, 1000)
+    s.span_mark(m, 0, 330, 500)
+    s.evict(m, [0])
+    pt_m, pt_a = s.page_table(m), s.page_table(a)
+    assert pt_m[:20] == pt_a[:20] and pt_m[20] != pt_a[20]
+    info = s.plan_info([m, a], sq.ATTN_AUTO)
+    tok = 8 * 128 * 2 * 2
+    assert info["n_groups"] == 1
+    assert info["kv_bytes"] == (20 * 16 + (830 - 320) + (1000 - 320)) * tok
