@@ -81,32 +81,6 @@ def read_traffic(name):
         return None
 
 
-def build_shared(sq, torch, wl, tasks, ctx, extra_tokens):
-    w = wl.shared128k(n_tasks=tasks, main_len=ctx, fork_at=ctx - 256, aux_private=512)
-    pages_task = ctx // 16 + w.aux_private // 16 + 2 * (extra_tokens // 16 + 2)
-    store = sq.Store(1, 32, 8, 128, num_pages=tasks * pages_task + 64, max_seqs=2 * tasks + 4,
-                     max_pages_per_seq=ctx // 16 + extra_tokens // 16 + 64)
-    seqs, sample = [], None
-    for t in range(tasks):
-        k = wl.device_normal_bf16((1, ctx, 8, 128), w.seed * 1000 + 4 * t, "cuda")
-        v = wl.device_normal_bf16((1, ctx, 8, 128), w.seed * 1000 + 4 * t + 1, "cuda")
-        ka = wl.device_normal_bf16((1, w.aux_private, 8, 128), w.seed * 1000 + 4 * t + 2, "cuda")
-        va = wl.device_normal_bf16((1, w.aux_private, 8, 128), w.seed * 1000 + 4 * t + 3, "cuda")
-        main = store.seq_create()
-        store.append(main, k[:, : w.fork_at], v[:, : w.fork_at])
-        aux = store.fork(main, w.fork_at)
-        store.append(main, k[:, w.fork_at:], v[:, w.fork_at:])
-        store.append(aux, ka, va)
-        seqs += [main, aux]
-        if t == 0:
-            sample = (k, v)
-        torch.cuda.synchronize()
-        del ka, va
-        if t:
-            del k, v
-    return store, seqs, sample, w
-
-
 def time_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
     """Warm up, then time `steps` decode steps (append + attention)."""
     n = len(seqs)
@@ -137,17 +111,10 @@ def time_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
 
 
 def evict_leg(sq, torch, wl, reps=8):
-    w = wl.compaction64k()
+    from paper_2602_22603_amd import drivers
+    store, base, w, k, v = drivers.build_compaction64k()
     L = w.length
-    store = sq.Store(1, 32, 8, 128, num_pages=2 * (L // 16) + 64, max_seqs=4,
-                     max_pages_per_seq=L // 16 + 32)
-    k = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000, "cuda")
-    v = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000 + 1, "cuda")
-    base = store.seq_create()
-    store.append(base, k, v)
     del k, v
-    for c, (s, e) in enumerate(w.spans):
-        store.span_mark(base, c, s, e)
     torch.cuda.synchronize()
     walls, stats = [], None
     store.profile_enable(True)
@@ -233,7 +200,10 @@ def main():
     n_modes = 3 if "modes" in legs else 0
     extra = total * (1 + n_modes) + 16
     log(f"building {args.tasks} tasks at {args.ctx} tokens ...")
-    store, seqs, sample, w = build_shared(sq, torch, wl, args.tasks, args.ctx, extra)
+    from paper_2602_22603_amd import drivers
+    store, seqs, inputs = drivers.build_shared128k(tasks=args.tasks, ctx=args.ctx,
+                                                   extra_tokens=extra)
+    sample = inputs[0][:2]
     B = len(seqs)
     kb = [wl.device_normal_bf16((1, B, 8, 128), 500 + 3 * i, "cuda") for i in range(total)]
     vb = [wl.device_normal_bf16((1, B, 8, 128), 501 + 3 * i, "cuda") for i in range(total)]

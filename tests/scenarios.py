@@ -173,6 +173,20 @@ class Twin:
         self.store.span_mark(h, cursor, s, e)
         self.model.span_mark(h, cursor, s, e)
 
+    def try_mark(self, h, cursor, s, e):
+        """Mark where the oracle accepts the span; both sides must agree."""
+        try:
+            self.model.span_mark(h, cursor, s, e)
+        except opg.OracleError as err:
+            try:
+                self.store.span_mark(h, cursor, s, e)
+            except self.sq.SqError as serr:
+                assert serr.code == err.code, (serr.code, err.code)
+                return False
+            raise AssertionError("the library accepted a span the oracle rejects")
+        self.store.span_mark(h, cursor, s, e)
+        return True
+
     def evict(self, h, ids):
         got = self.store.evict(h, ids)
         want = self.model.evict(h, ids)
