@@ -40,10 +40,12 @@
  *
  * Data layout in HBM (caller-allocated, sizes from sq_pool_bytes)
  * ---------------------------------------------------------------
- *   K pool  bf16  [NL][num_pages][Hkv][P][D]   token-major rows of D values
- *   V pool  bf16  [NL][num_pages][Hkv][D][P]   page-transposed: the P tokens
+ *   K pool  bf16  [NL][Hkv][num_pages][P][D]   token-major rows of D values
+ *   V pool  bf16  [NL][Hkv][num_pages][D][P]   page-transposed: the P tokens
  *                                               of one channel are contiguous
  *   pos     int32 [num_pages][P]               position of each cached token
+ * Head-major: all pages of one KV head of one layer form one contiguous
+ * region, which decode attention streams.
  * P (page_size) is 16 in device mode; D (head_dim) is 64 or 128; the query
  * group G = Hq / Hkv is 1, 2, 4 or 8.  Query head h reads KV head h / G.
  */

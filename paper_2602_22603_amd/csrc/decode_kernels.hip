@@ -41,6 +41,27 @@ typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef short s16x4_t __attribute__((__vector_size__(4 * sizeof(short))));
 typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// K/V page loads.  With NT (a page is read once per launch) they are
+// non-temporal; when several sequences of one launch read the same pages the
+// ordinary loads let L2 and the memory-side cache serve the repeats.
+template <bool NT> __device__ inline u32x4_t ld_kv4(const uint16_t *p) {
+  const u32x4_t *q = reinterpret_cast<const u32x4_t *>(p);
+  if constexpr (NT) return __builtin_nontemporal_load(q);
+  else return *q;
+}
+template <bool NT> __device__ inline uint4 ld_stream(const uint16_t *p) {
+  const u32x4_t x = ld_kv4<NT>(p);
+  return make_uint4(x.x, x.y, x.z, x.w);
+}
+template <bool NT> __device__ inline uint2 ld_stream2(const uint16_t *p) {
+  const u32x2_t *q = reinterpret_cast<const u32x2_t *>(p);
+  u32x2_t x;
+  if constexpr (NT) x = __builtin_nontemporal_load(q);
+  else x = *q;
+  return make_uint2(x.x, x.y);
+}
 
 __device__ inline float bf_lo(uint32_t x) { return __uint_as_float(x << 16); }
 __device__ inline float bf_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
@@ -127,7 +148,7 @@ __device__ inline ItemPos locate(const DecodeArgs &a, int item) {
 // LDS holds the page's K tile (row pitch 2D + 64 bytes) and V^T tile (groups
 // of D/16 channels, 32 bytes per channel, 32 bytes of padding per group), the
 // page's weights p[t][r] and the rescale factors alpha[r].
-template <int D, int G>
+template <int D, int G, bool NT>
 __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
   constexpr int KPITCH = 2 * D + 64;
   constexpr int DPL = D / 16;
@@ -171,15 +192,15 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
     l_run[k] = 0.f;
   }
 
-  const uint16_t *kbase = a.k + (int64_t)g * P * D + lane * 8;
-  const uint16_t *vbase = a.v + (int64_t)g * P * D + lane * 8;
+  const uint16_t *kbase = a.k + (int64_t)g * a.head_stride + lane * 8;
+  const uint16_t *vbase = a.v + (int64_t)g * a.head_stride + lane * 8;
   u32x4_t kreg[NLD], vreg[NLD];
   {
     const int64_t off = (int64_t)pt[ip.pbeg] * a.page_stride;
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      kreg[i] = *reinterpret_cast<const u32x4_t *>(kbase + off + i * 512);
-      vreg[i] = *reinterpret_cast<const u32x4_t *>(vbase + off + i * 512);
+      kreg[i] = ld_kv4<NT>(kbase + off + i * 512);
+      vreg[i] = ld_kv4<NT>(vbase + off + i * 512);
     }
   }
 
@@ -199,8 +220,8 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
       const int64_t off = (int64_t)pt[pg + 1] * a.page_stride;
 #pragma unroll
       for (int i = 0; i < NLD; ++i) {
-        kreg[i] = *reinterpret_cast<const u32x4_t *>(kbase + off + i * 512);
-        vreg[i] = *reinterpret_cast<const u32x4_t *>(vbase + off + i * 512);
+        kreg[i] = ld_kv4<NT>(kbase + off + i * 512);
+        vreg[i] = ld_kv4<NT>(vbase + off + i * 512);
       }
     }
 
@@ -336,8 +357,11 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
 }
 
 // ===========================================================================
-// MFMA multi-query tile: one wave per item; up to 16 query rows (nmem
-// sequences x G heads of one KV head) against the same pages.
+// MFMA multi-query tile: up to 16 query rows (nmem sequences x G heads of one
+// KV head) against the same pages.  A work item is processed by a workgroup
+// of kWaves waves; wave w takes pages w, w + kWaves, ... of the item's chunk
+// and the waves' softmax states are combined in LDS at the end, so one item
+// still yields one partial per row.
 // Lane l = n + 16 * kg (n = l & 15, kg = l >> 4):
 //   QK A operand  K[token n][channels 8 kg + 32 s .. +8]       (16x16x32)
 //   QK B operand  Q[row n][same channels]
@@ -347,11 +371,88 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
 //   O^T output    O[row n][channel 16 jd + 4 kg + i]
 // P is split into bf16 hi + lo parts (two MFMAs per block) so the weights
 // keep ~16 bits; the running sum l uses the same hi + lo values.
-template <int D, int G>
-__global__ __launch_bounds__(64) void k_decode_mfma(DecodeArgs a) {
+template <int D> struct MfmaFrag {
+  uint4 k[D / 32];
+  uint2 v[D / 16];
+};
+
+template <int D, bool NT>
+__device__ inline void mfma_load(MfmaFrag<D> &f, const uint16_t *kbase, const uint16_t *vbase,
+                                 int64_t off) {
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) f.k[s] = ld_stream<NT>(kbase + off + 32 * s);
+#pragma unroll
+  for (int j = 0; j < D / 16; ++j) f.v[j] = ld_stream2<NT>(vbase + off + 16 * P * j);
+}
+
+template <int D>
+__device__ inline void mfma_page(MfmaFrag<D> &f, int valid, int kg, float scale_log2,
+                                 const bf16x8_t (&qb)[D / 32], f32x4_t (&acc)[D / 16],
+                                 float &m_run, float &l_run) {
   constexpr int NS = D / 32;
   constexpr int NJ = D / 16;
-  const int lane = threadIdx.x;
+  f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int s = 0; s < NS; ++s)
+    st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, f.k[s]), qb[s], st,
+                                                 0, 0, 0);
+  float x[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) x[i] = (4 * kg + i < valid) ? st[i] * scale_log2 : kNegInf;
+  float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+  mx = max_xrow16(mx);
+  mx = max_xrow32(mx);
+  const float m_new = fmaxf(m_run, mx);
+  const bool none = m_new == kNegInf;
+  const float alpha = none ? 1.f : exp2_fast(m_run - m_new);
+  float p[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) p[i] = none ? 0.f : exp2_fast(x[i] - m_new);
+  const uint32_t h01 = pack_bf16(p[0], p[1]);
+  const uint32_t h23 = pack_bf16(p[2], p[3]);
+  const float r0 = p[0] - bf_lo(h01), r1 = p[1] - bf_hi(h01);
+  const float r2 = p[2] - bf_lo(h23), r3 = p[3] - bf_hi(h23);
+  const uint32_t l01 = pack_bf16(r0, r1);
+  const uint32_t l23 = pack_bf16(r2, r3);
+  const float psum = (bf_lo(h01) + bf_lo(l01)) + (bf_hi(h01) + bf_hi(l01)) +
+                     (bf_lo(h23) + bf_lo(l23)) + (bf_hi(h23) + bf_hi(l23));
+  l_run = l_run * alpha + psum;
+  m_run = m_new;
+  if (__any(alpha != 1.f)) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[j] *= alpha;
+  }
+  if (valid < P) { // values of absent tokens may be anything: keep 0 * v finite
+    const uint32_t m0 = (4 * kg + 0 < valid ? 0xffffu : 0u) | (4 * kg + 1 < valid ? 0xffff0000u : 0u);
+    const uint32_t m1 = (4 * kg + 2 < valid ? 0xffffu : 0u) | (4 * kg + 3 < valid ? 0xffff0000u : 0u);
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+      f.v[j].x &= m0;
+      f.v[j].y &= m1;
+    }
+  }
+  const s16x4_t phi = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
+  const s16x4_t plo = __builtin_bit_cast(s16x4_t, make_uint2(l01, l23));
+#pragma unroll
+  for (int j = 0; j < NJ; ++j) {
+    const s16x4_t vA = __builtin_bit_cast(s16x4_t, f.v[j]);
+    acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vA, phi, acc[j], 0, 0, 0);
+    acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vA, plo, acc[j], 0, 0, 0);
+  }
+}
+
+template <int D, int G, int kWaves, bool NT>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
+k_decode_mfma(DecodeArgs a) {
+  constexpr int NS = D / 32;
+  constexpr int NJ = D / 16;
+  constexpr int APITCH = D + 4; // floats per row of a wave's accumulator in LDS
+  __shared__ float s_m[kWaves][kRows];
+  __shared__ float s_l[kWaves][kRows];
+  __shared__ __attribute__((aligned(16))) float s_acc[kWaves][kRows * APITCH];
+
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   const int n = lane & 15, kg = lane >> 4;
   const int item = a.item_begin + blockIdx.x;
   const ItemPos ip = locate(a, item);
@@ -378,160 +479,214 @@ __global__ __launch_bounds__(64) void k_decode_mfma(DecodeArgs a) {
   for (int j = 0; j < NJ; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
 
-  const uint16_t *kbase = a.k + (int64_t)g * P * D + n * D + 8 * kg;
-  const uint16_t *vbase = a.v + (int64_t)g * P * D + n * P + 4 * kg;
-  uint4 ka[NS];
-  uint2 va[NJ];
-  auto load_page = [&](int pg) {
-    const int64_t off = (int64_t)pt[pg] * a.page_stride;
-#pragma unroll
-    for (int s = 0; s < NS; ++s) ka[s] = *reinterpret_cast<const uint4 *>(kbase + off + 32 * s);
-#pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      va[j] = *reinterpret_cast<const uint2 *>(vbase + off + 16 * P * j);
-  };
-  load_page(ip.pbeg);
-
-  for (int pg = ip.pbeg; pg < ip.pend; ++pg) {
-    const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
-    uint4 kc[NS];
-    uint2 vc[NJ];
-#pragma unroll
-    for (int s = 0; s < NS; ++s) kc[s] = ka[s];
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) vc[j] = va[j];
-    if (pg + 1 < ip.pend) load_page(pg + 1);
-
-    f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < NS; ++s)
-      st = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, kc[s]), qb[s],
-                                                   st, 0, 0, 0);
-    float x[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) x[i] = (4 * kg + i < valid) ? st[i] * a.scale_log2 : kNegInf;
-    float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
-    mx = max_xrow16(mx);
-    mx = max_xrow32(mx);
-    const float m_new = fmaxf(m_run, mx);
-    const bool none = m_new == kNegInf;
-    const float alpha = none ? 1.f : exp2_fast(m_run - m_new);
-    float p[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = none ? 0.f : exp2_fast(x[i] - m_new);
-    const uint32_t h01 = pack_bf16(p[0], p[1]);
-    const uint32_t h23 = pack_bf16(p[2], p[3]);
-    const float r0 = p[0] - bf_lo(h01), r1 = p[1] - bf_hi(h01);
-    const float r2 = p[2] - bf_lo(h23), r3 = p[3] - bf_hi(h23);
-    const uint32_t l01 = pack_bf16(r0, r1);
-    const uint32_t l23 = pack_bf16(r2, r3);
-    const float psum = (bf_lo(h01) + bf_lo(l01)) + (bf_hi(h01) + bf_hi(l01)) +
-                       (bf_lo(h23) + bf_lo(l23)) + (bf_hi(h23) + bf_hi(l23));
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-    if (__any(alpha != 1.f)) {
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) acc[j] *= alpha;
-    }
-    if (valid < P) { // values of absent tokens may be anything: keep 0 * v finite
-      const uint32_t m0 = (4 * kg + 0 < valid ? 0xffffu : 0u) | (4 * kg + 1 < valid ? 0xffff0000u : 0u);
-      const uint32_t m1 = (4 * kg + 2 < valid ? 0xffffu : 0u) | (4 * kg + 3 < valid ? 0xffff0000u : 0u);
-#pragma unroll
-      for (int j = 0; j < NJ; ++j) {
-        vc[j].x &= m0;
-        vc[j].y &= m1;
-      }
-    }
-    const s16x4_t phi = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
-    const s16x4_t plo = __builtin_bit_cast(s16x4_t, make_uint2(l01, l23));
-#pragma unroll
-    for (int j = 0; j < NJ; ++j) {
-      const s16x4_t vA = __builtin_bit_cast(s16x4_t, vc[j]);
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vA, phi, acc[j], 0, 0, 0);
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(vA, plo, acc[j], 0, 0, 0);
+  const uint16_t *kbase = a.k + (int64_t)g * a.head_stride + n * D + 8 * kg;
+  const uint16_t *vbase = a.v + (int64_t)g * a.head_stride + n * P + 4 * kg;
+  const int first = ip.pbeg + wave;
+  // this wave's pages: first, first + kWaves, ... < pend; ids come 64 at a time
+  const int count = first < ip.pend ? (ip.pend - first + kWaves - 1) / kWaves : 0;
+  for (int base = 0; base < count; base += 64) {
+    const int nb = min(64, count - base);
+    const int my = first + (base + lane) * kWaves;
+    const int ids = lane < nb ? pt[my] : 0;
+    MfmaFrag<D> nxt;
+    mfma_load<D, NT>(nxt, kbase, vbase, (int64_t)__builtin_amdgcn_readlane(ids, 0) * a.page_stride);
+    for (int i = 0; i < nb; ++i) {
+      MfmaFrag<D> cur = nxt;
+      if (i + 1 < nb)
+        mfma_load<D, NT>(nxt, kbase, vbase,
+                     (int64_t)__builtin_amdgcn_readlane(ids, i + 1) * a.page_stride);
+      const int pg = first + (base + i) * kWaves;
+      const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
+      mfma_page<D>(cur, valid, kg, a.scale_log2, qb, acc, m_run, l_run);
     }
   }
 
   float l_tot = sum_xrow16(l_run);
   l_tot = sum_xrow32(l_tot);
-  if (qvalid) {
-    const int64_t prow = (int64_t)item * kRows + n;
-    if (kg == 0) {
-      a.part_m[prow] = m_run;
-      a.part_l[prow] = l_tot;
-    }
-    float *dst = a.part_acc + prow * D + 4 * kg;
+  // combine the waves' states: M = max m_w, scale_w = 2^(m_w - M)
+  if (kg == 0) {
+    s_m[wave][n] = m_run;
+    s_l[wave][n] = l_tot;
+  }
 #pragma unroll
-    for (int j = 0; j < NJ; ++j)
-      *reinterpret_cast<float4 *>(dst + 16 * j) = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+  for (int j = 0; j < NJ; ++j)
+    *reinterpret_cast<float4 *>(&s_acc[wave][n * APITCH + 16 * j + 4 * kg]) =
+        make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+  __syncthreads();
+  const int64_t prow = (int64_t)item * kRows;
+  if (threadIdx.x < kRows && (int)threadIdx.x < nrows) {
+    const int r = threadIdx.x;
+    float mm = kNegInf;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) mm = fmaxf(mm, s_m[w][r]);
+    float ll = 0.f;
+    if (mm != kNegInf) {
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) ll += exp2_fast(s_m[w][r] - mm) * s_l[w][r];
+    }
+    a.part_m[prow + r] = mm;
+    a.part_l[prow + r] = ll;
+  }
+  constexpr int PER = kRows * D / (64 * kWaves); // output floats per thread
+  const int e0 = threadIdx.x * PER;
+  const int r = e0 / D;
+  if (r < nrows) {
+    float mm = kNegInf;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) mm = fmaxf(mm, s_m[w][r]);
+    float sc[kWaves];
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) sc[w] = mm == kNegInf ? 0.f : exp2_fast(s_m[w][r] - mm);
+    const int d0 = e0 % D;
+#pragma unroll
+    for (int e = 0; e < PER; e += 4) {
+      float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+      for (int w = 0; w < kWaves; ++w) {
+        const float4 x = *reinterpret_cast<const float4 *>(&s_acc[w][r * APITCH + d0 + e]);
+        o.x = fmaf(sc[w], x.x, o.x);
+        o.y = fmaf(sc[w], x.y, o.y);
+        o.z = fmaf(sc[w], x.z, o.z);
+        o.w = fmaf(sc[w], x.w, o.w);
+      }
+      *reinterpret_cast<float4 *>(a.part_acc + (prow + r) * D + d0 + e) = o;
+    }
   }
 }
 
 // ===========================================================================
-// Merge: one wave per (batch entry, query head).
+// Merge: one wave per (batch entry, query head).  Its partials are the chunks
+// of at most two segments.  Lanes first walk the chunks (max of m, then the
+// weights w_c = 2^(m_c - M) and the sum of w_c l_c), then walk the channels
+// while the loop over chunks issues independent row loads.
 template <int D>
 __global__ __launch_bounds__(64) void k_decode_merge(MergeArgs a) {
   constexpr int DPT = D / 64;
+  const int lane = threadIdx.x;
   const int b = blockIdx.x / a.hq;
   const int h = blockIdx.x - b * a.hq;
   const int g = h / a.group;
   const int hr = h - g * a.group;
   const int ns = a.n_src[b];
-  float big_m = kNegInf;
-  for (int e = 0; e < ns; ++e) {
-    const int nch = a.nchunk[b][e];
-    const int row = a.member[b][e] * a.group + hr;
-    const int64_t base = (int64_t)(a.item_base[b][e] + g * nch) * kRows + row;
-    for (int c = 0; c < nch; ++c) big_m = fmaxf(big_m, a.part_m[base + (int64_t)c * kRows]);
+  int n0 = 0, n1 = 0;
+  int64_t base0 = 0, base1 = 0;
+  if (ns > 0) {
+    n0 = a.nchunk[b][0];
+    base0 = (int64_t)(a.item_base[b][0] + g * n0) * kRows + a.member[b][0] * a.group + hr;
   }
+  if (ns > 1) {
+    n1 = a.nchunk[b][1];
+    base1 = (int64_t)(a.item_base[b][1] + g * n1) * kRows + a.member[b][1] * a.group + hr;
+  }
+  const int total = n0 + n1;
+  auto row_of = [&](int c) -> int64_t {
+    return c < n0 ? base0 + (int64_t)c * kRows : base1 + (int64_t)(c - n0) * kRows;
+  };
+  float big_m = kNegInf;
+  for (int c = lane; c < total; c += 64) big_m = fmaxf(big_m, a.part_m[row_of(c)]);
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) big_m = fmaxf(big_m, __shfl_xor(big_m, o));
   float num[DPT];
 #pragma unroll
   for (int i = 0; i < DPT; ++i) num[i] = 0.f;
   float den = 0.f;
   if (big_m != kNegInf) {
-    for (int e = 0; e < ns; ++e) {
-      const int nch = a.nchunk[b][e];
-      const int row = a.member[b][e] * a.group + hr;
-      const int64_t base = (int64_t)(a.item_base[b][e] + g * nch) * kRows + row;
-      for (int c = 0; c < nch; ++c) {
-        const int64_t idx = base + (int64_t)c * kRows;
-        const float w = exp2_fast(a.part_m[idx] - big_m);
-        den = fmaf(w, a.part_l[idx], den);
-        const float *src = a.part_acc + idx * D + threadIdx.x * DPT;
+    for (int c0 = 0; c0 < total; c0 += 64) {
+      const int c = c0 + lane;
+      float w = 0.f;
+      int64_t row = 0;
+      if (c < total) {
+        row = row_of(c);
+        w = exp2_fast(a.part_m[row] - big_m);
+        den = fmaf(w, a.part_l[row], den);
+      }
+      const int nb = min(64, total - c0);
+      int i = 0;
+      for (; i + 4 <= nb; i += 4) {
+        float wv[4];
+        const float *src[4];
 #pragma unroll
-        for (int i = 0; i < DPT; ++i) num[i] = fmaf(w, src[i], num[i]);
+        for (int u = 0; u < 4; ++u) {
+          wv[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i + u));
+          const int rlo = __builtin_amdgcn_readlane((int)(row & 0xffffffff), i + u);
+          const int rhi = __builtin_amdgcn_readlane((int)(row >> 32), i + u);
+          const int64_t r = ((int64_t)rhi << 32) | (uint32_t)rlo;
+          src[u] = a.part_acc + r * D + lane * DPT;
+        }
+        float x[4][DPT];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int q = 0; q < DPT; ++q) x[u][q] = src[u][q];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int q = 0; q < DPT; ++q) num[q] = fmaf(wv[u], x[u][q], num[q]);
+      }
+      for (; i < nb; ++i) {
+        const float wv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i));
+        const int rlo = __builtin_amdgcn_readlane((int)(row & 0xffffffff), i);
+        const int rhi = __builtin_amdgcn_readlane((int)(row >> 32), i);
+        const int64_t r = ((int64_t)rhi << 32) | (uint32_t)rlo;
+        const float *src = a.part_acc + r * D + lane * DPT;
+#pragma unroll
+        for (int q = 0; q < DPT; ++q) num[q] = fmaf(wv, src[q], num[q]);
       }
     }
   }
-  float *o = a.out + ((int64_t)b * a.hq + h) * D + threadIdx.x * DPT;
 #pragma unroll
-  for (int i = 0; i < DPT; ++i) o[i] = den > 0.f ? num[i] / den : 0.f;
+  for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o);
+  float *out = a.out + ((int64_t)b * a.hq + h) * D + lane * DPT;
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) out[q] = den > 0.f ? num[q] / den : 0.f;
+}
+
+template <int D, bool NT>
+hipError_t valu_dispatch_nt(int group, const DecodeArgs &a, hipStream_t s) {
+  const dim3 grid(a.n_items), block(64);
+  switch (group) {
+  case 1: hipLaunchKernelGGL((k_decode_valu<D, 1, NT>), grid, block, 0, s, a); break;
+  case 2: hipLaunchKernelGGL((k_decode_valu<D, 2, NT>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_decode_valu<D, 4, NT>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_decode_valu<D, 8, NT>), grid, block, 0, s, a); break;
+  default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
 }
 
 template <int D>
 hipError_t valu_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_items), block(64);
+  return a.nontemporal ? valu_dispatch_nt<D, true>(group, a, s)
+                       : valu_dispatch_nt<D, false>(group, a, s);
+}
+
+template <int D, int W, bool NT>
+hipError_t mfma_dispatch_w(int group, const DecodeArgs &a, hipStream_t s) {
+  const dim3 grid(a.n_items), block(64 * W);
   switch (group) {
-  case 1: hipLaunchKernelGGL((k_decode_valu<D, 1>), grid, block, 0, s, a); break;
-  case 2: hipLaunchKernelGGL((k_decode_valu<D, 2>), grid, block, 0, s, a); break;
-  case 4: hipLaunchKernelGGL((k_decode_valu<D, 4>), grid, block, 0, s, a); break;
-  case 8: hipLaunchKernelGGL((k_decode_valu<D, 8>), grid, block, 0, s, a); break;
+  case 1: hipLaunchKernelGGL((k_decode_mfma<D, 1, W, NT>), grid, block, 0, s, a); break;
+  case 2: hipLaunchKernelGGL((k_decode_mfma<D, 2, W, NT>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_decode_mfma<D, 4, W, NT>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_decode_mfma<D, 8, W, NT>), grid, block, 0, s, a); break;
   default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int D>
-hipError_t mfma_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_items), block(64);
-  switch (group) {
-  case 1: hipLaunchKernelGGL((k_decode_mfma<D, 1>), grid, block, 0, s, a); break;
-  case 2: hipLaunchKernelGGL((k_decode_mfma<D, 2>), grid, block, 0, s, a); break;
-  case 4: hipLaunchKernelGGL((k_decode_mfma<D, 4>), grid, block, 0, s, a); break;
-  case 8: hipLaunchKernelGGL((k_decode_mfma<D, 8>), grid, block, 0, s, a); break;
+template <int D, bool NT>
+hipError_t mfma_dispatch_nt(int group, int waves, const DecodeArgs &a, hipStream_t s) {
+  switch (waves) {
+  case 1: return mfma_dispatch_w<D, 1, NT>(group, a, s);
+  case 2: return mfma_dispatch_w<D, 2, NT>(group, a, s);
+  case 4: return mfma_dispatch_w<D, 4, NT>(group, a, s);
   default: return hipErrorInvalidValue;
   }
-  return hipGetLastError();
+}
+
+template <int D>
+hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t s) {
+  return a.nontemporal ? mfma_dispatch_nt<D, true>(group, waves, a, s)
+                       : mfma_dispatch_nt<D, false>(group, waves, a, s);
 }
 
 } // namespace
@@ -541,9 +696,9 @@ hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t
   return d == 128 ? valu_dispatch<128>(group, a, s) : valu_dispatch<64>(group, a, s);
 }
 
-hipError_t launch_decode_mfma(int d, int group, const DecodeArgs &a, hipStream_t s) {
+hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s) {
   if (a.n_items == 0) return hipSuccess;
-  return d == 128 ? mfma_dispatch<128>(group, a, s) : mfma_dispatch<64>(group, a, s);
+  return d == 128 ? mfma_dispatch<128>(group, waves, a, s) : mfma_dispatch<64>(group, waves, a, s);
 }
 
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s) {

@@ -5,9 +5,10 @@
 //   inverse map -> page-level gather into fresh pages.
 //
 // Layouts (elements are bf16 stored as uint16_t):
-//   K pool [NL][NP][Hkv][P][D]   one 16-token page of one head is P*D
-//                                 contiguous values, token-major
-//   V pool [NL][NP][Hkv][D][P]   the same page stored channel-major: the P
+//   K pool [NL][Hkv][NP][P][D]   one 16-token page of one head is P*D
+//                                 contiguous values, token-major; the pages
+//                                 of one head are contiguous (head-major)
+//   V pool [NL][Hkv][NP][D][P]   the same page stored channel-major: the P
 //                                 tokens of one channel are contiguous
 //   pos    [NP][P]               int32 position of each cached token
 // The page size is 16 throughout.

@@ -19,16 +19,17 @@ constexpr int kMaxItems = 8192;      // partial slots in the workspace
 constexpr int kScanBlock = 2048;     // tokens per block of the eviction scan
 constexpr int kScanThreads = 256;
 
-// Device pools and shapes.  K: [NL][NP][Hkv][P][D]; V: [NL][NP][Hkv][D][P];
-// pos: [NP][P].  Element strides are in bf16 units.
+// Device pools and shapes.  K: [NL][Hkv][NP][P][D]; V: [NL][Hkv][NP][D][P];
+// pos: [NP][P].  Element strides are in bf16 units.  Head-major: the pages of
+// one KV head are contiguous, so a decode work item streams one region.
 struct Pools {
   uint16_t *k;
   uint16_t *v;
   int32_t *pos;
   int32_t nl, hkv, d, np;
-  int64_t layer_stride; // NP * Hkv * P * D
-  int64_t page_stride;  // Hkv * P * D
-  int64_t head_stride;  // P * D
+  int64_t layer_stride; // Hkv * NP * P * D
+  int64_t page_stride;  // P * D
+  int64_t head_stride;  // NP * P * D
 };
 
 // ---- append ---------------------------------------------------------------
@@ -101,13 +102,15 @@ struct DecodeArgs {
   float *part_m;       // [kMaxItems][kRows]  (log2 domain)
   float *part_l;       // [kMaxItems][kRows]
   float *part_acc;     // [kMaxItems][kRows][D]
-  int64_t page_stride; // Hkv * P * D elements
+  int64_t page_stride; // P * D elements
+  int64_t head_stride; // NP * P * D elements
   int32_t max_pages;   // page-table row pitch
   int32_t hq;
   int32_t chunk_pages;
   int32_t n_segs;
   int32_t item_begin;  // global index of this launch's first item
   int32_t n_items;
+  int32_t nontemporal; // 1: every page is read once in this launch
   float scale_log2;    // scale * log2(e)
   Seg segs[kMaxSegs];
 };
@@ -143,7 +146,7 @@ hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, 
 hipError_t launch_evict_scan(const EvictArgs &a, hipStream_t s);
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
-hipError_t launch_decode_mfma(int d, int group, const DecodeArgs &a, hipStream_t s);
+hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s);
 
 } // namespace sq

@@ -202,6 +202,7 @@ struct sq_store {
   // tuning
   int target_items = 4096;
   bool auto_single_mfma = true;
+  int mfma_waves = 4; // waves per MFMA work item (1, 2 or 4)
 
   // profiling
   bool prof_on = false;
@@ -314,6 +315,7 @@ struct Plan {
   int n_groups = 0;
   int chunk_pages = 1;
   int n_items_valu = 0, n_items_mfma = 0;
+  bool pages_reread = false; // some page is read by more than one segment
   int64_t kv_bytes = 0, kv_bytes_logical = 0, io_bytes = 0;
   int64_t kv_bytes_valu = 0, kv_bytes_mfma = 0;
 };
@@ -325,7 +327,7 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   std::vector<std::vector<int>> groups;
   std::vector<int64_t> npre;
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
-  if (grouping) {
+  {
     // Sequences whose page lists start with the same physical page share a
     // prefix (the auxiliary branch aliases the main thread's pages).  Group
     // them, at most max_mem per group, in batch order.
@@ -341,6 +343,8 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
           break;
         }
       if (gi < 0) {
+        for (auto &o : open)
+          if (o.first == first) plan->pages_reread = true; // a full group already reads it
         gi = (int)groups.size();
         groups.push_back({});
         open.push_back({first, gi});
@@ -365,7 +369,8 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
         lcp = k;
       }
       npre[gi] = lcp;
-      if (lcp == 0)
+      if (lcp > 0 && !grouping) plan->pages_reread = true; // per-sequence modes re-read them
+      if (lcp == 0 || !grouping)
         for (int b : mem) group_of[b] = -1;
     }
   }
@@ -496,6 +501,10 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     if (v >= 1) s->target_items = v;
   }
   if (const char *e = std::getenv("SQ_AUTO_SINGLE")) s->auto_single_mfma = std::strcmp(e, "valu") != 0;
+  if (const char *e = std::getenv("SQ_MFMA_WAVES")) {
+    const int v = std::atoi(e);
+    if (v == 1 || v == 2 || v == 4) s->mfma_waves = v;
+  }
   if (device) {
     s->lay = lay;
     char *ws = static_cast<char *>(cfg->workspace);
@@ -516,9 +525,9 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     p.hkv = cfg->num_kv_heads;
     p.d = cfg->head_dim;
     p.np = cfg->num_pages;
-    p.head_stride = (int64_t)s->P * s->D;
-    p.page_stride = p.head_stride * cfg->num_kv_heads;
-    p.layer_stride = p.page_stride * cfg->num_pages;
+    p.page_stride = (int64_t)s->P * s->D;
+    p.head_stride = p.page_stride * cfg->num_pages;
+    p.layer_stride = p.head_stride * cfg->num_kv_heads;
     void *host = nullptr;
     hipError_t e = hipHostMalloc(&host, lay.upload_elems * 4, hipHostMallocDefault);
     if (e != hipSuccess) {
@@ -974,6 +983,7 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   base.part_l = s->part_l;
   base.part_acc = s->part_acc;
   base.page_stride = s->pools.page_stride;
+  base.head_stride = s->pools.head_stride;
   base.max_pages = s->cfg.max_pages_per_seq;
   base.hq = s->cfg.num_q_heads;
   base.chunk_pages = plan.chunk_pages;
@@ -999,12 +1009,13 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
     for (const PlanSeg &ps : plan.segs)
       if (ps.mfma == (pass == 1)) a.segs[a.n_segs++] = ps.seg;
     a.item_begin = pass == 0 ? 0 : plan.n_items_valu;
+    a.nontemporal = plan.pages_reread ? 0 : 1;
     a.n_items = pass == 0 ? plan.n_items_valu : plan.n_items_mfma;
     if (a.n_items == 0) continue;
     ProfPair pp;
     const bool on = s->prof_begin(strm, &pp, pass == 0 ? kProfValu : kProfMfma);
     hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, a, strm)
-                             : sq::launch_decode_mfma(s->D, s->G, a, strm);
+                             : sq::launch_decode_mfma(s->D, s->G, s->mfma_waves, a, strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "decode kernel");
   }

@@ -189,8 +189,8 @@ class Store:
             if kb == 0 or wb == 0:
                 raise SqError(ERR_INVALID, "invalid store configuration for device mode")
             dev = torch.device(device)
-            shape_k = (num_layers, num_pages, num_kv_heads, page_size, head_dim)
-            shape_v = (num_layers, num_pages, num_kv_heads, head_dim, page_size)
+            shape_k = (num_layers, num_kv_heads, num_pages, page_size, head_dim)
+            shape_v = (num_layers, num_kv_heads, num_pages, head_dim, page_size)
             self.k_pool = torch.zeros(shape_k, dtype=torch.bfloat16, device=dev)
             self.v_pool = torch.zeros(shape_v, dtype=torch.bfloat16, device=dev)
             self.pos_pool = torch.zeros((num_pages, page_size), dtype=torch.int32, device=dev)

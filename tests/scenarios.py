@@ -32,9 +32,9 @@ def seq_view(store, seq, layers=None):
     pages = torch.tensor(pt, device=dev, dtype=torch.int64)[tok // 16]
     slots = tok % 16
     lt = torch.tensor(layers, device=dev)
-    # K pool [NL, NP, Hkv, P, D]; V pool [NL, NP, Hkv, D, P] -> [NL, Hkv, NP, P, D]
-    kx = store.k_pool[lt].permute(0, 2, 1, 3, 4)
-    vx = store.v_pool[lt].permute(0, 2, 1, 4, 3)
+    # K pool [NL, Hkv, NP, P, D]; V pool [NL, Hkv, NP, D, P] -> [NL, Hkv, NP, P, D]
+    kx = store.k_pool[lt]
+    vx = store.v_pool[lt].permute(0, 1, 2, 4, 3)
     k = kx[:, :, pages, slots, :].permute(2, 0, 1, 3)     # [L, NL, Hkv, D]
     v = vx[:, :, pages, slots, :].permute(2, 0, 1, 3)
     pos = store.pos_pool[pages, slots]
