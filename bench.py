@@ -48,7 +48,8 @@ def parse_args():
     ap.add_argument("--tasks", type=int, default=8)
     ap.add_argument("--ctx", type=int, default=131072)
     ap.add_argument("--legs", default="decode,modes,evict,cpu",
-                    help="comma list of: decode, modes, evict, cpu")
+                    help="comma list of: decode, modes, evict, cpu, copy (a plain 1 GiB "
+                         "device copy used to calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
 
@@ -246,6 +247,14 @@ def main():
     if "evict" in legs:
         log("eviction leg (64K compaction) ...")
         evict = evict_leg(sq, torch, wl)
+    if "copy" in legs:
+        log("calibration copy: 1 GiB device-to-device ...")
+        src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     cpu = None
     if "cpu" in legs:
         log("oracle CPU baseline ...")
