@@ -47,9 +47,9 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--tasks", type=int, default=8)
     ap.add_argument("--ctx", type=int, default=131072)
-    ap.add_argument("--legs", default="decode,modes,evict,cpu",
-                    help="comma list of: decode, modes, evict, cpu, copy (a plain 1 GiB "
-                         "device copy used to calibrate HBM byte counters)")
+    ap.add_argument("--legs", default="decode,modes,evict,outlier,fullstack,cpu",
+                    help="comma list of: decode, modes, evict, outlier, fullstack, cpu, copy "
+                         "(a plain 1 GiB device copy used to calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
 
@@ -162,6 +162,66 @@ def evict_leg(sq, torch, wl, reps=8):
     return info
 
 
+def outlier_leg(sq, torch, wl):
+    """32K context with outlier channels: eviction of >= 50% of the tokens
+    while the auxiliary thread is alive, then 64 decode steps of [main, aux]
+    (append + attention)."""
+    from paper_2602_22603_amd import drivers
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    store, main, aux, w, stats = drivers.build_outlier32k()
+    torch.cuda.synchronize()
+    kb = [wl.to_torch_bf16(w.step_k[i], "cuda") for i in range(w.steps)]
+    vb = [wl.to_torch_bf16(w.step_v[i], "cuda") for i in range(w.steps)]
+    qs = [wl.to_torch_bf16(w.q[i], "cuda") for i in range(w.steps)]
+    out = torch.empty((2, 32, 128), dtype=torch.float32, device="cuda")
+    st0 = store.stats()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(w.steps):
+        store.append_batch([main, aux], kb[i], vb[i])
+        store.decode(0, [main, aux], qs[i], out=out)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / w.steps
+    st1 = store.stats()
+    kv = (st1["decode_kv_bytes"] - st0["decode_kv_bytes"]) / w.steps
+    store.close()
+    return dict(workload="32K tokens, 30 spans, 4 outlier channels x8, aux +512, evict >= 50% "
+                         f"(got {stats['tokens_removed'] / w.main_len:.3f}), 64 steps [main, aux]",
+                ms_per_step=round(ms, 4), kv_bytes_per_step=kv,
+                gbps=round(kv / (ms * 1e-3) / 1e9, 1), tokens_per_s=round(2 / (ms * 1e-3), 1))
+
+
+def fullstack_leg(sq, torch):
+    """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
+    turns; with and without eviction: peak KV bytes and the decode step
+    (all 36 layers) at each turn's end."""
+    from paper_2602_22603_amd import drivers
+    page_bytes = 36 * 8 * 16 * 128 * 2 * 2
+    res = {}
+    for ev in (True, False):
+        store, main, aux, log, w = drivers.run_full_stack(evict=ev)
+        st = store.stats()
+        final = log[-1]
+        dec = [r["decode_ms"] for r in log]
+        ev_ms = [r["evict_ms"] for r in log if "evict_ms" in r]
+        moved = sum(r["evict"]["bytes_moved"] for r in log if "evict" in r)
+        res["with_eviction" if ev else "without_eviction"] = dict(
+            peak_kv_bytes=st["peak_pages"] * page_bytes, final_tokens=final["length"],
+            decode_ms_final_step=round(final["decode_ms"], 3),
+            decode_gbps_final_step=round(final["kv_bytes"] / (final["decode_ms"] * 1e-3) / 1e9, 1),
+            decode_ms_sum_over_turns=round(sum(dec), 2),
+            kv_bytes_read_over_turns=sum(r["kv_bytes"] for r in log),
+            evictions=len(ev_ms), evict_ms_total=round(sum(ev_ms), 3),
+            evict_gbps=round(2 * moved / (sum(ev_ms) * 1e-3) / 1e9, 1) if ev_ms else None)
+        store.close()
+        torch.cuda.empty_cache()
+    a, b = res["with_eviction"], res["without_eviction"]
+    res["peak_kv_reduction"] = round(1 - a["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
+    res["kv_read_reduction"] = round(1 - a["kv_bytes_read_over_turns"] / b["kv_bytes_read_over_turns"], 4)
+    return res
+
+
 def cpu_leg(sample, wl, budget_s):
     import numpy as np
     from oracle import attention as oatt
@@ -255,6 +315,14 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    outlier = None
+    if "outlier" in legs:
+        log("32K outlier leg ...")
+        outlier = outlier_leg(sq, torch, wl)
+    fullstack = None
+    if "fullstack" in legs:
+        log("full-stack leg (36 layers, 16K -> 256K) ...")
+        fullstack = fullstack_leg(sq, torch)
     cpu = None
     if "cpu" in legs:
         log("oracle CPU baseline ...")
@@ -284,6 +352,8 @@ def main():
         "roofline": roofline,
         "modes": modes,
         "evict": evict,
+        "outlier32k": outlier,
+        "full_stack": fullstack,
         "cpu_baseline": cpu,
         "kernel_sources_sha": kernel_sha(),
     }

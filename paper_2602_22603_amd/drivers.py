@@ -8,6 +8,8 @@ against a reference computed from the same inputs.
 
 from __future__ import annotations
 
+import time
+
 from . import sq as _sq
 from . import workload as wl
 
@@ -84,3 +86,106 @@ def build_outlier32k(device="cuda"):
         store.span_mark(main, c, s, e)
     stats = store.evict(main, w.evict_ids)
     return store, main, aux, w, stats
+
+
+def full_stack_inputs(w, turn, device="cuda"):
+    """K/V of main-thread turn ``turn`` ([NL, turn_len, 8, 128] each) and of
+    the auxiliary thread forked at that turn ([NL, aux_private, 8, 128]).
+    turn = -1 gives the prefix ([NL, prefix, 8, 128])."""
+    n = w.prefix if turn < 0 else w.turn_len
+    base = w.seed * 1000 + 4 * (turn + 1)
+    k = wl.device_normal_bf16((w.num_layers, n, 8, 128), base, device)
+    v = wl.device_normal_bf16((w.num_layers, n, 8, 128), base + 1, device)
+    return k, v
+
+
+def full_stack_aux_inputs(w, turn, device="cuda"):
+    base = w.seed * 1000 + 4 * (turn + 1) + 2
+    k = wl.device_normal_bf16((w.num_layers, w.aux_private, 8, 128), base, device)
+    v = wl.device_normal_bf16((w.num_layers, w.aux_private, 8, 128), base + 1, device)
+    return k, v
+
+
+def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers=36,
+                   device="cuda", decode=True, on_turn=None, store=None):
+    """Algorithm 1 over a synthetic task: a non-evictable prefix, then turns
+    of reasoning plus one tool response each.  Phase 1 evicts the cursors the
+    auxiliary thread named (when it has finished) and releases it; Phase 2
+    forks a new auxiliary thread every ``interval`` turns, which appends its
+    private tokens and names seeded-random live tool spans until at least
+    60% of the live tool tokens are covered; Phase 3 appends the turn.
+    With ``decode``, one decode step ([main] or [main, aux], every layer) is
+    run at the end of each turn and ``on_turn(t, store, seqs, q, out)`` is
+    called after it.  Returns (store, main, aux, log, workload): aux is the
+    auxiliary thread still alive after the last turn (or None); log has one
+    record per turn."""
+    import torch
+    w = wl.full_stack(turns=turns, turn_len=turn_len, prefix=prefix, num_layers=num_layers)
+    rng = w._rng
+    max_tok = prefix + turns * turn_len
+    pages = max_tok // 16 + w.aux_private // 16 + 8
+    if store is None:
+        store = _sq.Store(num_layers, 32, 8, 128, num_pages=pages + pages // 8 + 64, max_seqs=4,
+                          max_pages_per_seq=max_tok // 16 + 64, device=device)
+    main = store.seq_create()
+    k, v = full_stack_inputs(w, -1, device)
+    store.append(main, k, v)
+    del k, v
+    aux, pending = None, []
+    log = []
+    for t in range(turns):
+        rec = dict(turn=t)
+        if aux is not None:                                  # Phase 1
+            store.release(aux)     # the finished thread's transient tokens go first
+            if evict and pending:
+                spans = store.spans(main)
+                rec["evicted_spans"] = sorted(spans[c] for c in pending)
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                rec["evict"] = store.evict(main, pending)
+                torch.cuda.synchronize()
+                rec["evict_ms"] = (time.perf_counter() - t0) * 1e3
+            aux, pending = None, []
+        if t % w.interval == 0:                              # Phase 2
+            aux = store.fork(main, store.seq_info(main)["length"])
+            ka, va = full_stack_aux_inputs(w, t, device)
+            store.append(aux, ka, va)
+            del ka, va
+            live = store.spans(main)
+            cur = sorted(live)
+            tool_total = sum(e - s for s, e in live.values())
+            if cur:
+                order = rng.permutation(len(cur))
+                got = 0
+                for i in order:
+                    if got >= w.evict_frac * tool_total:
+                        break
+                    c = cur[i]
+                    pending.append(c)
+                    got += live[c][1] - live[c][0]
+        r = w.reasoning[t]                                   # Phase 3
+        k, v = full_stack_inputs(w, t, device)
+        start = store.seq_info(main)["length"]
+        store.append(main, k, v)
+        store.span_mark(main, t, start + r, start + turn_len)
+        del k, v
+        seqs = [main] if aux is None else [main, aux]
+        rec["length"] = store.seq_info(main)["length"]
+        rec["batch"] = len(seqs)
+        if decode:
+            q = wl.device_normal_bf16((len(seqs), 32, 128), w.seed * 1000 + 7919 + t, device)
+            out = torch.empty((len(seqs), 32, 128), dtype=torch.float32, device=device)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            for layer in range(num_layers):
+                store.decode(layer, seqs, q, out=out)
+            torch.cuda.synchronize()
+            rec["decode_ms"] = (time.perf_counter() - t0) * 1e3
+            rec["kv_bytes"] = store.plan_info(seqs)["kv_bytes"] * num_layers
+            if on_turn is not None:
+                on_turn(t, store, seqs, q, out)
+        rec["live_pages"] = store.stats()["live_pages"]
+        rec["aux_fork_len"] = (store.seq_info(aux)["length"] - w.aux_private) if aux is not None else None
+        rec["aux_turn"] = (t - t % w.interval) if aux is not None else None
+        log.append(rec)
+    return store, main, aux, log, w

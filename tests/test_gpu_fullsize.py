@@ -167,3 +167,73 @@ def test_compaction64k_evict_and_decode(sq):
             err = sc.max_abs(o[b, 4 * g: 4 * g + 4], r)
             assert err <= TOL, (mode, b, g, err)
     store.close()
+
+
+def test_full_stack_sampled(sq):
+    """36 layers, 16K prefix + 30 turns of 8K tokens with an auxiliary thread
+    every 4 turns evicting >= 60% of the live tool tokens: positions against
+    a replay of the logged evictions, compacted K/V of sampled layers and
+    heads bit for bit against the regenerated inputs, and sampled decode
+    outputs of main and auxiliary against the oracle."""
+    import torch
+    from paper_2602_22603_amd import drivers
+    store, main, aux, log, w = drivers.run_full_stack(decode=True)
+    assert aux is None  # the last auxiliary thread finished and was released
+    # positions: replay appends and evictions on a plain list
+    pos = list(range(w.prefix))
+    nxt = w.prefix
+    for rec in log:
+        if "evicted_spans" in rec:
+            keep = oev.keep_mask(len(pos), rec["evicted_spans"])
+            pos = [p for p, k in zip(pos, keep) if k]
+        pos += list(range(nxt, nxt + w.turn_len))
+        nxt += w.turn_len
+    got = store.positions(main)
+    assert got.tolist() == pos
+    assert sum("evict" in r for r in log) == 7
+    # inputs of main, gathered by position, for sampled (layer, head)
+    samples = [(0, 0), (17, 5), (35, 7)]
+    pos_t = torch.tensor(pos, device="cuda")
+    rows_k = {s: [] for s in samples}
+    rows_v = {s: [] for s in samples}
+    for turn in range(-1, w.turns):
+        lo = 0 if turn < 0 else w.prefix + turn * w.turn_len
+        hi = w.prefix if turn < 0 else lo + w.turn_len
+        sel = pos_t[(pos_t >= lo) & (pos_t < hi)] - lo
+        k, v = drivers.full_stack_inputs(w, turn)
+        for (layer, g) in samples:
+            rows_k[(layer, g)].append(k[layer, sel, g])
+            rows_v[(layer, g)].append(v[layer, sel, g])
+        del k, v
+    main_kv = {s: (torch.cat(rows_k[s]), torch.cat(rows_v[s])) for s in samples}
+    # the GPU pools hold exactly those rows
+    for (layer, g), (kk, vv) in main_kv.items():
+        gk, gv, gp = sc.seq_view(store, main, layers=[layer])
+        assert np.array_equal(gk[:, 0, g], wl.torch_bf16_to_f64(kk)), (layer, g)
+        assert np.array_equal(gv[:, 0, g], wl.torch_bf16_to_f64(vv)), (layer, g)
+        del gk, gv
+    # a new auxiliary thread on the final context, with its own private tokens
+    fork_len = store.seq_info(main)["length"]
+    aux = store.fork(main, fork_len)
+    ka, va = drivers.full_stack_aux_inputs(w, w.turns)
+    store.append(aux, ka, va)
+    rng = np.random.default_rng([2602, 4, 9])
+    qb = wl.normal_bf16(rng, (2, 32, 128))
+    q = wl.to_torch_bf16(qb, "cuda")
+    qf = wl.bf16_value(qb)
+    scale = 1 / math.sqrt(128)
+    for (layer, g), (kk, vv) in main_kv.items():
+        qg_main = qf[0][4 * g: 4 * g + 4]
+        qg_aux = qf[1][4 * g: 4 * g + 4]
+        ref_main = _oracle_group(qg_main, kk[:, None], vv[:, None], 0, scale)
+        ak = torch.cat([kk, ka[layer, :, g]])[:, None]
+        av = torch.cat([vv, va[layer, :, g]])[:, None]
+        ref_aux = _oracle_group(qg_aux, ak, av, 0, scale)
+        for mode in _modes(sq):
+            out = store.decode(layer, [main, aux], q, mode=mode)
+            torch.cuda.synchronize()
+            o = out.cpu().numpy()
+            e1 = sc.max_abs(o[0, 4 * g: 4 * g + 4], ref_main)
+            e2 = sc.max_abs(o[1, 4 * g: 4 * g + 4], ref_aux)
+            assert e1 <= TOL and e2 <= TOL, (layer, g, mode, e1, e2)
+    store.close()
