@@ -555,14 +555,22 @@ k_decode_mfma(DecodeArgs a) {
 }
 
 // ===========================================================================
-// Merge: one wave per (batch entry, query head).  Its partials are the chunks
-// of at most two segments.  Lanes first walk the chunks (max of m, then the
-// weights w_c = 2^(m_c - M) and the sum of w_c l_c), then walk the channels
-// while the loop over chunks issues independent row loads.
+// Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
+// Its partials are the chunks of at most two segments; wave w takes chunks
+// w, w + kMergeWaves, ...  The global maximum M of m over all chunks comes
+// first (lanes over chunks, then across waves through LDS); each wave then
+// accumulates sum w_c l_c and sum w_c acc_c with w_c = 2^(m_c - M), lanes over
+// channels, issuing independent row loads; LDS adds the waves' sums.
+constexpr int kMergeWaves = 4;
+
 template <int D>
-__global__ __launch_bounds__(64) void k_decode_merge(MergeArgs a) {
+__global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) {
   constexpr int DPT = D / 64;
-  const int lane = threadIdx.x;
+  __shared__ float s_max[kMergeWaves];
+  __shared__ float s_den[kMergeWaves];
+  __shared__ float s_num[kMergeWaves][D];
+  const int lane = threadIdx.x & 63;
+  const int wave = threadIdx.x >> 6;
   const int b = blockIdx.x / a.hq;
   const int h = blockIdx.x - b * a.hq;
   const int g = h / a.group;
@@ -583,24 +591,30 @@ __global__ __launch_bounds__(64) void k_decode_merge(MergeArgs a) {
     return c < n0 ? base0 + (int64_t)c * kRows : base1 + (int64_t)(c - n0) * kRows;
   };
   float big_m = kNegInf;
-  for (int c = lane; c < total; c += 64) big_m = fmaxf(big_m, a.part_m[row_of(c)]);
+  for (int c = threadIdx.x; c < total; c += 64 * kMergeWaves) big_m = fmaxf(big_m, a.part_m[row_of(c)]);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) big_m = fmaxf(big_m, __shfl_xor(big_m, o));
+  if (lane == 0) s_max[wave] = big_m;
+  __syncthreads();
+#pragma unroll
+  for (int w = 0; w < kMergeWaves; ++w) big_m = fmaxf(big_m, s_max[w]);
   float num[DPT];
 #pragma unroll
   for (int i = 0; i < DPT; ++i) num[i] = 0.f;
   float den = 0.f;
   if (big_m != kNegInf) {
-    for (int c0 = 0; c0 < total; c0 += 64) {
-      const int c = c0 + lane;
+    // chunks of this wave: wave + kMergeWaves * j, handled 64 at a time
+    const int mine = total > wave ? (total - wave + kMergeWaves - 1) / kMergeWaves : 0;
+    for (int j0 = 0; j0 < mine; j0 += 64) {
+      const int j = j0 + lane;
       float w = 0.f;
       int64_t row = 0;
-      if (c < total) {
-        row = row_of(c);
+      if (j < mine) {
+        row = row_of(wave + kMergeWaves * j);
         w = exp2_fast(a.part_m[row] - big_m);
         den = fmaf(w, a.part_l[row], den);
       }
-      const int nb = min(64, total - c0);
+      const int nb = min(64, mine - j0);
       int i = 0;
       for (; i + 4 <= nb; i += 4) {
         float wv[4];
@@ -636,9 +650,23 @@ __global__ __launch_bounds__(64) void k_decode_merge(MergeArgs a) {
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o);
-  float *out = a.out + ((int64_t)b * a.hq + h) * D + lane * DPT;
+  if (lane == 0) s_den[wave] = den;
 #pragma unroll
-  for (int q = 0; q < DPT; ++q) out[q] = den > 0.f ? num[q] / den : 0.f;
+  for (int q = 0; q < DPT; ++q) s_num[wave][lane * DPT + q] = num[q];
+  __syncthreads();
+  if (wave == 0) {
+    float dt = 0.f;
+#pragma unroll
+    for (int w = 0; w < kMergeWaves; ++w) dt += s_den[w];
+    float *out = a.out + ((int64_t)b * a.hq + h) * D + lane * DPT;
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) {
+      float nt = 0.f;
+#pragma unroll
+      for (int w = 0; w < kMergeWaves; ++w) nt += s_num[w][lane * DPT + q];
+      out[q] = dt > 0.f ? nt / dt : 0.f;
+    }
+  }
 }
 
 template <int D, bool NT>
@@ -702,7 +730,7 @@ hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, 
 }
 
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s) {
-  const dim3 grid(batch * a.hq), block(64);
+  const dim3 grid(batch * a.hq), block(64 * kMergeWaves);
   if (d == 128)
     hipLaunchKernelGGL(k_decode_merge<128>, grid, block, 0, s, a);
   else

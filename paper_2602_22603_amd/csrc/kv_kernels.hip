@@ -146,10 +146,12 @@ __global__ __launch_bounds__(256) void k_copy_page(Pools p, int32_t src_page, in
 }
 
 // ---------------------------------------------------------------------------
-// Eviction scan.  keep[i] = 0 iff token i lies in one of the sorted, disjoint,
-// non-empty spans; dst = exclusive prefix sum of keep; src_of[dst[i]] = i.
-// Three passes over blocks of kScanBlock tokens: count, scan of the block
-// counts, then the in-block scan that writes dst and src_of.
+// Eviction index.  keep[i] = 0 iff token i lies in one of the evicted spans;
+// dst = exclusive prefix sum of keep; src_of[dst[i]] = i for kept i.  The
+// keep mask is a union of sorted spans, so its prefix sum at i is
+// i - (evicted tokens before i): the span-level exclusive prefix sums of the
+// span lengths (spans[k][2]) plus the part of the span that contains i.
+// Every token is independent, so one pass over the tokens suffices.
 constexpr int kPerThread = kScanBlock / kScanThreads; // 8
 
 __device__ inline int span_search(const int32_t *spans, int n_spans, int i) {
@@ -157,7 +159,7 @@ __device__ inline int span_search(const int32_t *spans, int n_spans, int i) {
   int lo = 0, hi = n_spans - 1, ans = -1;
   while (lo <= hi) {
     const int mid = (lo + hi) >> 1;
-    if (spans[2 * mid] <= i) {
+    if (spans[3 * mid] <= i) {
       ans = mid;
       lo = mid + 1;
     } else {
@@ -167,94 +169,34 @@ __device__ inline int span_search(const int32_t *spans, int n_spans, int i) {
   return ans;
 }
 
-__device__ inline int block_sum(int v, int *red) {
-  // 256 threads = 4 waves
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  const int w = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) red[w] = v;
-  __syncthreads();
-  const int total = red[0] + red[1] + red[2] + red[3];
-  __syncthreads();
-  return total;
-}
-
-__global__ __launch_bounds__(kScanThreads) void k_evict_count(EvictArgs a) {
-  __shared__ int red[4];
+__global__ __launch_bounds__(kScanThreads) void k_evict_index(EvictArgs a) {
   const int base = blockIdx.x * kScanBlock + threadIdx.x * kPerThread;
-  int cnt = 0;
-  if (base < a.n_tokens) {
-    int s = span_search(a.spans, a.n_spans, base);
-    for (int e = 0; e < kPerThread; ++e) {
-      const int i = base + e;
-      if (i >= a.n_tokens) break;
-      while (s + 1 < a.n_spans && a.spans[2 * (s + 1)] <= i) ++s;
-      const bool inside = s >= 0 && i < a.spans[2 * s + 1];
-      a.keep[i] = inside ? 0 : 1;
-      cnt += inside ? 0 : 1;
-    }
-  }
-  const int total = block_sum(cnt, red);
-  if (threadIdx.x == 0) a.blocks[blockIdx.x] = total;
-}
-
-// Exclusive scan of n block counts in place; blocks[n] = total.  One block.
-__global__ __launch_bounds__(1024) void k_evict_scan_blocks(int32_t *blocks, int32_t n) {
-  __shared__ int buf[1024];
-  int carry = 0;
-  for (int base = 0; base < n; base += 1024) {
-    const int i = base + threadIdx.x;
-    const int v = i < n ? blocks[i] : 0;
-    buf[threadIdx.x] = v;
-    __syncthreads();
-    for (int o = 1; o < 1024; o <<= 1) {
-      const int t = threadIdx.x >= o ? buf[threadIdx.x - o] : 0;
-      __syncthreads();
-      buf[threadIdx.x] += t;
-      __syncthreads();
-    }
-    if (i < n) blocks[i] = carry + buf[threadIdx.x] - v;
-    const int chunk_total = buf[1023];
-    __syncthreads();
-    carry += chunk_total;
-  }
-  if (threadIdx.x == 0) blocks[n] = carry;
-}
-
-__global__ __launch_bounds__(kScanThreads) void k_evict_finalize(EvictArgs a) {
-  __shared__ int buf[kScanThreads];
-  const int base = blockIdx.x * kScanBlock + threadIdx.x * kPerThread;
-  uint8_t kv[kPerThread];
-  int cnt = 0;
-#pragma unroll
-  for (int e = 0; e < kPerThread; ++e) {
-    const int i = base + e;
-    kv[e] = i < a.n_tokens ? a.keep[i] : 0;
-    cnt += kv[e];
-  }
-  buf[threadIdx.x] = cnt;
-  __syncthreads();
-  for (int o = 1; o < kScanThreads; o <<= 1) {
-    const int t = threadIdx.x >= o ? buf[threadIdx.x - o] : 0;
-    __syncthreads();
-    buf[threadIdx.x] += t;
-    __syncthreads();
-  }
-  int run = a.blocks[blockIdx.x] + buf[threadIdx.x] - cnt;
-#pragma unroll
+  if (base >= a.n_tokens) return;
+  int s = span_search(a.spans, a.n_spans, base);
   for (int e = 0; e < kPerThread; ++e) {
     const int i = base + e;
     if (i >= a.n_tokens) break;
-    a.dst[i] = run;
-    if (kv[e]) a.src_of[run] = i;
-    run += kv[e];
+    while (s + 1 < a.n_spans && a.spans[3 * (s + 1)] <= i) ++s;
+    int before = 0; // evicted tokens before i
+    bool inside = false;
+    if (s >= 0) {
+      const int st = a.spans[3 * s], en = a.spans[3 * s + 1];
+      inside = i < en;
+      before = a.spans[3 * s + 2] + (inside ? i - st : en - st);
+    }
+    const int d = i - before;
+    a.keep[i] = inside ? 0 : 1;
+    a.dst[i] = d;
+    if (!inside) a.src_of[d] = i;
   }
 }
 
 // ---------------------------------------------------------------------------
 // Gather: block (fresh page pi, layer * Hkv + head) fills destination page
 // fp + pi with the kept tokens (fp + pi) * P + j, j < P, j below L'.  Each
-// comes from token src_of[t] of the old pages (old_ids, from page fp on).
-// Old and fresh pages are distinct, so nothing is read after being written.
+// comes from token src_of[t] of the old pages, whose ids the page-table row
+// still holds (the new ids are written there by the next launch).  Old and
+// fresh pages are distinct, so nothing is read after being written.
 template <int D>
 __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   constexpr int U = D / 8;
@@ -271,7 +213,7 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
     const int t = t0 + threadIdx.x;
     if (t < a.new_len) {
       const int src = a.src_of[t];
-      spage[threadIdx.x] = a.old_ids[src / P - a.fp];
+      spage[threadIdx.x] = a.pt_row[src / P];
       sslot[threadIdx.x] = src % P;
     }
   }
@@ -291,12 +233,9 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
     const int j = idx % P, d = idx / P;
     if (j < nv) vd[d * P + j] = v_chunk(p, layer, spage[j], head)[d * P + sslot[j]];
   }
-  if (lh == 0) {
-    if (threadIdx.x < nv)
-      p.pos[(int64_t)dst_page * P + threadIdx.x] =
-          p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
-    if (threadIdx.x == 0) a.pt_row[a.fp + pi] = dst_page;
-  }
+  if (lh == 0 && threadIdx.x < nv)
+    p.pos[(int64_t)dst_page * P + threadIdx.x] =
+        p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
 }
 
 } // namespace
@@ -345,16 +284,10 @@ hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, 
   return hipGetLastError();
 }
 
-hipError_t launch_evict_scan(const EvictArgs &a, hipStream_t s) {
+hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s) {
   const int nblk = (a.n_tokens + kScanBlock - 1) / kScanBlock;
   if (nblk == 0) return hipSuccess;
-  hipLaunchKernelGGL(k_evict_count, dim3(nblk), dim3(kScanThreads), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_evict_scan_blocks, dim3(1), dim3(1024), 0, s, a.blocks, nblk);
-  e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(k_evict_finalize, dim3(nblk), dim3(kScanThreads), 0, s, a);
+  hipLaunchKernelGGL(k_evict_index, dim3(nblk), dim3(kScanThreads), 0, s, a);
   return hipGetLastError();
 }
 

@@ -59,24 +59,24 @@ struct AppendBatchArgs {
 };
 
 // ---- eviction -------------------------------------------------------------
+// Evicted spans as [n_spans][3] = (start, end, evicted tokens before start),
+// sorted, disjoint and non-empty.
 struct EvictArgs {
-  int32_t n_tokens;    // L
+  int32_t n_tokens;     // L
   int32_t n_spans;
-  const int32_t *spans; // [n_spans][2] sorted, disjoint, non-empty, device
-  uint8_t *keep;       // [L]
-  int32_t *dst;        // [L]
-  int32_t *src_of;     // [L']
-  int32_t *blocks;     // [ceil(L / kScanBlock) + 1]
+  const int32_t *spans; // device
+  uint8_t *keep;        // [L]
+  int32_t *dst;         // [L]
+  int32_t *src_of;      // [L']
 };
 
 struct GatherArgs {
-  int32_t fp;          // first affected page index
-  int32_t n_new;       // fresh pages
-  int32_t new_len;     // L'
+  int32_t fp;             // first affected page index
+  int32_t n_new;          // fresh pages
+  int32_t new_len;        // L'
   const int32_t *src_of;
-  const int32_t *old_ids; // old page ids from page index fp on, device
+  const int32_t *pt_row;  // device page-table row, still holding the old ids
   const int32_t *new_ids; // fresh page ids, device
-  int32_t *pt_row;        // device page-table row
 };
 
 // ---- decode ---------------------------------------------------------------
@@ -143,7 +143,7 @@ hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const v
 hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t tail_index,
                            int32_t tail_value, hipStream_t s);
 hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s);
-hipError_t launch_evict_scan(const EvictArgs &a, hipStream_t s);
+hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s);
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s);

@@ -49,7 +49,7 @@ constexpr uint64_t kAlign = 256;
 uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  uint64_t pt, keep, dst, src, blocks, upload, part_m, part_l, part_acc, total;
+  uint64_t pt, keep, dst, src, upload, part_m, part_l, part_acc, total;
   uint64_t upload_elems;
 };
 
@@ -66,8 +66,7 @@ Layout layout_of(const sq_store_config &c) {
   L.keep = take(max_tok);
   L.dst = take(max_tok * 4);
   L.src = take(max_tok * 4);
-  L.blocks = take((max_tok / sq::kScanBlock + 2) * 4);
-  L.upload_elems = 2ull * SQ_MAX_EVICT_SPANS + 2ull * c.max_pages_per_seq;
+  L.upload_elems = 3ull * SQ_MAX_EVICT_SPANS + (uint64_t)c.max_pages_per_seq;
   L.upload = take(L.upload_elems * 4);
   L.part_m = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
   L.part_l = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
@@ -190,7 +189,7 @@ struct sq_store {
   Layout lay{};
   int32_t *pt_dev = nullptr;
   uint8_t *ev_keep = nullptr;
-  int32_t *ev_dst = nullptr, *ev_src = nullptr, *ev_blocks = nullptr, *ev_upload = nullptr;
+  int32_t *ev_dst = nullptr, *ev_src = nullptr, *ev_upload = nullptr;
   float *part_m = nullptr, *part_l = nullptr, *part_acc = nullptr;
   int32_t *staging = nullptr;
   hipEvent_t staging_ev = nullptr;
@@ -201,6 +200,7 @@ struct sq_store {
 
   // tuning
   int target_items = 4096;
+  int min_chunk_pages = 32;
   bool auto_single_mfma = true;
   int mfma_waves = 4; // waves per MFMA work item (1, 2 or 4)
 
@@ -412,7 +412,9 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   int64_t work = 0;
   for (auto &ps : plan->segs) work += (ps.seg.ntok + s->P - 1) / s->P;
   work *= s->cfg.num_kv_heads;
-  int64_t chunk = std::max<int64_t>(1, (work + s->target_items - 1) / s->target_items);
+  // at least kMinChunkPages pages per item keeps the per-item fixed costs
+  // (query loads, the partial written and merged) small next to its pages
+  int64_t chunk = std::max<int64_t>(s->min_chunk_pages, (work + s->target_items - 1) / s->target_items);
   for (;;) {
     int64_t items = 0;
     for (auto &ps : plan->segs)
@@ -501,6 +503,10 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     if (v >= 1) s->target_items = v;
   }
   if (const char *e = std::getenv("SQ_AUTO_SINGLE")) s->auto_single_mfma = std::strcmp(e, "valu") != 0;
+  if (const char *e = std::getenv("SQ_MIN_CHUNK")) {
+    const int v = std::atoi(e);
+    if (v >= 1) s->min_chunk_pages = v;
+  }
   if (const char *e = std::getenv("SQ_MFMA_WAVES")) {
     const int v = std::atoi(e);
     if (v == 1 || v == 2 || v == 4) s->mfma_waves = v;
@@ -512,7 +518,6 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     s->ev_keep = reinterpret_cast<uint8_t *>(ws + lay.keep);
     s->ev_dst = reinterpret_cast<int32_t *>(ws + lay.dst);
     s->ev_src = reinterpret_cast<int32_t *>(ws + lay.src);
-    s->ev_blocks = reinterpret_cast<int32_t *>(ws + lay.blocks);
     s->ev_upload = reinterpret_cast<int32_t *>(ws + lay.upload);
     s->part_m = reinterpret_cast<float *>(ws + lay.part_m);
     s->part_l = reinterpret_cast<float *>(ws + lay.part_l);
@@ -830,15 +835,14 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
   if (s->device) {
     hipStream_t strm = static_cast<hipStream_t>(stream);
     s->last_stream = strm;
-    // upload: spans [2 * nsp] | old page ids from fp [n_old] | new page ids [n_new]
+    // upload: spans [nsp][3] (start, end, evicted before) | new page ids [n_new]
     std::vector<int32_t> up;
-    up.reserve(2 * sp.size() + old_tail.size() + new_ids.size());
-    for (auto &x : sp) {
-      up.push_back((int32_t)x.first);
-      up.push_back((int32_t)x.second);
+    up.reserve(3 * sp.size() + new_ids.size());
+    for (size_t k = 0; k < sp.size(); ++k) {
+      up.push_back((int32_t)sp[k].first);
+      up.push_back((int32_t)sp[k].second);
+      up.push_back((int32_t)prefix[k]);
     }
-    const size_t off_old = up.size();
-    up.insert(up.end(), old_tail.begin(), old_tail.end());
     const size_t off_new = up.size();
     up.insert(up.end(), new_ids.begin(), new_ids.end());
     sq_status us = upload(s, s->ev_upload, up.data(), up.size(), strm);
@@ -850,24 +854,27 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     ea.keep = s->ev_keep;
     ea.dst = s->ev_dst;
     ea.src_of = s->ev_src;
-    ea.blocks = s->ev_blocks;
     ProfPair pp;
     bool on = s->prof_begin(strm, &pp, kProfScan);
-    hipError_t e = sq::launch_evict_scan(ea, strm);
+    hipError_t e = sq::launch_evict_index(ea, strm);
     s->prof_end(strm, &pp, on);
-    if (e != hipSuccess) return hip_fail(e, "eviction scan");
+    if (e != hipSuccess) return hip_fail(e, "eviction index");
     sq::GatherArgs ga{};
     ga.fp = (int32_t)fp;
     ga.n_new = (int32_t)n_new;
     ga.new_len = (int32_t)Lp;
     ga.src_of = s->ev_src;
-    ga.old_ids = s->ev_upload + off_old;
-    ga.new_ids = s->ev_upload + off_new;
     ga.pt_row = s->pt_row(h);
+    ga.new_ids = s->ev_upload + off_new;
     on = s->prof_begin(strm, &pp, kProfGather);
     e = sq::launch_evict_gather(s->pools, ga, strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "eviction gather");
+    if (n_new > 0) { // the page-table row takes the fresh ids after the gather read the old
+      e = sq::launch_copy_i32(s->pt_row(h) + fp, s->ev_upload + off_new, (int32_t)n_new, -1, -1,
+                              strm);
+      if (e != hipSuccess) return hip_fail(e, "page-table update");
+    }
     s->have_last_evict = true;
     s->last_evict_L = L;
     s->last_evict_Lp = Lp;
