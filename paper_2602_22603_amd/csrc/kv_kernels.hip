@@ -170,25 +170,45 @@ __device__ inline int span_search(const int32_t *spans, int n_spans, int i) {
 }
 
 __global__ __launch_bounds__(kScanThreads) void k_evict_index(EvictArgs a) {
+  __shared__ int32_t lsp[3 * kInlineSpans];
+  const bool inl = a.n_spans <= kInlineSpans;
+  if (inl)
+    for (int i = threadIdx.x; i < 3 * a.n_spans; i += blockDim.x) lsp[i] = a.inl[i];
+  __syncthreads();
+  const int32_t *spans = inl ? lsp : a.spans;
   const int base = blockIdx.x * kScanBlock + threadIdx.x * kPerThread;
   if (base >= a.n_tokens) return;
-  int s = span_search(a.spans, a.n_spans, base);
+  int s = span_search(spans, a.n_spans, base);
   for (int e = 0; e < kPerThread; ++e) {
     const int i = base + e;
     if (i >= a.n_tokens) break;
-    while (s + 1 < a.n_spans && a.spans[3 * (s + 1)] <= i) ++s;
+    while (s + 1 < a.n_spans && spans[3 * (s + 1)] <= i) ++s;
     int before = 0; // evicted tokens before i
     bool inside = false;
     if (s >= 0) {
-      const int st = a.spans[3 * s], en = a.spans[3 * s + 1];
+      const int st = spans[3 * s], en = spans[3 * s + 1];
       inside = i < en;
-      before = a.spans[3 * s + 2] + (inside ? i - st : en - st);
+      before = spans[3 * s + 2] + (inside ? i - st : en - st);
     }
     const int d = i - before;
     a.keep[i] = inside ? 0 : 1;
     a.dst[i] = d;
     if (!inside) a.src_of[d] = i;
   }
+}
+
+// Fresh page id number i of an eviction.
+__device__ inline int32_t new_page_id(const NewIds &ids, int i) {
+  if (ids.list) return ids.list[i];
+  int r = 0;
+  while (r + 1 < ids.n_runs && ids.before[r + 1] <= i) ++r;
+  return ids.first[r] + (i - ids.before[r]);
+}
+
+// dst[i] = fresh id i: the page-table row takes the fresh ids after the gather.
+__global__ __launch_bounds__(256) void k_write_ids(int32_t *dst, NewIds ids, int32_t n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = new_page_id(ids, i);
 }
 
 // ---------------------------------------------------------------------------
@@ -207,7 +227,7 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   const int lh = blockIdx.y;
   const int layer = lh / p.hkv;
   const int head = lh % p.hkv;
-  const int dst_page = a.new_ids[pi];
+  const int dst_page = new_page_id(a.ids, pi);
   const int t0 = (a.fp + pi) * P;
   if (threadIdx.x < P) {
     const int t = t0 + threadIdx.x;
@@ -288,6 +308,12 @@ hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s) {
   const int nblk = (a.n_tokens + kScanBlock - 1) / kScanBlock;
   if (nblk == 0) return hipSuccess;
   hipLaunchKernelGGL(k_evict_index, dim3(nblk), dim3(kScanThreads), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  hipLaunchKernelGGL(k_write_ids, dim3((n + 255) / 256), dim3(256), 0, s, dst, ids, n);
   return hipGetLastError();
 }
 

@@ -60,14 +60,28 @@ struct AppendBatchArgs {
 
 // ---- eviction -------------------------------------------------------------
 // Evicted spans as [n_spans][3] = (start, end, evicted tokens before start),
-// sorted, disjoint and non-empty.
+// sorted, disjoint and non-empty: up to kInlineSpans travel in the kernel
+// arguments, more are read from device memory.
+constexpr int kInlineSpans = 96;
+constexpr int kInlineRanges = 60;
+
 struct EvictArgs {
   int32_t n_tokens;     // L
   int32_t n_spans;
-  const int32_t *spans; // device
+  const int32_t *spans; // device copy when n_spans > kInlineSpans
   uint8_t *keep;        // [L]
   int32_t *dst;         // [L]
   int32_t *src_of;      // [L']
+  int32_t inl[3 * kInlineSpans];
+};
+
+// The fresh page ids of an eviction: a device list, or (when they form at
+// most kInlineRanges runs of consecutive ids) the runs themselves.
+struct NewIds {
+  const int32_t *list;            // device, or null when the runs are used
+  int32_t n_runs;
+  int32_t first[kInlineRanges];   // first id of run r
+  int32_t before[kInlineRanges];  // fresh pages before run r
 };
 
 struct GatherArgs {
@@ -76,7 +90,7 @@ struct GatherArgs {
   int32_t new_len;        // L'
   const int32_t *src_of;
   const int32_t *pt_row;  // device page-table row, still holding the old ids
-  const int32_t *new_ids; // fresh page ids, device
+  NewIds ids;
 };
 
 // ---- decode ---------------------------------------------------------------
@@ -134,6 +148,8 @@ static_assert(sizeof(AppendArgs) < 4096, "append kernel arguments too large");
 static_assert(sizeof(AppendBatchArgs) < 4096, "append-batch kernel arguments too large");
 static_assert(sizeof(DecodeArgs) < 4096, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) < 4096, "merge kernel arguments too large");
+static_assert(sizeof(EvictArgs) < 4096, "eviction index arguments too large");
+static_assert(sizeof(GatherArgs) + sizeof(Pools) < 4096, "gather arguments too large");
 
 // ---- launchers (return the launch status) ------------------------------------
 hipError_t launch_append(const Pools &p, const AppendArgs &a, const void *k_new,
@@ -144,6 +160,7 @@ hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t 
                            int32_t tail_value, hipStream_t s);
 hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s);
 hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s);
+hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStream_t s);
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s);

@@ -231,6 +231,26 @@ struct sq_store {
     return -1; // callers check n_free first
   }
 
+  // n pages, lowest free ids first, in order (callers check n_free first)
+  void alloc_pages(int64_t n, int32_t *out) {
+    const int32_t nw = (int32_t)freebits.size();
+    int64_t got = 0;
+    for (int32_t w = free_hint / 64; w < nw && got < n; ++w) {
+      uint64_t bits = freebits[w];
+      while (bits && got < n) {
+        const int bit = __builtin_ctzll(bits);
+        const int32_t id = w * 64 + bit;
+        bits &= bits - 1;
+        refcount[id] = 1;
+        out[got++] = id;
+        free_hint = id + 1;
+      }
+      freebits[w] = bits;
+    }
+    n_free -= got;
+    peak_pages = std::max(peak_pages, live_pages());
+  }
+
   void unref(int32_t id, int64_t *freed) {
     if (--refcount[id] == 0) {
       freebits[id / 64] |= 1ull << (id % 64);
@@ -827,33 +847,60 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     return fail(SQ_ERR_NO_PAGES, "eviction needs %lld fresh pages, %lld free", (long long)n_new,
                 (long long)s->n_free);
 
-  // ---- commit: allocate, gather, release ----
+  // ---- commit: allocate, enqueue the device work, then the host bookkeeping ----
   std::vector<int32_t> new_ids(n_new);
-  for (int64_t i = 0; i < n_new; ++i) new_ids[i] = s->alloc_page();
+  s->alloc_pages(n_new, new_ids.data());
   std::vector<int32_t> old_tail(q->pages.begin() + fp, q->pages.end());
 
   if (s->device) {
     hipStream_t strm = static_cast<hipStream_t>(stream);
     s->last_stream = strm;
-    // upload: spans [nsp][3] (start, end, evicted before) | new page ids [n_new]
-    std::vector<int32_t> up;
-    up.reserve(3 * sp.size() + new_ids.size());
-    for (size_t k = 0; k < sp.size(); ++k) {
-      up.push_back((int32_t)sp[k].first);
-      up.push_back((int32_t)sp[k].second);
-      up.push_back((int32_t)prefix[k]);
-    }
-    const size_t off_new = up.size();
-    up.insert(up.end(), new_ids.begin(), new_ids.end());
-    sq_status us = upload(s, s->ev_upload, up.data(), up.size(), strm);
-    if (us != SQ_OK) return us;
     sq::EvictArgs ea{};
     ea.n_tokens = (int32_t)L;
     ea.n_spans = (int32_t)sp.size();
-    ea.spans = s->ev_upload;
     ea.keep = s->ev_keep;
     ea.dst = s->ev_dst;
     ea.src_of = s->ev_src;
+    sq::NewIds ids{};
+    // runs of consecutive fresh ids (the allocator usually hands out a few)
+    for (int64_t i = 0; i < n_new; ++i) {
+      if (i == 0 || new_ids[i] != new_ids[i - 1] + 1) {
+        if (ids.n_runs == sq::kInlineRanges) {
+          ids.n_runs = -1;
+          break;
+        }
+        ids.first[ids.n_runs] = new_ids[i];
+        ids.before[ids.n_runs] = (int32_t)i;
+        ++ids.n_runs;
+      }
+    }
+    // what does not fit in the kernel arguments goes up in one copy:
+    // spans [nsp][3] (start, end, evicted before) | fresh ids [n_new]
+    std::vector<int32_t> up;
+    const bool spans_inline = sp.size() <= (size_t)sq::kInlineSpans;
+    for (size_t k = 0; k < sp.size(); ++k) {
+      int32_t *dst3 = nullptr;
+      int32_t tmp[3] = {(int32_t)sp[k].first, (int32_t)sp[k].second, (int32_t)prefix[k]};
+      if (spans_inline) {
+        dst3 = ea.inl + 3 * k;
+        dst3[0] = tmp[0];
+        dst3[1] = tmp[1];
+        dst3[2] = tmp[2];
+      } else {
+        up.insert(up.end(), tmp, tmp + 3);
+      }
+    }
+    const size_t off_new = up.size();
+    if (ids.n_runs < 0) {
+      ids.n_runs = 0;
+      up.insert(up.end(), new_ids.begin(), new_ids.end());
+      ids.list = s->ev_upload + off_new;
+    }
+    if (!up.empty()) {
+      sq_status us = upload(s, s->ev_upload, up.data(), up.size(), strm);
+      if (us != SQ_OK) return us;
+    }
+    ea.spans = spans_inline ? nullptr : s->ev_upload;
     ProfPair pp;
     bool on = s->prof_begin(strm, &pp, kProfScan);
     hipError_t e = sq::launch_evict_index(ea, strm);
@@ -865,16 +912,14 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     ga.new_len = (int32_t)Lp;
     ga.src_of = s->ev_src;
     ga.pt_row = s->pt_row(h);
-    ga.new_ids = s->ev_upload + off_new;
+    ga.ids = ids;
     on = s->prof_begin(strm, &pp, kProfGather);
     e = sq::launch_evict_gather(s->pools, ga, strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "eviction gather");
-    if (n_new > 0) { // the page-table row takes the fresh ids after the gather read the old
-      e = sq::launch_copy_i32(s->pt_row(h) + fp, s->ev_upload + off_new, (int32_t)n_new, -1, -1,
-                              strm);
-      if (e != hipSuccess) return hip_fail(e, "page-table update");
-    }
+    // the page-table row takes the fresh ids after the gather has read the old
+    e = sq::launch_write_ids(s->pt_row(h) + fp, ids, (int32_t)n_new, strm);
+    if (e != hipSuccess) return hip_fail(e, "page-table update");
     s->have_last_evict = true;
     s->last_evict_L = L;
     s->last_evict_Lp = Lp;
