@@ -109,29 +109,36 @@ __device__ inline uint32_t pack_bf16(float lo, float hi) {
   return u;
 }
 
+// One piece of a workgroup's page range: pages [pbeg, pend) of KV head g of
+// segment sg, whose partial goes to slot.
 struct ItemPos {
   Seg sg;
   int g;        // KV head
   int pbeg;     // first page (segment-local)
   int pend;     // one past the last page
   int npages;   // pages in the segment
+  int slot;     // partial slot
 };
 
-__device__ inline ItemPos locate(const DecodeArgs &a, int item) {
+// The piece starting at flattened page x of workgroup w (range ends at xe);
+// advances x past it.
+__device__ inline ItemPos next_piece(const DecodeArgs &a, int w, int64_t &x, int64_t xe) {
   int lo = 0, hi = a.n_segs - 1;
   while (lo < hi) {
     const int mid = (lo + hi + 1) >> 1;
-    if (a.segs[mid].item0 <= item) lo = mid;
+    if (a.segs[mid].start <= x) lo = mid;
     else hi = mid - 1;
   }
   ItemPos ip;
   ip.sg = a.segs[lo];
-  const int local = item - ip.sg.item0;
-  ip.g = local / ip.sg.nchunk;
-  const int c = local - ip.g * ip.sg.nchunk;
   ip.npages = (ip.sg.ntok + P - 1) / P;
-  ip.pbeg = c * a.chunk_pages;
-  ip.pend = min(ip.pbeg + a.chunk_pages, ip.npages);
+  ip.g = (int)((x - ip.sg.start) / ip.npages);
+  const int64_t rs = ip.sg.start + (int64_t)ip.g * ip.npages;
+  const int64_t pe = min(xe, rs + ip.npages);
+  ip.pbeg = (int)(x - rs);
+  ip.pend = (int)(pe - rs);
+  ip.slot = a.slot_base + w + lo * a.hkv + ip.g;
+  x = pe;
   return ip;
 }
 
@@ -161,8 +168,10 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float sA[G];
 
   const int lane = threadIdx.x;
-  const int item = a.item_begin + blockIdx.x;
-  const ItemPos ip = locate(a, item);
+  const int64_t x_end = (int64_t)(blockIdx.x + 1) * a.total / a.n_wg;
+  int64_t x_pos = (int64_t)blockIdx.x * a.total / a.n_wg;
+  while (x_pos < x_end) {
+  const ItemPos ip = next_piece(a, blockIdx.x, x_pos, x_end);
   const int b = ip.sg.mem & 0xff;
   const int g = ip.g;
   const int32_t *pt = a.pt + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
@@ -335,7 +344,7 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
       acc[r][e] = y;
     }
 
-  const int64_t prow = (int64_t)item * kRows;
+  const int64_t prow = (int64_t)ip.slot * kRows;
   if (t == 0 && (G >= 4 || c < G)) {
 #pragma unroll
     for (int k = 0; k < RPL; ++k) {
@@ -354,6 +363,8 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
             make_float4(acc[r][e], acc[r][e + 1], acc[r][e + 2], acc[r][e + 3]);
     }
   }
+  __syncthreads();
+  } // pieces
 }
 
 // ===========================================================================
@@ -454,8 +465,10 @@ k_decode_mfma(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = threadIdx.x >> 6;
   const int n = lane & 15, kg = lane >> 4;
-  const int item = a.item_begin + blockIdx.x;
-  const ItemPos ip = locate(a, item);
+  const int64_t x_end = (int64_t)(blockIdx.x + 1) * a.total / a.n_wg;
+  int64_t x_pos = (int64_t)blockIdx.x * a.total / a.n_wg;
+  while (x_pos < x_end) {
+  const ItemPos ip = next_piece(a, blockIdx.x, x_pos, x_end);
   const int g = ip.g;
   const int nrows = ip.sg.nmem * G;
   const bool qvalid = n < nrows;
@@ -513,7 +526,7 @@ k_decode_mfma(DecodeArgs a) {
     *reinterpret_cast<float4 *>(&s_acc[wave][n * APITCH + 16 * j + 4 * kg]) =
         make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
   __syncthreads();
-  const int64_t prow = (int64_t)item * kRows;
+  const int64_t prow = (int64_t)ip.slot * kRows;
   if (threadIdx.x < kRows && (int)threadIdx.x < nrows) {
     const int r = threadIdx.x;
     float mm = kNegInf;
@@ -552,6 +565,8 @@ k_decode_mfma(DecodeArgs a) {
       *reinterpret_cast<float4 *>(a.part_acc + (prow + r) * D + d0 + e) = o;
     }
   }
+  __syncthreads(); // the next piece reuses the LDS
+  } // pieces
 }
 
 // ===========================================================================
@@ -578,13 +593,22 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
   const int ns = a.n_src[b];
   int n0 = 0, n1 = 0;
   int64_t base0 = 0, base1 = 0;
-  if (ns > 0) {
-    n0 = a.nchunk[b][0];
-    base0 = (int64_t)(a.item_base[b][0] + g * n0) * kRows + a.member[b][0] * a.group + hr;
-  }
-  if (ns > 1) {
-    n1 = a.nchunk[b][1];
-    base1 = (int64_t)(a.item_base[b][1] + g * n1) * kRows + a.member[b][1] * a.group + hr;
+  for (int e = 0; e < ns; ++e) {
+    const int L = a.src_launch[b][e];
+    const int np = a.src_npages[b][e];
+    const int64_t R = (int64_t)a.src_start[b][e] + (int64_t)g * np; // row start
+    const int w_lo = wg_of(R, a.total[L], a.n_wg[L]);
+    const int w_hi = wg_of(R + np - 1, a.total[L], a.n_wg[L]);
+    const int r = a.src_seg[b][e] * a.hkv + g;
+    const int64_t base = (int64_t)(a.slot_base[L] + w_lo + r) * kRows +
+                         a.src_member[b][e] * a.group + hr;
+    if (e == 0) {
+      n0 = w_hi - w_lo + 1;
+      base0 = base;
+    } else {
+      n1 = w_hi - w_lo + 1;
+      base1 = base;
+    }
   }
   const int total = n0 + n1;
   auto row_of = [&](int c) -> int64_t {
@@ -671,7 +695,7 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
 
 template <int D, bool NT>
 hipError_t valu_dispatch_nt(int group, const DecodeArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_items), block(64);
+  const dim3 grid(a.n_wg), block(64);
   switch (group) {
   case 1: hipLaunchKernelGGL((k_decode_valu<D, 1, NT>), grid, block, 0, s, a); break;
   case 2: hipLaunchKernelGGL((k_decode_valu<D, 2, NT>), grid, block, 0, s, a); break;
@@ -690,7 +714,7 @@ hipError_t valu_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
 
 template <int D, int W, bool NT>
 hipError_t mfma_dispatch_w(int group, const DecodeArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_items), block(64 * W);
+  const dim3 grid(a.n_wg), block(64 * W);
   switch (group) {
   case 1: hipLaunchKernelGGL((k_decode_mfma<D, 1, W, NT>), grid, block, 0, s, a); break;
   case 2: hipLaunchKernelGGL((k_decode_mfma<D, 2, W, NT>), grid, block, 0, s, a); break;
@@ -719,13 +743,46 @@ hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t 
 
 } // namespace
 
+namespace {
+template <int D> const void *valu_fn(int group) {
+  switch (group) {
+  case 1: return reinterpret_cast<const void *>(&k_decode_valu<D, 1, true>);
+  case 2: return reinterpret_cast<const void *>(&k_decode_valu<D, 2, true>);
+  case 4: return reinterpret_cast<const void *>(&k_decode_valu<D, 4, true>);
+  case 8: return reinterpret_cast<const void *>(&k_decode_valu<D, 8, true>);
+  default: return nullptr;
+  }
+}
+template <int D, int W> const void *mfma_fn_w(int group) {
+  switch (group) {
+  case 1: return reinterpret_cast<const void *>(&k_decode_mfma<D, 1, W, true>);
+  case 2: return reinterpret_cast<const void *>(&k_decode_mfma<D, 2, W, true>);
+  case 4: return reinterpret_cast<const void *>(&k_decode_mfma<D, 4, W, true>);
+  case 8: return reinterpret_cast<const void *>(&k_decode_mfma<D, 8, W, true>);
+  default: return nullptr;
+  }
+}
+template <int D> const void *mfma_fn(int group, int waves) {
+  return waves == 1 ? mfma_fn_w<D, 1>(group) : waves == 2 ? mfma_fn_w<D, 2>(group)
+                                                          : mfma_fn_w<D, 4>(group);
+}
+} // namespace
+
+hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out) {
+  const void *fn = kind == 0 ? (d == 128 ? valu_fn<128>(group) : valu_fn<64>(group))
+                             : (d == 128 ? mfma_fn<128>(group, waves) : mfma_fn<64>(group, waves));
+  if (!fn) return hipErrorInvalidValue;
+  const int block = kind == 0 ? 64 : 64 * waves;
+  return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, fn, block, 0);
+}
+
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s) {
-  if (a.n_items == 0) return hipSuccess;
+  if (a.n_wg == 0) return hipSuccess;
   return d == 128 ? valu_dispatch<128>(group, a, s) : valu_dispatch<64>(group, a, s);
 }
 
 hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s) {
-  if (a.n_items == 0) return hipSuccess;
+  if (a.n_wg == 0) return hipSuccess;
   return d == 128 ? mfma_dispatch<128>(group, waves, a, s) : mfma_dispatch<64>(group, waves, a, s);
 }
 

@@ -199,8 +199,11 @@ struct sq_store {
   int64_t last_evict_L = 0, last_evict_Lp = 0;
 
   // tuning
-  int target_items = 4096;
-  int min_chunk_pages = 32;
+  int grid_rounds = 2;        // workgroups per launch = rounds * CUs * workgroups per CU
+  int cus = 256;              // compute units (device query in device mode)
+  int wg_per_cu[2] = {8, 3};  // resident workgroups per CU (VALU, MFMA), from occupancy
+  int min_wg_pages_valu = 8;
+  int min_wg_pages_mfma = 32;
   bool auto_single_mfma = true;
   int mfma_waves = 4; // waves per MFMA work item (1, 2 or 4)
 
@@ -333,8 +336,10 @@ struct PlanSeg {
 struct Plan {
   std::vector<PlanSeg> segs;
   int n_groups = 0;
-  int chunk_pages = 1;
-  int n_items_valu = 0, n_items_mfma = 0;
+  int64_t total[2] = {0, 0}; // flattened pages per launch (0: VALU, 1: MFMA)
+  int32_t n_wg[2] = {0, 0};  // workgroups per launch
+  int32_t slot_base[2] = {0, 0};
+  int32_t seg_index[sq::kMaxSegs]; // index of each segment inside its launch
   bool pages_reread = false; // some page is read by more than one segment
   int64_t kv_bytes = 0, kv_bytes_logical = 0, io_bytes = 0;
   int64_t kv_bytes_valu = 0, kv_bytes_mfma = 0;
@@ -428,41 +433,42 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     if (rest > 0) add_seg(seqs[b], (int32_t)start_page, rest, single_mfma, {b});
   }
 
-  // chunking: roughly target_items work items over all segments
-  int64_t work = 0;
-  for (auto &ps : plan->segs) work += (ps.seg.ntok + s->P - 1) / s->P;
-  work *= s->cfg.num_kv_heads;
-  // at least kMinChunkPages pages per item keeps the per-item fixed costs
-  // (query loads, the partial written and merged) small next to its pages
-  int64_t chunk = std::max<int64_t>(s->min_chunk_pages, (work + s->target_items - 1) / s->target_items);
-  for (;;) {
-    int64_t items = 0;
-    for (auto &ps : plan->segs)
-      items += ((ps.seg.ntok + s->P - 1) / s->P + chunk - 1) / chunk * s->cfg.num_kv_heads;
-    if (items <= sq::kMaxItems) break;
-    chunk = chunk * 2;
-  }
-  plan->chunk_pages = (int)chunk;
-  // items: VALU segments first, then MFMA segments
-  int32_t item = 0;
-  for (int pass = 0; pass < 2; ++pass) {
-    for (auto &ps : plan->segs) {
-      if (ps.mfma != (pass == 1)) continue;
-      const int64_t np = (ps.seg.ntok + s->P - 1) / s->P;
-      ps.seg.nchunk = (int32_t)((np + chunk - 1) / chunk);
-      ps.seg.item0 = item;
-      item += ps.seg.nchunk * s->cfg.num_kv_heads;
-      if (pass == 0) plan->n_items_valu += ps.seg.nchunk * s->cfg.num_kv_heads;
-      else plan->n_items_mfma += ps.seg.nchunk * s->cfg.num_kv_heads;
-      plan->kv_bytes += (int64_t)ps.seg.ntok * tok_bytes;
-      (pass == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += (int64_t)ps.seg.ntok * tok_bytes;
-      plan->io_bytes += np * 4;
-    }
-  }
-  plan->io_bytes += (int64_t)batch * s->cfg.num_q_heads * s->cfg.head_dim * (2 + 4);
   if ((int)plan->segs.size() > sq::kMaxSegs)
     return fail(SQ_ERR_INVALID, "decode batch needs %d segments (max %d)", (int)plan->segs.size(),
                 sq::kMaxSegs);
+  // Each launch lays its segments' rows (segment, KV head) end to end in one
+  // flattened page range and splits it evenly over its workgroups: enough
+  // workgroups to fill the GPU `grid_rounds` times, at least `min_wg_pages`
+  // pages each, never more workgroups than pages.
+  const int hkv = s->cfg.num_kv_heads;
+  int count[2] = {0, 0};
+  for (size_t i = 0; i < plan->segs.size(); ++i) {
+    PlanSeg &ps = plan->segs[i];
+    const int L = ps.mfma ? 1 : 0;
+    const int64_t np = (ps.seg.ntok + s->P - 1) / s->P;
+    ps.seg.start = (int32_t)plan->total[L];
+    plan->seg_index[i] = count[L]++;
+    plan->total[L] += np * hkv;
+    plan->kv_bytes += (int64_t)ps.seg.ntok * tok_bytes;
+    (L == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += (int64_t)ps.seg.ntok * tok_bytes;
+    plan->io_bytes += np * 4;
+  }
+  int32_t slots = 0;
+  for (int L = 0; L < 2; ++L) {
+    if (plan->total[L] == 0) continue;
+    if (plan->total[L] > INT32_MAX) return fail(SQ_ERR_INVALID, "decode batch too large");
+    const int64_t fill = (int64_t)s->grid_rounds * s->cus * s->wg_per_cu[L];
+    const int64_t min_pages = L == 1 ? s->min_wg_pages_mfma : s->min_wg_pages_valu;
+    int64_t n = std::min<int64_t>(fill, (plan->total[L] + min_pages - 1) / min_pages);
+    n = std::max<int64_t>(1, std::min<int64_t>(n, plan->total[L]));
+    const int64_t room = sq::kMaxItems - slots - (int64_t)count[L] * hkv;
+    if (room < 1) return fail(SQ_ERR_INVALID, "decode batch needs too many partial slots");
+    n = std::min<int64_t>(n, room);
+    plan->n_wg[L] = (int32_t)n;
+    plan->slot_base[L] = slots;
+    slots += (int32_t)n + count[L] * hkv;
+  }
+  plan->io_bytes += (int64_t)batch * s->cfg.num_q_heads * s->cfg.head_dim * (2 + 4);
   return SQ_OK;
 }
 
@@ -518,15 +524,11 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
   for (int32_t i = 0; i < cfg->num_pages; ++i) s->freebits[i / 64] |= 1ull << (i % 64);
   s->n_free = cfg->num_pages;
   s->seqs.resize(cfg->max_seqs);
-  if (const char *e = std::getenv("SQ_TARGET_ITEMS")) {
+  if (const char *e = std::getenv("SQ_GRID_ROUNDS")) {
     const int v = std::atoi(e);
-    if (v >= 1) s->target_items = v;
+    if (v >= 1 && v <= 64) s->grid_rounds = v;
   }
   if (const char *e = std::getenv("SQ_AUTO_SINGLE")) s->auto_single_mfma = std::strcmp(e, "valu") != 0;
-  if (const char *e = std::getenv("SQ_MIN_CHUNK")) {
-    const int v = std::atoi(e);
-    if (v >= 1) s->min_chunk_pages = v;
-  }
   if (const char *e = std::getenv("SQ_MFMA_WAVES")) {
     const int v = std::atoi(e);
     if (v == 1 || v == 2 || v == 4) s->mfma_waves = v;
@@ -553,6 +555,17 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     p.page_stride = (int64_t)s->P * s->D;
     p.head_stride = p.page_stride * cfg->num_pages;
     p.layer_stride = p.head_stride * cfg->num_kv_heads;
+    {
+      int dev = 0, cus = 0, nb = 0;
+      if (hipGetDevice(&dev) == hipSuccess &&
+          hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+          cus > 0)
+        s->cus = cus;
+      if (sq::decode_blocks_per_cu(0, s->D, s->G, 1, &nb) == hipSuccess && nb > 0) s->wg_per_cu[0] = nb;
+      nb = 0;
+      if (sq::decode_blocks_per_cu(1, s->D, s->G, s->mfma_waves, &nb) == hipSuccess && nb > 0)
+        s->wg_per_cu[1] = nb;
+    }
     void *host = nullptr;
     hipError_t e = hipHostMalloc(&host, lay.upload_elems * 4, hipHostMallocDefault);
     if (e != hipSuccess) {
@@ -997,9 +1010,10 @@ sq_status sq_decode_plan_info(sq_store *s, const sq_seq *seqs, int32_t batch, in
   *out = sq_plan_info{};
   out->n_segments = (int32_t)plan.segs.size();
   out->n_groups = plan.n_groups;
-  out->n_items_valu = plan.n_items_valu;
-  out->n_items_mfma = plan.n_items_mfma;
-  out->chunk_pages = plan.chunk_pages;
+  out->n_items_valu = plan.n_wg[0];
+  out->n_items_mfma = plan.n_wg[1];
+  out->chunk_pages = plan.n_wg[1] ? (int32_t)(plan.total[1] / plan.n_wg[1])
+                                   : plan.n_wg[0] ? (int32_t)(plan.total[0] / plan.n_wg[0]) : 0;
   out->kv_bytes = plan.kv_bytes;
   out->kv_bytes_logical = plan.kv_bytes_logical;
   out->kv_bytes_valu = plan.kv_bytes_valu;
@@ -1038,8 +1052,9 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   base.head_stride = s->pools.head_stride;
   base.max_pages = s->cfg.max_pages_per_seq;
   base.hq = s->cfg.num_q_heads;
-  base.chunk_pages = plan.chunk_pages;
+  base.hkv = s->cfg.num_kv_heads;
   base.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  base.nontemporal = plan.pages_reread ? 0 : 1;
   sq::MergeArgs ma{};
   ma.out = out;
   ma.part_m = s->part_m;
@@ -1047,23 +1062,33 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   ma.part_acc = s->part_acc;
   ma.hq = s->cfg.num_q_heads;
   ma.group = s->G;
-  for (const PlanSeg &ps : plan.segs)
+  ma.hkv = s->cfg.num_kv_heads;
+  for (int L = 0; L < 2; ++L) {
+    ma.total[L] = (int32_t)plan.total[L];
+    ma.n_wg[L] = plan.n_wg[L];
+    ma.slot_base[L] = plan.slot_base[L];
+  }
+  for (size_t i = 0; i < plan.segs.size(); ++i) {
+    const PlanSeg &ps = plan.segs[i];
     for (int j = 0; j < ps.seg.nmem; ++j) {
       const int b = ps.members[j];
       const int e = ma.n_src[b]++;
-      ma.item_base[b][e] = ps.seg.item0;
-      ma.nchunk[b][e] = ps.seg.nchunk;
-      ma.member[b][e] = j;
+      ma.src_launch[b][e] = ps.mfma ? 1 : 0;
+      ma.src_seg[b][e] = plan.seg_index[i];
+      ma.src_start[b][e] = ps.seg.start;
+      ma.src_npages[b][e] = (ps.seg.ntok + s->P - 1) / s->P;
+      ma.src_member[b][e] = j;
     }
+  }
   for (int pass = 0; pass < 2; ++pass) {
     sq::DecodeArgs a = base;
     a.n_segs = 0;
     for (const PlanSeg &ps : plan.segs)
       if (ps.mfma == (pass == 1)) a.segs[a.n_segs++] = ps.seg;
-    a.item_begin = pass == 0 ? 0 : plan.n_items_valu;
-    a.nontemporal = plan.pages_reread ? 0 : 1;
-    a.n_items = pass == 0 ? plan.n_items_valu : plan.n_items_mfma;
-    if (a.n_items == 0) continue;
+    a.total = (int32_t)plan.total[pass];
+    a.n_wg = plan.n_wg[pass];
+    a.slot_base = plan.slot_base[pass];
+    if (a.n_wg == 0) continue;
     ProfPair pp;
     const bool on = s->prof_begin(strm, &pp, pass == 0 ? kProfValu : kProfMfma);
     hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, a, strm)
