@@ -258,7 +258,7 @@ def main():
     legs = set(args.legs.split(","))
     torch.cuda.set_device(0)
     total = args.warmup + args.steps
-    n_modes = 3 if "modes" in legs else 0
+    n_modes = 5 if "modes" in legs else 0
     extra = total * (1 + n_modes) + 16
     log(f"building {args.tasks} tasks at {args.ctx} tokens ...")
     from paper_2602_22603_amd import drivers
@@ -300,6 +300,20 @@ def main():
                                gbps_logical_bytes=round(r["kv_bytes_logical_per_step"] /
                                                         (r["ms_per_step"] * 1e-3) / 1e9, 1),
                                tokens_per_s=round(r["tokens_per_s"], 1))
+        # the per-sequence kernels on unique pages: the 8 main threads alone
+        mains = seqs[0::2]
+        for name, m in (("mains_only_stream_valu", sq.ATTN_STREAM),
+                        ("mains_only_mfma", sq.ATTN_MFMA)):
+            log(f"timing {name} ...")
+            r = time_steps(sq, torch, store, mains, m, args.steps, args.warmup,
+                           [x[:, 0::2].contiguous() for x in kb], [x[:, 0::2].contiguous() for x in vb],
+                           [x[0::2].contiguous() for x in qs], out[0::2].contiguous())
+            kern = r["prof"]["decode_valu_ms" if m == sq.ATTN_STREAM else "decode_mfma_ms"]
+            nk = r["prof"]["decode_valu_launches" if m == sq.ATTN_STREAM else "decode_mfma_launches"]
+            modes[name] = dict(ms_per_step=round(r["ms_per_step"], 4),
+                               gbps=round(r["gbps"], 1),
+                               kernel_ms=round(kern / max(1, nk), 4),
+                               kernel_gbps=round(r["kv_bytes_per_step"] / (kern / max(1, nk) * 1e-3) / 1e9, 1))
     store.close()
     del kb, vb, qs
     torch.cuda.empty_cache()
