@@ -93,11 +93,15 @@ def time_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
     store.profile_read()
     st0 = store.stats()
     plan = store.plan_info(seqs, mode)
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(steps)]
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for i in range(warmup, warmup + steps):
+    for j, i in enumerate(range(warmup, warmup + steps)):
+        ev[j][0].record()
         store.append_batch(seqs, kb[i], vb[i])
         store.decode(0, seqs, qs[i], out=out, mode=mode)
+        ev[j][1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     prof = store.profile_read()
@@ -108,7 +112,43 @@ def time_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
     logical = (st1["decode_kv_bytes_logical"] - st0["decode_kv_bytes_logical"]) / steps
     return dict(ms_per_step=ms, kv_bytes_per_step=kv_bytes, kv_bytes_logical_per_step=logical,
                 gbps=kv_bytes / (ms * 1e-3) / 1e9, tokens_per_s=n / (ms * 1e-3), prof=prof,
-                plan=plan)
+                plan=plan, step_ms=percentiles([a.elapsed_time(b) for a, b in ev]))
+
+
+def percentiles(xs):
+    """p10 / median / p90 of a list of step times (ms)."""
+    xs = sorted(xs)
+    pick = lambda f: xs[min(len(xs) - 1, int(round(f * (len(xs) - 1))))]
+    return dict(p10=round(pick(0.1), 4), median=round(pick(0.5), 4), p90=round(pick(0.9), 4))
+
+
+class Flusher:
+    """Writes a 1 GiB buffer (untimed) so that the next step starts with the
+    256 MB MALL and the L2 holding none of its data."""
+
+    def __init__(self, torch):
+        self.torch = torch
+        self.buf = torch.empty(1 << 30, dtype=torch.uint8, device="cuda")
+        self.n = 0
+
+    def __call__(self):
+        self.n += 1
+        self.buf.fill_(self.n & 255)
+
+
+def time_events(torch, fn, reps, flush=None):
+    """Per-call GPU time of fn() (HIP events on the current stream), optionally
+    with a cache flush before each call; returns percentiles in ms."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        if flush is not None:
+            flush()
+        a.record()
+        fn()
+        b.record()
+    torch.cuda.synchronize()
+    return percentiles([a.elapsed_time(b) for a, b in ev])
 
 
 def evict_leg(sq, torch, wl, reps=8):
@@ -139,16 +179,20 @@ def evict_leg(sq, torch, wl, reps=8):
     # decode on the compacted cache vs the full cache (batch 1)
     q = wl.device_normal_bf16((1, 32, 128), 77, "cuda")
     out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
-    res = {}
+    res, pct = {}, {}
+    flush = Flusher(torch)
     for name, seq in (("compacted", f), ("full", base)):
+        step = lambda: store.decode(0, [seq], q, out=out)
         for _ in range(3):
-            store.decode(0, [seq], q, out=out)
+            step()
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         for _ in range(32):
-            store.decode(0, [seq], q, out=out)
+            step()
         torch.cuda.synchronize()
         res[name] = (time.perf_counter() - t0) * 1e3 / 32
+        pct[name] = dict(warm=time_events(torch, step, 32), cold=time_events(torch, step, 16, flush))
+    del flush
     info = dict(
         workload=f"64K tokens, 40 tool + 40 reasoning spans, evict >= 65% (got "
                  f"{stats['tokens_removed'] / L:.3f})",
@@ -157,7 +201,8 @@ def evict_leg(sq, torch, wl, reps=8):
         evict_gbps=moved / (gather_ms * 1e-3) / 1e9,
         evict_gbps_wall=moved / (sorted(walls)[len(walls) // 2]) / 1e9,
         evict_wall_ms_median=sorted(walls)[len(walls) // 2] * 1e3,
-        decode_ms_compacted=res["compacted"], decode_ms_full=res["full"])
+        decode_ms_compacted=res["compacted"], decode_ms_full=res["full"],
+        decode_step_ms=pct)
     store.close()
     return info
 
@@ -185,11 +230,20 @@ def outlier_leg(sq, torch, wl):
     ms = (time.perf_counter() - t0) * 1e3 / w.steps
     st1 = store.stats()
     kv = (st1["decode_kv_bytes"] - st0["decode_kv_bytes"]) / w.steps
+    # the same steps' attention again, warm (back to back) and cold (MALL and
+    # L2 flushed before each): ~110 MB per step fits the 256 MB MALL
+    step = lambda: store.decode(0, [main, aux], qs[-1], out=out)
+    flush = Flusher(torch)
+    warm = time_events(torch, step, 32)
+    cold = time_events(torch, step, 16, flush)
+    del flush
     store.close()
     return dict(workload="32K tokens, 30 spans, 4 outlier channels x8, aux +512, evict >= 50% "
                          f"(got {stats['tokens_removed'] / w.main_len:.3f}), 64 steps [main, aux]",
                 ms_per_step=round(ms, 4), kv_bytes_per_step=kv,
-                gbps=round(kv / (ms * 1e-3) / 1e9, 1), tokens_per_s=round(2 / (ms * 1e-3), 1))
+                gbps=round(kv / (ms * 1e-3) / 1e9, 1), tokens_per_s=round(2 / (ms * 1e-3), 1),
+                attention_ms_warm=warm, attention_ms_cold=cold,
+                gbps_cold_median=round(kv / (cold["median"] * 1e-3) / 1e9, 1))
 
 
 def fullstack_leg(sq, torch):
@@ -222,27 +276,72 @@ def fullstack_leg(sq, torch):
     return res
 
 
-def cpu_leg(sample, wl, budget_s):
+def _bf16_bits_to_f64(bits):
     import numpy as np
+    return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+
+
+def _oracle_head(args):
+    """One KV head of the sample through the oracle (runs in a worker)."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
     from oracle import attention as oatt
+    q, kbits, vbits = args
+    with threadpool_limits(limits=1):
+        kf = _bf16_bits_to_f64(kbits)[:, None, :]
+        vf = _bf16_bits_to_f64(vbits)[:, None, :]
+        t0 = time.perf_counter()
+        oatt.attention(q, kf, vf, 1 / math.sqrt(128), 4)
+        return time.perf_counter() - t0
+
+
+def _cpu_model():
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_leg(sample, wl, budget_s):
+    """The float64 oracle on the host: KV heads of task 0's main thread, one
+    thread (BLAS pinned to 1), then one worker process per head in parallel."""
+    import concurrent.futures as cf
+    import multiprocessing as mp
+    import numpy as np
+    import torch
     k, v = sample
     ctx = k.shape[1]
     rng = np.random.default_rng([2602, 2, 7])
     q = wl.bf16_value(wl.normal_bf16(rng, (32, 128)))
-    done, t_total, heads = 0, 0.0, 0
-    for g in range(8):
-        kf = wl.torch_bf16_to_f64(k[0, :, g: g + 1])
-        vf = wl.torch_bf16_to_f64(v[0, :, g: g + 1])
-        t0 = time.perf_counter()
-        oatt.attention(q[4 * g: 4 * g + 4], kf, vf, 1 / math.sqrt(128), 4)
-        t_total += time.perf_counter() - t0
-        heads += 1
-        done += ctx * 512
-        if t_total >= budget_s:
+    bits = lambda t, g: t[0, :, g].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    heads = [(q[4 * g: 4 * g + 4], bits(k, g), bits(v, g)) for g in range(8)]
+    bytes_per_head = ctx * 512
+    t_one, n_one = 0.0, 0
+    for h in heads:
+        t_one += _oracle_head(h)
+        n_one += 1
+        if t_one >= budget_s:
             break
-    return dict(value=done / t_total / 1e9, unit="GB/s", cores=1, kind="oracle",
-                sample=f"main thread of task 0: {ctx} tokens x {heads} of 8 KV heads (4 query "
-                       f"heads each), float64 NumPy oracle, {t_total:.1f} s")
+    one = bytes_per_head * n_one / t_one / 1e9
+    avail = len(os.sched_getaffinity(0))
+    workers = max(1, min(len(heads), avail, 16))
+    with cf.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
+        list(ex.map(_oracle_head, [(h[0], h[1][:16], h[2][:16]) for h in heads[:workers]]))
+        t0 = time.perf_counter()
+        list(ex.map(_oracle_head, heads))
+        t_all = time.perf_counter() - t0
+    par = bytes_per_head * len(heads) / t_all / 1e9
+    return dict(value=par, unit="GB/s", cores=workers, kind="oracle",
+                sample=f"main thread of task 0: {ctx} tokens x 8 KV heads (4 query heads each), "
+                       f"float64 NumPy oracle, one worker process per KV head "
+                       f"({workers} processes, {t_all:.1f} s wall); single thread: {n_one} heads "
+                       f"in {t_one:.1f} s",
+                value_1_thread=one, cpu_model=_cpu_model(), affinity_cpus=avail,
+                blas_threads=1)
 
 
 def main():
@@ -259,7 +358,7 @@ def main():
     torch.cuda.set_device(0)
     total = args.warmup + args.steps
     n_modes = 5 if "modes" in legs else 0
-    extra = total * (1 + n_modes) + 16
+    extra = total * (2 + n_modes) + 16
     log(f"building {args.tasks} tasks at {args.ctx} tokens ...")
     from paper_2602_22603_amd import drivers
     store, seqs, inputs = drivers.build_shared128k(tasks=args.tasks, ctx=args.ctx,
@@ -274,6 +373,15 @@ def main():
     log("timing decode steps (AUTO) ...")
     main_res = time_steps(sq, torch, store, seqs, sq.ATTN_AUTO, args.steps, args.warmup,
                           kb, vb, qs, out)
+    flush = Flusher(torch)
+    ci = iter(range(total, 2 * total))
+
+    def cold_step():
+        i = next(ci)
+        store.append_batch(seqs, kb[i % total], vb[i % total])
+        store.decode(0, seqs, qs[i % total], out=out)
+    step_cold = time_events(torch, cold_step, min(args.steps, total), flush)
+    del flush
     prof, plan = main_res["prof"], main_res["plan"]
     if plan["n_items_mfma"]:
         kname, kms, kn, kbytes = ("k_decode_mfma", prof["decode_mfma_ms"],
@@ -361,6 +469,8 @@ def main():
                    "global_batch": B, "seq_len": args.ctx, "parallelism": "single GPU"},
         "frac_of_hbm_peak": round(main_res["gbps"] / HBM_PEAK_GBPS, 4),
         "tokens_per_s": round(main_res["tokens_per_s"], 1),
+        "step_ms_warm": main_res["step_ms"],
+        "step_ms_cold": step_cold,
         "kv_bytes_per_step": main_res["kv_bytes_per_step"],
         "kv_bytes_logical_per_step": main_res["kv_bytes_logical_per_step"],
         "roofline": roofline,
