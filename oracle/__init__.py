@@ -11,6 +11,9 @@ Modules
 attention
     Decode-phase attention of one query per head over a KV cache with grouped
     KV heads, its masked form, split partials and their merge.
+extend
+    Causal attention of a chunk of newly appended tokens over the cache
+    (the prefill of Algorithm 1's Phase 3 appends) with grouped KV heads.
 evict
     The keep-mask, exclusive prefix sum and inverse map that ``clear_kv``
     (Algorithm 1, Phase 1) reduces to, and the compaction of a logical view.
@@ -31,6 +34,6 @@ against closed forms, invariants, an independent library routine
 is "parity unpinned".
 """
 
-from . import attention, evict, pages  # noqa: F401
+from . import attention, evict, extend, pages  # noqa: F401
 
-__all__ = ["attention", "evict", "pages"]
+__all__ = ["attention", "evict", "extend", "pages"]

@@ -27,6 +27,7 @@ import torch
 
 from oracle import attention as att
 from oracle import evict as ev
+from oracle import extend as ex
 from oracle import pages as pg
 
 
@@ -479,6 +480,83 @@ def check_masked_equals_compacted(page_sizes=(1, 2, 4, 16), seed=14, n_tokens=40
                         assert np.array_equal(got, want)
 
 
+# --------------------------------------------------------------------------
+# extend (causal chunk) attention
+# --------------------------------------------------------------------------
+def check_extend_textbook(seed=15):
+    """Equal to torch's scaled_dot_product_attention in float64 with an
+    explicit boolean mask that lets new token j see keys 0 .. L - n + j."""
+    rng = np.random.default_rng(seed)
+    for hq, hkv, d, L, n, scale in [(4, 1, 64, 40, 40, 1 / 8), (4, 1, 64, 40, 1, 1 / 8),
+                                    (8, 2, 16, 57, 13, 0.3), (6, 3, 8, 20, 7, 1.1),
+                                    (32, 8, 128, 48, 16, 1 / math.sqrt(128))]:
+        g = hq // hkv
+        q = rng.standard_normal((n, hq, d))
+        k = rng.standard_normal((L, hkv, d))
+        v = rng.standard_normal((L, hkv, d))
+        out = ex.extend_attention(q, k, v, scale, g)
+        allowed = torch.arange(L)[None, :] <= (L - n + torch.arange(n))[:, None]
+        kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        qt = torch.from_numpy(q).permute(1, 0, 2).contiguous()
+        ref = torch.nn.functional.scaled_dot_product_attention(
+            qt, kt, vt, attn_mask=allowed, scale=scale).permute(1, 0, 2).numpy()
+        assert np.max(np.abs(out - ref)) <= 1e-12, np.max(np.abs(out - ref))
+
+
+def check_extend_first_token_alone(seed=16):
+    """With no prefix (n = L) the first new token sees only itself: its
+    output is its own V row, exactly."""
+    rng = np.random.default_rng(seed)
+    q = rng.standard_normal((9, 8, 16))
+    k = rng.standard_normal((9, 2, 16))
+    v = rng.standard_normal((9, 2, 16))
+    out = ex.extend_attention(q, k, v, 0.25, 4)
+    for h in range(8):
+        assert np.array_equal(out[0, h], v[0, h // 4])
+
+
+def check_extend_causal(seed=17):
+    """Changing a key after new token j's own index leaves row j unchanged
+    (bit for bit); changing its own key changes it."""
+    rng = np.random.default_rng(seed)
+    L, n = 30, 10
+    q = rng.standard_normal((n, 4, 8))
+    k = rng.standard_normal((L, 2, 8))
+    v = rng.standard_normal((L, 2, 8))
+    base = ex.extend_attention(q, k, v, 0.5, 2)
+    for t in (L - n, L - n + 4, L - 1):
+        k2, v2 = k.copy(), v.copy()
+        k2[t] += 1.0
+        v2[t] -= 2.0
+        out = ex.extend_attention(q, k2, v2, 0.5, 2)
+        for j in range(n):
+            if L - n + j < t:
+                assert np.array_equal(out[j], base[j])
+            else:
+                assert not np.array_equal(out[j], base[j])
+
+
+def check_extend_compacted_equals_masked(seed=18):
+    """A chunk appended after an eviction: extend attention over the
+    compacted cache equals masked extend attention over the full cache, bit
+    for bit, for every subset of 4 spans of the prefix."""
+    rng = np.random.default_rng(seed)
+    prefix, n, hq, hkv, d = 36, 6, 4, 2, 8
+    cuts = sorted(rng.choice(np.arange(prefix + 1), 8, replace=False).tolist())
+    spans = [(cuts[i], cuts[i + 1]) for i in range(0, 8, 2)]
+    k = rng.standard_normal((prefix + n, hkv, d))
+    v = rng.standard_normal((prefix + n, hkv, d))
+    q = rng.standard_normal((n, hq, d))
+    for r in range(len(spans) + 1):
+        for subset in itertools.combinations(spans, r):
+            keep = np.concatenate([ev.keep_mask(prefix, list(subset)),
+                                   np.ones(n, np.uint8)]).astype(bool)
+            got = ex.extend_attention(q, k[keep], v[keep], 0.35, hq // hkv)
+            want = ex.extend_attention(q, k, v, 0.35, hq // hkv, mask=keep)
+            assert np.array_equal(got, want)
+
+
 ALL_CHECKS = [
     check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
     check_uniform_closed_form, check_two_key_closed_form,
@@ -487,5 +565,6 @@ ALL_CHECKS = [
     check_hand_worked_page_tables, check_fork_is_zero_copy_and_release_restores,
     check_all_keep_eviction_is_identity, check_positions_carried,
     check_evict_parent_leaves_child, check_errors_leave_state_unchanged,
-    check_masked_equals_compacted,
+    check_masked_equals_compacted, check_extend_textbook, check_extend_first_token_alone,
+    check_extend_causal, check_extend_compacted_equals_masked,
 ]

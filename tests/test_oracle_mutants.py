@@ -12,6 +12,7 @@ import pytest
 
 from oracle import attention as att
 from oracle import evict as ev
+from oracle import extend as ex
 from oracle import pages as pg
 from tests import oracle_pins as pins
 
@@ -129,6 +130,33 @@ def _evict_keeps_old_refs(self, h, cursor_ids):
     return stats
 
 
+def _extend_excludes_self(q, k, v, scale, group, mask=None):
+    q = np.asarray(q, np.float64)
+    n, L = q.shape[0], np.asarray(k).shape[0]
+    out = np.zeros(q.shape)
+    for j in range(n):
+        last = L - n + j
+        out[j] = att.attention(q[j], k[:last], v[:last], scale, group,
+                               None if mask is None else mask[:last])
+    return out
+
+
+def _extend_no_prefix_offset(q, k, v, scale, group, mask=None):
+    q = np.asarray(q, np.float64)
+    out = np.zeros(q.shape)
+    for j in range(q.shape[0]):
+        out[j] = att.attention(q[j], k[: j + 1], v[: j + 1], scale, group,
+                               None if mask is None else mask[: j + 1])
+    return out
+
+
+def _extend_ignores_mask(q, k, v, scale, group, mask=None):
+    return _orig_extend(q, k, v, scale, group)
+
+
+_orig_extend = ex.extend_attention
+
+
 MUTANTS = {
     "gqa_head_modulo": (att, "scores", _scores_gqa_modulo),
     "missing_scale": (att, "scores", _scores_no_scale),
@@ -144,6 +172,9 @@ MUTANTS = {
     "fork_next_pos_from_parent": (pg.PageModel, "fork", _fork_next_pos_parent),
     "evict_recomputes_positions": (pg.PageModel, "evict", _evict_recompute_pos),
     "evict_leaks_old_pages": (pg.PageModel, "evict", _evict_keeps_old_refs),
+    "extend_excludes_own_key": (ex, "extend_attention", _extend_excludes_self),
+    "extend_drops_prefix_offset": (ex, "extend_attention", _extend_no_prefix_offset),
+    "extend_ignores_mask": (ex, "extend_attention", _extend_ignores_mask),
 }
 
 
