@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 1
+#define SQ_ABI_VERSION 2
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -135,6 +135,8 @@ typedef struct {
   int64_t decode_calls;
   int64_t decode_kv_bytes;    /* K/V bytes decode must read, shared prefixes once */
   int64_t decode_kv_bytes_logical; /* same with every query's own tokens counted */
+  int64_t extend_calls, extend_tokens; /* sq_extend_attn calls; query tokens they served */
+  int64_t extend_kv_bytes;    /* K/V bytes of the keys those calls attended, each key once */
 } sq_stats;
 
 typedef struct {
@@ -159,6 +161,8 @@ typedef struct {
   double evict_scan_ms, evict_gather_ms, append_ms;
   int64_t decode_valu_launches, decode_mfma_launches, decode_merge_launches;
   int64_t evict_scan_launches, evict_gather_launches, append_launches;
+  double extend_ms;
+  int64_t extend_launches;
 } sq_profile;
 
 /* ---- store -------------------------------------------------------------
@@ -256,6 +260,26 @@ sq_status sq_evict_spans(sq_store *store, sq_seq seq, const int32_t *cursor_ids,
  * metadata-only store. */
 sq_status sq_decode_attn(sq_store *store, int32_t layer, const sq_seq *seqs, int32_t batch,
                          const void *q, float *out, float scale, int32_t mode, void *stream);
+
+/* Causal attention of a chunk that was just appended: Algorithm 1 grows the
+ * context by whole chunks (Phase 3: C <- C + R, then C <- C + O), and every
+ * token of such a chunk attends to the cached prefix (compacted by Phase 1's
+ * evictions) and to the chunk's earlier tokens before decoding resumes.
+ *
+ * The chunk is the last n_new of seq's L tokens (append it with sq_append
+ * first).  For new token j (0 <= j < n_new) and query head h:
+ *   out[j][h] = sum_t softmax_t(scale * q[j][h] . k[t][h / G]) v[t][h / G]
+ * over the keys at logical indices t = 0 .. L - n_new + j, G = Hq / Hkv.
+ * Causality is by logical index: positions carried through evictions are
+ * increasing in that order, so the two agree.
+ *   q    device bf16 [n_new][Hq][D], 16-byte aligned (caller-owned)
+ *   out  device fp32 [n_new][Hq][D], 16-byte aligned (caller-owned)
+ * Work is enqueued on stream.  n_new = 0 does nothing.
+ * SQ_ERR_UNKNOWN_SEQ: seq is not live.  SQ_ERR_INVALID: n_new outside
+ * [0, L], bad layer, null or misaligned q / out, non-finite scale,
+ * metadata-only store. */
+sq_status sq_extend_attn(sq_store *store, int32_t layer, sq_seq seq, int32_t n_new,
+                         const void *q, float *out, float scale, void *stream);
 
 /* Host-only description of the work sq_decode_attn would do for this batch. */
 sq_status sq_decode_plan_info(sq_store *store, const sq_seq *seqs, int32_t batch,

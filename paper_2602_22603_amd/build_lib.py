@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG_DIR)
 CSRC = os.path.join(PKG_DIR, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 LIB_PATH = os.path.join(PKG_DIR, "libsq.so")
-SOURCES = ["store.cpp", "kv_kernels.hip", "decode_kernels.hip"]
+SOURCES = ["store.cpp", "kv_kernels.hip", "decode_kernels.hip", "extend_kernels.hip"]
 ARCH = "gfx950"
 
 # Packed fp32 VALU instructions are kept out of every HIP object.

@@ -158,6 +158,30 @@ struct MergeArgs {
   int32_t src_member[kMaxBatch][2];
 };
 
+// ---- extend (causal attention of an appended chunk) ------------------------
+// The chunk is the last n of the sequence's L tokens; new token j attends to
+// logical keys 0 .. L - n + j.  A workgroup takes 128 query rows (128 / G
+// tokens x the G query heads of one KV head) against the whole key range.
+constexpr int kExtRows = 128;
+constexpr int kExtKeys = 64; // keys per LDS block (4 pages)
+
+struct ExtendArgs {
+  const uint16_t *q;  // bf16 [n][Hq][D]
+  const uint16_t *k;  // K pool of the layer
+  const uint16_t *v;  // V pool of the layer
+  const int32_t *pt;  // device page-table row of the sequence
+  float *out;         // fp32 [n][Hq][D]
+  int64_t page_stride;
+  int64_t head_stride;
+  int32_t n_pages;    // pages in the sequence's list
+  int32_t L;          // tokens in the sequence (the chunk included)
+  int32_t n;          // new tokens
+  int32_t hq;
+  int32_t hkv;
+  int32_t n_qblocks;  // ceil(n / (kExtRows / G))
+  float scale_log2;
+};
+
 // Kernel arguments are passed by value; keep each well under 4 KiB.
 static_assert(sizeof(AppendArgs) < 4096, "append kernel arguments too large");
 static_assert(sizeof(AppendBatchArgs) < 4096, "append-batch kernel arguments too large");
@@ -180,6 +204,7 @@ hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t 
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s);
+hipError_t launch_extend(int d, int group, const ExtendArgs &a, hipStream_t s);
 // Workgroups of a decode kernel (kind 0: VALU, 1: MFMA) that fit on one CU.
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out);
 

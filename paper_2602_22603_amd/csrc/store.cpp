@@ -114,7 +114,8 @@ struct Seq {
   int32_t parent = -1;
 };
 
-enum ProfKind { kProfValu, kProfMfma, kProfMerge, kProfScan, kProfGather, kProfAppend, kProfKinds };
+enum ProfKind { kProfValu, kProfMfma, kProfMerge, kProfScan, kProfGather, kProfAppend, kProfExtend,
+                kProfKinds };
 
 struct ProfPair {
   hipEvent_t a, b;
@@ -1107,6 +1108,48 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   return SQ_OK;
 }
 
+sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, const void *q,
+                         float *out, float scale, void *stream) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
+  if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
+  Seq *sqn = s->get(seq);
+  if (!sqn) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seq);
+  if (n_new < 0 || n_new > sqn->length)
+    return fail(SQ_ERR_INVALID, "n_new %d outside [0, %lld]", n_new, (long long)sqn->length);
+  if (n_new == 0) return SQ_OK;
+  if (!q || !out || !aligned16(q) || !aligned16(out))
+    return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  sq::ExtendArgs a{};
+  a.q = static_cast<const uint16_t *>(q);
+  a.k = s->pools.k + layer * s->pools.layer_stride;
+  a.v = s->pools.v + layer * s->pools.layer_stride;
+  a.pt = s->pt_row(seq);
+  a.out = out;
+  a.page_stride = s->pools.page_stride;
+  a.head_stride = s->pools.head_stride;
+  a.n_pages = (int32_t)sqn->pages.size();
+  a.L = (int32_t)sqn->length;
+  a.n = n_new;
+  a.hq = s->cfg.num_q_heads;
+  a.hkv = s->cfg.num_kv_heads;
+  const int tq = sq::kExtRows / s->G;
+  a.n_qblocks = (n_new + tq - 1) / tq;
+  a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  ProfPair pp;
+  const bool on = s->prof_begin(strm, &pp, kProfExtend);
+  hipError_t e = sq::launch_extend(s->D, s->G, a, strm);
+  s->prof_end(strm, &pp, on);
+  if (e != hipSuccess) return hip_fail(e, "extend kernel");
+  ++s->st.extend_calls;
+  s->st.extend_tokens += n_new;
+  s->st.extend_kv_bytes += sqn->length * (int64_t)s->cfg.num_kv_heads * s->D * 2 * 2;
+  return SQ_OK;
+}
+
 sq_status sq_seq_info(sq_store *s, sq_seq h, sq_seq_desc *out) {
   if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
   Seq *q = s->get(h);
@@ -1225,6 +1268,8 @@ sq_status sq_profile_read(sq_store *s, sq_profile *out) {
   out->evict_scan_launches = s->prof_n[kProfScan];
   out->evict_gather_launches = s->prof_n[kProfGather];
   out->append_launches = s->prof_n[kProfAppend];
+  out->extend_ms = s->prof_ms[kProfExtend];
+  out->extend_launches = s->prof_n[kProfExtend];
   for (int k = 0; k < kProfKinds; ++k) {
     s->prof_ms[k] = 0;
     s->prof_n[k] = 0;

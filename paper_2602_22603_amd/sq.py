@@ -59,7 +59,7 @@ class Stats(C.Structure):
         "live_pages", "peak_pages", "free_pages", "live_seqs", "append_tokens",
         "fork_calls", "fork_tail_copies", "evict_calls", "evict_tokens_removed",
         "evict_tokens_moved", "evict_bytes_moved", "decode_calls", "decode_kv_bytes",
-        "decode_kv_bytes_logical")]
+        "decode_kv_bytes_logical", "extend_calls", "extend_tokens", "extend_kv_bytes")]
 
 
 class PlanInfo(C.Structure):
@@ -76,7 +76,8 @@ class Profile(C.Structure):
                                             "evict_scan_ms", "evict_gather_ms", "append_ms")] +
                 [(n, C.c_int64) for n in ("decode_valu_launches", "decode_mfma_launches",
                                            "decode_merge_launches", "evict_scan_launches",
-                                           "evict_gather_launches", "append_launches")])
+                                           "evict_gather_launches", "append_launches")] +
+                [("extend_ms", C.c_double), ("extend_launches", C.c_int64)])
 
 
 _LIB = None
@@ -100,6 +101,8 @@ _SIGS = {
                                  C.c_void_p, C.POINTER(EvictStats)]),
     "sq_decode_attn": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
                                  C.c_void_p, C.c_void_p, C.c_float, C.c_int32, C.c_void_p]),
+    "sq_extend_attn": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
+                                 C.c_void_p, C.c_float, C.c_void_p]),
     "sq_decode_plan_info": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
                                       C.POINTER(PlanInfo)]),
     "sq_seq_info": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(SeqDesc)]),
@@ -269,6 +272,18 @@ class Store:
             scale = 1.0 / float(self.head_dim) ** 0.5
         _check(lib().sq_decode_attn(self._handle, layer, _i32_array(seqs), len(seqs), _ptr(q),
                                     _ptr(out), float(scale), mode, _stream(stream)))
+        return out
+
+    def extend(self, layer, seq, q, out=None, scale=None, stream=None):
+        """Causal attention of the last n = q.shape[0] tokens of seq (just
+        appended) over the cache: q bf16 [n, Hq, D] -> out fp32 [n, Hq, D]."""
+        import torch
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        if scale is None:
+            scale = 1.0 / float(self.head_dim) ** 0.5
+        _check(lib().sq_extend_attn(self._handle, layer, seq, int(q.shape[0]), _ptr(q), _ptr(out),
+                                    float(scale), _stream(stream)))
         return out
 
     def plan_info(self, seqs, mode=ATTN_AUTO):

@@ -40,7 +40,8 @@ def test_library_exports_every_declared_symbol(sq):
     for name in sorted(declared):
         assert hasattr(lib, name), name
     assert declared == set(sq.EXPORTED)
-    assert lib.sq_abi_version() == 1
+    version = int(re.search(r"#define SQ_ABI_VERSION (\d+)", header).group(1))
+    assert lib.sq_abi_version() == version
 
 
 def _store(sq, num_pages, page, max_seqs, max_pages):
@@ -198,6 +199,22 @@ def test_error_paths_leave_state_unchanged(sq):
     with pytest.raises(pg.NoPages):
         m.evict(a, [9])
     assert before == (s.page_table(a), s.refcounts().tolist(), s.spans(a))
+
+
+def test_attention_needs_a_device_store(sq):
+    """Attention calls on a metadata-only store fail cleanly and change nothing."""
+    import ctypes as C
+    s = _store(sq, 8, 4, 2, 8)
+    a = s.seq_create()
+    s.append(a, n=6)
+    before = (s.page_table(a), s.stats())
+    rc = sq.lib().sq_extend_attn(s._handle, 0, a, 2, None, None, C.c_float(0.5), None)
+    assert rc == sq.ERR_INVALID
+    assert b"metadata-only" in sq.lib().sq_last_error()
+    seqs = (C.c_int32 * 1)(a)
+    rc = sq.lib().sq_decode_attn(s._handle, 0, seqs, 1, None, None, C.c_float(0.5), 0, None)
+    assert rc == sq.ERR_INVALID
+    assert before == (s.page_table(a), s.stats())
 
 
 def test_invalid_configurations(sq):
