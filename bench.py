@@ -47,8 +47,8 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--tasks", type=int, default=8)
     ap.add_argument("--ctx", type=int, default=131072)
-    ap.add_argument("--legs", default="decode,modes,evict,outlier,fullstack,cpu",
-                    help="comma list of: decode, modes, evict, outlier, fullstack, cpu, copy "
+    ap.add_argument("--legs", default="decode,modes,evict,extend,outlier,fullstack,cpu",
+                    help="comma list of: decode, modes, evict, extend, outlier, fullstack, cpu, copy "
                          "(a plain 1 GiB device copy used to calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
@@ -246,6 +246,54 @@ def outlier_leg(sq, torch, wl):
                 gbps_cold_median=round(kv / (cold["median"] * 1e-3) / 1e9, 1))
 
 
+BF16_PEAK_TFLOPS = 2500.0
+
+
+def extend_leg(sq, torch, wl, reps=10):
+    """An 8192-token chunk (a turn's tool output) appended to the 64K context
+    after its tool spans were evicted, and to the same context uncompacted:
+    causal extend attention over the cache (1 layer, 32q/8kv heads, 128)."""
+    from paper_2602_22603_amd import drivers
+    n = 8192
+    store, base, w, k, v = drivers.build_compaction64k(extra_tokens=n + 64)
+    del k, v
+    full = store.fork(base, w.length)       # keeps the uncompacted view
+    store.evict(base, w.evict_ids)
+    kn = wl.device_normal_bf16((1, n, 8, 128), 91, "cuda")
+    vn = wl.device_normal_bf16((1, n, 8, 128), 92, "cuda")
+    store.append(base, kn, vn)
+    store.append(full, kn, vn)
+    del kn, vn
+    q = wl.device_normal_bf16((n, 32, 128), 93, "cuda")
+    out = torch.empty((n, 32, 128), dtype=torch.float32, device="cuda")
+    res = {}
+    for name, seq in (("compacted", base), ("full", full)):
+        L = store.seq_info(seq)["length"]
+        step = lambda: store.extend(0, seq, q, out=out)
+        for _ in range(2):
+            step()
+        store.profile_enable(True)
+        store.profile_read()
+        pct = time_events(torch, step, reps)
+        prof = store.profile_read()
+        store.profile_enable(False)
+        kern_ms = prof["extend_ms"] / max(1, prof["extend_launches"])
+        # useful flops: q.k and p.v for every (query head, visible key) pair
+        pairs = n * (L - n) + n * (n + 1) // 2
+        flops = 32 * 4 * 128 * pairs
+        tflops = flops / (kern_ms * 1e-3) / 1e12
+        res[name] = dict(prefix_tokens=L - n, chunk_tokens=n, call_ms=pct,
+                         kernel_ms=round(kern_ms, 4), useful_tflops=round(tflops, 1),
+                         frac_of_bf16_peak=round(tflops / BF16_PEAK_TFLOPS, 4),
+                         tokens_per_s=round(n / (kern_ms * 1e-3), 1))
+    res["workload"] = ("8192-token chunk after the 64K context's tool spans were evicted "
+                       f"(>= 65%), vs the uncompacted 64K context; 1 layer, 32q/8kv, 128; "
+                       f"peak {BF16_PEAK_TFLOPS:.0f} TFLOP/s dense bf16")
+    res["compute_saved"] = round(1 - res["compacted"]["kernel_ms"] / res["full"]["kernel_ms"], 4)
+    store.close()
+    return res
+
+
 def fullstack_leg(sq, torch):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
     turns; with and without eviction: peak KV bytes and the decode step
@@ -437,6 +485,11 @@ def main():
             dst.copy_(src)
         torch.cuda.synchronize()
         del src, dst
+    extend = None
+    if "extend" in legs:
+        log("extend leg (8192-token chunk over the 64K context) ...")
+        extend = extend_leg(sq, torch, wl)
+        torch.cuda.empty_cache()
     outlier = None
     if "outlier" in legs:
         log("32K outlier leg ...")
@@ -476,6 +529,7 @@ def main():
         "roofline": roofline,
         "modes": modes,
         "evict": evict,
+        "extend": extend,
         "outlier32k": outlier,
         "full_stack": fullstack,
         "cpu_baseline": cpu,

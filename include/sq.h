@@ -276,8 +276,8 @@ sq_status sq_decode_attn(sq_store *store, int32_t layer, const sq_seq *seqs, int
  *   out  device fp32 [n_new][Hq][D], 16-byte aligned (caller-owned)
  * Work is enqueued on stream.  n_new = 0 does nothing.
  * SQ_ERR_UNKNOWN_SEQ: seq is not live.  SQ_ERR_INVALID: n_new outside
- * [0, L], bad layer, null or misaligned q / out, non-finite scale,
- * metadata-only store. */
+ * [0, L], bad layer, null or misaligned q / out, scale not finite and
+ * positive, metadata-only store. */
 sq_status sq_extend_attn(sq_store *store, int32_t layer, sq_seq seq, int32_t n_new,
                          const void *q, float *out, float scale, void *stream);
 

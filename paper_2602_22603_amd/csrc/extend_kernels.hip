@@ -11,18 +11,24 @@
 //   workgroup = 4 waves, 128 query rows = (128 / G tokens) x (G query heads
 //               of one KV head); each wave owns 32 rows as two MFMA column
 //               groups of 16.
-//   K/V       = blocks of 64 keys (4 pages) staged in LDS, the next block's
-//               global loads in flight while the current one is computed.
+//   K/V       = blocks of 64 keys (4 pages), copied global -> LDS by the
+//               gfx950 direct-to-LDS loads (global_load_lds_dwordx4) into a
+//               double buffer: block b + 1 is in flight while block b is
+//               computed, and no registers hold staging data.  16-byte
+//               chunks are XOR-swizzled within their row so that the MFMA
+//               operand reads below are free of bank conflicts.
 //   S^T       = K . Q^T      v_mfma_f32_16x16x32_bf16 (A = K rows from LDS,
 //                            B = Q^T held in registers for the whole pass)
-//   O^T      += V^T . P^T    v_mfma_f32_16x16x32_bf16 over 32 keys at once:
-//               the k slots of lane group kg are keys 4kg..4kg+3 of two
-//               consecutive 16-key tiles, which are exactly the S^T values
-//               that lane already holds, so P never moves between lanes;
-//               V^T is written to LDS in that slot order.  P is split into
-//               bf16 hi + lo halves (two MFMAs) so the weights keep ~16 bits.
+//   O^T      += V^T . P^T    v_mfma_f32_16x16x32_bf16 over 32 keys at once.
+//               The A rows of the S^T tiles are chosen so that lane group kg
+//               ends up holding the scores of keys 8kg .. 8kg+7 of each 32-key
+//               chunk: exactly the k slots of its P^T operand and, in the
+//               page-transposed V pool, one contiguous 16-byte piece of V^T.
+//               P never moves between lanes.  P is split into bf16 hi + lo
+//               halves (two MFMAs) so the weights keep ~16 bits.
 //   softmax   online, per query row, in log2 units (one v_exp_f32 per score);
-//               row max across the four lane groups by permlane swaps.
+//               row max across the four lane groups by permlane swaps; the
+//               reference max is raised lazily (see kLazy).
 //
 // Work order: workgroup w takes KV head w % Hkv (consecutive workgroups land
 // on different XCDs, so each XCD's L2 serves one head's K/V) and query block
@@ -37,6 +43,11 @@ namespace {
 constexpr int BK = kExtKeys;
 constexpr int kThreads = 256;
 constexpr float kNegInf = -__builtin_huge_valf();
+// Two waves per SIMD: two workgroups per CU share the matrix cores, so one
+// workgroup's softmax and barriers overlap the other's MFMAs.
+#ifndef EXT_WAVES_PER_EU
+#define EXT_WAVES_PER_EU 2
+#endif
 
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
@@ -71,77 +82,190 @@ __device__ inline uint32_t pack_bf16(float lo, float hi) {
 }
 
 template <int D> struct ExtLayout {
-  static constexpr int KP = D + 8;  // bf16 per LDS K row (16-byte pad: conflict-free A reads)
-  static constexpr int VP = BK + 8; // bf16 per LDS V^T row
-  static constexpr int NU = D / 32; // 16-byte K (and V) loads per thread per block
-  static constexpr int E = 2 * D;   // 16-byte pieces per page and head
+  static constexpr int CH = D / 8;             // 16-byte chunks per K row
+  static constexpr int KROWS = 1024 / (2 * D); // K rows one wave-wide DMA writes
+  static constexpr int K_ELEMS = BK * D;       // bf16 per K buffer
+  static constexpr int V_ELEMS = D * BK;       // bf16 per V^T buffer
+  static constexpr int NK = K_ELEMS * 2 / 1024 / 4; // K DMAs per wave per block
+  static constexpr int NV = V_ELEMS * 2 / 1024 / 4; // V DMAs per wave per block
 };
 
-// Global -> registers: the K and V pieces of block blk this thread stages.
-// Pages past the sequence's list read as zeros.
+// Swizzles: the physical 16-byte chunk of logical chunk c in a row.
+template <int D> __device__ inline int k_phys(int row, int c) {
+  return (c ^ (4 * (row & 3) + ((row >> 3) & 3))) & (D / 8 - 1);
+}
+__device__ inline int v_phys(int d, int j) { return j ^ ((d >> 1) & 7); }
+
+// The block key held by A row r of S^T tile t (0..3): tiles 2c and 2c + 1
+// cover the 32-key chunk c, row 4 kg + i of tile 2c + h being key
+// 32 c + 8 kg + 4 h + i.
+__device__ inline int tile_key(int t, int r) {
+  return 32 * (t >> 1) + 8 * (r >> 2) + 4 * (t & 1) + (r & 3);
+}
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Global -> LDS (direct) for block blk: this wave's share of the K rows and
+// V^T rows.  Pages past the sequence's list are skipped (their keys are
+// masked and their V zeroed before use).
 template <int D>
-__device__ inline void ext_load(uint4 (&kr)[ExtLayout<D>::NU], uint4 (&vr)[ExtLayout<D>::NU],
-                                const ExtendArgs &a, const uint16_t *kbase,
-                                const uint16_t *vbase, int blk, int tid) {
+__device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
+                               const uint16_t *kbase, const uint16_t *vbase, int blk, int wave,
+                               int lane) {
   using Lt = ExtLayout<D>;
 #pragma unroll
-  for (int u = 0; u < Lt::NU; ++u) {
-    const int c = u * kThreads + tid;
-    const int p = c / Lt::E, w = c % Lt::E;
-    const int pg = blk * (BK / kPage) + p;
-    if (pg < a.n_pages) {
-      const int64_t off = (int64_t)a.pt[pg] * a.page_stride + 8 * w;
-      kr[u] = *reinterpret_cast<const uint4 *>(kbase + off);
-      vr[u] = *reinterpret_cast<const uint4 *>(vbase + off);
-    } else {
-      kr[u] = make_uint4(0, 0, 0, 0);
-      vr[u] = make_uint4(0, 0, 0, 0);
-    }
+  for (int u = 0; u < Lt::NK; ++u) {
+    const int ins = wave * Lt::NK + u;
+    const int row = ins * Lt::KROWS + lane / Lt::CH;
+    const int c = k_phys<D>(row, lane % Lt::CH); // the swizzle is an involution
+    const int pg = blk * (BK / kPage) + row / kPage;
+    const int32_t id = pg < a.n_pages ? a.pt[pg] : -1;
+    if (id >= 0)
+      __builtin_amdgcn_global_load_lds(
+          kbase + (int64_t)id * a.page_stride + (row % kPage) * D + 8 * c,
+          (lds_void *)(sk + ins * 512), 16, 0, 0);
+  }
+#pragma unroll
+  for (int u = 0; u < Lt::NV; ++u) {
+    const int ins = wave * Lt::NV + u;
+    const int d = ins * 8 + lane / 8;
+    const int j = v_phys(d, lane % 8);
+    const int pg = blk * (BK / kPage) + j / 2;
+    const int32_t id = pg < a.n_pages ? a.pt[pg] : -1;
+    if (id >= 0)
+      __builtin_amdgcn_global_load_lds(
+          vbase + (int64_t)id * a.page_stride + d * kPage + 8 * (j & 1),
+          (lds_void *)(sv + ins * 512), 16, 0, 0);
   }
 }
 
-// Registers -> LDS.  K rows keep token order; V^T rows take the PV slot
-// order (block key t = 32c + 16h + 4r + i  ->  slot 32c + 8r + 4h + i), and
-// keys at or past L are zeroed so that 0 * v stays 0.
+// Zero V^T entries of keys at or past L in the block's buffer (the last
+// block only), so that 0 * v stays 0 whatever the pool holds there.
 template <int D>
-__device__ inline void ext_store(const uint4 (&kr)[ExtLayout<D>::NU], const uint4 (&vr)[ExtLayout<D>::NU],
-                                 uint16_t *sk, uint16_t *sv, int blk, int tid, int L) {
-  using Lt = ExtLayout<D>;
+__device__ inline void ext_zero_tail(uint16_t *sv, int blk, int L, int tid) {
+  for (int q = tid; q < D * 8; q += kThreads) {
+    const int d = q >> 3, j = q & 7;
+    const int k0 = blk * BK + 8 * j;
+    if (k0 + 8 <= L) continue;
+    uint4 *p = reinterpret_cast<uint4 *>(sv + d * BK + 8 * v_phys(d, j));
+    uint4 x = *p;
+    uint32_t m[4];
 #pragma unroll
-  for (int u = 0; u < Lt::NU; ++u) {
-    const int c = u * kThreads + tid;
-    const int p = c / Lt::E, w = c % Lt::E;
-    const int tok = kPage * p + w / (D / 8);
-    const int col = (w % (D / 8)) * 8;
-    *reinterpret_cast<uint4 *>(sk + tok * Lt::KP + col) = kr[u];
-    // V page is [D][16]: piece w holds channel w / 2, keys 8 (w % 2) .. +8
-    const int d = w >> 1, h8 = w & 1;
-    const int t0 = blk * BK + kPage * p + 8 * h8;
-    uint4 x = vr[u];
-    if (t0 + 8 > L) {
-      uint32_t m[4];
+    for (int e = 0; e < 4; ++e)
+      m[e] = (k0 + 2 * e < L ? 0xffffu : 0u) | (k0 + 2 * e + 1 < L ? 0xffff0000u : 0u);
+    x.x &= m[0];
+    x.y &= m[1];
+    x.z &= m[2];
+    x.w &= m[3];
+    *p = x;
+  }
+}
+
+// Softmax state of one lane: two query columns (rows of the attention).  m
+// is the reference maximum in log2 units; it is only raised when a block's
+// maximum exceeds it by more than kLazy, so the O^T rescale is rare and the
+// weights stay below 2^kLazy (exact for the final out = acc / l either way).
+constexpr float kLazy = 8.f;
+
+// One 64-key block against this wave's 32 query columns.  need_mask: the
+// block reaches past some column's last visible key (the chunk's diagonal,
+// or the cache's end); only then is the per-key test made.
+template <int D>
+__device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, int n, int kg,
+                                 float c, bool need_mask, const bf16x8_t (&qf)[2][D / 32],
+                                 const int (&lim)[2], f32x4_t (&acc)[D / 16][2], float (&m_run)[2],
+                                 float (&l_run)[2]) {
+  constexpr int NKC = D / 32;
+  constexpr int NDT = D / 16;
+  f32x4_t st[4][2];
 #pragma unroll
-      for (int e = 0; e < 4; ++e)
-        m[e] = (t0 + 2 * e < L ? 0xffffu : 0u) | (t0 + 2 * e + 1 < L ? 0xffff0000u : 0u);
-      x.x &= m[0];
-      x.y &= m[1];
-      x.z &= m[2];
-      x.w &= m[3];
+  for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+    for (int cg = 0; cg < 2; ++cg) st[tt][cg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+    for (int kc = 0; kc < NKC; ++kc) {
+      const int row = tile_key(tt, n);
+      const bf16x8_t ka = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const uint4 *>(sk + row * D + 8 * k_phys<D>(row, 4 * kc + kg)));
+#pragma unroll
+      for (int cg = 0; cg < 2; ++cg)
+        st[tt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[cg][kc], st[tt][cg], 0, 0, 0);
     }
-    const int s0 = 32 * (p >> 1) + 16 * h8 + 4 * (p & 1);
-    *reinterpret_cast<uint2 *>(sv + d * Lt::VP + s0) = make_uint2(x.x, x.y);
-    *reinterpret_cast<uint2 *>(sv + d * Lt::VP + s0 + 8) = make_uint2(x.z, x.w);
+  if (need_mask) {
+#pragma unroll
+    for (int cg = 0; cg < 2; ++cg)
+#pragma unroll
+      for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+          if (b * BK + tile_key(tt, 4 * kg + i) > lim[cg]) st[tt][cg][i] = kNegInf;
+  }
+  float alpha[2], nm[2];
+#pragma unroll
+  for (int cg = 0; cg < 2; ++cg) {
+    float mx = kNegInf;
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
+      mx = fmaxf(mx, fmaxf(fmaxf(st[tt][cg][0], st[tt][cg][1]), fmaxf(st[tt][cg][2], st[tt][cg][3])));
+    mx = max_xrow16(mx);
+    mx = max_xrow32(mx) * c; // scale > 0: the max commutes with it
+    const float m_new = mx > m_run[cg] + kLazy ? mx : m_run[cg];
+    alpha[cg] = m_new == m_run[cg] ? 1.f : exp2_fast(m_run[cg] - m_new);
+    m_run[cg] = m_new;
+    nm[cg] = m_new == kNegInf ? 0.f : -m_new;
+    l_run[cg] *= alpha[cg];
+  }
+  if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int cg = 0; cg < 2; ++cg) acc[dt][cg] *= alpha[cg];
+  }
+#pragma unroll
+  for (int c2 = 0; c2 < 2; ++c2) {
+    bf16x8_t phi[2], plo[2];
+#pragma unroll
+    for (int cg = 0; cg < 2; ++cg) {
+      uint32_t h[4], l[4];
+      float psum = 0.f;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int tt = 2 * c2 + (e >> 1);
+        const float p0 = exp2_fast(fmaf(st[tt][cg][2 * (e & 1)], c, nm[cg]));
+        const float p1 = exp2_fast(fmaf(st[tt][cg][2 * (e & 1) + 1], c, nm[cg]));
+        h[e] = pack_bf16(p0, p1);
+        l[e] = pack_bf16(p0 - bf_lo(h[e]), p1 - bf_hi(h[e]));
+        psum += p0 + p1;
+      }
+      l_run[cg] += psum;
+      phi[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+      plo[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+    }
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt) {
+      const int d = 16 * dt + n;
+      const bf16x8_t va = __builtin_bit_cast(
+          bf16x8_t, *reinterpret_cast<const uint4 *>(sv + d * BK + 8 * v_phys(d, 4 * c2 + kg)));
+#pragma unroll
+      for (int cg = 0; cg < 2; ++cg) {
+        acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[cg], acc[dt][cg], 0, 0, 0);
+        acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[cg], acc[dt][cg], 0, 0, 0);
+      }
+    }
   }
 }
 
 template <int D, int G>
-__global__ __launch_bounds__(kThreads) void k_extend(ExtendArgs a) {
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(EXT_WAVES_PER_EU, EXT_WAVES_PER_EU))) void
+k_extend(ExtendArgs a) {
   using Lt = ExtLayout<D>;
   constexpr int NKC = D / 32; // k chunks of S^T = K . Q^T
   constexpr int NDT = D / 16; // 16-channel tiles of O^T
   constexpr int TQ = kExtRows / G;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[BK * Lt::KP];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[D * Lt::VP];
+  __shared__ __attribute__((aligned(16))) uint16_t sk[2][Lt::K_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[2][Lt::V_ELEMS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
@@ -157,9 +281,9 @@ __global__ __launch_bounds__(kThreads) void k_extend(ExtendArgs a) {
   bool live[2];
 #pragma unroll
   for (int cg = 0; cg < 2; ++cg) {
-    const int c = 32 * wave + 16 * cg + n;
-    jrow[cg] = j0 + c / G;
-    hrow[cg] = g * G + c % G;
+    const int col = 32 * wave + 16 * cg + n;
+    jrow[cg] = j0 + col / G;
+    hrow[cg] = g * G + col % G;
     live[cg] = jrow[cg] < a.n;
     lim[cg] = live[cg] ? base + jrow[cg] : a.L - 1;
     const uint16_t *qp = a.q + ((int64_t)jrow[cg] * a.hq + hrow[cg]) * D + 8 * kg;
@@ -183,89 +307,19 @@ __global__ __launch_bounds__(kThreads) void k_extend(ExtendArgs a) {
 
   const uint16_t *kbase = a.k + (int64_t)g * a.head_stride;
   const uint16_t *vbase = a.v + (int64_t)g * a.head_stride;
-  uint4 kr[Lt::NU], vr[Lt::NU];
-  ext_load<D>(kr, vr, a, kbase, vbase, 0, tid);
+  ext_dma<D>(sk[0], sv[0], a, kbase, vbase, 0, wave, lane);
   for (int b = 0; b < nblk; ++b) {
-    if (b) __syncthreads(); // every wave is done reading the previous block
-    ext_store<D>(kr, vr, sk, sv, b, tid, a.L);
+    // block b has landed (every wave's copies) and every wave is done with
+    // block b - 1, whose buffer the next copy overwrites
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (b + 1 < nblk) ext_load<D>(kr, vr, a, kbase, vbase, b + 1, tid);
-
-    f32x4_t st[4][2];
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-      for (int cg = 0; cg < 2; ++cg) st[tt][cg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-      for (int kc = 0; kc < NKC; ++kc) {
-        const bf16x8_t ka = __builtin_bit_cast(
-            bf16x8_t, *reinterpret_cast<const uint4 *>(sk + (16 * tt + n) * Lt::KP + 32 * kc + 8 * kg));
-#pragma unroll
-        for (int cg = 0; cg < 2; ++cg)
-          st[tt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[cg][kc], st[tt][cg], 0, 0, 0);
-      }
-
-    const bool need_mask = b * BK + BK - 1 > mask_from;
-    uint4 phi[2][2], plo[2][2];
-    float alpha[2];
-#pragma unroll
-    for (int cg = 0; cg < 2; ++cg) {
-      float x[4][4];
-      float mx = kNegInf;
-#pragma unroll
-      for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int t = b * BK + 16 * tt + 4 * kg + i;
-          x[tt][i] = (need_mask && t > lim[cg]) ? kNegInf : st[tt][cg][i] * a.scale_log2;
-          mx = fmaxf(mx, x[tt][i]);
-        }
-      mx = max_xrow16(mx);
-      mx = max_xrow32(mx);
-      const float m_new = fmaxf(m_run[cg], mx);
-      const bool none = m_new == kNegInf;
-      alpha[cg] = none ? 1.f : exp2_fast(m_run[cg] - m_new);
-      float psum = 0.f;
-#pragma unroll
-      for (int c2 = 0; c2 < 2; ++c2) {
-        uint32_t h[4], l[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const int tt = 2 * c2 + (e >> 1);
-          const float p0 = none ? 0.f : exp2_fast(x[tt][2 * (e & 1)] - m_new);
-          const float p1 = none ? 0.f : exp2_fast(x[tt][2 * (e & 1) + 1] - m_new);
-          h[e] = pack_bf16(p0, p1);
-          l[e] = pack_bf16(p0 - bf_lo(h[e]), p1 - bf_hi(h[e]));
-          psum += (bf_lo(h[e]) + bf_lo(l[e])) + (bf_hi(h[e]) + bf_hi(l[e]));
-        }
-        phi[cg][c2] = make_uint4(h[0], h[1], h[2], h[3]);
-        plo[cg][c2] = make_uint4(l[0], l[1], l[2], l[3]);
-      }
-      l_run[cg] = l_run[cg] * alpha[cg] + psum;
-      m_run[cg] = m_new;
+    if ((b + 1) * BK > a.L) {
+      ext_zero_tail<D>(sv[b & 1], b, a.L, tid);
+      __syncthreads();
     }
-    if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-        for (int cg = 0; cg < 2; ++cg) acc[dt][cg] *= alpha[cg];
-    }
-#pragma unroll
-    for (int c2 = 0; c2 < 2; ++c2)
-#pragma unroll
-      for (int dt = 0; dt < NDT; ++dt) {
-        const bf16x8_t va = __builtin_bit_cast(
-            bf16x8_t, *reinterpret_cast<const uint4 *>(sv + (16 * dt + n) * Lt::VP + 32 * c2 + 8 * kg));
-#pragma unroll
-        for (int cg = 0; cg < 2; ++cg) {
-          acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              va, __builtin_bit_cast(bf16x8_t, phi[cg][c2]), acc[dt][cg], 0, 0, 0);
-          acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-              va, __builtin_bit_cast(bf16x8_t, plo[cg][c2]), acc[dt][cg], 0, 0, 0);
-        }
-      }
+    if (b + 1 < nblk) ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, b + 1, wave, lane);
+    ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2, b * BK + BK - 1 > mask_from, qf,
+                 lim, acc, m_run, l_run);
   }
 
 #pragma unroll

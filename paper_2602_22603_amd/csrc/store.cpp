@@ -1120,7 +1120,8 @@ sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, 
   if (n_new == 0) return SQ_OK;
   if (!q || !out || !aligned16(q) || !aligned16(out))
     return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
-  if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
+  if (!std::isfinite(scale) || !(scale > 0.f))
+    return fail(SQ_ERR_INVALID, "scale must be finite and positive");
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
   sq::ExtendArgs a{};
