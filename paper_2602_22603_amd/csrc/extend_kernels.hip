@@ -73,12 +73,13 @@ __device__ inline float sum_xrow32(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-// bf16 round-to-nearest-even of two floats, packed low | high << 16.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v_t __attribute__((ext_vector_type(2)));
+
+// bf16 round-to-nearest-even of two floats, packed low | high << 16 (one
+// v_cvt_pk_bf16_f32).
 __device__ inline uint32_t pack_bf16(float lo, float hi) {
-  const __hip_bfloat162 v = __float22bfloat162_rn(make_float2(lo, hi));
-  uint32_t u;
-  __builtin_memcpy(&u, &v, sizeof(u));
-  return u;
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector((f32x2_t){lo, hi}, bf16x2v_t));
 }
 
 template <int D> struct ExtLayout {
@@ -90,11 +91,23 @@ template <int D> struct ExtLayout {
   static constexpr int NV = V_ELEMS * 2 / 1024 / 4; // V DMAs per wave per block
 };
 
-// Swizzles: the physical 16-byte chunk of logical chunk c in a row.
+// Swizzles: the physical 16-byte chunk of logical chunk c in a row.  A
+// 16-byte LDS read (ds_read_b128) is served half a wave at a time from 128
+// four-byte banks (measured on gfx950 with the bank-conflict counter), so it
+// is conflict-free when the 32 chunks a half-wave reads are distinct modulo
+// 32.  An operand read has lane (n, kg) read logical chunk 4 kc + kg (K) or
+// 4 c2 + kg (V^T) of one of 16 rows picked by n.
+//   K: row = tile_key(t, n) = 32a + 8(n >> 2) + 4h + (n & 3).  With 256-byte
+//      rows the key (n & 3) + 4 (n >> 2) = n spreads the 8 rows of each
+//      parity over all 16 slots; with 128-byte rows rows of equal n & 3
+//      share a bank quarter, and 2 (n >> 2) separates them.
+//   V^T: row d = 16 dt + n of 128 bytes; rows of equal n & 3 share a bank
+//      quarter, separated by 2 ((d >> 2) & 3).
 template <int D> __device__ inline int k_phys(int row, int c) {
-  return (c ^ (4 * (row & 3) + ((row >> 3) & 3))) & (D / 8 - 1);
+  if constexpr (D == 128) return c ^ ((row & 3) + 4 * ((row >> 3) & 3));
+  else return c ^ (2 * ((row >> 3) & 3));
 }
-__device__ inline int v_phys(int d, int j) { return j ^ ((d >> 1) & 7); }
+__device__ inline int v_phys(int d, int j) { return j ^ (2 * ((d >> 2) & 3)); }
 
 // The block key held by A row r of S^T tile t (0..3): tiles 2c and 2c + 1
 // cover the 32-key chunk c, row 4 kg + i of tile 2c + h being key
@@ -105,37 +118,48 @@ __device__ inline int tile_key(int t, int r) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
-// Global -> LDS (direct) for block blk: this wave's share of the K rows and
-// V^T rows.  Pages past the sequence's list are skipped (their keys are
-// masked and their V zeroed before use).
+// Page ids of block blk (4 pages; ids past the sequence's list repeat its
+// last page: every key there is at or past L, so its score is masked and its
+// V zeroed before use).  The index is uniform, so these are scalar loads,
+// issued a block ahead of their use.
+__device__ inline void block_ids(int32_t (&ids)[4], const ExtendArgs &a, int blk) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+    ids[i] = __builtin_amdgcn_readfirstlane(a.pt[min(blk * (BK / kPage) + i, a.n_pages - 1)]);
+}
+
+// ids[q] for a q that may differ per lane, without branches.
+__device__ inline int32_t pick4(const int32_t (&ids)[4], int q) {
+  const int32_t lo = (q & 1) ? ids[1] : ids[0];
+  const int32_t hi = (q & 1) ? ids[3] : ids[2];
+  return (q & 2) ? hi : lo;
+}
+
+// Global -> LDS (direct) for one block: this wave's share of the K rows and
+// V^T rows.
 template <int D>
 __device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
-                               const uint16_t *kbase, const uint16_t *vbase, int blk, int wave,
-                               int lane) {
+                               const uint16_t *kbase, const uint16_t *vbase,
+                               const int32_t (&ids)[4], int wave, int lane) {
   using Lt = ExtLayout<D>;
 #pragma unroll
   for (int u = 0; u < Lt::NK; ++u) {
     const int ins = wave * Lt::NK + u;
     const int row = ins * Lt::KROWS + lane / Lt::CH;
     const int c = k_phys<D>(row, lane % Lt::CH); // the swizzle is an involution
-    const int pg = blk * (BK / kPage) + row / kPage;
-    const int32_t id = pg < a.n_pages ? a.pt[pg] : -1;
-    if (id >= 0)
-      __builtin_amdgcn_global_load_lds(
-          kbase + (int64_t)id * a.page_stride + (row % kPage) * D + 8 * c,
-          (lds_void *)(sk + ins * 512), 16, 0, 0);
+    const int p = (ins * Lt::KROWS) / kPage;     // uniform: a DMA stays in one page
+    __builtin_amdgcn_global_load_lds(
+        kbase + (int64_t)pick4(ids, p) * a.page_stride + (row % kPage) * D + 8 * c,
+        (lds_void *)(sk + ins * 512), 16, 0, 0);
   }
 #pragma unroll
   for (int u = 0; u < Lt::NV; ++u) {
     const int ins = wave * Lt::NV + u;
     const int d = ins * 8 + lane / 8;
     const int j = v_phys(d, lane % 8);
-    const int pg = blk * (BK / kPage) + j / 2;
-    const int32_t id = pg < a.n_pages ? a.pt[pg] : -1;
-    if (id >= 0)
-      __builtin_amdgcn_global_load_lds(
-          vbase + (int64_t)id * a.page_stride + d * kPage + 8 * (j & 1),
-          (lds_void *)(sv + ins * 512), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(
+        vbase + (int64_t)pick4(ids, j >> 1) * a.page_stride + d * kPage + 8 * (j & 1),
+        (lds_void *)(sv + ins * 512), 16, 0, 0);
   }
 }
 
@@ -268,7 +292,8 @@ k_extend(ExtendArgs a) {
   __shared__ __attribute__((aligned(16))) uint16_t sv[2][Lt::V_ELEMS];
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6); // uniform: the DMA destination is M0
   const int n = lane & 15, kg = lane >> 4;
   const int g = blockIdx.x % a.hkv;
   const int qb = a.n_qblocks - 1 - (int)(blockIdx.x / a.hkv);
@@ -307,7 +332,10 @@ k_extend(ExtendArgs a) {
 
   const uint16_t *kbase = a.k + (int64_t)g * a.head_stride;
   const uint16_t *vbase = a.v + (int64_t)g * a.head_stride;
-  ext_dma<D>(sk[0], sv[0], a, kbase, vbase, 0, wave, lane);
+  int32_t ids[4];
+  block_ids(ids, a, 0);
+  ext_dma<D>(sk[0], sv[0], a, kbase, vbase, ids, wave, lane);
+  block_ids(ids, a, 1);
   for (int b = 0; b < nblk; ++b) {
     // block b has landed (every wave's copies) and every wave is done with
     // block b - 1, whose buffer the next copy overwrites
@@ -317,7 +345,10 @@ k_extend(ExtendArgs a) {
       ext_zero_tail<D>(sv[b & 1], b, a.L, tid);
       __syncthreads();
     }
-    if (b + 1 < nblk) ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, b + 1, wave, lane);
+    if (b + 1 < nblk) {
+      ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, ids, wave, lane);
+      block_ids(ids, a, b + 2);
+    }
     ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2, b * BK + BK - 1 > mask_from, qf,
                  lim, acc, m_run, l_run);
   }
