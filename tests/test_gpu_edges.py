@@ -1,0 +1,148 @@
+"""GPU parity at the edges of the decode planner: the largest batch, empty
+and one-token sequences, duplicate entries, shared-prefix groups wider than
+one MFMA tile holds, sequences that share a workgroup's page range with a
+long one, negative and unusual scales, and layers past the first.  Every
+mode is compared with the oracle (max abs error <= 5e-4); page tables and
+views bit for bit."""
+
+import numpy as np
+import pytest
+
+from tests import scenarios as sc
+
+pytestmark = pytest.mark.gpu
+TOL = 5e-4
+
+
+@pytest.fixture(scope="module")
+def sq():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2602_22603_amd import sq as sqmod
+    sqmod.lib()
+    return sqmod
+
+
+@pytest.fixture(autouse=True)
+def _free_memory():
+    yield
+    import gc
+    import torch
+    gc.collect()
+    if torch.cuda.is_available():
+        torch.cuda.empty_cache()
+
+
+def _check(t, seqs, **kw):
+    errs, ref = t.decode_errors(seqs, **kw)
+    for m, e in errs.items():
+        assert e <= TOL, (m, e)
+    return errs, ref
+
+
+def test_largest_batch_with_empty_and_tiny_sequences(sq):
+    """64 queries: 24 main threads of mixed lengths (0, 1, 15, 16, 17, ...)
+    and 40 forks of them, some forked mid-page."""
+    rng = np.random.default_rng(7)
+    t = sc.Twin(sq, 1, 32, 8, 128, 2600, 64, 80, seed=71)
+    mains = []
+    lengths = [0, 1, 15, 16, 17, 31, 33, 64, 65, 100, 257, 500, 1023, 1024, 1025, 7, 2, 3, 48,
+               49, 200, 300, 640, 900]
+    for n in lengths:
+        a = t.create()
+        if n:
+            t.append(a, n)
+        mains.append(a)
+    seqs = list(mains)
+    while len(seqs) < 64:
+        i = int(rng.integers(0, len(mains)))
+        L = lengths[i]
+        f = int(rng.integers(0, L + 1))
+        c = t.fork(mains[i], f)
+        extra = int(rng.integers(0, 40))
+        if extra:
+            t.append(c, extra)
+        seqs.append(c)
+    t.check_state()
+    errs, ref = _check(t, seqs)
+    assert np.all(ref[0] == 0)          # the empty sequence attends to nothing
+    print("batch 64:", errs)
+
+
+def test_duplicate_entries_in_one_batch(sq):
+    t = sc.Twin(sq, 1, 8, 2, 64, 200, 4, 64, seed=72)
+    a = t.create()
+    t.append(a, 300)
+    b = t.fork(a, 250)
+    t.append(b, 11)
+    _check(t, [a, b, a, a, b])   # each entry has its own query
+
+
+@pytest.mark.parametrize("group", [2, 4, 8])
+def test_wide_fork_fanout(sq, group):
+    """One main thread with six auxiliary forks at the same point: more
+    members than one 16-row MFMA tile holds (16 / G), split into groups."""
+    hkv = 2
+    t = sc.Twin(sq, 1, hkv * group, hkv, 128, 400, 12, 64, seed=73 + group)
+    a = t.create()
+    t.append(a, 700)
+    seqs = [a]
+    for i in range(6):
+        c = t.fork(a, 640 if i % 2 else 700)
+        t.append(c, 5 + 7 * i)
+        seqs.append(c)
+    info = t.store.plan_info(seqs, sq.ATTN_AUTO)
+    assert info["n_groups"] >= 2
+    _check(t, seqs)
+
+
+def test_short_rows_share_a_workgroup_with_a_long_one(sq):
+    """A 20K-token sequence among one-page sequences: the balanced split
+    lays rows end to end, so one workgroup's range covers several short
+    rows and the start of the long one."""
+    t = sc.Twin(sq, 1, 32, 8, 128, 1400, 8, 1300, seed=74)
+    long_ = t.create()
+    t.append(long_, 20000)
+    seqs = []
+    for n in (1, 3, 16, 17, 5):
+        a = t.create()
+        t.append(a, n)
+        seqs.append(a)
+    seqs.insert(2, long_)
+    _check(t, seqs)
+
+
+def test_everything_evicted_then_regrown(sq):
+    t = sc.Twin(sq, 1, 8, 2, 64, 200, 4, 64, seed=75)
+    a = t.create()
+    t.append(a, 100)
+    t.mark(a, 0, 0, 60)
+    t.mark(a, 1, 60, 100)
+    t.evict(a, [0, 1])
+    assert t.store.seq_info(a)["length"] == 0
+    errs, ref = _check(t, [a])
+    assert np.all(ref == 0)
+    t.append(a, 1)
+    t.check_state()
+    _check(t, [a])
+
+
+@pytest.mark.parametrize("scale", [-0.2, 0.37, 2.5])
+def test_unusual_scales(sq, scale):
+    t = sc.Twin(sq, 1, 8, 2, 128, 200, 4, 80, seed=76)
+    a = t.create()
+    t.append(a, 1000)
+    b = t.fork(a, 992)
+    t.append(b, 20)
+    _check(t, [a, b], scale=scale)
+
+
+def test_later_layers(sq):
+    t = sc.Twin(sq, 4, 8, 2, 64, 300, 4, 80, seed=77)
+    a = t.create()
+    t.append(a, 777)
+    b = t.fork(a, 700)
+    t.append(b, 30)
+    for layer in (3, 1):
+        _check(t, [a, b], layer=layer)
