@@ -571,28 +571,36 @@ k_decode_mfma(DecodeArgs a) {
 
 // ===========================================================================
 // Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
-// Its partials are the chunks of at most two segments; wave w takes chunks
-// w, w + kMergeWaves, ...  The global maximum M of m over all chunks comes
-// first (lanes over chunks, then across waves through LDS); each wave then
-// accumulates sum w_c l_c and sum w_c acc_c with w_c = 2^(m_c - M), lanes over
-// channels, issuing independent row loads; LDS adds the waves' sums.
-constexpr int kMergeWaves = 4;
+// Its partials are the pieces of at most two segments.  Every thread first
+// loads the (m, l) of its partials and the block takes the global maximum M
+// of m; the weights w_c = 2^(m_c - M) and the row offsets go to LDS, and the
+// waves then accumulate sum w_c acc_c over disjoint partials, lanes over
+// channels, with 16 row loads in flight per wave; LDS adds the waves' sums.
+// Latency, not bandwidth, bounds this kernel (a few hundred KB per launch),
+// so the point is to have every load of a round issued before the first
+// is used.
+constexpr int kMergeWaves = 8;
+constexpr int kMergeChunk = 2048; // partials whose weights sit in LDS at once
+constexpr int kMergeUnroll = 16;
 
 template <int D>
 __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) {
   constexpr int DPT = D / 64;
-  __shared__ float s_max[kMergeWaves];
-  __shared__ float s_den[kMergeWaves];
+  constexpr int NT = 64 * kMergeWaves;
+  __shared__ float s_red[kMergeWaves];
+  __shared__ float s_w[kMergeChunk];
+  __shared__ int32_t s_off[kMergeChunk];
   __shared__ float s_num[kMergeWaves][D];
-  const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = tid >> 6;
   const int b = blockIdx.x / a.hq;
   const int h = blockIdx.x - b * a.hq;
   const int g = h / a.group;
   const int hr = h - g * a.group;
   const int ns = a.n_src[b];
   int n0 = 0, n1 = 0;
-  int64_t base0 = 0, base1 = 0;
+  int32_t base0 = 0, base1 = 0;
   for (int e = 0; e < ns; ++e) {
     const int L = a.src_launch[b][e];
     const int np = a.src_npages[b][e];
@@ -600,8 +608,7 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
     const int w_lo = wg_of(R, a.total[L], a.n_wg[L]);
     const int w_hi = wg_of(R + np - 1, a.total[L], a.n_wg[L]);
     const int r = a.src_seg[b][e] * a.hkv + g;
-    const int64_t base = (int64_t)(a.slot_base[L] + w_lo + r) * kRows +
-                         a.src_member[b][e] * a.group + hr;
+    const int32_t base = (a.slot_base[L] + w_lo + r) * kRows + a.src_member[b][e] * a.group + hr;
     if (e == 0) {
       n0 = w_hi - w_lo + 1;
       base0 = base;
@@ -611,77 +618,65 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
     }
   }
   const int total = n0 + n1;
-  auto row_of = [&](int c) -> int64_t {
-    return c < n0 ? base0 + (int64_t)c * kRows : base1 + (int64_t)(c - n0) * kRows;
-  };
+  auto row_of = [&](int c) -> int32_t { return c < n0 ? base0 + c * kRows : base1 + (c - n0) * kRows; };
+
   float big_m = kNegInf;
-  for (int c = threadIdx.x; c < total; c += 64 * kMergeWaves) big_m = fmaxf(big_m, a.part_m[row_of(c)]);
+  for (int c = tid; c < total; c += NT) big_m = fmaxf(big_m, a.part_m[row_of(c)]);
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) big_m = fmaxf(big_m, __shfl_xor(big_m, o));
-  if (lane == 0) s_max[wave] = big_m;
+  if (lane == 0) s_red[wave] = big_m;
   __syncthreads();
 #pragma unroll
-  for (int w = 0; w < kMergeWaves; ++w) big_m = fmaxf(big_m, s_max[w]);
+  for (int w = 0; w < kMergeWaves; ++w) big_m = fmaxf(big_m, s_red[w]);
+  __syncthreads(); // s_red is reused for the denominators
+
   float num[DPT];
 #pragma unroll
   for (int i = 0; i < DPT; ++i) num[i] = 0.f;
   float den = 0.f;
   if (big_m != kNegInf) {
-    // chunks of this wave: wave + kMergeWaves * j, handled 64 at a time
-    const int mine = total > wave ? (total - wave + kMergeWaves - 1) / kMergeWaves : 0;
-    for (int j0 = 0; j0 < mine; j0 += 64) {
-      const int j = j0 + lane;
-      float w = 0.f;
-      int64_t row = 0;
-      if (j < mine) {
-        row = row_of(wave + kMergeWaves * j);
-        w = exp2_fast(a.part_m[row] - big_m);
+    for (int c0 = 0; c0 < total; c0 += kMergeChunk) {
+      const int nc = min(kMergeChunk, total - c0);
+      for (int c = tid; c < nc; c += NT) {
+        const int32_t row = row_of(c0 + c);
+        const float w = exp2_fast(a.part_m[row] - big_m); // empty partials: 2^-inf = 0
         den = fmaf(w, a.part_l[row], den);
+        s_w[c] = w;
+        s_off[c] = row;
       }
-      const int nb = min(64, mine - j0);
-      int i = 0;
-      for (; i + 4 <= nb; i += 4) {
-        float wv[4];
-        const float *src[4];
+      __syncthreads();
+      // wave w takes partials [w * per, (w + 1) * per) of the chunk
+      const int per = (nc + kMergeWaves - 1) / kMergeWaves;
+      const int cb = wave * per, ce = min(nc, cb + per);
+      for (int i = cb; i < ce; i += kMergeUnroll) {
+        float x[kMergeUnroll][DPT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u) {
-          wv[u] = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i + u));
-          const int rlo = __builtin_amdgcn_readlane((int)(row & 0xffffffff), i + u);
-          const int rhi = __builtin_amdgcn_readlane((int)(row >> 32), i + u);
-          const int64_t r = ((int64_t)rhi << 32) | (uint32_t)rlo;
-          src[u] = a.part_acc + r * D + lane * DPT;
+        for (int u = 0; u < kMergeUnroll; ++u) {
+          const int c = min(i + u, ce - 1); // repeats of the last row carry weight 0
+          const float *src = a.part_acc + (int64_t)s_off[c] * D + lane * DPT;
+#pragma unroll
+          for (int q = 0; q < DPT; ++q) x[u][q] = src[q];
         }
-        float x[4][DPT];
 #pragma unroll
-        for (int u = 0; u < 4; ++u)
+        for (int u = 0; u < kMergeUnroll; ++u) {
+          const float w = i + u < ce ? s_w[i + u] : 0.f;
 #pragma unroll
-          for (int q = 0; q < DPT; ++q) x[u][q] = src[u][q];
-#pragma unroll
-        for (int u = 0; u < 4; ++u)
-#pragma unroll
-          for (int q = 0; q < DPT; ++q) num[q] = fmaf(wv[u], x[u][q], num[q]);
+          for (int q = 0; q < DPT; ++q) num[q] = fmaf(w, x[u][q], num[q]);
+        }
       }
-      for (; i < nb; ++i) {
-        const float wv = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i));
-        const int rlo = __builtin_amdgcn_readlane((int)(row & 0xffffffff), i);
-        const int rhi = __builtin_amdgcn_readlane((int)(row >> 32), i);
-        const int64_t r = ((int64_t)rhi << 32) | (uint32_t)rlo;
-        const float *src = a.part_acc + r * D + lane * DPT;
-#pragma unroll
-        for (int q = 0; q < DPT; ++q) num[q] = fmaf(wv, src[q], num[q]);
-      }
+      __syncthreads(); // the next chunk overwrites s_w / s_off
     }
   }
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o);
-  if (lane == 0) s_den[wave] = den;
+  if (lane == 0) s_red[wave] = den;
 #pragma unroll
   for (int q = 0; q < DPT; ++q) s_num[wave][lane * DPT + q] = num[q];
   __syncthreads();
   if (wave == 0) {
     float dt = 0.f;
 #pragma unroll
-    for (int w = 0; w < kMergeWaves; ++w) dt += s_den[w];
+    for (int w = 0; w < kMergeWaves; ++w) dt += s_red[w];
     float *out = a.out + ((int64_t)b * a.hq + h) * D + lane * DPT;
 #pragma unroll
     for (int q = 0; q < DPT; ++q) {
