@@ -55,8 +55,10 @@ def parse_args():
 
 
 def kernel_sha():
+    """Hash of the sources the decode kernels are built from (the committed
+    counter summaries are valid only for the sources they were taken on)."""
     h = hashlib.sha256()
-    for f in ("decode_kernels.hip", "kv_kernels.hip", "sq_kernels.hpp"):
+    for f in ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp"):
         with open(os.path.join(ROOT, "paper_2602_22603_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]

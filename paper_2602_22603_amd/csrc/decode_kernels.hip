@@ -28,7 +28,7 @@
 // every exponential is one v_exp_f32; m in the partials is in log2 units.
 #include <hip/hip_bf16.h>
 
-#include "sq_kernels.hpp"
+#include "decode_args.hpp"
 
 namespace sq {
 namespace {

@@ -1,0 +1,38 @@
+// extend_args.hpp - kernel arguments and launcher of the extend kernel
+// (extend_kernels.hip).
+// Internal to libsq.
+#pragma once
+
+#include "sq_common.hpp"
+
+namespace sq {
+
+// ---- extend (causal attention of an appended chunk) ------------------------
+// The chunk is the last n of the sequence's L tokens; new token j attends to
+// logical keys 0 .. L - n + j.  A workgroup takes 128 query rows (128 / G
+// tokens x the G query heads of one KV head) against the whole key range.
+constexpr int kExtRows = 128;
+constexpr int kExtKeys = 64; // keys per LDS block (4 pages)
+
+struct ExtendArgs {
+  const uint16_t *q;  // bf16 [n][Hq][D]
+  const uint16_t *k;  // K pool of the layer
+  const uint16_t *v;  // V pool of the layer
+  const int32_t *pt;  // device page-table row of the sequence
+  float *out;         // fp32 [n][Hq][D]
+  int64_t page_stride;
+  int64_t head_stride;
+  int32_t n_pages;    // pages in the sequence's list
+  int32_t L;          // tokens in the sequence (the chunk included)
+  int32_t n;          // new tokens
+  int32_t hq;
+  int32_t hkv;
+  int32_t n_qblocks;  // ceil(n / (kExtRows / G))
+  float scale_log2;
+};
+
+static_assert(sizeof(ExtendArgs) < 4096, "extend kernel arguments too large");
+
+hipError_t launch_extend(int d, int group, const ExtendArgs &a, hipStream_t s);
+
+} // namespace sq

@@ -35,7 +35,7 @@
 // (n_qblocks - 1 - w / Hkv): the blocks that see the most keys start first.
 #include <hip/hip_bf16.h>
 
-#include "sq_kernels.hpp"
+#include "extend_args.hpp"
 
 namespace sq {
 namespace {

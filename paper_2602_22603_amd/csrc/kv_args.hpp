@@ -1,0 +1,90 @@
+// kv_args.hpp - kernel arguments and launchers of the append, fork-copy and eviction
+// kernels (kv_kernels.hip).
+// Internal to libsq.
+#pragma once
+
+#include "sq_common.hpp"
+
+namespace sq {
+
+constexpr int kScanBlock = 2048;     // tokens per block of the eviction scan
+constexpr int kScanThreads = 256;
+
+// ---- append ---------------------------------------------------------------
+// Tokens [tok0, tok0 + n_tok) of an append of n_total tokens, landing in
+// pages page_ids[0..n_pages) starting at slot slot0 of the first page.
+struct AppendArgs {
+  int32_t n_tok;
+  int32_t n_total;
+  int32_t tok0;
+  int32_t slot0;
+  int32_t pos0;      // position of token tok0
+  int32_t n_pages;
+  int32_t pt_first;  // page-list index of page_ids[0]
+  int32_t new_from;  // page_ids[i] with i >= new_from are new: write them to the mirror
+  int32_t *pt_row;   // device page-table row of the sequence
+  int32_t page_ids[kMaxAppendPages];
+};
+
+// One token for each of n sequences.
+struct AppendBatchArgs {
+  int32_t n;
+  int32_t page[kMaxBatch];
+  int32_t slot[kMaxBatch];
+  int32_t pos[kMaxBatch];
+  int32_t pt_index[kMaxBatch]; // row * max_pages + index, or -1 if the page is not new
+  int32_t *pt;                 // device page-table mirror base
+};
+
+// ---- eviction -------------------------------------------------------------
+// Evicted spans as [n_spans][3] = (start, end, evicted tokens before start),
+// sorted, disjoint and non-empty: up to kInlineSpans travel in the kernel
+// arguments, more are read from device memory.
+constexpr int kInlineSpans = 96;
+constexpr int kInlineRanges = 60;
+
+struct EvictArgs {
+  int32_t n_tokens;     // L
+  int32_t n_spans;
+  const int32_t *spans; // device copy when n_spans > kInlineSpans
+  uint8_t *keep;        // [L]
+  int32_t *dst;         // [L]
+  int32_t *src_of;      // [L']
+  int32_t inl[3 * kInlineSpans];
+};
+
+// The fresh page ids of an eviction: a device list, or (when they form at
+// most kInlineRanges runs of consecutive ids) the runs themselves.
+struct NewIds {
+  const int32_t *list;            // device, or null when the runs are used
+  int32_t n_runs;
+  int32_t first[kInlineRanges];   // first id of run r
+  int32_t before[kInlineRanges];  // fresh pages before run r
+};
+
+struct GatherArgs {
+  int32_t fp;             // first affected page index
+  int32_t n_new;          // fresh pages
+  int32_t new_len;        // L'
+  const int32_t *src_of;
+  const int32_t *pt_row;  // device page-table row, still holding the old ids
+  NewIds ids;
+};
+
+static_assert(sizeof(AppendArgs) < 4096, "append kernel arguments too large");
+static_assert(sizeof(AppendBatchArgs) < 4096, "append-batch kernel arguments too large");
+static_assert(sizeof(EvictArgs) < 4096, "eviction index arguments too large");
+static_assert(sizeof(GatherArgs) + sizeof(Pools) < 4096, "gather arguments too large");
+
+hipError_t launch_append(const Pools &p, const AppendArgs &a, const void *k_new,
+                         const void *v_new, hipStream_t s);
+hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const void *k_new,
+                               const void *v_new, hipStream_t s);
+hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t tail_index,
+                           int32_t tail_value, hipStream_t s);
+hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s);
+hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s);
+hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStream_t s);
+hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);
+
+} // namespace sq

@@ -12,7 +12,7 @@
 //                                 tokens of one channel are contiguous
 //   pos    [NP][P]               int32 position of each cached token
 // The page size is 16 throughout.
-#include "sq_kernels.hpp"
+#include "kv_args.hpp"
 
 namespace sq {
 namespace {
