@@ -33,6 +33,14 @@ Readings adopted where the paper is silent (also listed in the design notes)
   loses one reference and is freed at zero.  Pages still referenced by another
   live branch survive, so evicting one branch never changes what another
   branch attends to.
+* Chunked eviction (a store option: chunk C > 0 pages) bounds the transient
+  pages: the new tail's pages are allocated C at a time, in page-list order;
+  once the kept tokens of a chunk's pages are gathered, every old page from
+  fp on whose tokens all lie before the old index of the next kept token to
+  move loses its reference (and is freed at zero, so the next chunk may take
+  it again); the old pages left lose theirs at the end.  Live pages never
+  exceed the count before the call plus C.  C = 0 is the one-shot rule
+  above.
 * Positions are carried, never recomputed: a kept token keeps its position and
   new tokens continue from the counter.
 * Validation happens before any change: a failing call leaves the model as it
@@ -94,8 +102,9 @@ class PageModel:
     """
 
     def __init__(self, num_pages, page_size, max_seqs, max_pages_per_seq,
-                 layers=1, kv_heads=1, head_dim=1, with_data=False):
+                 layers=1, kv_heads=1, head_dim=1, with_data=False, evict_chunk_pages=0):
         self.num_pages = int(num_pages)
+        self.evict_chunk_pages = int(evict_chunk_pages)
         self.P = int(page_size)
         self.max_seqs = int(max_seqs)
         self.max_pages_per_seq = int(max_pages_per_seq)
@@ -105,6 +114,7 @@ class PageModel:
         heapq.heapify(self._free)
         self.seqs = {}
         self.peak_pages = 0
+        self.last_schedule = []  # the last eviction's (allocated, released) pages per step
         self.with_data = with_data
         if with_data:
             shape = (self.num_pages, self.P, layers, kv_heads, head_dim)
@@ -133,6 +143,14 @@ class PageModel:
             heapq.heappush(self._free, page)
             return 1
         return 0
+
+    def _released_after(self, fp, released, n_old, consumed):
+        """Old-tail pages [0, result) hold only tokens before old index
+        ``consumed`` (the next kept token still to move): they may go."""
+        upto = released
+        while upto < n_old and (fp + upto + 1) * self.P <= consumed:
+            upto += 1
+        return upto
 
     def _seq(self, h):
         if h not in self.seqs:
@@ -240,18 +258,47 @@ class PageModel:
         keep, _dst, src_of, new_len, first = _evict.plan(seq.length, spans)
         fp = first // self.P
         n_new = math.ceil(new_len / self.P) - fp
-        if n_new > self.free_pages():
-            raise NoPages("not enough free pages for the compacted tail")
-        new_pages = [self._alloc() for _ in range(n_new)]
-        if self.with_data:
-            for j in range(fp * self.P, new_len):
-                src = int(src_of[j])
-                sp, ss = seq.pages[src // self.P], src % self.P
-                dp, ds = new_pages[j // self.P - fp], j % self.P
-                self.K[dp, ds] = self.K[sp, ss]
-                self.V[dp, ds] = self.V[sp, ss]
-                self.POS[dp, ds] = self.POS[sp, ss]
-        freed = sum(self._unref(p) for p in seq.pages[fp:])
+        old_tail = seq.pages[fp:]
+        C = self.evict_chunk_pages if self.evict_chunk_pages > 0 else max(1, n_new)
+        # the schedule: (pages to allocate, old-tail pages released after them)
+        steps, released = [], 0
+        for k0 in range(0, n_new, C):
+            c = min(C, n_new - k0)
+            j_end = min((fp + k0 + c) * self.P, new_len)
+            consumed = int(src_of[j_end]) if j_end < new_len else seq.length
+            upto = self._released_after(fp, released, len(old_tail), consumed) if C < n_new else released
+            steps.append((c, old_tail[released:upto]))
+            released = upto
+        steps.append((0, old_tail[released:]))
+        # validate: every allocation must find its pages free
+        free, refs = self.free_pages(), {}
+        for c, rel in steps:
+            if c > free:
+                raise NoPages("not enough free pages for the compacted tail")
+            free -= c
+            for page in rel:
+                refs[page] = refs.get(page, self.refcount[page]) - 1
+                free += refs[page] == 0
+        if self.with_data:  # read every kept token before any page is reused
+            src = [int(src_of[j]) for j in range(fp * self.P, new_len)]
+            src_p = [seq.pages[x // self.P] for x in src]
+            src_s = [x % self.P for x in src]
+            moved_k, moved_v = self.K[src_p, src_s].copy(), self.V[src_p, src_s].copy()
+            moved_pos = self.POS[src_p, src_s].copy()
+        new_pages, freed = [], 0
+        self.last_schedule = []  # (pages allocated, pages released) per step
+        for c, rel in steps:
+            got = [self._alloc() for _ in range(c)]
+            new_pages += got
+            freed += sum(self._unref(page) for page in rel)
+            self.last_schedule.append((got, list(rel)))
+        if self.with_data and new_len > fp * self.P:
+            j = np.arange(fp * self.P, new_len)
+            dp = [new_pages[x // self.P - fp] for x in j]
+            ds = list(j % self.P)
+            self.K[dp, ds] = moved_k
+            self.V[dp, ds] = moved_v
+            self.POS[dp, ds] = moved_pos
         seq.pages = seq.pages[:fp] + new_pages
         seq.pos = [p for p, k in zip(seq.pos, keep) if k]
         old_len = seq.length

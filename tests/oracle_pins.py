@@ -238,15 +238,15 @@ def _state(model):
                            for h, s in model.seqs.items()}, model.peak_pages))
 
 
-def check_against_list_model(seed=10, n_ops=60):
+def check_against_list_model(seed=10, n_ops=60, chunks=(0,)):
     """Random op sequences: the page model's logical views equal a naive list
-    model's, for page sizes 1, 2, 4 and 16."""
+    model's, for page sizes 1, 2, 4 and 16 (and each eviction chunk size)."""
     rng = np.random.default_rng(seed)
     nl, hkv, d = 2, 2, 3
-    for page in [1, 2, 4, 16]:
+    for page, chunk in itertools.product([1, 2, 4, 16], chunks):
         model = pg.PageModel(num_pages=400, page_size=page, max_seqs=6,
                              max_pages_per_seq=400, layers=nl, kv_heads=hkv,
-                             head_dim=d, with_data=True)
+                             head_dim=d, with_data=True, evict_chunk_pages=chunk)
         ref = ListModel()
         next_cursor = 0
         h0 = model.seq_create()
@@ -557,6 +557,131 @@ def check_extend_compacted_equals_masked(seed=18):
             assert np.array_equal(got, want)
 
 
+# --------------------------------------------------------------------------
+# chunked eviction (bounded transient pages)
+# --------------------------------------------------------------------------
+def check_chunked_eviction_against_list_model():
+    """With chunked eviction every logical view, span and position still
+    equals the naive list model's, and refcounts match the page lists."""
+    check_against_list_model(seed=19, n_ops=50, chunks=(1, 2, 3))
+
+
+def check_chunked_page_tables_by_hand():
+    """P = 2, 8 tokens in pages [0, 1, 2, 3]; evicting tokens 1 and 2 keeps
+    0, 3, 4, 5, 6, 7 (3 pages).  One-shot: fresh pages 4, 5, 6.  C = 1:
+    page 4 takes tokens 0, 3; the next source is token 4, so old pages 0 and
+    1 go; page 0 takes 4, 5 and old page 2 goes; page 1 takes 6, 7.  C = 2:
+    pages 4, 5 take 0, 3, 4, 5; old pages 0-2 go; page 0 takes 6, 7.  The
+    live count peaks at 4 + C."""
+    want = {0: [4, 5, 6], 1: [4, 0, 1], 2: [4, 5, 0], 3: [4, 5, 6]}
+    for chunk, table in want.items():
+        m = pg.PageModel(num_pages=10, page_size=2, max_seqs=2, max_pages_per_seq=8,
+                         with_data=True, evict_chunk_pages=chunk)
+        a = m.seq_create()
+        k = np.arange(8, dtype=np.float64).reshape(1, 8, 1, 1)
+        m.append(a, 8, k, -k)
+        m.span_mark(a, 0, 1, 3)
+        st = m.evict(a, [0])
+        assert m.page_table(a) == table, (chunk, m.page_table(a))
+        assert m.peak_pages == 4 + (3 if chunk in (0, 3) else chunk), (chunk, m.peak_pages)
+        assert st["pages_allocated"] == 3 and st["pages_freed"] == 4
+        kv, vv, pos = m.view(a)
+        assert kv[:, 0, 0, 0].tolist() == [0, 3, 4, 5, 6, 7]
+        assert vv[:, 0, 0, 0].tolist() == [0, -3, -4, -5, -6, -7]
+        assert pos.tolist() == [0, 3, 4, 5, 6, 7]
+        assert m.live_pages() == 3
+
+
+def _chunk_reads(old_pages, first, spans, length, P, schedule):
+    """Old page ids each step's gather reads (from the plan, independently of
+    the model): step k fills the fresh pages it allocated, in page order."""
+    keep, _dst, src_of, new_len, _f = ev.plan(length, spans)
+    fp = first // P
+    reads, pi = [], 0
+    for got, _rel in schedule:
+        r = set()
+        for _ in got:
+            for j in range((fp + pi) * P, min((fp + pi + 1) * P, new_len)):
+                r.add(old_pages[int(src_of[j]) // P])
+            pi += 1
+        reads.append(r)
+    return reads
+
+
+def check_chunked_eviction_never_overwrites_unread_tokens(seed=20):
+    """Each step of a chunked eviction is one parallel gather, so no page it
+    writes may be read by it or a later step, and no page released after a
+    step may be read later.  A hand-built case (a sequence whose old tail
+    pages are [5, 6, 0, 1], P = 2, C = 1) puts a page that is released too
+    early at the bottom of the free list; random cases follow."""
+    def one(m, h, cursor):
+        seq = m.seqs[h]
+        old_pages, length = list(seq.pages), seq.length
+        spans = [m.spans(h)[cursor]]
+        if spans[0][1] <= spans[0][0]:
+            return
+        m.evict(h, [cursor])
+        reads = _chunk_reads(old_pages, spans[0][0], spans, length, m.P, m.last_schedule)
+        for k, (got, rel) in enumerate(m.last_schedule):
+            later = set().union(*reads[k:]) if reads[k:] else set()
+            assert not set(got) & later, (k, got, later)
+            after = set().union(*reads[k + 1:]) if reads[k + 1:] else set()
+            assert not set(rel) & after, (k, rel, after)
+
+    m = pg.PageModel(num_pages=12, page_size=2, max_seqs=3, max_pages_per_seq=12,
+                     with_data=True, evict_chunk_pages=1)
+    b = m.seq_create()
+    m.append(b, 10, np.zeros((1, 10, 1, 1)), np.zeros((1, 10, 1, 1)))
+    a = m.seq_create()
+    k = np.arange(8, dtype=np.float64).reshape(1, 8, 1, 1)
+    m.append(a, 4, k[:, :4], k[:, :4])
+    m.release(b)
+    m.append(a, 4, k[:, 4:], k[:, 4:])
+    assert m.page_table(a) == [5, 6, 0, 1]
+    m.span_mark(a, 0, 1, 2)
+    one(m, a, 0)
+    assert m.page_table(a) == [2, 3, 4, 0]
+    assert m.view(a)[0][:, 0, 0, 0].tolist() == [0, 2, 3, 4, 5, 6, 7]
+    rng = np.random.default_rng(seed)
+    for trial in range(40):
+        m = pg.PageModel(num_pages=80, page_size=2, max_seqs=3, max_pages_per_seq=80,
+                         evict_chunk_pages=int(rng.integers(1, 4)))
+        hs = [m.seq_create(), m.seq_create()]
+        for step in range(14):
+            h = hs[int(rng.integers(0, 2))]
+            m.append(h, int(rng.integers(1, 9)))
+            L = m.info(h)["length"]
+            s0 = int(rng.integers(0, L))
+            e0 = int(rng.integers(s0, L + 1))
+            try:
+                m.span_mark(h, step, s0, e0)
+            except pg.SpanError:
+                continue
+            if rng.random() < 0.5:
+                one(m, h, step)
+
+
+def check_chunked_eviction_fits_where_one_shot_does_not():
+    """With one free page the one-shot eviction above needs three and fails
+    (changing nothing); chunks of one page recycle the old pages and fit."""
+    for chunk, ok in ((0, False), (1, True)):
+        m = pg.PageModel(num_pages=5, page_size=2, max_seqs=2, max_pages_per_seq=8,
+                         with_data=True, evict_chunk_pages=chunk)
+        a = m.seq_create()
+        k = np.arange(8, dtype=np.float64).reshape(1, 8, 1, 1)
+        m.append(a, 8, k, k)
+        m.span_mark(a, 0, 1, 3)
+        snap = _state(m)
+        try:
+            m.evict(a, [0])
+            assert ok
+            assert m.page_table(a) == [4, 0, 1]
+            assert m.view(a)[0][:, 0, 0, 0].tolist() == [0, 3, 4, 5, 6, 7]
+        except pg.NoPages:
+            assert not ok
+            assert _state(m) == snap
+
+
 ALL_CHECKS = [
     check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
     check_uniform_closed_form, check_two_key_closed_form,
@@ -567,4 +692,7 @@ ALL_CHECKS = [
     check_evict_parent_leaves_child, check_errors_leave_state_unchanged,
     check_masked_equals_compacted, check_extend_textbook, check_extend_first_token_alone,
     check_extend_causal, check_extend_compacted_equals_masked,
+    check_chunked_eviction_against_list_model, check_chunked_page_tables_by_hand,
+    check_chunked_eviction_fits_where_one_shot_does_not,
+    check_chunked_eviction_never_overwrites_unread_tokens,
 ]

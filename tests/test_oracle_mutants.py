@@ -157,6 +157,23 @@ def _extend_ignores_mask(q, k, v, scale, group, mask=None):
 _orig_extend = ex.extend_attention
 
 
+def _released_one_page_early(self, fp, released, n_old, consumed):
+    upto = released
+    while upto < n_old and (fp + upto) * self.P <= consumed:
+        upto += 1
+    return upto
+
+
+def _evict_chunk_never_recycles(self, h, cursor_ids):
+    # allocate every fresh page before releasing any old one, even in chunks
+    chunk = self.evict_chunk_pages
+    self.evict_chunk_pages = 0
+    try:
+        return _orig_evict(self, h, cursor_ids)
+    finally:
+        self.evict_chunk_pages = chunk
+
+
 MUTANTS = {
     "gqa_head_modulo": (att, "scores", _scores_gqa_modulo),
     "missing_scale": (att, "scores", _scores_no_scale),
@@ -175,6 +192,8 @@ MUTANTS = {
     "extend_excludes_own_key": (ex, "extend_attention", _extend_excludes_self),
     "extend_drops_prefix_offset": (ex, "extend_attention", _extend_no_prefix_offset),
     "extend_ignores_mask": (ex, "extend_attention", _extend_ignores_mask),
+    "evict_chunks_never_recycle": (pg.PageModel, "evict", _evict_chunk_never_recycles),
+    "evict_chunk_releases_a_page_early": (pg.PageModel, "_released_after", _released_one_page_early),
 }
 
 
