@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 2
+#define SQ_ABI_VERSION 3
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -106,6 +106,14 @@ typedef struct {
   void *workspace;           /* device scratch of sq_workspace_bytes() bytes */
   uint64_t workspace_bytes;
   uint32_t flags;            /* SQ_STORE_* */
+  int32_t evict_chunk_pages; /* 0: sq_evict_spans allocates every fresh page
+                                of the compacted tail before releasing old
+                                ones.  C > 0: C fresh pages at a time, and the
+                                old pages whose tokens are all gathered are
+                                released between chunks (and may be reused by
+                                the next chunk), so an eviction holds at most
+                                C transient pages; one gather launch per
+                                chunk.  The resulting page ids differ. */
 } sq_store_config;
 
 typedef struct {

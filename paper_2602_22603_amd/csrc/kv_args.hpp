@@ -64,7 +64,8 @@ struct NewIds {
 
 struct GatherArgs {
   int32_t fp;             // first affected page index
-  int32_t n_new;          // fresh pages
+  int32_t pi0;            // first fresh page (of the tail) this launch fills
+  int32_t n_new;          // fresh pages this launch fills; ids[i] is tail page pi0 + i
   int32_t new_len;        // L'
   const int32_t *src_of;
   const int32_t *pt_row;  // device page-table row, still holding the old ids

@@ -212,22 +212,24 @@ __global__ __launch_bounds__(256) void k_write_ids(int32_t *dst, NewIds ids, int
 }
 
 // ---------------------------------------------------------------------------
-// Gather: block (fresh page pi, layer * Hkv + head) fills destination page
-// fp + pi with the kept tokens (fp + pi) * P + j, j < P, j below L'.  Each
-// comes from token src_of[t] of the old pages, whose ids the page-table row
-// still holds (the new ids are written there by the next launch).  Old and
-// fresh pages are distinct, so nothing is read after being written.
+// Gather: block (fresh page pi0 + b, layer * Hkv + head) fills destination
+// page fp + pi0 + b with the kept tokens (fp + pi0 + b) * P + j, j < P, j
+// below L'.  Each comes from token src_of[t] of the old pages, whose ids the
+// page-table row still holds (the new ids are written there after the last
+// gather).  A fresh page is never a page this or a later gather reads: it is
+// either a page nothing held or an old page whose tokens earlier gathers have
+// all moved, so nothing is read after being written.
 template <int D>
 __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   constexpr int U = D / 8;
   __shared__ int spage[P];
   __shared__ int sslot[P];
   __shared__ int nvalid;
-  const int pi = blockIdx.x;
+  const int pi = a.pi0 + blockIdx.x;
   const int lh = blockIdx.y;
   const int layer = lh / p.hkv;
   const int head = lh % p.hkv;
-  const int dst_page = new_page_id(a.ids, pi);
+  const int dst_page = new_page_id(a.ids, blockIdx.x);
   const int t0 = (a.fp + pi) * P;
   if (threadIdx.x < P) {
     const int t = t0 + threadIdx.x;

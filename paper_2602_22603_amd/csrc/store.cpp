@@ -87,6 +87,7 @@ bool shape_ok(const sq_store_config *c, bool device, std::string *why) {
   if (c->num_q_heads % c->num_kv_heads) return bad("num_q_heads must be a multiple of num_kv_heads");
   if ((int64_t)c->max_pages_per_seq * c->page_size > (int64_t)INT32_MAX / 2)
     return bad("max_pages_per_seq * page_size too large");
+  if (c->evict_chunk_pages < 0) return bad("evict_chunk_pages must be >= 0");
   if (device) {
     const int grp = c->num_q_heads / c->num_kv_heads;
     if (c->page_size != sq::kPage) return bad("device mode needs page_size 16");
@@ -857,14 +858,67 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
   const int64_t fp = f / s->P;
   const int64_t new_np = (Lp + s->P - 1) / s->P;
   const int64_t n_new = new_np - fp;
-  if (n_new > s->n_free)
-    return fail(SQ_ERR_NO_PAGES, "eviction needs %lld fresh pages, %lld free", (long long)n_new,
-                (long long)s->n_free);
+  // Old index of the kept token that lands at new index j: kept run k (the
+  // gap after span k - 1) starts at new index gap_dst[k] and is shifted by
+  // the tokens evicted before it.
+  std::vector<int64_t> gap_dst(sp.size() + 1), gap_shift(sp.size() + 1);
+  for (size_t k = 0; k <= sp.size(); ++k) {
+    const int64_t g0 = k == 0 ? 0 : sp[k - 1].second;
+    gap_shift[k] = k == 0 ? 0 : prefix[k - 1] + (sp[k - 1].second - sp[k - 1].first);
+    gap_dst[k] = g0 - gap_shift[k];
+  }
+  auto src_index = [&](int64_t j) -> int64_t {
+    const size_t k = std::upper_bound(gap_dst.begin(), gap_dst.end(), j) - gap_dst.begin() - 1;
+    return j + gap_shift[k];
+  };
 
-  // ---- commit: allocate, enqueue the device work, then the host bookkeeping ----
+  // The schedule: fresh pages per step and the old-tail pages released after
+  // it.  One-shot (evict_chunk_pages = 0): every fresh page first, every old
+  // page at the end.  Chunked: C fresh pages per step, then the old pages
+  // whose tokens all lie before the next kept token to move.
+  const std::vector<int32_t> old_tail(q->pages.begin() + fp, q->pages.end());
+  const int64_t C = s->cfg.evict_chunk_pages > 0 ? s->cfg.evict_chunk_pages
+                                                 : std::max<int64_t>(1, n_new);
+  struct Step {
+    int64_t k0, c;
+    size_t rel_begin, rel_end;
+  };
+  std::vector<Step> steps;
+  {
+    size_t released = 0;
+    for (int64_t k0 = 0; k0 < n_new; k0 += C) {
+      const int64_t c = std::min(C, n_new - k0);
+      size_t upto = released;
+      if (C < n_new) {
+        const int64_t j_end = std::min((fp + k0 + c) * s->P, Lp);
+        const int64_t consumed = j_end < Lp ? src_index(j_end) : L;
+        while (upto < old_tail.size() && (fp + (int64_t)upto + 1) * s->P <= consumed) ++upto;
+      }
+      steps.push_back({k0, c, released, upto});
+      released = upto;
+    }
+    steps.push_back({n_new, 0, released, old_tail.size()});
+  }
+  {
+    int64_t free_now = s->n_free;
+    for (const Step &st : steps) {
+      if (st.c > free_now)
+        return fail(SQ_ERR_NO_PAGES, "eviction needs %lld fresh pages at once, %lld free",
+                    (long long)st.c, (long long)free_now);
+      free_now -= st.c;
+      for (size_t i = st.rel_begin; i < st.rel_end; ++i) free_now += s->refcount[old_tail[i]] == 1;
+    }
+  }
+
+  // ---- commit: allocate and release in schedule order, enqueue the device
+  // work (stream order keeps every gather ahead of the reuse of what it read),
+  // then the host bookkeeping ----
   std::vector<int32_t> new_ids(n_new);
-  s->alloc_pages(n_new, new_ids.data());
-  std::vector<int32_t> old_tail(q->pages.begin() + fp, q->pages.end());
+  int64_t freed = 0;
+  for (const Step &st : steps) {
+    if (st.c) s->alloc_pages(st.c, new_ids.data() + st.k0);
+    for (size_t i = st.rel_begin; i < st.rel_end; ++i) s->unref(old_tail[i], &freed);
+  }
 
   if (s->device) {
     hipStream_t strm = static_cast<hipStream_t>(stream);
@@ -875,40 +929,37 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     ea.keep = s->ev_keep;
     ea.dst = s->ev_dst;
     ea.src_of = s->ev_src;
-    sq::NewIds ids{};
-    // runs of consecutive fresh ids (the allocator usually hands out a few)
-    for (int64_t i = 0; i < n_new; ++i) {
-      if (i == 0 || new_ids[i] != new_ids[i - 1] + 1) {
-        if (ids.n_runs == sq::kInlineRanges) {
-          ids.n_runs = -1;
-          break;
+    // fresh ids of tail pages [k0, k0 + n) as runs of consecutive ids, or as
+    // a list in the workspace when there are too many runs
+    auto runs_of = [&](int64_t k0, int64_t n, sq::NewIds *ids) {
+      *ids = sq::NewIds{};
+      for (int64_t i = 0; i < n; ++i) {
+        const int32_t id = new_ids[k0 + i];
+        if (i == 0 || id != new_ids[k0 + i - 1] + 1) {
+          if (ids->n_runs == sq::kInlineRanges) return false;
+          ids->first[ids->n_runs] = id;
+          ids->before[ids->n_runs] = (int32_t)i;
+          ++ids->n_runs;
         }
-        ids.first[ids.n_runs] = new_ids[i];
-        ids.before[ids.n_runs] = (int32_t)i;
-        ++ids.n_runs;
       }
-    }
+      return true;
+    };
+    sq::NewIds all{};
+    const bool all_inline = runs_of(0, n_new, &all);
     // what does not fit in the kernel arguments goes up in one copy:
     // spans [nsp][3] (start, end, evicted before) | fresh ids [n_new]
     std::vector<int32_t> up;
     const bool spans_inline = sp.size() <= (size_t)sq::kInlineSpans;
     for (size_t k = 0; k < sp.size(); ++k) {
-      int32_t *dst3 = nullptr;
-      int32_t tmp[3] = {(int32_t)sp[k].first, (int32_t)sp[k].second, (int32_t)prefix[k]};
-      if (spans_inline) {
-        dst3 = ea.inl + 3 * k;
-        dst3[0] = tmp[0];
-        dst3[1] = tmp[1];
-        dst3[2] = tmp[2];
-      } else {
-        up.insert(up.end(), tmp, tmp + 3);
-      }
+      const int32_t tmp[3] = {(int32_t)sp[k].first, (int32_t)sp[k].second, (int32_t)prefix[k]};
+      if (spans_inline) std::copy(tmp, tmp + 3, ea.inl + 3 * k);
+      else up.insert(up.end(), tmp, tmp + 3);
     }
     const size_t off_new = up.size();
-    if (ids.n_runs < 0) {
-      ids.n_runs = 0;
+    if (!all_inline) {
       up.insert(up.end(), new_ids.begin(), new_ids.end());
-      ids.list = s->ev_upload + off_new;
+      all = sq::NewIds{};
+      all.list = s->ev_upload + off_new;
     }
     if (!up.empty()) {
       sq_status us = upload(s, s->ev_upload, up.data(), up.size(), strm);
@@ -920,27 +971,33 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     hipError_t e = sq::launch_evict_index(ea, strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "eviction index");
-    sq::GatherArgs ga{};
-    ga.fp = (int32_t)fp;
-    ga.n_new = (int32_t)n_new;
-    ga.new_len = (int32_t)Lp;
-    ga.src_of = s->ev_src;
-    ga.pt_row = s->pt_row(h);
-    ga.ids = ids;
-    on = s->prof_begin(strm, &pp, kProfGather);
-    e = sq::launch_evict_gather(s->pools, ga, strm);
-    s->prof_end(strm, &pp, on);
-    if (e != hipSuccess) return hip_fail(e, "eviction gather");
-    // the page-table row takes the fresh ids after the gather has read the old
-    e = sq::launch_write_ids(s->pt_row(h) + fp, ids, (int32_t)n_new, strm);
+    for (const Step &st : steps) {
+      if (st.c == 0) continue;
+      sq::GatherArgs ga{};
+      ga.fp = (int32_t)fp;
+      ga.pi0 = (int32_t)st.k0;
+      ga.n_new = (int32_t)st.c;
+      ga.new_len = (int32_t)Lp;
+      ga.src_of = s->ev_src;
+      ga.pt_row = s->pt_row(h);
+      if (all_inline) {
+        runs_of(st.k0, st.c, &ga.ids); // a sub-range has no more runs than the whole
+      } else {
+        ga.ids.list = all.list + st.k0;
+      }
+      on = s->prof_begin(strm, &pp, kProfGather);
+      e = sq::launch_evict_gather(s->pools, ga, strm);
+      s->prof_end(strm, &pp, on);
+      if (e != hipSuccess) return hip_fail(e, "eviction gather");
+    }
+    // the page-table row takes the fresh ids after the last gather has read the old
+    e = sq::launch_write_ids(s->pt_row(h) + fp, all, (int32_t)n_new, strm);
     if (e != hipSuccess) return hip_fail(e, "page-table update");
     s->have_last_evict = true;
     s->last_evict_L = L;
     s->last_evict_Lp = Lp;
   }
 
-  int64_t freed = 0;
-  for (int32_t p : old_tail) s->unref(p, &freed);
   q->pages.resize(fp);
   q->pages.insert(q->pages.end(), new_ids.begin(), new_ids.end());
   // positions: drop the evicted index ranges, re-index the rest

@@ -52,14 +52,14 @@ def shared_task_inputs(w, t, device="cuda"):
     return k, v, ka, va
 
 
-def build_compaction64k(device="cuda", extra_tokens=256):
+def build_compaction64k(device="cuda", extra_tokens=256, evict_chunk_pages=0):
     """The 64K compaction workload: one sequence with its 40 tool spans
     marked.  Returns (store, base_seq, workload, k, v)."""
     w = wl.compaction64k()
     L = w.length
     store = _sq.Store(1, 32, 8, 128, num_pages=2 * (L // 16) + 2 * (extra_tokens // 16) + 64,
                       max_seqs=4, max_pages_per_seq=L // 16 + extra_tokens // 16 + 32,
-                      device=device)
+                      device=device, evict_chunk_pages=evict_chunk_pages)
     k = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000, device)
     v = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000 + 1, device)
     base = store.seq_create()
@@ -107,7 +107,7 @@ def full_stack_aux_inputs(w, turn, device="cuda"):
 
 
 def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers=36,
-                   device="cuda", decode=True, on_turn=None, store=None):
+                   device="cuda", decode=True, on_turn=None, store=None, evict_chunk_pages=0):
     """Algorithm 1 over a synthetic task: a non-evictable prefix, then turns
     of reasoning plus one tool response each.  Phase 1 evicts the cursors the
     auxiliary thread named (when it has finished) and releases it; Phase 2
@@ -118,7 +118,8 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
     run at the end of each turn and ``on_turn(t, store, seqs, q, out)`` is
     called after it.  Returns (store, main, aux, log, workload): aux is the
     auxiliary thread still alive after the last turn (or None); log has one
-    record per turn."""
+    record per turn.  evict_chunk_pages > 0 evicts in chunks of that many
+    fresh pages (bounded transient pages)."""
     import torch
     w = wl.full_stack(turns=turns, turn_len=turn_len, prefix=prefix, num_layers=num_layers)
     rng = w._rng
@@ -126,7 +127,8 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
     pages = max_tok // 16 + w.aux_private // 16 + 8
     if store is None:
         store = _sq.Store(num_layers, 32, 8, 128, num_pages=pages + pages // 8 + 64, max_seqs=4,
-                          max_pages_per_seq=max_tok // 16 + 64, device=device)
+                          max_pages_per_seq=max_tok // 16 + 64, device=device,
+                          evict_chunk_pages=evict_chunk_pages)
     main = store.seq_create()
     k, v = full_stack_inputs(w, -1, device)
     store.append(main, k, v)

@@ -41,6 +41,7 @@ class StoreConfig(C.Structure):
         ("max_seqs", C.c_int32), ("max_pages_per_seq", C.c_int32),
         ("k_pool", C.c_void_p), ("v_pool", C.c_void_p), ("pos_pool", C.c_void_p),
         ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64), ("flags", C.c_uint32),
+        ("evict_chunk_pages", C.c_int32),
     ]
 
 
@@ -172,9 +173,12 @@ class Store:
     """
 
     def __init__(self, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages, max_seqs,
-                 max_pages_per_seq, page_size=16, device="cuda", metadata_only=False):
+                 max_pages_per_seq, page_size=16, device="cuda", metadata_only=False,
+                 evict_chunk_pages=0):
         self.cfg = StoreConfig(num_layers, num_q_heads, num_kv_heads, head_dim, page_size,
                                num_pages, max_seqs, max_pages_per_seq)
+        self.cfg.evict_chunk_pages = evict_chunk_pages
+        self.evict_chunk_pages = evict_chunk_pages
         self.metadata_only = metadata_only
         self.num_layers, self.num_q_heads, self.num_kv_heads = num_layers, num_q_heads, num_kv_heads
         self.head_dim, self.page_size, self.num_pages = head_dim, page_size, num_pages

@@ -46,7 +46,7 @@ def oracle_model_for(store, with_data=True):
     return opg.PageModel(store.num_pages, store.page_size, store.max_seqs,
                          store.max_pages_per_seq, layers=store.num_layers,
                          kv_heads=store.num_kv_heads, head_dim=store.head_dim,
-                         with_data=with_data)
+                         with_data=with_data, evict_chunk_pages=store.evict_chunk_pages)
 
 
 def run_tiny(sq, device="cuda", modes=None, with_oracle=True):
@@ -139,11 +139,12 @@ class Twin:
     (with data), drawing the same seeded bf16 inputs for both."""
 
     def __init__(self, sq, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
-                 max_seqs, max_pages_per_seq, seed=0, device="cuda"):
+                 max_seqs, max_pages_per_seq, seed=0, device="cuda", evict_chunk_pages=0):
         self.sq = sq
         self.device = device
         self.store = sq.Store(num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
-                              max_seqs, max_pages_per_seq, device=device)
+                              max_seqs, max_pages_per_seq, device=device,
+                              evict_chunk_pages=evict_chunk_pages)
         self.model = oracle_model_for(self.store)
         self.rng = np.random.default_rng([2602, 900, seed])
         self.nl, self.hq, self.hkv, self.d = num_layers, num_q_heads, num_kv_heads, head_dim

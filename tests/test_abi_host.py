@@ -44,10 +44,10 @@ def test_library_exports_every_declared_symbol(sq):
     assert lib.sq_abi_version() == version
 
 
-def _store(sq, num_pages, page, max_seqs, max_pages):
+def _store(sq, num_pages, page, max_seqs, max_pages, chunk=0):
     return sq.Store(num_layers=2, num_q_heads=4, num_kv_heads=2, head_dim=8,
                     num_pages=num_pages, max_seqs=max_seqs, max_pages_per_seq=max_pages,
-                    page_size=page, metadata_only=True)
+                    page_size=page, metadata_only=True, evict_chunk_pages=chunk)
 
 
 def _compare(store, model):
@@ -83,12 +83,12 @@ def _both(store, model, sq, fn_store, fn_model):
 
 
 @pytest.mark.parametrize("page", [1, 2, 4, 16])
-@pytest.mark.parametrize("seed", [0, 1])
-def test_random_ops_match_oracle(sq, page, seed):
+@pytest.mark.parametrize("seed,chunk", [(0, 0), (1, 0), (2, 1), (3, 2), (4, 5)])
+def test_random_ops_match_oracle(sq, page, seed, chunk):
     rng = np.random.default_rng(100 + seed * 7 + page)
     num_pages, max_seqs, max_pages = 300 // page + 40, 5, 400 // page + 8
-    store = _store(sq, num_pages, page, max_seqs, max_pages)
-    model = pg.PageModel(num_pages, page, max_seqs, max_pages)
+    store = _store(sq, num_pages, page, max_seqs, max_pages, chunk)
+    model = pg.PageModel(num_pages, page, max_seqs, max_pages, evict_chunk_pages=chunk)
     cursor = 0
     h0, _ = _both(store, model, sq, store.seq_create, model.seq_create)
     for _ in range(250):
@@ -153,6 +153,38 @@ def test_hand_worked_page_tables(sq):
     assert s.page_table(a) == [5, 6, 2]
     assert s.positions(a).tolist() == [0, 6, 7, 8, 9, 10, 11, 12, 13]
     assert s.stats()["peak_pages"] == 7
+
+
+def test_chunked_eviction_page_tables_by_hand(sq):
+    """P = 2, 8 tokens: evicting tokens 1-2 takes fresh pages [4, 5, 6] in one
+    shot, [4, 0, 1] one page at a time (old pages reused as soon as their
+    tokens are moved) and [4, 5, 0] two at a time; peak 4 + chunk."""
+    for chunk, table in ((0, [4, 5, 6]), (1, [4, 0, 1]), (2, [4, 5, 0])):
+        s = _store(sq, 10, 2, 2, 8, chunk)
+        a = s.seq_create()
+        s.append(a, n=8)
+        s.span_mark(a, 0, 1, 3)
+        st = s.evict(a, [0])
+        assert s.page_table(a) == table
+        assert s.positions(a).tolist() == [0, 3, 4, 5, 6, 7]
+        assert s.stats()["peak_pages"] == 4 + (chunk or 3)
+        assert (st["pages_allocated"], st["pages_freed"]) == (3, 4)
+    # one free page: one-shot fails and changes nothing, chunks of one fit
+    for chunk in (0, 1):
+        s = _store(sq, 5, 2, 2, 8, chunk)
+        a = s.seq_create()
+        s.append(a, n=8)
+        s.span_mark(a, 0, 1, 3)
+        if chunk == 0:
+            with pytest.raises(sq.SqError) as ei:
+                s.evict(a, [0])
+            assert ei.value.code == sq.ERR_NO_PAGES
+            assert s.page_table(a) == [0, 1, 2, 3]
+        else:
+            s.evict(a, [0])
+            assert s.page_table(a) == [4, 0, 1]
+    with pytest.raises(sq.SqError):
+        _store(sq, 10, 2, 2, 8, -1)
 
 
 def test_error_paths_leave_state_unchanged(sq):

@@ -169,6 +169,37 @@ def test_compaction64k_evict_and_decode(sq):
     store.close()
 
 
+def test_compaction64k_chunked_in_place_recycling(sq):
+    """The 64K compaction evicted in chunks of 64 pages with no other branch
+    holding the pages: old pages are reused inside the call.  The compacted
+    view equals the kept input rows bit for bit, the page table equals the
+    oracle's chunked schedule, and at most 64 transient pages are live."""
+    import torch
+    from oracle import pages as opg
+    from paper_2602_22603_amd import drivers
+    store, base, w, k, v = drivers.build_compaction64k(evict_chunk_pages=64)
+    L = w.length
+    before = store.stats()["live_pages"]
+    store.evict(base, w.evict_ids)
+    spans = [w.spans[c] for c in w.evict_ids]
+    keep, _dst, _src, n_kept, _first = oev.plan(L, spans)
+    model = opg.PageModel(store.num_pages, 16, store.max_seqs, store.max_pages_per_seq,
+                          evict_chunk_pages=64)
+    h = model.seq_create()
+    model.append(h, L)
+    for c, (s0, e0) in enumerate(w.spans):
+        model.span_mark(h, c, s0, e0)
+    model.evict(h, w.evict_ids)
+    assert store.page_table(base) == model.page_table(h)
+    assert store.stats()["peak_pages"] == model.peak_pages <= before + 64
+    keep_t = torch.from_numpy(keep.astype(bool)).to("cuda")
+    vk, vv, vp = sc.seq_view(store, base)
+    assert np.array_equal(vk[:, 0], wl.torch_bf16_to_f64(k[0][keep_t]))
+    assert np.array_equal(vv[:, 0], wl.torch_bf16_to_f64(v[0][keep_t]))
+    assert np.array_equal(vp, np.flatnonzero(keep))
+    store.close()
+
+
 def test_full_stack_sampled(sq):
     """36 layers, 16K prefix + 30 turns of 8K tokens with an auxiliary thread
     every 4 turns evicting >= 60% of the live tool tokens: positions against

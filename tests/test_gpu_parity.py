@@ -98,8 +98,9 @@ def test_random_shapes_with_forks(sq, nl, hq, hkv, d):
             assert e <= TOL, (m, e)
 
 
-def test_eviction_random_bitexact(sq):
-    t = sc.Twin(sq, 2, 8, 2, 64, 900, 8, 200, seed=11)
+@pytest.mark.parametrize("chunk", [0, 1, 7])
+def test_eviction_random_bitexact(sq, chunk):
+    t = sc.Twin(sq, 2, 8, 2, 64, 900, 8, 200, seed=11, evict_chunk_pages=chunk)
     rng = np.random.default_rng(5)
     main = t.create()
     t.append(main, 1500)
@@ -145,6 +146,37 @@ def test_eviction_random_bitexact(sq):
     t.check_state()
     errs, _ = t.decode_errors([main, aux])
     assert max(errs.values()) <= TOL
+
+
+@pytest.mark.parametrize("chunk", [1, 4, 32])
+def test_chunked_eviction_recycles_pages_bitexact(sq, chunk):
+    """With no other branch holding the pages, chunked eviction reuses old
+    pages of the sequence inside the same call; the compacted K/V/pos must
+    still equal the oracle's bit for bit, and the peak stays within chunk."""
+    t = sc.Twin(sq, 3, 8, 2, 128, 420, 4, 400, seed=21 + chunk, evict_chunk_pages=chunk)
+    rng = np.random.default_rng(chunk)
+    main = t.create()
+    t.append(main, 3000)
+    aux = t.fork(main, 2995)
+    t.append(aux, 40)
+    t.release(aux)                        # Phase 1: the auxiliary thread is done
+    cursor = 0
+    for rnd in range(4):
+        length = t.model.info(main)["length"]
+        cuts = sorted(rng.choice(np.arange(length + 1), 12, replace=False).tolist())
+        ids = []
+        for i in range(0, 12, 2):
+            if t.try_mark(main, cursor, cuts[i], cuts[i + 1]):
+                ids.append(cursor)
+            cursor += 1
+        before = t.store.stats()["live_pages"]
+        t.evict(main, ids)
+        assert t.store.stats()["peak_pages"] == t.model.peak_pages
+        t.check_state()
+        errs, _ = t.decode_errors([main], layer=rnd % 3)
+        assert max(errs.values()) <= TOL, errs
+        t.append(main, int(rng.integers(100, 400)))
+        assert before > 0
 
 
 def test_all_keep_eviction_leaves_bytes(sq):
