@@ -153,9 +153,9 @@ def time_events(torch, fn, reps, flush=None):
     return percentiles([a.elapsed_time(b) for a, b in ev])
 
 
-def evict_leg(sq, torch, wl, reps=8):
+def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True):
     from paper_2602_22603_amd import drivers
-    store, base, w, k, v = drivers.build_compaction64k()
+    store, base, w, k, v = drivers.build_compaction64k(evict_chunk_pages=chunk)
     L = w.length
     del k, v
     torch.cuda.synchronize()
@@ -178,6 +178,13 @@ def evict_leg(sq, torch, wl, reps=8):
     gather_ms = prof["evict_gather_ms"] / max(1, prof["evict_gather_launches"])
     scan_ms = prof["evict_scan_ms"] / max(1, prof["evict_scan_launches"])
     moved = 2 * stats["bytes_moved"]  # read + write
+    if not decode:
+        info = dict(evict_chunk_pages=chunk, gather_launches_per_call=prof["evict_gather_launches"] // reps,
+                    gather_ms_per_call=prof["evict_gather_ms"] / reps,
+                    evict_wall_ms_median=sorted(walls)[len(walls) // 2] * 1e3,
+                    evict_gbps_wall=2 * stats["bytes_moved"] / (sorted(walls)[len(walls) // 2]) / 1e9)
+        store.close()
+        return info
     # decode on the compacted cache vs the full cache (batch 1)
     q = wl.device_normal_bf16((1, 32, 128), 77, "cuda")
     out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
@@ -298,19 +305,21 @@ def extend_leg(sq, torch, wl, reps=10):
 
 def fullstack_leg(sq, torch):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
-    turns; with and without eviction: peak KV bytes and the decode step
+    turns; with one-shot eviction, with eviction in 64-page chunks (bounded
+    transient pages) and without eviction: peak KV bytes and the decode step
     (all 36 layers) at each turn's end."""
     from paper_2602_22603_amd import drivers
     page_bytes = 36 * 8 * 16 * 128 * 2 * 2
     res = {}
-    for ev in (True, False):
-        store, main, aux, log, w = drivers.run_full_stack(evict=ev)
+    for name, ev, chunk in (("with_eviction", True, 0), ("with_chunked_eviction", True, 64),
+                            ("without_eviction", False, 0)):
+        store, main, aux, log, w = drivers.run_full_stack(evict=ev, evict_chunk_pages=chunk)
         st = store.stats()
         final = log[-1]
         dec = [r["decode_ms"] for r in log]
         ev_ms = [r["evict_ms"] for r in log if "evict_ms" in r]
         moved = sum(r["evict"]["bytes_moved"] for r in log if "evict" in r)
-        res["with_eviction" if ev else "without_eviction"] = dict(
+        res[name] = dict(
             peak_kv_bytes=st["peak_pages"] * page_bytes, final_tokens=final["length"],
             decode_ms_final_step=round(final["decode_ms"], 3),
             decode_gbps_final_step=round(final["kv_bytes"] / (final["decode_ms"] * 1e-3) / 1e9, 1),
@@ -322,6 +331,8 @@ def fullstack_leg(sq, torch):
         torch.cuda.empty_cache()
     a, b = res["with_eviction"], res["without_eviction"]
     res["peak_kv_reduction"] = round(1 - a["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
+    res["peak_kv_reduction_chunked"] = round(
+        1 - res["with_chunked_eviction"]["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
     res["kv_read_reduction"] = round(1 - a["kv_bytes_read_over_turns"] / b["kv_bytes_read_over_turns"], 4)
     return res
 
@@ -479,6 +490,8 @@ def main():
     if "evict" in legs:
         log("eviction leg (64K compaction) ...")
         evict = evict_leg(sq, torch, wl)
+        torch.cuda.empty_cache()
+        evict["chunked_256_pages"] = evict_leg(sq, torch, wl, chunk=256, decode=False)
     if "copy" in legs:
         log("calibration copy: 1 GiB device-to-device ...")
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)
