@@ -206,10 +206,12 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
   for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
     for (int cg = 0; cg < 2; ++cg) st[tt][cg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+  // k chunks outermost: the 8 accumulators of a block are 8 independent
+  // chains, so consecutive MFMAs never wait on each other's result
 #pragma unroll
-  for (int tt = 0; tt < 4; ++tt)
+  for (int kc = 0; kc < NKC; ++kc)
 #pragma unroll
-    for (int kc = 0; kc < NKC; ++kc) {
+    for (int tt = 0; tt < 4; ++tt) {
       const int row = tile_key(tt, n);
       const bf16x8_t ka = __builtin_bit_cast(
           bf16x8_t, *reinterpret_cast<const uint4 *>(sk + row * D + 8 * k_phys<D>(row, 4 * kc + kg)));
@@ -267,17 +269,25 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
       phi[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
       plo[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
     }
+    // all hi products, then all lo: the two MFMAs into one accumulator are
+    // 2 * NDT instructions apart
+    bf16x8_t va[NDT];
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt) {
       const int d = 16 * dt + n;
-      const bf16x8_t va = __builtin_bit_cast(
+      va[dt] = __builtin_bit_cast(
           bf16x8_t, *reinterpret_cast<const uint4 *>(sv + d * BK + 8 * v_phys(d, 4 * c2 + kg)));
-#pragma unroll
-      for (int cg = 0; cg < 2; ++cg) {
-        acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, phi[cg], acc[dt][cg], 0, 0, 0);
-        acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va, plo[cg], acc[dt][cg], 0, 0, 0);
-      }
     }
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int cg = 0; cg < 2; ++cg)
+        acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[dt], phi[cg], acc[dt][cg], 0, 0, 0);
+#pragma unroll
+    for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+      for (int cg = 0; cg < 2; ++cg)
+        acc[dt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(va[dt], plo[cg], acc[dt][cg], 0, 0, 0);
   }
 }
 
