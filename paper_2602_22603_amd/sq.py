@@ -228,6 +228,37 @@ class Store:
     def __exit__(self, *exc):
         self.close()
 
+    # -- argument checks (the C ABI takes raw pointers and trusts the sizes) -----
+    def _tensor(self, t, shape, dtype, what):
+        """t must be a contiguous tensor of exactly this shape and dtype on the
+        store's device; returns its pointer."""
+        import torch
+        if not isinstance(t, torch.Tensor):
+            raise SqError(ERR_INVALID, f"{what} must be a torch tensor")
+        if t.dtype != dtype:
+            raise SqError(ERR_INVALID, f"{what} must be {dtype}, got {t.dtype}")
+        if tuple(t.shape) != tuple(shape):
+            raise SqError(ERR_INVALID, f"{what} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+        if not t.is_contiguous():
+            raise SqError(ERR_INVALID, f"{what} must be contiguous")
+        if t.device != self.k_pool.device:
+            raise SqError(ERR_INVALID, f"{what} must be on {self.k_pool.device}, got {t.device}")
+        return _ptr(t)
+
+    def _kv_ptrs(self, k_new, v_new, n):
+        import torch
+        if self.metadata_only:
+            return _ptr(None), _ptr(None)
+        shape = (self.num_layers, n, self.num_kv_heads, self.head_dim)
+        return (self._tensor(k_new, shape, torch.bfloat16, "k_new"),
+                self._tensor(v_new, shape, torch.bfloat16, "v_new"))
+
+    def _qo_ptrs(self, q, out, rows):
+        import torch
+        shape = (rows, self.num_q_heads, self.head_dim)
+        return (self._tensor(q, shape, torch.bfloat16, "q"),
+                self._tensor(out, shape, torch.float32, "out"))
+
     # -- sequences --------------------------------------------------------------
     def seq_create(self):
         out = C.c_int32()
@@ -238,14 +269,16 @@ class Store:
         """Append tokens; k_new, v_new: bf16 [NL, n, Hkv, D] on the device."""
         if n is None:
             n = int(k_new.shape[1])
+        kp, vp = self._kv_ptrs(k_new, v_new, n)
         st = C.c_void_p(0) if self.metadata_only else _stream(stream)
-        _check(lib().sq_append(self._handle, seq, n, _ptr(k_new), _ptr(v_new), st))
+        _check(lib().sq_append(self._handle, seq, n, kp, vp, st))
 
     def append_batch(self, seqs, k_new=None, v_new=None, stream=None):
         """One token per sequence; k_new, v_new: bf16 [NL, B, Hkv, D]."""
+        seqs = list(seqs)
+        kp, vp = self._kv_ptrs(k_new, v_new, len(seqs))
         st = C.c_void_p(0) if self.metadata_only else _stream(stream)
-        _check(lib().sq_append_batch(self._handle, _i32_array(seqs), len(seqs), _ptr(k_new),
-                                     _ptr(v_new), st))
+        _check(lib().sq_append_batch(self._handle, _i32_array(seqs), len(seqs), kp, vp, st))
 
     def span_mark(self, seq, cursor, start, end):
         _check(lib().sq_span_mark(self._handle, seq, cursor, start, end))
@@ -274,8 +307,10 @@ class Store:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
         if scale is None:
             scale = 1.0 / float(self.head_dim) ** 0.5
-        _check(lib().sq_decode_attn(self._handle, layer, _i32_array(seqs), len(seqs), _ptr(q),
-                                    _ptr(out), float(scale), mode, _stream(stream)))
+        seqs = list(seqs)
+        qp, op = (_ptr(q), _ptr(out)) if self.metadata_only else self._qo_ptrs(q, out, len(seqs))
+        _check(lib().sq_decode_attn(self._handle, layer, _i32_array(seqs), len(seqs), qp, op,
+                                    float(scale), mode, _stream(stream)))
         return out
 
     def extend(self, layer, seq, q, out=None, scale=None, stream=None):
@@ -286,8 +321,10 @@ class Store:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
         if scale is None:
             scale = 1.0 / float(self.head_dim) ** 0.5
-        _check(lib().sq_extend_attn(self._handle, layer, seq, int(q.shape[0]), _ptr(q), _ptr(out),
-                                    float(scale), _stream(stream)))
+        n = int(q.shape[0])
+        qp, op = (_ptr(q), _ptr(out)) if self.metadata_only else self._qo_ptrs(q, out, n)
+        _check(lib().sq_extend_attn(self._handle, layer, seq, n, qp, op, float(scale),
+                                    _stream(stream)))
         return out
 
     def plan_info(self, seqs, mode=ATTN_AUTO):

@@ -146,3 +146,29 @@ def test_later_layers(sq):
     t.append(b, 30)
     for layer in (3, 1):
         _check(t, [a, b], layer=layer)
+
+
+def test_binding_rejects_bad_tensors(sq):
+    """The C ABI trusts pointer sizes, so the binding checks shape, dtype,
+    contiguity and device before any call; nothing changes on a rejection."""
+    import torch
+    s = sq.Store(1, 8, 2, 64, 64, 4, 16, device="cuda")
+    a = s.seq_create()
+    k = torch.zeros((1, 5, 2, 64), dtype=torch.bfloat16, device="cuda")
+    bad_k = [k.float(), k[:, :4], k.transpose(2, 3).contiguous().transpose(2, 3), k.cpu(),
+             torch.zeros((1, 5, 2, 65), dtype=torch.bfloat16, device="cuda")]
+    for kb in bad_k:
+        with pytest.raises(sq.SqError) as ei:
+            s.append(a, kb, k, n=5)
+        assert ei.value.code == sq.ERR_INVALID
+    assert s.seq_info(a)["length"] == 0 and s.stats()["live_pages"] == 0
+    s.append(a, k, k)
+    q = torch.zeros((1, 8, 64), dtype=torch.bfloat16, device="cuda")
+    for qb, ob in [(q.float(), None), (q[:, :4], None), (q, torch.zeros((1, 8, 64), device="cuda").half()),
+                   (q, torch.zeros((1, 8, 64), device="cuda")[:, ::2]), (q.cpu(), None)]:
+        with pytest.raises(sq.SqError):
+            s.decode(0, [a], qb, out=ob if ob is not None else torch.zeros((1, 8, 64), device="cuda"))
+    with pytest.raises(sq.SqError):
+        s.extend(0, a, torch.zeros((2, 8, 64), dtype=torch.float32, device="cuda"))
+    assert s.stats()["decode_calls"] == 0 and s.stats()["extend_calls"] == 0
+    s.close()
