@@ -295,6 +295,23 @@ def extend_leg(sq, torch, wl, reps=10):
                          kernel_ms=round(kern_ms, 4), useful_tflops=round(tflops, 1),
                          frac_of_bf16_peak=round(tflops / BF16_PEAK_TFLOPS, 4),
                          tokens_per_s=round(n / (kern_ms * 1e-3), 1))
+    # an auxiliary thread's 512-token prompt over the compacted context: a
+    # short chunk, so the key range is split over several workgroups
+    aux = store.fork(base, store.seq_info(base)["length"])
+    ka = wl.device_normal_bf16((1, 512, 8, 128), 94, "cuda")
+    store.append(aux, ka, ka)
+    qa = wl.device_normal_bf16((512, 32, 128), 95, "cuda")
+    oa = torch.empty((512, 32, 128), dtype=torch.float32, device="cuda")
+    L = store.seq_info(aux)["length"]
+    step = lambda: store.extend(0, aux, qa, out=oa)
+    for _ in range(2):
+        step()
+    pct = time_events(torch, step, reps)
+    pairs = 512 * (L - 512) + 512 * 513 // 2
+    tf = 32 * 4 * 128 * pairs / (pct["median"] * 1e-3) / 1e12
+    res["aux_prompt_512"] = dict(prefix_tokens=L - 512, chunk_tokens=512, call_ms=pct,
+                                 useful_tflops=round(tf, 1),
+                                 frac_of_bf16_peak=round(tf / BF16_PEAK_TFLOPS, 4))
     res["workload"] = ("8192-token chunk after the 64K context's tool spans were evicted "
                        f"(>= 65%), vs the uncompacted 64K context; 1 layer, 32q/8kv, 128; "
                        f"peak {BF16_PEAK_TFLOPS:.0f} TFLOP/s dense bf16")

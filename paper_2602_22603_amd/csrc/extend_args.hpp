@@ -29,10 +29,21 @@ struct ExtendArgs {
   int32_t hkv;
   int32_t n_qblocks;  // ceil(n / (kExtRows / G))
   float scale_log2;
+  // Split of the key range (chunks too short to fill the GPU): each (query
+  // block, KV head) runs n_split workgroups over split_blocks key blocks
+  // each and writes partial (m, l, acc) rows; k_extend_merge combines them.
+  // n_split == 1: the workgroup writes out directly.
+  int32_t n_split;
+  int32_t split_blocks;
+  float *part_m;      // [slots][kExtRows] (log2 units), slot = (qb * Hkv + g) * n_split + s
+  float *part_l;      // [slots][kExtRows]
+  float *part_acc;    // [slots][kExtRows][D]
 };
 
 static_assert(sizeof(ExtendArgs) < 4096, "extend kernel arguments too large");
 
 hipError_t launch_extend(int d, int group, const ExtendArgs &a, hipStream_t s);
+// Partial rows of the split key range -> out (no-op when n_split == 1).
+hipError_t launch_extend_merge(int d, int group, const ExtendArgs &a, hipStream_t s);
 
 } // namespace sq

@@ -306,7 +306,9 @@ k_extend(ExtendArgs a) {
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6); // uniform: the DMA destination is M0
   const int n = lane & 15, kg = lane >> 4;
   const int g = blockIdx.x % a.hkv;
-  const int qb = a.n_qblocks - 1 - (int)(blockIdx.x / a.hkv);
+  const int rest = blockIdx.x / a.hkv;
+  const int sp = rest % a.n_split; // key-range split
+  const int qb = a.n_qblocks - 1 - rest / a.n_split;
   const int j0 = qb * TQ;
   const int base = a.L - a.n; // logical index of new token 0
 
@@ -329,8 +331,9 @@ k_extend(ExtendArgs a) {
       qf[cg][kc] = __builtin_bit_cast(bf16x8_t, w);
     }
   }
-  const int kend = min(a.L, base + j0 + TQ); // keys this workgroup needs
-  const int nblk = (kend + BK - 1) / BK;
+  const int kend = min(a.L, base + j0 + TQ); // keys this query block needs
+  const int b_lo = sp * a.split_blocks;      // this workgroup's blocks [b_lo, b_hi)
+  const int b_hi = min((kend + BK - 1) / BK, b_lo + a.split_blocks);
   const int mask_from = base + j0;           // keys above this need the causal test
 
   f32x4_t acc[NDT][2];
@@ -343,10 +346,12 @@ k_extend(ExtendArgs a) {
   const uint16_t *kbase = a.k + (int64_t)g * a.head_stride;
   const uint16_t *vbase = a.v + (int64_t)g * a.head_stride;
   int32_t ids[4];
-  block_ids(ids, a, 0);
-  ext_dma<D>(sk[0], sv[0], a, kbase, vbase, ids, wave, lane);
-  block_ids(ids, a, 1);
-  for (int b = 0; b < nblk; ++b) {
+  if (b_lo < b_hi) {
+    block_ids(ids, a, b_lo);
+    ext_dma<D>(sk[b_lo & 1], sv[b_lo & 1], a, kbase, vbase, ids, wave, lane);
+    block_ids(ids, a, b_lo + 1);
+  }
+  for (int b = b_lo; b < b_hi; ++b) {
     // block b has landed (every wave's copies) and every wave is done with
     // block b - 1, whose buffer the next copy overwrites
     __builtin_amdgcn_s_waitcnt(0);
@@ -355,7 +360,7 @@ k_extend(ExtendArgs a) {
       ext_zero_tail<D>(sv[b & 1], b, a.L, tid);
       __syncthreads();
     }
-    if (b + 1 < nblk) {
+    if (b + 1 < b_hi) {
       ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, ids, wave, lane);
       block_ids(ids, a, b + 2);
     }
@@ -363,6 +368,27 @@ k_extend(ExtendArgs a) {
                  lim, acc, m_run, l_run);
   }
 
+  if (a.n_split > 1) {
+    // partial rows (a split may see no key of some rows: m = -inf, l = 0)
+    const int64_t slot = ((int64_t)qb * a.hkv + g) * a.n_split + sp;
+#pragma unroll
+    for (int cg = 0; cg < 2; ++cg) {
+      float l = sum_xrow16(l_run[cg]);
+      l = sum_xrow32(l);
+      if (!live[cg]) continue;
+      const int64_t row = slot * kExtRows + 32 * wave + 16 * cg + n;
+      if (kg == 0) {
+        a.part_m[row] = m_run[cg];
+        a.part_l[row] = l;
+      }
+      float *pp = a.part_acc + row * D + 4 * kg;
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+        *reinterpret_cast<float4 *>(pp + 16 * dt) =
+            make_float4(acc[dt][cg][0], acc[dt][cg][1], acc[dt][cg][2], acc[dt][cg][3]);
+    }
+    return;
+  }
 #pragma unroll
   for (int cg = 0; cg < 2; ++cg) {
     float l = sum_xrow16(l_run[cg]);
@@ -378,8 +404,61 @@ k_extend(ExtendArgs a) {
   }
 }
 
+// Merge of the split key range: one wave per (new token j, query head h),
+// lanes over channels.  Its partials are row (j % TQ) * G + h % G of the
+// n_split slots of (query block j / TQ, KV head h / G):
+//   M = max m_s;  out = sum 2^(m_s - M) acc_s / sum 2^(m_s - M) l_s.
+template <int D, int G>
+__global__ __launch_bounds__(256) void k_extend_merge(ExtendArgs a) {
+  constexpr int DPT = D / 64;
+  constexpr int TQ = kExtRows / G;
+  constexpr int U = 8;
+  const int lane = threadIdx.x & 63;
+  const int64_t r = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6); // (j, h) row
+  if (r >= (int64_t)a.n * a.hq) return;
+  const int j = (int)(r / a.hq), h = (int)(r % a.hq);
+  const int g = h / G;
+  const int64_t slot0 = ((int64_t)(j / TQ) * a.hkv + g) * a.n_split;
+  const int col = (j % TQ) * G + h % G;
+  const int S = a.n_split;
+  float mine = kNegInf, lmine = 0.f;
+  if (lane < S) {
+    mine = a.part_m[(slot0 + lane) * kExtRows + col];
+    lmine = a.part_l[(slot0 + lane) * kExtRows + col];
+  }
+  float big = mine;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) big = fmaxf(big, __shfl_xor(big, o));
+  const float w = (lane < S && big != kNegInf) ? exp2_fast(mine - big) : 0.f;
+  float den = w * lmine;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o);
+  float num[DPT];
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) num[q] = 0.f;
+  for (int s0 = 0; s0 < S; s0 += U) {
+    float x[U][DPT];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int sidx = min(s0 + u, S - 1);
+      const float *p = a.part_acc + ((slot0 + sidx) * kExtRows + col) * D + lane * DPT;
+#pragma unroll
+      for (int q = 0; q < DPT; ++q) x[u][q] = p[q];
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float wu = s0 + u < S ? __shfl(w, s0 + u) : 0.f;
+#pragma unroll
+      for (int q = 0; q < DPT; ++q) num[q] = fmaf(wu, x[u][q], num[q]);
+    }
+  }
+  float *op = a.out + r * D + lane * DPT;
+#pragma unroll
+  for (int q = 0; q < DPT; ++q) op[q] = num[q] / den;
+}
+
 template <int D> hipError_t extend_dispatch(int group, const ExtendArgs &a, hipStream_t s) {
-  const dim3 grid((unsigned)a.n_qblocks * (unsigned)a.hkv), block(kThreads);
+  const dim3 grid((unsigned)a.n_qblocks * (unsigned)a.hkv * (unsigned)a.n_split), block(kThreads);
   switch (group) {
   case 1: hipLaunchKernelGGL((k_extend<D, 1>), grid, block, 0, s, a); break;
   case 2: hipLaunchKernelGGL((k_extend<D, 2>), grid, block, 0, s, a); break;
@@ -391,6 +470,26 @@ template <int D> hipError_t extend_dispatch(int group, const ExtendArgs &a, hipS
 }
 
 } // namespace
+
+template <int D> hipError_t extend_merge_dispatch(int group, const ExtendArgs &a, hipStream_t s) {
+  const int64_t rows = (int64_t)a.n * a.hq;
+  const dim3 grid((unsigned)((rows + 3) / 4)), block(256);
+  switch (group) {
+  case 1: hipLaunchKernelGGL((k_extend_merge<D, 1>), grid, block, 0, s, a); break;
+  case 2: hipLaunchKernelGGL((k_extend_merge<D, 2>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_extend_merge<D, 4>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_extend_merge<D, 8>), grid, block, 0, s, a); break;
+  default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_extend_merge(int d, int group, const ExtendArgs &a, hipStream_t s) {
+  if (a.n <= 0 || a.n_split <= 1) return hipSuccess;
+  if (d == 128) return extend_merge_dispatch<128>(group, a, s);
+  if (d == 64) return extend_merge_dispatch<64>(group, a, s);
+  return hipErrorInvalidValue;
+}
 
 hipError_t launch_extend(int d, int group, const ExtendArgs &a, hipStream_t s) {
   if (a.n <= 0) return hipSuccess;

@@ -1197,9 +1197,29 @@ sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, 
   const int tq = sq::kExtRows / s->G;
   a.n_qblocks = (n_new + tq - 1) / tq;
   a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  // A chunk too short to give every CU two rounds of workgroups splits the
+  // key range of each query block (at least 4 blocks of 64 keys per split)
+  // and merges the partial rows in a second launch.
+  const int64_t key_blocks = (sqn->length + sq::kExtKeys - 1) / sq::kExtKeys; // the last query block's
+  const int64_t base_wg = (int64_t)a.n_qblocks * a.hkv;
+  const int64_t target = 4LL * s->cus;
+  int64_t split = 1;
+  if (base_wg < target) {
+    split = (target + base_wg - 1) / base_wg;
+    split = std::min<int64_t>(split, std::max<int64_t>(1, key_blocks / 4));
+    split = std::min<int64_t>(split, 64);
+    split = std::min<int64_t>(split, (int64_t)sq::kMaxItems * sq::kRows / sq::kExtRows / base_wg);
+    split = std::max<int64_t>(split, 1);
+  }
+  a.n_split = (int32_t)split;
+  a.split_blocks = (int32_t)((key_blocks + split - 1) / split);
+  a.part_m = s->part_m;
+  a.part_l = s->part_l;
+  a.part_acc = s->part_acc;
   ProfPair pp;
   const bool on = s->prof_begin(strm, &pp, kProfExtend);
   hipError_t e = sq::launch_extend(s->D, s->G, a, strm);
+  if (e == hipSuccess) e = sq::launch_extend_merge(s->D, s->G, a, strm);
   s->prof_end(strm, &pp, on);
   if (e != hipSuccess) return hip_fail(e, "extend kernel");
   ++s->st.extend_calls;

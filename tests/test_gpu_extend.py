@@ -108,6 +108,27 @@ def test_extend_several_query_blocks(sq, hq, hkv, d, prefix, n):
     assert err <= TOL
 
 
+@pytest.mark.parametrize("hq,hkv,d,prefix,n", [(32, 8, 128, 20000, 1), (32, 8, 128, 20000, 7),
+                                                (32, 8, 128, 20000, 512), (16, 2, 64, 300, 1000),
+                                                (8, 8, 128, 5000, 130)])
+def test_extend_split_key_range(sq, hq, hkv, d, prefix, n):
+    """Short chunks over long prefixes split each query block's key range
+    over several workgroups and merge the partial rows (an auxiliary
+    thread's prompt is such a chunk); with a long chunk over a short prefix
+    the first query blocks leave later splits empty."""
+    s = _store(sq, hq, hkv, d, prefix + n)
+    a = s.seq_create()
+    _append(s, a, prefix, 91)
+    _append(s, a, n, 93)
+    if prefix + n > 5000:
+        pairs = [(j, g) for j in sorted({0, n // 2, n - 1}) for g in (0, hkv - 1)]
+        err = _extend_error(s, a, n, 97, pairs=pairs)
+    else:
+        err = _extend_error(s, a, n, 97)
+    print(f"extend split hq={hq} d={d} prefix={prefix} n={n}: max abs err {err:.2e}")
+    assert err <= TOL
+
+
 def test_extend_whole_sequence_prefill(sq):
     """n = L: the first token sees only itself, so its rows equal its V (to
     fp32 rounding: its weight is 2^r with r the rounding error of the scaled
