@@ -323,14 +323,16 @@ def extend_leg(sq, torch, wl, reps=10):
 def fullstack_leg(sq, torch):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
     turns; with one-shot eviction, with eviction in 64-page chunks (bounded
-    transient pages) and without eviction: peak KV bytes and the decode step
-    (all 36 layers) at each turn's end."""
+    transient pages) and without eviction: peak KV bytes, the causal extend
+    attention of every appended chunk (one-shot and no eviction) and the
+    decode step (all 36 layers) at each turn's end."""
     from paper_2602_22603_amd import drivers
     page_bytes = 36 * 8 * 16 * 128 * 2 * 2
     res = {}
     for name, ev, chunk in (("with_eviction", True, 0), ("with_chunked_eviction", True, 64),
                             ("without_eviction", False, 0)):
-        store, main, aux, log, w = drivers.run_full_stack(evict=ev, evict_chunk_pages=chunk)
+        store, main, aux, log, w = drivers.run_full_stack(evict=ev, evict_chunk_pages=chunk,
+                                                          extend=chunk == 0)
         st = store.stats()
         final = log[-1]
         dec = [r["decode_ms"] for r in log]
@@ -343,11 +345,14 @@ def fullstack_leg(sq, torch):
             decode_ms_sum_over_turns=round(sum(dec), 2),
             kv_bytes_read_over_turns=sum(r["kv_bytes"] for r in log),
             evictions=len(ev_ms), evict_ms_total=round(sum(ev_ms), 3),
-            evict_gbps=round(2 * moved / (sum(ev_ms) * 1e-3) / 1e9, 1) if ev_ms else None)
+            evict_gbps=round(2 * moved / (sum(ev_ms) * 1e-3) / 1e9, 1) if ev_ms else None,
+            extend_ms_over_turns=round(sum(r.get("extend_ms", 0) + r.get("aux_extend_ms", 0)
+                                           for r in log), 1) if chunk == 0 else None)
         store.close()
         torch.cuda.empty_cache()
     a, b = res["with_eviction"], res["without_eviction"]
     res["peak_kv_reduction"] = round(1 - a["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
+    res["extend_time_reduction"] = round(1 - a["extend_ms_over_turns"] / b["extend_ms_over_turns"], 4)
     res["peak_kv_reduction_chunked"] = round(
         1 - res["with_chunked_eviction"]["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
     res["kv_read_reduction"] = round(1 - a["kv_bytes_read_over_turns"] / b["kv_bytes_read_over_turns"], 4)

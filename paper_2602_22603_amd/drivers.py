@@ -106,8 +106,23 @@ def full_stack_aux_inputs(w, turn, device="cuda"):
     return k, v
 
 
+def _extend_all_layers(store, seq, n, num_layers, seed, device):
+    """Causal extend attention of seq's last n tokens on every layer (one
+    query tensor reused across layers); returns the elapsed ms."""
+    import torch
+    q = wl.device_normal_bf16((n, store.num_q_heads, store.head_dim), seed, device)
+    out = torch.empty(q.shape, dtype=torch.float32, device=device)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for layer in range(num_layers):
+        store.extend(layer, seq, q, out=out)
+    torch.cuda.synchronize()
+    return (time.perf_counter() - t0) * 1e3
+
+
 def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers=36,
-                   device="cuda", decode=True, on_turn=None, store=None, evict_chunk_pages=0):
+                   device="cuda", decode=True, on_turn=None, store=None, evict_chunk_pages=0,
+                   extend=False):
     """Algorithm 1 over a synthetic task: a non-evictable prefix, then turns
     of reasoning plus one tool response each.  Phase 1 evicts the cursors the
     auxiliary thread named (when it has finished) and releases it; Phase 2
@@ -119,7 +134,9 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
     called after it.  Returns (store, main, aux, log, workload): aux is the
     auxiliary thread still alive after the last turn (or None); log has one
     record per turn.  evict_chunk_pages > 0 evicts in chunks of that many
-    fresh pages (bounded transient pages)."""
+    fresh pages (bounded transient pages).  With ``extend`` every appended
+    chunk (the auxiliary prompt, each turn) also runs its causal extend
+    attention over every layer, timed in the record."""
     import torch
     w = wl.full_stack(turns=turns, turn_len=turn_len, prefix=prefix, num_layers=num_layers)
     rng = w._rng
@@ -153,6 +170,9 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
             ka, va = full_stack_aux_inputs(w, t, device)
             store.append(aux, ka, va)
             del ka, va
+            if extend:
+                rec["aux_extend_ms"] = _extend_all_layers(store, aux, w.aux_private, num_layers,
+                                                          w.seed * 1000 + 6151 + t, device)
             live = store.spans(main)
             cur = sorted(live)
             tool_total = sum(e - s for s, e in live.values())
@@ -171,6 +191,9 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
         store.append(main, k, v)
         store.span_mark(main, t, start + r, start + turn_len)
         del k, v
+        if extend:
+            rec["extend_ms"] = _extend_all_layers(store, main, turn_len, num_layers,
+                                                  w.seed * 1000 + 4049 + t, device)
         seqs = [main] if aux is None else [main, aux]
         rec["length"] = store.seq_info(main)["length"]
         rec["batch"] = len(seqs)
