@@ -52,6 +52,10 @@ __host__ __device__ inline int32_t wg_of(int64_t x, int64_t total, int64_t n_wg)
   return (int32_t)(((x + 1) * n_wg - 1) / total);
 }
 
+// A batch entry attends to the segments on its path through the tree of
+// shared page runs: at most kMaxSrc (shared levels, then its own suffix).
+constexpr int kMaxSrc = 4;
+
 struct MergeArgs {
   float *out;  // [B][Hq][D]
   const float *part_m;
@@ -62,14 +66,13 @@ struct MergeArgs {
   int32_t hkv;
   int32_t pad;
   int32_t total[2], n_wg[2], slot_base[2]; // per launch (0: VALU, 1: MFMA)
-  // per batch entry: up to two segments it attends (launch, segment index,
-  // flattened start, pages, member index inside the segment)
+  // per batch entry: the segments it attends; meta packs the launch (bit 0),
+  // the segment index inside that launch (bits 1-8) and the member index
+  // inside the segment (bits 9-10)
   int32_t n_src[kMaxBatch];
-  int32_t src_launch[kMaxBatch][2];
-  int32_t src_seg[kMaxBatch][2];
-  int32_t src_start[kMaxBatch][2];
-  int32_t src_npages[kMaxBatch][2];
-  int32_t src_member[kMaxBatch][2];
+  int32_t src_meta[kMaxBatch][kMaxSrc];
+  int32_t src_start[kMaxBatch][kMaxSrc];  // flattened start of the segment's rows
+  int32_t src_npages[kMaxBatch][kMaxSrc];
 };
 
 static_assert(sizeof(DecodeArgs) < 4096, "decode kernel arguments too large");

@@ -599,26 +599,32 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
   const int g = h / a.group;
   const int hr = h - g * a.group;
   const int ns = a.n_src[b];
-  int n0 = 0, n1 = 0;
-  int32_t base0 = 0, base1 = 0;
-  for (int e = 0; e < ns; ++e) {
-    const int L = a.src_launch[b][e];
-    const int np = a.src_npages[b][e];
-    const int64_t R = (int64_t)a.src_start[b][e] + (int64_t)g * np; // row start
-    const int w_lo = wg_of(R, a.total[L], a.n_wg[L]);
-    const int w_hi = wg_of(R + np - 1, a.total[L], a.n_wg[L]);
-    const int r = a.src_seg[b][e] * a.hkv + g;
-    const int32_t base = (a.slot_base[L] + w_lo + r) * kRows + a.src_member[b][e] * a.group + hr;
-    if (e == 0) {
-      n0 = w_hi - w_lo + 1;
-      base0 = base;
-    } else {
-      n1 = w_hi - w_lo + 1;
-      base1 = base;
+  int cum[kMaxSrc + 1];
+  int32_t base[kMaxSrc];
+  cum[0] = 0;
+#pragma unroll
+  for (int e = 0; e < kMaxSrc; ++e) {
+    int cnt = 0;
+    base[e] = 0;
+    if (e < ns) {
+      const int meta = a.src_meta[b][e];
+      const int L = meta & 1, seg = (meta >> 1) & 0xff, member = (meta >> 9) & 3;
+      const int np = a.src_npages[b][e];
+      const int64_t R = (int64_t)a.src_start[b][e] + (int64_t)g * np; // row start
+      const int w_lo = wg_of(R, a.total[L], a.n_wg[L]);
+      const int w_hi = wg_of(R + np - 1, a.total[L], a.n_wg[L]);
+      cnt = w_hi - w_lo + 1;
+      base[e] = (a.slot_base[L] + w_lo + seg * a.hkv + g) * kRows + member * a.group + hr;
     }
+    cum[e + 1] = cum[e] + cnt;
   }
-  const int total = n0 + n1;
-  auto row_of = [&](int c) -> int32_t { return c < n0 ? base0 + c * kRows : base1 + (c - n0) * kRows; };
+  const int total = cum[kMaxSrc];
+  auto row_of = [&](int c) -> int32_t {
+    int e = 0;
+#pragma unroll
+    for (int k = 1; k < kMaxSrc; ++k) e += c >= cum[k];
+    return base[e] + (c - cum[e]) * kRows;
+  };
 
   float big_m = kNegInf;
   for (int c = tid; c < total; c += NT) big_m = fmaxf(big_m, a.part_m[row_of(c)]);

@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <functional>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -350,57 +351,8 @@ struct Plan {
 sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode, Plan *plan) {
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
   const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
-  std::vector<int> group_of(batch, -1);
-  std::vector<std::vector<int>> groups;
-  std::vector<int64_t> npre;
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
-  {
-    // Sequences whose page lists start with the same physical page share a
-    // prefix (the auxiliary branch aliases the main thread's pages).  Group
-    // them, at most max_mem per group, in batch order.
-    std::vector<std::pair<int32_t, int>> open; // (first page, group index)
-    for (int b = 0; b < batch; ++b) {
-      const Seq &q = s->seqs[seqs[b]];
-      if (q.length < s->P) continue; // no full page to share
-      const int32_t first = q.pages[0];
-      int gi = -1;
-      for (auto &o : open)
-        if (o.first == first && (int)groups[o.second].size() < max_mem) {
-          gi = o.second;
-          break;
-        }
-      if (gi < 0) {
-        for (auto &o : open)
-          if (o.first == first) plan->pages_reread = true; // a full group already reads it
-        gi = (int)groups.size();
-        groups.push_back({});
-        open.push_back({first, gi});
-      }
-      groups[gi].push_back(b);
-      group_of[b] = gi;
-    }
-    npre.assign(groups.size(), 0);
-    for (size_t gi = 0; gi < groups.size(); ++gi) {
-      auto &mem = groups[gi];
-      if (mem.size() < 2) {
-        for (int b : mem) group_of[b] = -1;
-        continue;
-      }
-      const Seq &lead = s->seqs[seqs[mem[0]]];
-      int64_t lcp = lead.length / s->P;
-      for (size_t j = 1; j < mem.size(); ++j) {
-        const Seq &o = s->seqs[seqs[mem[j]]];
-        int64_t k = 0;
-        const int64_t lim = std::min<int64_t>(lcp, o.length / s->P);
-        while (k < lim && o.pages[k] == lead.pages[k]) ++k;
-        lcp = k;
-      }
-      npre[gi] = lcp;
-      if (lcp > 0 && !grouping) plan->pages_reread = true; // per-sequence modes re-read them
-      if (lcp == 0 || !grouping)
-        for (int b : mem) group_of[b] = -1;
-    }
-  }
+  const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma);
 
   auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
                      const std::vector<int> &members) {
@@ -417,22 +369,74 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     ps.mfma = mfma;
     plan->segs.push_back(ps);
   };
+  auto full_pages = [&](int b) { return s->seqs[seqs[b]].length / s->P; };
+  auto page_at = [&](int b, int64_t i) { return s->seqs[seqs[b]].pages[i]; };
+  auto add_private = [&](int b, int64_t p0) {
+    const int64_t rest = s->seqs[seqs[b]].length - p0 * s->P;
+    if (rest > 0) add_seg(seqs[b], (int32_t)p0, rest, single_mfma, {b});
+  };
 
-  const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma);
-  std::vector<bool> done(groups.size(), false);
-  for (int b = 0; b < batch; ++b) {
-    const Seq &q = s->seqs[seqs[b]];
-    plan->kv_bytes_logical += q.length * tok_bytes;
-    const int gi = group_of[b];
-    if (gi >= 0 && !done[gi]) {
-      done[gi] = true;
-      ++plan->n_groups;
-      const int lead = groups[gi][0];
-      add_seg(seqs[lead], 0, npre[gi] * s->P, true, groups[gi]);
-    }
-    const int64_t start_page = gi >= 0 ? npre[gi] : 0;
-    const int64_t rest = q.length - start_page * s->P;
-    if (rest > 0) add_seg(seqs[b], (int32_t)start_page, rest, single_mfma, {b});
+  // Sequences whose page lists agree on a run of physical pages share that
+  // run (an auxiliary branch aliases its parent's pages, a branch of a
+  // branch aliases both).  The entries reaching page p0 together split by
+  // the id of their page p0; each part of two or more reads the run they
+  // all share once, on the multi-query tile (at most max_mem entries per
+  // tile, so a wider part is read once per tile), then splits again after
+  // it: a tree of shared runs, at most kMaxSrc - 1 deep, each entry's own
+  // suffix at the leaf.
+  std::function<void(const std::vector<int> &, int64_t, int)> node =
+      [&](const std::vector<int> &mem, int64_t p0, int depth) {
+        std::vector<std::pair<int32_t, std::vector<int>>> parts; // first-seen order
+        for (int b : mem) {
+          const int32_t key = full_pages(b) > p0 ? page_at(b, p0) : -1;
+          auto it = std::find_if(parts.begin(), parts.end(),
+                                 [&](const auto &pt) { return key >= 0 && pt.first == key; });
+          if (it == parts.end()) parts.push_back({key, {b}});
+          else it->second.push_back(b);
+        }
+        for (auto &pt : parts) {
+          const std::vector<int> &part = pt.second;
+          if (pt.first < 0 || part.size() < 2 || depth >= sq::kMaxSrc - 1) {
+            if (pt.first >= 0 && part.size() >= 2) plan->pages_reread = true; // too deep
+            for (int b : part) add_private(b, p0);
+            continue;
+          }
+          if ((int)part.size() > max_mem) plan->pages_reread = true;
+          for (size_t c0 = 0; c0 < part.size(); c0 += max_mem) {
+            const std::vector<int> tile(part.begin() + c0,
+                                        part.begin() + std::min(part.size(), c0 + max_mem));
+            if (tile.size() < 2) {
+              add_private(tile[0], p0);
+              continue;
+            }
+            int64_t p1 = p0 + 1; // they share page p0
+            for (;;) {
+              bool same = true;
+              for (int b : tile) same = same && full_pages(b) > p1 && page_at(b, p1) == page_at(tile[0], p1);
+              if (!same) break;
+              ++p1;
+            }
+            ++plan->n_groups;
+            add_seg(seqs[tile[0]], (int32_t)p0, (p1 - p0) * s->P, true, tile);
+            node(tile, p1, depth + 1);
+          }
+        }
+      };
+
+  for (int b = 0; b < batch; ++b) plan->kv_bytes_logical += s->seqs[seqs[b]].length * tok_bytes;
+  if (grouping) {
+    std::vector<int> all(batch);
+    for (int b = 0; b < batch; ++b) all[b] = b;
+    node(all, 0, 0);
+  } else {
+    // per-sequence tiles; pages two entries share are read twice
+    for (int b = 0; b < batch && !plan->pages_reread; ++b)
+      for (int c = b + 1; c < batch; ++c)
+        if (full_pages(b) > 0 && full_pages(c) > 0 && page_at(b, 0) == page_at(c, 0)) {
+          plan->pages_reread = true;
+          break;
+        }
+    for (int b = 0; b < batch; ++b) add_private(b, 0);
   }
 
   if ((int)plan->segs.size() > sq::kMaxSegs)
@@ -1131,11 +1135,9 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
     for (int j = 0; j < ps.seg.nmem; ++j) {
       const int b = ps.members[j];
       const int e = ma.n_src[b]++;
-      ma.src_launch[b][e] = ps.mfma ? 1 : 0;
-      ma.src_seg[b][e] = plan.seg_index[i];
+      ma.src_meta[b][e] = (ps.mfma ? 1 : 0) | plan.seg_index[i] << 1 | j << 9;
       ma.src_start[b][e] = ps.seg.start;
       ma.src_npages[b][e] = (ps.seg.ntok + s->P - 1) / s->P;
-      ma.src_member[b][e] = j;
     }
   }
   for (int pass = 0; pass < 2; ++pass) {

@@ -307,3 +307,37 @@ def test_decode_plan_after_eviction(sq):
     tok = 8 * 128 * 2 * 2
     assert info["n_groups"] == 1
     assert info["kv_bytes"] == (20 * 16 + (830 - 320) + (1000 - 320)) * tok
+
+
+def test_decode_plan_reads_a_tree_of_shared_runs_once(sq):
+    """M (1000 tokens); A forked from M at 640 (+200); B forked from A at
+    800 (+100); C forked from M at 960 (+20).  All four share pages [0, 40),
+    M and C share [40, 60), A and B share [40, 50): three shared runs, four
+    own suffixes, 1320 tokens read instead of 3720 (or 1800 with one level)."""
+    s = sq.Store(1, 8, 2, 128, num_pages=400, max_seqs=12, max_pages_per_seq=100,
+                 metadata_only=True)
+    m = s.seq_create()
+    s.append(m, n=1000)
+    a = s.fork(m, 640)
+    s.append(a, n=200)
+    b = s.fork(a, 800)
+    s.append(b, n=100)
+    c = s.fork(m, 960)
+    s.append(c, n=20)
+    tok = 2 * 128 * 2 * 2
+    for mode in (sq.ATTN_AUTO, sq.ATTN_SHARED_PREFIX):
+        info = s.plan_info([m, a, b, c], mode)
+        assert (info["n_segments"], info["n_groups"]) == (7, 3)
+        assert info["kv_bytes"] == 1320 * tok and info["kv_bytes_logical"] == 3720 * tok
+    info = s.plan_info([m, a, b, c], sq.ATTN_STREAM)
+    assert (info["n_segments"], info["n_groups"], info["kv_bytes"]) == (4, 0, 3720 * tok)
+    # a chain of six nested forks: more entries than one tile holds (4 for
+    # G = 4), so the root run is read once per tile: tile {m, c1, c2, c3}
+    # nests three runs, tile {c4, c5} one
+    chain = [m]
+    for i in range(5):
+        nxt = s.fork(chain[-1], s.seq_info(chain[-1])["length"])
+        s.append(nxt, n=40)
+        chain.append(nxt)
+    info = s.plan_info(chain, sq.ATTN_AUTO)
+    assert info["n_groups"] == 4 and info["kv_bytes"] < info["kv_bytes_logical"]

@@ -172,3 +172,32 @@ def test_binding_rejects_bad_tensors(sq):
         s.extend(0, a, torch.zeros((2, 8, 64), dtype=torch.float32, device="cuda"))
     assert s.stats()["decode_calls"] == 0 and s.stats()["extend_calls"] == 0
     s.close()
+
+
+@pytest.mark.parametrize("group", [1, 2, 4])
+def test_tree_of_forks(sq, group):
+    """Forks of forks at page-aligned and mid-page points: the shared-prefix
+    plan reads a tree of shared runs (up to three levels deep) once each and
+    merges up to four partial sources per entry."""
+    hkv = 2
+    t = sc.Twin(sq, 1, hkv * group, hkv, 128, 600, 12, 120, seed=80 + group)
+    m = t.create()
+    t.append(m, 1000)
+    a = t.fork(m, 640)
+    t.append(a, 200)
+    b = t.fork(a, 800)
+    t.append(b, 100)
+    c = t.fork(m, 960)
+    t.append(c, 20)
+    d = t.fork(b, 853)          # mid-page: its tail page is a copy
+    t.append(d, 33)
+    chain = [m]
+    for _ in range(3):
+        nxt = t.fork(chain[-1], t.model.info(chain[-1])["length"])
+        t.append(nxt, 32)
+        chain.append(nxt)
+    t.check_state()
+    for seqs in ([m, a, b, c], [d, b, a, m, c], chain, [m, a, b, c] + chain[1:]):
+        info = t.store.plan_info(seqs, sq.ATTN_AUTO)
+        assert info["kv_bytes"] < info["kv_bytes_logical"]
+        _check(t, seqs)
