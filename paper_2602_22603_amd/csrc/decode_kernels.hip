@@ -4,9 +4,10 @@
 // Decode attention is the memory-bound step of long agentic contexts (§1;
 // §3.4 "Compute and Memory Movement Cost").  One decode step of a batch of
 // main-thread and auxiliary-thread queries (§3.1 "Parallel Execution") is
-// split over work items (segment, KV head, chunk of pages), each producing
-// an unnormalised partial (m, l, acc) per query row; a merge kernel combines
-// the partials of every chunk a query attends to.
+// split over workgroups that each take an equal share of the launch's
+// (segment, KV head) page rows, writing an unnormalised partial (m, l, acc)
+// per query row for every row piece they cover; a merge kernel combines the
+// partials of every piece a query attends to.
 //
 //   k_decode_valu  one query sequence per item: K and V page tiles staged in
 //                  LDS, bf16 dot products on the VALU (v_dot2_f32_bf16), the
@@ -571,7 +572,8 @@ k_decode_mfma(DecodeArgs a) {
 
 // ===========================================================================
 // Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
-// Its partials are the pieces of at most two segments.  Every thread first
+// Its partials are the pieces of at most kMaxSrc segments (the shared runs on
+// its path through the tree of forks, then its own suffix).  Every thread first
 // loads the (m, l) of its partials and the block takes the global maximum M
 // of m; the weights w_c = 2^(m_c - M) and the row offsets go to LDS, and the
 // waves then accumulate sum w_c acc_c over disjoint partials, lanes over
