@@ -341,3 +341,50 @@ def test_decode_plan_reads_a_tree_of_shared_runs_once(sq):
         chain.append(nxt)
     info = s.plan_info(chain, sq.ATTN_AUTO)
     assert info["n_groups"] == 4 and info["kv_bytes"] < info["kv_bytes_logical"]
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_tree_plan_reads_every_distinct_page_once(sq, seed):
+    """Random forests of forks, appends and evictions (metadata only): for
+    any batch of at most four entries (one tile when G <= 4) the
+    shared-prefix plan reads each distinct page once; the count comes from
+    the page tables alone: P tokens per distinct full page plus each
+    entry's partial last page."""
+    rng = np.random.default_rng(1000 + seed)
+    P, tok = 16, 2 * 128 * 2 * 2
+    s = sq.Store(1, 8, 2, 128, num_pages=3000, max_seqs=16, max_pages_per_seq=400,
+                 metadata_only=True)
+    live = [s.seq_create()]
+    s.append(live[0], n=int(rng.integers(100, 2000)))
+    cursor = 0
+    for _ in range(40):
+        h = live[int(rng.integers(0, len(live)))]
+        op = rng.random()
+        L = s.seq_info(h)["length"]
+        if op < 0.35 and len(live) < 12:
+            live.append(s.fork(h, int(rng.integers(0, L + 1))))
+        elif op < 0.7:
+            s.append(h, n=int(rng.integers(1, 300)))
+        elif op < 0.85 and L > 2:
+            a0 = int(rng.integers(0, L - 1))
+            a1 = int(rng.integers(a0 + 1, L + 1))
+            try:
+                s.span_mark(h, cursor, a0, a1)
+                s.evict(h, [cursor])
+            except sq.SqError:
+                pass
+            cursor += 1
+        elif len(live) > 2:
+            s.release(h)
+            live.remove(h)
+        for _ in range(3):
+            k = int(rng.integers(1, min(4, len(live)) + 1))
+            batch = [live[i] for i in rng.choice(len(live), k, replace=False)]
+            full = set()
+            partial = 0
+            for b in batch:
+                L = s.seq_info(b)["length"]
+                full.update(s.page_table(b)[: L // P])
+                partial += L % P
+            info = s.plan_info(batch, sq.ATTN_AUTO)
+            assert info["kv_bytes"] == (len(full) * P + partial) * tok, (batch, info)
