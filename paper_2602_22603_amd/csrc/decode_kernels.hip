@@ -573,25 +573,22 @@ k_decode_mfma(DecodeArgs a) {
 // ===========================================================================
 // Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
 // Its partials are the pieces of at most kMaxSrc segments (the shared runs on
-// its path through the tree of forks, then its own suffix).  Every thread first
-// loads the (m, l) of its partials and the block takes the global maximum M
-// of m; the weights w_c = 2^(m_c - M) and the row offsets go to LDS, and the
-// waves then accumulate sum w_c acc_c over disjoint partials, lanes over
-// channels, with 16 row loads in flight per wave; LDS adds the waves' sums.
-// Latency, not bandwidth, bounds this kernel (a few hundred KB per launch),
-// so the point is to have every load of a round issued before the first
-// is used.
+// its path through the tree of forks, then its own suffix).  Wave w takes a
+// contiguous share of them, kMergeUnroll at a time: the acc rows (lanes over
+// channels) and the (m, l) pairs (lanes over partials) of a round are loaded
+// together, then folded into the wave's running (m_w, l_w, acc_w) with the
+// usual rescale.  The waves' states combine through LDS the same way.  One
+// round of global loads covers kMergeWaves * kMergeUnroll partials: latency,
+// not bandwidth, bounds this kernel.
 constexpr int kMergeWaves = 8;
-constexpr int kMergeChunk = 2048; // partials whose weights sit in LDS at once
 constexpr int kMergeUnroll = 16;
 
 template <int D>
 __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) {
   constexpr int DPT = D / 64;
-  constexpr int NT = 64 * kMergeWaves;
-  __shared__ float s_red[kMergeWaves];
-  __shared__ float s_w[kMergeChunk];
-  __shared__ int32_t s_off[kMergeChunk];
+  constexpr int U = kMergeUnroll;
+  __shared__ float s_m[kMergeWaves];
+  __shared__ float s_l[kMergeWaves];
   __shared__ float s_num[kMergeWaves][D];
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -628,69 +625,71 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
     return base[e] + (c - cum[e]) * kRows;
   };
 
-  float big_m = kNegInf;
-  for (int c = tid; c < total; c += NT) big_m = fmaxf(big_m, a.part_m[row_of(c)]);
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) big_m = fmaxf(big_m, __shfl_xor(big_m, o));
-  if (lane == 0) s_red[wave] = big_m;
-  __syncthreads();
-#pragma unroll
-  for (int w = 0; w < kMergeWaves; ++w) big_m = fmaxf(big_m, s_red[w]);
-  __syncthreads(); // s_red is reused for the denominators
-
+  const int per = (total + kMergeWaves - 1) / kMergeWaves;
+  const int cb = wave * per, ce = min(total, cb + per);
+  float m_w = kNegInf, l_w = 0.f;
   float num[DPT];
 #pragma unroll
-  for (int i = 0; i < DPT; ++i) num[i] = 0.f;
-  float den = 0.f;
-  if (big_m != kNegInf) {
-    for (int c0 = 0; c0 < total; c0 += kMergeChunk) {
-      const int nc = min(kMergeChunk, total - c0);
-      for (int c = tid; c < nc; c += NT) {
-        const int32_t row = row_of(c0 + c);
-        const float w = exp2_fast(a.part_m[row] - big_m); // empty partials: 2^-inf = 0
-        den = fmaf(w, a.part_l[row], den);
-        s_w[c] = w;
-        s_off[c] = row;
-      }
-      __syncthreads();
-      // wave w takes partials [w * per, (w + 1) * per) of the chunk
-      const int per = (nc + kMergeWaves - 1) / kMergeWaves;
-      const int cb = wave * per, ce = min(nc, cb + per);
-      for (int i = cb; i < ce; i += kMergeUnroll) {
-        float x[kMergeUnroll][DPT];
+  for (int q = 0; q < DPT; ++q) num[q] = 0.f;
+  for (int i = cb; i < ce; i += U) {
+    float x[U][DPT];
 #pragma unroll
-        for (int u = 0; u < kMergeUnroll; ++u) {
-          const int c = min(i + u, ce - 1); // repeats of the last row carry weight 0
-          const float *src = a.part_acc + (int64_t)s_off[c] * D + lane * DPT;
+    for (int u = 0; u < U; ++u) {
+      const float *src = a.part_acc + (int64_t)row_of(min(i + u, ce - 1)) * D + lane * DPT;
 #pragma unroll
-          for (int q = 0; q < DPT; ++q) x[u][q] = src[q];
-        }
-#pragma unroll
-        for (int u = 0; u < kMergeUnroll; ++u) {
-          const float w = i + u < ce ? s_w[i + u] : 0.f;
-#pragma unroll
-          for (int q = 0; q < DPT; ++q) num[q] = fmaf(w, x[u][q], num[q]);
-        }
-      }
-      __syncthreads(); // the next chunk overwrites s_w / s_off
+      for (int q = 0; q < DPT; ++q) x[u][q] = src[q];
     }
-  }
+    float mu = kNegInf, lu = 0.f;
+    if (lane < U && i + lane < ce) {
+      const int32_t row = row_of(i + lane);
+      mu = a.part_m[row];
+      lu = a.part_l[row];
+    }
+    float rmax = mu;
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o);
-  if (lane == 0) s_red[wave] = den;
+    for (int o = 32; o > 0; o >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, o));
+    const float m_new = fmaxf(m_w, rmax);
+    if (m_new == kNegInf) continue; // only empty partials so far
+    const float sc = exp2_fast(m_w - m_new); // 0 while m_w is -inf
+    const float wu_lane = exp2_fast(mu - m_new); // 0 for empty partials and idle lanes
+    float lsum = wu_lane * lu;
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) lsum += __shfl_xor(lsum, o);
+    l_w = l_w * sc + lsum;
+#pragma unroll
+    for (int q = 0; q < DPT; ++q) num[q] *= sc;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wu_lane), u));
+#pragma unroll
+      for (int q = 0; q < DPT; ++q) num[q] = fmaf(wu, x[u][q], num[q]);
+    }
+    m_w = m_new;
+  }
+  if (lane == 0) {
+    s_m[wave] = m_w;
+    s_l[wave] = l_w;
+  }
 #pragma unroll
   for (int q = 0; q < DPT; ++q) s_num[wave][lane * DPT + q] = num[q];
   __syncthreads();
   if (wave == 0) {
+    float mm = kNegInf;
+#pragma unroll
+    for (int w = 0; w < kMergeWaves; ++w) mm = fmaxf(mm, s_m[w]);
+    float sc[kMergeWaves];
     float dt = 0.f;
 #pragma unroll
-    for (int w = 0; w < kMergeWaves; ++w) dt += s_red[w];
+    for (int w = 0; w < kMergeWaves; ++w) {
+      sc[w] = mm == kNegInf ? 0.f : exp2_fast(s_m[w] - mm);
+      dt = fmaf(sc[w], s_l[w], dt);
+    }
     float *out = a.out + ((int64_t)b * a.hq + h) * D + lane * DPT;
 #pragma unroll
     for (int q = 0; q < DPT; ++q) {
       float nt = 0.f;
 #pragma unroll
-      for (int w = 0; w < kMergeWaves; ++w) nt += s_num[w][lane * DPT + q];
+      for (int w = 0; w < kMergeWaves; ++w) nt = fmaf(sc[w], s_num[w][lane * DPT + q], nt);
       out[q] = dt > 0.f ? nt / dt : 0.f;
     }
   }
