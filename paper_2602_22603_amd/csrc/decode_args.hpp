@@ -11,7 +11,11 @@ namespace sq {
 // A segment: `ntok` tokens read from page-table row `row` from page index
 // `page0` on, attended by `nmem` query sequences (batch indices packed as
 // bytes in `mem`).  Its Hkv rows (one per KV head g) occupy the flattened
-// page range [start + g * npages, start + (g + 1) * npages) of its launch.
+// page ranges [start + g * (npages + row_pad), ... + npages) of its launch;
+// each row is followed by row_pad flattened pages that map to nothing.  They
+// stand for the fixed start-up cost of a piece (its query, page-id and
+// first page loads), so that the even split gives a workgroup that covers
+// many short rows fewer pages.
 struct Seg {
   int32_t row;
   int32_t page0;
@@ -43,6 +47,7 @@ struct DecodeArgs {
   int32_t n_wg;        // workgroups of this launch
   int32_t slot_base;   // first partial slot of this launch
   int32_t nontemporal; // 1: every page is read once in this launch
+  int32_t row_pad;     // flattened pages after each row that map to nothing
   float scale_log2;    // scale * log2(e)
   Seg segs[kMaxSegs];
 };
@@ -65,7 +70,7 @@ struct MergeArgs {
   int32_t group; // G
   int32_t hkv;
   int32_t pad;
-  int32_t total[2], n_wg[2], slot_base[2]; // per launch (0: VALU, 1: MFMA)
+  int32_t total[2], n_wg[2], slot_base[2], row_pad[2]; // per launch (0: VALU, 1: MFMA)
   // per batch entry: the segments it attends; meta packs the launch (bit 0),
   // the segment index inside that launch (bits 1-8) and the member index
   // inside the segment (bits 9-10)

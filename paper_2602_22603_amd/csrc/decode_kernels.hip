@@ -121,26 +121,34 @@ struct ItemPos {
   int slot;     // partial slot
 };
 
-// The piece starting at flattened page x of workgroup w (range ends at xe);
-// advances x past it.
-__device__ inline ItemPos next_piece(const DecodeArgs &a, int w, int64_t &x, int64_t xe) {
-  int lo = 0, hi = a.n_segs - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (a.segs[mid].start <= x) lo = mid;
-    else hi = mid - 1;
+// The next piece of workgroup w's range [x, xe): the real pages of one row
+// from x on (skipping row padding); advances x past it.  False when the
+// range holds no more real pages.
+__device__ inline bool next_piece(const DecodeArgs &a, int w, int64_t &x, int64_t xe, ItemPos &ip) {
+  while (x < xe) {
+    int lo = 0, hi = a.n_segs - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (a.segs[mid].start <= x) lo = mid;
+      else hi = mid - 1;
+    }
+    ip.sg = a.segs[lo];
+    ip.npages = (ip.sg.ntok + P - 1) / P;
+    const int64_t rl = ip.npages + a.row_pad;
+    ip.g = (int)((x - ip.sg.start) / rl);
+    const int64_t rs = ip.sg.start + (int64_t)ip.g * rl;
+    if (x - rs >= ip.npages) { // in the row's padding
+      x = rs + rl;
+      continue;
+    }
+    const int64_t pe = min(xe, rs + ip.npages);
+    ip.pbeg = (int)(x - rs);
+    ip.pend = (int)(pe - rs);
+    ip.slot = a.slot_base + w + lo * a.hkv + ip.g;
+    x = pe;
+    return true;
   }
-  ItemPos ip;
-  ip.sg = a.segs[lo];
-  ip.npages = (ip.sg.ntok + P - 1) / P;
-  ip.g = (int)((x - ip.sg.start) / ip.npages);
-  const int64_t rs = ip.sg.start + (int64_t)ip.g * ip.npages;
-  const int64_t pe = min(xe, rs + ip.npages);
-  ip.pbeg = (int)(x - rs);
-  ip.pend = (int)(pe - rs);
-  ip.slot = a.slot_base + w + lo * a.hkv + ip.g;
-  x = pe;
-  return ip;
+  return false;
 }
 
 // ===========================================================================
@@ -171,8 +179,8 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
   const int lane = threadIdx.x;
   const int64_t x_end = (int64_t)(blockIdx.x + 1) * a.total / a.n_wg;
   int64_t x_pos = (int64_t)blockIdx.x * a.total / a.n_wg;
-  while (x_pos < x_end) {
-  const ItemPos ip = next_piece(a, blockIdx.x, x_pos, x_end);
+  ItemPos ip;
+  while (next_piece(a, blockIdx.x, x_pos, x_end, ip)) {
   const int b = ip.sg.mem & 0xff;
   const int g = ip.g;
   const int32_t *pt = a.pt + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
@@ -383,24 +391,49 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
 //   O^T output    O[row n][channel 16 jd + 4 kg + i]
 // P is split into bf16 hi + lo parts (two MFMAs per block) so the weights
 // keep ~16 bits; the running sum l uses the same hi + lo values.
-template <int D> struct MfmaFrag {
+template <int D> struct KFrag {
   uint4 k[D / 32];
+};
+template <int D> struct VFrag {
   uint2 v[D / 16];
 };
 
+// A buffer resource over one page of one KV head (the pools are read only
+// through these): a page that is not wanted gets num_records 0, so its loads
+// return zeros without touching memory and every loop iteration issues the
+// same loads - which keeps the hardware's in-order load counter waits exact.
+constexpr int kRsrcWord3 = 0x00020000;
+__device__ inline __amdgpu_buffer_rsrc_t page_rsrc(const uint16_t *page, bool want, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(page), (short)0, want ? bytes : 0,
+                                           kRsrcWord3);
+}
+template <bool NT> constexpr int kAux = NT ? 2 : 0; // nt: streamed once
+
+// K fragment: lane (n, kg) takes channels 8 kg + 32 s .. +8 of token n.
 template <int D, bool NT>
-__device__ inline void mfma_load(MfmaFrag<D> &f, const uint16_t *kbase, const uint16_t *vbase,
-                                 int64_t off) {
+__device__ inline void load_k(KFrag<D> &f, __amdgpu_buffer_rsrc_t r, int lane_off) {
 #pragma unroll
-  for (int s = 0; s < D / 32; ++s) f.k[s] = ld_stream<NT>(kbase + off + 32 * s);
+  for (int s = 0; s < D / 32; ++s) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + 64 * s, 0, kAux<NT>);
+    f.k[s] = make_uint4(x[0], x[1], x[2], x[3]);
+  }
+}
+// V^T fragment: lane (n, kg) takes tokens 4 kg .. +4 of channel n + 16 j.
+template <int D, bool NT>
+__device__ inline void load_v(VFrag<D> &f, __amdgpu_buffer_rsrc_t r, int lane_off) {
 #pragma unroll
-  for (int j = 0; j < D / 16; ++j) f.v[j] = ld_stream2<NT>(vbase + off + 16 * P * j);
+  for (int j = 0; j < D / 16; ++j) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b64(r, lane_off + 32 * P * j, 0, kAux<NT>);
+    f.v[j] = make_uint2(x[0], x[1]);
+  }
 }
 
+// S^T = K . Q^T for one page, then the online-softmax update of (m, l, acc);
+// returns the page's weights P as bf16 hi and lo parts.
 template <int D>
-__device__ inline void mfma_page(MfmaFrag<D> &f, int valid, int kg, float scale_log2,
-                                 const bf16x8_t (&qb)[D / 32], f32x4_t (&acc)[D / 16],
-                                 float &m_run, float &l_run) {
+__device__ inline void mfma_scores(const KFrag<D> &f, int valid, int kg, float scale_log2,
+                                   const bf16x8_t (&qb)[D / 32], f32x4_t (&acc)[D / 16],
+                                   float &m_run, float &l_run, s16x4_t &phi, s16x4_t &plo) {
   constexpr int NS = D / 32;
   constexpr int NJ = D / 16;
   f32x4_t st = f32x4_t{0.f, 0.f, 0.f, 0.f};
@@ -434,6 +467,15 @@ __device__ inline void mfma_page(MfmaFrag<D> &f, int valid, int kg, float scale_
 #pragma unroll
     for (int j = 0; j < NJ; ++j) acc[j] *= alpha;
   }
+  phi = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
+  plo = __builtin_bit_cast(s16x4_t, make_uint2(l01, l23));
+}
+
+// O^T += V^T . P^T for one page (hi and lo parts of P).
+template <int D>
+__device__ inline void mfma_values(VFrag<D> &f, int valid, int kg, s16x4_t phi, s16x4_t plo,
+                                   f32x4_t (&acc)[D / 16]) {
+  constexpr int NJ = D / 16;
   if (valid < P) { // values of absent tokens may be anything: keep 0 * v finite
     const uint32_t m0 = (4 * kg + 0 < valid ? 0xffffu : 0u) | (4 * kg + 1 < valid ? 0xffff0000u : 0u);
     const uint32_t m1 = (4 * kg + 2 < valid ? 0xffffu : 0u) | (4 * kg + 3 < valid ? 0xffff0000u : 0u);
@@ -443,8 +485,6 @@ __device__ inline void mfma_page(MfmaFrag<D> &f, int valid, int kg, float scale_
       f.v[j].y &= m1;
     }
   }
-  const s16x4_t phi = __builtin_bit_cast(s16x4_t, make_uint2(h01, h23));
-  const s16x4_t plo = __builtin_bit_cast(s16x4_t, make_uint2(l01, l23));
 #pragma unroll
   for (int j = 0; j < NJ; ++j) {
     const s16x4_t vA = __builtin_bit_cast(s16x4_t, f.v[j]);
@@ -464,12 +504,12 @@ k_decode_mfma(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float s_acc[kWaves][kRows * APITCH];
 
   const int lane = threadIdx.x & 63;
-  const int wave = threadIdx.x >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); // uniform in the wave
   const int n = lane & 15, kg = lane >> 4;
   const int64_t x_end = (int64_t)(blockIdx.x + 1) * a.total / a.n_wg;
   int64_t x_pos = (int64_t)blockIdx.x * a.total / a.n_wg;
-  while (x_pos < x_end) {
-  const ItemPos ip = next_piece(a, blockIdx.x, x_pos, x_end);
+  ItemPos ip;
+  while (next_piece(a, blockIdx.x, x_pos, x_end, ip)) {
   const int g = ip.g;
   const int nrows = ip.sg.nmem * G;
   const bool qvalid = n < nrows;
@@ -482,8 +522,9 @@ k_decode_mfma(DecodeArgs a) {
     const uint16_t *qp = a.q + ((int64_t)bq * a.hq + g * G + n % G) * D;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      uint4 w = qvalid ? *reinterpret_cast<const uint4 *>(qp + 8 * kg + 32 * s)
-                       : make_uint4(0, 0, 0, 0);
+      // rows past nrows read member 0's row (in bounds) and are zeroed
+      uint4 w = *reinterpret_cast<const uint4 *>(qp + 8 * kg + 32 * s);
+      if (!qvalid) w = make_uint4(0, 0, 0, 0);
       qb[s] = __builtin_bit_cast(bf16x8_t, w);
     }
   }
@@ -493,43 +534,87 @@ k_decode_mfma(DecodeArgs a) {
   for (int j = 0; j < NJ; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
 
-  const uint16_t *kbase = a.k + (int64_t)g * a.head_stride + n * D + 8 * kg;
-  const uint16_t *vbase = a.v + (int64_t)g * a.head_stride + n * P + 4 * kg;
-  const int first = ip.pbeg + wave;
-  // this wave's pages: first, first + kWaves, ... < pend; ids come 64 at a time
-  const int count = first < ip.pend ? (ip.pend - first + kWaves - 1) / kWaves : 0;
-  for (int base = 0; base < count; base += 64) {
-    const int nb = min(64, count - base);
-    const int my = first + (base + lane) * kWaves;
-    const int ids = lane < nb ? pt[my] : 0;
-    MfmaFrag<D> nxt;
-    mfma_load<D, NT>(nxt, kbase, vbase, (int64_t)__builtin_amdgcn_readlane(ids, 0) * a.page_stride);
-    for (int i = 0; i < nb; ++i) {
-      MfmaFrag<D> cur = nxt;
-      if (i + 1 < nb)
-        mfma_load<D, NT>(nxt, kbase, vbase,
-                     (int64_t)__builtin_amdgcn_readlane(ids, i + 1) * a.page_stride);
-      const int pg = first + (base + i) * kWaves;
-      const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
-      mfma_page<D>(cur, valid, kg, a.scale_log2, qb, acc, m_run, l_run);
+  const uint16_t *khead = a.k + (int64_t)g * a.head_stride;
+  const uint16_t *vhead = a.v + (int64_t)g * a.head_stride;
+  const int koff = (n * D + 8 * kg) * 2; // byte offsets within a page
+  const int voff = (n * P + 4 * kg) * 2;
+  constexpr int kPageBytes = P * D * 2;
+  // Wave w takes the w-th of kWaves contiguous shares of the piece's pages.
+  // Two pages are in flight while one is computed: page j + 2's K is loaded
+  // into page j's K registers as soon as its scores are taken, and its V
+  // into page j's V registers after the values, so every load has two
+  // pages' worth of time to land.  Every iteration issues the same loads
+  // (a page past the end gets an empty buffer and reads zeros), so the waits
+  // on the in-order vector load counter stay exact.  Page ids are scalar
+  // loads (their own counter), fetched an iteration before they are needed.
+  const int np_piece = ip.pend - ip.pbeg;
+  const int wbeg = ip.pbeg + np_piece * wave / kWaves;
+  const int count = ip.pbeg + np_piece * (wave + 1) / kWaves - wbeg;
+  typedef const int32_t __attribute__((address_space(4))) *sptr_t;
+  const sptr_t ids = (sptr_t)(pt + wbeg);
+  auto sid = [&](int j) -> int { return ids[min(j, max(count - 1, 0))]; };
+  auto rsrc = [&](const uint16_t *head, int id, bool want) {
+    return page_rsrc(head + (int64_t)(want ? id : 0) * a.page_stride, want, kPageBytes);
+  };
+  auto valid_of = [&](int j) -> int {
+    const int pg = wbeg + j;
+    return j >= count ? 0 : (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
+  };
+  KFrag<D> k0, k1;
+  VFrag<D> v0, v1;
+  int n0 = 0, n1 = 0; // ids of pages j + 2 and j + 3
+  if (count > 0) {
+    const int i0 = sid(0), i1 = sid(1);
+    load_k<D, NT>(k0, rsrc(khead, i0, true), koff);
+    load_v<D, NT>(v0, rsrc(vhead, i0, true), voff);
+    load_k<D, NT>(k1, rsrc(khead, i1, count > 1), koff);
+    load_v<D, NT>(v1, rsrc(vhead, i1, count > 1), voff);
+    n0 = sid(2);
+    n1 = sid(3);
+  }
+  for (int j = 0; j < count; j += 2) {
+    {
+      const int valid = valid_of(j);
+      s16x4_t phi, plo;
+      mfma_scores<D>(k0, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      load_k<D, NT>(k0, rsrc(khead, n0, j + 2 < count), koff);
+      mfma_values<D>(v0, valid, kg, phi, plo, acc);
+      load_v<D, NT>(v0, rsrc(vhead, n0, j + 2 < count), voff);
     }
+    {
+      // page j + 1 may not exist (count odd): its fragments are then zeros
+      // and with no valid token the update leaves (m, l, acc) as they are.
+      const int valid = valid_of(j + 1);
+      s16x4_t phi, plo;
+      mfma_scores<D>(k1, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      load_k<D, NT>(k1, rsrc(khead, n1, j + 3 < count), koff);
+      mfma_values<D>(v1, valid, kg, phi, plo, acc);
+      load_v<D, NT>(v1, rsrc(vhead, n1, j + 3 < count), voff);
+    }
+    n0 = sid(j + 4);
+    n1 = sid(j + 5);
   }
 
   float l_tot = sum_xrow16(l_run);
   l_tot = sum_xrow32(l_tot);
-  // combine the waves' states: M = max m_w, scale_w = 2^(m_w - M)
-  if (kg == 0) {
-    s_m[wave][n] = m_run;
-    s_l[wave][n] = l_tot;
+  // combine the waves' states: M = max m_w, scale_w = 2^(m_w - M).  The
+  // thread index is re-read here so that the LDS addresses below are
+  // computed after the page loop instead of being held through it.
+  int tx = threadIdx.x;
+  __asm__ volatile("" : "+v"(tx));
+  const int ew = tx >> 6, en = tx & 15, ekg = (tx >> 4) & 3;
+  if (ekg == 0) {
+    s_m[ew][en] = m_run;
+    s_l[ew][en] = l_tot;
   }
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
-    *reinterpret_cast<float4 *>(&s_acc[wave][n * APITCH + 16 * j + 4 * kg]) =
+    *reinterpret_cast<float4 *>(&s_acc[ew][en * APITCH + 16 * j + 4 * ekg]) =
         make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
   __syncthreads();
   const int64_t prow = (int64_t)ip.slot * kRows;
-  if (threadIdx.x < kRows && (int)threadIdx.x < nrows) {
-    const int r = threadIdx.x;
+  if (tx < kRows && tx < nrows) {
+    const int r = tx;
     float mm = kNegInf;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) mm = fmaxf(mm, s_m[w][r]);
@@ -542,7 +627,7 @@ k_decode_mfma(DecodeArgs a) {
     a.part_l[prow + r] = ll;
   }
   constexpr int PER = kRows * D / (64 * kWaves); // output floats per thread
-  const int e0 = threadIdx.x * PER;
+  const int e0 = tx * PER;
   const int r = e0 / D;
   if (r < nrows) {
     float mm = kNegInf;
@@ -609,7 +694,7 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
       const int meta = a.src_meta[b][e];
       const int L = meta & 1, seg = (meta >> 1) & 0xff, member = (meta >> 9) & 3;
       const int np = a.src_npages[b][e];
-      const int64_t R = (int64_t)a.src_start[b][e] + (int64_t)g * np; // row start
+      const int64_t R = (int64_t)a.src_start[b][e] + (int64_t)g * (np + a.row_pad[L]); // row start
       const int w_lo = wg_of(R, a.total[L], a.n_wg[L]);
       const int w_hi = wg_of(R + np - 1, a.total[L], a.n_wg[L]);
       cnt = w_hi - w_lo + 1;

@@ -202,11 +202,14 @@ struct sq_store {
   int64_t last_evict_L = 0, last_evict_Lp = 0;
 
   // tuning
-  int grid_rounds = 2;        // workgroups per launch = rounds * CUs * workgroups per CU
+  int grid_rounds = 1;        // workgroups per launch = rounds * CUs * workgroups per CU
   int cus = 256;              // compute units (device query in device mode)
   int wg_per_cu[2] = {8, 3};  // resident workgroups per CU (VALU, MFMA), from occupancy
   int min_wg_pages_valu = 8;
   int min_wg_pages_mfma = 32;
+  // flattened pages appended to every row of a launch (VALU, MFMA): a
+  // piece's start-up cost in page equivalents, so the even split evens time
+  int row_pad[2] = {2, 16};
   bool auto_single_mfma = true;
   int mfma_waves = 4; // waves per MFMA work item (1, 2 or 4)
 
@@ -454,7 +457,7 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     const int64_t np = (ps.seg.ntok + s->P - 1) / s->P;
     ps.seg.start = (int32_t)plan->total[L];
     plan->seg_index[i] = count[L]++;
-    plan->total[L] += np * hkv;
+    plan->total[L] += (np + s->row_pad[L]) * hkv;
     plan->kv_bytes += (int64_t)ps.seg.ntok * tok_bytes;
     (L == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += (int64_t)ps.seg.ntok * tok_bytes;
     plan->io_bytes += np * 4;
@@ -534,6 +537,11 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     const int v = std::atoi(e);
     if (v >= 1 && v <= 64) s->grid_rounds = v;
   }
+  for (int L = 0; L < 2; ++L)
+    if (const char *e = std::getenv(L ? "SQ_ROW_PAD_MFMA" : "SQ_ROW_PAD_VALU")) {
+      const int v = std::atoi(e);
+      if (v >= 0 && v <= 4096) s->row_pad[L] = v;
+    }
   if (const char *e = std::getenv("SQ_AUTO_SINGLE")) s->auto_single_mfma = std::strcmp(e, "valu") != 0;
   if (const char *e = std::getenv("SQ_MFMA_WAVES")) {
     const int v = std::atoi(e);
@@ -1127,6 +1135,7 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   ma.hkv = s->cfg.num_kv_heads;
   for (int L = 0; L < 2; ++L) {
     ma.total[L] = (int32_t)plan.total[L];
+    ma.row_pad[L] = s->row_pad[L];
     ma.n_wg[L] = plan.n_wg[L];
     ma.slot_base[L] = plan.slot_base[L];
   }
@@ -1146,6 +1155,7 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
     for (const PlanSeg &ps : plan.segs)
       if (ps.mfma == (pass == 1)) a.segs[a.n_segs++] = ps.seg;
     a.total = (int32_t)plan.total[pass];
+    a.row_pad = s->row_pad[pass];
     a.n_wg = plan.n_wg[pass];
     a.slot_base = plan.slot_base[pass];
     if (a.n_wg == 0) continue;
