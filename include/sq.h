@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 3
+#define SQ_ABI_VERSION 4
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -268,6 +268,47 @@ sq_status sq_evict_spans(sq_store *store, sq_seq seq, const int32_t *cursor_ids,
  * metadata-only store. */
 sq_status sq_decode_attn(sq_store *store, int32_t layer, const sq_seq *seqs, int32_t batch,
                          const void *q, float *out, float scale, int32_t mode, void *stream);
+
+/* ---- decode step with the append fused (graph-capturable) ----------------
+ * The decode loop of §3.1 appends one token to every running thread and
+ * attends over the result.  sq_step_begin does the host part of that for
+ * `batch` distinct sequences once per step: it appends one token slot to
+ * each (length + 1, a new page when the last one is full, positions
+ * continue) and writes the step's attention plan to device memory on
+ * stream.  sq_step_attn then runs one layer: it stores the new token's K
+ * and V in that layer and attends with q over every token of each
+ * sequence, the new one included - the same result as sq_append_batch
+ * followed by sq_decode_attn.  The new token joins in the merge kernel as
+ * one more partial of the split softmax (score q . k_new, weight 1, value
+ * v_new), so a layer costs two launches (one when the plan needs both the
+ * VALU and MFMA kernels: three) and no separate append.
+ *
+ * The launches of sq_step_attn and their arguments depend on (layer,
+ * pointers, scale, the step's batch size and mode) only: a stream capture
+ * (hipStreamBeginCapture) of one step's sq_step_attn calls replays correctly
+ * for every later step of the same batch size and mode, each after its own
+ * sq_step_begin on the same stream, with the caller's q / k_new / v_new /
+ * out buffers at the same addresses.  Replays do not update sq_stats.
+ *
+ * Between sq_step_begin and the last layer's sq_step_attn the new tokens'
+ * slots hold stale K/V: every other call that changes a sequence (append,
+ * fork, release, evict, a new step) ends the step, and sq_step_attn then
+ * fails.  mode: SQ_ATTN_*.  sq_step_begin errors change nothing;
+ * SQ_ERR_INVALID for a repeated sequence, batch outside [1, SQ_MAX_BATCH],
+ * a sequence at its page-list capacity; SQ_ERR_NO_PAGES; in a
+ * metadata-only store it updates the metadata only. */
+sq_status sq_step_begin(sq_store *store, const sq_seq *seqs, int32_t batch, int32_t mode,
+                        void *stream);
+
+/* One layer of the open step.  k_new, v_new: device bf16 [batch][Hkv][D];
+ * q: device bf16 [batch][Hq][D]; out: device fp32 [batch][Hq][D]; all
+ * 16-byte aligned, caller-owned; entry b is seqs[b] of sq_step_begin.
+ *   out[b][h] = sum_i softmax_i(scale * q[b][h] . K[i][h/G]) * V[i][h/G]
+ * over the L_b + 1 tokens of the sequence after the append.
+ * SQ_ERR_INVALID: no open step, bad layer, null or misaligned buffers,
+ * scale not finite, metadata-only store. */
+sq_status sq_step_attn(sq_store *store, int32_t layer, const void *k_new, const void *v_new,
+                       const void *q, float *out, float scale, void *stream);
 
 /* Causal attention of a chunk that was just appended: Algorithm 1 grows the
  * context by whole chunks (Phase 3: C <- C + R, then C <- C + O), and every

@@ -25,11 +25,8 @@ struct Seg {
   uint32_t mem; // byte j = batch index of member j
 };
 
-// A launch splits its flattened pages [0, total) evenly over n_wg <= total
-// workgroups: workgroup w takes [w * total / n_wg, (w + 1) * total / n_wg).
-// The piece of row r = segment * Hkv + g that workgroup w processes writes
-// the partial slot slot_base + w + r.
-struct DecodeArgs {
+// What a decode launch needs that does not change from call to call.
+struct DecodeStatic {
   const uint16_t *q;   // [B][Hq][D] bf16
   const uint16_t *k;   // K pool at this layer
   const uint16_t *v;   // V pool at this layer
@@ -42,14 +39,31 @@ struct DecodeArgs {
   int32_t max_pages;   // page-table row pitch
   int32_t hq;
   int32_t hkv;
-  int32_t n_segs;
-  int32_t total;       // flattened pages of this launch
-  int32_t n_wg;        // workgroups of this launch
-  int32_t slot_base;   // first partial slot of this launch
   int32_t nontemporal; // 1: every page is read once in this launch
-  int32_t row_pad;     // flattened pages after each row that map to nothing
   float scale_log2;    // scale * log2(e)
+  int32_t pad;
+};
+
+// The plan of one launch.  It splits its flattened pages [0, total) evenly
+// over n_wg <= total workgroups: workgroup w takes [w * total / n_wg,
+// (w + 1) * total / n_wg).  The piece of row r = segment * Hkv + g that
+// workgroup w processes writes the partial slot slot_base + w + r.  A launch
+// may have more workgroups than n_wg (a step launch is sized once for every
+// step); the extra ones do nothing.
+struct DecodeDyn {
+  int32_t n_segs;
+  int32_t total;     // flattened pages of this launch
+  int32_t n_wg;      // workgroups that share them
+  int32_t slot_base; // first partial slot of this launch
+  int32_t row_pad;   // flattened pages after each row that map to nothing
+  int32_t pad;
   Seg segs[kMaxSegs];
+};
+
+// A plain decode call passes its plan with the launch.
+struct DecodeArgs {
+  DecodeStatic st;
+  DecodeDyn dyn;
 };
 
 // The workgroup whose range holds flattened page x.
@@ -61,8 +75,8 @@ __host__ __device__ inline int32_t wg_of(int64_t x, int64_t total, int64_t n_wg)
 // shared page runs: at most kMaxSrc (shared levels, then its own suffix).
 constexpr int kMaxSrc = 4;
 
-struct MergeArgs {
-  float *out;  // [B][Hq][D]
+struct MergeStatic {
+  float *out; // [B][Hq][D]
   const float *part_m;
   const float *part_l;
   const float *part_acc;
@@ -70,6 +84,9 @@ struct MergeArgs {
   int32_t group; // G
   int32_t hkv;
   int32_t pad;
+};
+
+struct MergeDyn {
   int32_t total[2], n_wg[2], slot_base[2], row_pad[2]; // per launch (0: VALU, 1: MFMA)
   // per batch entry: the segments it attends; meta packs the launch (bit 0),
   // the segment index inside that launch (bits 1-8) and the member index
@@ -80,12 +97,62 @@ struct MergeArgs {
   int32_t src_npages[kMaxBatch][kMaxSrc];
 };
 
+struct MergeArgs {
+  MergeStatic st;
+  MergeDyn dyn;
+};
+
+// ---- decode step (append fused) -------------------------------------------
+// One decode step appends a token to every entry and attends over the old
+// tokens plus the new one.  The decode launches read the old tokens from
+// the pools; the merge adds the new token as one more partial (its score
+// against the entry's query, weight 1, value v_new) and stores its K, V,
+// position and, when it opens a page, the page-table entry.
+struct StepAppend {
+  int32_t page[kMaxBatch];     // physical page of the new token
+  int32_t slot[kMaxBatch];     // its slot in that page
+  int32_t pos[kMaxBatch];      // its position
+  int32_t pt_index[kMaxBatch]; // page-table mirror index to set to page, or -1
+};
+
+// The step plan, in device memory: written once per step, read by every
+// layer's launches, whose arguments therefore stay the same from step to
+// step.
+struct StepPlan {
+  DecodeDyn dec[2]; // VALU, MFMA launch
+  MergeDyn merge;
+  StepAppend app;
+};
+
+struct StepMergeArgs {
+  MergeStatic st;
+  const StepPlan *plan;
+  const uint16_t *q;     // [B][Hq][D] bf16
+  const uint16_t *k_new; // [B][Hkv][D] bf16
+  const uint16_t *v_new; // [B][Hkv][D] bf16
+  uint16_t *k;           // K pool at this layer
+  uint16_t *v;           // V pool at this layer
+  int32_t *pos;          // position pool [NP][P]
+  int32_t *pt;           // page-table mirror
+  int64_t page_stride;
+  int64_t head_stride;
+  float scale_log2;
+  int32_t pad;
+};
+
 static_assert(sizeof(DecodeArgs) < 4096, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) < 4096, "merge kernel arguments too large");
 
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s);
+// Step launches: `n_wg` workgroups (at least the plan's), the plan in device
+// memory at `dyn`.
+hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const DecodeDyn *dyn,
+                            int n_wg, hipStream_t s);
+hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
+                            const DecodeDyn *dyn, int n_wg, hipStream_t s);
+hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, hipStream_t s);
 // Workgroups of a decode kernel (kind 0: VALU, 1: MFMA) that fit on one CU.
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out);
 

@@ -121,20 +121,56 @@ struct ItemPos {
   int slot;     // partial slot
 };
 
+// A plain decode launch carries its plan in its arguments; a step launch
+// reads it from device memory (scalar loads through the constant address
+// space), so that its arguments stay the same from step to step.
+#define SQ_CONST __attribute__((address_space(4)))
+struct ArgPlan {
+  const DecodeDyn &d;
+  __device__ int n_segs() const { return d.n_segs; }
+  __device__ int total() const { return d.total; }
+  __device__ int n_wg() const { return d.n_wg; }
+  __device__ int slot_base() const { return d.slot_base; }
+  __device__ int row_pad() const { return d.row_pad; }
+  __device__ int seg_start(int i) const { return d.segs[i].start; }
+  __device__ Seg seg(int i) const { return d.segs[i]; }
+};
+struct DevPlan {
+  const SQ_CONST DecodeDyn *d;
+  __device__ int n_segs() const { return d->n_segs; }
+  __device__ int total() const { return d->total; }
+  __device__ int n_wg() const { return d->n_wg; }
+  __device__ int slot_base() const { return d->slot_base; }
+  __device__ int row_pad() const { return d->row_pad; }
+  __device__ int seg_start(int i) const { return d->segs[i].start; }
+  __device__ Seg seg(int i) const {
+    const SQ_CONST Seg &x = d->segs[i];
+    Seg y;
+    y.row = x.row;
+    y.page0 = x.page0;
+    y.ntok = x.ntok;
+    y.start = x.start;
+    y.nmem = x.nmem;
+    y.mem = x.mem;
+    return y;
+  }
+};
+
 // The next piece of workgroup w's range [x, xe): the real pages of one row
 // from x on (skipping row padding); advances x past it.  False when the
 // range holds no more real pages.
-__device__ inline bool next_piece(const DecodeArgs &a, int w, int64_t &x, int64_t xe, ItemPos &ip) {
+template <class PL>
+__device__ inline bool next_piece(const PL &pl, int hkv, int w, int64_t &x, int64_t xe, ItemPos &ip) {
   while (x < xe) {
-    int lo = 0, hi = a.n_segs - 1;
+    int lo = 0, hi = pl.n_segs() - 1;
     while (lo < hi) {
       const int mid = (lo + hi + 1) >> 1;
-      if (a.segs[mid].start <= x) lo = mid;
+      if (pl.seg_start(mid) <= x) lo = mid;
       else hi = mid - 1;
     }
-    ip.sg = a.segs[lo];
+    ip.sg = pl.seg(lo);
     ip.npages = (ip.sg.ntok + P - 1) / P;
-    const int64_t rl = ip.npages + a.row_pad;
+    const int64_t rl = ip.npages + pl.row_pad();
     ip.g = (int)((x - ip.sg.start) / rl);
     const int64_t rs = ip.sg.start + (int64_t)ip.g * rl;
     if (x - rs >= ip.npages) { // in the row's padding
@@ -144,7 +180,7 @@ __device__ inline bool next_piece(const DecodeArgs &a, int w, int64_t &x, int64_
     const int64_t pe = min(xe, rs + ip.npages);
     ip.pbeg = (int)(x - rs);
     ip.pend = (int)(pe - rs);
-    ip.slot = a.slot_base + w + lo * a.hkv + ip.g;
+    ip.slot = pl.slot_base() + w + lo * hkv + ip.g;
     x = pe;
     return true;
   }
@@ -164,8 +200,8 @@ __device__ inline bool next_piece(const DecodeArgs &a, int w, int64_t &x, int64_
 // LDS holds the page's K tile (row pitch 2D + 64 bytes) and V^T tile (groups
 // of D/16 channels, 32 bytes per channel, 32 bytes of padding per group), the
 // page's weights p[t][r] and the rescale factors alpha[r].
-template <int D, int G, bool NT>
-__global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
+template <int D, int G, bool NT, class PL>
+__device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
   constexpr int KPITCH = 2 * D + 64;
   constexpr int DPL = D / 16;
   constexpr int VGP = DPL * 32 + 32;
@@ -177,10 +213,11 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
   __shared__ __attribute__((aligned(16))) float sA[G];
 
   const int lane = threadIdx.x;
-  const int64_t x_end = (int64_t)(blockIdx.x + 1) * a.total / a.n_wg;
-  int64_t x_pos = (int64_t)blockIdx.x * a.total / a.n_wg;
+  if ((int)blockIdx.x >= pl.n_wg()) return;
+  const int64_t x_end = (int64_t)(blockIdx.x + 1) * pl.total() / pl.n_wg();
+  int64_t x_pos = (int64_t)blockIdx.x * pl.total() / pl.n_wg();
   ItemPos ip;
-  while (next_piece(a, blockIdx.x, x_pos, x_end, ip)) {
+  while (next_piece(pl, a.hkv, blockIdx.x, x_pos, x_end, ip)) {
   const int b = ip.sg.mem & 0xff;
   const int g = ip.g;
   const int32_t *pt = a.pt + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
@@ -376,6 +413,15 @@ __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
   } // pieces
 }
 
+template <int D, int G, bool NT>
+__global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
+  valu_body<D, G, NT>(a.st, ArgPlan{a.dyn});
+}
+template <int D, int G>
+__global__ __launch_bounds__(64) void k_step_valu(DecodeStatic a, const DecodeDyn *dyn) {
+  valu_body<D, G, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
+}
+
 // ===========================================================================
 // MFMA multi-query tile: up to 16 query rows (nmem sequences x G heads of one
 // KV head) against the same pages.  A work item is processed by a workgroup
@@ -493,9 +539,8 @@ __device__ inline void mfma_values(VFrag<D> &f, int valid, int kg, s16x4_t phi, 
   }
 }
 
-template <int D, int G, int kWaves, bool NT>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
-k_decode_mfma(DecodeArgs a) {
+template <int D, int G, int kWaves, bool NT, class PL>
+__device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   constexpr int NS = D / 32;
   constexpr int NJ = D / 16;
   constexpr int APITCH = D + 4; // floats per row of a wave's accumulator in LDS
@@ -506,10 +551,11 @@ k_decode_mfma(DecodeArgs a) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); // uniform in the wave
   const int n = lane & 15, kg = lane >> 4;
-  const int64_t x_end = (int64_t)(blockIdx.x + 1) * a.total / a.n_wg;
-  int64_t x_pos = (int64_t)blockIdx.x * a.total / a.n_wg;
+  if ((int)blockIdx.x >= pl.n_wg()) return;
+  const int64_t x_end = (int64_t)(blockIdx.x + 1) * pl.total() / pl.n_wg();
+  int64_t x_pos = (int64_t)blockIdx.x * pl.total() / pl.n_wg();
   ItemPos ip;
-  while (next_piece(a, blockIdx.x, x_pos, x_end, ip)) {
+  while (next_piece(pl, a.hkv, blockIdx.x, x_pos, x_end, ip)) {
   const int g = ip.g;
   const int nrows = ip.sg.nmem * G;
   const bool qvalid = n < nrows;
@@ -655,6 +701,17 @@ k_decode_mfma(DecodeArgs a) {
   } // pieces
 }
 
+template <int D, int G, int kWaves, bool NT>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
+k_decode_mfma(DecodeArgs a) {
+  mfma_body<D, G, kWaves, NT>(a.st, ArgPlan{a.dyn});
+}
+template <int D, int G, int kWaves>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
+k_step_mfma(DecodeStatic a, const DecodeDyn *dyn) {
+  mfma_body<D, G, kWaves, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
+}
+
 // ===========================================================================
 // Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
 // Its partials are the pieces of at most kMaxSrc segments (the shared runs on
@@ -668,8 +725,35 @@ k_decode_mfma(DecodeArgs a) {
 constexpr int kMergeWaves = 8;
 constexpr int kMergeUnroll = 16;
 
-template <int D>
-__global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) {
+struct ArgMerge {
+  const MergeDyn &d;
+  __device__ int total(int L) const { return d.total[L]; }
+  __device__ int n_wg(int L) const { return d.n_wg[L]; }
+  __device__ int slot_base(int L) const { return d.slot_base[L]; }
+  __device__ int row_pad(int L) const { return d.row_pad[L]; }
+  __device__ int n_src(int b) const { return d.n_src[b]; }
+  __device__ int src_meta(int b, int e) const { return d.src_meta[b][e]; }
+  __device__ int src_start(int b, int e) const { return d.src_start[b][e]; }
+  __device__ int src_npages(int b, int e) const { return d.src_npages[b][e]; }
+};
+struct DevMerge {
+  const SQ_CONST MergeDyn *d;
+  __device__ int total(int L) const { return d->total[L]; }
+  __device__ int n_wg(int L) const { return d->n_wg[L]; }
+  __device__ int slot_base(int L) const { return d->slot_base[L]; }
+  __device__ int row_pad(int L) const { return d->row_pad[L]; }
+  __device__ int n_src(int b) const { return d->n_src[b]; }
+  __device__ int src_meta(int b, int e) const { return d->src_meta[b][e]; }
+  __device__ int src_start(int b, int e) const { return d->src_start[b][e]; }
+  __device__ int src_npages(int b, int e) const { return d->src_npages[b][e]; }
+};
+
+// With APPEND (a decode step), the last wave starts from the entry's new
+// token as a partial of its own - score q . k_new, weight 1, value v_new -
+// and the workgroup of the first query head of each KV head stores the new
+// token's K, V, position and page-table entry for later steps.
+template <int D, bool APPEND, class MP, class SA>
+__device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &sa) {
   constexpr int DPT = D / 64;
   constexpr int U = kMergeUnroll;
   __shared__ float s_m[kMergeWaves];
@@ -682,7 +766,7 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
   const int h = blockIdx.x - b * a.hq;
   const int g = h / a.group;
   const int hr = h - g * a.group;
-  const int ns = a.n_src[b];
+  const int ns = mp.n_src(b);
   int cum[kMaxSrc + 1];
   int32_t base[kMaxSrc];
   cum[0] = 0;
@@ -691,14 +775,14 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
     int cnt = 0;
     base[e] = 0;
     if (e < ns) {
-      const int meta = a.src_meta[b][e];
+      const int meta = mp.src_meta(b, e);
       const int L = meta & 1, seg = (meta >> 1) & 0xff, member = (meta >> 9) & 3;
-      const int np = a.src_npages[b][e];
-      const int64_t R = (int64_t)a.src_start[b][e] + (int64_t)g * (np + a.row_pad[L]); // row start
-      const int w_lo = wg_of(R, a.total[L], a.n_wg[L]);
-      const int w_hi = wg_of(R + np - 1, a.total[L], a.n_wg[L]);
+      const int np = mp.src_npages(b, e);
+      const int64_t R = (int64_t)mp.src_start(b, e) + (int64_t)g * (np + mp.row_pad(L)); // row start
+      const int w_lo = wg_of(R, mp.total(L), mp.n_wg(L));
+      const int w_hi = wg_of(R + np - 1, mp.total(L), mp.n_wg(L));
       cnt = w_hi - w_lo + 1;
-      base[e] = (a.slot_base[L] + w_lo + seg * a.hkv + g) * kRows + member * a.group + hr;
+      base[e] = (mp.slot_base(L) + w_lo + seg * a.hkv + g) * kRows + member * a.group + hr;
     }
     cum[e + 1] = cum[e] + cnt;
   }
@@ -716,6 +800,43 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
   float num[DPT];
 #pragma unroll
   for (int q = 0; q < DPT; ++q) num[q] = 0.f;
+  if constexpr (APPEND) {
+    if (wave == kMergeWaves - 1) { // the last wave has the smallest share
+      const int64_t kv = (int64_t)b * a.hkv + g;
+      const uint16_t *qr = sa.q + ((int64_t)b * a.hq + h) * D + lane * DPT;
+      const uint16_t *kr = sa.k_new + kv * D + lane * DPT;
+      const uint16_t *vr = sa.v_new + kv * D + lane * DPT;
+      float dot = 0.f;
+      uint16_t kb[DPT], vb[DPT];
+#pragma unroll
+      for (int q = 0; q < DPT; ++q) {
+        kb[q] = kr[q];
+        vb[q] = vr[q];
+        dot = fmaf(__uint_as_float((uint32_t)qr[q] << 16), __uint_as_float((uint32_t)kb[q] << 16), dot);
+        num[q] = __uint_as_float((uint32_t)vb[q] << 16);
+      }
+#pragma unroll
+      for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
+      m_w = dot * sa.scale_log2;
+      l_w = 1.f;
+      if (hr == 0) { // store the new token of KV head g (the same in every head's workgroup)
+        const SQ_CONST StepAppend &ap = ((const SQ_CONST StepPlan *)sa.plan)->app;
+        const int page = ap.page[b], slot = ap.slot[b];
+        const int64_t pb = (int64_t)g * sa.head_stride + (int64_t)page * sa.page_stride;
+#pragma unroll
+        for (int q = 0; q < DPT; ++q) {
+          const int c = lane * DPT + q;
+          sa.k[pb + (int64_t)slot * D + c] = kb[q];
+          sa.v[pb + (int64_t)c * P + slot] = vb[q];
+        }
+        if (lane == 0 && g == 0) {
+          sa.pos[(int64_t)page * P + slot] = ap.pos[b];
+          const int pti = ap.pt_index[b];
+          if (pti >= 0) sa.pt[pti] = page;
+        }
+      }
+    }
+  }
   for (int i = cb; i < ce; i += U) {
     float x[U][DPT];
 #pragma unroll
@@ -780,9 +901,18 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) {
+  merge_body<D, false>(a.st, ArgMerge{a.dyn}, 0);
+}
+template <int D>
+__global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge(StepMergeArgs a) {
+  merge_body<D, true>(a.st, DevMerge{&((const SQ_CONST StepPlan *)a.plan)->merge}, a);
+}
+
 template <int D, bool NT>
 hipError_t valu_dispatch_nt(int group, const DecodeArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_wg), block(64);
+  const dim3 grid(a.dyn.n_wg), block(64);
   switch (group) {
   case 1: hipLaunchKernelGGL((k_decode_valu<D, 1, NT>), grid, block, 0, s, a); break;
   case 2: hipLaunchKernelGGL((k_decode_valu<D, 2, NT>), grid, block, 0, s, a); break;
@@ -795,13 +925,13 @@ hipError_t valu_dispatch_nt(int group, const DecodeArgs &a, hipStream_t s) {
 
 template <int D>
 hipError_t valu_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
-  return a.nontemporal ? valu_dispatch_nt<D, true>(group, a, s)
+  return a.st.nontemporal ? valu_dispatch_nt<D, true>(group, a, s)
                        : valu_dispatch_nt<D, false>(group, a, s);
 }
 
 template <int D, int W, bool NT>
 hipError_t mfma_dispatch_w(int group, const DecodeArgs &a, hipStream_t s) {
-  const dim3 grid(a.n_wg), block(64 * W);
+  const dim3 grid(a.dyn.n_wg), block(64 * W);
   switch (group) {
   case 1: hipLaunchKernelGGL((k_decode_mfma<D, 1, W, NT>), grid, block, 0, s, a); break;
   case 2: hipLaunchKernelGGL((k_decode_mfma<D, 2, W, NT>), grid, block, 0, s, a); break;
@@ -824,7 +954,7 @@ hipError_t mfma_dispatch_nt(int group, int waves, const DecodeArgs &a, hipStream
 
 template <int D>
 hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t s) {
-  return a.nontemporal ? mfma_dispatch_nt<D, true>(group, waves, a, s)
+  return a.st.nontemporal ? mfma_dispatch_nt<D, true>(group, waves, a, s)
                        : mfma_dispatch_nt<D, false>(group, waves, a, s);
 }
 
@@ -864,21 +994,74 @@ hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out)
 }
 
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s) {
-  if (a.n_wg == 0) return hipSuccess;
+  if (a.dyn.n_wg == 0) return hipSuccess;
   return d == 128 ? valu_dispatch<128>(group, a, s) : valu_dispatch<64>(group, a, s);
 }
 
 hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s) {
-  if (a.n_wg == 0) return hipSuccess;
+  if (a.dyn.n_wg == 0) return hipSuccess;
   return d == 128 ? mfma_dispatch<128>(group, waves, a, s) : mfma_dispatch<64>(group, waves, a, s);
 }
 
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s) {
-  const dim3 grid(batch * a.hq), block(64 * kMergeWaves);
+  const dim3 grid(batch * a.st.hq), block(64 * kMergeWaves);
   if (d == 128)
     hipLaunchKernelGGL(k_decode_merge<128>, grid, block, 0, s, a);
   else
     hipLaunchKernelGGL(k_decode_merge<64>, grid, block, 0, s, a);
+  return hipGetLastError();
+}
+
+namespace {
+template <int D>
+hipError_t step_valu_dispatch(int group, const DecodeStatic &st, const DecodeDyn *dyn, int n_wg,
+                              hipStream_t s) {
+  const dim3 grid(n_wg), block(64);
+  switch (group) {
+  case 1: hipLaunchKernelGGL((k_step_valu<D, 1>), grid, block, 0, s, st, dyn); break;
+  case 2: hipLaunchKernelGGL((k_step_valu<D, 2>), grid, block, 0, s, st, dyn); break;
+  case 4: hipLaunchKernelGGL((k_step_valu<D, 4>), grid, block, 0, s, st, dyn); break;
+  case 8: hipLaunchKernelGGL((k_step_valu<D, 8>), grid, block, 0, s, st, dyn); break;
+  default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+template <int D>
+hipError_t step_mfma_dispatch(int group, const DecodeStatic &st, const DecodeDyn *dyn, int n_wg,
+                              hipStream_t s) {
+  constexpr int W = 4;
+  const dim3 grid(n_wg), block(64 * W);
+  switch (group) {
+  case 1: hipLaunchKernelGGL((k_step_mfma<D, 1, W>), grid, block, 0, s, st, dyn); break;
+  case 2: hipLaunchKernelGGL((k_step_mfma<D, 2, W>), grid, block, 0, s, st, dyn); break;
+  case 4: hipLaunchKernelGGL((k_step_mfma<D, 4, W>), grid, block, 0, s, st, dyn); break;
+  case 8: hipLaunchKernelGGL((k_step_mfma<D, 8, W>), grid, block, 0, s, st, dyn); break;
+  default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+} // namespace
+
+hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const DecodeDyn *dyn,
+                            int n_wg, hipStream_t s) {
+  if (n_wg <= 0) return hipErrorInvalidValue;
+  return d == 128 ? step_valu_dispatch<128>(group, st, dyn, n_wg, s)
+                  : step_valu_dispatch<64>(group, st, dyn, n_wg, s);
+}
+
+hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
+                            const DecodeDyn *dyn, int n_wg, hipStream_t s) {
+  if (n_wg <= 0 || waves != 4) return hipErrorInvalidValue;
+  return d == 128 ? step_mfma_dispatch<128>(group, st, dyn, n_wg, s)
+                  : step_mfma_dispatch<64>(group, st, dyn, n_wg, s);
+}
+
+hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, hipStream_t s) {
+  const dim3 grid(batch * a.st.hq), block(64 * kMergeWaves);
+  if (d == 128)
+    hipLaunchKernelGGL(k_step_merge<128>, grid, block, 0, s, a);
+  else
+    hipLaunchKernelGGL(k_step_merge<64>, grid, block, 0, s, a);
   return hipGetLastError();
 }
 

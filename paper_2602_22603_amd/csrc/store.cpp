@@ -50,7 +50,7 @@ constexpr uint64_t kAlign = 256;
 uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  uint64_t pt, keep, dst, src, upload, part_m, part_l, part_acc, total;
+  uint64_t pt, keep, dst, src, upload, part_m, part_l, part_acc, step, total;
   uint64_t upload_elems;
 };
 
@@ -72,6 +72,7 @@ Layout layout_of(const sq_store_config &c) {
   L.part_m = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
   L.part_l = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
   L.part_acc = take((uint64_t)sq::kMaxItems * sq::kRows * c.head_dim * 4);
+  L.step = take(sizeof(sq::StepPlan));
   L.total = off;
   return L;
 }
@@ -198,6 +199,10 @@ struct sq_store {
   hipEvent_t staging_ev = nullptr;
   bool staging_pending = false;
   hipStream_t last_stream = nullptr;
+  sq::StepPlan *step_dev = nullptr;     // the step plan in the workspace
+  sq::StepPlan *step_staging = nullptr; // its pinned host copy
+  hipEvent_t step_ev = nullptr;
+  bool step_pending = false;
   bool have_last_evict = false;
   int64_t last_evict_L = 0, last_evict_Lp = 0;
 
@@ -212,6 +217,18 @@ struct sq_store {
   int row_pad[2] = {2, 16};
   bool auto_single_mfma = true;
   int mfma_waves = 4; // waves per MFMA work item (1, 2 or 4)
+
+  // every call that changes sequence metadata bumps gen; a begun decode
+  // step is valid while gen is what sq_step_begin left
+  uint64_t gen = 0;
+  struct Step {
+    bool active = false;
+    uint64_t gen = 0;
+    int32_t batch = 0, mode = 0;
+    bool launch[2] = {false, false}; // VALU, MFMA
+    int32_t grid[2] = {0, 0};
+    int64_t kv_bytes = 0, kv_bytes_logical = 0;
+  } step;
 
   // profiling
   bool prof_on = false;
@@ -481,6 +498,66 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   return SQ_OK;
 }
 
+// The arguments of a layer's decode launches that no plan changes.
+sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float scale, bool nt) {
+  sq::DecodeStatic st{};
+  st.q = static_cast<const uint16_t *>(q);
+  st.k = s->pools.k + layer * s->pools.layer_stride;
+  st.v = s->pools.v + layer * s->pools.layer_stride;
+  st.pt = s->pt_dev;
+  st.part_m = s->part_m;
+  st.part_l = s->part_l;
+  st.part_acc = s->part_acc;
+  st.page_stride = s->pools.page_stride;
+  st.head_stride = s->pools.head_stride;
+  st.max_pages = s->cfg.max_pages_per_seq;
+  st.hq = s->cfg.num_q_heads;
+  st.hkv = s->cfg.num_kv_heads;
+  st.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  st.nontemporal = nt ? 1 : 0;
+  return st;
+}
+
+sq::MergeStatic merge_static(sq_store *s, float *out) {
+  sq::MergeStatic st{};
+  st.out = out;
+  st.part_m = s->part_m;
+  st.part_l = s->part_l;
+  st.part_acc = s->part_acc;
+  st.hq = s->cfg.num_q_heads;
+  st.group = s->G;
+  st.hkv = s->cfg.num_kv_heads;
+  return st;
+}
+
+// The two launches' plans and every entry's merge sources.
+void fill_dyn(sq_store *s, const Plan &plan, sq::DecodeDyn dyn[2], sq::MergeDyn *md) {
+  for (int L = 0; L < 2; ++L) {
+    sq::DecodeDyn &d = dyn[L];
+    d.n_segs = 0;
+    for (const PlanSeg &ps : plan.segs)
+      if (ps.mfma == (L == 1)) d.segs[d.n_segs++] = ps.seg;
+    d.total = (int32_t)plan.total[L];
+    d.row_pad = s->row_pad[L];
+    d.n_wg = plan.n_wg[L];
+    d.slot_base = plan.slot_base[L];
+    md->total[L] = d.total;
+    md->row_pad[L] = d.row_pad;
+    md->n_wg[L] = d.n_wg;
+    md->slot_base[L] = d.slot_base;
+  }
+  for (size_t i = 0; i < plan.segs.size(); ++i) {
+    const PlanSeg &ps = plan.segs[i];
+    for (int j = 0; j < ps.seg.nmem; ++j) {
+      const int b = ps.members[j];
+      const int e = md->n_src[b]++;
+      md->src_meta[b][e] = (ps.mfma ? 1 : 0) | plan.seg_index[i] << 1 | j << 9;
+      md->src_start[b][e] = ps.seg.start;
+      md->src_npages[b][e] = (ps.seg.ntok + s->P - 1) / s->P;
+    }
+  }
+}
+
 } // namespace
 
 // ===========================================================================
@@ -558,6 +635,7 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     s->part_m = reinterpret_cast<float *>(ws + lay.part_m);
     s->part_l = reinterpret_cast<float *>(ws + lay.part_l);
     s->part_acc = reinterpret_cast<float *>(ws + lay.part_acc);
+    s->step_dev = reinterpret_cast<sq::StepPlan *>(ws + lay.step);
     sq::Pools &p = s->pools;
     p.k = static_cast<uint16_t *>(cfg->k_pool);
     p.v = static_cast<uint16_t *>(cfg->v_pool);
@@ -593,6 +671,19 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
       delete s;
       return hip_fail(e, "hipEventCreate");
     }
+    void *sh = nullptr;
+    e = hipHostMalloc(&sh, sizeof(sq::StepPlan), hipHostMallocDefault);
+    if (e == hipSuccess) {
+      s->step_staging = static_cast<sq::StepPlan *>(sh);
+      e = hipEventCreateWithFlags(&s->step_ev, hipEventDisableTiming);
+    }
+    if (e != hipSuccess) {
+      (void)hipEventDestroy(s->staging_ev);
+      (void)hipHostFree(host);
+      if (sh) (void)hipHostFree(sh);
+      delete s;
+      return hip_fail(e, "step plan staging");
+    }
   }
   *out = s;
   return SQ_OK;
@@ -610,6 +701,9 @@ sq_status sq_store_destroy(sq_store *s) {
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
     if (s->staging_ev) (void)hipEventDestroy(s->staging_ev);
     if (s->staging) (void)hipHostFree(s->staging);
+    if (s->step_pending) (void)hipEventSynchronize(s->step_ev);
+    if (s->step_ev) (void)hipEventDestroy(s->step_ev);
+    if (s->step_staging) (void)hipHostFree(s->step_staging);
   }
   delete s;
   return SQ_OK;
@@ -649,6 +743,7 @@ sq_status sq_append(sq_store *s, sq_seq h, int32_t n, const void *k_new, const v
     if (!aligned16(k_new) || !aligned16(v_new)) return fail(SQ_ERR_INVALID, "K/V must be 16-byte aligned");
     if (q->next_pos + n > INT32_MAX) return fail(SQ_ERR_INVALID, "positions exceed int32");
   }
+  ++s->gen;
   const int64_t old_len = q->length;
   const int32_t old_np = (int32_t)q->pages.size();
   while ((int64_t)q->pages.size() < want) q->pages.push_back(s->alloc_page());
@@ -713,6 +808,7 @@ sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const 
     if (!k_new || !v_new) return fail(SQ_ERR_INVALID, "null K/V");
     if (!aligned16(k_new) || !aligned16(v_new)) return fail(SQ_ERR_INVALID, "K/V must be 16-byte aligned");
   }
+  ++s->gen;
   sq::AppendBatchArgs a{};
   a.n = batch;
   a.pt = s->pt_dev;
@@ -784,6 +880,7 @@ sq_status sq_fork(sq_store *s, sq_seq parent, int64_t fork_len, sq_seq *child, v
   const int64_t tail = fork_len % s->P;
   if (tail && s->n_free < 1) return fail(SQ_ERR_NO_PAGES, "no page for the fork's tail copy");
 
+  ++s->gen;
   Seq c;
   c.live = true;
   c.pages.assign(par->pages.begin(), par->pages.begin() + full);
@@ -826,6 +923,7 @@ sq_status sq_release(sq_store *s, sq_seq h) {
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  ++s->gen;
   for (int32_t p : q->pages) s->unref(p, nullptr);
   *q = Seq();
   --s->st.live_seqs;
@@ -837,6 +935,7 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  ++s->gen; // ends a begun decode step even when the call fails
   if (n < 0 || n > SQ_MAX_EVICT_SPANS)
     return fail(SQ_ERR_INVALID, "cursor count %d outside [0, %d]", n, SQ_MAX_EVICT_SPANS);
   if (n > 0 && !cursor_ids) return fail(SQ_ERR_INVALID, "null cursor list");
@@ -1110,59 +1209,20 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
 
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
-  sq::DecodeArgs base{};
-  base.q = static_cast<const uint16_t *>(q);
-  base.k = s->pools.k + layer * s->pools.layer_stride;
-  base.v = s->pools.v + layer * s->pools.layer_stride;
-  base.pt = s->pt_dev;
-  base.part_m = s->part_m;
-  base.part_l = s->part_l;
-  base.part_acc = s->part_acc;
-  base.page_stride = s->pools.page_stride;
-  base.head_stride = s->pools.head_stride;
-  base.max_pages = s->cfg.max_pages_per_seq;
-  base.hq = s->cfg.num_q_heads;
-  base.hkv = s->cfg.num_kv_heads;
-  base.scale_log2 = (float)((double)scale * 1.4426950408889634);
-  base.nontemporal = plan.pages_reread ? 0 : 1;
+  sq::DecodeArgs da[2]{};
   sq::MergeArgs ma{};
-  ma.out = out;
-  ma.part_m = s->part_m;
-  ma.part_l = s->part_l;
-  ma.part_acc = s->part_acc;
-  ma.hq = s->cfg.num_q_heads;
-  ma.group = s->G;
-  ma.hkv = s->cfg.num_kv_heads;
-  for (int L = 0; L < 2; ++L) {
-    ma.total[L] = (int32_t)plan.total[L];
-    ma.row_pad[L] = s->row_pad[L];
-    ma.n_wg[L] = plan.n_wg[L];
-    ma.slot_base[L] = plan.slot_base[L];
-  }
-  for (size_t i = 0; i < plan.segs.size(); ++i) {
-    const PlanSeg &ps = plan.segs[i];
-    for (int j = 0; j < ps.seg.nmem; ++j) {
-      const int b = ps.members[j];
-      const int e = ma.n_src[b]++;
-      ma.src_meta[b][e] = (ps.mfma ? 1 : 0) | plan.seg_index[i] << 1 | j << 9;
-      ma.src_start[b][e] = ps.seg.start;
-      ma.src_npages[b][e] = (ps.seg.ntok + s->P - 1) / s->P;
-    }
-  }
+  da[0].st = decode_static(s, layer, q, scale, !plan.pages_reread);
+  da[1].st = da[0].st;
+  ma.st = merge_static(s, out);
+  sq::DecodeDyn dyn[2]{};
+  fill_dyn(s, plan, dyn, &ma.dyn);
   for (int pass = 0; pass < 2; ++pass) {
-    sq::DecodeArgs a = base;
-    a.n_segs = 0;
-    for (const PlanSeg &ps : plan.segs)
-      if (ps.mfma == (pass == 1)) a.segs[a.n_segs++] = ps.seg;
-    a.total = (int32_t)plan.total[pass];
-    a.row_pad = s->row_pad[pass];
-    a.n_wg = plan.n_wg[pass];
-    a.slot_base = plan.slot_base[pass];
-    if (a.n_wg == 0) continue;
+    da[pass].dyn = dyn[pass];
+    if (da[pass].dyn.n_wg == 0) continue;
     ProfPair pp;
     const bool on = s->prof_begin(strm, &pp, pass == 0 ? kProfValu : kProfMfma);
-    hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, a, strm)
-                             : sq::launch_decode_mfma(s->D, s->G, s->mfma_waves, a, strm);
+    hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, da[pass], strm)
+                             : sq::launch_decode_mfma(s->D, s->G, s->mfma_waves, da[pass], strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "decode kernel");
   }
@@ -1174,6 +1234,144 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   ++s->st.decode_calls;
   s->st.decode_kv_bytes += plan.kv_bytes;
   s->st.decode_kv_bytes_logical += plan.kv_bytes_logical;
+  return SQ_OK;
+}
+
+sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,
+                        void *stream) {
+  if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
+  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
+  if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
+  if (s->device && mode != SQ_ATTN_STREAM && s->mfma_waves != 4)
+    return fail(SQ_ERR_INVALID, "decode steps need 4 waves per MFMA work item");
+  int64_t need = 0;
+  for (int b = 0; b < batch; ++b) {
+    Seq *q = s->get(seqs[b]);
+    if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
+    for (int c = 0; c < b; ++c)
+      if (seqs[c] == seqs[b]) return fail(SQ_ERR_INVALID, "sequence %d repeated in the batch", seqs[b]);
+    if (q->length % s->P == 0) {
+      if (q->length / s->P + 1 > s->cfg.max_pages_per_seq)
+        return fail(SQ_ERR_INVALID, "sequence %d is at its page-list capacity", seqs[b]);
+      ++need;
+    }
+    if (s->device && q->next_pos + 1 > INT32_MAX) return fail(SQ_ERR_INVALID, "positions exceed int32");
+  }
+  if (need > s->n_free) return fail(SQ_ERR_NO_PAGES, "step needs %lld pages, %lld free",
+                                    (long long)need, (long long)s->n_free);
+  // attention over the tokens before the step; the new ones join in the merge
+  Plan plan;
+  sq_status r = build_plan(s, seqs, batch, mode, &plan);
+  if (r != SQ_OK) return r;
+  // which launches a layer makes depends on the mode only, so that a
+  // captured step replays for every later step of the same batch and mode
+  const bool launch[2] = {mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
+                              (mode == SQ_ATTN_AUTO && !s->auto_single_mfma),
+                          mode != SQ_ATTN_STREAM};
+  for (int L = 0; L < 2; ++L)
+    if (plan.n_wg[L] > 0 && !launch[L]) return fail(SQ_ERR_INVALID, "internal: step plan needs an unlaunched kernel");
+  if (s->device && s->step_pending) { // the staging copy of the last step's plan
+    hipError_t e = hipEventSynchronize(s->step_ev);
+    if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(step plan)");
+    s->step_pending = false;
+  }
+  sq::StepPlan *sp = s->device ? s->step_staging : nullptr;
+  if (sp) {
+    std::memset(sp, 0, sizeof(*sp));
+    fill_dyn(s, plan, sp->dec, &sp->merge);
+  }
+  const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
+  ++s->gen;
+  for (int b = 0; b < batch; ++b) {
+    Seq &q = s->seqs[seqs[b]];
+    int32_t pti = -1;
+    if (q.length % s->P == 0) {
+      q.pages.push_back(s->alloc_page());
+      pti = seqs[b] * s->cfg.max_pages_per_seq + (int32_t)q.pages.size() - 1;
+    }
+    if (sp) {
+      sp->app.page[b] = q.pages[q.length / s->P];
+      sp->app.slot[b] = (int32_t)(q.length % s->P);
+      sp->app.pos[b] = (int32_t)q.next_pos;
+      sp->app.pt_index[b] = pti;
+    }
+    runs_append(q, 1);
+    q.length += 1;
+    q.next_pos += 1;
+  }
+  s->st.append_tokens += batch;
+  sq_store::Step &st = s->step;
+  st = sq_store::Step{};
+  st.active = true;
+  st.gen = s->gen;
+  st.batch = batch;
+  st.mode = mode;
+  for (int L = 0; L < 2; ++L) {
+    st.launch[L] = launch[L];
+    st.grid[L] = s->grid_rounds * s->cus * s->wg_per_cu[L]; // >= plan.n_wg[L]
+  }
+  st.kv_bytes = plan.kv_bytes + batch * tok_bytes;
+  st.kv_bytes_logical = plan.kv_bytes_logical + batch * tok_bytes;
+  if (!s->device) return SQ_OK;
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  hipError_t e = hipMemcpyAsync(s->step_dev, sp, sizeof(*sp), hipMemcpyHostToDevice, strm);
+  if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(step plan)");
+  e = hipEventRecord(s->step_ev, strm);
+  if (e != hipSuccess) return hip_fail(e, "hipEventRecord(step plan)");
+  s->step_pending = true;
+  return SQ_OK;
+}
+
+sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void *v_new,
+                       const void *q, float *out, float scale, void *stream) {
+  if (!s) return fail(SQ_ERR_INVALID, "null store");
+  if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
+  const sq_store::Step &st = s->step;
+  if (!st.active || st.gen != s->gen)
+    return fail(SQ_ERR_INVALID, "no decode step is open (none begun, or the store changed since)");
+  if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
+  if (!k_new || !v_new || !q || !out || !aligned16(k_new) || !aligned16(v_new) || !aligned16(q) ||
+      !aligned16(out))
+    return fail(SQ_ERR_INVALID, "k_new, v_new, q and out must be non-null and 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
+  (void)hipStreamIsCapturing(strm, &cap);
+  const bool prof = cap == hipStreamCaptureStatusNone; // no timing events in a capture
+  const sq::DecodeStatic ds = decode_static(s, layer, q, scale, true);
+  for (int L = 0; L < 2; ++L) {
+    if (!st.launch[L]) continue;
+    ProfPair pp;
+    const bool on = prof && s->prof_begin(strm, &pp, L == 0 ? kProfValu : kProfMfma);
+    hipError_t e = L == 0 ? sq::launch_step_valu(s->D, s->G, ds, &s->step_dev->dec[0], st.grid[0], strm)
+                          : sq::launch_step_mfma(s->D, s->G, s->mfma_waves, ds, &s->step_dev->dec[1],
+                                                 st.grid[1], strm);
+    s->prof_end(strm, &pp, on);
+    if (e != hipSuccess) return hip_fail(e, "decode step kernel");
+  }
+  sq::StepMergeArgs ma{};
+  ma.st = merge_static(s, out);
+  ma.plan = s->step_dev;
+  ma.q = static_cast<const uint16_t *>(q);
+  ma.k_new = static_cast<const uint16_t *>(k_new);
+  ma.v_new = static_cast<const uint16_t *>(v_new);
+  ma.k = s->pools.k + layer * s->pools.layer_stride;
+  ma.v = s->pools.v + layer * s->pools.layer_stride;
+  ma.pos = s->pools.pos;
+  ma.pt = s->pt_dev;
+  ma.page_stride = s->pools.page_stride;
+  ma.head_stride = s->pools.head_stride;
+  ma.scale_log2 = ds.scale_log2;
+  ProfPair pp;
+  const bool on = prof && s->prof_begin(strm, &pp, kProfMerge);
+  hipError_t e = sq::launch_step_merge(s->D, st.batch, ma, strm);
+  s->prof_end(strm, &pp, on);
+  if (e != hipSuccess) return hip_fail(e, "decode step merge");
+  ++s->st.decode_calls;
+  s->st.decode_kv_bytes += st.kv_bytes;
+  s->st.decode_kv_bytes_logical += st.kv_bytes_logical;
   return SQ_OK;
 }
 

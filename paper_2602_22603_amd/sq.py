@@ -102,6 +102,10 @@ _SIGS = {
                                  C.c_void_p, C.POINTER(EvictStats)]),
     "sq_decode_attn": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
                                  C.c_void_p, C.c_void_p, C.c_float, C.c_int32, C.c_void_p]),
+    "sq_step_begin": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
+                                C.c_void_p]),
+    "sq_step_attn": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                               C.c_void_p, C.c_float, C.c_void_p]),
     "sq_extend_attn": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_float, C.c_void_p]),
     "sq_decode_plan_info": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
@@ -311,6 +315,39 @@ class Store:
         qp, op = (_ptr(q), _ptr(out)) if self.metadata_only else self._qo_ptrs(q, out, len(seqs))
         _check(lib().sq_decode_attn(self._handle, layer, _i32_array(seqs), len(seqs), qp, op,
                                     float(scale), mode, _stream(stream)))
+        return out
+
+    def step_begin(self, seqs, mode=ATTN_AUTO, stream=None):
+        """Open a decode step: one token slot appended to each of seqs (their
+        K/V arrive layer by layer through step_attn)."""
+        seqs = list(seqs)
+        st = C.c_void_p(0) if self.metadata_only else _stream(stream)
+        # the C side trusts buffer sizes: step_attn checks them against the
+        # batch of the last step this binding opened, and refuses after a
+        # failed step_begin
+        self._step_batch = None
+        _check(lib().sq_step_begin(self._handle, _i32_array(seqs), len(seqs), mode, st))
+        self._step_batch = len(seqs)
+
+    def step_attn(self, layer, k_new, v_new, q, out=None, scale=None, stream=None):
+        """One layer of the open step: store k_new, v_new (bf16 [B, Hkv, D])
+        and attend with q (bf16 [B, Hq, D]) over every token, the new one
+        included; returns out (fp32 [B, Hq, D])."""
+        import torch
+        if out is None:
+            out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
+        if scale is None:
+            scale = 1.0 / float(self.head_dim) ** 0.5
+        if self.metadata_only:
+            ptrs = (_ptr(k_new), _ptr(v_new), _ptr(q), _ptr(out))
+        else:
+            b = getattr(self, "_step_batch", None)
+            if b is None:
+                raise SqError(ERR_INVALID, "no decode step opened by this binding")
+            kv = (b, self.num_kv_heads, self.head_dim)
+            ptrs = (self._tensor(k_new, kv, torch.bfloat16, "k_new"),
+                    self._tensor(v_new, kv, torch.bfloat16, "v_new"), *self._qo_ptrs(q, out, b))
+        _check(lib().sq_step_attn(self._handle, layer, *ptrs, float(scale), _stream(stream)))
         return out
 
     def extend(self, layer, seq, q, out=None, scale=None, stream=None):

@@ -227,3 +227,42 @@ class Twin:
             torch.cuda.synchronize()
             errs[m] = max_abs(out.cpu().numpy(), ref)
         return errs, ref
+
+    def step(self, seqs, mode=None, scale=None, graph=None):
+        """One decode step of every layer through sq_step_begin / sq_step_attn
+        (or, with ``graph``, a replay of captured sq_step_attn calls: a dict
+        with the graph and its fixed k/v/q/out buffers), mirrored in the
+        oracle as a one-token append to each sequence followed by attention.
+        Returns the max abs error over all layers and entries."""
+        import torch
+        sq = self.sq
+        mode = sq.ATTN_AUTO if mode is None else mode
+        scale = scale_for(self.d) if scale is None else scale
+        b = len(seqs)
+        kb = wl.normal_bf16(self.rng, (self.nl, b, self.hkv, self.d))
+        vb = wl.normal_bf16(self.rng, (self.nl, b, self.hkv, self.d))
+        qb = wl.normal_bf16(self.rng, (self.nl, b, self.hq, self.d))
+        self.store.step_begin(seqs, mode)
+        if graph is None:
+            k, v, q = (wl.to_torch_bf16(x, self.device) for x in (kb, vb, qb))
+            outs = [self.store.step_attn(l, k[l], v[l], q[l], scale=scale) for l in range(self.nl)]
+        else:
+            for name, x in (("k", kb), ("v", vb), ("q", qb)):
+                graph[name].copy_(wl.to_torch_bf16(x, self.device))
+            graph["graph"].replay()
+            outs = graph["out"]
+        torch.cuda.synchronize()
+        got = [o.cpu().numpy() for o in outs]
+        kf, vf = wl.bf16_value(kb), wl.bf16_value(vb)
+        for j, h in enumerate(seqs):
+            self.model.append(h, 1, kf[:, j:j + 1], vf[:, j:j + 1])
+        err = 0.0
+        qf = wl.bf16_value(qb)
+        for l in range(self.nl):
+            views = []
+            for h in seqs:
+                kk, vv, _ = self.model.view(h)
+                views.append((kk[:, l], vv[:, l]))
+            ref = oatt.decode_batch(qf[l], views, scale, self.group)
+            err = max(err, max_abs(got[l], ref))
+        return err, got

@@ -95,8 +95,23 @@ def test_random_ops_match_oracle(sq, page, seed, chunk):
         live = sorted(model.seqs)
         h = int(rng.choice(live)) if live else 0
         op = rng.choice(["append", "append", "mark", "mark", "fork", "evict", "release",
-                         "bad"])
-        if op == "append":
+                         "bad", "step"])
+        if op == "step":
+            # a decode step opens one slot per sequence, all or nothing
+            batch = [int(x) for x in rng.permutation(live)[:int(rng.integers(1, len(live) + 1))]]
+            need = sum(model.info(x)["length"] % page == 0 for x in batch)
+            full = any(model.info(x)["length"] // page + 1 > max_pages
+                       for x in batch if model.info(x)["length"] % page == 0)
+            before = [store.page_table(x) for x in batch], store.refcounts().tolist()
+            if full or need > model.stats()["free_pages"]:
+                with pytest.raises(sq.SqError):
+                    store.step_begin(batch)
+                assert before == ([store.page_table(x) for x in batch], store.refcounts().tolist())
+            else:
+                store.step_begin(batch)
+                for x in batch:
+                    model.append(x, 1)
+        elif op == "append":
             n = int(rng.integers(0, 3 * page + 5))
             _both(store, model, sq, lambda: store.append(h, n=n), lambda: model.append(h, n))
         elif op == "mark":
@@ -247,6 +262,51 @@ def test_attention_needs_a_device_store(sq):
     rc = sq.lib().sq_decode_attn(s._handle, 0, seqs, 1, None, None, C.c_float(0.5), 0, None)
     assert rc == sq.ERR_INVALID
     assert before == (s.page_table(a), s.stats())
+
+
+def test_decode_step_metadata(sq):
+    """sq_step_begin opens one token slot per sequence exactly as
+    sq_append_batch appends one token (pages, positions, refcounts, stats);
+    its errors change nothing; the layers need a device store."""
+    import ctypes as C
+    stores = [_store(sq, 8, 4, 4, 4) for _ in range(2)]   # 8 pages of 4 tokens, 16 per sequence
+    for s in stores:
+        a = s.seq_create()
+        s.append(a, n=7)               # pages [0, 1]
+        s.fork(a, 4)                   # aliases page 0
+        s.seq_create()                 # an empty sequence
+    stores[0].append_batch([0, 1, 2])
+    stores[1].step_begin([0, 1, 2])
+    for h in (0, 1, 2):
+        assert stores[0].page_table(h) == stores[1].page_table(h)
+        assert stores[0].positions(h).tolist() == stores[1].positions(h).tolist()
+        assert stores[0].seq_info(h) == stores[1].seq_info(h)
+    assert stores[1].page_table(1) == [0, 2] and stores[1].page_table(2) == [3]
+    assert stores[0].refcounts().tolist() == stores[1].refcounts().tolist()
+    assert stores[0].stats()["append_tokens"] == stores[1].stats()["append_tokens"]
+    s = stores[1]
+    snap = lambda: ([s.page_table(h) for h in (0, 1, 2)], s.refcounts().tolist(), s.stats())
+    before = snap()
+    for bad, code in (([0, 0], sq.ERR_INVALID), ([0, 9], sq.ERR_UNKNOWN_SEQ), ([], sq.ERR_INVALID)):
+        with pytest.raises(sq.SqError) as ei:
+            s.step_begin(bad)
+        assert ei.value.code == code
+        assert snap() == before
+    s.append(2, n=3)                   # sequence 2 fills its page: its next step opens one
+    s.append(1, n=11)                  # sequence 1 reaches its capacity (16 tokens, pages 4 and 5 added)
+    before = snap()
+    with pytest.raises(sq.SqError) as ei:
+        s.step_begin([2, 1])
+    assert ei.value.code == sq.ERR_INVALID and snap() == before
+    d = s.seq_create()
+    s.append(d, n=8)                   # takes the last two free pages
+    assert s.stats()["free_pages"] == 0
+    before = snap()
+    with pytest.raises(sq.SqError) as ei:
+        s.step_begin([2])
+    assert ei.value.code == sq.ERR_NO_PAGES and snap() == before
+    rc = sq.lib().sq_step_attn(s._handle, 0, None, None, None, None, C.c_float(0.5), None)
+    assert rc == sq.ERR_INVALID and b"metadata-only" in sq.lib().sq_last_error()
 
 
 def test_invalid_configurations(sq):
