@@ -131,6 +131,93 @@ def time_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
                 instrumented_ms_per_step=(t3 - t2) * 1e3 / steps)
 
 
+def time_fused_steps(sq, torch, store, seqs, mode, steps, warmup, kb, vb, qs, out):
+    """The same decode steps through sq_step_begin + sq_step_attn (the append
+    fused into the merge kernel): bare wall clock, then instrumented."""
+    n = len(seqs)
+
+    def step(i):
+        store.step_begin(seqs, mode)
+        store.step_attn(0, kb[i][0], vb[i][0], qs[i], out=out)
+    for i in range(warmup):
+        step(i)
+    torch.cuda.synchronize()
+    st0 = store.stats()
+    t0 = time.perf_counter()
+    for i in range(warmup, warmup + steps):
+        step(i)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    st1 = store.stats()
+    ms = (t1 - t0) * 1e3 / steps
+    kv_bytes = (st1["decode_kv_bytes"] - st0["decode_kv_bytes"]) / steps
+    store.profile_enable(True)
+    store.profile_read()
+    for i in range(warmup, warmup + steps):
+        step(i)
+    torch.cuda.synchronize()
+    prof = store.profile_read()
+    store.profile_enable(False)
+    kern = prof["decode_mfma_ms"] / max(1, prof["decode_mfma_launches"])
+    return dict(ms_per_step=round(ms, 4), gbps=round(kv_bytes / (ms * 1e-3) / 1e9, 1),
+                tokens_per_s=round(n / (ms * 1e-3), 1), kv_bytes_per_step=kv_bytes,
+                kernel_ms=round(kern, 5),
+                merge_ms=round(prof["decode_merge_ms"] / max(1, prof["decode_merge_launches"]), 5))
+
+
+def decode_step_paths(torch, wl, store, seqs, reps=10):
+    """One decode step of every layer at the store's current state, three ways:
+    sq_append_batch then sq_decode_attn per layer; sq_step_begin then
+    sq_step_attn per layer; sq_step_begin then a replay of the captured
+    sq_step_attn calls.  Median wall clock per step (synchronised after each),
+    so host time counts."""
+    nl, b = store.num_layers, len(seqs)
+    kn = wl.device_normal_bf16((nl, b, store.num_kv_heads, store.head_dim), 71, "cuda")
+    vn = wl.device_normal_bf16((nl, b, store.num_kv_heads, store.head_dim), 72, "cuda")
+    q = wl.device_normal_bf16((nl, b, store.num_q_heads, store.head_dim), 73, "cuda")
+    outs = [torch.empty((b, store.num_q_heads, store.head_dim), dtype=torch.float32, device="cuda")
+            for _ in range(nl)]
+
+    def per_call():
+        store.append_batch(seqs, kn, vn)
+        for l in range(nl):
+            store.decode(l, seqs, q[l], out=outs[l])
+
+    def layers():
+        for l in range(nl):
+            store.step_attn(l, kn[l], vn[l], q[l], out=outs[l])
+
+    def fused():
+        store.step_begin(seqs)
+        layers()
+    fused()                       # an open step for the capture to record
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        layers()
+
+    def graph():
+        store.step_begin(seqs)
+        g.replay()
+    res = {}
+    kv = store.plan_info(seqs)["kv_bytes"] * nl
+    for name, fn in (("per_call", per_call), ("fused", fused), ("fused_graph", graph)):
+        for _ in range(2):
+            fn()
+        walls = []
+        for _ in range(reps):
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            fn()
+            torch.cuda.synchronize()
+            walls.append((time.perf_counter() - t0) * 1e3)
+        med = sorted(walls)[len(walls) // 2]
+        res[name + "_ms"] = round(med, 3)
+        res[name + "_gbps"] = round(kv / (med * 1e-3) / 1e9, 1)
+    del g
+    return res
+
+
 def percentiles(xs):
     """p10 / median / p90 of a list of step times (ms)."""
     xs = sorted(xs)
@@ -334,7 +421,7 @@ def extend_leg(sq, torch, wl, reps=10):
     return res
 
 
-def fullstack_leg(sq, torch):
+def fullstack_leg(sq, torch, wl):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
     turns; with one-shot eviction, with eviction in 64-page chunks (bounded
     transient pages) and without eviction: peak KV bytes, the causal extend
@@ -348,6 +435,8 @@ def fullstack_leg(sq, torch):
         store, main, aux, log, w = drivers.run_full_stack(evict=ev, evict_chunk_pages=chunk,
                                                           extend=chunk == 0)
         st = store.stats()
+        paths = decode_step_paths(torch, wl, store, [main] + ([aux] if aux is not None else [])) \
+            if chunk == 0 else None
         final = log[-1]
         dec = [r["decode_ms"] for r in log]
         ev_ms = [r["evict_ms"] for r in log if "evict_ms" in r]
@@ -361,7 +450,8 @@ def fullstack_leg(sq, torch):
             evictions=len(ev_ms), evict_ms_total=round(sum(ev_ms), 3),
             evict_gbps=round(2 * moved / (sum(ev_ms) * 1e-3) / 1e9, 1) if ev_ms else None,
             extend_ms_over_turns=round(sum(r.get("extend_ms", 0) + r.get("aux_extend_ms", 0)
-                                           for r in log), 1) if chunk == 0 else None)
+                                           for r in log), 1) if chunk == 0 else None,
+            decode_step_paths_final=paths)
         store.close()
         torch.cuda.empty_cache()
     a, b = res["with_eviction"], res["without_eviction"]
@@ -456,7 +546,7 @@ def main():
     total = args.warmup + args.steps
     n_modes = 5 if "modes" in legs else 0
     per_call = args.warmup + 2 * args.steps      # tokens one time_steps call appends
-    extra = per_call * (1 + n_modes) + total + 16
+    extra = per_call * (2 + n_modes) + total + 16
     log(f"building {args.tasks} tasks at {args.ctx} tokens ...")
     from paper_2602_22603_amd import drivers
     store, seqs, inputs = drivers.build_shared128k(tasks=args.tasks, ctx=args.ctx,
@@ -480,6 +570,9 @@ def main():
         store.decode(0, seqs, qs[i % total], out=out)
     step_cold = time_events(torch, cold_step, min(args.steps, total), flush)
     del flush
+    log("timing fused decode steps (append in the merge) ...")
+    fused = time_fused_steps(sq, torch, store, seqs, sq.ATTN_AUTO, args.steps, args.warmup,
+                             kb, vb, qs, out)
     prof, plan = main_res["prof"], main_res["plan"]
     if plan["n_items_mfma"]:
         kname, kms, kn, kbytes = ("k_decode_mfma", prof["decode_mfma_ms"],
@@ -549,7 +642,7 @@ def main():
     fullstack = None
     if "fullstack" in legs:
         log("full-stack leg (36 layers, 16K -> 256K) ...")
-        fullstack = fullstack_leg(sq, torch)
+        fullstack = fullstack_leg(sq, torch, wl)
     cpu = None
     if "cpu" in legs:
         log("oracle CPU baseline ...")
@@ -576,6 +669,7 @@ def main():
         "tokens_per_s": round(main_res["tokens_per_s"], 1),
         "step_ms_warm": main_res["step_ms"],
         "instrumented_ms_per_step": round(main_res["instrumented_ms_per_step"], 4),
+        "fused_step": fused,
         "step_ms_cold": step_cold,
         "kv_bytes_per_step": main_res["kv_bytes_per_step"],
         "kv_bytes_logical_per_step": main_res["kv_bytes_logical_per_step"],

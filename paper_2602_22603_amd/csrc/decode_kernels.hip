@@ -25,6 +25,13 @@
 //                  A operand V^T.
 //   k_decode_merge M = max m_s; out = sum e^(m_s - M) acc_s / sum e^(m_s - M) l_s.
 //
+// A decode step of the model appends one token per thread before it attends
+// (Algorithm 1, Phase 3 grows the context token by token while decoding).
+// k_step_valu / k_step_mfma / k_step_merge are the same kernels for a step
+// whose plan lives in device memory (so a captured step replays for later
+// steps); the step's merge adds each entry's new token as one more partial
+// and stores it in the pools, which saves the append launch.
+//
 // Scores are kept in log2 units (scale * log2 e folded into one multiply) so
 // every exponential is one v_exp_f32; m in the partials is in log2 units.
 #include <hip/hip_bf16.h>
@@ -424,10 +431,10 @@ __global__ __launch_bounds__(64) void k_step_valu(DecodeStatic a, const DecodeDy
 
 // ===========================================================================
 // MFMA multi-query tile: up to 16 query rows (nmem sequences x G heads of one
-// KV head) against the same pages.  A work item is processed by a workgroup
-// of kWaves waves; wave w takes pages w, w + kWaves, ... of the item's chunk
-// and the waves' softmax states are combined in LDS at the end, so one item
-// still yields one partial per row.
+// KV head) against the same pages.  A piece is processed by a workgroup of
+// kWaves waves; wave w takes the w-th contiguous share of its pages and the
+// waves' softmax states are combined in LDS at the end, so one piece still
+// yields one partial per row.
 // Lane l = n + 16 * kg (n = l & 15, kg = l >> 4):
 //   QK A operand  K[token n][channels 8 kg + 32 s .. +8]       (16x16x32)
 //   QK B operand  Q[row n][same channels]
@@ -794,14 +801,17 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
     return base[e] + (c - cum[e]) * kRows;
   };
 
-  const int per = (total + kMergeWaves - 1) / kMergeWaves;
-  const int cb = wave * per, ce = min(total, cb + per);
+  // with APPEND the last wave takes the new token only, so its loads overlap
+  // the other waves' partials instead of adding to a share of its own
+  constexpr int NW = APPEND ? kMergeWaves - 1 : kMergeWaves;
+  const int per = (total + NW - 1) / NW;
+  const int cb = min(total, wave * per), ce = min(total, cb + per);
   float m_w = kNegInf, l_w = 0.f;
   float num[DPT];
 #pragma unroll
   for (int q = 0; q < DPT; ++q) num[q] = 0.f;
   if constexpr (APPEND) {
-    if (wave == kMergeWaves - 1) { // the last wave has the smallest share
+    if (wave == kMergeWaves - 1) {
       const int64_t kv = (int64_t)b * a.hkv + g;
       const uint16_t *qr = sa.q + ((int64_t)b * a.hq + h) * D + lane * DPT;
       const uint16_t *kr = sa.k_new + kv * D + lane * DPT;
