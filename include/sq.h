@@ -78,6 +78,14 @@ typedef enum {
 #define SQ_STORE_METADATA_ONLY 1u /* host bookkeeping only: no pools, no
                                      workspace, no HIP calls; any page size;
                                      sq_decode_attn is rejected */
+#define SQ_STORE_EVICT_REMAP 2u   /* page-aligned remap in sq_evict_spans: a
+                                     tail page whose P kept tokens are one old
+                                     page's P tokens in order (the tokens
+                                     evicted before it are a multiple of P)
+                                     takes that old page by reference instead
+                                     of a fresh page and a copy.  Logical
+                                     views are the same; page tables and
+                                     refcounts differ from the default. */
 
 /* sq_decode_attn modes */
 #define SQ_ATTN_AUTO 0          /* shared-prefix tiles where queries share
@@ -127,12 +135,14 @@ typedef struct {
 
 typedef struct {
   int64_t tokens_removed;  /* L - L' */
-  int64_t tokens_moved;    /* kept tokens gathered into new pages: L' - P*floor(f/P) */
+  int64_t tokens_moved;    /* kept tokens gathered into new pages: L' - P*floor(f/P),
+                              less P per remapped page */
   int64_t bytes_moved;     /* bytes written by the gather: tokens_moved * (NL*Hkv*D*2*2 + 4);
                               the gather reads as many */
   int64_t pages_allocated; /* fresh pages taken for the compacted tail */
   int64_t pages_freed;     /* old pages whose last reference went away */
   int64_t first_evicted;   /* f, the first evicted index (L if none) */
+  int64_t pages_remapped;  /* tail pages taken by reference (SQ_STORE_EVICT_REMAP) */
 } sq_evict_stats;
 
 typedef struct {

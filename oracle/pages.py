@@ -102,9 +102,11 @@ class PageModel:
     """
 
     def __init__(self, num_pages, page_size, max_seqs, max_pages_per_seq,
-                 layers=1, kv_heads=1, head_dim=1, with_data=False, evict_chunk_pages=0):
+                 layers=1, kv_heads=1, head_dim=1, with_data=False, evict_chunk_pages=0,
+                 evict_remap=False):
         self.num_pages = int(num_pages)
         self.evict_chunk_pages = int(evict_chunk_pages)
+        self.evict_remap = bool(evict_remap)
         self.P = int(page_size)
         self.max_seqs = int(max_seqs)
         self.max_pages_per_seq = int(max_pages_per_seq)
@@ -151,6 +153,17 @@ class PageModel:
         while upto < n_old and (fp + upto + 1) * self.P <= consumed:
             upto += 1
         return upto
+
+    def _remap_source(self, src_of, j0, new_len):
+        """Page-aligned remap: the old index of the first of the P tokens that
+        land at new indices j0 .. j0 + P - 1 when they are one whole old page
+        in order (first at a page start, last P - 1 after it); else None."""
+        if j0 + self.P > new_len:
+            return None
+        a0 = int(src_of[j0])
+        if a0 % self.P == 0 and int(src_of[j0 + self.P - 1]) == a0 + self.P - 1:
+            return a0
+        return None
 
     def _seq(self, h):
         if h not in self.seqs:
@@ -250,7 +263,7 @@ class PageModel:
                 raise UnknownCursor(f"cursor {c} not registered")
         spans = sorted(seq.spans[c] for c in ids if seq.spans[c][1] > seq.spans[c][0])
         stats = dict(tokens_removed=0, tokens_moved=0, pages_allocated=0,
-                     pages_freed=0, first_evicted=seq.length)
+                     pages_freed=0, first_evicted=seq.length, pages_remapped=0)
         if not spans:
             for c in ids:
                 del seq.spans[c]
@@ -259,6 +272,15 @@ class PageModel:
         fp = first // self.P
         n_new = math.ceil(new_len / self.P) - fp
         old_tail = seq.pages[fp:]
+        # page-aligned remap: a full tail page whose P tokens are one old
+        # page's P tokens in order is that old page, taken by reference
+        alias = [None] * n_new
+        if self.evict_remap:
+            for k in range(n_new):
+                a0 = self._remap_source(src_of, (fp + k) * self.P, new_len)
+                if a0 is not None:
+                    alias[k] = seq.pages[a0 // self.P]
+        n_alias = sum(a is not None for a in alias)
         C = self.evict_chunk_pages if self.evict_chunk_pages > 0 else max(1, n_new)
         # the schedule: (pages to allocate, old-tail pages released after them)
         steps, released = [], 0
@@ -267,15 +289,19 @@ class PageModel:
             j_end = min((fp + k0 + c) * self.P, new_len)
             consumed = int(src_of[j_end]) if j_end < new_len else seq.length
             upto = self._released_after(fp, released, len(old_tail), consumed) if C < n_new else released
-            steps.append((c, old_tail[released:upto]))
+            steps.append((k0, c, old_tail[released:upto]))
             released = upto
-        steps.append((0, old_tail[released:]))
+        steps.append((n_new, 0, old_tail[released:]))
         # validate: every allocation must find its pages free
         free, refs = self.free_pages(), {}
-        for c, rel in steps:
-            if c > free:
+        for a in alias:
+            if a is not None:
+                refs[a] = refs.get(a, self.refcount[a]) + 1
+        for k0, c, rel in steps:
+            fresh = sum(alias[k] is None for k in range(k0, k0 + c))
+            if fresh > free:
                 raise NoPages("not enough free pages for the compacted tail")
-            free -= c
+            free -= fresh
             for page in rel:
                 refs[page] = refs.get(page, self.refcount[page]) - 1
                 free += refs[page] == 0
@@ -286,10 +312,16 @@ class PageModel:
             moved_k, moved_v = self.K[src_p, src_s].copy(), self.V[src_p, src_s].copy()
             moved_pos = self.POS[src_p, src_s].copy()
         new_pages, freed = [], 0
+        for a in alias:
+            if a is not None:
+                self.refcount[a] += 1
         self.last_schedule = []  # (pages allocated, pages released) per step
-        for c, rel in steps:
-            got = [self._alloc() for _ in range(c)]
-            new_pages += got
+        for k0, c, rel in steps:
+            got = []
+            for k in range(k0, k0 + c):
+                new_pages.append(alias[k] if alias[k] is not None else self._alloc())
+                if alias[k] is None:
+                    got.append(new_pages[-1])
             freed += sum(self._unref(page) for page in rel)
             self.last_schedule.append((got, list(rel)))
         if self.with_data and new_len > fp * self.P:
@@ -307,8 +339,9 @@ class PageModel:
             del seq.spans[c]
         seq.spans = {c: _evict.shift_span(s, e, spans) for c, (s, e) in seq.spans.items()}
         stats.update(tokens_removed=old_len - new_len,
-                     tokens_moved=new_len - fp * self.P,
-                     pages_allocated=n_new, pages_freed=freed, first_evicted=first)
+                     tokens_moved=new_len - fp * self.P - n_alias * self.P,
+                     pages_allocated=n_new - n_alias, pages_freed=freed, first_evicted=first,
+                     pages_remapped=n_alias)
         return stats
 
     # -- inspection --------------------------------------------------------

@@ -69,6 +69,9 @@ struct GatherArgs {
   int32_t new_len;        // L'
   const int32_t *src_of;
   const int32_t *pt_row;  // device page-table row, still holding the old ids
+  int32_t remap;          // 1: skip tail pages that are one old page in order
+                          //    (the host maps them to that page; same rule)
+  int32_t pad;
   NewIds ids;
 };
 

@@ -229,8 +229,12 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   const int lh = blockIdx.y;
   const int layer = lh / p.hkv;
   const int head = lh % p.hkv;
-  const int dst_page = new_page_id(a.ids, blockIdx.x);
   const int t0 = (a.fp + pi) * P;
+  if (a.remap && t0 + P <= a.new_len) {
+    const int s0 = a.src_of[t0];
+    if (s0 % P == 0 && a.src_of[t0 + P - 1] == s0 + P - 1) return; // remapped, not copied
+  }
+  const int dst_page = new_page_id(a.ids, blockIdx.x);
   if (threadIdx.x < P) {
     const int t = t0 + threadIdx.x;
     if (t < a.new_len) {

@@ -90,6 +90,7 @@ bool shape_ok(const sq_store_config *c, bool device, std::string *why) {
   if ((int64_t)c->max_pages_per_seq * c->page_size > (int64_t)INT32_MAX / 2)
     return bad("max_pages_per_seq * page_size too large");
   if (c->evict_chunk_pages < 0) return bad("evict_chunk_pages must be >= 0");
+  if (c->flags & ~(SQ_STORE_METADATA_ONLY | SQ_STORE_EVICT_REMAP)) return bad("unknown flags");
   if (device) {
     const int grp = c->num_q_heads / c->num_kv_heads;
     if (c->page_size != sq::kPage) return bad("device mode needs page_size 16");
@@ -982,6 +983,26 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     const size_t k = std::upper_bound(gap_dst.begin(), gap_dst.end(), j) - gap_dst.begin() - 1;
     return j + gap_shift[k];
   };
+  // Page-aligned remap: tail page k whose P tokens are one old page's P
+  // tokens in order takes that page by reference (no fresh page, no copy).
+  const bool remap = (s->cfg.flags & SQ_STORE_EVICT_REMAP) != 0;
+  std::vector<int32_t> alias(n_new, -1);
+  int64_t n_alias = 0;
+  if (remap)
+    for (int64_t k = 0; k < n_new; ++k) {
+      const int64_t j0 = (fp + k) * s->P;
+      if (j0 + s->P > Lp) continue;
+      const int64_t a0 = src_index(j0);
+      if (a0 % s->P == 0 && src_index(j0 + s->P - 1) == a0 + s->P - 1) {
+        alias[k] = q->pages[a0 / s->P];
+        ++n_alias;
+      }
+    }
+  auto fresh_in = [&](int64_t k0, int64_t c) {
+    int64_t n = 0;
+    for (int64_t k = k0; k < k0 + c; ++k) n += alias[k] < 0;
+    return n;
+  };
 
   // The schedule: fresh pages per step and the old-tail pages released after
   // it.  One-shot (evict_chunk_pages = 0): every fresh page first, every old
@@ -1011,13 +1032,23 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     steps.push_back({n_new, 0, released, old_tail.size()});
   }
   {
+    std::vector<int32_t> extra; // references the remap adds to old pages
+    for (int64_t k = 0; k < n_new; ++k)
+      if (alias[k] >= 0) extra.push_back(alias[k]);
+    std::sort(extra.begin(), extra.end());
     int64_t free_now = s->n_free;
     for (const Step &st : steps) {
-      if (st.c > free_now)
+      const int64_t c = fresh_in(st.k0, st.c);
+      if (c > free_now)
         return fail(SQ_ERR_NO_PAGES, "eviction needs %lld fresh pages at once, %lld free",
-                    (long long)st.c, (long long)free_now);
-      free_now -= st.c;
-      for (size_t i = st.rel_begin; i < st.rel_end; ++i) free_now += s->refcount[old_tail[i]] == 1;
+                    (long long)c, (long long)free_now);
+      free_now -= c;
+      for (size_t i = st.rel_begin; i < st.rel_end; ++i) {
+        const int32_t pg = old_tail[i];
+        const int32_t add = (int32_t)(std::upper_bound(extra.begin(), extra.end(), pg) -
+                                      std::lower_bound(extra.begin(), extra.end(), pg));
+        free_now += s->refcount[pg] + add == 1;
+      }
     }
   }
 
@@ -1026,8 +1057,14 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
   // then the host bookkeeping ----
   std::vector<int32_t> new_ids(n_new);
   int64_t freed = 0;
+  for (int64_t k = 0; k < n_new; ++k)
+    if (alias[k] >= 0) {
+      ++s->refcount[alias[k]];
+      new_ids[k] = alias[k];
+    }
   for (const Step &st : steps) {
-    if (st.c) s->alloc_pages(st.c, new_ids.data() + st.k0);
+    for (int64_t k = st.k0; k < st.k0 + st.c; ++k)
+      if (alias[k] < 0) s->alloc_pages(1, &new_ids[k]);
     for (size_t i = st.rel_begin; i < st.rel_end; ++i) s->unref(old_tail[i], &freed);
   }
 
@@ -1091,6 +1128,7 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
       ga.new_len = (int32_t)Lp;
       ga.src_of = s->ev_src;
       ga.pt_row = s->pt_row(h);
+      ga.remap = remap ? 1 : 0;
       if (all_inline) {
         runs_of(st.k0, st.c, &ga.ids); // a sub-range has no more runs than the whole
       } else {
@@ -1150,12 +1188,13 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     se = {ns, ne};
     if (ne > ns) q->nonempty[ns] = ne;
   }
-  const int64_t moved = Lp - fp * s->P;
+  const int64_t moved = Lp - fp * s->P - n_alias * s->P;
   const int64_t per_tok = (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2 + 4;
   es.tokens_removed = removed;
   es.tokens_moved = moved;
   es.bytes_moved = moved * per_tok;
-  es.pages_allocated = n_new;
+  es.pages_allocated = n_new - n_alias;
+  es.pages_remapped = n_alias;
   es.pages_freed = freed;
   es.first_evicted = f;
   ++s->st.evict_calls;

@@ -17,6 +17,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsq.so")
 
 OK, ERR_INVALID, ERR_NO_PAGES, ERR_UNKNOWN_SEQ, ERR_UNKNOWN_CURSOR, ERR_SPAN, ERR_HIP = range(7)
 STORE_METADATA_ONLY = 1
+STORE_EVICT_REMAP = 2
 ATTN_AUTO, ATTN_STREAM, ATTN_SHARED_PREFIX, ATTN_MFMA = 0, 1, 2, 3
 MAX_BATCH = 64
 MAX_EVICT_SPANS = 16384
@@ -52,7 +53,8 @@ class SeqDesc(C.Structure):
 
 class EvictStats(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("tokens_removed", "tokens_moved", "bytes_moved",
-                                         "pages_allocated", "pages_freed", "first_evicted")]
+                                         "pages_allocated", "pages_freed", "first_evicted",
+                                         "pages_remapped")]
 
 
 class Stats(C.Structure):
@@ -178,19 +180,21 @@ class Store:
 
     def __init__(self, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages, max_seqs,
                  max_pages_per_seq, page_size=16, device="cuda", metadata_only=False,
-                 evict_chunk_pages=0):
+                 evict_chunk_pages=0, evict_remap=False):
         self.cfg = StoreConfig(num_layers, num_q_heads, num_kv_heads, head_dim, page_size,
                                num_pages, max_seqs, max_pages_per_seq)
         self.cfg.evict_chunk_pages = evict_chunk_pages
         self.evict_chunk_pages = evict_chunk_pages
+        self.evict_remap = bool(evict_remap)
         self.metadata_only = metadata_only
         self.num_layers, self.num_q_heads, self.num_kv_heads = num_layers, num_q_heads, num_kv_heads
         self.head_dim, self.page_size, self.num_pages = head_dim, page_size, num_pages
         self.max_seqs, self.max_pages_per_seq = max_seqs, max_pages_per_seq
         L = lib()
         self._handle = C.c_void_p()
+        self.cfg.flags = STORE_EVICT_REMAP if evict_remap else 0
         if metadata_only:
-            self.cfg.flags = STORE_METADATA_ONLY
+            self.cfg.flags |= STORE_METADATA_ONLY
             self.k_pool = self.v_pool = self.pos_pool = self.workspace = None
         else:
             import torch

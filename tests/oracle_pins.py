@@ -238,15 +238,19 @@ def _state(model):
                            for h, s in model.seqs.items()}, model.peak_pages))
 
 
-def check_against_list_model(seed=10, n_ops=60, chunks=(0,)):
+def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False):
     """Random op sequences: the page model's logical views equal a naive list
-    model's, for page sizes 1, 2, 4 and 16 (and each eviction chunk size)."""
+    model's, for page sizes 1, 2, 4 and 16 (and each eviction chunk size).
+    With ``remap`` half the marked spans are whole multiples of the page size,
+    so that page-aligned remaps happen; returns the pages remapped."""
     rng = np.random.default_rng(seed)
     nl, hkv, d = 2, 2, 3
+    remapped = 0
     for page, chunk in itertools.product([1, 2, 4, 16], chunks):
         model = pg.PageModel(num_pages=400, page_size=page, max_seqs=6,
                              max_pages_per_seq=400, layers=nl, kv_heads=hkv,
-                             head_dim=d, with_data=True, evict_chunk_pages=chunk)
+                             head_dim=d, with_data=True, evict_chunk_pages=chunk,
+                             evict_remap=remap)
         ref = ListModel()
         next_cursor = 0
         h0 = model.seq_create()
@@ -265,6 +269,9 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,)):
                 length = model.info(h)["length"]
                 s = int(rng.integers(0, length + 1))
                 e = int(rng.integers(s, length + 1))
+                if remap and rng.random() < 0.5:
+                    s = s // page * page
+                    e = s + (e - s) // page * page
                 try:
                     model.span_mark(h, next_cursor, s, e)
                     ref.spans[h][next_cursor] = (s, e)
@@ -278,7 +285,7 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,)):
             elif op == "evict":
                 cur = list(model.spans(h))
                 pick = [c for c in cur if rng.random() < 0.5]
-                model.evict(h, pick)
+                remapped += model.evict(h, pick)["pages_remapped"]
                 ref.evict(h, pick)
             elif op == "release" and len(live) > 1:
                 model.release(h)
@@ -302,6 +309,7 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,)):
         for h in list(model.seqs):
             model.release(h)
         assert model.live_pages() == 0
+    return remapped
 
 
 def check_hand_worked_page_tables():
@@ -322,7 +330,7 @@ def check_hand_worked_page_tables():
     st = m.evict(a, [7])                 # L' = 5 -> 2 new pages: 5, 6
     assert m.page_table(a) == [5, 6]
     assert st == dict(tokens_removed=5, tokens_moved=5, pages_allocated=2,
-                      pages_freed=1, first_evicted=1)  # page 2 was a's alone
+                      pages_freed=1, first_evicted=1, pages_remapped=0)  # page 2 was a's alone
     assert m.view(a)[2].tolist() == [0, 6, 7, 8, 9]
     assert m.refcount[:7].tolist() == [2, 1, 0, 1, 1, 1, 1]
     m.release(c)                         # page 0 -> 1 ref, page 3 freed
@@ -682,6 +690,48 @@ def check_chunked_eviction_fits_where_one_shot_does_not():
             assert _state(m) == snap
 
 
+# --------------------------------------------------------------------------
+# page-aligned remap
+# --------------------------------------------------------------------------
+def check_remap_against_list_model():
+    """With page-aligned remap (alone and with chunks) every logical view,
+    span and position equals the naive list model's, refcounts match the page
+    lists, and remaps do happen."""
+    assert check_against_list_model(seed=21, n_ops=60, chunks=(0, 2), remap=True) > 0
+
+
+def check_remap_page_tables_by_hand():
+    """P = 4, 16 tokens in pages [0, 1, 2, 3].  Evicting [0, 4) shifts by one
+    page: pages 1, 2, 3 become the whole list, nothing is copied, page 0 is
+    freed.  Evicting [2, 6) also shifts by 4: new page 0 holds tokens
+    0, 1, 6, 7 (fresh page 4), new pages 1 and 2 are old pages 2 and 3.
+    Evicting [1, 3) shifts by 2: nothing lines up, as without remap."""
+    cases = [((0, 4), [1, 2, 3], dict(pages_remapped=3, pages_allocated=0, pages_freed=1,
+                                      tokens_moved=0)),
+             ((2, 6), [4, 2, 3], dict(pages_remapped=2, pages_allocated=1, pages_freed=2,
+                                      tokens_moved=4)),
+             ((1, 3), [4, 5, 6, 7], dict(pages_remapped=0, pages_allocated=4, pages_freed=4,
+                                         tokens_moved=14))]
+    for chunk in (0, 1):
+        for (s0, e0), table, want in cases:
+            m = pg.PageModel(num_pages=12, page_size=4, max_seqs=2, max_pages_per_seq=8,
+                             with_data=True, evict_chunk_pages=chunk, evict_remap=True)
+            a = m.seq_create()
+            k = np.arange(16, dtype=np.float64).reshape(1, 16, 1, 1)
+            m.append(a, 16, k, -k)
+            m.span_mark(a, 0, s0, e0)
+            st = m.evict(a, [0])
+            keep = [t for t in range(16) if not s0 <= t < e0]
+            assert m.view(a)[0][:, 0, 0, 0].tolist() == keep
+            assert m.view(a)[1][:, 0, 0, 0].tolist() == [-t for t in keep]
+            assert m.view(a)[2].tolist() == keep
+            if chunk == 0 or want["pages_remapped"]:
+                assert m.page_table(a) == table, (chunk, s0, m.page_table(a))
+            for key, val in want.items():
+                assert st[key] == val, (chunk, s0, key, st[key], val)
+            assert m.refcount.sum() == len(m.page_table(a))
+
+
 ALL_CHECKS = [
     check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
     check_uniform_closed_form, check_two_key_closed_form,
@@ -695,4 +745,5 @@ ALL_CHECKS = [
     check_chunked_eviction_against_list_model, check_chunked_page_tables_by_hand,
     check_chunked_eviction_fits_where_one_shot_does_not,
     check_chunked_eviction_never_overwrites_unread_tokens,
+    check_remap_against_list_model, check_remap_page_tables_by_hand,
 ]

@@ -46,7 +46,8 @@ def oracle_model_for(store, with_data=True):
     return opg.PageModel(store.num_pages, store.page_size, store.max_seqs,
                          store.max_pages_per_seq, layers=store.num_layers,
                          kv_heads=store.num_kv_heads, head_dim=store.head_dim,
-                         with_data=with_data, evict_chunk_pages=store.evict_chunk_pages)
+                         with_data=with_data, evict_chunk_pages=store.evict_chunk_pages,
+                         evict_remap=store.evict_remap)
 
 
 def run_tiny(sq, device="cuda", modes=None, with_oracle=True):
@@ -139,12 +140,13 @@ class Twin:
     (with data), drawing the same seeded bf16 inputs for both."""
 
     def __init__(self, sq, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
-                 max_seqs, max_pages_per_seq, seed=0, device="cuda", evict_chunk_pages=0):
+                 max_seqs, max_pages_per_seq, seed=0, device="cuda", evict_chunk_pages=0,
+                 evict_remap=False):
         self.sq = sq
         self.device = device
         self.store = sq.Store(num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
                               max_seqs, max_pages_per_seq, device=device,
-                              evict_chunk_pages=evict_chunk_pages)
+                              evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap)
         self.model = oracle_model_for(self.store)
         self.rng = np.random.default_rng([2602, 900, seed])
         self.nl, self.hq, self.hkv, self.d = num_layers, num_q_heads, num_kv_heads, head_dim
@@ -266,3 +268,29 @@ class Twin:
             ref = oatt.decode_batch(qf[l], views, scale, self.group)
             err = max(err, max_abs(got[l], ref))
         return err, got
+
+
+def tiny_step_error(sq, res, device="cuda"):
+    """One fused decode step (sq_step_begin + sq_step_attn) of the tiny case's
+    main and auxiliary threads after its eviction, against the oracle's
+    one-token append and attention; returns the max abs error."""
+    import torch
+    w, o = res["workload"], res["oracle"]
+    store, model = res["store"], o["model"]
+    rng = np.random.default_rng([2602, 0, 77])
+    hkv, hq, d = w.num_kv_heads, w.num_q_heads, w.head_dim
+    kb = wl.normal_bf16(rng, (1, 2, hkv, d))
+    vb = wl.normal_bf16(rng, (1, 2, hkv, d))
+    qb = wl.normal_bf16(rng, (2, hq, d))
+    store.step_begin([res["main"], res["aux"]])
+    out = store.step_attn(0, wl.to_torch_bf16(kb[0], device), wl.to_torch_bf16(vb[0], device),
+                          wl.to_torch_bf16(qb, device), scale=w.scale)
+    torch.cuda.synchronize()
+    kf, vf = wl.bf16_value(kb), wl.bf16_value(vb)
+    views = []
+    for j, h in enumerate((o["main"], o["aux"])):
+        model.append(h, 1, kf[:, j:j + 1], vf[:, j:j + 1])
+        k, v, _ = model.view(h)
+        views.append((k[:, 0], v[:, 0]))
+    ref = oatt.decode_batch(wl.bf16_value(qb), views, w.scale, hq // hkv)
+    return max_abs(out.cpu().numpy(), ref)

@@ -44,10 +44,11 @@ def test_library_exports_every_declared_symbol(sq):
     assert lib.sq_abi_version() == version
 
 
-def _store(sq, num_pages, page, max_seqs, max_pages, chunk=0):
+def _store(sq, num_pages, page, max_seqs, max_pages, chunk=0, remap=False):
     return sq.Store(num_layers=2, num_q_heads=4, num_kv_heads=2, head_dim=8,
                     num_pages=num_pages, max_seqs=max_seqs, max_pages_per_seq=max_pages,
-                    page_size=page, metadata_only=True, evict_chunk_pages=chunk)
+                    page_size=page, metadata_only=True, evict_chunk_pages=chunk,
+                    evict_remap=remap)
 
 
 def _compare(store, model):
@@ -83,12 +84,15 @@ def _both(store, model, sq, fn_store, fn_model):
 
 
 @pytest.mark.parametrize("page", [1, 2, 4, 16])
-@pytest.mark.parametrize("seed,chunk", [(0, 0), (1, 0), (2, 1), (3, 2), (4, 5)])
-def test_random_ops_match_oracle(sq, page, seed, chunk):
+@pytest.mark.parametrize("seed,chunk,remap", [(0, 0, False), (1, 0, False), (2, 1, False),
+                                              (3, 2, False), (4, 5, False), (5, 0, True),
+                                              (6, 2, True)])
+def test_random_ops_match_oracle(sq, page, seed, chunk, remap):
     rng = np.random.default_rng(100 + seed * 7 + page)
     num_pages, max_seqs, max_pages = 300 // page + 40, 5, 400 // page + 8
-    store = _store(sq, num_pages, page, max_seqs, max_pages, chunk)
-    model = pg.PageModel(num_pages, page, max_seqs, max_pages, evict_chunk_pages=chunk)
+    store = _store(sq, num_pages, page, max_seqs, max_pages, chunk, remap)
+    model = pg.PageModel(num_pages, page, max_seqs, max_pages, evict_chunk_pages=chunk,
+                         evict_remap=remap)
     cursor = 0
     h0, _ = _both(store, model, sq, store.seq_create, model.seq_create)
     for _ in range(250):
@@ -118,6 +122,9 @@ def test_random_ops_match_oracle(sq, page, seed, chunk):
             length = model.info(h)["length"]
             s = int(rng.integers(0, length + 1))
             e = int(rng.integers(s, min(length, s + 40) + 1))
+            if remap and rng.random() < 0.5:  # whole pages: remaps happen
+                s = s // page * page
+                e = s + (e - s) // page * page
             c = cursor if rng.random() < 0.9 else int(rng.integers(0, cursor + 1))
             _both(store, model, sq, lambda: store.span_mark(h, c, s, e),
                   lambda: model.span_mark(h, c, s, e))

@@ -179,6 +179,49 @@ def test_chunked_eviction_recycles_pages_bitexact(sq, chunk):
         assert before > 0
 
 
+@pytest.mark.parametrize("chunk", [0, 2])
+def test_remap_eviction_bitexact(sq, chunk):
+    """Page-aligned remap: spans of whole pages (and some ragged ones) evicted
+    from a main thread whose auxiliary fork is still alive; tail pages that
+    are one old page in order are taken by reference, the rest gathered.
+    Page tables, refcounts and the K/V/pos views equal the oracle's remap
+    mode bit for bit; decode matches the oracle; forks and decode steps of
+    the result too."""
+    t = sc.Twin(sq, 2, 8, 2, 128, 700, 6, 200, seed=31 + chunk, evict_chunk_pages=chunk,
+                evict_remap=True)
+    rng = np.random.default_rng(31)
+    main = t.create()
+    t.append(main, 2000)
+    aux = t.fork(main, 1600)
+    t.append(aux, 21)
+    cursor, remapped = 0, 0
+    for rnd in range(5):
+        length = t.model.info(main)["length"]
+        cuts = sorted(rng.choice(np.arange(length // 16), 8, replace=False).tolist())
+        ids = []
+        for i in range(0, 8, 2):
+            s0, e0 = 16 * cuts[i], 16 * cuts[i + 1]
+            if i == 6 and rnd % 2:
+                e0 -= 5                  # one ragged span per odd round
+            if t.try_mark(main, cursor, s0, e0):
+                ids.append(cursor)
+            cursor += 1
+        st = t.evict(main, ids)
+        remapped += st["pages_remapped"]
+        t.check_state()
+        errs, _ = t.decode_errors([main, aux], layer=rnd % 2)
+        assert max(errs.values()) <= TOL, errs
+        t.append(main, 16 * int(rng.integers(1, 6)))
+        err, _ = t.step([main, aux])
+        assert err <= TOL
+    assert remapped > 0
+    c = t.fork(main, 160)              # a fork of remapped pages
+    t.append(c, 9)
+    t.check_state()
+    errs, _ = t.decode_errors([main, aux, c])
+    assert max(errs.values()) <= TOL, errs
+
+
 def test_all_keep_eviction_leaves_bytes(sq):
     import torch
     t = sc.Twin(sq, 1, 4, 1, 64, 64, 4, 32, seed=3)

@@ -174,6 +174,22 @@ def _evict_chunk_never_recycles(self, h, cursor_ids):
         self.evict_chunk_pages = chunk
 
 
+def _remap_page_start_only(self, src_of, j0, new_len):
+    # takes the old page whenever the first token starts one, runs or not
+    if j0 + self.P > new_len:
+        return None
+    a0 = int(src_of[j0])
+    return a0 if a0 % self.P == 0 else None
+
+
+_orig_remap_source = pg.PageModel._remap_source
+
+
+def _remap_next_page(self, src_of, j0, new_len):
+    a0 = _orig_remap_source(self, src_of, j0, new_len)
+    return None if a0 is None else a0 + self.P
+
+
 MUTANTS = {
     "gqa_head_modulo": (att, "scores", _scores_gqa_modulo),
     "missing_scale": (att, "scores", _scores_no_scale),
@@ -194,6 +210,8 @@ MUTANTS = {
     "extend_ignores_mask": (ex, "extend_attention", _extend_ignores_mask),
     "evict_chunks_never_recycle": (pg.PageModel, "evict", _evict_chunk_never_recycles),
     "evict_chunk_releases_a_page_early": (pg.PageModel, "_released_after", _released_one_page_early),
+    "remap_without_run_check": (pg.PageModel, "_remap_source", _remap_page_start_only),
+    "remap_takes_the_next_page": (pg.PageModel, "_remap_source", _remap_next_page),
 }
 
 
