@@ -254,9 +254,10 @@ def time_events(torch, fn, reps, flush=None):
     return percentiles([a.elapsed_time(b) for a, b in ev])
 
 
-def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True):
+def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False):
     from paper_2602_22603_amd import drivers
-    store, base, w, k, v = drivers.build_compaction64k(evict_chunk_pages=chunk)
+    store, base, w, k, v = drivers.build_compaction64k(evict_chunk_pages=chunk, align=align,
+                                                       evict_remap=remap)
     L = w.length
     del k, v
     torch.cuda.synchronize()
@@ -280,7 +281,11 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True):
     scan_ms = prof["evict_scan_ms"] / max(1, prof["evict_scan_launches"])
     moved = 2 * stats["bytes_moved"]  # read + write
     if not decode:
-        info = dict(evict_chunk_pages=chunk, gather_launches_per_call=prof["evict_gather_launches"] // reps,
+        info = dict(evict_chunk_pages=chunk, remap=remap, span_align=align,
+                    tokens_removed=stats["tokens_removed"], tokens_moved=stats["tokens_moved"],
+                    pages_allocated=stats["pages_allocated"], pages_remapped=stats["pages_remapped"],
+                    bytes_read_plus_written=2 * stats["bytes_moved"],
+                    gather_launches_per_call=prof["evict_gather_launches"] // reps,
                     gather_ms_per_call=prof["evict_gather_ms"] / reps,
                     evict_wall_ms_median=sorted(walls)[len(walls) // 2] * 1e3,
                     evict_gbps_wall=2 * stats["bytes_moved"] / (sorted(walls)[len(walls) // 2]) / 1e9)
@@ -622,6 +627,10 @@ def main():
         evict = evict_leg(sq, torch, wl)
         torch.cuda.empty_cache()
         evict["chunked_256_pages"] = evict_leg(sq, torch, wl, chunk=256, decode=False)
+        # tool spans that start and end on page boundaries: gathered, or remapped
+        evict["page_aligned_spans_copy"] = evict_leg(sq, torch, wl, decode=False, align=16)
+        evict["page_aligned_spans_remap"] = evict_leg(sq, torch, wl, decode=False, align=16,
+                                                      remap=True)
     if "copy" in legs:
         log("calibration copy: 1 GiB device-to-device ...")
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)

@@ -987,6 +987,7 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
   // tokens in order takes that page by reference (no fresh page, no copy).
   const bool remap = (s->cfg.flags & SQ_STORE_EVICT_REMAP) != 0;
   std::vector<int32_t> alias(n_new, -1);
+  std::vector<char> old_aliased(q->pages.size() - fp, 0); // by old-tail index
   int64_t n_alias = 0;
   if (remap)
     for (int64_t k = 0; k < n_new; ++k) {
@@ -995,6 +996,7 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
       const int64_t a0 = src_index(j0);
       if (a0 % s->P == 0 && src_index(j0 + s->P - 1) == a0 + s->P - 1) {
         alias[k] = q->pages[a0 / s->P];
+        old_aliased[a0 / s->P - fp] = 1;
         ++n_alias;
       }
     }
@@ -1032,10 +1034,6 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     steps.push_back({n_new, 0, released, old_tail.size()});
   }
   {
-    std::vector<int32_t> extra; // references the remap adds to old pages
-    for (int64_t k = 0; k < n_new; ++k)
-      if (alias[k] >= 0) extra.push_back(alias[k]);
-    std::sort(extra.begin(), extra.end());
     int64_t free_now = s->n_free;
     for (const Step &st : steps) {
       const int64_t c = fresh_in(st.k0, st.c);
@@ -1043,12 +1041,8 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
         return fail(SQ_ERR_NO_PAGES, "eviction needs %lld fresh pages at once, %lld free",
                     (long long)c, (long long)free_now);
       free_now -= c;
-      for (size_t i = st.rel_begin; i < st.rel_end; ++i) {
-        const int32_t pg = old_tail[i];
-        const int32_t add = (int32_t)(std::upper_bound(extra.begin(), extra.end(), pg) -
-                                      std::lower_bound(extra.begin(), extra.end(), pg));
-        free_now += s->refcount[pg] + add == 1;
-      }
+      for (size_t i = st.rel_begin; i < st.rel_end; ++i)
+        free_now += s->refcount[old_tail[i]] + old_aliased[i] == 1; // a remap adds a reference
     }
   }
 

@@ -52,19 +52,24 @@ def shared_task_inputs(w, t, device="cuda"):
     return k, v, ka, va
 
 
-def build_compaction64k(device="cuda", extra_tokens=256, evict_chunk_pages=0):
+def build_compaction64k(device="cuda", extra_tokens=256, evict_chunk_pages=0, align=0,
+                        evict_remap=False):
     """The 64K compaction workload: one sequence with its 40 tool spans
-    marked.  Returns (store, base_seq, workload, k, v)."""
+    marked (with ``align`` > 0 each span's ends rounded down to a multiple of
+    it, as when every tool response starts on a page).  Returns (store,
+    base_seq, workload, k, v)."""
     w = wl.compaction64k()
     L = w.length
     store = _sq.Store(1, 32, 8, 128, num_pages=2 * (L // 16) + 2 * (extra_tokens // 16) + 64,
                       max_seqs=4, max_pages_per_seq=L // 16 + extra_tokens // 16 + 32,
-                      device=device, evict_chunk_pages=evict_chunk_pages)
+                      device=device, evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap)
     k = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000, device)
     v = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000 + 1, device)
     base = store.seq_create()
     store.append(base, k, v)
     for c, (s, e) in enumerate(w.spans):
+        if align:
+            s, e = s // align * align, e // align * align
         store.span_mark(base, c, s, e)
     return store, base, w, k, v
 
