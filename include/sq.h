@@ -255,8 +255,14 @@ sq_status sq_release(sq_store *store, sq_seq seq);
  * tokens [P*floor(f/P), L') from the old pages: K, V of every layer and head
  * and their positions, which are carried unchanged.  Then every old page
  * from f/P on loses one reference.  Pages another live branch still holds
- * survive, so other branches keep attending to what they saw.  Remaining
- * spans shift left by the evicted tokens before them.  Evicting only empty
+ * survive, so other branches keep attending to what they saw.  With
+ * evict_chunk_pages > 0 the fresh pages come in chunks (see the config).
+ * With SQ_STORE_EVICT_REMAP a full tail page whose P kept tokens are one old
+ * page's P tokens in order takes that old page by reference (no fresh page,
+ * nothing copied): this happens behind every evicted run whose evicted
+ * tokens so far are a multiple of P, e.g. spans that start and end on
+ * pages.  Remaining spans shift left by the evicted tokens before them.
+ * Evicting only empty
  * spans (or none) only unregisters the cursors.  Issue it after the main
  * thread's turn (§3.1 step 4).  stats may be NULL.
  * SQ_ERR_UNKNOWN_CURSOR: a cursor is not registered on seq;

@@ -1114,7 +1114,7 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "eviction index");
     for (const Step &st : steps) {
-      if (st.c == 0) continue;
+      if (st.c == 0 || fresh_in(st.k0, st.c) == 0) continue; // nothing to copy
       sq::GatherArgs ga{};
       ga.fp = (int32_t)fp;
       ga.pi0 = (int32_t)st.k0;
