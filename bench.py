@@ -54,11 +54,15 @@ def parse_args():
     return ap.parse_args()
 
 
-def kernel_sha():
-    """Hash of the sources the decode kernels are built from (the committed
-    counter summaries are valid only for the sources they were taken on)."""
+DECODE_SOURCES = ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp")
+EXTEND_SOURCES = ("extend_kernels.hip", "extend_args.hpp", "sq_common.hpp")
+
+
+def kernel_sha(files=DECODE_SOURCES):
+    """Hash of the sources a kernel is built from (the committed counter
+    summaries are valid only for the sources they were taken on)."""
     h = hashlib.sha256()
-    for f in ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp"):
+    for f in files:
         with open(os.path.join(ROOT, "paper_2602_22603_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -690,6 +694,7 @@ def main():
         "full_stack": fullstack,
         "cpu_baseline": cpu,
         "kernel_sources_sha": kernel_sha(),
+        "extend_kernel_sources_sha": kernel_sha(EXTEND_SOURCES),
     }
     print(json.dumps(res), flush=True)
 

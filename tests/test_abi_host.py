@@ -316,6 +316,31 @@ def test_decode_step_metadata(sq):
     assert rc == sq.ERR_INVALID and b"metadata-only" in sq.lib().sq_last_error()
 
 
+def test_decode_plan_worst_case_segments(sq):
+    """The most segments 64 entries can need: with at most 4 entries per MFMA
+    tile, a tile's run splits into two shared pairs and four private tails
+    (7 segments per 4 entries, 112 for 64), below the 128 one decode call
+    holds.  Eight trees of root -> 2 -> 4 -> 8 forks (P = 4) reach it."""
+    s = _store(sq, 4000, 4, 255, 64)
+    leaves = []
+    for _ in range(8):
+        r = s.seq_create()
+        s.append(r, n=8)
+        for _ in range(2):
+            m = s.fork(r, 8)
+            s.append(m, n=4)
+            for _ in range(2):
+                x = s.fork(m, 12)
+                s.append(x, n=4)
+                for _ in range(2):
+                    y = s.fork(x, 16)
+                    s.append(y, n=1)
+                    leaves.append(y)
+    info = s.plan_info(leaves)
+    assert info["n_segments"] == 112 and info["n_groups"] == 48
+    assert info["kv_bytes"] < info["kv_bytes_logical"]
+
+
 def test_invalid_configurations(sq):
     with pytest.raises(sq.SqError):
         sq.Store(1, 3, 2, 8, 16, 2, 4, page_size=4, metadata_only=True)  # 3 % 2

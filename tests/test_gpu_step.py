@@ -40,7 +40,8 @@ def _modes(sq):
 
 
 @pytest.mark.parametrize("mi", [0, 1, 2, 3])
-@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64), (4, 4, 128)])
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64), (4, 4, 128), (64, 8, 64),
+                                      (8, 4, 128)])
 def test_steps_match_oracle(sq, mi, hq, hkv, d):
     """A main thread, its forked auxiliary thread, a sequence ending mid-page
     and an empty one, stepped 20 times in every mode (page boundaries are
