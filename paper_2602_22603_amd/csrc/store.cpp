@@ -786,8 +786,11 @@ sq_status sq_append(sq_store *s, sq_seq h, int32_t n, const void *k_new, const v
   return SQ_OK;
 }
 
-sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const void *k_new,
-                          const void *v_new, void *stream) {
+namespace {
+
+// One token for each of `batch` distinct sequences (sq_append_batch and
+// sq_step_begin): the checks, made before anything changes.
+sq_status check_one_token_each(sq_store *s, const sq_seq *seqs, int32_t batch) {
   if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
   if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
   int64_t need = 0;
@@ -805,29 +808,56 @@ sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const 
   }
   if (need > s->n_free) return fail(SQ_ERR_NO_PAGES, "append needs %lld pages, %lld free",
                                     (long long)need, (long long)s->n_free);
-  if (s->device) {
-    if (!k_new || !v_new) return fail(SQ_ERR_INVALID, "null K/V");
-    if (!aligned16(k_new) || !aligned16(v_new)) return fail(SQ_ERR_INVALID, "K/V must be 16-byte aligned");
-  }
+  return SQ_OK;
+}
+
+// ... and the change: each sequence gets its next slot (a new page when its
+// last one is full, lowest id first, in batch order) and position.  Returns
+// where each token goes: page, slot, position and the page-table index to
+// set (or -1).
+struct TokenSlots {
+  int32_t page[sq::kMaxBatch], slot[sq::kMaxBatch], pos[sq::kMaxBatch], pt_index[sq::kMaxBatch];
+};
+void take_one_token_each(sq_store *s, const sq_seq *seqs, int32_t batch, TokenSlots *t) {
   ++s->gen;
-  sq::AppendBatchArgs a{};
-  a.n = batch;
-  a.pt = s->pt_dev;
   for (int b = 0; b < batch; ++b) {
     Seq &q = s->seqs[seqs[b]];
-    a.pt_index[b] = -1;
+    t->pt_index[b] = -1;
     if (q.length % s->P == 0) {
       q.pages.push_back(s->alloc_page());
-      a.pt_index[b] = seqs[b] * s->cfg.max_pages_per_seq + (int32_t)q.pages.size() - 1;
+      t->pt_index[b] = seqs[b] * s->cfg.max_pages_per_seq + (int32_t)q.pages.size() - 1;
     }
-    a.page[b] = q.pages[q.length / s->P];
-    a.slot[b] = (int32_t)(q.length % s->P);
-    a.pos[b] = (int32_t)q.next_pos;
+    t->page[b] = q.pages[q.length / s->P];
+    t->slot[b] = (int32_t)(q.length % s->P);
+    t->pos[b] = (int32_t)q.next_pos;
     runs_append(q, 1);
     q.length += 1;
     q.next_pos += 1;
   }
   s->st.append_tokens += batch;
+}
+
+} // namespace
+
+sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const void *k_new,
+                          const void *v_new, void *stream) {
+  sq_status r = check_one_token_each(s, seqs, batch);
+  if (r != SQ_OK) return r;
+  if (s->device) {
+    if (!k_new || !v_new) return fail(SQ_ERR_INVALID, "null K/V");
+    if (!aligned16(k_new) || !aligned16(v_new)) return fail(SQ_ERR_INVALID, "K/V must be 16-byte aligned");
+  }
+  TokenSlots t;
+  take_one_token_each(s, seqs, batch, &t);
+  sq::AppendBatchArgs a{};
+  a.n = batch;
+  a.pt = s->pt_dev;
+  for (int b = 0; b < batch; ++b) {
+    a.page[b] = t.page[b];
+    a.slot[b] = t.slot[b];
+    a.pos[b] = t.pos[b];
+    a.pt_index[b] = t.pt_index[b];
+  }
   if (!s->device) return SQ_OK;
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
@@ -1272,29 +1302,14 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
 
 sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,
                         void *stream) {
-  if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
-  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
+  sq_status r = check_one_token_each(s, seqs, batch);
+  if (r != SQ_OK) return r;
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
   if (s->device && mode != SQ_ATTN_STREAM && s->mfma_waves != 4)
     return fail(SQ_ERR_INVALID, "decode steps need 4 waves per MFMA work item");
-  int64_t need = 0;
-  for (int b = 0; b < batch; ++b) {
-    Seq *q = s->get(seqs[b]);
-    if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
-    for (int c = 0; c < b; ++c)
-      if (seqs[c] == seqs[b]) return fail(SQ_ERR_INVALID, "sequence %d repeated in the batch", seqs[b]);
-    if (q->length % s->P == 0) {
-      if (q->length / s->P + 1 > s->cfg.max_pages_per_seq)
-        return fail(SQ_ERR_INVALID, "sequence %d is at its page-list capacity", seqs[b]);
-      ++need;
-    }
-    if (s->device && q->next_pos + 1 > INT32_MAX) return fail(SQ_ERR_INVALID, "positions exceed int32");
-  }
-  if (need > s->n_free) return fail(SQ_ERR_NO_PAGES, "step needs %lld pages, %lld free",
-                                    (long long)need, (long long)s->n_free);
   // attention over the tokens before the step; the new ones join in the merge
   Plan plan;
-  sq_status r = build_plan(s, seqs, batch, mode, &plan);
+  r = build_plan(s, seqs, batch, mode, &plan);
   if (r != SQ_OK) return r;
   // which launches a layer makes depends on the mode only, so that a
   // captured step replays for every later step of the same batch and mode
@@ -1314,25 +1329,15 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
     fill_dyn(s, plan, sp->dec, &sp->merge);
   }
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
-  ++s->gen;
-  for (int b = 0; b < batch; ++b) {
-    Seq &q = s->seqs[seqs[b]];
-    int32_t pti = -1;
-    if (q.length % s->P == 0) {
-      q.pages.push_back(s->alloc_page());
-      pti = seqs[b] * s->cfg.max_pages_per_seq + (int32_t)q.pages.size() - 1;
+  TokenSlots t;
+  take_one_token_each(s, seqs, batch, &t);
+  if (sp)
+    for (int b = 0; b < batch; ++b) {
+      sp->app.page[b] = t.page[b];
+      sp->app.slot[b] = t.slot[b];
+      sp->app.pos[b] = t.pos[b];
+      sp->app.pt_index[b] = t.pt_index[b];
     }
-    if (sp) {
-      sp->app.page[b] = q.pages[q.length / s->P];
-      sp->app.slot[b] = (int32_t)(q.length % s->P);
-      sp->app.pos[b] = (int32_t)q.next_pos;
-      sp->app.pt_index[b] = pti;
-    }
-    runs_append(q, 1);
-    q.length += 1;
-    q.next_pos += 1;
-  }
-  s->st.append_tokens += batch;
   sq_store::Step &st = s->step;
   st = sq_store::Step{};
   st.active = true;
