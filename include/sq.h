@@ -307,9 +307,11 @@ sq_status sq_decode_attn(sq_store *store, int32_t layer, const sq_seq *seqs, int
  * out buffers at the same addresses.  Replays do not update sq_stats.
  *
  * Between sq_step_begin and the last layer's sq_step_attn the new tokens'
- * slots hold stale K/V: every other call that changes a sequence (append,
+ * slots hold stale K/V (a page the step opens is in the page table from
+ * sq_step_begin on): every other call that changes a sequence (append,
  * fork, release, evict, a new step) ends the step, and sq_step_attn then
- * fails.  mode: SQ_ATTN_*.  sq_step_begin errors change nothing;
+ * fails.  A replay sized for a larger batch than the open step's leaves the
+ * extra entries untouched; one sized for a smaller batch misses entries.  mode: SQ_ATTN_*.  sq_step_begin errors change nothing;
  * SQ_ERR_INVALID for a repeated sequence, batch outside [1, SQ_MAX_BATCH],
  * a sequence at its page-list capacity; SQ_ERR_NO_PAGES; in a
  * metadata-only store it updates the metadata only. */

@@ -106,13 +106,13 @@ struct MergeArgs {
 // One decode step appends a token to every entry and attends over the old
 // tokens plus the new one.  The decode launches read the old tokens from
 // the pools; the merge adds the new token as one more partial (its score
-// against the entry's query, weight 1, value v_new) and stores its K, V,
-// position and, when it opens a page, the page-table entry.
+// against the entry's query, weight 1, value v_new) and stores its K, V and
+// position.  (A page the step opens enters the page-table mirror when the
+// step begins, so the mirror never holds an unset entry.)
 struct StepAppend {
-  int32_t page[kMaxBatch];     // physical page of the new token
-  int32_t slot[kMaxBatch];     // its slot in that page
-  int32_t pos[kMaxBatch];      // its position
-  int32_t pt_index[kMaxBatch]; // page-table mirror index to set to page, or -1
+  int32_t page[kMaxBatch]; // physical page of the new token
+  int32_t slot[kMaxBatch]; // its slot in that page
+  int32_t pos[kMaxBatch];  // its position
 };
 
 // The step plan, in device memory: written once per step, read by every
@@ -122,6 +122,8 @@ struct StepPlan {
   DecodeDyn dec[2]; // VALU, MFMA launch
   MergeDyn merge;
   StepAppend app;
+  int32_t batch;    // entries of the step; merge workgroups past it do nothing
+  int32_t pad;
 };
 
 struct StepMergeArgs {
@@ -133,7 +135,6 @@ struct StepMergeArgs {
   uint16_t *k;           // K pool at this layer
   uint16_t *v;           // V pool at this layer
   int32_t *pos;          // position pool [NP][P]
-  int32_t *pt;           // page-table mirror
   int64_t page_stride;
   int64_t head_stride;
   float scale_log2;

@@ -839,11 +839,7 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
           sa.k[pb + (int64_t)slot * D + c] = kb[q];
           sa.v[pb + (int64_t)c * P + slot] = vb[q];
         }
-        if (lane == 0 && g == 0) {
-          sa.pos[(int64_t)page * P + slot] = ap.pos[b];
-          const int pti = ap.pt_index[b];
-          if (pti >= 0) sa.pt[pti] = page;
-        }
+        if (lane == 0 && g == 0) sa.pos[(int64_t)page * P + slot] = ap.pos[b];
       }
     }
   }
@@ -917,7 +913,9 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) 
 }
 template <int D>
 __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge(StepMergeArgs a) {
-  merge_body<D, true>(a.st, DevMerge{&((const SQ_CONST StepPlan *)a.plan)->merge}, a);
+  const SQ_CONST StepPlan *plan = (const SQ_CONST StepPlan *)a.plan;
+  if ((int)(blockIdx.x / a.st.hq) >= plan->batch) return; // a replay sized for a larger batch
+  merge_body<D, true>(a.st, DevMerge{&plan->merge}, a);
 }
 
 template <int D, bool NT>

@@ -36,6 +36,15 @@ struct AppendBatchArgs {
   int32_t *pt;                 // device page-table mirror base
 };
 
+// base[index[i]] = value[i] for i < n (a decode step's new page-table
+// entries).
+struct SetEntries {
+  int32_t *base;
+  int32_t n;
+  int32_t index[kMaxBatch];
+  int32_t value[kMaxBatch];
+};
+
 // ---- eviction -------------------------------------------------------------
 // Evicted spans as [n_spans][3] = (start, end, evicted tokens before start),
 // sorted, disjoint and non-empty: up to kInlineSpans travel in the kernel
@@ -84,6 +93,7 @@ hipError_t launch_append(const Pools &p, const AppendArgs &a, const void *k_new,
                          const void *v_new, hipStream_t s);
 hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const void *k_new,
                                const void *v_new, hipStream_t s);
+hipError_t launch_set_entries(const SetEntries &a, hipStream_t s);
 hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t tail_index,
                            int32_t tail_value, hipStream_t s);
 hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s);

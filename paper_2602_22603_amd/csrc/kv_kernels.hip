@@ -119,6 +119,10 @@ __global__ __launch_bounds__(64) void k_append_batch(Pools p, AppendBatchArgs a,
 }
 
 // dst[i] = src[i] for i < n, then dst[n] = tail_value when tail_value >= 0.
+__global__ __launch_bounds__(64) void k_set_entries(SetEntries a) {
+  if ((int)threadIdx.x < a.n) a.base[a.index[threadIdx.x]] = a.value[threadIdx.x];
+}
+
 __global__ __launch_bounds__(256) void k_copy_i32(int32_t *dst, const int32_t *src, int32_t n,
                                                   int32_t tail_value) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
@@ -288,6 +292,13 @@ hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const v
     hipLaunchKernelGGL(k_append_batch<128>, grid, dim3(64), 0, s, p, a, kn, vn);
   else
     hipLaunchKernelGGL(k_append_batch<64>, grid, dim3(64), 0, s, p, a, kn, vn);
+  return hipGetLastError();
+}
+
+hipError_t launch_set_entries(const SetEntries &a, hipStream_t s) {
+  if (a.n <= 0) return hipSuccess;
+  if (a.n > kMaxBatch) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(k_set_entries, dim3(1), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 

@@ -1331,13 +1331,14 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
   TokenSlots t;
   take_one_token_each(s, seqs, batch, &t);
-  if (sp)
+  if (sp) {
     for (int b = 0; b < batch; ++b) {
       sp->app.page[b] = t.page[b];
       sp->app.slot[b] = t.slot[b];
       sp->app.pos[b] = t.pos[b];
-      sp->app.pt_index[b] = t.pt_index[b];
     }
+    sp->batch = batch;
+  }
   sq_store::Step &st = s->step;
   st = sq_store::Step{};
   st.active = true;
@@ -1353,7 +1354,19 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
   if (!s->device) return SQ_OK;
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
-  hipError_t e = hipMemcpyAsync(s->step_dev, sp, sizeof(*sp), hipMemcpyHostToDevice, strm);
+  // pages the step opens enter the page-table mirror now, whatever happens
+  // to the step's layers
+  sq::SetEntries se{};
+  se.base = s->pt_dev;
+  for (int b = 0; b < batch; ++b)
+    if (t.pt_index[b] >= 0) {
+      se.index[se.n] = t.pt_index[b];
+      se.value[se.n] = t.page[b];
+      ++se.n;
+    }
+  hipError_t e = sq::launch_set_entries(se, strm);
+  if (e != hipSuccess) return hip_fail(e, "page-table entries");
+  e = hipMemcpyAsync(s->step_dev, sp, sizeof(*sp), hipMemcpyHostToDevice, strm);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(step plan)");
   e = hipEventRecord(s->step_ev, strm);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord(step plan)");
@@ -1398,7 +1411,6 @@ sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void
   ma.k = s->pools.k + layer * s->pools.layer_stride;
   ma.v = s->pools.v + layer * s->pools.layer_stride;
   ma.pos = s->pools.pos;
-  ma.pt = s->pt_dev;
   ma.page_stride = s->pools.page_stride;
   ma.head_stride = s->pools.head_stride;
   ma.scale_log2 = ds.scale_log2;

@@ -168,6 +168,41 @@ def test_captured_step_replays(sq, mi):
     t.check_state()
 
 
+def _device_page_table(store, seq):
+    """The device page-table mirror row of seq (the workspace starts with it:
+    int32 [max_seqs][max_pages_per_seq])."""
+    import torch
+    n = store.max_seqs * store.max_pages_per_seq
+    rows = store.workspace[: 4 * n].view(torch.int32).view(store.max_seqs, store.max_pages_per_seq)
+    return rows[seq, : store.seq_info(seq)["n_pages"]].tolist()
+
+
+def test_step_begin_sets_the_page_table_at_once(sq):
+    """A step that opens pages writes their page-table entries when it
+    begins, so a step whose layers never run leaves no unset entry behind:
+    the device mirror equals the host page table right after sq_step_begin,
+    and the regular calls afterwards work (the abandoned tokens' slots hold
+    whatever the fresh page held: zeros here)."""
+    import torch
+    t = sc.Twin(sq, 1, 8, 2, 64, 64, 4, 16, seed=150)
+    a = t.create()
+    t.append(a, 32)                    # two full pages: the step opens a third
+    b = t.create()
+    t.append(b, 5)
+    t.store.step_begin([a, b])
+    torch.cuda.synchronize()
+    for h in (a, b):
+        assert _device_page_table(t.store, h) == t.store.page_table(h)
+    z = np.zeros((1, 1, 2, 64))
+    for h in (a, b):                   # the oracle's view of the abandoned tokens
+        t.model.append(h, 1, z, z)
+    errs, _ = t.decode_errors([a, b])
+    assert max(errs.values()) <= TOL, errs
+    t.append(a, 3)
+    errs, _ = t.decode_errors([a, b])
+    assert max(errs.values()) <= TOL, errs
+
+
 def test_step_arguments(sq):
     import torch
     s = sq.Store(2, 8, 2, 64, 32, 4, 8, device="cuda")
