@@ -81,6 +81,27 @@ def test_shared128k_sampled_heads(sq):
             assert err <= TOL, (mode, b, g, err)
     info = store.plan_info(seqs, sq.ATTN_AUTO)
     assert info["n_groups"] == 8 and info["kv_bytes"] == 4_311_744_512
+    # the fused decode step bench.py also times: one token appended to all 16
+    # sequences inside the step, then attention over every token
+    kn = wl.device_normal_bf16((16, 8, 128), 2602_301, "cuda")
+    vn = wl.device_normal_bf16((16, 8, 128), 2602_302, "cuda")
+    q2 = wl.device_normal_bf16((16, 32, 128), 2602_303, "cuda")
+    q2f = wl.torch_bf16_to_f64(q2)
+    store.step_begin(seqs)
+    out = store.step_attn(0, kn, vn, q2)
+    torch.cuda.synchronize()
+    o = out.cpu().numpy()
+    for t, b_main, b_aux, groups in ((0, 0, 1, (0, 7)), (7, 14, 15, (3,))):
+        k, v, ka, va = inputs[t]
+        fork_at = k.shape[1] - 256
+        for b, kk, vv in ((b_main, k[0], v[0]),
+                          (b_aux, torch.cat([k[0, :fork_at], ka[0]]),
+                           torch.cat([v[0, :fork_at], va[0]]))):
+            kk = torch.cat([kk, kn[b: b + 1].to(kk.device)])
+            vv = torch.cat([vv, vn[b: b + 1].to(vv.device)])
+            for g in groups:
+                err = sc.max_abs(o[b, 4 * g: 4 * g + 4], _oracle_group(q2f[b], kk, vv, g, scale))
+                assert err <= TOL, ("step", b, g, err)
     store.close()
 
 
