@@ -29,6 +29,19 @@ compacted cache and masked attention over the uncompacted cache are
 bit-identical in float64: a masked key contributes an exact +0.0 and leaves
 the maximum over the kept keys unchanged.
 
+Sinks and windows (model variants; the paper names only its model)
+--------------------------------------------------------------------
+Two options of the attention itself, as some models define it:
+
+* a learned sink logit per query head, ``sinks[h]`` (in the units of the
+  scaled scores), joins the softmax as one more term of its denominator with
+  no value:  out[h] = sum_i e^(s[h,i] - M) v_i / (e^(sinks[h] - M) +
+  sum_i e^(s[h,i] - M)),  M = max(sinks[h], max_i s[h,i]).  A head whose
+  keys are all masked then returns zeros as before.
+* a window of W keys: a query attends only to the W most recent keys up to
+  and including its own position (for a decode step, the last W of the L
+  keys); it is the band mask ``window_mask(L, W)``.
+
 Split partials
 --------------
 ``partial`` returns (m, l, acc) with l = sum_i exp(s_i - m) and
@@ -113,13 +126,34 @@ def weights(q, k, scale, group, mask=None):
     return p
 
 
-def attention(q, k, v, scale, group, mask=None):
-    """out[h] = sum_i p[h, i] v[i, h // group]; zeros for an all-masked head."""
+def attention(q, k, v, scale, group, mask=None, sinks=None):
+    """out[h] = sum_i p[h, i] v[i, h // group]; zeros for an all-masked head.
+    With ``sinks`` ([Hq]) each head's softmax has one more denominator term
+    e^(sinks[h]) carrying no value."""
     m, l, acc = partial(q, k, v, scale, group, mask)
     out = np.zeros_like(acc)
+    if sinks is not None:
+        sinks = _as_f64(sinks)
+        for h in range(acc.shape[0]):
+            if l[h] == 0:
+                continue
+            big = max(m[h], sinks[h])
+            scale_kv = np.exp(m[h] - big)    # rescales the keys' sum and values
+            l_all = l[h] * scale_kv + np.exp(sinks[h] - big)
+            out[h] = acc[h] * scale_kv / l_all
+        return out
     live = l > 0
     out[live] = acc[live] / l[live][:, None]
     return out
+
+
+def window_mask(n_keys, window):
+    """Keep mask of a decode query over n_keys keys with a window of
+    ``window`` keys (0: every key): the last ``window`` keys."""
+    keep = np.ones(n_keys, dtype=np.uint8)
+    if window > 0:
+        keep[: max(0, n_keys - window)] = 0
+    return keep
 
 
 def masked_attention(q, k, v, mask, scale, group):
@@ -147,12 +181,16 @@ def merge(parts):
     return out
 
 
-def decode_batch(q, views, scale, group, masks=None):
+def decode_batch(q, views, scale, group, masks=None, window=0, sinks=None):
     """One decode step for a batch: q [B, Hq, D]; views[b] = (k, v) with
-    k, v: [L_b, Hkv, D] (the sequence's logical view for one layer)."""
+    k, v: [L_b, Hkv, D] (the sequence's logical view for one layer);
+    optional window (in keys) and per-head sinks [Hq]."""
     q = _as_f64(q)
     out = np.zeros((q.shape[0], q.shape[1], q.shape[2]))
     for b, (k, v) in enumerate(views):
         mask = None if masks is None else masks[b]
-        out[b] = attention(q[b], k, v, scale, group, mask)
+        if window > 0:
+            band = window_mask(np.asarray(k).shape[0], window)
+            mask = band if mask is None else band * np.asarray(mask)
+        out[b] = attention(q[b], k, v, scale, group, mask, sinks)
     return out

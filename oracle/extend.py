@@ -23,7 +23,10 @@ eviction the positions of the retained keys are no longer contiguous, but
 they stay strictly increasing in logical order, so the two orders agree.
 
 A key mask (the masked form of eviction, Algorithm 2 ``BuildMask``) removes
-keys of the prefix for every query, exactly as in ``attention``.
+keys of the prefix for every query, exactly as in ``attention``.  A window
+of W keys restricts new token j to the keys at logical indices
+max(0, L - n + j - W + 1) .. L - n + j; per-head sinks join every softmax as
+in ``attention``.
 """
 
 from __future__ import annotations
@@ -33,12 +36,13 @@ import numpy as np
 from . import attention as _att
 
 
-def extend_attention(q, k, v, scale, group, mask=None):
+def extend_attention(q, k, v, scale, group, mask=None, window=0, sinks=None):
     """Causal attention of the last n cached tokens.
 
     q: [n, Hq, D] (the new tokens' queries); k, v: [L, Hkv, D], the logical
     view of the cache after the n new tokens were appended (L >= n);
-    mask: optional [L] (nonzero = keep).  Returns out [n, Hq, D].
+    mask: optional [L] (nonzero = keep); window: keys per query (0: all);
+    sinks: optional [Hq].  Returns out [n, Hq, D].
     """
     q = np.asarray(q, dtype=np.float64)
     k = np.asarray(k, dtype=np.float64)
@@ -50,6 +54,7 @@ def extend_attention(q, k, v, scale, group, mask=None):
     out = np.zeros((n, hq, d))
     for j in range(n):
         last = n_keys - n + j          # logical index of new token j
-        m = None if mask is None else np.asarray(mask)[: last + 1]
-        out[j] = _att.attention(q[j], k[: last + 1], v[: last + 1], scale, group, m)
+        lo = max(0, last - window + 1) if window > 0 else 0
+        m = None if mask is None else np.asarray(mask)[lo: last + 1]
+        out[j] = _att.attention(q[j], k[lo: last + 1], v[lo: last + 1], scale, group, m, sinks)
     return out

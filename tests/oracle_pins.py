@@ -732,6 +732,87 @@ def check_remap_page_tables_by_hand():
             assert m.refcount.sum() == len(m.page_table(a))
 
 
+# --------------------------------------------------------------------------
+# sinks and windows (model variants)
+# --------------------------------------------------------------------------
+def check_sinks_textbook(seed=22):
+    """Per-head sinks: equal to torch.softmax over the logits with the sink
+    appended as one more column (dropped after the softmax) times V, in
+    float64; a sink of -inf changes nothing at all."""
+    rng = np.random.default_rng(seed)
+    for hq, hkv, d, n, scale in [(4, 1, 64, 50, 1 / 8), (8, 2, 8, 17, 0.5),
+                                 (64, 8, 64, 30, 1 / 8), (2, 2, 4, 1, 1.0)]:
+        q, k, v = _rand_qkv(rng, hq, hkv, d, n)
+        g = hq // hkv
+        sinks = rng.standard_normal(hq) * 3
+        out = att.attention(q, k, v, scale, g, sinks=sinks)
+        kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        qt = torch.from_numpy(q)[:, None, :]
+        logits = scale * torch.bmm(qt, kt.transpose(1, 2).contiguous())
+        logits = torch.cat([logits, torch.from_numpy(sinks)[:, None, None]], dim=-1)
+        p = torch.softmax(logits, dim=-1)[:, :, :n]
+        ref = torch.bmm(p, vt)[:, 0, :].numpy()
+        assert np.max(np.abs(out - ref)) <= 1e-12, np.max(np.abs(out - ref))
+        same = att.attention(q, k, v, scale, g, sinks=np.full(hq, -np.inf))
+        assert np.array_equal(same, att.attention(q, k, v, scale, g))
+
+
+def check_sink_closed_form():
+    """One key of score s and a sink c: the output is v * e^s / (e^s + e^c),
+    i.e. v times the logistic function of s - c."""
+    q = np.array([[1.0, 0.5]])
+    k = np.array([[[2.0, -1.0]]])
+    v = np.array([[[3.0, -4.0]]])
+    s = 0.7 * (1.0 * 2.0 + 0.5 * -1.0)
+    for c in (-2.0, 0.0, s, 5.0):
+        out = att.attention(q, k, v, 0.7, 1, sinks=np.array([c]))
+        want = v[0, 0] / (1.0 + math.exp(c - s))
+        assert np.max(np.abs(out[0] - want)) <= 1e-15, (c, out, want)
+
+
+def check_windows(seed=23):
+    """A window of W keys: W >= L changes nothing; W = 1 returns the last
+    key's V exactly; otherwise equal to torch's scaled_dot_product_attention
+    with the band mask, for decode and for extend (band and causal)."""
+    rng = np.random.default_rng(seed)
+    for hq, hkv, d, L, scale in [(4, 1, 16, 40, 0.25), (8, 2, 8, 17, 0.5), (64, 8, 64, 33, 1 / 8)]:
+        q, k, v = _rand_qkv(rng, hq, hkv, d, L)
+        g = hq // hkv
+        full = att.decode_batch(q[None], [(k, v)], scale, g)
+        assert np.array_equal(att.decode_batch(q[None], [(k, v)], scale, g, window=L), full)
+        one = att.decode_batch(q[None], [(k, v)], scale, g, window=1)[0]
+        assert np.array_equal(one, np.repeat(v[-1], g, axis=0))
+        kt = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        vt = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(g, dim=0)
+        for w in (2, 5, L - 1):
+            out = att.decode_batch(q[None], [(k, v)], scale, g, window=w)[0]
+            allowed = (torch.arange(L) >= L - w)[None, :]
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(q)[:, None, :], kt, vt, attn_mask=allowed,
+                scale=scale)[:, 0, :].numpy()
+            assert np.max(np.abs(out - ref)) <= 1e-12, (w, np.max(np.abs(out - ref)))
+        n = 9
+        qn = rng.standard_normal((n, hq, d))
+        for w in (1, 4, 12):
+            out = ex.extend_attention(qn, k, v, scale, g, window=w)
+            j = torch.arange(n)[:, None] + (L - n)
+            key = torch.arange(L)[None, :]
+            allowed = (key <= j) & (key > j - w)
+            ref = torch.nn.functional.scaled_dot_product_attention(
+                torch.from_numpy(qn).permute(1, 0, 2).contiguous(), kt, vt, attn_mask=allowed,
+                scale=scale).permute(1, 0, 2).numpy()
+            assert np.max(np.abs(out - ref)) <= 1e-12, (w, np.max(np.abs(out - ref)))
+            sinks = rng.standard_normal(hq)
+            with_s = ex.extend_attention(qn, k, v, scale, g, window=w, sinks=sinks)
+            for jj in range(n):
+                last = L - n + jj
+                lo = max(0, last - w + 1)
+                want = att.attention(qn[jj], k[lo: last + 1], v[lo: last + 1], scale, g,
+                                     sinks=sinks)
+                assert np.array_equal(with_s[jj], want)
+
+
 ALL_CHECKS = [
     check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
     check_uniform_closed_form, check_two_key_closed_form,
@@ -746,4 +827,5 @@ ALL_CHECKS = [
     check_chunked_eviction_fits_where_one_shot_does_not,
     check_chunked_eviction_never_overwrites_unread_tokens,
     check_remap_against_list_model, check_remap_page_tables_by_hand,
+    check_sinks_textbook, check_sink_closed_form, check_windows,
 ]

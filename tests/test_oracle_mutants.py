@@ -190,6 +190,35 @@ def _remap_next_page(self, src_of, j0, new_len):
     return None if a0 is None else a0 + self.P
 
 
+_orig_attention = att.attention
+_orig_window_mask = att.window_mask
+
+
+def _sinks_ignored(q, k, v, scale, group, mask=None, sinks=None):
+    return _orig_attention(q, k, v, scale, group, mask)
+
+
+def _sink_carries_a_value(q, k, v, scale, group, mask=None, sinks=None):
+    # as if the sink were a key whose value is all ones
+    out = _orig_attention(q, k, v, scale, group, mask, sinks)
+    if sinks is None:
+        return out
+    m, l, acc = att.partial(q, k, v, scale, group, mask)
+    for h in range(out.shape[0]):
+        if l[h] > 0:
+            big = max(m[h], sinks[h])
+            out[h] += np.exp(sinks[h] - big) / (l[h] * np.exp(m[h] - big) + np.exp(sinks[h] - big))
+    return out
+
+
+def _window_one_too_wide(n_keys, window):
+    return _orig_window_mask(n_keys, window + 1 if window > 0 else 0)
+
+
+def _extend_window_one_too_wide(q, k, v, scale, group, mask=None, window=0, sinks=None):
+    return _orig_extend(q, k, v, scale, group, mask, window + 1 if window > 0 else 0, sinks)
+
+
 MUTANTS = {
     "gqa_head_modulo": (att, "scores", _scores_gqa_modulo),
     "missing_scale": (att, "scores", _scores_no_scale),
@@ -212,6 +241,10 @@ MUTANTS = {
     "evict_chunk_releases_a_page_early": (pg.PageModel, "_released_after", _released_one_page_early),
     "remap_without_run_check": (pg.PageModel, "_remap_source", _remap_page_start_only),
     "remap_takes_the_next_page": (pg.PageModel, "_remap_source", _remap_next_page),
+    "sinks_ignored": (att, "attention", _sinks_ignored),
+    "sink_carries_a_value": (att, "attention", _sink_carries_a_value),
+    "window_one_key_too_wide": (att, "window_mask", _window_one_too_wide),
+    "extend_window_one_key_too_wide": (ex, "extend_attention", _extend_window_one_too_wide),
 }
 
 
