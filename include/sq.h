@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 4
+#define SQ_ABI_VERSION 5
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -347,6 +347,55 @@ sq_status sq_step_attn(sq_store *store, int32_t layer, const void *k_new, const 
  * positive, metadata-only store. */
 sq_status sq_extend_attn(sq_store *store, int32_t layer, sq_seq seq, int32_t n_new,
                          const void *q, float *out, float scale, void *stream);
+
+/* ---- attention options (model variants) ---------------------------------
+ * Some models change the softmax of the attention above in two ways; the
+ * paper's method (eviction, fork, shared prefixes) applies unchanged.
+ *   sinks   device fp32 [Hq] (caller-owned, finite), or NULL: a learned
+ *           logit per query head, in the units of the scaled scores, that
+ *           joins each softmax as one more term with no value:
+ *             out = sum_i e^(s_i - M) v_i / (e^(sink - M) + sum_i e^(s_i - M)),
+ *           M = max(sink, max_i s_i).  A query with no keys still gets 0.
+ *   window  0: every key; W > 0: a query at logical index t attends only
+ *           to the keys at indices t - W + 1 .. t (the W most recent ones,
+ *           its own included).  A decode query of a sequence of L tokens
+ *           is at index L - 1; extend token j at L - n_new + j.
+ *   reserved  must be 0.
+ * The window is over logical indices of the (compacted) cache, as the
+ * causal mask is.  SQ_ERR_INVALID: window < 0, reserved != 0, or a sinks
+ * pointer that is not 4-byte aligned. */
+typedef struct sq_attn_opts {
+  const float *sinks;
+  int32_t window;
+  int32_t reserved;
+} sq_attn_opts;
+
+/* sq_decode_attn with options; opts NULL = sq_decode_attn.  A windowed
+ * batch reads each entry's window on its own (no shared-prefix tiles). */
+sq_status sq_decode_attn_ex(sq_store *store, int32_t layer, const sq_seq *seqs, int32_t batch,
+                            const void *q, float *out, float scale, int32_t mode,
+                            const sq_attn_opts *opts, void *stream);
+
+/* sq_extend_attn with options; opts NULL = sq_extend_attn. */
+sq_status sq_extend_attn_ex(sq_store *store, int32_t layer, sq_seq seq, int32_t n_new,
+                            const void *q, float *out, float scale, const sq_attn_opts *opts,
+                            void *stream);
+
+/* sq_step_begin for a step whose layers may use a window of `window` keys
+ * (0: none): besides the full plan it writes a windowed one, and every
+ * sq_step_attn_ex of the step may then pick either (models alternate
+ * windowed and full layers).  sq_step_begin = window 0.
+ * SQ_ERR_INVALID also for window < 0. */
+sq_status sq_step_begin_ex(sq_store *store, const sq_seq *seqs, int32_t batch, int32_t mode,
+                           int32_t window, void *stream);
+
+/* sq_step_attn with options; opts NULL = sq_step_attn.  opts->window is 0
+ * (every key) or the window of sq_step_begin_ex.  A capture replays with
+ * the same options, each step begun with the same window.
+ * SQ_ERR_INVALID also for any other window. */
+sq_status sq_step_attn_ex(sq_store *store, int32_t layer, const void *k_new, const void *v_new,
+                          const void *q, float *out, float scale, const sq_attn_opts *opts,
+                          void *stream);
 
 /* Host-only description of the work sq_decode_attn would do for this batch. */
 sq_status sq_decode_plan_info(sq_store *store, const sq_seq *seqs, int32_t batch,

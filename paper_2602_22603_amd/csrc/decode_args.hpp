@@ -8,9 +8,10 @@
 namespace sq {
 
 // ---- decode ---------------------------------------------------------------
-// A segment: `ntok` tokens read from page-table row `row` from page index
-// `page0` on, attended by `nmem` query sequences (batch indices packed as
-// bytes in `mem`).  Its Hkv rows (one per KV head g) occupy the flattened
+// A segment: tokens [tok0, ntok) counted from the first slot of page index
+// `page0` of page-table row `row` (tok0 < 16: a window may start inside
+// its first page), attended by `nmem` query sequences (batch indices packed
+// as bytes in `mem`).  Its Hkv rows (one per KV head g) occupy the flattened
 // page ranges [start + g * (npages + row_pad), ... + npages) of its launch;
 // each row is followed by row_pad flattened pages that map to nothing.  They
 // stand for the fixed start-up cost of a piece (its query, page-id and
@@ -23,6 +24,7 @@ struct Seg {
   int32_t start;
   int32_t nmem;
   uint32_t mem; // byte j = batch index of member j
+  int32_t tok0;
 };
 
 // What a decode launch needs that does not change from call to call.
@@ -80,10 +82,11 @@ struct MergeStatic {
   const float *part_m;
   const float *part_l;
   const float *part_acc;
+  const float *sinks; // [Hq] learned softmax sink logits (log2 units after sink_scale), or null
+  float sink_scale;   // log2(e): the sinks are in the units of the scaled scores
   int32_t hq;
   int32_t group; // G
   int32_t hkv;
-  int32_t pad;
 };
 
 struct MergeDyn {
@@ -119,16 +122,20 @@ struct StepAppend {
 // layer's launches, whose arguments therefore stay the same from step to
 // step.
 struct StepPlan {
-  DecodeDyn dec[2]; // VALU, MFMA launch
+  DecodeDyn dec[2];   // VALU, MFMA launch over every old token
   MergeDyn merge;
+  DecodeDyn dec_w[2]; // the same over the window's old tokens (a windowed step)
+  MergeDyn merge_w;
   StepAppend app;
-  int32_t batch;    // entries of the step; merge workgroups past it do nothing
+  int32_t batch;      // entries of the step; merge workgroups past it do nothing
   int32_t pad;
 };
 
 struct StepMergeArgs {
   MergeStatic st;
   const StepPlan *plan;
+  int32_t windowed; // 1: the plan's windowed merge sources
+  int32_t pad2;
   const uint16_t *q;     // [B][Hq][D] bf16
   const uint16_t *k_new; // [B][Hkv][D] bf16
   const uint16_t *v_new; // [B][Hkv][D] bf16

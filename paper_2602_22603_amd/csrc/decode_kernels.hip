@@ -159,6 +159,7 @@ struct DevPlan {
     y.start = x.start;
     y.nmem = x.nmem;
     y.mem = x.mem;
+    y.tok0 = x.tok0;
     return y;
   }
 };
@@ -268,6 +269,7 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
 
   for (int pg = ip.pbeg; pg < ip.pend; ++pg) {
     const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
+    const int lo = pg == 0 ? ip.sg.tok0 : 0; // tokens before lo: outside a window
     // stage the page in LDS
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
@@ -315,7 +317,7 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
       float x = s[0];
 #pragma unroll
       for (int r = 1; r < G; ++r) x = (row == r) ? s[r] : x;
-      x = (t < valid) ? x * a.scale_log2 : kNegInf;
+      x = (t >= lo && t < valid) ? x * a.scale_log2 : kNegInf;
       float mx = x;
       mx = fmaxf(mx, dpp<kRowRor4>(mx));
       mx = fmaxf(mx, dpp<kRowRor8>(mx));
@@ -357,11 +359,11 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
     for (int e = 0; e < DPL; ++e) {
       const uint2 vv = *reinterpret_cast<const uint2 *>(sV + dg * VGP + e * 32 + 8 * R);
       float v0 = bf_lo(vv.x), v1 = bf_hi(vv.x), v2 = bf_lo(vv.y), v3 = bf_hi(vv.y);
-      if (valid < P) { // values of absent tokens may be anything: keep 0 * v finite
-        v0 = 4 * R + 0 < valid ? v0 : 0.f;
-        v1 = 4 * R + 1 < valid ? v1 : 0.f;
-        v2 = 4 * R + 2 < valid ? v2 : 0.f;
-        v3 = 4 * R + 3 < valid ? v3 : 0.f;
+      if (valid < P || lo > 0) { // values of absent tokens may be anything: keep 0 * v finite
+        v0 = 4 * R + 0 >= lo && 4 * R + 0 < valid ? v0 : 0.f;
+        v1 = 4 * R + 1 >= lo && 4 * R + 1 < valid ? v1 : 0.f;
+        v2 = 4 * R + 2 >= lo && 4 * R + 2 < valid ? v2 : 0.f;
+        v3 = 4 * R + 3 >= lo && 4 * R + 3 < valid ? v3 : 0.f;
       }
 #pragma unroll
       for (int r = 0; r < G; ++r) {
@@ -484,7 +486,7 @@ __device__ inline void load_v(VFrag<D> &f, __amdgpu_buffer_rsrc_t r, int lane_of
 // S^T = K . Q^T for one page, then the online-softmax update of (m, l, acc);
 // returns the page's weights P as bf16 hi and lo parts.
 template <int D>
-__device__ inline void mfma_scores(const KFrag<D> &f, int valid, int kg, float scale_log2,
+__device__ inline void mfma_scores(const KFrag<D> &f, int lo, int valid, int kg, float scale_log2,
                                    const bf16x8_t (&qb)[D / 32], f32x4_t (&acc)[D / 16],
                                    float &m_run, float &l_run, s16x4_t &phi, s16x4_t &plo) {
   constexpr int NS = D / 32;
@@ -496,7 +498,8 @@ __device__ inline void mfma_scores(const KFrag<D> &f, int valid, int kg, float s
                                                  0, 0, 0);
   float x[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) x[i] = (4 * kg + i < valid) ? st[i] * scale_log2 : kNegInf;
+  for (int i = 0; i < 4; ++i)
+    x[i] = (4 * kg + i >= lo && 4 * kg + i < valid) ? st[i] * scale_log2 : kNegInf;
   float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
   mx = max_xrow16(mx);
   mx = max_xrow32(mx);
@@ -526,12 +529,13 @@ __device__ inline void mfma_scores(const KFrag<D> &f, int valid, int kg, float s
 
 // O^T += V^T . P^T for one page (hi and lo parts of P).
 template <int D>
-__device__ inline void mfma_values(VFrag<D> &f, int valid, int kg, s16x4_t phi, s16x4_t plo,
-                                   f32x4_t (&acc)[D / 16]) {
+__device__ inline void mfma_values(VFrag<D> &f, int lo, int valid, int kg, s16x4_t phi,
+                                   s16x4_t plo, f32x4_t (&acc)[D / 16]) {
   constexpr int NJ = D / 16;
-  if (valid < P) { // values of absent tokens may be anything: keep 0 * v finite
-    const uint32_t m0 = (4 * kg + 0 < valid ? 0xffffu : 0u) | (4 * kg + 1 < valid ? 0xffff0000u : 0u);
-    const uint32_t m1 = (4 * kg + 2 < valid ? 0xffffu : 0u) | (4 * kg + 3 < valid ? 0xffff0000u : 0u);
+  if (valid < P || lo > 0) { // values of absent tokens may be anything: keep 0 * v finite
+    auto in = [&](int t) { return t >= lo && t < valid; };
+    const uint32_t m0 = (in(4 * kg + 0) ? 0xffffu : 0u) | (in(4 * kg + 1) ? 0xffff0000u : 0u);
+    const uint32_t m1 = (in(4 * kg + 2) ? 0xffffu : 0u) | (in(4 * kg + 3) ? 0xffff0000u : 0u);
 #pragma unroll
     for (int j = 0; j < NJ; ++j) {
       f.v[j].x &= m0;
@@ -613,6 +617,7 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     const int pg = wbeg + j;
     return j >= count ? 0 : (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
   };
+  auto lo_of = [&](int j) -> int { return wbeg + j == 0 ? ip.sg.tok0 : 0; };
   KFrag<D> k0, k1;
   VFrag<D> v0, v1;
   int n0 = 0, n1 = 0; // ids of pages j + 2 and j + 3
@@ -627,21 +632,21 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   }
   for (int j = 0; j < count; j += 2) {
     {
-      const int valid = valid_of(j);
+      const int valid = valid_of(j), lo = lo_of(j);
       s16x4_t phi, plo;
-      mfma_scores<D>(k0, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      mfma_scores<D>(k0, lo, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
       load_k<D, NT>(k0, rsrc(khead, n0, j + 2 < count), koff);
-      mfma_values<D>(v0, valid, kg, phi, plo, acc);
+      mfma_values<D>(v0, lo, valid, kg, phi, plo, acc);
       load_v<D, NT>(v0, rsrc(vhead, n0, j + 2 < count), voff);
     }
     {
       // page j + 1 may not exist (count odd): its fragments are then zeros
       // and with no valid token the update leaves (m, l, acc) as they are.
-      const int valid = valid_of(j + 1);
+      const int valid = valid_of(j + 1), lo = lo_of(j + 1);
       s16x4_t phi, plo;
-      mfma_scores<D>(k1, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      mfma_scores<D>(k1, lo, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
       load_k<D, NT>(k1, rsrc(khead, n1, j + 3 < count), koff);
-      mfma_values<D>(v1, valid, kg, phi, plo, acc);
+      mfma_values<D>(v1, lo, valid, kg, phi, plo, acc);
       load_v<D, NT>(v1, rsrc(vhead, n1, j + 3 < count), voff);
     }
     n0 = sid(j + 4);
@@ -810,6 +815,10 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
   float num[DPT];
 #pragma unroll
   for (int q = 0; q < DPT; ++q) num[q] = 0.f;
+  if (a.sinks && wave == 0) { // the sink: one more softmax term, with no value
+    m_w = a.sinks[h] * a.sink_scale;
+    l_w = 1.f;
+  }
   if constexpr (APPEND) {
     if (wave == kMergeWaves - 1) {
       const int64_t kv = (int64_t)b * a.hkv + g;
@@ -915,7 +924,7 @@ template <int D>
 __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge(StepMergeArgs a) {
   const SQ_CONST StepPlan *plan = (const SQ_CONST StepPlan *)a.plan;
   if ((int)(blockIdx.x / a.st.hq) >= plan->batch) return; // a replay sized for a larger batch
-  merge_body<D, true>(a.st, DevMerge{&plan->merge}, a);
+  merge_body<D, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a);
 }
 
 template <int D, bool NT>

@@ -38,6 +38,12 @@ struct ExtendArgs {
   float *part_m;      // [slots][kExtRows] (log2 units), slot = (qb * Hkv + g) * n_split + s
   float *part_l;      // [slots][kExtRows]
   float *part_acc;    // [slots][kExtRows][D]
+  // Model variants: a window of `window` keys (0: none) ends at each
+  // token's own index; sinks[h] (or null) joins each softmax as a term with
+  // no value, scaled by sink_scale into the log2 units of the scores.
+  const float *sinks;
+  int32_t window;
+  float sink_scale;
 };
 
 static_assert(sizeof(ExtendArgs) < 4096, "extend kernel arguments too large");

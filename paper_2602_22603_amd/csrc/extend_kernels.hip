@@ -193,12 +193,13 @@ constexpr float kLazy = 8.f;
 
 // One 64-key block against this wave's 32 query columns.  need_mask: the
 // block reaches past some column's last visible key (the chunk's diagonal,
-// or the cache's end); only then is the per-key test made.
+// or the cache's end) or before some column's first one (a window); only
+// then is the per-key test made.
 template <int D>
 __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, int n, int kg,
                                  float c, bool need_mask, const bf16x8_t (&qf)[2][D / 32],
-                                 const int (&lim)[2], f32x4_t (&acc)[D / 16][2], float (&m_run)[2],
-                                 float (&l_run)[2]) {
+                                 const int (&first)[2], const int (&lim)[2],
+                                 f32x4_t (&acc)[D / 16][2], float (&m_run)[2], float (&l_run)[2]) {
   constexpr int NKC = D / 32;
   constexpr int NDT = D / 16;
   f32x4_t st[4][2];
@@ -226,7 +227,8 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
       for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (b * BK + tile_key(tt, 4 * kg + i) > lim[cg]) st[tt][cg][i] = kNegInf;
+          if (b * BK + tile_key(tt, 4 * kg + i) > lim[cg] || b * BK + tile_key(tt, 4 * kg + i) < first[cg])
+            st[tt][cg][i] = kNegInf;
   }
   float alpha[2], nm[2];
 #pragma unroll
@@ -314,7 +316,7 @@ k_extend(ExtendArgs a) {
 
   // this lane's two query columns (rows of the attention)
   bf16x8_t qf[2][NKC];
-  int lim[2], jrow[2], hrow[2];
+  int lim[2], first[2], jrow[2], hrow[2];
   bool live[2];
 #pragma unroll
   for (int cg = 0; cg < 2; ++cg) {
@@ -323,6 +325,7 @@ k_extend(ExtendArgs a) {
     hrow[cg] = g * G + col % G;
     live[cg] = jrow[cg] < a.n;
     lim[cg] = live[cg] ? base + jrow[cg] : a.L - 1;
+    first[cg] = a.window > 0 ? lim[cg] - a.window + 1 : 0; // may be negative
     const uint16_t *qp = a.q + ((int64_t)jrow[cg] * a.hq + hrow[cg]) * D + 8 * kg;
 #pragma unroll
     for (int kc = 0; kc < NKC; ++kc) {
@@ -331,10 +334,13 @@ k_extend(ExtendArgs a) {
       qf[cg][kc] = __builtin_bit_cast(bf16x8_t, w);
     }
   }
-  const int kend = min(a.L, base + j0 + TQ); // keys this query block needs
-  const int b_lo = sp * a.split_blocks;      // this workgroup's blocks [b_lo, b_hi)
+  const int kend = min(a.L, base + j0 + TQ); // keys this query block needs: [kbeg, kend)
+  const int kbeg = a.window > 0 ? max(0, base + j0 - a.window + 1) : 0;
+  const int b_lo = kbeg / BK + sp * a.split_blocks; // this workgroup's blocks [b_lo, b_hi)
   const int b_hi = min((kend + BK - 1) / BK, b_lo + a.split_blocks);
   const int mask_from = base + j0;           // keys above this need the causal test
+  // keys below this are outside the window of the block's last token
+  const int mask_below = a.window > 0 ? min(a.L - 1, base + j0 + TQ - 1) - a.window + 1 : 0;
 
   f32x4_t acc[NDT][2];
 #pragma unroll
@@ -364,8 +370,9 @@ k_extend(ExtendArgs a) {
       ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, ids, wave, lane);
       block_ids(ids, a, b + 2);
     }
-    ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2, b * BK + BK - 1 > mask_from, qf,
-                 lim, acc, m_run, l_run);
+    ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2,
+                 b * BK + BK - 1 > mask_from || b * BK < mask_below, qf, first, lim, acc, m_run,
+                 l_run);
   }
 
   if (a.n_split > 1) {
@@ -394,7 +401,14 @@ k_extend(ExtendArgs a) {
     float l = sum_xrow16(l_run[cg]);
     l = sum_xrow32(l);
     if (!live[cg]) continue;
-    const float inv = 1.f / l;
+    float sc = 1.f;
+    if (a.sinks) { // one more term of the sum, no value: rescale both to the larger maximum
+      const float sk_l2 = a.sinks[hrow[cg]] * a.sink_scale;
+      const float big = fmaxf(m_run[cg], sk_l2);
+      sc = exp2_fast(m_run[cg] - big);
+      l = fmaf(l, sc, exp2_fast(sk_l2 - big));
+    }
+    const float inv = sc / l;
     float *op = a.out + ((int64_t)jrow[cg] * a.hq + hrow[cg]) * D + 4 * kg;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -429,10 +443,13 @@ __global__ __launch_bounds__(256) void k_extend_merge(ExtendArgs a) {
   float big = mine;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) big = fmaxf(big, __shfl_xor(big, o));
+  const float sink = a.sinks ? a.sinks[h] * a.sink_scale : kNegInf;
+  big = fmaxf(big, sink);
   const float w = (lane < S && big != kNegInf) ? exp2_fast(mine - big) : 0.f;
   float den = w * lmine;
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) den += __shfl_xor(den, o);
+  if (a.sinks) den += exp2_fast(sink - big); // the sink's term, no value
   float num[DPT];
 #pragma unroll
   for (int q = 0; q < DPT; ++q) num[q] = 0.f;

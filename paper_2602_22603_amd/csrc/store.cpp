@@ -228,7 +228,9 @@ struct sq_store {
     int32_t batch = 0, mode = 0;
     bool launch[2] = {false, false}; // VALU, MFMA
     int32_t grid[2] = {0, 0};
+    int32_t window = 0; // the windowed plan's window (0: no windowed plan)
     int64_t kv_bytes = 0, kv_bytes_logical = 0;
+    int64_t kv_bytes_w = 0, kv_bytes_logical_w = 0;
   } step;
 
   // profiling
@@ -369,18 +371,22 @@ struct Plan {
   int64_t kv_bytes_valu = 0, kv_bytes_mfma = 0;
 };
 
-sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode, Plan *plan) {
+// keep_last >= 0: each entry attends only to its last keep_last cached
+// tokens (a window), read on its own; < 0: every token.
+sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode, Plan *plan,
+                     int64_t keep_last = -1) {
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
   const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
   const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma);
 
   auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
-                     const std::vector<int> &members) {
+                     const std::vector<int> &members, int32_t tok0 = 0) {
     PlanSeg ps{};
     ps.seg.row = row;
     ps.seg.page0 = page0;
     ps.seg.ntok = (int32_t)ntok;
+    ps.seg.tok0 = tok0;
     ps.seg.nmem = (int32_t)members.size();
     ps.seg.mem = 0;
     for (size_t j = 0; j < members.size(); ++j) {
@@ -444,12 +450,22 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
         }
       };
 
-  for (int b = 0; b < batch; ++b) plan->kv_bytes_logical += s->seqs[seqs[b]].length * tok_bytes;
-  if (grouping) {
+  if (keep_last >= 0) {
+    // windows: [lo, L) from page lo / P, masked below lo % P on that page
+    for (int b = 0; b < batch; ++b) {
+      const int64_t L = s->seqs[seqs[b]].length, lo = std::max<int64_t>(0, L - keep_last);
+      plan->kv_bytes_logical += (L - lo) * tok_bytes;
+      const int64_t p0 = lo / s->P;
+      if (L > lo) add_seg(seqs[b], (int32_t)p0, L - p0 * s->P, single_mfma, {b}, (int32_t)(lo - p0 * s->P));
+    }
+    plan->pages_reread = batch > 1; // branches' windows often meet on shared pages
+  } else if (grouping) {
+    for (int b = 0; b < batch; ++b) plan->kv_bytes_logical += s->seqs[seqs[b]].length * tok_bytes;
     std::vector<int> all(batch);
     for (int b = 0; b < batch; ++b) all[b] = b;
     node(all, 0, 0);
   } else {
+    for (int b = 0; b < batch; ++b) plan->kv_bytes_logical += s->seqs[seqs[b]].length * tok_bytes;
     // per-sequence tiles; pages two entries share are read twice
     for (int b = 0; b < batch && !plan->pages_reread; ++b)
       for (int c = b + 1; c < batch; ++c)
@@ -476,8 +492,9 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     ps.seg.start = (int32_t)plan->total[L];
     plan->seg_index[i] = count[L]++;
     plan->total[L] += (np + s->row_pad[L]) * hkv;
-    plan->kv_bytes += (int64_t)ps.seg.ntok * tok_bytes;
-    (L == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += (int64_t)ps.seg.ntok * tok_bytes;
+    const int64_t seg_bytes = (int64_t)(ps.seg.ntok - ps.seg.tok0) * tok_bytes;
+    plan->kv_bytes += seg_bytes;
+    (L == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += seg_bytes;
     plan->io_bytes += np * 4;
   }
   int32_t slots = 0;
@@ -519,9 +536,11 @@ sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float 
   return st;
 }
 
-sq::MergeStatic merge_static(sq_store *s, float *out) {
+sq::MergeStatic merge_static(sq_store *s, float *out, const float *sinks) {
   sq::MergeStatic st{};
   st.out = out;
+  st.sinks = sinks;
+  st.sink_scale = 1.4426950408889634f;
   st.part_m = s->part_m;
   st.part_l = s->part_l;
   st.part_acc = s->part_acc;
@@ -790,6 +809,17 @@ namespace {
 
 // One token for each of `batch` distinct sequences (sq_append_batch and
 // sq_step_begin): the checks, made before anything changes.
+// Attention options, checked; null = none.
+sq_status take_opts(const sq_attn_opts *opts, sq_attn_opts *o) {
+  *o = sq_attn_opts{};
+  if (!opts) return SQ_OK;
+  if (opts->window < 0) return fail(SQ_ERR_INVALID, "window %d < 0", opts->window);
+  if (opts->reserved != 0) return fail(SQ_ERR_INVALID, "sq_attn_opts.reserved must be 0");
+  if (((uintptr_t)opts->sinks & 3u) != 0) return fail(SQ_ERR_INVALID, "sinks must be 4-byte aligned");
+  *o = *opts;
+  return SQ_OK;
+}
+
 sq_status check_one_token_each(sq_store *s, const sq_seq *seqs, int32_t batch) {
   if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
   if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
@@ -1256,6 +1286,15 @@ sq_status sq_decode_plan_info(sq_store *s, const sq_seq *seqs, int32_t batch, in
 
 sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
                          const void *q, float *out, float scale, int32_t mode, void *stream) {
+  return sq_decode_attn_ex(s, layer, seqs, batch, q, out, scale, mode, nullptr, stream);
+}
+
+sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
+                            const void *q, float *out, float scale, int32_t mode,
+                            const sq_attn_opts *opts, void *stream) {
+  sq_attn_opts o{};
+  sq_status r = take_opts(opts, &o);
+  if (r != SQ_OK) return r;
   if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
   if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
   if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
@@ -1267,7 +1306,7 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   for (int b = 0; b < batch; ++b)
     if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
   Plan plan;
-  sq_status r = build_plan(s, seqs, batch, mode, &plan);
+  r = build_plan(s, seqs, batch, mode, &plan, o.window > 0 ? o.window : -1);
   if (r != SQ_OK) return r;
 
   hipStream_t strm = static_cast<hipStream_t>(stream);
@@ -1276,7 +1315,7 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
   sq::MergeArgs ma{};
   da[0].st = decode_static(s, layer, q, scale, !plan.pages_reread);
   da[1].st = da[0].st;
-  ma.st = merge_static(s, out);
+  ma.st = merge_static(s, out, o.sinks);
   sq::DecodeDyn dyn[2]{};
   fill_dyn(s, plan, dyn, &ma.dyn);
   for (int pass = 0; pass < 2; ++pass) {
@@ -1302,22 +1341,34 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
 
 sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,
                         void *stream) {
+  return sq_step_begin_ex(s, seqs, batch, mode, 0, stream);
+}
+
+sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,
+                           int32_t window, void *stream) {
   sq_status r = check_one_token_each(s, seqs, batch);
   if (r != SQ_OK) return r;
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
+  if (window < 0) return fail(SQ_ERR_INVALID, "window %d < 0", window);
   if (s->device && mode != SQ_ATTN_STREAM && s->mfma_waves != 4)
     return fail(SQ_ERR_INVALID, "decode steps need 4 waves per MFMA work item");
-  // attention over the tokens before the step; the new ones join in the merge
-  Plan plan;
+  // attention over the tokens before the step; the new ones join in the
+  // merge (a window of W keys: the new token and the last W - 1 old ones)
+  Plan plan, plan_w;
   r = build_plan(s, seqs, batch, mode, &plan);
   if (r != SQ_OK) return r;
+  if (window > 0) {
+    r = build_plan(s, seqs, batch, mode, &plan_w, window - 1);
+    if (r != SQ_OK) return r;
+  }
   // which launches a layer makes depends on the mode only, so that a
   // captured step replays for every later step of the same batch and mode
   const bool launch[2] = {mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
                               (mode == SQ_ATTN_AUTO && !s->auto_single_mfma),
                           mode != SQ_ATTN_STREAM};
   for (int L = 0; L < 2; ++L)
-    if (plan.n_wg[L] > 0 && !launch[L]) return fail(SQ_ERR_INVALID, "internal: step plan needs an unlaunched kernel");
+    if ((plan.n_wg[L] > 0 || plan_w.n_wg[L] > 0) && !launch[L])
+      return fail(SQ_ERR_INVALID, "internal: step plan needs an unlaunched kernel");
   if (s->device && s->step_pending) { // the staging copy of the last step's plan
     hipError_t e = hipEventSynchronize(s->step_ev);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(step plan)");
@@ -1327,6 +1378,7 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
   if (sp) {
     std::memset(sp, 0, sizeof(*sp));
     fill_dyn(s, plan, sp->dec, &sp->merge);
+    if (window > 0) fill_dyn(s, plan_w, sp->dec_w, &sp->merge_w);
   }
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
   TokenSlots t;
@@ -1351,6 +1403,9 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
   }
   st.kv_bytes = plan.kv_bytes + batch * tok_bytes;
   st.kv_bytes_logical = plan.kv_bytes_logical + batch * tok_bytes;
+  st.window = window;
+  st.kv_bytes_w = plan_w.kv_bytes + batch * tok_bytes;
+  st.kv_bytes_logical_w = plan_w.kv_bytes_logical + batch * tok_bytes;
   if (!s->device) return SQ_OK;
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
@@ -1376,6 +1431,15 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
 
 sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void *v_new,
                        const void *q, float *out, float scale, void *stream) {
+  return sq_step_attn_ex(s, layer, k_new, v_new, q, out, scale, nullptr, stream);
+}
+
+sq_status sq_step_attn_ex(sq_store *s, int32_t layer, const void *k_new, const void *v_new,
+                          const void *q, float *out, float scale, const sq_attn_opts *opts,
+                          void *stream) {
+  sq_attn_opts o{};
+  sq_status r = take_opts(opts, &o);
+  if (r != SQ_OK) return r;
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
   const sq_store::Step &st = s->step;
@@ -1386,6 +1450,9 @@ sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void
       !aligned16(out))
     return fail(SQ_ERR_INVALID, "k_new, v_new, q and out must be non-null and 16-byte aligned");
   if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
+  if (o.window != 0 && o.window != st.window)
+    return fail(SQ_ERR_INVALID, "window %d: the step was begun with window %d", o.window, st.window);
+  const bool win = o.window != 0;
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
   hipStreamCaptureStatus cap = hipStreamCaptureStatusNone;
@@ -1396,15 +1463,16 @@ sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void
     if (!st.launch[L]) continue;
     ProfPair pp;
     const bool on = prof && s->prof_begin(strm, &pp, L == 0 ? kProfValu : kProfMfma);
-    hipError_t e = L == 0 ? sq::launch_step_valu(s->D, s->G, ds, &s->step_dev->dec[0], st.grid[0], strm)
-                          : sq::launch_step_mfma(s->D, s->G, s->mfma_waves, ds, &s->step_dev->dec[1],
-                                                 st.grid[1], strm);
+    const sq::DecodeDyn *dd = win ? s->step_dev->dec_w : s->step_dev->dec;
+    hipError_t e = L == 0 ? sq::launch_step_valu(s->D, s->G, ds, &dd[0], st.grid[0], strm)
+                          : sq::launch_step_mfma(s->D, s->G, s->mfma_waves, ds, &dd[1], st.grid[1], strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "decode step kernel");
   }
   sq::StepMergeArgs ma{};
-  ma.st = merge_static(s, out);
+  ma.st = merge_static(s, out, o.sinks);
   ma.plan = s->step_dev;
+  ma.windowed = win ? 1 : 0;
   ma.q = static_cast<const uint16_t *>(q);
   ma.k_new = static_cast<const uint16_t *>(k_new);
   ma.v_new = static_cast<const uint16_t *>(v_new);
@@ -1420,13 +1488,21 @@ sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void
   s->prof_end(strm, &pp, on);
   if (e != hipSuccess) return hip_fail(e, "decode step merge");
   ++s->st.decode_calls;
-  s->st.decode_kv_bytes += st.kv_bytes;
-  s->st.decode_kv_bytes_logical += st.kv_bytes_logical;
+  s->st.decode_kv_bytes += win ? st.kv_bytes_w : st.kv_bytes;
+  s->st.decode_kv_bytes_logical += win ? st.kv_bytes_logical_w : st.kv_bytes_logical;
   return SQ_OK;
 }
 
 sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, const void *q,
                          float *out, float scale, void *stream) {
+  return sq_extend_attn_ex(s, layer, seq, n_new, q, out, scale, nullptr, stream);
+}
+
+sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, const void *q,
+                            float *out, float scale, const sq_attn_opts *opts, void *stream) {
+  sq_attn_opts o{};
+  sq_status r = take_opts(opts, &o);
+  if (r != SQ_OK) return r;
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
   if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
@@ -1457,10 +1533,15 @@ sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, 
   const int tq = sq::kExtRows / s->G;
   a.n_qblocks = (n_new + tq - 1) / tq;
   a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  a.sinks = o.sinks;
+  a.window = o.window;
+  a.sink_scale = 1.4426950408889634f;
   // A chunk too short to give every CU two rounds of workgroups splits the
   // key range of each query block (at least 4 blocks of 64 keys per split)
   // and merges the partial rows in a second launch.
-  const int64_t key_blocks = (sqn->length + sq::kExtKeys - 1) / sq::kExtKeys; // the last query block's
+  int64_t key_blocks = (sqn->length + sq::kExtKeys - 1) / sq::kExtKeys; // the last query block's
+  if (o.window > 0) // a query block's keys span at most W + TQ - 1 indices
+    key_blocks = std::min<int64_t>(key_blocks, ((int64_t)o.window + tq - 2) / sq::kExtKeys + 2);
   const int64_t base_wg = (int64_t)a.n_qblocks * a.hkv;
   const int64_t target = 4LL * s->cus;
   int64_t split = 1;
@@ -1484,7 +1565,9 @@ sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, 
   if (e != hipSuccess) return hip_fail(e, "extend kernel");
   ++s->st.extend_calls;
   s->st.extend_tokens += n_new;
-  s->st.extend_kv_bytes += sqn->length * (int64_t)s->cfg.num_kv_heads * s->D * 2 * 2;
+  const int64_t keys_read = o.window > 0 ? std::min<int64_t>(sqn->length, (int64_t)n_new + o.window - 1)
+                                         : sqn->length;
+  s->st.extend_kv_bytes += keys_read * (int64_t)s->cfg.num_kv_heads * s->D * 2 * 2;
   return SQ_OK;
 }
 

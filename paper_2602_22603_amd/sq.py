@@ -74,6 +74,10 @@ class PlanInfo(C.Structure):
                 ("io_bytes", C.c_int64)]
 
 
+class AttnOpts(C.Structure):
+    _fields_ = [("sinks", C.c_void_p), ("window", C.c_int32), ("reserved", C.c_int32)]
+
+
 class Profile(C.Structure):
     _fields_ = ([(n, C.c_double) for n in ("decode_valu_ms", "decode_mfma_ms", "decode_merge_ms",
                                             "evict_scan_ms", "evict_gather_ms", "append_ms")] +
@@ -110,6 +114,15 @@ _SIGS = {
                                C.c_void_p, C.c_float, C.c_void_p]),
     "sq_extend_attn": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_float, C.c_void_p]),
+    "sq_decode_attn_ex": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
+                                    C.c_void_p, C.c_void_p, C.c_float, C.c_int32,
+                                    C.POINTER(AttnOpts), C.c_void_p]),
+    "sq_extend_attn_ex": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
+                                    C.c_void_p, C.c_float, C.POINTER(AttnOpts), C.c_void_p]),
+    "sq_step_begin_ex": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
+                                   C.c_int32, C.c_void_p]),
+    "sq_step_attn_ex": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
+                                  C.c_void_p, C.c_float, C.POINTER(AttnOpts), C.c_void_p]),
     "sq_decode_plan_info": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
                                       C.POINTER(PlanInfo)]),
     "sq_seq_info": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(SeqDesc)]),
@@ -261,6 +274,19 @@ class Store:
         return (self._tensor(k_new, shape, torch.bfloat16, "k_new"),
                 self._tensor(v_new, shape, torch.bfloat16, "v_new"))
 
+    def _opts(self, window, sinks):
+        """AttnOpts for (window, sinks) or None when neither is set; sinks is
+        a float32 tensor [Hq] on the store's device."""
+        import torch
+        if not window and sinks is None:
+            return None
+        o = AttnOpts()
+        o.window = int(window)
+        if sinks is not None:
+            o.sinks = (_ptr(sinks) if self.metadata_only else
+                       self._tensor(sinks, (self.num_q_heads,), torch.float32, "sinks"))
+        return o
+
     def _qo_ptrs(self, q, out, rows):
         import torch
         shape = (rows, self.num_q_heads, self.head_dim)
@@ -308,8 +334,10 @@ class Store:
                                     C.byref(es)))
         return {n: getattr(es, n) for n, _ in EvictStats._fields_}
 
-    def decode(self, layer, seqs, q, out=None, scale=None, mode=ATTN_AUTO, stream=None):
-        """out[b, h] = attention of q[b, h] (bf16 [B, Hq, D]) over seqs[b]; fp32."""
+    def decode(self, layer, seqs, q, out=None, scale=None, mode=ATTN_AUTO, stream=None,
+               window=0, sinks=None):
+        """out[b, h] = attention of q[b, h] (bf16 [B, Hq, D]) over seqs[b]; fp32.
+        window > 0: the last `window` keys only; sinks: fp32 [Hq] sink logits."""
         import torch
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
@@ -317,26 +345,38 @@ class Store:
             scale = 1.0 / float(self.head_dim) ** 0.5
         seqs = list(seqs)
         qp, op = (_ptr(q), _ptr(out)) if self.metadata_only else self._qo_ptrs(q, out, len(seqs))
-        _check(lib().sq_decode_attn(self._handle, layer, _i32_array(seqs), len(seqs), qp, op,
-                                    float(scale), mode, _stream(stream)))
+        o = self._opts(window, sinks)
+        if o is None:
+            _check(lib().sq_decode_attn(self._handle, layer, _i32_array(seqs), len(seqs), qp, op,
+                                        float(scale), mode, _stream(stream)))
+        else:
+            _check(lib().sq_decode_attn_ex(self._handle, layer, _i32_array(seqs), len(seqs), qp,
+                                           op, float(scale), mode, C.byref(o), _stream(stream)))
         return out
 
-    def step_begin(self, seqs, mode=ATTN_AUTO, stream=None):
+    def step_begin(self, seqs, mode=ATTN_AUTO, stream=None, window=0):
         """Open a decode step: one token slot appended to each of seqs (their
-        K/V arrive layer by layer through step_attn)."""
+        K/V arrive layer by layer through step_attn).  window > 0 also plans
+        layers that attend to the last `window` keys only."""
         seqs = list(seqs)
         st = C.c_void_p(0) if self.metadata_only else _stream(stream)
         # the C side trusts buffer sizes: step_attn checks them against the
         # batch of the last step this binding opened, and refuses after a
         # failed step_begin
         self._step_batch = None
-        _check(lib().sq_step_begin(self._handle, _i32_array(seqs), len(seqs), mode, st))
+        if window:
+            _check(lib().sq_step_begin_ex(self._handle, _i32_array(seqs), len(seqs), mode,
+                                          int(window), st))
+        else:
+            _check(lib().sq_step_begin(self._handle, _i32_array(seqs), len(seqs), mode, st))
         self._step_batch = len(seqs)
 
-    def step_attn(self, layer, k_new, v_new, q, out=None, scale=None, stream=None):
+    def step_attn(self, layer, k_new, v_new, q, out=None, scale=None, stream=None, window=0,
+                  sinks=None):
         """One layer of the open step: store k_new, v_new (bf16 [B, Hkv, D])
         and attend with q (bf16 [B, Hq, D]) over every token, the new one
-        included; returns out (fp32 [B, Hq, D])."""
+        included; returns out (fp32 [B, Hq, D]).  window: 0 or the step's
+        window; sinks: fp32 [Hq] sink logits."""
         import torch
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
@@ -351,12 +391,18 @@ class Store:
             kv = (b, self.num_kv_heads, self.head_dim)
             ptrs = (self._tensor(k_new, kv, torch.bfloat16, "k_new"),
                     self._tensor(v_new, kv, torch.bfloat16, "v_new"), *self._qo_ptrs(q, out, b))
-        _check(lib().sq_step_attn(self._handle, layer, *ptrs, float(scale), _stream(stream)))
+        o = self._opts(window, sinks)
+        if o is None:
+            _check(lib().sq_step_attn(self._handle, layer, *ptrs, float(scale), _stream(stream)))
+        else:
+            _check(lib().sq_step_attn_ex(self._handle, layer, *ptrs, float(scale), C.byref(o),
+                                         _stream(stream)))
         return out
 
-    def extend(self, layer, seq, q, out=None, scale=None, stream=None):
+    def extend(self, layer, seq, q, out=None, scale=None, stream=None, window=0, sinks=None):
         """Causal attention of the last n = q.shape[0] tokens of seq (just
-        appended) over the cache: q bf16 [n, Hq, D] -> out fp32 [n, Hq, D]."""
+        appended) over the cache: q bf16 [n, Hq, D] -> out fp32 [n, Hq, D].
+        window > 0: each token sees its last `window` keys; sinks: fp32 [Hq]."""
         import torch
         if out is None:
             out = torch.empty(q.shape, dtype=torch.float32, device=q.device)
@@ -364,8 +410,13 @@ class Store:
             scale = 1.0 / float(self.head_dim) ** 0.5
         n = int(q.shape[0])
         qp, op = (_ptr(q), _ptr(out)) if self.metadata_only else self._qo_ptrs(q, out, n)
-        _check(lib().sq_extend_attn(self._handle, layer, seq, n, qp, op, float(scale),
-                                    _stream(stream)))
+        o = self._opts(window, sinks)
+        if o is None:
+            _check(lib().sq_extend_attn(self._handle, layer, seq, n, qp, op, float(scale),
+                                        _stream(stream)))
+        else:
+            _check(lib().sq_extend_attn_ex(self._handle, layer, seq, n, qp, op, float(scale),
+                                           C.byref(o), _stream(stream)))
         return out
 
     def plan_info(self, seqs, mode=ATTN_AUTO):

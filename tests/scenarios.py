@@ -211,7 +211,13 @@ class Twin:
             assert np.array_equal(gk, ok), f"K of {h}"
             assert np.array_equal(gv, ov), f"V of {h}"
 
-    def decode_errors(self, seqs, modes=None, layer=0, scale=None):
+    def sinks(self, spread=2.0):
+        """Seeded fp32 sink logits [Hq] (float32 values, as the kernels read them)."""
+        return (self.rng.standard_normal(self.hq) * spread).astype(np.float32)
+
+    def decode_errors(self, seqs, modes=None, layer=0, scale=None, window=0, sinks=None):
+        """Max abs error of sq_decode_attn in each mode against the oracle;
+        window and sinks (fp32 [Hq] numpy) are the model-variant options."""
         import torch
         sq = self.sq
         modes = [sq.ATTN_AUTO, sq.ATTN_STREAM, sq.ATTN_SHARED_PREFIX, sq.ATTN_MFMA] if modes is None else modes
@@ -222,20 +228,26 @@ class Twin:
         for h in seqs:
             k, v, _ = self.model.view(h)
             views.append((k[:, layer], v[:, layer]))
-        ref = oatt.decode_batch(wl.bf16_value(qb), views, scale, self.group)
+        ref = oatt.decode_batch(wl.bf16_value(qb), views, scale, self.group, window=window,
+                                sinks=None if sinks is None else sinks.astype(np.float64))
+        sk = None if sinks is None else torch.from_numpy(sinks).to(self.device)
         errs = {}
         for m in modes:
-            out = self.store.decode(layer, seqs, q, scale=scale, mode=m)
+            out = self.store.decode(layer, seqs, q, scale=scale, mode=m, window=window, sinks=sk)
             torch.cuda.synchronize()
             errs[m] = max_abs(out.cpu().numpy(), ref)
         return errs, ref
 
-    def step(self, seqs, mode=None, scale=None, graph=None):
+    def step(self, seqs, mode=None, scale=None, graph=None, window=0, layer_windows=None,
+             sinks=None):
         """One decode step of every layer through sq_step_begin / sq_step_attn
         (or, with ``graph``, a replay of captured sq_step_attn calls: a dict
         with the graph and its fixed k/v/q/out buffers), mirrored in the
         oracle as a one-token append to each sequence followed by attention.
-        Returns the max abs error over all layers and entries."""
+        ``window`` opens the step with a windowed plan, ``layer_windows[l]``
+        (0 or window) is layer l's window, ``sinks`` (fp32 [Hq] numpy, or a
+        list of one per layer) its sink logits.  Returns the max abs error
+        over all layers and entries."""
         import torch
         sq = self.sq
         mode = sq.ATTN_AUTO if mode is None else mode
@@ -244,10 +256,14 @@ class Twin:
         kb = wl.normal_bf16(self.rng, (self.nl, b, self.hkv, self.d))
         vb = wl.normal_bf16(self.rng, (self.nl, b, self.hkv, self.d))
         qb = wl.normal_bf16(self.rng, (self.nl, b, self.hq, self.d))
-        self.store.step_begin(seqs, mode)
+        lw = [0] * self.nl if layer_windows is None else list(layer_windows)
+        ls = sinks if isinstance(sinks, list) else [sinks] * self.nl
+        self.store.step_begin(seqs, mode, window=window)
         if graph is None:
             k, v, q = (wl.to_torch_bf16(x, self.device) for x in (kb, vb, qb))
-            outs = [self.store.step_attn(l, k[l], v[l], q[l], scale=scale) for l in range(self.nl)]
+            sk = [None if x is None else torch.from_numpy(x).to(self.device) for x in ls]
+            outs = [self.store.step_attn(l, k[l], v[l], q[l], scale=scale, window=lw[l], sinks=sk[l])
+                    for l in range(self.nl)]
         else:
             for name, x in (("k", kb), ("v", vb), ("q", qb)):
                 graph[name].copy_(wl.to_torch_bf16(x, self.device))
@@ -265,7 +281,8 @@ class Twin:
             for h in seqs:
                 kk, vv, _ = self.model.view(h)
                 views.append((kk[:, l], vv[:, l]))
-            ref = oatt.decode_batch(qf[l], views, scale, self.group)
+            ref = oatt.decode_batch(qf[l], views, scale, self.group, window=lw[l],
+                                    sinks=None if ls[l] is None else ls[l].astype(np.float64))
             err = max(err, max_abs(got[l], ref))
         return err, got
 

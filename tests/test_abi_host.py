@@ -271,6 +271,35 @@ def test_attention_needs_a_device_store(sq):
     assert before == (s.page_table(a), s.stats())
 
 
+def test_attention_options_are_checked_first(sq):
+    """sq_attn_opts errors (negative window, reserved field, misaligned
+    sinks) are reported before anything else and change nothing; a windowed
+    step opens on a metadata-only store exactly like a plain one."""
+    import ctypes as C
+    s = _store(sq, 8, 4, 2, 8)
+    a = s.seq_create()
+    s.append(a, n=6)
+    seqs = (C.c_int32 * 1)(a)
+    before = (s.page_table(a), s.stats())
+    for window, reserved, sinks, what in ((-1, 0, None, b"window"), (0, 1, None, b"reserved"),
+                                          (4, 0, 6, b"aligned")):
+        o = sq.AttnOpts()
+        o.window, o.reserved, o.sinks = window, reserved, sinks
+        rc = sq.lib().sq_decode_attn_ex(s._handle, 0, seqs, 1, None, None, C.c_float(0.5), 0,
+                                        C.byref(o), None)
+        assert rc == sq.ERR_INVALID and what in sq.lib().sq_last_error()
+        rc = sq.lib().sq_extend_attn_ex(s._handle, 0, a, 2, None, None, C.c_float(0.5),
+                                        C.byref(o), None)
+        assert rc == sq.ERR_INVALID and what in sq.lib().sq_last_error()
+        rc = sq.lib().sq_step_attn_ex(s._handle, 0, None, None, None, None, C.c_float(0.5),
+                                      C.byref(o), None)
+        assert rc == sq.ERR_INVALID and what in sq.lib().sq_last_error()
+    assert sq.lib().sq_step_begin_ex(s._handle, seqs, 1, 0, -2, None) == sq.ERR_INVALID
+    assert before == (s.page_table(a), s.stats())
+    s.step_begin([a], window=3)
+    assert s.seq_info(a)["length"] == 7
+
+
 def test_decode_step_metadata(sq):
     """sq_step_begin opens one token slot per sequence exactly as
     sq_append_batch appends one token (pages, positions, refcounts, stats);
