@@ -47,7 +47,7 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--tasks", type=int, default=8)
     ap.add_argument("--ctx", type=int, default=131072)
-    ap.add_argument("--legs", default="decode,modes,evict,extend,outlier,fullstack,cpu",
+    ap.add_argument("--legs", default="decode,modes,evict,extend,outlier,variants,fullstack,cpu",
                     help="comma list of: decode, modes, evict, extend, outlier, fullstack, cpu, copy "
                          "(a plain 1 GiB device copy used to calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -430,6 +430,61 @@ def extend_leg(sq, torch, wl, reps=10):
     return res
 
 
+def variants_leg(sq, torch, wl, reps=20, window=128):
+    """Attention options on the 128K shared-prefix batch with 64 query / 8 KV
+    heads of dimension 64 and two layers: layer 0 attends to a window of the
+    last 128 keys, layer 1 to every key, both with per-head sinks (a model
+    whose layers alternate).  Times each layer's decode call and a fused
+    step over both layers."""
+    from paper_2602_22603_amd import drivers
+    store, seqs, _ = drivers.build_shared128k(layers=2, heads=(64, 8, 64), keep_inputs=(),
+                                              extra_tokens=2 * (reps + 8) + 16)
+    B = len(seqs)
+    q = wl.device_normal_bf16((B, 64, 64), 700, "cuda")
+    kn = wl.device_normal_bf16((B, 8, 64), 701, "cuda")
+    out = torch.empty((B, 64, 64), dtype=torch.float32, device="cuda")
+    sinks = torch.randn(64, generator=torch.Generator().manual_seed(702)).float().to("cuda")
+    res = {}
+    for name, layer, w, sk in (("full", 1, 0, None), ("full_sinks", 1, 0, sinks),
+                               ("window_sinks", 0, window, sinks)):
+        call = lambda: store.decode(layer, seqs, q, out=out, window=w, sinks=sk)
+        for _ in range(3):
+            call()
+        st0 = store.stats()
+        store.profile_enable(True)
+        store.profile_read()
+        pct = time_events(torch, call, reps)
+        prof = store.profile_read()
+        store.profile_enable(False)
+        kv = (store.stats()["decode_kv_bytes"] - st0["decode_kv_bytes"]) / reps
+        kern = (prof["decode_mfma_ms"] + prof["decode_valu_ms"]) / max(1, reps)
+        res[name] = dict(call_ms=pct, kernel_ms=round(kern, 5), kv_bytes=kv,
+                         merge_ms=round(prof["decode_merge_ms"] / max(1, prof["decode_merge_launches"]), 5),
+                         kernel_gbps=round(kv / (kern * 1e-3) / 1e9, 1))
+
+    def step():
+        store.step_begin(seqs, window=window)
+        store.step_attn(0, kn, kn, q, out=out, window=window, sinks=sinks)
+        store.step_attn(1, kn, kn, q, out=out, sinks=sinks)
+    for _ in range(3):
+        step()
+    torch.cuda.synchronize()
+    st0 = store.stats()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        step()
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    kv = (store.stats()["decode_kv_bytes"] - st0["decode_kv_bytes"]) / reps
+    res["fused_step_two_layers"] = dict(ms_per_step=round(ms, 4), kv_bytes=kv,
+                                        gbps=round(kv / (ms * 1e-3) / 1e9, 1))
+    res["workload"] = (f"8 tasks x (main 131072 + forked aux 130816+512) tokens, 16 queries, "
+                       f"64q/8kv heads, head_dim 64, layer 0 window {window} + sinks, "
+                       f"layer 1 full (+ sinks), AUTO mode")
+    store.close()
+    return res
+
+
 def fullstack_leg(sq, torch, wl):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
     turns; with one-shot eviction, with eviction in 64-page chunks (bounded
@@ -652,6 +707,11 @@ def main():
     if "outlier" in legs:
         log("32K outlier leg ...")
         outlier = outlier_leg(sq, torch, wl)
+    variants = None
+    if "variants" in legs:
+        log("attention options leg (windows and sinks, 64q/8kv/64) ...")
+        variants = variants_leg(sq, torch, wl)
+        torch.cuda.empty_cache()
     fullstack = None
     if "fullstack" in legs:
         log("full-stack leg (36 layers, 16K -> 256K) ...")
@@ -691,6 +751,7 @@ def main():
         "evict": evict,
         "extend": extend,
         "outlier32k": outlier,
+        "attention_options": variants,
         "full_stack": fullstack,
         "cpu_baseline": cpu,
         "kernel_sources_sha": kernel_sha(),

@@ -15,24 +15,27 @@ from . import workload as wl
 
 
 def build_shared128k(tasks=8, ctx=131072, aux_private=512, parallel=256, extra_tokens=256,
-                     keep_inputs=(0,), device="cuda"):
+                     keep_inputs=(0,), device="cuda", layers=1, heads=(32, 8, 128)):
     """``tasks`` main threads of ``ctx`` tokens, each with an auxiliary thread
     forked at ctx - parallel (the main thread then decodes ``parallel`` more
     tokens) that adds ``aux_private`` tokens.  Returns (store, seqs, inputs)
     with seqs = [main_0, aux_0, main_1, aux_1, ...] and inputs[t] =
-    (k, v, k_aux, v_aux) for the tasks in ``keep_inputs``."""
+    (k, v, k_aux, v_aux) for the tasks in ``keep_inputs``.  heads = (query
+    heads, KV heads, head_dim)."""
     import torch
     w = wl.shared128k(n_tasks=tasks, main_len=ctx, fork_at=ctx - parallel, aux_private=aux_private)
     pages_task = ctx // 16 + aux_private // 16 + 2 * (extra_tokens // 16 + 2)
-    store = _sq.Store(1, 32, 8, 128, num_pages=tasks * pages_task + 64, max_seqs=2 * tasks + 4,
+    hq, hkv, d = heads
+    store = _sq.Store(layers, hq, hkv, d, num_pages=tasks * pages_task + 64, max_seqs=2 * tasks + 4,
                       max_pages_per_seq=ctx // 16 + extra_tokens // 16 + 64, device=device)
     seqs, inputs = [], {}
     for t in range(tasks):
-        k, v, ka, va = shared_task_inputs(w, t, device)
+        k, v, ka, va = shared_task_inputs(w, t, device, layers, hkv, d)
         main = store.seq_create()
-        store.append(main, k[:, : w.fork_at], v[:, : w.fork_at])
+        cut = lambda x, a, b: x[:, a:b].contiguous() if layers > 1 else x[:, a:b]
+        store.append(main, cut(k, 0, w.fork_at), cut(v, 0, w.fork_at))
         aux = store.fork(main, w.fork_at)
-        store.append(main, k[:, w.fork_at:], v[:, w.fork_at:])
+        store.append(main, cut(k, w.fork_at, None), cut(v, w.fork_at, None))
         store.append(aux, ka, va)
         seqs += [main, aux]
         torch.cuda.synchronize()
@@ -43,12 +46,12 @@ def build_shared128k(tasks=8, ctx=131072, aux_private=512, parallel=256, extra_t
     return store, seqs, inputs
 
 
-def shared_task_inputs(w, t, device="cuda"):
+def shared_task_inputs(w, t, device="cuda", layers=1, hkv=8, d=128):
     """The K/V inputs of task t of a Shared128K workload (regenerable)."""
-    k = wl.device_normal_bf16((1, w.main_len, 8, 128), w.seed * 1000 + 4 * t, device)
-    v = wl.device_normal_bf16((1, w.main_len, 8, 128), w.seed * 1000 + 4 * t + 1, device)
-    ka = wl.device_normal_bf16((1, w.aux_private, 8, 128), w.seed * 1000 + 4 * t + 2, device)
-    va = wl.device_normal_bf16((1, w.aux_private, 8, 128), w.seed * 1000 + 4 * t + 3, device)
+    k = wl.device_normal_bf16((layers, w.main_len, hkv, d), w.seed * 1000 + 4 * t, device)
+    v = wl.device_normal_bf16((layers, w.main_len, hkv, d), w.seed * 1000 + 4 * t + 1, device)
+    ka = wl.device_normal_bf16((layers, w.aux_private, hkv, d), w.seed * 1000 + 4 * t + 2, device)
+    va = wl.device_normal_bf16((layers, w.aux_private, hkv, d), w.seed * 1000 + 4 * t + 3, device)
     return k, v, ka, va
 
 
