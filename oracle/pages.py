@@ -43,6 +43,16 @@ Readings adopted where the paper is silent (also listed in the design notes)
   above.
 * Positions are carried, never recomputed: a kept token keeps its position and
   new tokens continue from the counter.
+* Deferred eviction (NEXT-2 variant; the paper evicts at once, and masks
+  tokens only to simulate eviction, §3.3 and Algorithm 2): ``evict(...,
+  deferred=True)`` clears the keep flags of the spans' slots and drops their
+  cursors; pages, slots, length and the other spans stay as they are, and
+  attention sees the kept slots only (``view``).  A fork inherits the flags
+  of its slots.  The masked slots leave the store at the next physical
+  eviction of the sequence, which removes them together with its own spans
+  (the union, as maximal runs), or at ``compact``, which removes only them;
+  every remaining span then shifts left by the slots removed before its
+  ends.
 * Validation happens before any change: a failing call leaves the model as it
   was.  Error kinds: Invalid, NoPages, UnknownSeq, UnknownCursor, SpanError.
 * Sequence handles are small integers, lowest free handle first.
@@ -83,7 +93,7 @@ class SpanError(OracleError):
 
 
 class Seq:
-    __slots__ = ("pages", "length", "next_pos", "pos", "spans", "parent")
+    __slots__ = ("pages", "length", "next_pos", "pos", "spans", "parent", "keep")
 
     def __init__(self):
         self.pages = []
@@ -92,6 +102,7 @@ class Seq:
         self.pos = []  # logical position of each token
         self.spans = {}  # cursor id -> (start, end), current coordinates
         self.parent = -1
+        self.keep = []  # per slot: False once a deferred eviction masked it
 
 
 class PageModel:
@@ -200,6 +211,7 @@ class PageModel:
                 self.V[page, slot] = np.asarray(v_new, dtype=np.float64)[:, i]
                 self.POS[page, slot] = seq.next_pos
             seq.pos.append(seq.next_pos)
+            seq.keep.append(True)
             seq.next_pos += 1
             seq.length += 1
 
@@ -242,6 +254,7 @@ class PageModel:
             child.pages.append(page)
         child.length = fork_len
         child.pos = list(par.pos[:fork_len])
+        child.keep = list(par.keep[:fork_len])
         child.next_pos = par.next_pos if fork_len == par.length else par.pos[fork_len]
         child.spans = {c: se for c, se in par.spans.items() if se[1] <= fork_len}
         child.parent = parent
@@ -254,16 +267,53 @@ class PageModel:
         del self.seqs[h]
         return freed
 
-    def evict(self, h, cursor_ids):
-        """``clear_kv``: remove the tokens of ``cursor_ids`` from sequence h."""
+    @staticmethod
+    def _masked_runs(keep, extra=()):
+        """Maximal runs [s, e) of slots that are masked or inside one of the
+        ``extra`` spans, in order."""
+        out = np.logical_not(np.asarray(keep, dtype=bool))
+        for s, e in extra:
+            out[s:e] = True
+        runs, i, n = [], 0, len(out)
+        while i < n:
+            if out[i]:
+                j = i
+                while j < n and out[j]:
+                    j += 1
+                runs.append((i, j))
+                i = j
+            else:
+                i += 1
+        return runs
+
+    def compact(self, h):
+        """Remove the slots deferred evictions masked (a physical eviction
+        of no cursor)."""
+        return self.evict(h, [])
+
+    def evict(self, h, cursor_ids, deferred=False):
+        """``clear_kv``: remove the tokens of ``cursor_ids`` from sequence h
+        (and any slots earlier deferred evictions masked); ``deferred`` only
+        masks them."""
         seq = self._seq(h)
         ids = list(dict.fromkeys(int(c) for c in cursor_ids))
         for c in ids:
             if c not in seq.spans:
                 raise UnknownCursor(f"cursor {c} not registered")
-        spans = sorted(seq.spans[c] for c in ids if seq.spans[c][1] > seq.spans[c][0])
+        own = [seq.spans[c] for c in ids if seq.spans[c][1] > seq.spans[c][0]]
         stats = dict(tokens_removed=0, tokens_moved=0, pages_allocated=0,
-                     pages_freed=0, first_evicted=seq.length, pages_remapped=0)
+                     pages_freed=0, first_evicted=seq.length, pages_remapped=0,
+                     tokens_masked=0)
+        if deferred:
+            for s0, e0 in own:
+                stats["tokens_masked"] += sum(seq.keep[s0:e0])
+                seq.keep[s0:e0] = [False] * (e0 - s0)
+            for c in ids:
+                del seq.spans[c]
+            masked = [i for i, k in enumerate(seq.keep) if not k]
+            stats["first_evicted"] = masked[0] if masked else seq.length
+            return stats
+        spans = self._masked_runs(seq.keep, own)
         if not spans:
             for c in ids:
                 del seq.spans[c]
@@ -333,6 +383,7 @@ class PageModel:
             self.POS[dp, ds] = moved_pos
         seq.pages = seq.pages[:fp] + new_pages
         seq.pos = [p for p, k in zip(seq.pos, keep) if k]
+        seq.keep = [True] * new_len
         old_len = seq.length
         seq.length = new_len
         for c in ids:
@@ -351,15 +402,29 @@ class PageModel:
     def info(self, h):
         seq = self._seq(h)
         return dict(length=seq.length, next_pos=seq.next_pos, n_pages=len(seq.pages),
-                    parent=seq.parent, n_spans=len(seq.spans))
+                    parent=seq.parent, n_spans=len(seq.spans),
+                    n_masked=len(seq.keep) - sum(seq.keep))
+
+    def keep_flags(self, h):
+        """Per slot: 1 = attended, 0 = masked by a deferred eviction."""
+        return np.asarray(self._seq(h).keep, dtype=np.uint8)
 
     def spans(self, h):
         return dict(self._seq(h).spans)
 
     def view(self, h):
-        """Logical view of sequence h: (K [L, NL, Hkv, D], V, pos [L]).
+        """What attention sees of sequence h, its kept slots in order:
+        (K [L, NL, Hkv, D], V, pos [L]).  Without data only pos is returned
+        (K and V are None)."""
+        k, v, pos = self.slot_view(h)
+        keep = self.keep_flags(h).astype(bool)
+        if keep.all():
+            return k, v, pos
+        return (None if k is None else k[keep]), (None if v is None else v[keep]), pos[keep]
 
-        Without data only pos is returned (K and V are None)."""
+    def slot_view(self, h):
+        """Every slot of sequence h, masked ones included, as the pools hold
+        them: (K [L, NL, Hkv, D], V, pos [L])."""
         seq = self._seq(h)
         if not self.with_data:
             return None, None, np.asarray(seq.pos, dtype=np.int64)

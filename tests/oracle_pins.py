@@ -191,7 +191,8 @@ def check_span_shift(seed=9):
 # --------------------------------------------------------------------------
 class ListModel:
     """Naive context model: each sequence is a Python list of token records
-    (K row, V row, position); fork copies a prefix, evict filters."""
+    (K row, V row, position, attended); fork copies a prefix, evict filters,
+    a deferred eviction clears the attended flags in place."""
 
     def __init__(self):
         self.seqs = {}
@@ -203,7 +204,7 @@ class ListModel:
 
     def append(self, h, k_new, v_new):
         for i in range(k_new.shape[1]):
-            self.seqs[h].append((k_new[:, i].copy(), v_new[:, i].copy(), self.next_pos[h]))
+            self.seqs[h].append((k_new[:, i].copy(), v_new[:, i].copy(), self.next_pos[h], True))
             self.next_pos[h] += 1
 
     def fork(self, parent, f, child):
@@ -212,12 +213,20 @@ class ListModel:
         self.next_pos[child] = self.next_pos[parent] if f == len(par) else par[f][2]
         self.spans[child] = {c: se for c, se in self.spans[parent].items() if se[1] <= f}
 
+    def defer(self, h, cursors):
+        old = self.seqs[h]
+        for c in cursors:
+            s, e = self.spans[h][c]
+            for i in range(s, e):
+                old[i] = old[i][:3] + (False,)
+        self.spans[h] = {c: se for c, se in self.spans[h].items() if c not in cursors}
+
     def evict(self, h, cursors):
-        gone = set()
+        old = self.seqs[h]
+        gone = {i for i, t in enumerate(old) if not t[3]}
         for c in cursors:
             s, e = self.spans[h][c]
             gone.update(range(s, e))
-        old = self.seqs[h]
         # a span's new coordinates: count the surviving tokens before each end
         survivors_before = np.cumsum([0] + [0 if i in gone else 1 for i in range(len(old))])
         self.spans[h] = {c: (int(survivors_before[s]), int(survivors_before[e]))
@@ -225,7 +234,7 @@ class ListModel:
         self.seqs[h] = [t for i, t in enumerate(old) if i not in gone]
 
     def view(self, h):
-        toks = self.seqs[h]
+        toks = [t for t in self.seqs[h] if t[3]]
         if not toks:
             return None
         return (np.stack([t[0] for t in toks]), np.stack([t[1] for t in toks]),
@@ -238,11 +247,12 @@ def _state(model):
                            for h, s in model.seqs.items()}, model.peak_pages))
 
 
-def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False):
+def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False, deferred=False):
     """Random op sequences: the page model's logical views equal a naive list
     model's, for page sizes 1, 2, 4 and 16 (and each eviction chunk size).
     With ``remap`` half the marked spans are whole multiples of the page size,
-    so that page-aligned remaps happen; returns the pages remapped."""
+    so that page-aligned remaps happen; returns the pages remapped.  With
+    ``deferred`` evictions are also deferred and compactions happen."""
     rng = np.random.default_rng(seed)
     nl, hkv, d = 2, 2, 3
     remapped = 0
@@ -257,7 +267,10 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False):
         ref.create(h0)
         for _ in range(n_ops):
             live = sorted(model.seqs)
-            op = rng.choice(["append", "append", "mark", "fork", "evict", "release"])
+            ops = ["append", "append", "mark", "fork", "evict", "release"]
+            if deferred:
+                ops += ["defer", "defer", "compact"]
+            op = rng.choice(ops)
             h = int(rng.choice(live))
             if op == "append":
                 n = int(rng.integers(0, 2 * page + 3))
@@ -287,14 +300,27 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False):
                 pick = [c for c in cur if rng.random() < 0.5]
                 remapped += model.evict(h, pick)["pages_remapped"]
                 ref.evict(h, pick)
+            elif op == "defer":
+                cur = list(model.spans(h))
+                pick = [c for c in cur if rng.random() < 0.5]
+                pages = model.page_table(h)
+                model.evict(h, pick, deferred=True)
+                assert model.page_table(h) == pages  # nothing moves
+                ref.defer(h, pick)
+            elif op == "compact":
+                model.compact(h)
+                ref.evict(h, [])
+                assert model.info(h)["n_masked"] == 0
             elif op == "release" and len(live) > 1:
                 model.release(h)
                 del ref.seqs[h]
             for hh in model.seqs:
                 k, v, pos = model.view(hh)
                 want = ref.view(hh)
+                assert model.info(hh)["length"] == len(ref.seqs[hh])
+                assert model.keep_flags(hh).tolist() == [int(t[3]) for t in ref.seqs[hh]]
                 if want is None:
-                    assert model.info(hh)["length"] == 0
+                    assert len(pos) == 0
                     continue
                 assert np.array_equal(k, want[0]) and np.array_equal(v, want[1])
                 assert np.array_equal(pos, want[2])
@@ -330,7 +356,8 @@ def check_hand_worked_page_tables():
     st = m.evict(a, [7])                 # L' = 5 -> 2 new pages: 5, 6
     assert m.page_table(a) == [5, 6]
     assert st == dict(tokens_removed=5, tokens_moved=5, pages_allocated=2,
-                      pages_freed=1, first_evicted=1, pages_remapped=0)  # page 2 was a's alone
+                      pages_freed=1, first_evicted=1, pages_remapped=0,
+                      tokens_masked=0)  # page 2 was a's alone
     assert m.view(a)[2].tolist() == [0, 6, 7, 8, 9]
     assert m.refcount[:7].tolist() == [2, 1, 0, 1, 1, 1, 1]
     m.release(c)                         # page 0 -> 1 ref, page 3 freed
@@ -813,6 +840,72 @@ def check_windows(seed=23):
                 assert np.array_equal(with_s[jj], want)
 
 
+def check_deferred_against_list_model():
+    """Deferred evictions and compactions among the random ops (one-shot and
+    chunked schedules, with and without remap)."""
+    check_against_list_model(seed=24, n_ops=80, chunks=(0, 1), deferred=True)
+    check_against_list_model(seed=25, n_ops=60, remap=True, deferred=True)
+
+
+def check_deferred_by_hand():
+    """P = 4, ten tokens: a deferred eviction masks in place, a fork keeps
+    the masks of its slots, a later physical eviction removes the masked
+    slots with its own span (their union), and compaction alone removes only
+    the masked ones; worked by hand."""
+    m = pg.PageModel(num_pages=16, page_size=4, max_seqs=4, max_pages_per_seq=16)
+    a = m.seq_create()
+    m.append(a, 10)                                      # pages 0, 1, 2
+    m.span_mark(a, 1, 1, 3)
+    m.span_mark(a, 2, 6, 7)
+    m.span_mark(a, 3, 8, 9)
+    st = m.evict(a, [1, 2], deferred=True)
+    assert st["tokens_masked"] == 3 and st["tokens_removed"] == 0 and st["first_evicted"] == 1
+    assert m.page_table(a) == [0, 1, 2] and m.info(a)["length"] == 10
+    assert m.keep_flags(a).tolist() == [1, 0, 0, 1, 1, 1, 0, 1, 1, 1]
+    assert m.spans(a) == {3: (8, 9)}                     # unshifted
+    assert m.view(a)[2].tolist() == [0, 3, 4, 5, 7, 8, 9]
+    b = m.fork(a, 7)                                     # 1 page + 3 slots: page 3
+    assert m.page_table(b) == [0, 3]
+    assert m.keep_flags(b).tolist() == [1, 0, 0, 1, 1, 1, 0]
+    assert m.view(b)[2].tolist() == [0, 3, 4, 5]
+    m.span_mark(a, 4, 2, 5)                              # covers masked slot 2
+    st = m.evict(a, [4])                                 # removes [1, 5) and [6, 7)
+    assert st["tokens_removed"] == 5 and st["first_evicted"] == 1
+    assert m.info(a)["length"] == 5 and m.info(a)["n_masked"] == 0
+    assert m.view(a)[2].tolist() == [0, 5, 7, 8, 9]
+    assert m.spans(a) == {3: (3, 4)}                     # 8 - 5 removed before it
+    st = m.compact(b)                                    # b: [1, 3) and [6, 7)
+    assert st["tokens_removed"] == 3 and m.info(b)["length"] == 4
+    assert m.view(b)[2].tolist() == [0, 3, 4, 5] and m.keep_flags(b).tolist() == [1, 1, 1, 1]
+
+
+def check_deferred_then_compact_equals_immediate(seed=26):
+    """Deferring then compacting a set of spans leaves exactly the state an
+    immediate eviction of the same spans leaves (page tables, refcounts,
+    data, spans, stats but tokens_masked)."""
+    rng = np.random.default_rng(seed)
+    for page in (1, 4, 16):
+        models = [pg.PageModel(num_pages=600, page_size=page, max_seqs=4, max_pages_per_seq=300,
+                               layers=1, kv_heads=1, head_dim=2, with_data=True) for _ in range(2)]
+        k = rng.standard_normal((1, 200, 1, 2))
+        spans = [(s0, s0 + int(rng.integers(1, 20))) for s0 in range(5, 180, 23)]
+        for m in models:
+            h = m.seq_create()
+            m.append(h, 200, k, k)
+            m.fork(h, 150)
+            for c, (s0, e0) in enumerate(spans):
+                m.span_mark(h, c, s0, e0)
+        pick = [0, 2, 3, 7]
+        models[0].evict(0, pick, deferred=True)
+        st0 = models[0].compact(0)
+        st1 = models[1].evict(0, pick)
+        st0.pop("tokens_masked")
+        st1.pop("tokens_masked")
+        assert st0 == st1
+        assert _state(models[0]) == _state(models[1])
+        assert np.array_equal(models[0].K, models[1].K)
+
+
 ALL_CHECKS = [
     check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
     check_uniform_closed_form, check_two_key_closed_form,
@@ -828,4 +921,6 @@ ALL_CHECKS = [
     check_chunked_eviction_never_overwrites_unread_tokens,
     check_remap_against_list_model, check_remap_page_tables_by_hand,
     check_sinks_textbook, check_sink_closed_form, check_windows,
+    check_deferred_against_list_model, check_deferred_by_hand,
+    check_deferred_then_compact_equals_immediate,
 ]

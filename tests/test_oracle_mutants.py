@@ -16,6 +16,10 @@ from oracle import extend as ex
 from oracle import pages as pg
 from tests import oracle_pins as pins
 
+_ORIG_RUNS = pg.PageModel._masked_runs
+_ORIG_FORK = pg.PageModel.fork
+_ORIG_EVICT = pg.PageModel.evict
+
 
 def _scores_gqa_modulo(q, k, scale, group, mask=None):
     q = np.asarray(q, np.float64)
@@ -215,6 +219,25 @@ def _window_one_too_wide(n_keys, window):
     return _orig_window_mask(n_keys, window + 1 if window > 0 else 0)
 
 
+def _runs_ignore_masks(keep, extra=()):
+    return _ORIG_RUNS(np.ones(len(keep), dtype=bool), extra)
+
+
+def _fork_drops_masks(self, parent, fork_len):
+    h = _ORIG_FORK(self, parent, fork_len)
+    self.seqs[h].keep = [True] * fork_len
+    return h
+
+
+def _deferred_shifts_spans(self, h, cursor_ids, deferred=False):
+    seq = self.seqs[h]
+    gone = sorted(seq.spans[c] for c in cursor_ids if c in seq.spans)
+    st = _ORIG_EVICT(self, h, cursor_ids, deferred)
+    if deferred:
+        seq.spans = {c: ev.shift_span(a, b, gone) for c, (a, b) in seq.spans.items()}
+    return st
+
+
 def _extend_window_one_too_wide(q, k, v, scale, group, mask=None, window=0, sinks=None):
     return _orig_extend(q, k, v, scale, group, mask, window + 1 if window > 0 else 0, sinks)
 
@@ -245,6 +268,9 @@ MUTANTS = {
     "sink_carries_a_value": (att, "attention", _sink_carries_a_value),
     "window_one_key_too_wide": (att, "window_mask", _window_one_too_wide),
     "extend_window_one_key_too_wide": (ex, "extend_attention", _extend_window_one_too_wide),
+    "eviction_ignores_masked_slots": (pg.PageModel, "_masked_runs", staticmethod(_runs_ignore_masks)),
+    "fork_drops_masks": (pg.PageModel, "fork", _fork_drops_masks),
+    "deferred_eviction_shifts_spans": (pg.PageModel, "evict", _deferred_shifts_spans),
 }
 
 
