@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 5
+#define SQ_ABI_VERSION 6
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -130,7 +130,7 @@ typedef struct {
   int32_t n_pages;  /* entries in its page list */
   int32_t parent;   /* handle it was forked from, -1 if none */
   int32_t n_spans;  /* registered cursor spans */
-  int32_t reserved;
+  int32_t n_masked; /* slots masked by deferred evictions (still in length) */
 } sq_seq_desc;
 
 typedef struct {
@@ -143,6 +143,7 @@ typedef struct {
   int64_t pages_freed;     /* old pages whose last reference went away */
   int64_t first_evicted;   /* f, the first evicted index (L if none) */
   int64_t pages_remapped;  /* tail pages taken by reference (SQ_STORE_EVICT_REMAP) */
+  int64_t tokens_masked;   /* SQ_EVICT_DEFER: slots this call masked (0 otherwise) */
 } sq_evict_stats;
 
 typedef struct {
@@ -270,6 +271,37 @@ sq_status sq_release(sq_store *store, sq_seq seq);
  * SQ_ERR_INVALID: n < 0 or n > SQ_MAX_EVICT_SPANS. */
 sq_status sq_evict_spans(sq_store *store, sq_seq seq, const int32_t *cursor_ids,
                          int32_t n, void *stream, sq_evict_stats *stats);
+
+/* ---- deferred eviction (a variant of clear_kv) ---------------------------
+ * sq_evict_spans_ex with SQ_EVICT_DEFER masks the spans' slots instead of
+ * removing them: from the call on, decode, step and extend attention skip
+ * those slots (the §3.3 masking of evicted tokens, exactly: attention over
+ * the kept slots equals attention after a physical eviction), while pages,
+ * slot indices, length, positions and the other spans stay as they are, so
+ * the call moves nothing and needs no page.  Its cursors are unregistered.
+ * A fork inherits the masks of its slots.  The masked slots leave the store
+ * at the sequence's next physical eviction, which removes them together
+ * with its own spans, or at sq_compact, which removes only them; remaining
+ * spans then shift left by the slots removed before each end.  Windowed
+ * attention (sq_attn_opts.window > 0) on a sequence with masked slots is
+ * rejected (a window counts kept tokens).  A sequence may hold at most
+ * SQ_MAX_EVICT_SPANS maximal runs of masked slots: a deferred call that
+ * would exceed it fails with SQ_ERR_INVALID and changes nothing.
+ * flags: 0 (= sq_evict_spans) or SQ_EVICT_DEFER; the other arguments,
+ * stats and errors as for sq_evict_spans. */
+#define SQ_EVICT_DEFER 1u
+sq_status sq_evict_spans_ex(sq_store *store, sq_seq seq, const int32_t *cursor_ids, int32_t n,
+                            uint32_t flags, void *stream, sq_evict_stats *stats);
+
+/* Physical eviction of the slots deferred evictions masked on seq (no
+ * cursor); nothing to do when there are none.  Enqueued on stream like
+ * sq_evict_spans, with the same stats (tokens_removed = the masked slots)
+ * and errors (SQ_ERR_NO_PAGES). */
+sq_status sq_compact(sq_store *store, sq_seq seq, void *stream, sq_evict_stats *stats);
+
+/* Host copy of seq's per-slot keep flags (1 attended, 0 masked): up to cap
+ * bytes into out; *n = its length. */
+sq_status sq_keep_flags(sq_store *store, sq_seq seq, uint8_t *out, int64_t cap, int64_t *n);
 
 /* ---- decode attention (the memory-bound decode step of §1 / §3.4) --------
  * One decode step of layer `layer` for `batch` sequences (main threads and

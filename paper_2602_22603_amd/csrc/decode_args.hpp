@@ -33,6 +33,8 @@ struct DecodeStatic {
   const uint16_t *k;   // K pool at this layer
   const uint16_t *v;   // V pool at this layer
   const int32_t *pt;   // page-table mirror base
+  const int32_t *mask; // keep-mask mirror, the page table's shape: bit s of an
+                       // entry = slot s attended (read only when the plan says)
   float *part_m;       // [kMaxItems][kRows]  (log2 domain)
   float *part_l;       // [kMaxItems][kRows]
   float *part_acc;     // [kMaxItems][kRows][D]
@@ -58,7 +60,7 @@ struct DecodeDyn {
   int32_t n_wg;      // workgroups that share them
   int32_t slot_base; // first partial slot of this launch
   int32_t row_pad;   // flattened pages after each row that map to nothing
-  int32_t pad;
+  int32_t masked;    // 1: some segment's sequence has masked slots (read the masks)
   Seg segs[kMaxSegs];
 };
 

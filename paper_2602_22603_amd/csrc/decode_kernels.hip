@@ -139,6 +139,7 @@ struct ArgPlan {
   __device__ int n_wg() const { return d.n_wg; }
   __device__ int slot_base() const { return d.slot_base; }
   __device__ int row_pad() const { return d.row_pad; }
+  __device__ bool masked() const { return d.masked != 0; }
   __device__ int seg_start(int i) const { return d.segs[i].start; }
   __device__ Seg seg(int i) const { return d.segs[i]; }
 };
@@ -149,6 +150,7 @@ struct DevPlan {
   __device__ int n_wg() const { return d->n_wg; }
   __device__ int slot_base() const { return d->slot_base; }
   __device__ int row_pad() const { return d->row_pad; }
+  __device__ bool masked() const { return d->masked != 0; }
   __device__ int seg_start(int i) const { return d->segs[i].start; }
   __device__ Seg seg(int i) const {
     const SQ_CONST Seg &x = d->segs[i];
@@ -229,6 +231,8 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
   const int b = ip.sg.mem & 0xff;
   const int g = ip.g;
   const int32_t *pt = a.pt + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
+  const int32_t *mrow = a.mask + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
+  const bool use_mask = pl.masked();
 
   const int t = lane >> 2, c = lane & 3; // score role
   const int R = lane & 3, dg = lane >> 2; // value role
@@ -270,6 +274,8 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
   for (int pg = ip.pbeg; pg < ip.pend; ++pg) {
     const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
     const int lo = pg == 0 ? ip.sg.tok0 : 0; // tokens before lo: outside a window
+    // slots attended: [lo, valid) less those a deferred eviction masked
+    const int live = (use_mask ? mrow[pg] : 0xffff) & ((1 << valid) - 1) & ~((1 << lo) - 1);
     // stage the page in LDS
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
@@ -317,7 +323,7 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
       float x = s[0];
 #pragma unroll
       for (int r = 1; r < G; ++r) x = (row == r) ? s[r] : x;
-      x = (t >= lo && t < valid) ? x * a.scale_log2 : kNegInf;
+      x = ((live >> t) & 1) ? x * a.scale_log2 : kNegInf;
       float mx = x;
       mx = fmaxf(mx, dpp<kRowRor4>(mx));
       mx = fmaxf(mx, dpp<kRowRor8>(mx));
@@ -484,9 +490,12 @@ __device__ inline void load_v(VFrag<D> &f, __amdgpu_buffer_rsrc_t r, int lane_of
 }
 
 // S^T = K . Q^T for one page, then the online-softmax update of (m, l, acc);
-// returns the page's weights P as bf16 hi and lo parts.
-template <int D>
-__device__ inline void mfma_scores(const KFrag<D> &f, int lo, int valid, int kg, float scale_log2,
+// returns the page's weights P as bf16 hi and lo parts.  Slots [lo, valid)
+// are attended, and with MK only those whose bit is set in mk (the keep mask
+// of deferred evictions).
+template <int D, bool MK>
+__device__ inline void mfma_scores(const KFrag<D> &f, int lo, int valid, int mk, int kg,
+                                   float scale_log2,
                                    const bf16x8_t (&qb)[D / 32], f32x4_t (&acc)[D / 16],
                                    float &m_run, float &l_run, s16x4_t &phi, s16x4_t &plo) {
   constexpr int NS = D / 32;
@@ -498,8 +507,11 @@ __device__ inline void mfma_scores(const KFrag<D> &f, int lo, int valid, int kg,
                                                  0, 0, 0);
   float x[4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    x[i] = (4 * kg + i >= lo && 4 * kg + i < valid) ? st[i] * scale_log2 : kNegInf;
+  for (int i = 0; i < 4; ++i) {
+    bool in = 4 * kg + i >= lo && 4 * kg + i < valid;
+    if constexpr (MK) in = in && ((mk >> (4 * kg + i)) & 1);
+    x[i] = in ? st[i] * scale_log2 : kNegInf;
+  }
   float mx = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
   mx = max_xrow16(mx);
   mx = max_xrow32(mx);
@@ -550,7 +562,9 @@ __device__ inline void mfma_values(VFrag<D> &f, int lo, int valid, int kg, s16x4
   }
 }
 
-template <int D, int G, int kWaves, bool NT, class PL>
+// MK: the plan may carry keep masks (decided at run time by the plan; false
+// compiles the mask path out)
+template <int D, int G, int kWaves, bool NT, bool MK, class PL>
 __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   constexpr int NS = D / 32;
   constexpr int NJ = D / 16;
@@ -618,9 +632,17 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     return j >= count ? 0 : (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
   };
   auto lo_of = [&](int j) -> int { return wbeg + j == 0 ? ip.sg.tok0 : 0; };
+  // keep masks of deferred evictions, scalar loads like the ids (all ones
+  // when the plan has none)
+  const bool use_mask = MK && pl.masked();
+  const sptr_t mids =
+      (sptr_t)(a.mask + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0 + wbeg);
+  auto smask = [&](int j) -> int { return use_mask ? mids[min(j, max(count - 1, 0))] : 0xffff; };
   KFrag<D> k0, k1;
   VFrag<D> v0, v1;
-  int n0 = 0, n1 = 0; // ids of pages j + 2 and j + 3
+  int n0 = 0, n1 = 0;   // ids of pages j + 2 and j + 3
+  int mk0 = 0, mk1 = 0; // masks of pages j and j + 1 (in the fragments)
+  int q0 = 0, q1 = 0;   // masks of pages j + 2 and j + 3
   if (count > 0) {
     const int i0 = sid(0), i1 = sid(1);
     load_k<D, NT>(k0, rsrc(khead, i0, true), koff);
@@ -629,28 +651,36 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     load_v<D, NT>(v1, rsrc(vhead, i1, count > 1), voff);
     n0 = sid(2);
     n1 = sid(3);
+    mk0 = smask(0);
+    mk1 = smask(1);
+    q0 = smask(2);
+    q1 = smask(3);
   }
   for (int j = 0; j < count; j += 2) {
     {
       const int valid = valid_of(j), lo = lo_of(j);
       s16x4_t phi, plo;
-      mfma_scores<D>(k0, lo, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      mfma_scores<D, MK>(k0, lo, valid, mk0, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
       load_k<D, NT>(k0, rsrc(khead, n0, j + 2 < count), koff);
       mfma_values<D>(v0, lo, valid, kg, phi, plo, acc);
       load_v<D, NT>(v0, rsrc(vhead, n0, j + 2 < count), voff);
+      mk0 = q0;
     }
     {
       // page j + 1 may not exist (count odd): its fragments are then zeros
       // and with no valid token the update leaves (m, l, acc) as they are.
       const int valid = valid_of(j + 1), lo = lo_of(j + 1);
       s16x4_t phi, plo;
-      mfma_scores<D>(k1, lo, valid, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      mfma_scores<D, MK>(k1, lo, valid, mk1, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
       load_k<D, NT>(k1, rsrc(khead, n1, j + 3 < count), koff);
       mfma_values<D>(v1, lo, valid, kg, phi, plo, acc);
       load_v<D, NT>(v1, rsrc(vhead, n1, j + 3 < count), voff);
+      mk1 = q1;
     }
     n0 = sid(j + 4);
     n1 = sid(j + 5);
+    q0 = smask(j + 4);
+    q1 = smask(j + 5);
   }
 
   float l_tot = sum_xrow16(l_run);
@@ -713,15 +743,15 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   } // pieces
 }
 
-template <int D, int G, int kWaves, bool NT>
+template <int D, int G, int kWaves, bool NT, bool MK>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
 k_decode_mfma(DecodeArgs a) {
-  mfma_body<D, G, kWaves, NT>(a.st, ArgPlan{a.dyn});
+  mfma_body<D, G, kWaves, NT, MK>(a.st, ArgPlan{a.dyn});
 }
 template <int D, int G, int kWaves>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
 k_step_mfma(DecodeStatic a, const DecodeDyn *dyn) {
-  mfma_body<D, G, kWaves, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
+  mfma_body<D, G, kWaves, true, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
 }
 
 // ===========================================================================
@@ -946,33 +976,35 @@ hipError_t valu_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
                        : valu_dispatch_nt<D, false>(group, a, s);
 }
 
-template <int D, int W, bool NT>
+template <int D, int W, bool NT, bool MK>
 hipError_t mfma_dispatch_w(int group, const DecodeArgs &a, hipStream_t s) {
   const dim3 grid(a.dyn.n_wg), block(64 * W);
   switch (group) {
-  case 1: hipLaunchKernelGGL((k_decode_mfma<D, 1, W, NT>), grid, block, 0, s, a); break;
-  case 2: hipLaunchKernelGGL((k_decode_mfma<D, 2, W, NT>), grid, block, 0, s, a); break;
-  case 4: hipLaunchKernelGGL((k_decode_mfma<D, 4, W, NT>), grid, block, 0, s, a); break;
-  case 8: hipLaunchKernelGGL((k_decode_mfma<D, 8, W, NT>), grid, block, 0, s, a); break;
+  case 1: hipLaunchKernelGGL((k_decode_mfma<D, 1, W, NT, MK>), grid, block, 0, s, a); break;
+  case 2: hipLaunchKernelGGL((k_decode_mfma<D, 2, W, NT, MK>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_decode_mfma<D, 4, W, NT, MK>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_decode_mfma<D, 8, W, NT, MK>), grid, block, 0, s, a); break;
   default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
 }
 
-template <int D, bool NT>
+template <int D, bool NT, bool MK>
 hipError_t mfma_dispatch_nt(int group, int waves, const DecodeArgs &a, hipStream_t s) {
   switch (waves) {
-  case 1: return mfma_dispatch_w<D, 1, NT>(group, a, s);
-  case 2: return mfma_dispatch_w<D, 2, NT>(group, a, s);
-  case 4: return mfma_dispatch_w<D, 4, NT>(group, a, s);
+  case 1: return mfma_dispatch_w<D, 1, NT, MK>(group, a, s);
+  case 2: return mfma_dispatch_w<D, 2, NT, MK>(group, a, s);
+  case 4: return mfma_dispatch_w<D, 4, NT, MK>(group, a, s);
   default: return hipErrorInvalidValue;
   }
 }
 
+// a plan with keep masks takes the masked variant (ordinary loads)
 template <int D>
 hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t s) {
-  return a.st.nontemporal ? mfma_dispatch_nt<D, true>(group, waves, a, s)
-                       : mfma_dispatch_nt<D, false>(group, waves, a, s);
+  if (a.dyn.masked) return mfma_dispatch_nt<D, false, true>(group, waves, a, s);
+  return a.st.nontemporal ? mfma_dispatch_nt<D, true, false>(group, waves, a, s)
+                       : mfma_dispatch_nt<D, false, false>(group, waves, a, s);
 }
 
 } // namespace
@@ -989,10 +1021,10 @@ template <int D> const void *valu_fn(int group) {
 }
 template <int D, int W> const void *mfma_fn_w(int group) {
   switch (group) {
-  case 1: return reinterpret_cast<const void *>(&k_decode_mfma<D, 1, W, true>);
-  case 2: return reinterpret_cast<const void *>(&k_decode_mfma<D, 2, W, true>);
-  case 4: return reinterpret_cast<const void *>(&k_decode_mfma<D, 4, W, true>);
-  case 8: return reinterpret_cast<const void *>(&k_decode_mfma<D, 8, W, true>);
+  case 1: return reinterpret_cast<const void *>(&k_decode_mfma<D, 1, W, true, false>);
+  case 2: return reinterpret_cast<const void *>(&k_decode_mfma<D, 2, W, true, false>);
+  case 4: return reinterpret_cast<const void *>(&k_decode_mfma<D, 4, W, true, false>);
+  case 8: return reinterpret_cast<const void *>(&k_decode_mfma<D, 8, W, true, false>);
   default: return nullptr;
   }
 }

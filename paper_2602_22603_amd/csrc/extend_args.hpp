@@ -44,6 +44,11 @@ struct ExtendArgs {
   const float *sinks;
   int32_t window;
   float sink_scale;
+  // Keep masks of deferred evictions: entry i of the sequence's mask row
+  // holds bit s = slot s of its page i attended; read only when masked.
+  const int32_t *mask_row;
+  int32_t masked;
+  int32_t pad;
 };
 
 static_assert(sizeof(ExtendArgs) < 4096, "extend kernel arguments too large");

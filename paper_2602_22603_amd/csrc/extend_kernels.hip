@@ -193,12 +193,13 @@ constexpr float kLazy = 8.f;
 
 // One 64-key block against this wave's 32 query columns.  need_mask: the
 // block reaches past some column's last visible key (the chunk's diagonal,
-// or the cache's end) or before some column's first one (a window); only
-// then is the per-key test made.
+// or the cache's end) or before some column's first one (a window), or holds
+// slots a deferred eviction masked (lm: bit 4 tt + i = this lane's key
+// tile_key(tt, 4 kg + i) is kept); only then is the per-key test made.
 template <int D>
 __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, int n, int kg,
                                  float c, bool need_mask, const bf16x8_t (&qf)[2][D / 32],
-                                 const int (&first)[2], const int (&lim)[2],
+                                 const int (&first)[2], const int (&lim)[2], uint32_t lm,
                                  f32x4_t (&acc)[D / 16][2], float (&m_run)[2], float (&l_run)[2]) {
   constexpr int NKC = D / 32;
   constexpr int NDT = D / 16;
@@ -227,8 +228,10 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
       for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
         for (int i = 0; i < 4; ++i)
-          if (b * BK + tile_key(tt, 4 * kg + i) > lim[cg] || b * BK + tile_key(tt, 4 * kg + i) < first[cg])
-            st[tt][cg][i] = kNegInf;
+        {
+          const int key = b * BK + tile_key(tt, 4 * kg + i);
+          if (key > lim[cg] || key < first[cg] || !((lm >> (4 * tt + i)) & 1)) st[tt][cg][i] = kNegInf;
+        }
   }
   float alpha[2], nm[2];
 #pragma unroll
@@ -358,6 +361,27 @@ k_extend(ExtendArgs a) {
     block_ids(ids, a, b_lo + 1);
   }
   for (int b = b_lo; b < b_hi; ++b) {
+    // keep bits of this lane's 16 keys of the block (deferred evictions)
+    uint32_t lm = 0xffffu;
+    bool masked_here = false;
+    if (a.masked) {
+      int32_t mk[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        mk[i] = __builtin_amdgcn_readfirstlane(a.mask_row[min(b * (BK / kPage) + i, a.n_pages - 1)]);
+        masked_here = masked_here || mk[i] != 0xffff;
+      }
+      if (masked_here) {
+        lm = 0;
+#pragma unroll
+        for (int tt = 0; tt < 4; ++tt)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int kk = tile_key(tt, 4 * kg + i);
+            lm |= (uint32_t)((pick4(mk, kk >> 4) >> (kk & 15)) & 1) << (4 * tt + i);
+          }
+      }
+    }
     // block b has landed (every wave's copies) and every wave is done with
     // block b - 1, whose buffer the next copy overwrites
     __builtin_amdgcn_s_waitcnt(0);
@@ -371,8 +395,8 @@ k_extend(ExtendArgs a) {
       block_ids(ids, a, b + 2);
     }
     ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2,
-                 b * BK + BK - 1 > mask_from || b * BK < mask_below, qf, first, lim, acc, m_run,
-                 l_run);
+                 b * BK + BK - 1 > mask_from || b * BK < mask_below || masked_here, qf, first, lim,
+                 lm, acc, m_run, l_run);
   }
 
   if (a.n_split > 1) {

@@ -97,6 +97,8 @@ hipError_t launch_set_entries(const SetEntries &a, hipStream_t s);
 hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t tail_index,
                            int32_t tail_value, hipStream_t s);
 hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s);
+// dst[i] = value for i < n.
+hipError_t launch_fill_i32(int32_t *dst, int32_t value, int32_t n, hipStream_t s);
 hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s);
 hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStream_t s);
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);

@@ -130,6 +130,11 @@ __global__ __launch_bounds__(256) void k_copy_i32(int32_t *dst, const int32_t *s
   if (i == n && tail_value >= 0) dst[n] = tail_value;
 }
 
+__global__ __launch_bounds__(256) void k_fill_i32(int32_t *dst, int32_t value, int32_t n) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) dst[i] = value;
+}
+
 // Whole-page copy (every layer and head, K, V and pos): the fork's tail page.
 template <int D>
 __global__ __launch_bounds__(256) void k_copy_page(Pools p, int32_t src_page, int32_t dst_page) {
@@ -292,6 +297,12 @@ hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const v
     hipLaunchKernelGGL(k_append_batch<128>, grid, dim3(64), 0, s, p, a, kn, vn);
   else
     hipLaunchKernelGGL(k_append_batch<64>, grid, dim3(64), 0, s, p, a, kn, vn);
+  return hipGetLastError();
+}
+
+hipError_t launch_fill_i32(int32_t *dst, int32_t value, int32_t n, hipStream_t s) {
+  if (n <= 0) return hipSuccess;
+  hipLaunchKernelGGL(k_fill_i32, dim3((n + 255) / 256), dim3(256), 0, s, dst, value, n);
   return hipGetLastError();
 }
 

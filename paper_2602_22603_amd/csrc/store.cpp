@@ -50,7 +50,7 @@ constexpr uint64_t kAlign = 256;
 uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  uint64_t pt, keep, dst, src, upload, part_m, part_l, part_acc, step, total;
+  uint64_t pt, mask, keep, dst, src, upload, part_m, part_l, part_acc, step, total;
   uint64_t upload_elems;
 };
 
@@ -64,10 +64,13 @@ Layout layout_of(const sq_store_config &c) {
     return o;
   };
   L.pt = take((uint64_t)c.max_seqs * c.max_pages_per_seq * 4);
+  L.mask = take((uint64_t)c.max_seqs * c.max_pages_per_seq * 4);
   L.keep = take(max_tok);
   L.dst = take(max_tok * 4);
   L.src = take(max_tok * 4);
-  L.upload_elems = 3ull * SQ_MAX_EVICT_SPANS + (uint64_t)c.max_pages_per_seq;
+  // spans of an eviction: its own and the masked runs, at most
+  // SQ_MAX_EVICT_SPANS each; then the fresh ids (or a keep-mask row)
+  L.upload_elems = 6ull * SQ_MAX_EVICT_SPANS + (uint64_t)c.max_pages_per_seq;
   L.upload = take(L.upload_elems * 4);
   L.part_m = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
   L.part_l = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
@@ -116,7 +119,38 @@ struct Seq {
   std::map<int32_t, std::pair<int64_t, int64_t>> spans; // cursor -> [start, end)
   std::map<int64_t, int64_t> nonempty;                  // start -> end of non-empty spans
   int32_t parent = -1;
+  // Keep masks of deferred evictions, one 16-bit word per page (bit s = slot
+  // s attended); empty while no slot is masked.
+  std::vector<uint16_t> kmask;
+  int64_t n_masked = 0;
 };
+
+bool slot_kept(const Seq &q, int64_t i, int P) {
+  return q.kmask.empty() || ((q.kmask[i / P] >> (i % P)) & 1);
+}
+
+// Maximal runs [s, e) of masked slots, in order.
+std::vector<std::pair<int64_t, int64_t>> masked_runs(const Seq &q, int P) {
+  std::vector<std::pair<int64_t, int64_t>> runs;
+  if (q.kmask.empty()) return runs;
+  int64_t i = 0;
+  while (i < q.length) {
+    if (slot_kept(q, i, P)) {
+      ++i;
+      continue;
+    }
+    int64_t j = i;
+    while (j < q.length && !slot_kept(q, j, P)) ++j;
+    runs.push_back({i, j});
+    i = j;
+  }
+  return runs;
+}
+
+// New pages of a masked sequence start with every slot kept.
+void grow_kmask(Seq &q) {
+  if (!q.kmask.empty()) q.kmask.resize(q.pages.size(), 0xffff);
+}
 
 enum ProfKind { kProfValu, kProfMfma, kProfMerge, kProfScan, kProfGather, kProfAppend, kProfExtend,
                 kProfKinds };
@@ -193,6 +227,12 @@ struct sq_store {
   sq::Pools pools{};
   Layout lay{};
   int32_t *pt_dev = nullptr;
+  // keep-mask mirror, the page table's shape.  A masked sequence's row is
+  // uploaded whole; other rows are read only by plans that include a masked
+  // sequence, which first set them to all-kept if mask_dirty says they may
+  // hold old masks (of a released or compacted sequence, or never written).
+  int32_t *mask_dev = nullptr;
+  std::vector<char> mask_dirty;
   uint8_t *ev_keep = nullptr;
   int32_t *ev_dst = nullptr, *ev_src = nullptr, *ev_upload = nullptr;
   float *part_m = nullptr, *part_l = nullptr, *part_acc = nullptr;
@@ -295,6 +335,7 @@ struct sq_store {
   }
 
   int32_t *pt_row(sq_seq h) { return pt_dev + (int64_t)h * cfg.max_pages_per_seq; }
+  int32_t *mask_row(sq_seq h) { return mask_dev + (int64_t)h * cfg.max_pages_per_seq; }
 
   // ---- profiling ----
   hipEvent_t take_event() {
@@ -351,6 +392,28 @@ sq_status upload(sq_store *s, int32_t *dev_dst, const int32_t *src, size_t n, hi
   return SQ_OK;
 }
 
+// The whole keep-mask row of sequence h (all-kept past its pages).
+sq_status upload_mask_row(sq_store *s, sq_seq h, hipStream_t strm) {
+  const Seq &q = s->seqs[h];
+  std::vector<int32_t> row(s->cfg.max_pages_per_seq, 0xffff);
+  for (size_t i = 0; i < q.kmask.size(); ++i) row[i] = q.kmask[i];
+  s->mask_dirty[h] = 1;
+  return upload(s, s->mask_row(h), row.data(), row.size(), strm);
+}
+
+// Before a plan that reads keep masks: rows of unmasked sequences in it
+// that may hold old masks become all-kept.
+sq_status clean_mask_rows(sq_store *s, const sq_seq *seqs, int32_t batch, hipStream_t strm) {
+  for (int b = 0; b < batch; ++b) {
+    const sq_seq h = seqs[b];
+    if (s->seqs[h].n_masked > 0 || !s->mask_dirty[h]) continue;
+    hipError_t e = sq::launch_fill_i32(s->mask_row(h), 0xffff, s->cfg.max_pages_per_seq, strm);
+    if (e != hipSuccess) return hip_fail(e, "keep-mask row");
+    s->mask_dirty[h] = 0;
+  }
+  return SQ_OK;
+}
+
 // ---------------------------------------------------------------------------
 // Decode planning.
 struct PlanSeg {
@@ -367,9 +430,20 @@ struct Plan {
   int32_t slot_base[2] = {0, 0};
   int32_t seg_index[sq::kMaxSegs]; // index of each segment inside its launch
   bool pages_reread = false; // some page is read by more than one segment
+  bool masked = false;       // some entry has slots masked by deferred evictions
   int64_t kv_bytes = 0, kv_bytes_logical = 0, io_bytes = 0;
   int64_t kv_bytes_valu = 0, kv_bytes_mfma = 0;
 };
+
+// Index of the first i < n with a[i] != b[i] (n if none): memcmp over blocks,
+// then the block that differs element by element.
+template <class T> int64_t first_diff(const T *a, const T *b, int64_t n) {
+  constexpr int64_t B = 256;
+  int64_t i = 0;
+  while (i + B <= n && std::memcmp(a + i, b + i, B * sizeof(T)) == 0) i += B;
+  while (i < n && a[i] == b[i]) ++i;
+  return i;
+}
 
 // keep_last >= 0: each entry attends only to its last keep_last cached
 // tokens (a window), read on its own; < 0: every token.
@@ -396,8 +470,23 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     ps.mfma = mfma;
     plan->segs.push_back(ps);
   };
-  auto full_pages = [&](int b) { return s->seqs[seqs[b]].length / s->P; };
-  auto page_at = [&](int b, int64_t i) { return s->seqs[seqs[b]].pages[i]; };
+  // per entry: page list, keep masks (null: none) and full pages
+  const int32_t *pages_of[sq::kMaxBatch];
+  const uint16_t *kmask_of[sq::kMaxBatch];
+  int64_t full_of[sq::kMaxBatch];
+  for (int b = 0; b < batch; ++b) {
+    const Seq &q = s->seqs[seqs[b]];
+    pages_of[b] = q.pages.data();
+    kmask_of[b] = q.kmask.empty() ? nullptr : q.kmask.data();
+    full_of[b] = q.length / s->P;
+    plan->masked = plan->masked || q.n_masked > 0;
+  }
+  auto full_pages = [&](int b) { return full_of[b]; };
+  auto page_at = [&](int b, int64_t i) { return pages_of[b][i]; };
+  // entries share a page only when they also mask the same slots of it
+  auto key_at = [&](int b, int64_t i) -> int64_t {
+    return (int64_t)pages_of[b][i] | (int64_t)(kmask_of[b] ? kmask_of[b][i] : 0xffff) << 32;
+  };
   auto add_private = [&](int b, int64_t p0) {
     const int64_t rest = s->seqs[seqs[b]].length - p0 * s->P;
     if (rest > 0) add_seg(seqs[b], (int32_t)p0, rest, single_mfma, {b});
@@ -413,9 +502,9 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   // suffix at the leaf.
   std::function<void(const std::vector<int> &, int64_t, int)> node =
       [&](const std::vector<int> &mem, int64_t p0, int depth) {
-        std::vector<std::pair<int32_t, std::vector<int>>> parts; // first-seen order
+        std::vector<std::pair<int64_t, std::vector<int>>> parts; // first-seen order
         for (int b : mem) {
-          const int32_t key = full_pages(b) > p0 ? page_at(b, p0) : -1;
+          const int64_t key = full_pages(b) > p0 ? key_at(b, p0) : -1;
           auto it = std::find_if(parts.begin(), parts.end(),
                                  [&](const auto &pt) { return key >= 0 && pt.first == key; });
           if (it == parts.end()) parts.push_back({key, {b}});
@@ -436,12 +525,22 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
               add_private(tile[0], p0);
               continue;
             }
-            int64_t p1 = p0 + 1; // they share page p0
-            for (;;) {
-              bool same = true;
-              for (int b : tile) same = same && full_pages(b) > p1 && page_at(b, p1) == page_at(tile[0], p1);
-              if (!same) break;
-              ++p1;
+            // they share page p0, and every later full page both the page
+            // ids and the keep masks of the tile agree on
+            int64_t p1 = full_pages(tile[0]);
+            for (int b : tile) p1 = std::min(p1, full_pages(b));
+            for (size_t m = 1; m < tile.size(); ++m) {
+              const int b = tile[m], b0 = tile[0];
+              const int64_t n = p1 - p0 - 1;
+              int64_t d = first_diff(pages_of[b] + p0 + 1, pages_of[b0] + p0 + 1, n);
+              if (kmask_of[b] || kmask_of[b0]) {
+                for (int64_t i = 0; i < d; ++i)
+                  if (key_at(b, p0 + 1 + i) != key_at(b0, p0 + 1 + i)) {
+                    d = i;
+                    break;
+                  }
+              }
+              p1 = p0 + 1 + d;
             }
             ++plan->n_groups;
             add_seg(seqs[tile[0]], (int32_t)p0, (p1 - p0) * s->P, true, tile);
@@ -523,6 +622,7 @@ sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float 
   st.k = s->pools.k + layer * s->pools.layer_stride;
   st.v = s->pools.v + layer * s->pools.layer_stride;
   st.pt = s->pt_dev;
+  st.mask = s->mask_dev;
   st.part_m = s->part_m;
   st.part_l = s->part_l;
   st.part_acc = s->part_acc;
@@ -559,6 +659,7 @@ void fill_dyn(sq_store *s, const Plan &plan, sq::DecodeDyn dyn[2], sq::MergeDyn 
       if (ps.mfma == (L == 1)) d.segs[d.n_segs++] = ps.seg;
     d.total = (int32_t)plan.total[L];
     d.row_pad = s->row_pad[L];
+    d.masked = plan.masked ? 1 : 0;
     d.n_wg = plan.n_wg[L];
     d.slot_base = plan.slot_base[L];
     md->total[L] = d.total;
@@ -648,6 +749,8 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     s->lay = lay;
     char *ws = static_cast<char *>(cfg->workspace);
     s->pt_dev = reinterpret_cast<int32_t *>(ws + lay.pt);
+    s->mask_dev = reinterpret_cast<int32_t *>(ws + lay.mask);
+    s->mask_dirty.assign(cfg->max_seqs, 1);
     s->ev_keep = reinterpret_cast<uint8_t *>(ws + lay.keep);
     s->ev_dst = reinterpret_cast<int32_t *>(ws + lay.dst);
     s->ev_src = reinterpret_cast<int32_t *>(ws + lay.src);
@@ -767,6 +870,7 @@ sq_status sq_append(sq_store *s, sq_seq h, int32_t n, const void *k_new, const v
   const int64_t old_len = q->length;
   const int32_t old_np = (int32_t)q->pages.size();
   while ((int64_t)q->pages.size() < want) q->pages.push_back(s->alloc_page());
+  grow_kmask(*q);
   runs_append(*q, n);
   const int64_t pos0 = q->next_pos;
   q->length = new_len;
@@ -855,6 +959,7 @@ void take_one_token_each(sq_store *s, const sq_seq *seqs, int32_t batch, TokenSl
     t->pt_index[b] = -1;
     if (q.length % s->P == 0) {
       q.pages.push_back(s->alloc_page());
+      grow_kmask(q);
       t->pt_index[b] = seqs[b] * s->cfg.max_pages_per_seq + (int32_t)q.pages.size() - 1;
     }
     t->page[b] = q.pages[q.length / s->P];
@@ -960,6 +1065,12 @@ sq_status sq_fork(sq_store *s, sq_seq parent, int64_t fork_len, sq_seq *child, v
       if (kv.second.second > kv.second.first) c.nonempty[kv.second.first] = kv.second.second;
     }
   c.parent = parent;
+  if (par->n_masked > 0) { // the child's slots keep their masks
+    c.kmask.assign(par->kmask.begin(), par->kmask.begin() + full);
+    if (tail) c.kmask.push_back((uint16_t)(par->kmask[full] | (0xffffu << tail)));
+    for (int64_t i = 0; i < fork_len; ++i) c.n_masked += !slot_kept(c, i, s->P);
+    if (c.n_masked == 0) c.kmask.clear();
+  }
   const int32_t src_tail_page = tail ? par->pages[full] : -1;
   s->seqs[h] = std::move(c);
   ++s->st.live_seqs;
@@ -977,6 +1088,10 @@ sq_status sq_fork(sq_store *s, sq_seq parent, int64_t fork_len, sq_seq *child, v
     e = sq::launch_copy_page(s->pools, src_tail_page, tail_page, strm);
     if (e != hipSuccess) return hip_fail(e, "fork tail copy");
   }
+  if (s->seqs[h].n_masked > 0) {
+    sq_status r = upload_mask_row(s, h, strm);
+    if (r != SQ_OK) return r;
+  }
   return SQ_OK;
 }
 
@@ -993,6 +1108,58 @@ sq_status sq_release(sq_store *s, sq_seq h) {
 
 sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32_t n,
                          void *stream, sq_evict_stats *stats) {
+  return sq_evict_spans_ex(s, h, cursor_ids, n, 0, stream, stats);
+}
+
+sq_status sq_compact(sq_store *s, sq_seq h, void *stream, sq_evict_stats *stats) {
+  return sq_evict_spans_ex(s, h, nullptr, 0, 0, stream, stats);
+}
+
+namespace {
+// Deferred eviction: the spans' slots are masked, nothing moves.
+sq_status evict_deferred(sq_store *s, sq_seq h, const std::vector<int32_t> &ids,
+                         const std::vector<std::pair<int64_t, int64_t>> &sp, void *stream,
+                         sq_evict_stats *stats) {
+  Seq *q = s->get(h);
+  std::vector<uint16_t> km = q->kmask;
+  if (km.empty()) km.assign(q->pages.size(), 0xffff);
+  int64_t newly = 0;
+  for (const auto &se : sp)
+    for (int64_t i = se.first; i < se.second; ++i) {
+      uint16_t &w = km[i / s->P];
+      const uint16_t bit = (uint16_t)(1u << (i % s->P));
+      newly += (w & bit) != 0;
+      w &= (uint16_t)~bit;
+    }
+  Seq probe;
+  probe.length = q->length;
+  probe.kmask = km;
+  const auto runs = masked_runs(probe, s->P);
+  if ((int64_t)runs.size() > SQ_MAX_EVICT_SPANS)
+    return fail(SQ_ERR_INVALID, "sequence %d would hold %zu masked runs (max %d): compact it first",
+                h, runs.size(), SQ_MAX_EVICT_SPANS);
+  sq_evict_stats es{};
+  es.first_evicted = runs.empty() ? q->length : runs[0].first;
+  es.tokens_masked = newly;
+  q->kmask = std::move(km);
+  q->n_masked += newly;
+  if (q->n_masked == 0) q->kmask.clear();
+  for (int32_t c : ids) {
+    auto it = q->spans.find(c);
+    if (it->second.second > it->second.first) q->nonempty.erase(it->second.first);
+    q->spans.erase(it);
+  }
+  ++s->st.evict_calls;
+  if (stats) *stats = es;
+  if (!s->device || newly == 0) return SQ_OK;
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  return upload_mask_row(s, h, strm);
+}
+} // namespace
+
+sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32_t n,
+                            uint32_t flags, void *stream, sq_evict_stats *stats) {
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
@@ -1005,12 +1172,25 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
   ids.erase(std::unique(ids.begin(), ids.end()), ids.end());
   for (int32_t c : ids)
     if (!q->spans.count(c)) return fail(SQ_ERR_UNKNOWN_CURSOR, "cursor %d not registered on sequence %d", c, h);
+  if (flags & ~SQ_EVICT_DEFER) return fail(SQ_ERR_INVALID, "unknown eviction flags 0x%x", flags);
   std::vector<std::pair<int64_t, int64_t>> sp;
   for (int32_t c : ids) {
     auto se = q->spans[c];
     if (se.second > se.first) sp.push_back(se);
   }
   std::sort(sp.begin(), sp.end());
+  if (flags & SQ_EVICT_DEFER) return evict_deferred(s, h, ids, sp, stream, stats);
+  if (q->n_masked > 0) {
+    // masked slots leave with the spans: the union, as maximal runs
+    std::vector<std::pair<int64_t, int64_t>> all = masked_runs(*q, s->P);
+    all.insert(all.end(), sp.begin(), sp.end());
+    std::sort(all.begin(), all.end());
+    sp.clear();
+    for (const auto &se : all) {
+      if (!sp.empty() && se.first <= sp.back().second) sp.back().second = std::max(sp.back().second, se.second);
+      else sp.push_back(se);
+    }
+  }
   sq_evict_stats es{};
   es.first_evicted = q->length;
   const int64_t L = q->length;
@@ -1242,6 +1422,8 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
     se = {ns, ne};
     if (ne > ns) q->nonempty[ns] = ne;
   }
+  q->kmask.clear(); // the masked slots are gone (their device row stays dirty)
+  q->n_masked = 0;
   const int64_t moved = Lp - fp * s->P - n_alias * s->P;
   const int64_t per_tok = (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2 + 4;
   es.tokens_removed = removed;
@@ -1308,9 +1490,15 @@ sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int3
   Plan plan;
   r = build_plan(s, seqs, batch, mode, &plan, o.window > 0 ? o.window : -1);
   if (r != SQ_OK) return r;
+  if (plan.masked && o.window > 0)
+    return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
 
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
+  if (plan.masked) {
+    r = clean_mask_rows(s, seqs, batch, strm);
+    if (r != SQ_OK) return r;
+  }
   sq::DecodeArgs da[2]{};
   sq::MergeArgs ma{};
   da[0].st = decode_static(s, layer, q, scale, !plan.pages_reread);
@@ -1358,6 +1546,8 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   r = build_plan(s, seqs, batch, mode, &plan);
   if (r != SQ_OK) return r;
   if (window > 0) {
+    if (plan.masked)
+      return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
     r = build_plan(s, seqs, batch, mode, &plan_w, window - 1);
     if (r != SQ_OK) return r;
   }
@@ -1409,6 +1599,10 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   if (!s->device) return SQ_OK;
   hipStream_t strm = static_cast<hipStream_t>(stream);
   s->last_stream = strm;
+  if (plan.masked) {
+    r = clean_mask_rows(s, seqs, batch, strm);
+    if (r != SQ_OK) return r;
+  }
   // pages the step opens enter the page-table mirror now, whatever happens
   // to the step's layers
   sq::SetEntries se{};
@@ -1536,6 +1730,10 @@ sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_ne
   a.sinks = o.sinks;
   a.window = o.window;
   a.sink_scale = 1.4426950408889634f;
+  a.mask_row = s->mask_row(seq);
+  a.masked = sqn->n_masked > 0 ? 1 : 0;
+  if (a.masked && o.window > 0)
+    return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
   // A chunk too short to give every CU two rounds of workgroups splits the
   // key range of each query block (at least 4 blocks of 64 keys per split)
   // and merges the partial rows in a second launch.
@@ -1581,6 +1779,17 @@ sq_status sq_seq_info(sq_store *s, sq_seq h, sq_seq_desc *out) {
   out->n_pages = (int32_t)q->pages.size();
   out->parent = q->parent;
   out->n_spans = (int32_t)q->spans.size();
+  out->n_masked = (int32_t)q->n_masked;
+  return SQ_OK;
+}
+
+sq_status sq_keep_flags(sq_store *s, sq_seq h, uint8_t *out, int64_t cap, int64_t *n) {
+  if (!s || !n) return fail(SQ_ERR_INVALID, "null argument");
+  Seq *q = s->get(h);
+  if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
+  if (cap > 0 && !out) return fail(SQ_ERR_INVALID, "null output with cap > 0");
+  *n = q->length;
+  for (int64_t i = 0; i < std::min(cap, q->length); ++i) out[i] = slot_kept(*q, i, s->P) ? 1 : 0;
   return SQ_OK;
 }
 

@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsq.so")
 OK, ERR_INVALID, ERR_NO_PAGES, ERR_UNKNOWN_SEQ, ERR_UNKNOWN_CURSOR, ERR_SPAN, ERR_HIP = range(7)
 STORE_METADATA_ONLY = 1
 STORE_EVICT_REMAP = 2
+EVICT_DEFER = 1
 ATTN_AUTO, ATTN_STREAM, ATTN_SHARED_PREFIX, ATTN_MFMA = 0, 1, 2, 3
 MAX_BATCH = 64
 MAX_EVICT_SPANS = 16384
@@ -48,13 +49,13 @@ class StoreConfig(C.Structure):
 
 class SeqDesc(C.Structure):
     _fields_ = [("length", C.c_int64), ("next_pos", C.c_int64), ("n_pages", C.c_int32),
-                ("parent", C.c_int32), ("n_spans", C.c_int32), ("reserved", C.c_int32)]
+                ("parent", C.c_int32), ("n_spans", C.c_int32), ("n_masked", C.c_int32)]
 
 
 class EvictStats(C.Structure):
     _fields_ = [(n, C.c_int64) for n in ("tokens_removed", "tokens_moved", "bytes_moved",
                                          "pages_allocated", "pages_freed", "first_evicted",
-                                         "pages_remapped")]
+                                         "pages_remapped", "tokens_masked")]
 
 
 class Stats(C.Structure):
@@ -114,6 +115,11 @@ _SIGS = {
                                C.c_void_p, C.c_float, C.c_void_p]),
     "sq_extend_attn": (C.c_int, [C.c_void_p, C.c_int32, C.c_int32, C.c_int32, C.c_void_p,
                                  C.c_void_p, C.c_float, C.c_void_p]),
+    "sq_evict_spans_ex": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
+                                    C.c_uint32, C.c_void_p, C.POINTER(EvictStats)]),
+    "sq_compact": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.POINTER(EvictStats)]),
+    "sq_keep_flags": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_uint8), C.c_int64,
+                                C.POINTER(C.c_int64)]),
     "sq_decode_attn_ex": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
                                     C.c_void_p, C.c_void_p, C.c_float, C.c_int32,
                                     C.POINTER(AttnOpts), C.c_void_p]),
@@ -326,13 +332,34 @@ class Store:
     def release(self, seq):
         _check(lib().sq_release(self._handle, seq))
 
-    def evict(self, seq, cursor_ids, stream=None):
+    def evict(self, seq, cursor_ids, stream=None, deferred=False):
+        """Evict the cursors' spans (deferred: mask their slots, move nothing)."""
         es = EvictStats()
         st = C.c_void_p(0) if self.metadata_only else _stream(stream)
         ids = list(cursor_ids)
-        _check(lib().sq_evict_spans(self._handle, seq, _i32_array(ids), len(ids), st,
-                                    C.byref(es)))
+        if deferred:
+            _check(lib().sq_evict_spans_ex(self._handle, seq, _i32_array(ids), len(ids),
+                                           EVICT_DEFER, st, C.byref(es)))
+        else:
+            _check(lib().sq_evict_spans(self._handle, seq, _i32_array(ids), len(ids), st,
+                                        C.byref(es)))
         return {n: getattr(es, n) for n, _ in EvictStats._fields_}
+
+    def compact(self, seq, stream=None):
+        """Remove the slots deferred evictions masked."""
+        es = EvictStats()
+        st = C.c_void_p(0) if self.metadata_only else _stream(stream)
+        _check(lib().sq_compact(self._handle, seq, st, C.byref(es)))
+        return {n: getattr(es, n) for n, _ in EvictStats._fields_}
+
+    def keep_flags(self, seq):
+        """Per slot: 1 attended, 0 masked by a deferred eviction."""
+        n = C.c_int64()
+        _check(lib().sq_keep_flags(self._handle, seq, None, 0, C.byref(n)))
+        buf = np.zeros(max(1, n.value), dtype=np.uint8)
+        _check(lib().sq_keep_flags(self._handle, seq, buf.ctypes.data_as(C.POINTER(C.c_uint8)),
+                                   n.value, C.byref(n)))
+        return buf[: n.value]
 
     def decode(self, layer, seqs, q, out=None, scale=None, mode=ATTN_AUTO, stream=None,
                window=0, sinks=None):
@@ -429,7 +456,7 @@ class Store:
     def seq_info(self, seq):
         d = SeqDesc()
         _check(lib().sq_seq_info(self._handle, seq, C.byref(d)))
-        return {n: getattr(d, n) for n, _ in SeqDesc._fields_ if n != "reserved"}
+        return {n: getattr(d, n) for n, _ in SeqDesc._fields_}
 
     def page_table(self, seq):
         n = C.c_int32()

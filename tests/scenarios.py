@@ -190,9 +190,16 @@ class Twin:
         self.store.span_mark(h, cursor, s, e)
         return True
 
-    def evict(self, h, ids):
-        got = self.store.evict(h, ids)
-        want = self.model.evict(h, ids)
+    def evict(self, h, ids, deferred=False):
+        got = self.store.evict(h, ids, deferred=deferred)
+        want = self.model.evict(h, ids, deferred=deferred)
+        for k in want:
+            assert got[k] == want[k], (k, got, want)
+        return got
+
+    def compact(self, h):
+        got = self.store.compact(h)
+        want = self.model.compact(h)
         for k in want:
             assert got[k] == want[k], (k, got, want)
         return got
@@ -205,8 +212,9 @@ class Twin:
         assert self.store.refcounts().tolist() == self.model.refcount.tolist()
         for h in self.model.seqs:
             assert self.store.page_table(h) == self.model.page_table(h), h
+            assert self.store.keep_flags(h).tolist() == self.model.keep_flags(h).tolist()
             gk, gv, gp = seq_view(self.store, h)
-            ok, ov, op = self.model.view(h)
+            ok, ov, op = self.model.slot_view(h)
             assert np.array_equal(gp, op), f"positions of {h}"
             assert np.array_equal(gk, ok), f"K of {h}"
             assert np.array_equal(gv, ov), f"V of {h}"

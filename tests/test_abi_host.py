@@ -61,9 +61,10 @@ def _compare(store, model):
         assert store.page_table(h) == model.page_table(h)
         info = store.seq_info(h)
         want = model.info(h)
-        for k in ("length", "next_pos", "n_pages", "parent", "n_spans"):
+        for k in ("length", "next_pos", "n_pages", "parent", "n_spans", "n_masked"):
             assert info[k] == want[k], (k, info[k], want[k])
-        assert store.positions(h).tolist() == model.view(h)[2].tolist()
+        assert store.positions(h).tolist() == model.slot_view(h)[2].tolist()
+        assert store.keep_flags(h).tolist() == model.keep_flags(h).tolist()
         assert store.spans(h) == model.spans(h)
 
 
@@ -84,10 +85,11 @@ def _both(store, model, sq, fn_store, fn_model):
 
 
 @pytest.mark.parametrize("page", [1, 2, 4, 16])
-@pytest.mark.parametrize("seed,chunk,remap", [(0, 0, False), (1, 0, False), (2, 1, False),
-                                              (3, 2, False), (4, 5, False), (5, 0, True),
-                                              (6, 2, True)])
-def test_random_ops_match_oracle(sq, page, seed, chunk, remap):
+@pytest.mark.parametrize("seed,chunk,remap,deferred",
+                         [(0, 0, False, False), (1, 0, False, False), (2, 1, False, False),
+                          (3, 2, False, False), (4, 5, False, False), (5, 0, True, False),
+                          (6, 2, True, False), (7, 0, False, True), (8, 2, True, True)])
+def test_random_ops_match_oracle(sq, page, seed, chunk, remap, deferred):
     rng = np.random.default_rng(100 + seed * 7 + page)
     num_pages, max_seqs, max_pages = 300 // page + 40, 5, 400 // page + 8
     store = _store(sq, num_pages, page, max_seqs, max_pages, chunk, remap)
@@ -98,8 +100,10 @@ def test_random_ops_match_oracle(sq, page, seed, chunk, remap):
     for _ in range(250):
         live = sorted(model.seqs)
         h = int(rng.choice(live)) if live else 0
-        op = rng.choice(["append", "append", "mark", "mark", "fork", "evict", "release",
-                         "bad", "step"])
+        ops = ["append", "append", "mark", "mark", "fork", "evict", "release", "bad", "step"]
+        if deferred:
+            ops += ["defer", "defer", "compact"]
+        op = rng.choice(ops)
         if op == "step":
             # a decode step opens one slot per sequence, all or nothing
             batch = [int(x) for x in rng.permutation(live)[:int(rng.integers(1, len(live) + 1))]]
@@ -140,6 +144,19 @@ def test_random_ops_match_oracle(sq, page, seed, chunk, remap):
             pick += pick[:1]                   # a duplicate
             got, want = _both(store, model, sq, lambda: store.evict(h, pick),
                               lambda: model.evict(h, pick))
+            if want is not None:
+                for k in want:
+                    assert got[k] == want[k], (k, got, want)
+        elif op == "defer":
+            cur = list(model.spans(h))
+            pick = [c for c in cur if rng.random() < 0.5] + cur[:1]
+            got, want = _both(store, model, sq, lambda: store.evict(h, pick, deferred=True),
+                              lambda: model.evict(h, pick, deferred=True))
+            if want is not None:
+                for k in want:
+                    assert got[k] == want[k], (k, got, want)
+        elif op == "compact":
+            got, want = _both(store, model, sq, lambda: store.compact(h), lambda: model.compact(h))
             if want is not None:
                 for k in want:
                     assert got[k] == want[k], (k, got, want)
