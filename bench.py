@@ -326,6 +326,54 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False)
     return info
 
 
+def deferred_leg(sq, torch, wl, reps=8):
+    """The 64K compaction's spans evicted deferred: the call's wall time
+    (masks only, nothing moves), decode over the masked cache (every slot is
+    still read, masked ones are skipped), then the compaction's wall time and
+    decode over the compacted cache (batch 1)."""
+    from paper_2602_22603_amd import drivers
+    store, base, w, k, v = drivers.build_compaction64k()
+    del k, v
+    L = w.length
+    q = wl.device_normal_bf16((1, 32, 128), 78, "cuda")
+    out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
+    defer_walls, compact_walls, dec = [], [], {}
+    for r in range(reps + 2):
+        f = store.fork(base, L)
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        st = store.evict(f, w.evict_ids, deferred=True)
+        torch.cuda.synchronize()
+        t1 = time.perf_counter()
+        if r == reps + 1:
+            step = lambda: store.decode(0, [f], q, out=out)
+            for _ in range(3):
+                step()
+            dec["masked"] = time_events(torch, step, 32)
+        torch.cuda.synchronize()
+        t2 = time.perf_counter()
+        cst = store.compact(f)
+        torch.cuda.synchronize()
+        t3 = time.perf_counter()
+        if r >= 2:
+            defer_walls.append(t1 - t0)
+            compact_walls.append(t3 - t2)
+        if r == reps + 1:
+            step = lambda: store.decode(0, [f], q, out=out)
+            for _ in range(3):
+                step()
+            dec["compacted"] = time_events(torch, step, 32)
+        store.release(f)
+    med = lambda xs: sorted(xs)[len(xs) // 2] * 1e3
+    store.close()
+    return dict(workload=f"64K tokens, the same 40 tool spans as the eviction leg, deferred "
+                         f"(masked {st['tokens_masked']} of {L}), then compacted",
+                tokens_masked=st["tokens_masked"], tokens_removed_by_compact=cst["tokens_removed"],
+                defer_wall_ms_median=round(med(defer_walls), 4),
+                compact_wall_ms_median=round(med(compact_walls), 4),
+                decode_ms_masked=dec["masked"], decode_ms_compacted=dec["compacted"])
+
+
 def outlier_leg(sq, torch, wl):
     """32K context with outlier channels: eviction of >= 50% of the tokens
     while the auxiliary thread is alive, then 64 decode steps of [main, aux]
@@ -690,6 +738,7 @@ def main():
         evict["page_aligned_spans_copy"] = evict_leg(sq, torch, wl, decode=False, align=16)
         evict["page_aligned_spans_remap"] = evict_leg(sq, torch, wl, decode=False, align=16,
                                                       remap=True)
+        evict["deferred"] = deferred_leg(sq, torch, wl)
     if "copy" in legs:
         log("calibration copy: 1 GiB device-to-device ...")
         src = torch.empty(1 << 30, dtype=torch.uint8, device="cuda").fill_(1)

@@ -129,12 +129,16 @@ bool slot_kept(const Seq &q, int64_t i, int P) {
   return q.kmask.empty() || ((q.kmask[i / P] >> (i % P)) & 1);
 }
 
-// Maximal runs [s, e) of masked slots, in order.
+// Maximal runs [s, e) of masked slots, in order (whole kept pages skipped).
 std::vector<std::pair<int64_t, int64_t>> masked_runs(const Seq &q, int P) {
   std::vector<std::pair<int64_t, int64_t>> runs;
   if (q.kmask.empty()) return runs;
   int64_t i = 0;
   while (i < q.length) {
+    if (i % P == 0 && q.kmask[i / P] == 0xffff) {
+      i += P;
+      continue;
+    }
     if (slot_kept(q, i, P)) {
       ++i;
       continue;
@@ -145,6 +149,19 @@ std::vector<std::pair<int64_t, int64_t>> masked_runs(const Seq &q, int P) {
     i = j;
   }
   return runs;
+}
+
+// Number of maximal masked runs in the keep words km (P <= 16 slots a word).
+int64_t count_runs(const std::vector<uint16_t> &km, int P) {
+  int64_t n = 0;
+  uint32_t prev_masked = 0; // the last slot of the previous page is masked
+  for (uint16_t w : km) {
+    const uint32_t z = ~(uint32_t)w & ((1u << P) - 1u);   // masked slots
+    const uint32_t starts = z & ~((z << 1) | prev_masked); // a run starts where the slot before is kept
+    n += __builtin_popcount(starts);
+    prev_masked = (z >> (P - 1)) & 1u;
+  }
+  return n;
 }
 
 // New pages of a masked sequence start with every slot kept.
@@ -1120,26 +1137,30 @@ namespace {
 sq_status evict_deferred(sq_store *s, sq_seq h, const std::vector<int32_t> &ids,
                          const std::vector<std::pair<int64_t, int64_t>> &sp, void *stream,
                          sq_evict_stats *stats) {
+  if (s->P > 16) return fail(SQ_ERR_INVALID, "deferred eviction needs page_size <= 16");
   Seq *q = s->get(h);
   std::vector<uint16_t> km = q->kmask;
   if (km.empty()) km.assign(q->pages.size(), 0xffff);
   int64_t newly = 0;
-  for (const auto &se : sp)
-    for (int64_t i = se.first; i < se.second; ++i) {
-      uint16_t &w = km[i / s->P];
-      const uint16_t bit = (uint16_t)(1u << (i % s->P));
-      newly += (w & bit) != 0;
-      w &= (uint16_t)~bit;
+  for (const auto &se : sp) // clear the span's bits page by page
+    for (int64_t pg = se.first / s->P; pg * s->P < se.second; ++pg) {
+      const int64_t lo = std::max<int64_t>(se.first - pg * s->P, 0);
+      const int64_t hi = std::min<int64_t>(se.second - pg * s->P, s->P);
+      const uint32_t bits = ((1u << hi) - 1u) & ~((1u << lo) - 1u);
+      newly += __builtin_popcount(km[pg] & bits);
+      km[pg] = (uint16_t)(km[pg] & ~bits);
     }
-  Seq probe;
-  probe.length = q->length;
-  probe.kmask = km;
-  const auto runs = masked_runs(probe, s->P);
-  if ((int64_t)runs.size() > SQ_MAX_EVICT_SPANS)
-    return fail(SQ_ERR_INVALID, "sequence %d would hold %zu masked runs (max %d): compact it first",
-                h, runs.size(), SQ_MAX_EVICT_SPANS);
+  const int64_t n_runs = count_runs(km, s->P);
+  if (n_runs > SQ_MAX_EVICT_SPANS)
+    return fail(SQ_ERR_INVALID, "sequence %d would hold %lld masked runs (max %d): compact it first",
+                h, (long long)n_runs, SQ_MAX_EVICT_SPANS);
   sq_evict_stats es{};
-  es.first_evicted = runs.empty() ? q->length : runs[0].first;
+  es.first_evicted = q->length;
+  for (size_t pg = 0; pg < km.size(); ++pg)
+    if (km[pg] != 0xffff) {
+      es.first_evicted = (int64_t)pg * s->P + __builtin_ctz(~(uint32_t)km[pg]);
+      break;
+    }
   es.tokens_masked = newly;
   q->kmask = std::move(km);
   q->n_masked += newly;

@@ -288,6 +288,26 @@ def test_attention_needs_a_device_store(sq):
     assert before == (s.page_table(a), s.stats())
 
 
+def test_deferred_run_limit(sq):
+    """A deferred eviction that would leave more than SQ_MAX_EVICT_SPANS
+    masked runs fails and changes nothing; compaction then removes them."""
+    s = _store(sq, 3300, 16, 2, 2200)
+    a = s.seq_create()
+    s.append(a, n=2 * sq.MAX_EVICT_SPANS + 8)
+    for c in range(sq.MAX_EVICT_SPANS + 1):
+        s.span_mark(a, c, 2 * c + 1, 2 * c + 2)
+    st = s.evict(a, list(range(sq.MAX_EVICT_SPANS)), deferred=True)
+    assert st["tokens_masked"] == sq.MAX_EVICT_SPANS and st["first_evicted"] == 1
+    before = (s.keep_flags(a).tolist(), s.spans(a), s.seq_info(a))
+    with pytest.raises(sq.SqError) as ei:
+        s.evict(a, [sq.MAX_EVICT_SPANS], deferred=True)
+    assert ei.value.code == sq.ERR_INVALID
+    assert before == (s.keep_flags(a).tolist(), s.spans(a), s.seq_info(a))
+    st = s.compact(a)
+    assert st["tokens_removed"] == sq.MAX_EVICT_SPANS
+    assert s.spans(a) == {sq.MAX_EVICT_SPANS: (sq.MAX_EVICT_SPANS + 1, sq.MAX_EVICT_SPANS + 2)}
+
+
 def test_attention_options_are_checked_first(sq):
     """sq_attn_opts errors (negative window, reserved field, misaligned
     sinks) are reported before anything else and change nothing; a windowed
