@@ -286,7 +286,9 @@ sq_status sq_evict_spans(sq_store *store, sq_seq seq, const int32_t *cursor_ids,
  * attention (sq_attn_opts.window > 0) on a sequence with masked slots is
  * rejected (a window counts kept tokens).  A sequence may hold at most
  * SQ_MAX_EVICT_SPANS maximal runs of masked slots: a deferred call that
- * would exceed it fails with SQ_ERR_INVALID and changes nothing.
+ * would exceed it fails with SQ_ERR_INVALID and changes nothing, as does
+ * one on a metadata-only store with page_size > 16 (masks are 16-bit words
+ * per page).
  * flags: 0 (= sq_evict_spans) or SQ_EVICT_DEFER; the other arguments,
  * stats and errors as for sq_evict_spans. */
 #define SQ_EVICT_DEFER 1u
