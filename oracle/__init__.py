@@ -17,6 +17,9 @@ extend
 evict
     The keep-mask, exclusive prefix sum and inverse map that ``clear_kv``
     (Algorithm 1, Phase 1) reduces to, and the compaction of a logical view.
+fp8
+    The 8-bit E4M3 code of the optional 8-bit KV cache: decode, nearest
+    encode with saturation, per-layer scales.
 pages
     A page-level model of the KV store: lowest-free-first page allocator,
     refcounts, per-sequence page lists, zero-copy fork of the auxiliary
@@ -34,6 +37,6 @@ against closed forms, invariants, an independent library routine
 is "parity unpinned".
 """
 
-from . import attention, evict, extend, pages  # noqa: F401
+from . import attention, evict, extend, fp8, pages  # noqa: F401
 
-__all__ = ["attention", "evict", "extend", "pages"]
+__all__ = ["attention", "evict", "extend", "fp8", "pages"]

@@ -66,6 +66,7 @@ import math
 import numpy as np
 
 from . import evict as _evict
+from . import fp8 as _fp8
 
 
 class OracleError(Exception):
@@ -114,7 +115,7 @@ class PageModel:
 
     def __init__(self, num_pages, page_size, max_seqs, max_pages_per_seq,
                  layers=1, kv_heads=1, head_dim=1, with_data=False, evict_chunk_pages=0,
-                 evict_remap=False):
+                 evict_remap=False, kv_scales=None):
         self.num_pages = int(num_pages)
         self.evict_chunk_pages = int(evict_chunk_pages)
         self.evict_remap = bool(evict_remap)
@@ -129,6 +130,9 @@ class PageModel:
         self.peak_pages = 0
         self.last_schedule = []  # the last eviction's (allocated, released) pages per step
         self.with_data = with_data
+        # 8-bit cache: [NL][2] scales (K, V); appended K/V are stored as
+        # their E4M3 round trip (see the fp8 module)
+        self.kv_scales = None if kv_scales is None else np.asarray(kv_scales, dtype=np.float32)
         if with_data:
             shape = (self.num_pages, self.P, layers, kv_heads, head_dim)
             self.K = np.zeros(shape)
@@ -202,6 +206,11 @@ class PageModel:
             raise NoPages("not enough free pages")
         if seq.length % self.P:
             assert self.refcount[seq.pages[-1]] == 1, "partial tail page must be private"
+        if self.with_data and self.kv_scales is not None and n:
+            k_new = np.stack([_fp8.roundtrip(np.asarray(k_new)[l], self.kv_scales[l, 0])
+                              for l in range(self.layers)])
+            v_new = np.stack([_fp8.roundtrip(np.asarray(v_new)[l], self.kv_scales[l, 1])
+                              for l in range(self.layers)])
         for i in range(n):
             if seq.length % self.P == 0:
                 seq.pages.append(self._alloc())

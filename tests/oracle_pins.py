@@ -906,6 +906,78 @@ def check_deferred_then_compact_equals_immediate(seed=26):
         assert np.array_equal(models[0].K, models[1].K)
 
 
+def check_fp8_decode_table():
+    """All 256 E4M3 codes decode to what torch's float8_e4m3fn type holds
+    (an independent implementation of the same format)."""
+    import torch
+    from oracle import fp8
+    codes = np.arange(256, dtype=np.uint8)
+    want = torch.from_numpy(codes).view(torch.float8_e4m3fn).to(torch.float64).numpy()
+    got = fp8.decode(codes)
+    assert np.array_equal(np.isnan(got), np.isnan(want))
+    ok = ~np.isnan(want)
+    assert np.array_equal(got[ok], want[ok])
+    assert np.array_equal(np.signbit(got[ok]), np.signbit(want[ok]))
+    assert got[0x7E] == 448.0 and got[0x01] == 2.0 ** -9 and got[0x08] == 2.0 ** -6
+
+
+def check_fp8_encode(seed=27):
+    """Nearest-even encoding: equal to torch's conversion wherever torch does
+    not overflow (|y| < 464), including exact ties and subnormals; equal to a
+    brute-force nearest search over every finite code; saturating at 448."""
+    import torch
+    from oracle import fp8
+    rng = np.random.default_rng(seed)
+    mags = fp8.decode(np.arange(0x7F))
+    mids = (mags[:-1] + mags[1:]) / 2                       # exact ties
+    y = np.concatenate([
+        rng.standard_normal(4000) * 30, rng.standard_normal(2000) * 1e-3,
+        rng.uniform(-460, 460, 2000), mids, -mids, mags, -mags, [0.0, -0.0, 463.9, -463.9],
+    ]).astype(np.float32)
+    got = fp8.encode(y)
+    want = torch.from_numpy(y).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(got, want)
+    finite = np.array([c for c in range(256) if (c & 0x7F) != 0x7F])
+    vals = fp8.decode(finite)
+    for x in y[::37]:
+        d = np.abs(vals - np.float64(x))
+        best = finite[d == d.min()]
+        best = best[np.signbit(fp8.decode(best)) == np.signbit(x)] if len(best) > 1 else best
+        if len(best) > 1:
+            best = best[best % 2 == 0]
+        assert fp8.encode(np.float32(x)) == best[0], x
+    big = np.array([448.0, 464.0, 500.0, 1e6, -448.0, -1e30], dtype=np.float32)
+    assert fp8.encode(big).tolist() == [0x7E, 0x7E, 0x7E, 0x7E, 0xFE, 0xFE]
+
+
+def check_fp8_store_values(seed=28):
+    """An 8-bit store holds each appended value's E4M3 round trip with its
+    layer's scale (relative error <= 1/16 in the normal range), and fork and
+    eviction move those values unchanged."""
+    from oracle import fp8
+    rng = np.random.default_rng(seed)
+    scales = np.array([[0.05, 0.02], [0.5, 0.25]], dtype=np.float32)
+    m = pg.PageModel(num_pages=40, page_size=4, max_seqs=3, max_pages_per_seq=40, layers=2,
+                     kv_heads=2, head_dim=3, with_data=True, kv_scales=scales)
+    a = m.seq_create()
+    k = rng.standard_normal((2, 30, 2, 3))
+    v = rng.standard_normal((2, 30, 2, 3))
+    m.append(a, 30, k, v)
+    kk, vv, _ = m.view(a)
+    for l in range(2):
+        assert np.array_equal(kk[:, l], fp8.roundtrip(k[l], scales[l, 0]))
+        assert np.array_equal(vv[:, l], fp8.roundtrip(v[l], scales[l, 1]))
+        y = np.abs(k[l] / scales[l, 0])
+        normal = (y >= 2.0 ** -6) & (y < 448)
+        assert np.all(np.abs(kk[:, l] - k[l])[normal] <= np.abs(k[l])[normal] / 16 + 1e-12)
+    b = m.fork(a, 13)
+    m.span_mark(a, 0, 2, 9)
+    m.evict(a, [0])
+    keep = np.ones(30, bool)
+    keep[2:9] = False
+    assert np.array_equal(m.view(a)[0], kk[keep]) and np.array_equal(m.view(b)[1], vv[:13])
+
+
 ALL_CHECKS = [
     check_weights_sum_to_one, check_single_key_returns_v, check_textbook_softmax,
     check_uniform_closed_form, check_two_key_closed_form,
@@ -923,4 +995,5 @@ ALL_CHECKS = [
     check_sinks_textbook, check_sink_closed_form, check_windows,
     check_deferred_against_list_model, check_deferred_by_hand,
     check_deferred_then_compact_equals_immediate,
+    check_fp8_decode_table, check_fp8_encode, check_fp8_store_values,
 ]

@@ -13,10 +13,13 @@ import pytest
 from oracle import attention as att
 from oracle import evict as ev
 from oracle import extend as ex
+from oracle import fp8 as f8
 from oracle import pages as pg
 from tests import oracle_pins as pins
 
 _ORIG_RUNS = pg.PageModel._masked_runs
+_ORIG_DECODE = f8.decode
+_ORIG_ENCODE = f8.encode
 _ORIG_FORK = pg.PageModel.fork
 _ORIG_EVICT = pg.PageModel.evict
 
@@ -238,6 +241,26 @@ def _deferred_shifts_spans(self, h, cursor_ids, deferred=False):
     return st
 
 
+def _fp8_decode_bias_8(codes):
+    return _ORIG_DECODE(codes) / 2.0
+
+
+def _fp8_ties_away(y):
+    y = np.asarray(y, dtype=np.float32)
+    code = _ORIG_ENCODE(y).astype(np.int64)
+    mags = _ORIG_DECODE(np.arange(0x7F))
+    a = np.abs(y.astype(np.float64))
+    mid = np.isin(a, (mags[:-1] + mags[1:]) / 2)
+    up = np.where(mid & ((code & 0x7F) < 0x7E), code + ((code & 1) == 0), code)
+    return up.astype(np.uint8)
+
+
+def _fp8_no_saturation(y):
+    code = _ORIG_ENCODE(y)
+    a = np.abs(np.asarray(y, dtype=np.float64))
+    return np.where(a > 464, code | 0x7F, code).astype(np.uint8)
+
+
 def _extend_window_one_too_wide(q, k, v, scale, group, mask=None, window=0, sinks=None):
     return _orig_extend(q, k, v, scale, group, mask, window + 1 if window > 0 else 0, sinks)
 
@@ -271,6 +294,9 @@ MUTANTS = {
     "eviction_ignores_masked_slots": (pg.PageModel, "_masked_runs", staticmethod(_runs_ignore_masks)),
     "fork_drops_masks": (pg.PageModel, "fork", _fork_drops_masks),
     "deferred_eviction_shifts_spans": (pg.PageModel, "evict", _deferred_shifts_spans),
+    "fp8_exponent_bias_8": (f8, "decode", _fp8_decode_bias_8),
+    "fp8_ties_away_from_zero": (f8, "encode", _fp8_ties_away),
+    "fp8_overflow_to_nan": (f8, "encode", _fp8_no_saturation),
 }
 
 
