@@ -47,7 +47,7 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--tasks", type=int, default=8)
     ap.add_argument("--ctx", type=int, default=131072)
-    ap.add_argument("--legs", default="decode,modes,evict,extend,outlier,variants,fullstack,cpu",
+    ap.add_argument("--legs", default="decode,modes,evict,extend,outlier,variants,fp8,fullstack,cpu",
                     help="comma list of: decode, modes, evict, extend, outlier, fullstack, cpu, copy "
                          "(a plain 1 GiB device copy used to calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -533,6 +533,33 @@ def variants_leg(sq, torch, wl, reps=20, window=128):
     return res
 
 
+def fp8_leg(sq, torch, wl, steps=20, warmup=3):
+    """The headline decode step on an 8-bit (E4M3) store: the same 128K
+    shared-prefix batch, K/V scales 0.011 / 0.0095 (unit-variance K/V),
+    append + attention per step."""
+    from paper_2602_22603_amd import drivers
+    total = steps + warmup
+    store, seqs, _ = drivers.build_shared128k(keep_inputs=(), extra_tokens=2 * total + 16,
+                                              kv_scales=[[0.011, 0.0095]])
+    B = len(seqs)
+    kb = [wl.device_normal_bf16((1, B, 8, 128), 800 + 3 * i, "cuda") for i in range(total)]
+    vb = [wl.device_normal_bf16((1, B, 8, 128), 801 + 3 * i, "cuda") for i in range(total)]
+    qs = [wl.device_normal_bf16((B, 32, 128), 802 + 3 * i, "cuda") for i in range(total)]
+    out = torch.empty((B, 32, 128), dtype=torch.float32, device="cuda")
+    r = time_steps(sq, torch, store, seqs, sq.ATTN_AUTO, steps, warmup, kb, vb, qs, out)
+    prof, plan = r["prof"], r["plan"]
+    kern = prof["decode_mfma_ms"] / max(1, prof["decode_mfma_launches"])
+    store.close()
+    return dict(workload="8 tasks x (main 131072 + forked aux 130816+512) tokens, 16-query step "
+                         "(append + attention), 32q/8kv heads, head_dim 128, E4M3 K/V",
+                ms_per_step=round(r["ms_per_step"], 4), gbps=round(r["gbps"], 1),
+                tokens_per_s=round(r["tokens_per_s"], 1),
+                kv_bytes_per_step=r["kv_bytes_per_step"], kernel_ms=round(kern, 5),
+                kernel_gbps=round(plan["kv_bytes_mfma"] / (kern * 1e-3) / 1e9, 1),
+                kernel_frac_of_hbm_peak=round(plan["kv_bytes_mfma"] / (kern * 1e-3) / 1e9 /
+                                              HBM_PEAK_GBPS, 4))
+
+
 def fullstack_leg(sq, torch, wl):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
     turns; with one-shot eviction, with eviction in 64-page chunks (bounded
@@ -756,6 +783,11 @@ def main():
     if "outlier" in legs:
         log("32K outlier leg ...")
         outlier = outlier_leg(sq, torch, wl)
+    fp8 = None
+    if "fp8" in legs:
+        log("8-bit KV store leg (128K shared prefix) ...")
+        fp8 = fp8_leg(sq, torch, wl, args.steps, args.warmup)
+        torch.cuda.empty_cache()
     variants = None
     if "variants" in legs:
         log("attention options leg (windows and sinks, 64q/8kv/64) ...")
@@ -801,6 +833,7 @@ def main():
         "extend": extend,
         "outlier32k": outlier,
         "attention_options": variants,
+        "kv_fp8": fp8,
         "full_stack": fullstack,
         "cpu_baseline": cpu,
         "kernel_sources_sha": kernel_sha(),

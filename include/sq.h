@@ -41,6 +41,7 @@
  * Data layout in HBM (caller-allocated, sizes from sq_pool_bytes)
  * ---------------------------------------------------------------
  *   K pool  bf16  [NL][Hkv][num_pages][P][D]   token-major rows of D values
+ *                                               (E4M3 bytes with SQ_STORE_KV_FP8)
  *   V pool  bf16  [NL][Hkv][num_pages][D][P]   page-transposed: the P tokens
  *                                               of one channel are contiguous
  *   pos     int32 [num_pages][P]               position of each cached token
@@ -59,7 +60,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 6
+#define SQ_ABI_VERSION 7
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -86,6 +87,18 @@ typedef enum {
                                      of a fresh page and a copy.  Logical
                                      views are the same; page tables and
                                      refcounts differ from the default. */
+#define SQ_STORE_KV_FP8 4u        /* 8-bit KV cache (a model-serving option;
+                                     the paper states no precision): the K and
+                                     V pools hold E4M3 codes, one byte per
+                                     element in the same layouts.  Appends
+                                     take bf16 and store the code nearest to
+                                     float(x) * float(1 / scale) (ties to
+                                     even, saturating at 448) with the
+                                     layer's scale from kv_scales; attention
+                                     reads code * scale.  Decode and steps run
+                                     on the MFMA tile only (SQ_ATTN_STREAM is
+                                     rejected, other modes read every segment
+                                     on it); sq_extend_attn is rejected. */
 
 /* sq_decode_attn modes */
 #define SQ_ATTN_AUTO 0          /* shared-prefix tiles where queries share
@@ -122,6 +135,9 @@ typedef struct {
                                 the next chunk), so an eviction holds at most
                                 C transient pages; one gather launch per
                                 chunk.  The resulting page ids differ. */
+  const float *kv_scales;    /* SQ_STORE_KV_FP8: host [num_layers][2], the K
+                                and V scale of each layer (finite, > 0),
+                                copied at creation; ignored otherwise */
 } sq_store_config;
 
 typedef struct {
@@ -137,7 +153,8 @@ typedef struct {
   int64_t tokens_removed;  /* L - L' */
   int64_t tokens_moved;    /* kept tokens gathered into new pages: L' - P*floor(f/P),
                               less P per remapped page */
-  int64_t bytes_moved;     /* bytes written by the gather: tokens_moved * (NL*Hkv*D*2*2 + 4);
+  int64_t bytes_moved;     /* bytes written by the gather: tokens_moved * (NL*Hkv*D*2*E + 4),
+                              E = 2 bytes per element (1 in an 8-bit store);
                               the gather reads as many */
   int64_t pages_allocated; /* fresh pages taken for the compacted tail */
   int64_t pages_freed;     /* old pages whose last reference went away */

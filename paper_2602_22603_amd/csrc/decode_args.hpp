@@ -44,8 +44,8 @@ struct DecodeStatic {
   int32_t hq;
   int32_t hkv;
   int32_t nontemporal; // 1: every page is read once in this launch
-  float scale_log2;    // scale * log2(e)
-  int32_t pad;
+  float scale_log2;    // scale * log2(e) (times the layer's K scale in an 8-bit store)
+  int32_t kv8;         // 1: the pools hold E4M3 codes (MFMA kernels only)
 };
 
 // The plan of one launch.  It splits its flattened pages [0, total) evenly
@@ -86,6 +86,8 @@ struct MergeStatic {
   const float *part_acc;
   const float *sinks; // [Hq] learned softmax sink logits (log2 units after sink_scale), or null
   float sink_scale;   // log2(e): the sinks are in the units of the scaled scores
+  float out_scale;    // V scale of the layer in an 8-bit store (1 otherwise)
+  int32_t pad;
   int32_t hq;
   int32_t group; // G
   int32_t hkv;
@@ -137,6 +139,8 @@ struct StepMergeArgs {
   MergeStatic st;
   const StepPlan *plan;
   int32_t windowed; // 1: the plan's windowed merge sources
+  float inv_k;      // 8-bit store: 1 / K and 1 / V scale of the layer (the new
+  float inv_v;      // token is stored as E4M3 codes and attended as stored)
   int32_t pad2;
   const uint16_t *q;     // [B][Hq][D] bf16
   const uint16_t *k_new; // [B][Hkv][D] bf16
@@ -162,8 +166,9 @@ hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const Deco
                             int n_wg, hipStream_t s);
 hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
                             const DecodeDyn *dyn, int n_wg, hipStream_t s);
-hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, hipStream_t s);
+hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8, hipStream_t s);
 // Workgroups of a decode kernel (kind 0: VALU, 1: MFMA) that fit on one CU.
+// kind: 0 VALU, 1 MFMA, 2 the 8-bit MFMA kernel (four waves)
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out);
 
 } // namespace sq

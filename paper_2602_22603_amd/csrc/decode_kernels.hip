@@ -37,6 +37,7 @@
 #include <hip/hip_bf16.h>
 
 #include "decode_args.hpp"
+#include "fp8.hpp"
 
 namespace sq {
 namespace {
@@ -464,11 +465,22 @@ template <int D> struct VFrag {
 // return zeros without touching memory and every loop iteration issues the
 // same loads - which keeps the hardware's in-order load counter waits exact.
 constexpr int kRsrcWord3 = 0x00020000;
-__device__ inline __amdgpu_buffer_rsrc_t page_rsrc(const uint16_t *page, bool want, int bytes) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t *>(page), (short)0, want ? bytes : 0,
+__device__ inline __amdgpu_buffer_rsrc_t page_rsrc(const char *page, bool want, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char *>(page), (short)0, want ? bytes : 0,
                                            kRsrcWord3);
 }
 template <bool NT> constexpr int kAux = NT ? 2 : 0; // nt: streamed once
+// pages in flight per wave of the 8-bit MFMA tile
+#ifndef SQ_FP8_STAGES_64
+#define SQ_FP8_STAGES_64 4
+#endif
+#ifndef SQ_FP8_STAGES_128
+#define SQ_FP8_STAGES_128 2
+#endif
+#ifndef SQ_FP8_WAVES_EU
+#define SQ_FP8_WAVES_EU 3
+#endif
+template <int D> constexpr int kStages8 = D == 64 ? SQ_FP8_STAGES_64 : SQ_FP8_STAGES_128;
 
 // K fragment: lane (n, kg) takes channels 8 kg + 32 s .. +8 of token n.
 template <int D, bool NT>
@@ -487,6 +499,54 @@ __device__ inline void load_v(VFrag<D> &f, __amdgpu_buffer_rsrc_t r, int lane_of
     const auto x = __builtin_amdgcn_raw_buffer_load_b64(r, lane_off + 32 * P * j, 0, kAux<NT>);
     f.v[j] = make_uint2(x[0], x[1]);
   }
+}
+
+// The same fragments in an 8-bit store (E4M3 codes, half the bytes); they
+// become bf16 fragments just before the matrix-core instructions.
+template <int D> struct KFrag8 {
+  uint2 k[D / 32];
+};
+template <int D> struct VFrag8 {
+  uint32_t v[D / 16];
+};
+template <int D, bool NT>
+__device__ inline void load_k(KFrag8<D> &f, __amdgpu_buffer_rsrc_t r, int lane_off) {
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b64(r, lane_off + 32 * s, 0, kAux<NT>);
+    f.k[s] = make_uint2(x[0], x[1]);
+  }
+}
+template <int D, bool NT>
+__device__ inline void load_v(VFrag8<D> &f, __amdgpu_buffer_rsrc_t r, int lane_off) {
+#pragma unroll
+  for (int j = 0; j < D / 16; ++j)
+    f.v[j] = __builtin_amdgcn_raw_buffer_load_b32(r, lane_off + 16 * P * j, 0, kAux<NT>);
+}
+template <int D> __device__ inline KFrag<D> to_bf16(const KFrag8<D> &f) {
+  KFrag<D> o;
+#pragma unroll
+  for (int s = 0; s < D / 32; ++s) {
+    const uint2 lo = e4m3x4_to_bf16(f.k[s].x), hi = e4m3x4_to_bf16(f.k[s].y);
+    o.k[s] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+  return o;
+}
+template <int D, bool KV8> struct Frags {
+  using K = KFrag<D>;
+  using V = VFrag<D>;
+};
+template <int D> struct Frags<D, true> {
+  using K = KFrag8<D>;
+  using V = VFrag8<D>;
+};
+template <int D> __device__ inline const KFrag<D> &to_bf16(const KFrag<D> &f) { return f; }
+template <int D> __device__ inline const VFrag<D> &to_bf16(const VFrag<D> &f) { return f; }
+template <int D> __device__ inline VFrag<D> to_bf16(const VFrag8<D> &f) {
+  VFrag<D> o;
+#pragma unroll
+  for (int j = 0; j < D / 16; ++j) o.v[j] = e4m3x4_to_bf16(f.v[j]);
+  return o;
 }
 
 // S^T = K . Q^T for one page, then the online-softmax update of (m, l, acc);
@@ -563,8 +623,8 @@ __device__ inline void mfma_values(VFrag<D> &f, int lo, int valid, int kg, s16x4
 }
 
 // MK: the plan may carry keep masks (decided at run time by the plan; false
-// compiles the mask path out)
-template <int D, int G, int kWaves, bool NT, bool MK, class PL>
+// compiles the mask path out).  KV8: the pools hold E4M3 codes.
+template <int D, int G, int kWaves, bool NT, bool MK, class PL, bool KV8 = false>
 __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   constexpr int NS = D / 32;
   constexpr int NJ = D / 16;
@@ -605,11 +665,12 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   for (int j = 0; j < NJ; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
   float m_run = kNegInf, l_run = 0.f;
 
-  const uint16_t *khead = a.k + (int64_t)g * a.head_stride;
-  const uint16_t *vhead = a.v + (int64_t)g * a.head_stride;
-  const int koff = (n * D + 8 * kg) * 2; // byte offsets within a page
-  const int voff = (n * P + 4 * kg) * 2;
-  constexpr int kPageBytes = P * D * 2;
+  constexpr int ES = KV8 ? 1 : 2; // bytes per element
+  const char *khead = reinterpret_cast<const char *>(a.k) + (int64_t)g * a.head_stride * ES;
+  const char *vhead = reinterpret_cast<const char *>(a.v) + (int64_t)g * a.head_stride * ES;
+  const int koff = (n * D + 8 * kg) * ES; // byte offsets within a page
+  const int voff = (n * P + 4 * kg) * ES;
+  constexpr int kPageBytes = P * D * ES;
   // Wave w takes the w-th of kWaves contiguous shares of the piece's pages.
   // Two pages are in flight while one is computed: page j + 2's K is loaded
   // into page j's K registers as soon as its scores are taken, and its V
@@ -624,8 +685,8 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   typedef const int32_t __attribute__((address_space(4))) *sptr_t;
   const sptr_t ids = (sptr_t)(pt + wbeg);
   auto sid = [&](int j) -> int { return ids[min(j, max(count - 1, 0))]; };
-  auto rsrc = [&](const uint16_t *head, int id, bool want) {
-    return page_rsrc(head + (int64_t)(want ? id : 0) * a.page_stride, want, kPageBytes);
+  auto rsrc = [&](const char *head, int id, bool want) {
+    return page_rsrc(head + (int64_t)(want ? id : 0) * a.page_stride * ES, want, kPageBytes);
   };
   auto valid_of = [&](int j) -> int {
     const int pg = wbeg + j;
@@ -638,8 +699,51 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   const sptr_t mids =
       (sptr_t)(a.mask + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0 + wbeg);
   auto smask = [&](int j) -> int { return use_mask ? mids[min(j, max(count - 1, 0))] : 0xffff; };
-  KFrag<D> k0, k1;
-  VFrag<D> v0, v1;
+  if constexpr (KV8 && kStages8<D> > 2) {
+  // An 8-bit page is half the bytes: more pages in flight, the same scheme
+  // in arrays.
+  constexpr int NST = kStages8<D>;
+  KFrag8<D> kf[NST];
+  VFrag8<D> vf[NST];
+  int nid[NST], mkc[NST], mkn[NST]; // ids and masks of pages j + NST + st; masks in flight
+  if (count > 0) {
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      const int id = sid(st);
+      load_k<D, NT>(kf[st], rsrc(khead, id, st == 0 || st < count), koff);
+      load_v<D, NT>(vf[st], rsrc(vhead, id, st == 0 || st < count), voff);
+      mkc[st] = smask(st);
+    }
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      nid[st] = sid(NST + st);
+      mkn[st] = smask(NST + st);
+    }
+  }
+  for (int j = 0; j < count; j += NST) {
+    // pages past count have zero fragments and no valid token: the update
+    // leaves (m, l, acc) as they are
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      const int valid = valid_of(j + st), lo = lo_of(j + st);
+      s16x4_t phi, plo;
+      mfma_scores<D, MK>(to_bf16(kf[st]), lo, valid, mkc[st], kg, a.scale_log2, qb, acc, m_run, l_run,
+                         phi, plo);
+      load_k<D, NT>(kf[st], rsrc(khead, nid[st], j + NST + st < count), koff);
+      VFrag<D> vb = to_bf16(vf[st]);
+      mfma_values<D>(vb, lo, valid, kg, phi, plo, acc);
+      load_v<D, NT>(vf[st], rsrc(vhead, nid[st], j + NST + st < count), voff);
+      mkc[st] = mkn[st];
+    }
+#pragma unroll
+    for (int st = 0; st < NST; ++st) {
+      nid[st] = sid(j + 2 * NST + st);
+      mkn[st] = smask(j + 2 * NST + st);
+    }
+  }
+  } else {
+  typename Frags<D, KV8>::K k0, k1;
+  typename Frags<D, KV8>::V v0, v1;
   int n0 = 0, n1 = 0;   // ids of pages j + 2 and j + 3
   int mk0 = 0, mk1 = 0; // masks of pages j and j + 1 (in the fragments)
   int q0 = 0, q1 = 0;   // masks of pages j + 2 and j + 3
@@ -660,9 +764,10 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     {
       const int valid = valid_of(j), lo = lo_of(j);
       s16x4_t phi, plo;
-      mfma_scores<D, MK>(k0, lo, valid, mk0, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      mfma_scores<D, MK>(to_bf16(k0), lo, valid, mk0, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
       load_k<D, NT>(k0, rsrc(khead, n0, j + 2 < count), koff);
-      mfma_values<D>(v0, lo, valid, kg, phi, plo, acc);
+      VFrag<D> vb0 = to_bf16(v0);
+      mfma_values<D>(vb0, lo, valid, kg, phi, plo, acc);
       load_v<D, NT>(v0, rsrc(vhead, n0, j + 2 < count), voff);
       mk0 = q0;
     }
@@ -671,9 +776,10 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
       // and with no valid token the update leaves (m, l, acc) as they are.
       const int valid = valid_of(j + 1), lo = lo_of(j + 1);
       s16x4_t phi, plo;
-      mfma_scores<D, MK>(k1, lo, valid, mk1, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      mfma_scores<D, MK>(to_bf16(k1), lo, valid, mk1, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
       load_k<D, NT>(k1, rsrc(khead, n1, j + 3 < count), koff);
-      mfma_values<D>(v1, lo, valid, kg, phi, plo, acc);
+      VFrag<D> vb1 = to_bf16(v1);
+      mfma_values<D>(vb1, lo, valid, kg, phi, plo, acc);
       load_v<D, NT>(v1, rsrc(vhead, n1, j + 3 < count), voff);
       mk1 = q1;
     }
@@ -681,6 +787,8 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     n1 = sid(j + 5);
     q0 = smask(j + 4);
     q1 = smask(j + 5);
+  }
+
   }
 
   float l_tot = sum_xrow16(l_run);
@@ -753,6 +861,17 @@ __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 
 k_step_mfma(DecodeStatic a, const DecodeDyn *dyn) {
   mfma_body<D, G, kWaves, true, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
 }
+// 8-bit store: four waves, streaming loads
+template <int D, int G, bool MK>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SQ_FP8_WAVES_EU, SQ_FP8_WAVES_EU))) void
+k_decode_mfma8(DecodeArgs a) {
+  mfma_body<D, G, 4, true, MK, ArgPlan, true>(a.st, ArgPlan{a.dyn});
+}
+template <int D, int G>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SQ_FP8_WAVES_EU, SQ_FP8_WAVES_EU))) void
+k_step_mfma8(DecodeStatic a, const DecodeDyn *dyn) {
+  mfma_body<D, G, 4, true, true, DevPlan, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
+}
 
 // ===========================================================================
 // Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
@@ -794,7 +913,10 @@ struct DevMerge {
 // token as a partial of its own - score q . k_new, weight 1, value v_new -
 // and the workgroup of the first query head of each KV head stores the new
 // token's K, V, position and page-table entry for later steps.
-template <int D, bool APPEND, class MP, class SA>
+// KV8 (with APPEND): the new token is stored as E4M3 codes and joins the
+// softmax as stored (its codes; the K scale is in scale_log2, the V scale in
+// out_scale).
+template <int D, bool APPEND, class MP, class SA, bool KV8 = false>
 __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &sa) {
   constexpr int DPT = D / 64;
   constexpr int U = kMergeUnroll;
@@ -861,8 +983,15 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
       for (int q = 0; q < DPT; ++q) {
         kb[q] = kr[q];
         vb[q] = vr[q];
-        dot = fmaf(__uint_as_float((uint32_t)qr[q] << 16), __uint_as_float((uint32_t)kb[q] << 16), dot);
-        num[q] = __uint_as_float((uint32_t)vb[q] << 16);
+        float kf = __uint_as_float((uint32_t)kb[q] << 16), vf = __uint_as_float((uint32_t)vb[q] << 16);
+        if constexpr (KV8) { // the codes, and their values as the store holds them
+          kb[q] = (uint16_t)e4m3_encode(kf * sa.inv_k);
+          vb[q] = (uint16_t)e4m3_encode(vf * sa.inv_v);
+          kf = __uint_as_float(e4m3x4_to_bf16(kb[q]).x << 16);
+          vf = __uint_as_float(e4m3x4_to_bf16(vb[q]).x << 16);
+        }
+        dot = fmaf(__uint_as_float((uint32_t)qr[q] << 16), kf, dot);
+        num[q] = vf;
       }
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
@@ -875,8 +1004,14 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
 #pragma unroll
         for (int q = 0; q < DPT; ++q) {
           const int c = lane * DPT + q;
-          sa.k[pb + (int64_t)slot * D + c] = kb[q];
-          sa.v[pb + (int64_t)c * P + slot] = vb[q];
+          if constexpr (KV8) {
+            uint8_t *k8 = reinterpret_cast<uint8_t *>(sa.k), *v8 = reinterpret_cast<uint8_t *>(sa.v);
+            k8[pb + (int64_t)slot * D + c] = (uint8_t)kb[q];
+            v8[pb + (int64_t)c * P + slot] = (uint8_t)vb[q];
+          } else {
+            sa.k[pb + (int64_t)slot * D + c] = kb[q];
+            sa.v[pb + (int64_t)c * P + slot] = vb[q];
+          }
         }
         if (lane == 0 && g == 0) sa.pos[(int64_t)page * P + slot] = ap.pos[b];
       }
@@ -941,7 +1076,7 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
       float nt = 0.f;
 #pragma unroll
       for (int w = 0; w < kMergeWaves; ++w) nt = fmaf(sc[w], s_num[w][lane * DPT + q], nt);
-      out[q] = dt > 0.f ? nt / dt : 0.f;
+      out[q] = dt > 0.f ? nt / dt * a.out_scale : 0.f;
     }
   }
 }
@@ -955,6 +1090,11 @@ __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge(StepMergeArgs a
   const SQ_CONST StepPlan *plan = (const SQ_CONST StepPlan *)a.plan;
   if ((int)(blockIdx.x / a.st.hq) >= plan->batch) return; // a replay sized for a larger batch
   merge_body<D, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a);
+}
+template <int D> __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge8(StepMergeArgs a) {
+  const SQ_CONST StepPlan *plan = (const SQ_CONST StepPlan *)a.plan;
+  if ((int)blockIdx.x / a.st.hq >= plan->batch) return;
+  merge_body<D, true, DevMerge, StepMergeArgs, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a);
 }
 
 template <int D, bool NT>
@@ -999,9 +1139,27 @@ hipError_t mfma_dispatch_nt(int group, int waves, const DecodeArgs &a, hipStream
   }
 }
 
-// a plan with keep masks takes the masked variant (ordinary loads)
+template <int D, bool MK>
+hipError_t mfma8_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
+  const dim3 grid(a.dyn.n_wg), block(256);
+  switch (group) {
+  case 1: hipLaunchKernelGGL((k_decode_mfma8<D, 1, MK>), grid, block, 0, s, a); break;
+  case 2: hipLaunchKernelGGL((k_decode_mfma8<D, 2, MK>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_decode_mfma8<D, 4, MK>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_decode_mfma8<D, 8, MK>), grid, block, 0, s, a); break;
+  default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
+// a plan with keep masks takes the masked variant (ordinary loads); an
+// 8-bit store its own kernel (four waves)
 template <int D>
 hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t s) {
+  if (a.st.kv8) {
+    if (waves != 4) return hipErrorInvalidValue;
+    return a.dyn.masked ? mfma8_dispatch<D, true>(group, a, s) : mfma8_dispatch<D, false>(group, a, s);
+  }
   if (a.dyn.masked) return mfma_dispatch_nt<D, false, true>(group, waves, a, s);
   return a.st.nontemporal ? mfma_dispatch_nt<D, true, false>(group, waves, a, s)
                        : mfma_dispatch_nt<D, false, false>(group, waves, a, s);
@@ -1028,6 +1186,15 @@ template <int D, int W> const void *mfma_fn_w(int group) {
   default: return nullptr;
   }
 }
+template <int D> const void *mfma8_fn(int group) {
+  switch (group) {
+  case 1: return reinterpret_cast<const void *>(&k_decode_mfma8<D, 1, false>);
+  case 2: return reinterpret_cast<const void *>(&k_decode_mfma8<D, 2, false>);
+  case 4: return reinterpret_cast<const void *>(&k_decode_mfma8<D, 4, false>);
+  case 8: return reinterpret_cast<const void *>(&k_decode_mfma8<D, 8, false>);
+  default: return nullptr;
+  }
+}
 template <int D> const void *mfma_fn(int group, int waves) {
   return waves == 1 ? mfma_fn_w<D, 1>(group) : waves == 2 ? mfma_fn_w<D, 2>(group)
                                                           : mfma_fn_w<D, 4>(group);
@@ -1035,8 +1202,9 @@ template <int D> const void *mfma_fn(int group, int waves) {
 } // namespace
 
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out) {
-  const void *fn = kind == 0 ? (d == 128 ? valu_fn<128>(group) : valu_fn<64>(group))
-                             : (d == 128 ? mfma_fn<128>(group, waves) : mfma_fn<64>(group, waves));
+  const void *fn = kind == 0   ? (d == 128 ? valu_fn<128>(group) : valu_fn<64>(group))
+                   : kind == 2 ? (d == 128 ? mfma8_fn<128>(group) : mfma8_fn<64>(group))
+                               : (d == 128 ? mfma_fn<128>(group, waves) : mfma_fn<64>(group, waves));
   if (!fn) return hipErrorInvalidValue;
   const int block = kind == 0 ? 64 : 64 * waves;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, fn, block, 0);
@@ -1080,6 +1248,16 @@ hipError_t step_mfma_dispatch(int group, const DecodeStatic &st, const DecodeDyn
                               hipStream_t s) {
   constexpr int W = 4;
   const dim3 grid(n_wg), block(64 * W);
+  if (st.kv8) {
+    switch (group) {
+    case 1: hipLaunchKernelGGL((k_step_mfma8<D, 1>), grid, block, 0, s, st, dyn); break;
+    case 2: hipLaunchKernelGGL((k_step_mfma8<D, 2>), grid, block, 0, s, st, dyn); break;
+    case 4: hipLaunchKernelGGL((k_step_mfma8<D, 4>), grid, block, 0, s, st, dyn); break;
+    case 8: hipLaunchKernelGGL((k_step_mfma8<D, 8>), grid, block, 0, s, st, dyn); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (group) {
   case 1: hipLaunchKernelGGL((k_step_mfma<D, 1, W>), grid, block, 0, s, st, dyn); break;
   case 2: hipLaunchKernelGGL((k_step_mfma<D, 2, W>), grid, block, 0, s, st, dyn); break;
@@ -1105,9 +1283,14 @@ hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
                   : step_mfma_dispatch<64>(group, st, dyn, n_wg, s);
 }
 
-hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, hipStream_t s) {
+hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8, hipStream_t s) {
   const dim3 grid(batch * a.st.hq), block(64 * kMergeWaves);
-  if (d == 128)
+  if (kv8) {
+    if (d == 128)
+      hipLaunchKernelGGL(k_step_merge8<128>, grid, block, 0, s, a);
+    else
+      hipLaunchKernelGGL(k_step_merge8<64>, grid, block, 0, s, a);
+  } else if (d == 128)
     hipLaunchKernelGGL(k_step_merge<128>, grid, block, 0, s, a);
   else
     hipLaunchKernelGGL(k_step_merge<64>, grid, block, 0, s, a);

@@ -12,6 +12,7 @@
 //                                 tokens of one channel are contiguous
 //   pos    [NP][P]               int32 position of each cached token
 // The page size is 16 throughout.
+#include "fp8.hpp"
 #include "kv_args.hpp"
 
 namespace sq {
@@ -94,6 +95,79 @@ __global__ __launch_bounds__(256) void k_append(Pools p, AppendArgs a,
   }
 }
 
+// The same for an 8-bit store: each bf16 value x becomes the E4M3 code of
+// float(x) * (1 / scale) of its layer (K and V scales apart).
+__device__ inline float bf16_val(uint16_t b) { return __uint_as_float((uint32_t)b << 16); }
+__device__ inline uint2 quant8(uint4 w, float inv) { // 8 bf16 -> 8 codes
+  const uint32_t x[4] = {w.x, w.y, w.z, w.w};
+  uint32_t c[8];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    c[2 * i] = e4m3_encode(__uint_as_float(x[i] << 16) * inv);
+    c[2 * i + 1] = e4m3_encode(__uint_as_float(x[i] & 0xffff0000u) * inv);
+  }
+  return make_uint2(c[0] | c[1] << 8 | c[2] << 16 | c[3] << 24,
+                    c[4] | c[5] << 8 | c[6] << 16 | c[7] << 24);
+}
+
+template <int D>
+__global__ __launch_bounds__(256) void k_append8(Pools p, AppendArgs a,
+                                                 const uint16_t *__restrict__ kn,
+                                                 const uint16_t *__restrict__ vn) {
+  constexpr int U = D / 8; // 8-element units per row
+  __shared__ uint16_t tile[P][D + 8];
+  const int pi = blockIdx.x;
+  const int lh = blockIdx.y;
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  const float inv_k = p.scales[4 * layer + 2], inv_v = p.scales[4 * layer + 3];
+  const int page = a.page_ids[pi];
+  const int s_begin = pi == 0 ? a.slot0 : 0;
+  const int t_begin = pi == 0 ? 0 : pi * P - a.slot0;
+  int s_end = s_begin + (a.n_tok - t_begin);
+  if (s_end > P) s_end = P;
+  const int ns = s_end - s_begin;
+  const int64_t tok_stride = (int64_t)p.hkv * D;
+  const int64_t src0 = ((int64_t)layer * a.n_total + a.tok0 + t_begin) * tok_stride + head * D;
+  const int64_t chunk = layer * p.layer_stride + (int64_t)page * p.page_stride + head * p.head_stride;
+
+  uint8_t *kd = reinterpret_cast<uint8_t *>(p.k) + chunk;
+  for (int idx = threadIdx.x; idx < ns * U; idx += blockDim.x) {
+    const int j = idx / U, u = idx % U;
+    const uint4 val = *(reinterpret_cast<const uint4 *>(kn + src0 + j * tok_stride) + u);
+    *reinterpret_cast<uint2 *>(kd + (s_begin + j) * D + 8 * u) = quant8(val, inv_k);
+  }
+
+  uint8_t *vd = reinterpret_cast<uint8_t *>(p.v) + chunk;
+  if (ns == P) {
+    for (int idx = threadIdx.x; idx < P * U; idx += blockDim.x) {
+      const int j = idx / U, u = idx % U;
+      const uint4 val = *(reinterpret_cast<const uint4 *>(vn + src0 + j * tok_stride) + u);
+      *reinterpret_cast<uint4 *>(&tile[j][u * 8]) = val;
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < D * 2; idx += blockDim.x) {
+      const int d = idx >> 1, h = idx & 1;
+      uint32_t w[2] = {0u, 0u};
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        w[e >> 2] |= e4m3_encode(bf16_val(tile[h * 8 + e][d]) * inv_v) << (8 * (e & 3));
+      *reinterpret_cast<uint2 *>(vd + d * P + h * 8) = make_uint2(w[0], w[1]);
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < ns * D; idx += blockDim.x) {
+      const int j = idx % ns, d = idx / ns;
+      vd[d * P + s_begin + j] = (uint8_t)e4m3_encode(bf16_val(vn[src0 + j * tok_stride + d]) * inv_v);
+    }
+  }
+
+  if (lh == 0) {
+    for (int j = threadIdx.x; j < ns; j += blockDim.x)
+      p.pos[(int64_t)page * P + s_begin + j] = a.pos0 + t_begin + j;
+    if (threadIdx.x == 0 && pi >= a.new_from) a.pt_row[a.pt_first + pi] = page;
+  }
+}
+
 // One token for each of n sequences: block (b, layer * Hkv + head).
 template <int D>
 __global__ __launch_bounds__(64) void k_append_batch(Pools p, AppendBatchArgs a,
@@ -118,6 +192,32 @@ __global__ __launch_bounds__(64) void k_append_batch(Pools p, AppendBatchArgs a,
   }
 }
 
+template <int D>
+__global__ __launch_bounds__(64) void k_append_batch8(Pools p, AppendBatchArgs a,
+                                                      const uint16_t *__restrict__ kn,
+                                                      const uint16_t *__restrict__ vn) {
+  constexpr int U = D / 8;
+  const int b = blockIdx.x;
+  const int lh = blockIdx.y;
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  const float inv_k = p.scales[4 * layer + 2], inv_v = p.scales[4 * layer + 3];
+  const int page = a.page[b];
+  const int slot = a.slot[b];
+  const int64_t src = (((int64_t)layer * a.n + b) * p.hkv + head) * D;
+  const int64_t chunk = layer * p.layer_stride + (int64_t)page * p.page_stride + head * p.head_stride;
+  uint8_t *kd = reinterpret_cast<uint8_t *>(p.k) + chunk + slot * D;
+  for (int u = threadIdx.x; u < U; u += blockDim.x)
+    *reinterpret_cast<uint2 *>(kd + 8 * u) = quant8(*(reinterpret_cast<const uint4 *>(kn + src) + u), inv_k);
+  uint8_t *vd = reinterpret_cast<uint8_t *>(p.v) + chunk + slot;
+  for (int d = threadIdx.x; d < D; d += blockDim.x)
+    vd[d * P] = (uint8_t)e4m3_encode(bf16_val(vn[src + d]) * inv_v);
+  if (lh == 0 && threadIdx.x == 0) {
+    p.pos[(int64_t)page * P + slot] = a.pos[b];
+    if (a.pt_index[b] >= 0) a.pt[a.pt_index[b]] = page;
+  }
+}
+
 // dst[i] = src[i] for i < n, then dst[n] = tail_value when tail_value >= 0.
 __global__ __launch_bounds__(64) void k_set_entries(SetEntries a) {
   if ((int)threadIdx.x < a.n) a.base[a.index[threadIdx.x]] = a.value[threadIdx.x];
@@ -135,17 +235,25 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t *dst, int32_t value, i
   if (i < n) dst[i] = value;
 }
 
+// Element E of the pools (bf16 bits, or E4M3 bytes): the chunk of one
+// (layer, page, head), strides counted in elements.
+template <class E> __device__ inline E *chunk_of(uint16_t *pool, const Pools &p, int layer, int page,
+                                                 int head) {
+  return reinterpret_cast<E *>(pool) + layer * p.layer_stride + (int64_t)page * p.page_stride +
+         head * p.head_stride;
+}
+
 // Whole-page copy (every layer and head, K, V and pos): the fork's tail page.
-template <int D>
+template <int D, class E>
 __global__ __launch_bounds__(256) void k_copy_page(Pools p, int32_t src_page, int32_t dst_page) {
-  constexpr int U = P * D / 8;
+  constexpr int U = P * D * (int)sizeof(E) / 16;
   const int lh = blockIdx.x;
   const int layer = lh / p.hkv;
   const int head = lh % p.hkv;
-  const uint4 *ks = reinterpret_cast<const uint4 *>(k_chunk(p, layer, src_page, head));
-  const uint4 *vs = reinterpret_cast<const uint4 *>(v_chunk(p, layer, src_page, head));
-  uint4 *kd = reinterpret_cast<uint4 *>(k_chunk_w(p, layer, dst_page, head));
-  uint4 *vd = reinterpret_cast<uint4 *>(v_chunk_w(p, layer, dst_page, head));
+  const uint4 *ks = reinterpret_cast<const uint4 *>(chunk_of<E>(p.k, p, layer, src_page, head));
+  const uint4 *vs = reinterpret_cast<const uint4 *>(chunk_of<E>(p.v, p, layer, src_page, head));
+  uint4 *kd = reinterpret_cast<uint4 *>(chunk_of<E>(p.k, p, layer, dst_page, head));
+  uint4 *vd = reinterpret_cast<uint4 *>(chunk_of<E>(p.v, p, layer, dst_page, head));
   for (int u = threadIdx.x; u < U; u += blockDim.x) {
     kd[u] = ks[u];
     vd[u] = vs[u];
@@ -228,9 +336,9 @@ __global__ __launch_bounds__(256) void k_write_ids(int32_t *dst, NewIds ids, int
 // gather).  A fresh page is never a page this or a later gather reads: it is
 // either a page nothing held or an old page whose tokens earlier gathers have
 // all moved, so nothing is read after being written.
-template <int D>
+template <int D, class E>
 __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
-  constexpr int U = D / 8;
+  constexpr int U = D * (int)sizeof(E) / 16; // 16-byte units per K row
   __shared__ int spage[P];
   __shared__ int sslot[P];
   __shared__ int nvalid;
@@ -256,17 +364,17 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   __syncthreads();
   const int nv = nvalid;
 
-  uint16_t *kd = k_chunk_w(p, layer, dst_page, head);
+  E *kd = chunk_of<E>(p.k, p, layer, dst_page, head);
   for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) {
     const int j = idx / U, u = idx % U;
-    const uint4 *ks = reinterpret_cast<const uint4 *>(k_chunk(p, layer, spage[j], head) +
+    const uint4 *ks = reinterpret_cast<const uint4 *>(chunk_of<E>(p.k, p, layer, spage[j], head) +
                                                       sslot[j] * D);
     *(reinterpret_cast<uint4 *>(kd + j * D) + u) = ks[u];
   }
-  uint16_t *vd = v_chunk_w(p, layer, dst_page, head);
+  E *vd = chunk_of<E>(p.v, p, layer, dst_page, head);
   for (int idx = threadIdx.x; idx < D * P; idx += blockDim.x) {
     const int j = idx % P, d = idx / P;
-    if (j < nv) vd[d * P + j] = v_chunk(p, layer, spage[j], head)[d * P + sslot[j]];
+    if (j < nv) vd[d * P + j] = chunk_of<E>(p.v, p, layer, spage[j], head)[d * P + sslot[j]];
   }
   if (lh == 0 && threadIdx.x < nv)
     p.pos[(int64_t)dst_page * P + threadIdx.x] =
@@ -281,7 +389,12 @@ hipError_t launch_append(const Pools &p, const AppendArgs &a, const void *k_new,
   dim3 grid(a.n_pages, p.nl * p.hkv);
   const auto *kn = static_cast<const uint16_t *>(k_new);
   const auto *vn = static_cast<const uint16_t *>(v_new);
-  if (p.d == 128)
+  if (p.kv8) {
+    if (p.d == 128)
+      hipLaunchKernelGGL(k_append8<128>, grid, dim3(256), 0, s, p, a, kn, vn);
+    else
+      hipLaunchKernelGGL(k_append8<64>, grid, dim3(256), 0, s, p, a, kn, vn);
+  } else if (p.d == 128)
     hipLaunchKernelGGL(k_append<128>, grid, dim3(256), 0, s, p, a, kn, vn);
   else
     hipLaunchKernelGGL(k_append<64>, grid, dim3(256), 0, s, p, a, kn, vn);
@@ -293,7 +406,12 @@ hipError_t launch_append_batch(const Pools &p, const AppendBatchArgs &a, const v
   dim3 grid(a.n, p.nl * p.hkv);
   const auto *kn = static_cast<const uint16_t *>(k_new);
   const auto *vn = static_cast<const uint16_t *>(v_new);
-  if (p.d == 128)
+  if (p.kv8) {
+    if (p.d == 128)
+      hipLaunchKernelGGL(k_append_batch8<128>, grid, dim3(64), 0, s, p, a, kn, vn);
+    else
+      hipLaunchKernelGGL(k_append_batch8<64>, grid, dim3(64), 0, s, p, a, kn, vn);
+  } else if (p.d == 128)
     hipLaunchKernelGGL(k_append_batch<128>, grid, dim3(64), 0, s, p, a, kn, vn);
   else
     hipLaunchKernelGGL(k_append_batch<64>, grid, dim3(64), 0, s, p, a, kn, vn);
@@ -323,12 +441,16 @@ hipError_t launch_copy_i32(int32_t *dst, const int32_t *src, int32_t n, int32_t 
 }
 
 hipError_t launch_copy_page(const Pools &p, int32_t src_page, int32_t dst_page, hipStream_t s) {
-  if (p.d == 128)
-    hipLaunchKernelGGL(k_copy_page<128>, dim3(p.nl * p.hkv), dim3(256), 0, s, p, src_page,
-                       dst_page);
+  const dim3 grid(p.nl * p.hkv), block(256);
+  if (p.kv8) {
+    if (p.d == 128)
+      hipLaunchKernelGGL((k_copy_page<128, uint8_t>), grid, block, 0, s, p, src_page, dst_page);
+    else
+      hipLaunchKernelGGL((k_copy_page<64, uint8_t>), grid, block, 0, s, p, src_page, dst_page);
+  } else if (p.d == 128)
+    hipLaunchKernelGGL((k_copy_page<128, uint16_t>), grid, block, 0, s, p, src_page, dst_page);
   else
-    hipLaunchKernelGGL(k_copy_page<64>, dim3(p.nl * p.hkv), dim3(256), 0, s, p, src_page,
-                       dst_page);
+    hipLaunchKernelGGL((k_copy_page<64, uint16_t>), grid, block, 0, s, p, src_page, dst_page);
   return hipGetLastError();
 }
 
@@ -348,10 +470,15 @@ hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStrea
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s) {
   if (a.n_new == 0) return hipSuccess;
   dim3 grid(a.n_new, p.nl * p.hkv);
-  if (p.d == 128)
-    hipLaunchKernelGGL(k_evict_gather<128>, grid, dim3(256), 0, s, p, a);
+  if (p.kv8) {
+    if (p.d == 128)
+      hipLaunchKernelGGL((k_evict_gather<128, uint8_t>), grid, dim3(256), 0, s, p, a);
+    else
+      hipLaunchKernelGGL((k_evict_gather<64, uint8_t>), grid, dim3(256), 0, s, p, a);
+  } else if (p.d == 128)
+    hipLaunchKernelGGL((k_evict_gather<128, uint16_t>), grid, dim3(256), 0, s, p, a);
   else
-    hipLaunchKernelGGL(k_evict_gather<64>, grid, dim3(256), 0, s, p, a);
+    hipLaunchKernelGGL((k_evict_gather<64, uint16_t>), grid, dim3(256), 0, s, p, a);
   return hipGetLastError();
 }
 

@@ -50,7 +50,7 @@ constexpr uint64_t kAlign = 256;
 uint64_t align_up(uint64_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Layout {
-  uint64_t pt, mask, keep, dst, src, upload, part_m, part_l, part_acc, step, total;
+  uint64_t pt, mask, keep, dst, src, upload, part_m, part_l, part_acc, step, scales, total;
   uint64_t upload_elems;
 };
 
@@ -76,6 +76,7 @@ Layout layout_of(const sq_store_config &c) {
   L.part_l = take((uint64_t)sq::kMaxItems * sq::kRows * 4);
   L.part_acc = take((uint64_t)sq::kMaxItems * sq::kRows * c.head_dim * 4);
   L.step = take(sizeof(sq::StepPlan));
+  L.scales = take((uint64_t)c.num_layers * 4 * 4);
   L.total = off;
   return L;
 }
@@ -93,7 +94,14 @@ bool shape_ok(const sq_store_config *c, bool device, std::string *why) {
   if ((int64_t)c->max_pages_per_seq * c->page_size > (int64_t)INT32_MAX / 2)
     return bad("max_pages_per_seq * page_size too large");
   if (c->evict_chunk_pages < 0) return bad("evict_chunk_pages must be >= 0");
-  if (c->flags & ~(SQ_STORE_METADATA_ONLY | SQ_STORE_EVICT_REMAP)) return bad("unknown flags");
+  if (c->flags & ~(SQ_STORE_METADATA_ONLY | SQ_STORE_EVICT_REMAP | SQ_STORE_KV_FP8))
+    return bad("unknown flags");
+  if (c->flags & SQ_STORE_KV_FP8) {
+    if (!c->kv_scales) return bad("an 8-bit store needs kv_scales");
+    for (int i = 0; i < 2 * c->num_layers; ++i)
+      if (!std::isfinite(c->kv_scales[i]) || !(c->kv_scales[i] > 0.f))
+        return bad("kv_scales must be finite and positive");
+  }
   if (device) {
     const int grp = c->num_q_heads / c->num_kv_heads;
     if (c->page_size != sq::kPage) return bad("device mode needs page_size 16");
@@ -231,6 +239,12 @@ int64_t evicted_before(const std::vector<std::pair<int64_t, int64_t>> &sp,
 struct sq_store {
   sq_store_config cfg{};
   bool device = false;
+  bool kv8 = false;              // the pools hold E4M3 codes
+  std::vector<float> kv_scales;  // [NL][2] (8-bit store)
+  float k_scale(int l) const { return kv8 ? kv_scales[2 * l] : 1.f; }
+  float v_scale(int l) const { return kv8 ? kv_scales[2 * l + 1] : 1.f; }
+  float inv(float x) const { return (float)(1.0 / (double)x); }
+  int64_t elem_bytes() const { return kv8 ? 1 : 2; } // bytes per K or V element
   int P = 16, G = 1, D = 128;
   std::vector<int32_t> refcount;
   std::vector<uint64_t> freebits;
@@ -466,10 +480,11 @@ template <class T> int64_t first_diff(const T *a, const T *b, int64_t n) {
 // tokens (a window), read on its own; < 0: every token.
 sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode, Plan *plan,
                      int64_t keep_last = -1) {
-  const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
+  const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes();
   const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
-  const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma);
+  const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma) ||
+                           s->kv8; // an 8-bit store reads everything on the MFMA tile
 
   auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
                      const std::vector<int> &members, int32_t tok0 = 0) {
@@ -632,12 +647,18 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   return SQ_OK;
 }
 
+// A layer's region of a pool (element strides; E4M3 elements are bytes).
+uint16_t *layer_pool(sq_store *s, uint16_t *pool, int32_t layer) {
+  return reinterpret_cast<uint16_t *>(reinterpret_cast<char *>(pool) +
+                                      layer * s->pools.layer_stride * (s->kv8 ? 1 : 2));
+}
+
 // The arguments of a layer's decode launches that no plan changes.
 sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float scale, bool nt) {
   sq::DecodeStatic st{};
   st.q = static_cast<const uint16_t *>(q);
-  st.k = s->pools.k + layer * s->pools.layer_stride;
-  st.v = s->pools.v + layer * s->pools.layer_stride;
+  st.k = layer_pool(s, s->pools.k, layer);
+  st.v = layer_pool(s, s->pools.v, layer);
   st.pt = s->pt_dev;
   st.mask = s->mask_dev;
   st.part_m = s->part_m;
@@ -648,16 +669,19 @@ sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float 
   st.max_pages = s->cfg.max_pages_per_seq;
   st.hq = s->cfg.num_q_heads;
   st.hkv = s->cfg.num_kv_heads;
-  st.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  // an 8-bit store's K scale joins the score scale
+  st.scale_log2 = (float)((double)scale * 1.4426950408889634 * (double)s->k_scale(layer));
   st.nontemporal = nt ? 1 : 0;
+  st.kv8 = s->kv8 ? 1 : 0;
   return st;
 }
 
-sq::MergeStatic merge_static(sq_store *s, float *out, const float *sinks) {
+sq::MergeStatic merge_static(sq_store *s, int32_t layer, float *out, const float *sinks) {
   sq::MergeStatic st{};
   st.out = out;
   st.sinks = sinks;
   st.sink_scale = 1.4426950408889634f;
+  st.out_scale = s->v_scale(layer); // 1 unless the store is 8-bit
   st.part_m = s->part_m;
   st.part_l = s->part_l;
   st.part_acc = s->part_acc;
@@ -714,7 +738,7 @@ uint64_t sq_workspace_bytes(const sq_store_config *cfg) {
 uint64_t sq_pool_bytes(const sq_store_config *cfg, int32_t which) {
   if (!shape_ok(cfg, false, nullptr)) return 0;
   const uint64_t kv = (uint64_t)cfg->num_layers * cfg->num_pages * cfg->num_kv_heads *
-                      cfg->page_size * cfg->head_dim * 2;
+                      cfg->page_size * cfg->head_dim * ((cfg->flags & SQ_STORE_KV_FP8) ? 1 : 2);
   if (which == 0 || which == 1) return kv;
   if (which == 2) return (uint64_t)cfg->num_pages * cfg->page_size * 4;
   return 0;
@@ -740,6 +764,9 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
   sq_store *s = new sq_store();
   s->cfg = *cfg;
   s->device = device;
+  s->kv8 = (cfg->flags & SQ_STORE_KV_FP8) != 0;
+  if (s->kv8) s->kv_scales.assign(cfg->kv_scales, cfg->kv_scales + 2 * cfg->num_layers);
+  s->cfg.kv_scales = s->kv8 ? s->kv_scales.data() : nullptr;
   s->P = cfg->page_size;
   s->G = cfg->num_q_heads / cfg->num_kv_heads;
   s->D = cfg->head_dim;
@@ -787,6 +814,23 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
     p.page_stride = (int64_t)s->P * s->D;
     p.head_stride = p.page_stride * cfg->num_pages;
     p.layer_stride = p.head_stride * cfg->num_kv_heads;
+    p.kv8 = s->kv8 ? 1 : 0;
+    if (s->kv8) { // K scale, V scale and their inverses per layer, on the device
+      std::vector<float> sc(4 * cfg->num_layers);
+      for (int l = 0; l < cfg->num_layers; ++l) {
+        sc[4 * l] = s->k_scale(l);
+        sc[4 * l + 1] = s->v_scale(l);
+        sc[4 * l + 2] = s->inv(s->k_scale(l));
+        sc[4 * l + 3] = s->inv(s->v_scale(l));
+      }
+      float *dev = reinterpret_cast<float *>(ws + lay.scales);
+      hipError_t e = hipMemcpy(dev, sc.data(), sc.size() * 4, hipMemcpyHostToDevice);
+      if (e != hipSuccess) {
+        delete s;
+        return hip_fail(e, "hipMemcpy(kv scales)");
+      }
+      p.scales = dev;
+    }
     {
       int dev = 0, cus = 0, nb = 0;
       if (hipGetDevice(&dev) == hipSuccess &&
@@ -795,7 +839,7 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
         s->cus = cus;
       if (sq::decode_blocks_per_cu(0, s->D, s->G, 1, &nb) == hipSuccess && nb > 0) s->wg_per_cu[0] = nb;
       nb = 0;
-      if (sq::decode_blocks_per_cu(1, s->D, s->G, s->mfma_waves, &nb) == hipSuccess && nb > 0)
+      if (sq::decode_blocks_per_cu(s->kv8 ? 2 : 1, s->D, s->G, s->mfma_waves, &nb) == hipSuccess && nb > 0)
         s->wg_per_cu[1] = nb;
     }
     void *host = nullptr;
@@ -1446,7 +1490,8 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
   q->kmask.clear(); // the masked slots are gone (their device row stays dirty)
   q->n_masked = 0;
   const int64_t moved = Lp - fp * s->P - n_alias * s->P;
-  const int64_t per_tok = (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2 + 4;
+  const int64_t per_tok =
+      (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes() + 4;
   es.tokens_removed = removed;
   es.tokens_moved = moved;
   es.bytes_moved = moved * per_tok;
@@ -1502,6 +1547,8 @@ sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int3
   if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
   if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
   if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
+  if (s && s->kv8 && mode == SQ_ATTN_STREAM)
+    return fail(SQ_ERR_INVALID, "an 8-bit store has no STREAM mode (the MFMA tile reads it)");
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
   if (!q || !out || !aligned16(q) || !aligned16(out))
     return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
@@ -1524,7 +1571,7 @@ sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int3
   sq::MergeArgs ma{};
   da[0].st = decode_static(s, layer, q, scale, !plan.pages_reread);
   da[1].st = da[0].st;
-  ma.st = merge_static(s, out, o.sinks);
+  ma.st = merge_static(s, layer, out, o.sinks);
   sq::DecodeDyn dyn[2]{};
   fill_dyn(s, plan, dyn, &ma.dyn);
   for (int pass = 0; pass < 2; ++pass) {
@@ -1559,6 +1606,8 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   if (r != SQ_OK) return r;
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
   if (window < 0) return fail(SQ_ERR_INVALID, "window %d < 0", window);
+  if (s->kv8 && mode == SQ_ATTN_STREAM)
+    return fail(SQ_ERR_INVALID, "an 8-bit store has no STREAM mode (the MFMA tile reads it)");
   if (s->device && mode != SQ_ATTN_STREAM && s->mfma_waves != 4)
     return fail(SQ_ERR_INVALID, "decode steps need 4 waves per MFMA work item");
   // attention over the tokens before the step; the new ones join in the
@@ -1574,8 +1623,8 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   }
   // which launches a layer makes depends on the mode only, so that a
   // captured step replays for every later step of the same batch and mode
-  const bool launch[2] = {mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
-                              (mode == SQ_ATTN_AUTO && !s->auto_single_mfma),
+  const bool launch[2] = {!s->kv8 && (mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
+                                       (mode == SQ_ATTN_AUTO && !s->auto_single_mfma)),
                           mode != SQ_ATTN_STREAM};
   for (int L = 0; L < 2; ++L)
     if ((plan.n_wg[L] > 0 || plan_w.n_wg[L] > 0) && !launch[L])
@@ -1591,7 +1640,7 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
     fill_dyn(s, plan, sp->dec, &sp->merge);
     if (window > 0) fill_dyn(s, plan_w, sp->dec_w, &sp->merge_w);
   }
-  const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * 2;
+  const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes();
   TokenSlots t;
   take_one_token_each(s, seqs, batch, &t);
   if (sp) {
@@ -1685,21 +1734,23 @@ sq_status sq_step_attn_ex(sq_store *s, int32_t layer, const void *k_new, const v
     if (e != hipSuccess) return hip_fail(e, "decode step kernel");
   }
   sq::StepMergeArgs ma{};
-  ma.st = merge_static(s, out, o.sinks);
+  ma.st = merge_static(s, layer, out, o.sinks);
   ma.plan = s->step_dev;
   ma.windowed = win ? 1 : 0;
   ma.q = static_cast<const uint16_t *>(q);
   ma.k_new = static_cast<const uint16_t *>(k_new);
   ma.v_new = static_cast<const uint16_t *>(v_new);
-  ma.k = s->pools.k + layer * s->pools.layer_stride;
-  ma.v = s->pools.v + layer * s->pools.layer_stride;
+  ma.k = layer_pool(s, s->pools.k, layer);
+  ma.v = layer_pool(s, s->pools.v, layer);
+  ma.inv_k = s->inv(s->k_scale(layer));
+  ma.inv_v = s->inv(s->v_scale(layer));
   ma.pos = s->pools.pos;
   ma.page_stride = s->pools.page_stride;
   ma.head_stride = s->pools.head_stride;
   ma.scale_log2 = ds.scale_log2;
   ProfPair pp;
   const bool on = prof && s->prof_begin(strm, &pp, kProfMerge);
-  hipError_t e = sq::launch_step_merge(s->D, st.batch, ma, strm);
+  hipError_t e = sq::launch_step_merge(s->D, st.batch, ma, s->kv8, strm);
   s->prof_end(strm, &pp, on);
   if (e != hipSuccess) return hip_fail(e, "decode step merge");
   ++s->st.decode_calls;
@@ -1734,8 +1785,8 @@ sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_ne
   s->last_stream = strm;
   sq::ExtendArgs a{};
   a.q = static_cast<const uint16_t *>(q);
-  a.k = s->pools.k + layer * s->pools.layer_stride;
-  a.v = s->pools.v + layer * s->pools.layer_stride;
+  a.k = layer_pool(s, s->pools.k, layer);
+  a.v = layer_pool(s, s->pools.v, layer);
   a.pt = s->pt_row(seq);
   a.out = out;
   a.page_stride = s->pools.page_stride;
@@ -1751,6 +1802,7 @@ sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_ne
   a.sinks = o.sinks;
   a.window = o.window;
   a.sink_scale = 1.4426950408889634f;
+  if (s->kv8) return fail(SQ_ERR_INVALID, "extend attention over an 8-bit store is not supported");
   a.mask_row = s->mask_row(seq);
   a.masked = sqn->n_masked > 0 ? 1 : 0;
   if (a.masked && o.window > 0)
@@ -1786,7 +1838,7 @@ sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_ne
   s->st.extend_tokens += n_new;
   const int64_t keys_read = o.window > 0 ? std::min<int64_t>(sqn->length, (int64_t)n_new + o.window - 1)
                                          : sqn->length;
-  s->st.extend_kv_bytes += keys_read * (int64_t)s->cfg.num_kv_heads * s->D * 2 * 2;
+  s->st.extend_kv_bytes += keys_read * (int64_t)s->cfg.num_kv_heads * s->D * 2 * s->elem_bytes();
   return SQ_OK;
 }
 

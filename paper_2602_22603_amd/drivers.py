@@ -15,19 +15,21 @@ from . import workload as wl
 
 
 def build_shared128k(tasks=8, ctx=131072, aux_private=512, parallel=256, extra_tokens=256,
-                     keep_inputs=(0,), device="cuda", layers=1, heads=(32, 8, 128)):
+                     keep_inputs=(0,), device="cuda", layers=1, heads=(32, 8, 128),
+                     kv_scales=None):
     """``tasks`` main threads of ``ctx`` tokens, each with an auxiliary thread
     forked at ctx - parallel (the main thread then decodes ``parallel`` more
     tokens) that adds ``aux_private`` tokens.  Returns (store, seqs, inputs)
     with seqs = [main_0, aux_0, main_1, aux_1, ...] and inputs[t] =
     (k, v, k_aux, v_aux) for the tasks in ``keep_inputs``.  heads = (query
-    heads, KV heads, head_dim)."""
+    heads, KV heads, head_dim); kv_scales: an 8-bit store's [layers][2] scales."""
     import torch
     w = wl.shared128k(n_tasks=tasks, main_len=ctx, fork_at=ctx - parallel, aux_private=aux_private)
     pages_task = ctx // 16 + aux_private // 16 + 2 * (extra_tokens // 16 + 2)
     hq, hkv, d = heads
     store = _sq.Store(layers, hq, hkv, d, num_pages=tasks * pages_task + 64, max_seqs=2 * tasks + 4,
-                      max_pages_per_seq=ctx // 16 + extra_tokens // 16 + 64, device=device)
+                      max_pages_per_seq=ctx // 16 + extra_tokens // 16 + 64, device=device,
+                      kv_scales=kv_scales)
     seqs, inputs = [], {}
     for t in range(tasks):
         k, v, ka, va = shared_task_inputs(w, t, device, layers, hkv, d)

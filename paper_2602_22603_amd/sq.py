@@ -18,6 +18,7 @@ LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libsq.so")
 OK, ERR_INVALID, ERR_NO_PAGES, ERR_UNKNOWN_SEQ, ERR_UNKNOWN_CURSOR, ERR_SPAN, ERR_HIP = range(7)
 STORE_METADATA_ONLY = 1
 STORE_EVICT_REMAP = 2
+STORE_KV_FP8 = 4
 EVICT_DEFER = 1
 ATTN_AUTO, ATTN_STREAM, ATTN_SHARED_PREFIX, ATTN_MFMA = 0, 1, 2, 3
 MAX_BATCH = 64
@@ -43,7 +44,7 @@ class StoreConfig(C.Structure):
         ("max_seqs", C.c_int32), ("max_pages_per_seq", C.c_int32),
         ("k_pool", C.c_void_p), ("v_pool", C.c_void_p), ("pos_pool", C.c_void_p),
         ("workspace", C.c_void_p), ("workspace_bytes", C.c_uint64), ("flags", C.c_uint32),
-        ("evict_chunk_pages", C.c_int32),
+        ("evict_chunk_pages", C.c_int32), ("kv_scales", C.c_void_p),
     ]
 
 
@@ -199,7 +200,9 @@ class Store:
 
     def __init__(self, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages, max_seqs,
                  max_pages_per_seq, page_size=16, device="cuda", metadata_only=False,
-                 evict_chunk_pages=0, evict_remap=False):
+                 evict_chunk_pages=0, evict_remap=False, kv_scales=None):
+        """kv_scales: [num_layers][2] K and V scales of an 8-bit (E4M3) store
+        (None: bf16 pools)."""
         self.cfg = StoreConfig(num_layers, num_q_heads, num_kv_heads, head_dim, page_size,
                                num_pages, max_seqs, max_pages_per_seq)
         self.cfg.evict_chunk_pages = evict_chunk_pages
@@ -212,6 +215,13 @@ class Store:
         L = lib()
         self._handle = C.c_void_p()
         self.cfg.flags = STORE_EVICT_REMAP if evict_remap else 0
+        self.kv_fp8 = kv_scales is not None
+        self.kv_scales = None
+        if self.kv_fp8:
+            self.kv_scales = np.ascontiguousarray(np.asarray(kv_scales, dtype=np.float32)
+                                                  .reshape(num_layers, 2))
+            self.cfg.flags |= STORE_KV_FP8
+            self.cfg.kv_scales = self.kv_scales.ctypes.data
         if metadata_only:
             self.cfg.flags |= STORE_METADATA_ONLY
             self.k_pool = self.v_pool = self.pos_pool = self.workspace = None
@@ -225,11 +235,13 @@ class Store:
             dev = torch.device(device)
             shape_k = (num_layers, num_kv_heads, num_pages, page_size, head_dim)
             shape_v = (num_layers, num_kv_heads, num_pages, head_dim, page_size)
-            self.k_pool = torch.zeros(shape_k, dtype=torch.bfloat16, device=dev)
-            self.v_pool = torch.zeros(shape_v, dtype=torch.bfloat16, device=dev)
+            kv_dtype = torch.uint8 if self.kv_fp8 else torch.bfloat16  # E4M3 codes as bytes
+            self.k_pool = torch.zeros(shape_k, dtype=kv_dtype, device=dev)
+            self.v_pool = torch.zeros(shape_v, dtype=kv_dtype, device=dev)
             self.pos_pool = torch.zeros((num_pages, page_size), dtype=torch.int32, device=dev)
             self.workspace = torch.empty(wb, dtype=torch.uint8, device=dev)
-            assert self.k_pool.numel() * 2 == kb and self.pos_pool.numel() * 4 == pb
+            assert self.k_pool.numel() * self.k_pool.element_size() == kb
+            assert self.pos_pool.numel() * 4 == pb
             self.cfg.k_pool = self.k_pool.data_ptr()
             self.cfg.v_pool = self.v_pool.data_ptr()
             self.cfg.pos_pool = self.pos_pool.data_ptr()

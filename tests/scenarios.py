@@ -13,6 +13,7 @@ import numpy as np
 
 from oracle import attention as oatt
 from oracle import evict as oev
+from oracle import fp8 as of8
 from oracle import pages as opg
 from paper_2602_22603_amd import workload as wl
 
@@ -38,6 +39,11 @@ def seq_view(store, seq, layers=None):
     k = kx[:, :, pages, slots, :].permute(2, 0, 1, 3)     # [L, NL, Hkv, D]
     v = vx[:, :, pages, slots, :].permute(2, 0, 1, 3)
     pos = store.pos_pool[pages, slots]
+    if getattr(store, "kv_fp8", False):  # E4M3 codes times the layer's scales
+        sc = store.kv_scales[layers].astype(np.float64)
+        kf = of8.decode(k.cpu().numpy()) * sc[None, :, 0, None, None]
+        vf = of8.decode(v.cpu().numpy()) * sc[None, :, 1, None, None]
+        return kf, vf, pos.cpu().numpy().astype(np.int64)
     return (wl.torch_bf16_to_f64(k), wl.torch_bf16_to_f64(v),
             pos.cpu().numpy().astype(np.int64))
 
@@ -47,7 +53,8 @@ def oracle_model_for(store, with_data=True):
                          store.max_pages_per_seq, layers=store.num_layers,
                          kv_heads=store.num_kv_heads, head_dim=store.head_dim,
                          with_data=with_data, evict_chunk_pages=store.evict_chunk_pages,
-                         evict_remap=store.evict_remap)
+                         evict_remap=store.evict_remap,
+                         kv_scales=getattr(store, "kv_scales", None))
 
 
 def run_tiny(sq, device="cuda", modes=None, with_oracle=True):
@@ -141,12 +148,13 @@ class Twin:
 
     def __init__(self, sq, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
                  max_seqs, max_pages_per_seq, seed=0, device="cuda", evict_chunk_pages=0,
-                 evict_remap=False):
+                 evict_remap=False, kv_scales=None):
         self.sq = sq
         self.device = device
         self.store = sq.Store(num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
                               max_seqs, max_pages_per_seq, device=device,
-                              evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap)
+                              evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap,
+                              kv_scales=kv_scales)
         self.model = oracle_model_for(self.store)
         self.rng = np.random.default_rng([2602, 900, seed])
         self.nl, self.hq, self.hkv, self.d = num_layers, num_q_heads, num_kv_heads, head_dim
