@@ -54,7 +54,7 @@ def parse_args():
     return ap.parse_args()
 
 
-DECODE_SOURCES = ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp")
+DECODE_SOURCES = ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp", "fp8.hpp")
 EXTEND_SOURCES = ("extend_kernels.hip", "extend_args.hpp", "sq_common.hpp")
 
 
