@@ -502,9 +502,15 @@ __device__ inline void load_v(VFrag<D> &f, __amdgpu_buffer_rsrc_t r, int lane_of
 }
 
 // The same fragments in an 8-bit store (E4M3 codes, half the bytes); they
-// become bf16 fragments just before the matrix-core instructions.
+// become bf16 fragments just before the matrix-core instructions.  A K lane
+// loads 16 contiguous codes, channels 16 kg + 64 s' .. +16 of token n, in
+// one request (a token's row is read in full-line halves, as in bf16); its
+// two 8-channel halves feed QK chunks 2 s' and 2 s' + 1, and the query
+// fragments take the same channels, so each chunk still pairs q and k
+// channel by channel (the dot product is a sum over a permutation of the
+// channels).
 template <int D> struct KFrag8 {
-  uint2 k[D / 32];
+  uint4 k[D / 64];
 };
 template <int D> struct VFrag8 {
   uint32_t v[D / 16];
@@ -512,9 +518,9 @@ template <int D> struct VFrag8 {
 template <int D, bool NT>
 __device__ inline void load_k(KFrag8<D> &f, __amdgpu_buffer_rsrc_t r, int lane_off) {
 #pragma unroll
-  for (int s = 0; s < D / 32; ++s) {
-    const auto x = __builtin_amdgcn_raw_buffer_load_b64(r, lane_off + 32 * s, 0, kAux<NT>);
-    f.k[s] = make_uint2(x[0], x[1]);
+  for (int s = 0; s < D / 64; ++s) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + 64 * s, 0, kAux<NT>);
+    f.k[s] = make_uint4(x[0], x[1], x[2], x[3]);
   }
 }
 template <int D, bool NT>
@@ -526,9 +532,11 @@ __device__ inline void load_v(VFrag8<D> &f, __amdgpu_buffer_rsrc_t r, int lane_o
 template <int D> __device__ inline KFrag<D> to_bf16(const KFrag8<D> &f) {
   KFrag<D> o;
 #pragma unroll
-  for (int s = 0; s < D / 32; ++s) {
-    const uint2 lo = e4m3x4_to_bf16(f.k[s].x), hi = e4m3x4_to_bf16(f.k[s].y);
-    o.k[s] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  for (int s = 0; s < D / 64; ++s) {
+    const uint2 a = e4m3x4_to_bf16(f.k[s].x), b = e4m3x4_to_bf16(f.k[s].y);
+    const uint2 c = e4m3x4_to_bf16(f.k[s].z), d = e4m3x4_to_bf16(f.k[s].w);
+    o.k[2 * s] = make_uint4(a.x, a.y, b.x, b.y);
+    o.k[2 * s + 1] = make_uint4(c.x, c.y, d.x, d.y);
   }
   return o;
 }
@@ -653,8 +661,10 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     const uint16_t *qp = a.q + ((int64_t)bq * a.hq + g * G + n % G) * D;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-      // rows past nrows read member 0's row (in bounds) and are zeroed
-      uint4 w = *reinterpret_cast<const uint4 *>(qp + 8 * kg + 32 * s);
+      // rows past nrows read member 0's row (in bounds) and are zeroed; an
+      // 8-bit store's chunk s takes the channels its K fragments hold
+      const int c0 = KV8 ? 16 * kg + 64 * (s >> 1) + 8 * (s & 1) : 8 * kg + 32 * s;
+      uint4 w = *reinterpret_cast<const uint4 *>(qp + c0);
       if (!qvalid) w = make_uint4(0, 0, 0, 0);
       qb[s] = __builtin_bit_cast(bf16x8_t, w);
     }
@@ -668,7 +678,7 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   constexpr int ES = KV8 ? 1 : 2; // bytes per element
   const char *khead = reinterpret_cast<const char *>(a.k) + (int64_t)g * a.head_stride * ES;
   const char *vhead = reinterpret_cast<const char *>(a.v) + (int64_t)g * a.head_stride * ES;
-  const int koff = (n * D + 8 * kg) * ES; // byte offsets within a page
+  const int koff = KV8 ? n * D + 16 * kg : (n * D + 8 * kg) * ES; // byte offsets within a page
   const int voff = (n * P + 4 * kg) * ES;
   constexpr int kPageBytes = P * D * ES;
   // Wave w takes the w-th of kWaves contiguous shares of the piece's pages.
