@@ -98,7 +98,7 @@ typedef enum {
                                      reads code * scale.  Decode and steps run
                                      on the MFMA tile only (SQ_ATTN_STREAM is
                                      rejected, other modes read every segment
-                                     on it); sq_extend_attn is rejected. */
+                                     on it). */
 
 /* sq_decode_attn modes */
 #define SQ_ATTN_AUTO 0          /* shared-prefix tiles where queries share

@@ -48,6 +48,8 @@ struct ExtendArgs {
   // holds bit s = slot s of its page i attended; read only when masked.
   const int32_t *mask_row;
   int32_t masked;
+  int32_t kv8;        // 1: the pools hold E4M3 codes (K scale in scale_log2)
+  float out_scale;    // the layer's V scale in an 8-bit store (1 otherwise)
   int32_t pad;
 };
 

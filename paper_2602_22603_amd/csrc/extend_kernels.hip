@@ -36,6 +36,7 @@
 #include <hip/hip_bf16.h>
 
 #include "extend_args.hpp"
+#include "fp8.hpp"
 
 namespace sq {
 namespace {
@@ -160,6 +161,49 @@ __device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
     __builtin_amdgcn_global_load_lds(
         vbase + (int64_t)pick4(ids, j >> 1) * a.page_stride + d * kPage + 8 * (j & 1),
         (lds_void *)(sv + ins * 512), 16, 0, 0);
+  }
+}
+
+// An 8-bit store: the same block through registers.  ext_load8 loads the 8
+// codes each lane's DMA would have copied as 8 bf16 values (half the bytes);
+// ext_store8 converts them and writes the bf16 tile exactly where the DMA
+// writes it, so the compute is unchanged.
+template <int D>
+__device__ inline void ext_load8(uint2 (&kr)[ExtLayout<D>::NK], uint2 (&vr)[ExtLayout<D>::NV],
+                                 const ExtendArgs &a, const uint8_t *kbase, const uint8_t *vbase,
+                                 const int32_t (&ids)[4], int wave, int lane) {
+  using Lt = ExtLayout<D>;
+#pragma unroll
+  for (int u = 0; u < Lt::NK; ++u) {
+    const int ins = wave * Lt::NK + u;
+    const int row = ins * Lt::KROWS + lane / Lt::CH;
+    const int c = k_phys<D>(row, lane % Lt::CH);
+    const int p = (ins * Lt::KROWS) / kPage;
+    kr[u] = *reinterpret_cast<const uint2 *>(kbase + (int64_t)pick4(ids, p) * a.page_stride +
+                                             (row % kPage) * D + 8 * c);
+  }
+#pragma unroll
+  for (int u = 0; u < Lt::NV; ++u) {
+    const int ins = wave * Lt::NV + u;
+    const int d = ins * 8 + lane / 8;
+    const int j = v_phys(d, lane % 8);
+    vr[u] = *reinterpret_cast<const uint2 *>(vbase + (int64_t)pick4(ids, j >> 1) * a.page_stride +
+                                             d * kPage + 8 * (j & 1));
+  }
+}
+template <int D>
+__device__ inline void ext_store8(uint16_t *sk, uint16_t *sv, const uint2 (&kr)[ExtLayout<D>::NK],
+                                  const uint2 (&vr)[ExtLayout<D>::NV], int wave, int lane) {
+  using Lt = ExtLayout<D>;
+#pragma unroll
+  for (int u = 0; u < Lt::NK; ++u) {
+    const uint2 lo = e4m3x4_to_bf16(kr[u].x), hi = e4m3x4_to_bf16(kr[u].y);
+    *reinterpret_cast<uint4 *>(sk + (wave * Lt::NK + u) * 512 + lane * 8) = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  }
+#pragma unroll
+  for (int u = 0; u < Lt::NV; ++u) {
+    const uint2 lo = e4m3x4_to_bf16(vr[u].x), hi = e4m3x4_to_bf16(vr[u].y);
+    *reinterpret_cast<uint4 *>(sv + (wave * Lt::NV + u) * 512 + lane * 8) = make_uint4(lo.x, lo.y, hi.x, hi.y);
   }
 }
 
@@ -296,7 +340,7 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
   }
 }
 
-template <int D, int G>
+template <int D, int G, bool KV8 = false>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(EXT_WAVES_PER_EU, EXT_WAVES_PER_EU))) void
 k_extend(ExtendArgs a) {
   using Lt = ExtLayout<D>;
@@ -354,10 +398,18 @@ k_extend(ExtendArgs a) {
 
   const uint16_t *kbase = a.k + (int64_t)g * a.head_stride;
   const uint16_t *vbase = a.v + (int64_t)g * a.head_stride;
+  const uint8_t *kbase8 = reinterpret_cast<const uint8_t *>(a.k) + (int64_t)g * a.head_stride;
+  const uint8_t *vbase8 = reinterpret_cast<const uint8_t *>(a.v) + (int64_t)g * a.head_stride;
+  uint2 kr[Lt::NK], vr[Lt::NV]; // an 8-bit store's next block, in flight
   int32_t ids[4];
   if (b_lo < b_hi) {
     block_ids(ids, a, b_lo);
-    ext_dma<D>(sk[b_lo & 1], sv[b_lo & 1], a, kbase, vbase, ids, wave, lane);
+    if constexpr (KV8) {
+      ext_load8<D>(kr, vr, a, kbase8, vbase8, ids, wave, lane);
+      ext_store8<D>(sk[b_lo & 1], sv[b_lo & 1], kr, vr, wave, lane);
+    } else {
+      ext_dma<D>(sk[b_lo & 1], sv[b_lo & 1], a, kbase, vbase, ids, wave, lane);
+    }
     block_ids(ids, a, b_lo + 1);
   }
   for (int b = b_lo; b < b_hi; ++b) {
@@ -391,12 +443,19 @@ k_extend(ExtendArgs a) {
       __syncthreads();
     }
     if (b + 1 < b_hi) {
-      ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, ids, wave, lane);
+      if constexpr (KV8) {
+        ext_load8<D>(kr, vr, a, kbase8, vbase8, ids, wave, lane); // stored after this block
+      } else {
+        ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, ids, wave, lane);
+      }
       block_ids(ids, a, b + 2);
     }
     ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2,
                  b * BK + BK - 1 > mask_from || b * BK < mask_below || masked_here, qf, first, lim,
                  lm, acc, m_run, l_run);
+    if constexpr (KV8) { // the other buffer, which every wave left at the top of this block
+      if (b + 1 < b_hi) ext_store8<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], kr, vr, wave, lane);
+    }
   }
 
   if (a.n_split > 1) {
@@ -432,7 +491,7 @@ k_extend(ExtendArgs a) {
       sc = exp2_fast(m_run[cg] - big);
       l = fmaf(l, sc, exp2_fast(sk_l2 - big));
     }
-    const float inv = sc / l;
+    const float inv = sc / l * a.out_scale;
     float *op = a.out + ((int64_t)jrow[cg] * a.hq + hrow[cg]) * D + 4 * kg;
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
@@ -495,11 +554,21 @@ __global__ __launch_bounds__(256) void k_extend_merge(ExtendArgs a) {
   }
   float *op = a.out + r * D + lane * DPT;
 #pragma unroll
-  for (int q = 0; q < DPT; ++q) op[q] = num[q] / den;
+  for (int q = 0; q < DPT; ++q) op[q] = num[q] / den * a.out_scale;
 }
 
 template <int D> hipError_t extend_dispatch(int group, const ExtendArgs &a, hipStream_t s) {
   const dim3 grid((unsigned)a.n_qblocks * (unsigned)a.hkv * (unsigned)a.n_split), block(kThreads);
+  if (a.kv8) {
+    switch (group) {
+    case 1: hipLaunchKernelGGL((k_extend<D, 1, true>), grid, block, 0, s, a); break;
+    case 2: hipLaunchKernelGGL((k_extend<D, 2, true>), grid, block, 0, s, a); break;
+    case 4: hipLaunchKernelGGL((k_extend<D, 4, true>), grid, block, 0, s, a); break;
+    case 8: hipLaunchKernelGGL((k_extend<D, 8, true>), grid, block, 0, s, a); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (group) {
   case 1: hipLaunchKernelGGL((k_extend<D, 1>), grid, block, 0, s, a); break;
   case 2: hipLaunchKernelGGL((k_extend<D, 2>), grid, block, 0, s, a); break;

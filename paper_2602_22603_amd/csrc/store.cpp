@@ -1798,11 +1798,12 @@ sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_ne
   a.hkv = s->cfg.num_kv_heads;
   const int tq = sq::kExtRows / s->G;
   a.n_qblocks = (n_new + tq - 1) / tq;
-  a.scale_log2 = (float)((double)scale * 1.4426950408889634);
+  a.scale_log2 = (float)((double)scale * 1.4426950408889634 * (double)s->k_scale(layer));
   a.sinks = o.sinks;
   a.window = o.window;
   a.sink_scale = 1.4426950408889634f;
-  if (s->kv8) return fail(SQ_ERR_INVALID, "extend attention over an 8-bit store is not supported");
+  a.kv8 = s->kv8 ? 1 : 0;
+  a.out_scale = s->v_scale(layer);
   a.mask_row = s->mask_row(seq);
   a.masked = sqn->n_masked > 0 ? 1 : 0;
   if (a.masked && o.window > 0)

@@ -121,7 +121,7 @@ def test_fp8_decode_fork_evict(sq, hq, hkv, d):
     """Main thread, its fork (aligned and mid-page), eviction while the
     branch lives and a deferred eviction: pools equal the oracle's values bit
     for bit, attention in AUTO, SHARED_PREFIX and MFMA mode within 5e-4;
-    STREAM mode and extend are refused."""
+    STREAM mode is refused."""
     import torch
     t = sc.Twin(sq, 2, hq, hkv, d, 400, 6, 80, seed=710 + hq + d, kv_scales=_scales(2))
     main = t.create()
@@ -147,9 +147,36 @@ def test_fp8_decode_fork_evict(sq, hq, hkv, d):
     q = wl.device_normal_bf16((3, hq, d), 1, "cuda")
     with pytest.raises(sq.SqError):
         t.store.decode(0, [main, aux, mid], q, mode=sq.ATTN_STREAM)
-    with pytest.raises(sq.SqError):
-        t.store.extend(0, main, q[:1])
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64), (64, 8, 64)])
+@pytest.mark.parametrize("prefix,n,window", [(0, 45, 0), (250, 130, 0), (600, 300, 50),
+                                             (9000, 7, 0)])
+def test_fp8_extend(sq, hq, hkv, d, prefix, n, window):
+    """Extend over an 8-bit store (codes converted as each block is staged):
+    one launch, several query blocks, a window, a split key range; sinks."""
+    import math
+    import torch
+    from oracle import extend as oex
+    t = sc.Twin(sq, 2, hq, hkv, d, (prefix + n) // 16 + 24, 2, (prefix + n) // 16 + 8,
+                seed=740 + prefix + n, kv_scales=_scales(2))
+    a = t.create()
+    if prefix:
+        t.append(a, prefix)
+    t.append(a, n)
+    sinks = t.sinks()
+    qb = wl.normal_bf16(t.rng, (n, hq, d))
+    for layer in (0, 1):
+        out = t.store.extend(layer, a, wl.to_torch_bf16(qb, "cuda"), window=window,
+                             sinks=torch.from_numpy(sinks).to("cuda"))
+        torch.cuda.synchronize()
+        k, v, _ = t.model.view(a)
+        ref = oex.extend_attention(wl.bf16_value(qb), k[:, layer], v[:, layer], 1 / math.sqrt(d),
+                                   hq // hkv, window=window, sinks=sinks.astype(np.float64))
+        err = float(np.max(np.abs(out.cpu().numpy() - ref)))
+        print(f"fp8 extend layer={layer} prefix={prefix} n={n} window={window}: {err:.2e}")
+        assert err <= TOL
 
 
 @pytest.mark.parametrize("mi", [0, 2, 3])
