@@ -539,7 +539,8 @@ def fp8_leg(sq, torch, wl, steps=20, warmup=3):
     append + attention per step."""
     from paper_2602_22603_amd import drivers
     total = steps + warmup
-    store, seqs, _ = drivers.build_shared128k(keep_inputs=(), extra_tokens=2 * total + 16,
+    chunk = 2048
+    store, seqs, _ = drivers.build_shared128k(keep_inputs=(), extra_tokens=2 * total + 16 + chunk,
                                               kv_scales=[[0.011, 0.0095]])
     B = len(seqs)
     kb = [wl.device_normal_bf16((1, B, 8, 128), 800 + 3 * i, "cuda") for i in range(total)]
@@ -549,6 +550,18 @@ def fp8_leg(sq, torch, wl, steps=20, warmup=3):
     r = time_steps(sq, torch, store, seqs, sq.ATTN_AUTO, steps, warmup, kb, vb, qs, out)
     prof, plan = r["prof"], r["plan"]
     kern = prof["decode_mfma_ms"] / max(1, prof["decode_mfma_launches"])
+    # a 2048-token chunk appended to one main thread (131K prefix), extended
+    kn = wl.device_normal_bf16((1, chunk, 8, 128), 890, "cuda")
+    store.append(seqs[0], kn, kn)
+    qx = wl.device_normal_bf16((chunk, 32, 128), 891, "cuda")
+    ox = torch.empty((chunk, 32, 128), dtype=torch.float32, device="cuda")
+    call = lambda: store.extend(0, seqs[0], qx, out=ox)
+    for _ in range(2):
+        call()
+    ext = time_events(torch, call, 5)
+    L = store.seq_info(seqs[0])["length"]
+    pairs = chunk * (L - chunk) + chunk * (chunk + 1) // 2
+    ext_tflops = 32 * 4 * 128 * pairs / (ext["median"] * 1e-3) / 1e12
     store.close()
     return dict(workload="8 tasks x (main 131072 + forked aux 130816+512) tokens, 16-query step "
                          "(append + attention), 32q/8kv heads, head_dim 128, E4M3 K/V",
@@ -557,7 +570,8 @@ def fp8_leg(sq, torch, wl, steps=20, warmup=3):
                 kv_bytes_per_step=r["kv_bytes_per_step"], kernel_ms=round(kern, 5),
                 kernel_gbps=round(plan["kv_bytes_mfma"] / (kern * 1e-3) / 1e9, 1),
                 kernel_frac_of_hbm_peak=round(plan["kv_bytes_mfma"] / (kern * 1e-3) / 1e9 /
-                                              HBM_PEAK_GBPS, 4))
+                                              HBM_PEAK_GBPS, 4),
+                extend_2048_over_131k=dict(call_ms=ext, useful_tflops=round(ext_tflops, 1)))
 
 
 def fullstack_leg(sq, torch, wl):
