@@ -308,6 +308,45 @@ def test_deferred_run_limit(sq):
     assert s.spans(a) == {sq.MAX_EVICT_SPANS: (sq.MAX_EVICT_SPANS + 1, sq.MAX_EVICT_SPANS + 2)}
 
 
+def test_new_entry_point_errors(sq):
+    """Deferred eviction, compaction, keep flags and 8-bit configurations
+    reject bad arguments without changing anything."""
+    import ctypes as C
+    s = _store(sq, 16, 4, 2, 8)
+    a = s.seq_create()
+    s.append(a, n=10)
+    s.span_mark(a, 0, 2, 5)
+    before = (s.page_table(a), s.spans(a), s.keep_flags(a).tolist(), s.stats())
+    es = sq.EvictStats()
+    ids = (C.c_int32 * 1)(0)
+    assert sq.lib().sq_evict_spans_ex(s._handle, a, ids, 1, 2, None, C.byref(es)) == sq.ERR_INVALID
+    assert b"flags" in sq.lib().sq_last_error()
+    bad = (C.c_int32 * 1)(7)
+    assert sq.lib().sq_evict_spans_ex(s._handle, a, bad, 1, sq.EVICT_DEFER, None,
+                                      C.byref(es)) == sq.ERR_UNKNOWN_CURSOR
+    assert sq.lib().sq_compact(s._handle, 9, None, C.byref(es)) == sq.ERR_UNKNOWN_SEQ
+    n = C.c_int64()
+    assert sq.lib().sq_keep_flags(s._handle, a, None, 4, C.byref(n)) == sq.ERR_INVALID
+    assert sq.lib().sq_keep_flags(s._handle, 9, None, 0, C.byref(n)) == sq.ERR_UNKNOWN_SEQ
+    assert before == (s.page_table(a), s.spans(a), s.keep_flags(a).tolist(), s.stats())
+    st = s.compact(a)                      # nothing masked: nothing to do
+    assert st["tokens_removed"] == 0 and s.page_table(a) == before[0]
+    # an 8-bit store needs finite positive scales (checked in every mode)
+    cfg = sq.StoreConfig(2, 4, 2, 8, 4, 16, 2, 8)
+    cfg.flags = sq.STORE_METADATA_ONLY | sq.STORE_KV_FP8
+    h = C.c_void_p()
+    assert sq.lib().sq_store_create(C.byref(cfg), C.byref(h)) == sq.ERR_INVALID  # no scales
+    for vals in ([1.0, 1.0, 0.0, 1.0], [1.0, float("inf"), 1.0, 1.0]):
+        sc = (C.c_float * 4)(*vals)
+        cfg.kv_scales = C.cast(sc, C.c_void_p)
+        assert sq.lib().sq_store_create(C.byref(cfg), C.byref(h)) == sq.ERR_INVALID
+    sc = (C.c_float * 4)(0.5, 0.25, 1.0, 2.0)
+    cfg.kv_scales = C.cast(sc, C.c_void_p)
+    assert sq.lib().sq_store_create(C.byref(cfg), C.byref(h)) == sq.OK
+    assert sq.lib().sq_pool_bytes(C.byref(cfg), 0) == 2 * 16 * 2 * 4 * 8  # one byte per element
+    sq.lib().sq_store_destroy(h)
+
+
 def test_attention_options_are_checked_first(sq):
     """sq_attn_opts errors (negative window, reserved field, misaligned
     sinks) are reported before anything else and change nothing; a windowed
