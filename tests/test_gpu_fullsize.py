@@ -105,6 +105,51 @@ def test_shared128k_sampled_heads(sq):
     store.close()
 
 
+def test_shared128k_fp8_sampled_heads(sq):
+    """The 8-bit store's decode step at full size (the bench's kv_fp8 leg):
+    sampled heads against the oracle over the round-tripped K/V, and the
+    stored codes of those heads against the oracle's quantisation."""
+    import torch
+    from oracle import fp8 as of8
+    from paper_2602_22603_amd import drivers
+    scales = np.array([[0.011, 0.0095]], dtype=np.float32)
+    store, seqs, inputs = drivers.build_shared128k(keep_inputs=(0,), kv_scales=scales)
+    rng = np.random.default_rng([2602, 2, 12])
+    qb = wl.normal_bf16(rng, (16, 32, 128))
+    q = wl.to_torch_bf16(qb, "cuda")
+    qf = wl.bf16_value(qb)
+    scale = 1 / math.sqrt(128)
+    k, v, ka, va = inputs[0]
+    fork_at = k.shape[1] - 256
+    main_k, main_v = k[0], v[0]
+    pt = store.page_table(seqs[0])
+    refs = {}
+    g = 5  # one KV head (the round trip of 16.7M values takes the oracle ~15 s)
+    rk = of8.roundtrip(wl.torch_bf16_to_f64(main_k[:, g: g + 1]), scales[0, 0])
+    rv = of8.roundtrip(wl.torch_bf16_to_f64(main_v[:, g: g + 1]), scales[0, 1])
+    refs[(0, g)] = oatt.attention(qf[0][4 * g: 4 * g + 4], rk, rv, scale, 4)
+    # the branch: the shared prefix's round trip, then its own tokens'
+    ak = np.concatenate([rk[:fork_at], of8.roundtrip(wl.torch_bf16_to_f64(ka[0][:, g: g + 1]),
+                                                     scales[0, 0])])
+    av = np.concatenate([rv[:fork_at], of8.roundtrip(wl.torch_bf16_to_f64(va[0][:, g: g + 1]),
+                                                     scales[0, 1])])
+    refs[(1, g)] = oatt.attention(qf[1][4 * g: 4 * g + 4], ak, av, scale, 4)
+    for mode in (sq.ATTN_AUTO, sq.ATTN_MFMA):
+        out = store.decode(0, seqs, q, mode=mode)
+        torch.cuda.synchronize()
+        o = out.cpu().numpy()
+        for (b, g), ref in refs.items():
+            err = sc.max_abs(o[b, 4 * g: 4 * g + 4], ref)
+            assert err <= TOL, (mode, b, g, err)
+    # codes of KV head 5 of the main thread's first and last pages
+    for i in (0, len(pt) - 1):
+        got = store.k_pool[0, 5, pt[i]].cpu().numpy()
+        toks = main_k[16 * i: 16 * i + 16, 5]
+        want = of8.quantize(wl.torch_bf16_to_f64(toks), scales[0, 0])
+        assert np.array_equal(got[: len(want)], want), i
+    store.close()
+
+
 def test_outlier32k_evict_and_steps(sq):
     import torch
     from paper_2602_22603_amd import drivers
