@@ -89,9 +89,12 @@ def test_deferred_fork_shares_masks_and_pages(sq):
     t.evict(main, [1, 4], deferred=True)
     late = t.fork(main, 896)
     t.append(late, 40)
+    mid = t.fork(main, 310)            # mid-page, inside the masked span [300, 517)
+    t.append(mid, 9)
+    assert t.store.keep_flags(mid).tolist()[300:310] == [0] * 10
     t.check_state()
     for _ in range(2):
-        errs, _ = t.decode_errors([main, early, late])
+        errs, _ = t.decode_errors([main, early, late, mid])
         assert max(errs.values()) <= TOL, errs
     plan = t.store.plan_info([main, late], t.sq.ATTN_AUTO)
     assert plan["n_groups"] >= 1
