@@ -272,9 +272,12 @@ struct sq_store {
   bool staging_pending = false;
   hipStream_t last_stream = nullptr;
   sq::StepPlan *step_dev = nullptr;     // the step plan in the workspace
-  sq::StepPlan *step_staging = nullptr; // its pinned host copy
-  hipEvent_t step_ev = nullptr;
-  bool step_pending = false;
+  // two pinned host copies of the plan, used in turn: a step waits only for
+  // the upload of the step before the last, so the host runs a step ahead
+  sq::StepPlan *step_staging[2] = {nullptr, nullptr};
+  hipEvent_t step_ev[2] = {nullptr, nullptr};
+  bool step_pending[2] = {false, false};
+  int step_buf = 0;
   bool have_last_evict = false;
   int64_t last_evict_L = 0, last_evict_Lp = 0;
 
@@ -855,16 +858,21 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
       delete s;
       return hip_fail(e, "hipEventCreate");
     }
-    void *sh = nullptr;
-    e = hipHostMalloc(&sh, sizeof(sq::StepPlan), hipHostMallocDefault);
-    if (e == hipSuccess) {
-      s->step_staging = static_cast<sq::StepPlan *>(sh);
-      e = hipEventCreateWithFlags(&s->step_ev, hipEventDisableTiming);
+    for (int i = 0; i < 2 && e == hipSuccess; ++i) {
+      void *sh = nullptr;
+      e = hipHostMalloc(&sh, sizeof(sq::StepPlan), hipHostMallocDefault);
+      if (e == hipSuccess) {
+        s->step_staging[i] = static_cast<sq::StepPlan *>(sh);
+        e = hipEventCreateWithFlags(&s->step_ev[i], hipEventDisableTiming);
+      }
     }
     if (e != hipSuccess) {
       (void)hipEventDestroy(s->staging_ev);
       (void)hipHostFree(host);
-      if (sh) (void)hipHostFree(sh);
+      for (int i = 0; i < 2; ++i) {
+        if (s->step_staging[i]) (void)hipHostFree(s->step_staging[i]);
+        if (s->step_ev[i]) (void)hipEventDestroy(s->step_ev[i]);
+      }
       delete s;
       return hip_fail(e, "step plan staging");
     }
@@ -885,9 +893,11 @@ sq_status sq_store_destroy(sq_store *s) {
     for (hipEvent_t e : s->ev_pool) (void)hipEventDestroy(e);
     if (s->staging_ev) (void)hipEventDestroy(s->staging_ev);
     if (s->staging) (void)hipHostFree(s->staging);
-    if (s->step_pending) (void)hipEventSynchronize(s->step_ev);
-    if (s->step_ev) (void)hipEventDestroy(s->step_ev);
-    if (s->step_staging) (void)hipHostFree(s->step_staging);
+    for (int i = 0; i < 2; ++i) {
+      if (s->step_pending[i]) (void)hipEventSynchronize(s->step_ev[i]);
+      if (s->step_ev[i]) (void)hipEventDestroy(s->step_ev[i]);
+      if (s->step_staging[i]) (void)hipHostFree(s->step_staging[i]);
+    }
   }
   delete s;
   return SQ_OK;
@@ -1629,12 +1639,13 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   for (int L = 0; L < 2; ++L)
     if ((plan.n_wg[L] > 0 || plan_w.n_wg[L] > 0) && !launch[L])
       return fail(SQ_ERR_INVALID, "internal: step plan needs an unlaunched kernel");
-  if (s->device && s->step_pending) { // the staging copy of the last step's plan
-    hipError_t e = hipEventSynchronize(s->step_ev);
+  const int sb = s->step_buf;
+  if (s->device && s->step_pending[sb]) { // this staging copy's last upload
+    hipError_t e = hipEventSynchronize(s->step_ev[sb]);
     if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize(step plan)");
-    s->step_pending = false;
+    s->step_pending[sb] = false;
   }
-  sq::StepPlan *sp = s->device ? s->step_staging : nullptr;
+  sq::StepPlan *sp = s->device ? s->step_staging[sb] : nullptr;
   if (sp) {
     std::memset(sp, 0, sizeof(*sp));
     fill_dyn(s, plan, sp->dec, &sp->merge);
@@ -1687,9 +1698,10 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   if (e != hipSuccess) return hip_fail(e, "page-table entries");
   e = hipMemcpyAsync(s->step_dev, sp, sizeof(*sp), hipMemcpyHostToDevice, strm);
   if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync(step plan)");
-  e = hipEventRecord(s->step_ev, strm);
+  e = hipEventRecord(s->step_ev[sb], strm);
   if (e != hipSuccess) return hip_fail(e, "hipEventRecord(step plan)");
-  s->step_pending = true;
+  s->step_pending[sb] = true;
+  s->step_buf = 1 - sb;
   return SQ_OK;
 }
 
