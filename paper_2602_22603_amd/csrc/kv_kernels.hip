@@ -329,21 +329,42 @@ __global__ __launch_bounds__(256) void k_write_ids(int32_t *dst, NewIds ids, int
 }
 
 // ---------------------------------------------------------------------------
-// Gather: block (fresh page pi0 + b, layer * Hkv + head) fills destination
-// page fp + pi0 + b with the kept tokens (fp + pi0 + b) * P + j, j < P, j
-// below L'.  Each comes from token src_of[t] of the old pages, whose ids the
+// Gather: a workgroup per (fresh page pi0 + b, layer * Hkv + head) fills
+// destination page fp + pi0 + b with the kept tokens (fp + pi0 + b) * P + j,
+// j < P, j below L'.  K rows move as 16-byte units; V^T rows are assembled
+// in LDS from the (at most four, usually one or two) source pages staged
+// whole with 16-byte loads, then written as 16-byte units (more source pages
+// fall back to element moves).  Each comes from token src_of[t] of the old pages, whose ids the
 // page-table row still holds (the new ids are written there after the last
 // gather).  A fresh page is never a page this or a later gather reads: it is
 // either a page nothing held or an old page whose tokens earlier gathers have
 // all moved, so nothing is read after being written.
 template <int D, class E>
 __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
-  constexpr int U = D * (int)sizeof(E) / 16; // 16-byte units per K row
+  constexpr int U = D * (int)sizeof(E) / 16;      // 16-byte units per K row
+  constexpr int VU = D * P * (int)sizeof(E) / 16; // 16-byte units of one page's V^T
+  constexpr int EPU = 16 / (int)sizeof(E);        // V^T elements per unit
+  constexpr int kMaxSrc = 4;                       // source pages staged in LDS
   __shared__ int spage[P];
   __shared__ int sslot[P];
+  __shared__ int sidx[P];  // the source's page index in the old list
   __shared__ int nvalid;
-  const int pi = a.pi0 + blockIdx.x;
-  const int lh = blockIdx.y;
+  __shared__ int upage[P]; // the distinct source pages, in order
+  __shared__ int uidx[P];  // slot j's source page in upage
+  __shared__ int n_up;
+  __shared__ uint4 vbuf[kMaxSrc][VU];
+  // Work item w = (KV row lh, tail page pl), page fastest.  Workgroups are
+  // dealt to the 8 XCDs in turn, so each XCD takes a contiguous range of
+  // w: neighbouring destination pages, which share source pages, then hit
+  // the same L2.
+  const int n = gridDim.x;
+  const int total = n * gridDim.y;
+  const int lin = blockIdx.x + blockIdx.y * n;
+  const int x = lin % 8, q = total / 8, r = total % 8;
+  const int w = x * q + min(x, r) + lin / 8;
+  const int pl = w % n;
+  const int lh = w / n;
+  const int pi = a.pi0 + pl;
   const int layer = lh / p.hkv;
   const int head = lh % p.hkv;
   const int t0 = (a.fp + pi) * P;
@@ -351,18 +372,28 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
     const int s0 = a.src_of[t0];
     if (s0 % P == 0 && a.src_of[t0 + P - 1] == s0 + P - 1) return; // remapped, not copied
   }
-  const int dst_page = new_page_id(a.ids, blockIdx.x);
+  const int dst_page = new_page_id(a.ids, pl);
   if (threadIdx.x < P) {
     const int t = t0 + threadIdx.x;
     if (t < a.new_len) {
       const int src = a.src_of[t];
       spage[threadIdx.x] = a.pt_row[src / P];
       sslot[threadIdx.x] = src % P;
+      sidx[threadIdx.x] = src / P;
     }
   }
   if (threadIdx.x == 0) nvalid = min(P, a.new_len - t0);
   __syncthreads();
   const int nv = nvalid;
+  if ((int)threadIdx.x < nv) {
+    // sources are in increasing old order, so slot j's source page is the
+    // number of page changes among slots 1..j
+    int f = 0;
+    for (int i = 1; i <= (int)threadIdx.x; ++i) f += sidx[i] != sidx[i - 1];
+    uidx[threadIdx.x] = f;
+    upage[f] = spage[threadIdx.x];
+    if ((int)threadIdx.x == nv - 1) n_up = f + 1;
+  }
 
   E *kd = chunk_of<E>(p.k, p, layer, dst_page, head);
   for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) {
@@ -371,10 +402,34 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
                                                       sslot[j] * D);
     *(reinterpret_cast<uint4 *>(kd + j * D) + u) = ks[u];
   }
+  __syncthreads();
+  const int nu = n_up;
   E *vd = chunk_of<E>(p.v, p, layer, dst_page, head);
-  for (int idx = threadIdx.x; idx < D * P; idx += blockDim.x) {
-    const int j = idx % P, d = idx / P;
-    if (j < nv) vd[d * P + j] = chunk_of<E>(p.v, p, layer, spage[j], head)[d * P + sslot[j]];
+  if (nu <= kMaxSrc) {
+    // stage the source pages' V^T (16-byte loads), then assemble each
+    // destination unit of EPU slots of one channel from LDS
+    for (int u = 0; u < nu; ++u) {
+      const uint4 *vs = reinterpret_cast<const uint4 *>(chunk_of<E>(p.v, p, layer, upage[u], head));
+      for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) vbuf[u][idx] = vs[idx];
+    }
+    __syncthreads();
+    for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) {
+      const int d = idx / (P / EPU), c = idx % (P / EPU);
+      E out[EPU];
+#pragma unroll
+      for (int e = 0; e < EPU; ++e) {
+        const int j = c * EPU + e;
+        out[e] = j < nv ? reinterpret_cast<const E *>(vbuf[uidx[j]])[d * P + sslot[j]] : (E)0;
+      }
+      uint4 o;
+      __builtin_memcpy(&o, out, 16);
+      *reinterpret_cast<uint4 *>(vd + d * P + c * EPU) = o;
+    }
+  } else {
+    for (int idx = threadIdx.x; idx < D * P; idx += blockDim.x) {
+      const int j = idx % P, d = idx / P;
+      if (j < nv) vd[d * P + j] = chunk_of<E>(p.v, p, layer, spage[j], head)[d * P + sslot[j]];
+    }
   }
   if (lh == 0 && threadIdx.x < nv)
     p.pos[(int64_t)dst_page * P + threadIdx.x] =
