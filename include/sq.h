@@ -95,10 +95,9 @@ typedef enum {
                                      float(x) * float(1 / scale) (ties to
                                      even, saturating at 448) with the
                                      layer's scale from kv_scales; attention
-                                     reads code * scale.  Decode and steps run
-                                     on the MFMA tile only (SQ_ATTN_STREAM is
-                                     rejected, other modes read every segment
-                                     on it). */
+                                     reads code * scale.  Every mode runs;
+                                     SQ_ATTN_AUTO reads every segment on the
+                                     MFMA tile. */
 
 /* sq_decode_attn modes */
 #define SQ_ATTN_AUTO 0          /* shared-prefix tiles where queries share

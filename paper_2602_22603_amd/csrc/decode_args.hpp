@@ -45,7 +45,7 @@ struct DecodeStatic {
   int32_t hkv;
   int32_t nontemporal; // 1: every page is read once in this launch
   float scale_log2;    // scale * log2(e) (times the layer's K scale in an 8-bit store)
-  int32_t kv8;         // 1: the pools hold E4M3 codes (MFMA kernels only)
+  int32_t kv8;         // 1: the pools hold E4M3 codes
 };
 
 // The plan of one launch.  It splits its flattened pages [0, total) evenly
@@ -167,8 +167,8 @@ hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const Deco
 hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
                             const DecodeDyn *dyn, int n_wg, hipStream_t s);
 hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8, hipStream_t s);
-// Workgroups of a decode kernel (kind 0: VALU, 1: MFMA) that fit on one CU.
-// kind: 0 VALU, 1 MFMA, 2 the 8-bit MFMA kernel (four waves)
+// Workgroups of a decode kernel that fit on one CU.  kind: 0 VALU, 1 MFMA,
+// 2 the 8-bit MFMA kernel (four waves), 3 the 8-bit VALU kernel
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out);
 
 } // namespace sq

@@ -12,7 +12,8 @@
 //   k_decode_valu  one query sequence per item: K and V page tiles staged in
 //                  LDS, bf16 dot products on the VALU (v_dot2_f32_bf16), the
 //                  online-softmax max and sum reduced with DPP and permlane
-//                  swaps.
+//                  swaps.  In an 8-bit store each lane loads 8 codes and
+//                  converts them to bf16 on the way into LDS.
 //   k_decode_mfma  up to four query sequences stacked as the 16 rows of an
 //                  MFMA tile against the same pages - the prefix the main
 //                  thread and its forked auxiliary thread share (§3.4 points
@@ -59,6 +60,16 @@ template <bool NT> __device__ inline u32x4_t ld_kv4(const uint16_t *p) {
   const u32x4_t *q = reinterpret_cast<const u32x4_t *>(p);
   if constexpr (NT) return __builtin_nontemporal_load(q);
   else return *q;
+}
+// Eight E4M3 codes (8 bytes) as eight bf16 values in one 16-byte register
+// group, element order kept.
+template <bool NT> __device__ inline u32x4_t ld_kv4_8(const uint8_t *p) {
+  const u32x2_t *q = reinterpret_cast<const u32x2_t *>(p);
+  u32x2_t x;
+  if constexpr (NT) x = __builtin_nontemporal_load(q);
+  else x = *q;
+  const uint2 lo = e4m3x4_to_bf16(x.x), hi = e4m3x4_to_bf16(x.y);
+  return u32x4_t{lo.x, lo.y, hi.x, hi.y};
 }
 template <bool NT> __device__ inline uint4 ld_stream(const uint16_t *p) {
   const u32x4_t x = ld_kv4<NT>(p);
@@ -211,7 +222,7 @@ __device__ inline bool next_piece(const PL &pl, int hkv, int w, int64_t &x, int6
 // LDS holds the page's K tile (row pitch 2D + 64 bytes) and V^T tile (groups
 // of D/16 channels, 32 bytes per channel, 32 bytes of padding per group), the
 // page's weights p[t][r] and the rescale factors alpha[r].
-template <int D, int G, bool NT, class PL>
+template <int D, int G, bool NT, class PL, bool KV8 = false>
 __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
   constexpr int KPITCH = 2 * D + 64;
   constexpr int DPL = D / 16;
@@ -260,17 +271,26 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
     l_run[k] = 0.f;
   }
 
+  // 8 elements per lane per load: 16 bytes of bf16, or 8 codes of an 8-bit
+  // store converted to bf16 as they arrive (strides count elements)
   const uint16_t *kbase = a.k + (int64_t)g * a.head_stride + lane * 8;
   const uint16_t *vbase = a.v + (int64_t)g * a.head_stride + lane * 8;
+  const uint8_t *kbase8 = reinterpret_cast<const uint8_t *>(a.k) + (int64_t)g * a.head_stride + lane * 8;
+  const uint8_t *vbase8 = reinterpret_cast<const uint8_t *>(a.v) + (int64_t)g * a.head_stride + lane * 8;
   u32x4_t kreg[NLD], vreg[NLD];
-  {
-    const int64_t off = (int64_t)pt[ip.pbeg] * a.page_stride;
+  auto load_page = [&](int64_t off) {
 #pragma unroll
     for (int i = 0; i < NLD; ++i) {
-      kreg[i] = ld_kv4<NT>(kbase + off + i * 512);
-      vreg[i] = ld_kv4<NT>(vbase + off + i * 512);
+      if constexpr (KV8) {
+        kreg[i] = ld_kv4_8<NT>(kbase8 + off + i * 512);
+        vreg[i] = ld_kv4_8<NT>(vbase8 + off + i * 512);
+      } else {
+        kreg[i] = ld_kv4<NT>(kbase + off + i * 512);
+        vreg[i] = ld_kv4<NT>(vbase + off + i * 512);
+      }
     }
-  }
+  };
+  load_page((int64_t)pt[ip.pbeg] * a.page_stride);
 
   for (int pg = ip.pbeg; pg < ip.pend; ++pg) {
     const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
@@ -287,14 +307,8 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
       *reinterpret_cast<u32x4_t *>(sV + (vd / DPL) * VGP + (vd % DPL) * 32 + vh * 16) = vreg[i];
     }
     __syncthreads();
-    if (pg + 1 < ip.pend) { // prefetch the next page while this one is used
-      const int64_t off = (int64_t)pt[pg + 1] * a.page_stride;
-#pragma unroll
-      for (int i = 0; i < NLD; ++i) {
-        kreg[i] = ld_kv4<NT>(kbase + off + i * 512);
-        vreg[i] = ld_kv4<NT>(vbase + off + i * 512);
-      }
-    }
+    if (pg + 1 < ip.pend) // prefetch the next page while this one is used
+      load_page((int64_t)pt[pg + 1] * a.page_stride);
 
     // scores: partial dot products over this lane's channels, then the quad
     float s[G];
@@ -429,13 +443,13 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
   } // pieces
 }
 
-template <int D, int G, bool NT>
+template <int D, int G, bool NT, bool KV8>
 __global__ __launch_bounds__(64) void k_decode_valu(DecodeArgs a) {
-  valu_body<D, G, NT>(a.st, ArgPlan{a.dyn});
+  valu_body<D, G, NT, ArgPlan, KV8>(a.st, ArgPlan{a.dyn});
 }
-template <int D, int G>
+template <int D, int G, bool KV8>
 __global__ __launch_bounds__(64) void k_step_valu(DecodeStatic a, const DecodeDyn *dyn) {
-  valu_body<D, G, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
+  valu_body<D, G, true, DevPlan, KV8>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
 }
 
 // ===========================================================================
@@ -1107,14 +1121,14 @@ template <int D> __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merg
   merge_body<D, true, DevMerge, StepMergeArgs, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a);
 }
 
-template <int D, bool NT>
+template <int D, bool NT, bool KV8>
 hipError_t valu_dispatch_nt(int group, const DecodeArgs &a, hipStream_t s) {
   const dim3 grid(a.dyn.n_wg), block(64);
   switch (group) {
-  case 1: hipLaunchKernelGGL((k_decode_valu<D, 1, NT>), grid, block, 0, s, a); break;
-  case 2: hipLaunchKernelGGL((k_decode_valu<D, 2, NT>), grid, block, 0, s, a); break;
-  case 4: hipLaunchKernelGGL((k_decode_valu<D, 4, NT>), grid, block, 0, s, a); break;
-  case 8: hipLaunchKernelGGL((k_decode_valu<D, 8, NT>), grid, block, 0, s, a); break;
+  case 1: hipLaunchKernelGGL((k_decode_valu<D, 1, NT, KV8>), grid, block, 0, s, a); break;
+  case 2: hipLaunchKernelGGL((k_decode_valu<D, 2, NT, KV8>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_decode_valu<D, 4, NT, KV8>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_decode_valu<D, 8, NT, KV8>), grid, block, 0, s, a); break;
   default: return hipErrorInvalidValue;
   }
   return hipGetLastError();
@@ -1122,8 +1136,11 @@ hipError_t valu_dispatch_nt(int group, const DecodeArgs &a, hipStream_t s) {
 
 template <int D>
 hipError_t valu_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
-  return a.st.nontemporal ? valu_dispatch_nt<D, true>(group, a, s)
-                       : valu_dispatch_nt<D, false>(group, a, s);
+  if (a.st.kv8)
+    return a.st.nontemporal ? valu_dispatch_nt<D, true, true>(group, a, s)
+                            : valu_dispatch_nt<D, false, true>(group, a, s);
+  return a.st.nontemporal ? valu_dispatch_nt<D, true, false>(group, a, s)
+                       : valu_dispatch_nt<D, false, false>(group, a, s);
 }
 
 template <int D, int W, bool NT, bool MK>
@@ -1178,12 +1195,12 @@ hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t 
 } // namespace
 
 namespace {
-template <int D> const void *valu_fn(int group) {
+template <int D, bool KV8> const void *valu_fn(int group) {
   switch (group) {
-  case 1: return reinterpret_cast<const void *>(&k_decode_valu<D, 1, true>);
-  case 2: return reinterpret_cast<const void *>(&k_decode_valu<D, 2, true>);
-  case 4: return reinterpret_cast<const void *>(&k_decode_valu<D, 4, true>);
-  case 8: return reinterpret_cast<const void *>(&k_decode_valu<D, 8, true>);
+  case 1: return reinterpret_cast<const void *>(&k_decode_valu<D, 1, true, KV8>);
+  case 2: return reinterpret_cast<const void *>(&k_decode_valu<D, 2, true, KV8>);
+  case 4: return reinterpret_cast<const void *>(&k_decode_valu<D, 4, true, KV8>);
+  case 8: return reinterpret_cast<const void *>(&k_decode_valu<D, 8, true, KV8>);
   default: return nullptr;
   }
 }
@@ -1212,11 +1229,12 @@ template <int D> const void *mfma_fn(int group, int waves) {
 } // namespace
 
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out) {
-  const void *fn = kind == 0   ? (d == 128 ? valu_fn<128>(group) : valu_fn<64>(group))
+  const void *fn = kind == 0   ? (d == 128 ? valu_fn<128, false>(group) : valu_fn<64, false>(group))
+                   : kind == 3 ? (d == 128 ? valu_fn<128, true>(group) : valu_fn<64, true>(group))
                    : kind == 2 ? (d == 128 ? mfma8_fn<128>(group) : mfma8_fn<64>(group))
                                : (d == 128 ? mfma_fn<128>(group, waves) : mfma_fn<64>(group, waves));
   if (!fn) return hipErrorInvalidValue;
-  const int block = kind == 0 ? 64 : 64 * waves;
+  const int block = kind == 0 || kind == 3 ? 64 : 64 * waves;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, fn, block, 0);
 }
 
@@ -1244,11 +1262,21 @@ template <int D>
 hipError_t step_valu_dispatch(int group, const DecodeStatic &st, const DecodeDyn *dyn, int n_wg,
                               hipStream_t s) {
   const dim3 grid(n_wg), block(64);
+  if (st.kv8) {
+    switch (group) {
+    case 1: hipLaunchKernelGGL((k_step_valu<D, 1, true>), grid, block, 0, s, st, dyn); break;
+    case 2: hipLaunchKernelGGL((k_step_valu<D, 2, true>), grid, block, 0, s, st, dyn); break;
+    case 4: hipLaunchKernelGGL((k_step_valu<D, 4, true>), grid, block, 0, s, st, dyn); break;
+    case 8: hipLaunchKernelGGL((k_step_valu<D, 8, true>), grid, block, 0, s, st, dyn); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+  }
   switch (group) {
-  case 1: hipLaunchKernelGGL((k_step_valu<D, 1>), grid, block, 0, s, st, dyn); break;
-  case 2: hipLaunchKernelGGL((k_step_valu<D, 2>), grid, block, 0, s, st, dyn); break;
-  case 4: hipLaunchKernelGGL((k_step_valu<D, 4>), grid, block, 0, s, st, dyn); break;
-  case 8: hipLaunchKernelGGL((k_step_valu<D, 8>), grid, block, 0, s, st, dyn); break;
+  case 1: hipLaunchKernelGGL((k_step_valu<D, 1, false>), grid, block, 0, s, st, dyn); break;
+  case 2: hipLaunchKernelGGL((k_step_valu<D, 2, false>), grid, block, 0, s, st, dyn); break;
+  case 4: hipLaunchKernelGGL((k_step_valu<D, 4, false>), grid, block, 0, s, st, dyn); break;
+  case 8: hipLaunchKernelGGL((k_step_valu<D, 8, false>), grid, block, 0, s, st, dyn); break;
   default: return hipErrorInvalidValue;
   }
   return hipGetLastError();

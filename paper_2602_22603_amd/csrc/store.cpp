@@ -486,8 +486,9 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes();
   const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
-  const bool single_mfma = mode == SQ_ATTN_MFMA || (mode == SQ_ATTN_AUTO && s->auto_single_mfma) ||
-                           s->kv8; // an 8-bit store reads everything on the MFMA tile
+  // AUTO in an 8-bit store reads every sequence on the MFMA tile
+  const bool single_mfma = mode == SQ_ATTN_MFMA ||
+                           (mode == SQ_ATTN_AUTO && (s->auto_single_mfma || s->kv8));
 
   auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
                      const std::vector<int> &members, int32_t tok0 = 0) {
@@ -840,7 +841,8 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
           hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
           cus > 0)
         s->cus = cus;
-      if (sq::decode_blocks_per_cu(0, s->D, s->G, 1, &nb) == hipSuccess && nb > 0) s->wg_per_cu[0] = nb;
+      if (sq::decode_blocks_per_cu(s->kv8 ? 3 : 0, s->D, s->G, 1, &nb) == hipSuccess && nb > 0)
+        s->wg_per_cu[0] = nb;
       nb = 0;
       if (sq::decode_blocks_per_cu(s->kv8 ? 2 : 1, s->D, s->G, s->mfma_waves, &nb) == hipSuccess && nb > 0)
         s->wg_per_cu[1] = nb;
@@ -1557,8 +1559,6 @@ sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int3
   if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
   if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
   if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
-  if (s && s->kv8 && mode == SQ_ATTN_STREAM)
-    return fail(SQ_ERR_INVALID, "an 8-bit store has no STREAM mode (the MFMA tile reads it)");
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
   if (!q || !out || !aligned16(q) || !aligned16(out))
     return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
@@ -1616,8 +1616,6 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   if (r != SQ_OK) return r;
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
   if (window < 0) return fail(SQ_ERR_INVALID, "window %d < 0", window);
-  if (s->kv8 && mode == SQ_ATTN_STREAM)
-    return fail(SQ_ERR_INVALID, "an 8-bit store has no STREAM mode (the MFMA tile reads it)");
   if (s->device && mode != SQ_ATTN_STREAM && s->mfma_waves != 4)
     return fail(SQ_ERR_INVALID, "decode steps need 4 waves per MFMA work item");
   // attention over the tokens before the step; the new ones join in the
@@ -1633,8 +1631,8 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   }
   // which launches a layer makes depends on the mode only, so that a
   // captured step replays for every later step of the same batch and mode
-  const bool launch[2] = {!s->kv8 && (mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
-                                       (mode == SQ_ATTN_AUTO && !s->auto_single_mfma)),
+  const bool launch[2] = {mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
+                              (mode == SQ_ATTN_AUTO && !s->auto_single_mfma && !s->kv8),
                           mode != SQ_ATTN_STREAM};
   for (int L = 0; L < 2; ++L)
     if ((plan.n_wg[L] > 0 || plan_w.n_wg[L] > 0) && !launch[L])

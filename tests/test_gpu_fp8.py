@@ -120,8 +120,8 @@ def test_appended_codes_are_the_oracle_quantisation(sq, d):
 def test_fp8_decode_fork_evict(sq, hq, hkv, d):
     """Main thread, its fork (aligned and mid-page), eviction while the
     branch lives and a deferred eviction: pools equal the oracle's values bit
-    for bit, attention in AUTO, SHARED_PREFIX and MFMA mode within 5e-4;
-    STREAM mode is refused."""
+    for bit, attention in every mode within 5e-4 (STREAM and the singletons
+    of SHARED_PREFIX read the codes on the VALU kernel)."""
     import torch
     t = sc.Twin(sq, 2, hq, hkv, d, 400, 6, 80, seed=710 + hq + d, kv_scales=_scales(2))
     main = t.create()
@@ -133,7 +133,7 @@ def test_fp8_decode_fork_evict(sq, hq, hkv, d):
     for c, (x, y) in enumerate([(10, 90), (200, 230), (400, 433)]):
         t.mark(main, c, x, y)
     t.check_state()
-    modes = [sq.ATTN_AUTO, sq.ATTN_SHARED_PREFIX, sq.ATTN_MFMA]
+    modes = [sq.ATTN_AUTO, sq.ATTN_STREAM, sq.ATTN_SHARED_PREFIX, sq.ATTN_MFMA]
     for layer in (0, 1):
         errs, _ = t.decode_errors([main, aux, mid], modes=modes, layer=layer)
         assert max(errs.values()) <= TOL, (layer, errs)
@@ -144,9 +144,8 @@ def test_fp8_decode_fork_evict(sq, hq, hkv, d):
     assert max(errs.values()) <= TOL, errs
     t.compact(main)
     t.check_state()
-    q = wl.device_normal_bf16((3, hq, d), 1, "cuda")
-    with pytest.raises(sq.SqError):
-        t.store.decode(0, [main, aux, mid], q, mode=sq.ATTN_STREAM)
+    errs, _ = t.decode_errors([main, aux, mid], modes=modes)
+    assert max(errs.values()) <= TOL, errs
     torch.cuda.synchronize()
 
 
@@ -179,7 +178,7 @@ def test_fp8_extend(sq, hq, hkv, d, prefix, n, window):
         assert err <= TOL
 
 
-@pytest.mark.parametrize("mi", [0, 2, 3])
+@pytest.mark.parametrize("mi", [0, 1, 2, 3])
 def test_fp8_steps(sq, mi):
     """Fused decode steps on an 8-bit store: the new token is stored as its
     codes in the merge and attended as stored (pools equal the oracle's after
@@ -198,8 +197,6 @@ def test_fp8_steps(sq, mi):
         err, _ = t.step(seqs, mode, window=24, layer_windows=[24, 0], sinks=sinks)
         assert err <= TOL, (r, err)
     t.check_state()
-    with pytest.raises(sq.SqError):
-        t.store.step_begin(seqs, sq.ATTN_STREAM)
 
 
 def test_fp8_captured_step_replays(sq):
