@@ -537,11 +537,19 @@ __device__ inline void load_k(KFrag8<D> &f, __amdgpu_buffer_rsrc_t r, int lane_o
     f.k[s] = make_uint4(x[0], x[1], x[2], x[3]);
   }
 }
+// A V lane loads the 16 codes of one channel row, c = 64 J + 16 kg + n, in
+// one request (four b32 requests would each carry 4 codes).  Word t of that
+// row (tokens 4t .. 4t+3) belongs to the lane with the same n in lane row t,
+// for matrix-core instruction 4 J + kg: a 4 x 4 transpose across the wave's
+// four lane rows, done as the fragment is converted.
 template <int D, bool NT>
 __device__ inline void load_v(VFrag8<D> &f, __amdgpu_buffer_rsrc_t r, int lane_off) {
 #pragma unroll
-  for (int j = 0; j < D / 16; ++j)
-    f.v[j] = __builtin_amdgcn_raw_buffer_load_b32(r, lane_off + 16 * P * j, 0, kAux<NT>);
+  for (int J = 0; J < D / 64; ++J) {
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, lane_off + 64 * P * J, 0, kAux<NT>);
+#pragma unroll
+    for (int t = 0; t < 4; ++t) f.v[4 * J + t] = x[t];
+  }
 }
 template <int D> __device__ inline KFrag<D> to_bf16(const KFrag8<D> &f) {
   KFrag<D> o;
@@ -564,10 +572,24 @@ template <int D> struct Frags<D, true> {
 };
 template <int D> __device__ inline const KFrag<D> &to_bf16(const KFrag<D> &f) { return f; }
 template <int D> __device__ inline const VFrag<D> &to_bf16(const VFrag<D> &f) { return f; }
+// Lane row r holds words w[0..3] of rows c = 64 J + 16 r + n; afterwards it
+// holds word r of those rows for r' = 0..3.  Swapping lane rows {0,1} with
+// {2,3} across word pairs (0,2) and (1,3) exchanges the off-diagonal 2 x 2
+// blocks; swapping odd with even lane rows across pairs (0,1) and (2,3)
+// transposes each block.
 template <int D> __device__ inline VFrag<D> to_bf16(const VFrag8<D> &f) {
   VFrag<D> o;
 #pragma unroll
-  for (int j = 0; j < D / 16; ++j) o.v[j] = e4m3x4_to_bf16(f.v[j]);
+  for (int J = 0; J < D / 64; ++J) {
+    const auto a = __builtin_amdgcn_permlane32_swap(f.v[4 * J], f.v[4 * J + 2], false, false);
+    const auto b = __builtin_amdgcn_permlane32_swap(f.v[4 * J + 1], f.v[4 * J + 3], false, false);
+    const auto c = __builtin_amdgcn_permlane16_swap(a[0], b[0], false, false);
+    const auto d = __builtin_amdgcn_permlane16_swap(a[1], b[1], false, false);
+    o.v[4 * J] = e4m3x4_to_bf16(c[0]);
+    o.v[4 * J + 1] = e4m3x4_to_bf16(c[1]);
+    o.v[4 * J + 2] = e4m3x4_to_bf16(d[0]);
+    o.v[4 * J + 3] = e4m3x4_to_bf16(d[1]);
+  }
   return o;
 }
 
@@ -693,7 +715,7 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   const char *khead = reinterpret_cast<const char *>(a.k) + (int64_t)g * a.head_stride * ES;
   const char *vhead = reinterpret_cast<const char *>(a.v) + (int64_t)g * a.head_stride * ES;
   const int koff = KV8 ? n * D + 16 * kg : (n * D + 8 * kg) * ES; // byte offsets within a page
-  const int voff = (n * P + 4 * kg) * ES;
+  const int voff = KV8 ? (16 * kg + n) * P : (n * P + 4 * kg) * ES;
   constexpr int kPageBytes = P * D * ES;
   // Wave w takes the w-th of kWaves contiguous shares of the piece's pages.
   // Two pages are in flight while one is computed: page j + 2's K is loaded
