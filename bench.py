@@ -536,11 +536,11 @@ def variants_leg(sq, torch, wl, reps=20, window=128):
 def fp8_leg(sq, torch, wl, steps=20, warmup=3):
     """The headline decode step on an 8-bit (E4M3) store: the same 128K
     shared-prefix batch, K/V scales 0.011 / 0.0095 (unit-variance K/V),
-    append + attention per step."""
+    append + attention per step; STREAM mode on the main threads alone."""
     from paper_2602_22603_amd import drivers
     total = steps + warmup
     chunk = 2048
-    store, seqs, _ = drivers.build_shared128k(keep_inputs=(), extra_tokens=2 * total + 16 + chunk,
+    store, seqs, _ = drivers.build_shared128k(keep_inputs=(), extra_tokens=3 * total + 16 + chunk,
                                               kv_scales=[[0.011, 0.0095]])
     B = len(seqs)
     kb = [wl.device_normal_bf16((1, B, 8, 128), 800 + 3 * i, "cuda") for i in range(total)]
@@ -550,6 +550,12 @@ def fp8_leg(sq, torch, wl, steps=20, warmup=3):
     r = time_steps(sq, torch, store, seqs, sq.ATTN_AUTO, steps, warmup, kb, vb, qs, out)
     prof, plan = r["prof"], r["plan"]
     kern = prof["decode_mfma_ms"] / max(1, prof["decode_mfma_launches"])
+    # STREAM mode (the VALU kernel) on the 8 main threads alone (unique pages)
+    mains = seqs[0::2]
+    rs = time_steps(sq, torch, store, mains, sq.ATTN_STREAM, steps, warmup,
+                    [x[:, 0::2].contiguous() for x in kb], [x[:, 0::2].contiguous() for x in vb],
+                    [x[0::2].contiguous() for x in qs], out[0::2].contiguous())
+    skern = rs["prof"]["decode_valu_ms"] / max(1, rs["prof"]["decode_valu_launches"])
     # a 2048-token chunk appended to one main thread (131K prefix), extended
     kn = wl.device_normal_bf16((1, chunk, 8, 128), 890, "cuda")
     store.append(seqs[0], kn, kn)
@@ -571,6 +577,9 @@ def fp8_leg(sq, torch, wl, steps=20, warmup=3):
                 kernel_gbps=round(plan["kv_bytes_mfma"] / (kern * 1e-3) / 1e9, 1),
                 kernel_frac_of_hbm_peak=round(plan["kv_bytes_mfma"] / (kern * 1e-3) / 1e9 /
                                               HBM_PEAK_GBPS, 4),
+                mains_only_stream_valu=dict(
+                    ms_per_step=round(rs["ms_per_step"], 4), kernel_ms=round(skern, 5),
+                    kernel_gbps=round(rs["kv_bytes_per_step"] / (skern * 1e-3) / 1e9, 1)),
                 extend_2048_over_131k=dict(call_ms=ext, useful_tflops=round(ext_tflops, 1)))
 
 
