@@ -55,7 +55,7 @@ def parse_args():
 
 
 DECODE_SOURCES = ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp", "fp8.hpp")
-EXTEND_SOURCES = ("extend_kernels.hip", "extend_args.hpp", "sq_common.hpp")
+EXTEND_SOURCES = ("extend_kernels.hip", "extend_args.hpp", "sq_common.hpp", "fp8.hpp")
 
 
 def kernel_sha(files=DECODE_SOURCES):
