@@ -107,8 +107,10 @@ def test_shared128k_sampled_heads(sq):
 
 def test_shared128k_fp8_sampled_heads(sq):
     """The 8-bit store's decode step at full size (the bench's kv_fp8 leg):
-    sampled heads against the oracle over the round-tripped K/V, and the
-    stored codes of those heads against the oracle's quantisation."""
+    sampled heads against the oracle over the round-tripped K/V in every
+    mode (STREAM on the VALU kernel, the branches' private suffixes too in
+    SHARED_PREFIX), and the stored codes of those heads against the
+    oracle's quantisation."""
     import torch
     from oracle import fp8 as of8
     from paper_2602_22603_amd import drivers
@@ -134,7 +136,7 @@ def test_shared128k_fp8_sampled_heads(sq):
     av = np.concatenate([rv[:fork_at], of8.roundtrip(wl.torch_bf16_to_f64(va[0][:, g: g + 1]),
                                                      scales[0, 1])])
     refs[(1, g)] = oatt.attention(qf[1][4 * g: 4 * g + 4], ak, av, scale, 4)
-    for mode in (sq.ATTN_AUTO, sq.ATTN_MFMA):
+    for mode in (sq.ATTN_AUTO, sq.ATTN_MFMA, sq.ATTN_STREAM, sq.ATTN_SHARED_PREFIX):
         out = store.decode(0, seqs, q, mode=mode)
         torch.cuda.synchronize()
         o = out.cpu().numpy()
