@@ -1,7 +1,12 @@
 """GPU parity of extend attention (a chunk appended to the cache attends
 causally to the cached prefix and to itself) through the C ABI, against the
-float64 oracle on the same bf16 inputs: max abs error <= 5e-4 on the fp32
-outputs."""
+float64 oracle: max abs error <= 5e-4 on the fp32 outputs.
+
+Every reference is computed from the seeded bf16 inputs themselves, never
+from what the library's pools hold: the small cases replay each append,
+fork and eviction in the oracle's page model (``scenarios.Twin``), whose
+logical view supplies the keys and values; the full-size case removes the
+evicted spans from the seeded inputs with the oracle's keep mask."""
 
 import math
 
@@ -9,6 +14,7 @@ import numpy as np
 import pytest
 
 from tests import scenarios as sc
+from oracle import evict as oev
 from oracle import extend as oex
 from paper_2602_22603_amd import workload as wl
 
@@ -36,45 +42,39 @@ def _free_memory():
         torch.cuda.empty_cache()
 
 
-def _store(sq, hq, hkv, d, tokens, nl=1, seqs=4):
-    pages = 2 * (tokens // 16 + 8) + 16
-    return sq.Store(nl, hq, hkv, d, num_pages=pages, max_seqs=seqs,
-                    max_pages_per_seq=tokens // 16 + 8, device="cuda")
+def _twin(sq, hq, hkv, d, tokens, nl=1, seqs=4, seed=0):
+    """A GPU store and the oracle's page model (with data) side by side."""
+    return sc.Twin(sq, nl, hq, hkv, d, num_pages=2 * (tokens // 16 + 8) + 16, max_seqs=seqs,
+                   max_pages_per_seq=tokens // 16 + 8, seed=seed)
 
 
-def _append(store, seq, n, seed, outlier=False):
-    k = wl.device_normal_bf16((store.num_layers, n, store.num_kv_heads, store.head_dim), seed, "cuda")
-    v = wl.device_normal_bf16((store.num_layers, n, store.num_kv_heads, store.head_dim), seed + 1, "cuda")
-    if outlier:  # four channels x8 (exact in bf16)
-        k[..., :4] *= 8
-        v[..., 5:9] *= 8
-    store.append(seq, k, v)
-
-
-def _extend_error(store, seq, n, seed, layer=0, pairs=None):
-    """Runs extend for the last n tokens of seq and returns the max abs error
-    against the oracle (all rows, or the sampled (row, KV head) pairs)."""
+def _extend_error(tw, seq, n, layer=0, pairs=None):
+    """Runs extend for the last n tokens of seq on the GPU store and returns
+    the max abs error against the oracle over the page model's view of the
+    same sequence (all rows, or the sampled (row, KV head) pairs)."""
     import torch
-    hq, hkv, d = store.num_q_heads, store.num_kv_heads, store.head_dim
+    hq, hkv, d = tw.hq, tw.hkv, tw.d
     g = hq // hkv
-    q = wl.device_normal_bf16((n, hq, d), seed, "cuda")
-    out = store.extend(layer, seq, q)
+    qb = wl.normal_bf16(tw.rng, (n, hq, d))
+    out = tw.store.extend(layer, seq, wl.to_torch_bf16(qb, tw.device))
     torch.cuda.synchronize()
-    k, v, _ = sc.seq_view(store, seq, layers=[layer])
-    qf = wl.torch_bf16_to_f64(q)
+    k, v, _ = tw.model.view(seq)
+    k, v = k[:, layer], v[:, layer]
+    assert k.shape[0] == tw.store.seq_info(seq)["length"]
+    qf = wl.bf16_value(qb)
     got = out.cpu().numpy()
     scale = 1 / math.sqrt(d)
+    assert np.all(np.isfinite(got))
     if pairs is None:
-        ref = oex.extend_attention(qf, k[:, 0], v[:, 0], scale, g)
-        assert np.all(np.isfinite(got))
+        ref = oex.extend_attention(qf, k, v, scale, g)
         return float(np.max(np.abs(got - ref)))
     L = k.shape[0]
     err = 0.0
     for j, kv in pairs:
         last = L - n + j
         hs = slice(kv * g, kv * g + g)
-        ref = oex.extend_attention(qf[j:j + 1, hs], k[: last + 1, 0, kv:kv + 1],
-                                   v[: last + 1, 0, kv:kv + 1], scale, g)
+        ref = oex.extend_attention(qf[j:j + 1, hs], k[: last + 1, kv:kv + 1],
+                                   v[: last + 1, kv:kv + 1], scale, g)
         err = max(err, float(np.max(np.abs(got[j, hs] - ref[0]))))
     return err
 
@@ -86,12 +86,12 @@ CHUNKS = [(0, 1), (0, 45), (37, 33), (250, 130)]
 @pytest.mark.parametrize("hq,hkv,d", SHAPES)
 @pytest.mark.parametrize("prefix,n", CHUNKS)
 def test_extend_matches_oracle(sq, hq, hkv, d, prefix, n):
-    s = _store(sq, hq, hkv, d, prefix + n)
-    a = s.seq_create()
+    tw = _twin(sq, hq, hkv, d, prefix + n, seed=11 + prefix + hq + d)
+    a = tw.create()
     if prefix:
-        _append(s, a, prefix, 11 + prefix)
-    _append(s, a, n, 13 + n)
-    err = _extend_error(s, a, n, 17 + hq + d)
+        tw.append(a, prefix)
+    tw.append(a, n)
+    err = _extend_error(tw, a, n)
     print(f"extend hq={hq} hkv={hkv} d={d} prefix={prefix} n={n}: max abs err {err:.2e}")
     assert err <= TOL
 
@@ -99,11 +99,11 @@ def test_extend_matches_oracle(sq, hq, hkv, d, prefix, n):
 @pytest.mark.parametrize("hq,hkv,d,prefix,n", [(8, 8, 128, 300, 257), (32, 8, 128, 900, 200),
                                                 (16, 2, 64, 1000, 61)])
 def test_extend_several_query_blocks(sq, hq, hkv, d, prefix, n):
-    s = _store(sq, hq, hkv, d, prefix + n)
-    a = s.seq_create()
-    _append(s, a, prefix, 21)
-    _append(s, a, n, 23)
-    err = _extend_error(s, a, n, 29)
+    tw = _twin(sq, hq, hkv, d, prefix + n, seed=21)
+    a = tw.create()
+    tw.append(a, prefix)
+    tw.append(a, n)
+    err = _extend_error(tw, a, n)
     print(f"extend hq={hq} hkv={hkv} d={d} prefix={prefix} n={n}: max abs err {err:.2e}")
     assert err <= TOL
 
@@ -116,15 +116,15 @@ def test_extend_split_key_range(sq, hq, hkv, d, prefix, n):
     over several workgroups and merge the partial rows (an auxiliary
     thread's prompt is such a chunk); with a long chunk over a short prefix
     the first query blocks leave later splits empty."""
-    s = _store(sq, hq, hkv, d, prefix + n)
-    a = s.seq_create()
-    _append(s, a, prefix, 91)
-    _append(s, a, n, 93)
+    tw = _twin(sq, hq, hkv, d, prefix + n, seed=91)
+    a = tw.create()
+    tw.append(a, prefix)
+    tw.append(a, n)
     if prefix + n > 5000:
         pairs = [(j, g) for j in sorted({0, n // 2, n - 1}) for g in (0, hkv - 1)]
-        err = _extend_error(s, a, n, 97, pairs=pairs)
+        err = _extend_error(tw, a, n, pairs=pairs)
     else:
-        err = _extend_error(s, a, n, 97)
+        err = _extend_error(tw, a, n)
     print(f"extend split hq={hq} d={d} prefix={prefix} n={n}: max abs err {err:.2e}")
     assert err <= TOL
 
@@ -134,67 +134,89 @@ def test_extend_whole_sequence_prefill(sq):
     fp32 rounding: its weight is 2^r with r the rounding error of the scaled
     score, |r| < 1e-6)."""
     import torch
-    s = _store(sq, 8, 2, 128, 300)
-    a = s.seq_create()
-    _append(s, a, 300, 31)
-    q = wl.device_normal_bf16((300, 8, 128), 37, "cuda")
-    out = s.extend(0, a, q)
+    tw = _twin(sq, 8, 2, 128, 300, seed=31)
+    a = tw.create()
+    tw.append(a, 300)
+    qb = wl.normal_bf16(tw.rng, (300, 8, 128))
+    out = tw.store.extend(0, a, wl.to_torch_bf16(qb, "cuda"))
     torch.cuda.synchronize()
-    k, v, _ = sc.seq_view(s, a, layers=[0])
+    k, v, _ = tw.model.view(a)
     got = out.cpu().numpy()
     for h in range(8):
         assert np.max(np.abs(got[0, h] - v[0, 0, h // 4])) <= 1e-6
-    ref = oex.extend_attention(wl.torch_bf16_to_f64(q), k[:, 0], v[:, 0], 1 / math.sqrt(128), 4)
+    ref = oex.extend_attention(wl.bf16_value(qb), k[:, 0], v[:, 0], 1 / math.sqrt(128), 4)
     assert float(np.max(np.abs(got - ref))) <= TOL
 
 
 def test_extend_after_eviction(sq):
-    """A chunk appended after Phase 1 compacted the prefix (positions carried)."""
-    s = _store(sq, 32, 8, 128, 1400)
-    a = s.seq_create()
-    _append(s, a, 1200, 41, outlier=True)
+    """A chunk appended after Phase 1 compacted the prefix (positions
+    carried): the oracle evicts the same spans from the seeded inputs, and
+    the pools must hold its compacted view bit for bit."""
+    tw = _twin(sq, 32, 8, 128, 1400, seed=41)
+    a = tw.create()
+    tw.append(a, 1200, outlier=True)
     spans = [(17, 100), (130, 131), (300, 520), (600, 640), (900, 1111)]
     for c, (x, y) in enumerate(spans):
-        s.span_mark(a, c, x, y)
-    s.evict(a, [0, 2, 4])
-    L0 = s.seq_info(a)["length"]
+        tw.mark(a, c, x, y)
+    tw.evict(a, [0, 2, 4])
+    L0 = tw.store.seq_info(a)["length"]
     assert L0 == 1200 - 83 - 220 - 211
-    _append(s, a, 150, 43, outlier=True)
-    err = _extend_error(s, a, 150, 47)
+    tw.append(a, 150, outlier=True)
+    err = _extend_error(tw, a, 150)
     print(f"extend after eviction (prefix {L0}): max abs err {err:.2e}")
     assert err <= TOL
+    tw.check_state()
+
+
+def test_extend_after_deferred_then_compacted(sq):
+    """Spans masked by a deferred eviction, then compacted, before the chunk
+    is appended: the oracle's view is the seeded inputs without them."""
+    tw = _twin(sq, 16, 2, 64, 1000, seed=42)
+    a = tw.create()
+    tw.append(a, 800)
+    for c, (x, y) in enumerate([(5, 60), (200, 333), (500, 517)]):
+        tw.mark(a, c, x, y)
+    tw.evict(a, [1], deferred=True)
+    tw.evict(a, [0, 2])
+    tw.append(a, 90)
+    err = _extend_error(tw, a, 90)
+    print(f"extend after deferred + physical eviction: max abs err {err:.2e}")
+    assert err <= TOL
+    tw.check_state()
 
 
 def test_extend_on_forked_branch(sq):
     """The auxiliary thread forked mid-page (tail page copied) appends a chunk
     and attends over the aliased prefix pages."""
-    s = _store(sq, 8, 2, 64, 700)
-    m = s.seq_create()
-    _append(s, m, 500, 51)
-    aux = s.fork(m, 489)
-    _append(s, aux, 77, 53)
-    _append(s, m, 20, 55)
-    err = _extend_error(s, aux, 77, 57)
-    err_m = _extend_error(s, m, 20, 59)
+    tw = _twin(sq, 8, 2, 64, 700, seed=51)
+    m = tw.create()
+    tw.append(m, 500)
+    aux = tw.fork(m, 489)
+    tw.append(aux, 77)
+    tw.append(m, 20)
+    err = _extend_error(tw, aux, 77)
+    err_m = _extend_error(tw, m, 20)
     print(f"extend on aux: {err:.2e}, on main: {err_m:.2e}")
     assert err <= TOL and err_m <= TOL
+    tw.check_state()
 
 
 def test_extend_other_layers(sq):
-    s = _store(sq, 8, 2, 128, 400, nl=3)
-    a = s.seq_create()
-    _append(s, a, 333, 61)
-    _append(s, a, 40, 63)
+    tw = _twin(sq, 8, 2, 128, 400, nl=3, seed=61)
+    a = tw.create()
+    tw.append(a, 333)
+    tw.append(a, 40)
     for layer in (2, 0):
-        err = _extend_error(s, a, 40, 67 + layer, layer=layer)
+        err = _extend_error(tw, a, 40, layer=layer)
         assert err <= TOL, (layer, err)
 
 
 def test_extend_arguments(sq):
     import torch
-    s = _store(sq, 8, 2, 64, 64)
-    a = s.seq_create()
-    _append(s, a, 20, 71)
+    tw = _twin(sq, 8, 2, 64, 64, seed=71)
+    s = tw.store
+    a = tw.create()
+    tw.append(a, 20)
     q = wl.device_normal_bf16((21, 8, 64), 73, "cuda")
     with pytest.raises(sq.SqError) as ei:
         s.extend(0, a, q)              # more new tokens than cached
@@ -217,20 +239,43 @@ def test_extend_arguments(sq):
 def test_extend_full_size_sampled(sq):
     """The measured configuration: an 8192-token chunk appended to the 64K
     context after its tool spans were evicted (>= 65% of the tokens), 32
-    query / 8 KV heads, head_dim 128; sampled rows against the oracle."""
+    query / 8 KV heads, head_dim 128.  The reference keys are the seeded
+    inputs with the oracle's keep mask of the evicted spans applied, then
+    the chunk's own; sampled rows of every KV head against the oracle."""
     import torch
     from paper_2602_22603_amd import drivers
     store, base, w, k, v = drivers.build_compaction64k(extra_tokens=8192 + 64)
+    L = w.length
+    keep, _dst, _src, n_kept, _f = oev.plan(L, [w.spans[c] for c in w.evict_ids])
+    kept = torch.from_numpy(keep.astype(bool))
+    k_kept, v_kept = k[0].cpu()[kept], v[0].cpu()[kept]   # bf16 [L', Hkv, D]
     del k, v
     store.evict(base, w.evict_ids)
     L0 = store.seq_info(base)["length"]
+    assert L0 == n_kept
+    assert np.array_equal(store.positions(base), np.flatnonzero(keep))
     n = 8192
     kn = wl.device_normal_bf16((1, n, 8, 128), 81, "cuda")
     vn = wl.device_normal_bf16((1, n, 8, 128), 82, "cuda")
     store.append(base, kn, vn)
-    del kn, vn
-    pairs = [(0, 0), (1, 7), (31, 3), (32, 4), (4095, 1), (4096, 6), (8190, 2), (8191, 5)]
-    err = _extend_error(store, base, n, 83, pairs=pairs)
+    kf = wl.torch_bf16_to_f64(torch.cat([k_kept, kn[0].cpu()]))   # [L' + n, Hkv, D]
+    vf = wl.torch_bf16_to_f64(torch.cat([v_kept, vn[0].cpu()]))
+    del kn, vn, k_kept, v_kept
+    q = wl.device_normal_bf16((n, 32, 128), 83, "cuda")
+    out = store.extend(0, base, q)
+    torch.cuda.synchronize()
+    got = out.cpu().numpy()
+    qf = wl.torch_bf16_to_f64(q)
+    scale = 1 / math.sqrt(128)
+    rows = [0, 1, 31, 32, 127, 128, 4095, 4096, 8190, 8191]
+    err = 0.0
+    for j in rows:
+        last = n_kept + j
+        for kv in range(8):
+            hs = slice(4 * kv, 4 * kv + 4)
+            ref = oex.extend_attention(qf[j:j + 1, hs], kf[: last + 1, kv:kv + 1],
+                                       vf[: last + 1, kv:kv + 1], scale, 4)
+            err = max(err, float(np.max(np.abs(got[j, hs] - ref[0]))))
     print(f"extend 8192 over compacted prefix {L0}: sampled max abs err {err:.2e}")
     assert err <= TOL
     st = store.stats()
