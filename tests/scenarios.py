@@ -54,6 +54,7 @@ def oracle_model_for(store, with_data=True):
                          kv_heads=store.num_kv_heads, head_dim=store.head_dim,
                          with_data=with_data, evict_chunk_pages=store.evict_chunk_pages,
                          evict_remap=store.evict_remap,
+                         evict_inplace=getattr(store, "evict_inplace", False),
                          kv_scales=getattr(store, "kv_scales", None))
 
 
@@ -148,12 +149,13 @@ class Twin:
 
     def __init__(self, sq, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
                  max_seqs, max_pages_per_seq, seed=0, device="cuda", evict_chunk_pages=0,
-                 evict_remap=False, kv_scales=None):
+                 evict_remap=False, kv_scales=None, evict_inplace=False):
         self.sq = sq
         self.device = device
         self.store = sq.Store(num_layers, num_q_heads, num_kv_heads, head_dim, num_pages,
                               max_seqs, max_pages_per_seq, device=device,
                               evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap,
+                              evict_inplace=evict_inplace,
                               kv_scales=kv_scales)
         self.model = oracle_model_for(self.store)
         self.rng = np.random.default_rng([2602, 900, seed])
@@ -166,11 +168,18 @@ class Twin:
         assert a == b
         return a
 
-    def append(self, h, n, const_v=None):
+    def append(self, h, n, const_v=None, outlier=False):
+        """n seeded tokens; ``outlier`` scales K channels 0-3 and V channels
+        5-8 by 8 (exact in bf16), the outlier-channel shape."""
         kb = wl.normal_bf16(self.rng, (self.nl, n, self.hkv, self.d))
         vb = wl.normal_bf16(self.rng, (self.nl, n, self.hkv, self.d))
         if const_v is not None:
             vb[...] = wl.bf16_bits(np.full(vb.shape, const_v, np.float32))
+        if outlier:
+            kf, vf = wl.bf16_value(kb), wl.bf16_value(vb)
+            kf[..., :4] *= 8
+            vf[..., 5:9] *= 8
+            kb, vb = wl.bf16_bits(kf.astype(np.float32)), wl.bf16_bits(vf.astype(np.float32))
         self.store.append(h, wl.to_torch_bf16(kb, self.device), wl.to_torch_bf16(vb, self.device))
         self.model.append(h, n, wl.bf16_value(kb), wl.bf16_value(vb))
 
