@@ -158,17 +158,19 @@ static_assert(sizeof(DecodeArgs) < 4096, "decode kernel arguments too large");
 static_assert(sizeof(MergeArgs) < 4096, "merge kernel arguments too large");
 
 hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t s);
-hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s);
+// The MFMA tile kernels run kMfmaWaves waves per workgroup.
+constexpr int kMfmaWaves = 4;
+hipError_t launch_decode_mfma(int d, int group, const DecodeArgs &a, hipStream_t s);
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s);
 // Step launches: `n_wg` workgroups (at least the plan's), the plan in device
 // memory at `dyn`.
 hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const DecodeDyn *dyn,
                             int n_wg, hipStream_t s);
-hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
-                            const DecodeDyn *dyn, int n_wg, hipStream_t s);
+hipError_t launch_step_mfma(int d, int group, const DecodeStatic &st, const DecodeDyn *dyn,
+                            int n_wg, hipStream_t s);
 hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8, hipStream_t s);
 // Workgroups of a decode kernel that fit on one CU.  kind: 0 VALU, 1 MFMA,
 // 2 the 8-bit MFMA kernel (four waves), 3 the 8-bit VALU kernel
-hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out);
+hipError_t decode_blocks_per_cu(int kind, int d, int group, int *out);
 
 } // namespace sq

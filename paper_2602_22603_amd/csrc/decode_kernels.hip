@@ -484,17 +484,11 @@ __device__ inline __amdgpu_buffer_rsrc_t page_rsrc(const char *page, bool want, 
                                            kRsrcWord3);
 }
 template <bool NT> constexpr int kAux = NT ? 2 : 0; // nt: streamed once
-// pages in flight per wave of the 8-bit MFMA tile
-#ifndef SQ_FP8_STAGES_64
-#define SQ_FP8_STAGES_64 4
-#endif
-#ifndef SQ_FP8_STAGES_128
-#define SQ_FP8_STAGES_128 2
-#endif
-#ifndef SQ_FP8_WAVES_EU
-#define SQ_FP8_WAVES_EU 3
-#endif
-template <int D> constexpr int kStages8 = D == 64 ? SQ_FP8_STAGES_64 : SQ_FP8_STAGES_128;
+// pages in flight per wave of the 8-bit MFMA tile (a 64-channel page is
+// half the bytes, so twice as many keep the same bytes in flight)
+template <int D> constexpr int kStages8 = D == 64 ? 4 : 2;
+// waves per SIMD of the MFMA tiles
+constexpr int kMfmaWavesPerEu = 3;
 
 // K fragment: lane (n, kg) takes channels 8 kg + 32 s .. +8 of token n.
 template <int D, bool NT>
@@ -904,23 +898,23 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
 }
 
 template <int D, int G, int kWaves, bool NT, bool MK>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kMfmaWavesPerEu, kMfmaWavesPerEu))) void
 k_decode_mfma(DecodeArgs a) {
   mfma_body<D, G, kWaves, NT, MK>(a.st, ArgPlan{a.dyn});
 }
 template <int D, int G, int kWaves>
-__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(3, 3))) void
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kMfmaWavesPerEu, kMfmaWavesPerEu))) void
 k_step_mfma(DecodeStatic a, const DecodeDyn *dyn) {
   mfma_body<D, G, kWaves, true, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
 }
 // 8-bit store: four waves, streaming loads
 template <int D, int G, bool MK>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SQ_FP8_WAVES_EU, SQ_FP8_WAVES_EU))) void
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kMfmaWavesPerEu, kMfmaWavesPerEu))) void
 k_decode_mfma8(DecodeArgs a) {
   mfma_body<D, G, 4, true, MK, ArgPlan, true>(a.st, ArgPlan{a.dyn});
 }
 template <int D, int G>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(SQ_FP8_WAVES_EU, SQ_FP8_WAVES_EU))) void
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(kMfmaWavesPerEu, kMfmaWavesPerEu))) void
 k_step_mfma8(DecodeStatic a, const DecodeDyn *dyn) {
   mfma_body<D, G, 4, true, true, DevPlan, true>(a, DevPlan{(const SQ_CONST DecodeDyn *)dyn});
 }
@@ -1184,16 +1178,6 @@ hipError_t mfma_dispatch_w(int group, const DecodeArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
-template <int D, bool NT, bool MK>
-hipError_t mfma_dispatch_nt(int group, int waves, const DecodeArgs &a, hipStream_t s) {
-  switch (waves) {
-  case 1: return mfma_dispatch_w<D, 1, NT, MK>(group, a, s);
-  case 2: return mfma_dispatch_w<D, 2, NT, MK>(group, a, s);
-  case 4: return mfma_dispatch_w<D, 4, NT, MK>(group, a, s);
-  default: return hipErrorInvalidValue;
-  }
-}
-
 template <int D, bool MK>
 hipError_t mfma8_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
   const dim3 grid(a.dyn.n_wg), block(256);
@@ -1210,14 +1194,12 @@ hipError_t mfma8_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
 // a plan with keep masks takes the masked variant (ordinary loads); an
 // 8-bit store its own kernel (four waves)
 template <int D>
-hipError_t mfma_dispatch(int group, int waves, const DecodeArgs &a, hipStream_t s) {
-  if (a.st.kv8) {
-    if (waves != 4) return hipErrorInvalidValue;
+hipError_t mfma_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
+  if (a.st.kv8)
     return a.dyn.masked ? mfma8_dispatch<D, true>(group, a, s) : mfma8_dispatch<D, false>(group, a, s);
-  }
-  if (a.dyn.masked) return mfma_dispatch_nt<D, false, true>(group, waves, a, s);
-  return a.st.nontemporal ? mfma_dispatch_nt<D, true, false>(group, waves, a, s)
-                       : mfma_dispatch_nt<D, false, false>(group, waves, a, s);
+  if (a.dyn.masked) return mfma_dispatch_w<D, kMfmaWaves, false, true>(group, a, s);
+  return a.st.nontemporal ? mfma_dispatch_w<D, kMfmaWaves, true, false>(group, a, s)
+                       : mfma_dispatch_w<D, kMfmaWaves, false, false>(group, a, s);
 }
 
 } // namespace
@@ -1250,19 +1232,16 @@ template <int D> const void *mfma8_fn(int group) {
   default: return nullptr;
   }
 }
-template <int D> const void *mfma_fn(int group, int waves) {
-  return waves == 1 ? mfma_fn_w<D, 1>(group) : waves == 2 ? mfma_fn_w<D, 2>(group)
-                                                          : mfma_fn_w<D, 4>(group);
-}
+template <int D> const void *mfma_fn(int group) { return mfma_fn_w<D, kMfmaWaves>(group); }
 } // namespace
 
-hipError_t decode_blocks_per_cu(int kind, int d, int group, int waves, int *out) {
+hipError_t decode_blocks_per_cu(int kind, int d, int group, int *out) {
   const void *fn = kind == 0   ? (d == 128 ? valu_fn<128, false>(group) : valu_fn<64, false>(group))
                    : kind == 3 ? (d == 128 ? valu_fn<128, true>(group) : valu_fn<64, true>(group))
                    : kind == 2 ? (d == 128 ? mfma8_fn<128>(group) : mfma8_fn<64>(group))
-                               : (d == 128 ? mfma_fn<128>(group, waves) : mfma_fn<64>(group, waves));
+                               : (d == 128 ? mfma_fn<128>(group) : mfma_fn<64>(group));
   if (!fn) return hipErrorInvalidValue;
-  const int block = kind == 0 || kind == 3 ? 64 : 64 * waves;
+  const int block = kind == 0 || kind == 3 ? 64 : 64 * kMfmaWaves;
   return hipOccupancyMaxActiveBlocksPerMultiprocessor(out, fn, block, 0);
 }
 
@@ -1271,9 +1250,9 @@ hipError_t launch_decode_valu(int d, int group, const DecodeArgs &a, hipStream_t
   return d == 128 ? valu_dispatch<128>(group, a, s) : valu_dispatch<64>(group, a, s);
 }
 
-hipError_t launch_decode_mfma(int d, int group, int waves, const DecodeArgs &a, hipStream_t s) {
+hipError_t launch_decode_mfma(int d, int group, const DecodeArgs &a, hipStream_t s) {
   if (a.dyn.n_wg == 0) return hipSuccess;
-  return d == 128 ? mfma_dispatch<128>(group, waves, a, s) : mfma_dispatch<64>(group, waves, a, s);
+  return d == 128 ? mfma_dispatch<128>(group, a, s) : mfma_dispatch<64>(group, a, s);
 }
 
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s) {
@@ -1312,7 +1291,7 @@ hipError_t step_valu_dispatch(int group, const DecodeStatic &st, const DecodeDyn
 template <int D>
 hipError_t step_mfma_dispatch(int group, const DecodeStatic &st, const DecodeDyn *dyn, int n_wg,
                               hipStream_t s) {
-  constexpr int W = 4;
+  constexpr int W = kMfmaWaves;
   const dim3 grid(n_wg), block(64 * W);
   if (st.kv8) {
     switch (group) {
@@ -1342,9 +1321,9 @@ hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const Deco
                   : step_valu_dispatch<64>(group, st, dyn, n_wg, s);
 }
 
-hipError_t launch_step_mfma(int d, int group, int waves, const DecodeStatic &st,
-                            const DecodeDyn *dyn, int n_wg, hipStream_t s) {
-  if (n_wg <= 0 || waves != 4) return hipErrorInvalidValue;
+hipError_t launch_step_mfma(int d, int group, const DecodeStatic &st, const DecodeDyn *dyn,
+                            int n_wg, hipStream_t s) {
+  if (n_wg <= 0) return hipErrorInvalidValue;
   return d == 128 ? step_mfma_dispatch<128>(group, st, dyn, n_wg, s)
                   : step_mfma_dispatch<64>(group, st, dyn, n_wg, s);
 }

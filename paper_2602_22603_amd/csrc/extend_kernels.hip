@@ -46,9 +46,7 @@ constexpr int kThreads = 256;
 constexpr float kNegInf = -__builtin_huge_valf();
 // Two waves per SIMD: two workgroups per CU share the matrix cores, so one
 // workgroup's softmax and barriers overlap the other's MFMAs.
-#ifndef EXT_WAVES_PER_EU
-#define EXT_WAVES_PER_EU 2
-#endif
+constexpr int kExtWavesPerEu = 2;
 
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
 typedef float f32x4_t __attribute__((__vector_size__(4 * sizeof(float))));
@@ -341,7 +339,7 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
 }
 
 template <int D, int G, bool KV8 = false>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(EXT_WAVES_PER_EU, EXT_WAVES_PER_EU))) void
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(kExtWavesPerEu, kExtWavesPerEu))) void
 k_extend(ExtendArgs a) {
   using Lt = ExtLayout<D>;
   constexpr int NKC = D / 32; // k chunks of S^T = K . Q^T
