@@ -115,10 +115,13 @@ class PageModel:
 
     def __init__(self, num_pages, page_size, max_seqs, max_pages_per_seq,
                  layers=1, kv_heads=1, head_dim=1, with_data=False, evict_chunk_pages=0,
-                 evict_remap=False, kv_scales=None):
+                 evict_remap=False, kv_scales=None, evict_inplace=False):
         self.num_pages = int(num_pages)
         self.evict_chunk_pages = int(evict_chunk_pages)
         self.evict_remap = bool(evict_remap)
+        self.evict_inplace = bool(evict_inplace)
+        if self.evict_inplace and (self.evict_remap or self.evict_chunk_pages):
+            raise Invalid("in-place eviction takes neither chunks nor remaps")
         self.P = int(page_size)
         self.max_seqs = int(max_seqs)
         self.max_pages_per_seq = int(max_pages_per_seq)
@@ -327,49 +330,30 @@ class PageModel:
             for c in ids:
                 del seq.spans[c]
             return stats
+
+        # 1. What eviction computes, by its plain definition: the kept
+        #    tokens in their order (keep, src_of) and their data, which is
+        #    the old logical view under the keep mask.
         keep, _dst, src_of, new_len, first = _evict.plan(seq.length, spans)
+        if self.with_data:
+            old_k, old_v, old_pos = self.slot_view(h)
+            new_k = _evict.compact(old_k, keep)
+            new_v = _evict.compact(old_v, keep)
+            new_pos = _evict.compact(old_pos, keep)
+
+        # 2. Where the result lives.  Pages before fp = floor(f / P) hold
+        #    only tokens before f and stay.  The tail (new indices from
+        #    fp * P on) fills n_new pages; tail page k is an old page taken
+        #    by reference (remap, in-place) or a fresh page.
         fp = first // self.P
         n_new = math.ceil(new_len / self.P) - fp
         old_tail = seq.pages[fp:]
-        # page-aligned remap: a full tail page whose P tokens are one old
-        # page's P tokens in order is that old page, taken by reference
-        alias = [None] * n_new
-        if self.evict_remap:
-            for k in range(n_new):
-                a0 = self._remap_source(src_of, (fp + k) * self.P, new_len)
-                if a0 is not None:
-                    alias[k] = seq.pages[a0 // self.P]
-        n_alias = sum(a is not None for a in alias)
-        C = self.evict_chunk_pages if self.evict_chunk_pages > 0 else max(1, n_new)
-        # the schedule: (pages to allocate, old-tail pages released after them)
-        steps, released = [], 0
-        for k0 in range(0, n_new, C):
-            c = min(C, n_new - k0)
-            j_end = min((fp + k0 + c) * self.P, new_len)
-            consumed = int(src_of[j_end]) if j_end < new_len else seq.length
-            upto = self._released_after(fp, released, len(old_tail), consumed) if C < n_new else released
-            steps.append((k0, c, old_tail[released:upto]))
-            released = upto
-        steps.append((n_new, 0, old_tail[released:]))
-        # validate: every allocation must find its pages free
-        free, refs = self.free_pages(), {}
-        for a in alias:
-            if a is not None:
-                refs[a] = refs.get(a, self.refcount[a]) + 1
-        for k0, c, rel in steps:
-            fresh = sum(alias[k] is None for k in range(k0, k0 + c))
-            if fresh > free:
-                raise NoPages("not enough free pages for the compacted tail")
-            free -= fresh
-            for page in rel:
-                refs[page] = refs.get(page, self.refcount[page]) - 1
-                free += refs[page] == 0
-        if self.with_data:  # read every kept token before any page is reused
-            src = [int(src_of[j]) for j in range(fp * self.P, new_len)]
-            src_p = [seq.pages[x // self.P] for x in src]
-            src_s = [x % self.P for x in src]
-            moved_k, moved_v = self.K[src_p, src_s].copy(), self.V[src_p, src_s].copy()
-            moved_pos = self.POS[src_p, src_s].copy()
+        alias, kind = self._place_tail(seq, fp, n_new, src_of, new_len)
+        steps = self._alloc_release_steps(seq, fp, n_new, old_tail, src_of, new_len)
+        self._check_pages_suffice(alias, steps)
+
+        # 3. Apply: references to the pages taken, fresh pages and releases
+        #    in schedule order, then the tail tokens written to their pages.
         new_pages, freed = [], 0
         for a in alias:
             if a is not None:
@@ -387,9 +371,9 @@ class PageModel:
             j = np.arange(fp * self.P, new_len)
             dp = [new_pages[x // self.P - fp] for x in j]
             ds = list(j % self.P)
-            self.K[dp, ds] = moved_k
-            self.V[dp, ds] = moved_v
-            self.POS[dp, ds] = moved_pos
+            self.K[dp, ds] = new_k[fp * self.P:]
+            self.V[dp, ds] = new_v[fp * self.P:]
+            self.POS[dp, ds] = new_pos[fp * self.P:]
         seq.pages = seq.pages[:fp] + new_pages
         seq.pos = [p for p, k in zip(seq.pos, keep) if k]
         seq.keep = [True] * new_len
@@ -398,11 +382,64 @@ class PageModel:
         for c in ids:
             del seq.spans[c]
         seq.spans = {c: _evict.shift_span(s, e, spans) for c, (s, e) in seq.spans.items()}
+        n_remap = kind.count("remap")
         stats.update(tokens_removed=old_len - new_len,
-                     tokens_moved=new_len - fp * self.P - n_alias * self.P,
-                     pages_allocated=n_new - n_alias, pages_freed=freed, first_evicted=first,
-                     pages_remapped=n_alias)
+                     tokens_moved=new_len - fp * self.P - n_remap * self.P,
+                     pages_allocated=kind.count("fresh"), pages_freed=freed, first_evicted=first,
+                     pages_remapped=n_remap)
         return stats
+
+    def _place_tail(self, seq, fp, n_new, src_of, new_len):
+        """The page each tail page k < n_new is, when it is an old page taken
+        by reference (else None: a fresh page), and the kind of each.
+
+        * remap: a full tail page whose P tokens are one old page's P tokens
+          in order is that old page, unchanged;
+        * in-place: tail page k is the old page at the same list index,
+          fp + k, rewritten, when this sequence alone holds it;
+        * otherwise (and for a page another branch holds) a fresh page."""
+        alias, kind = [None] * n_new, ["fresh"] * n_new
+        for k in range(n_new):
+            if self.evict_remap:
+                a0 = self._remap_source(src_of, (fp + k) * self.P, new_len)
+                if a0 is not None:
+                    alias[k], kind[k] = seq.pages[a0 // self.P], "remap"
+            elif self.evict_inplace and self.refcount[seq.pages[fp + k]] == 1:
+                alias[k], kind[k] = seq.pages[fp + k], "inplace"
+        return alias, kind
+
+    def _alloc_release_steps(self, seq, fp, n_new, old_tail, src_of, new_len):
+        """[(first tail page, pages, old pages released after them)]: one
+        step taking every tail page, then the release of the old tail; with
+        chunks of C pages, after each chunk the old pages whose tokens all
+        lie before the next kept token still to move."""
+        C = self.evict_chunk_pages if self.evict_chunk_pages > 0 else max(1, n_new)
+        steps, released = [], 0
+        for k0 in range(0, n_new, C):
+            c = min(C, n_new - k0)
+            j_end = min((fp + k0 + c) * self.P, new_len)
+            consumed = int(src_of[j_end]) if j_end < new_len else seq.length
+            upto = self._released_after(fp, released, len(old_tail), consumed) if C < n_new else released
+            steps.append((k0, c, old_tail[released:upto]))
+            released = upto
+        steps.append((n_new, 0, old_tail[released:]))
+        return steps
+
+    def _check_pages_suffice(self, alias, steps):
+        """Every step must find its fresh pages free, counting the pages
+        released before it (nothing changes when one does not)."""
+        free, refs = self.free_pages(), {}
+        for a in alias:
+            if a is not None:
+                refs[a] = refs.get(a, self.refcount[a]) + 1
+        for k0, c, rel in steps:
+            fresh = sum(alias[k] is None for k in range(k0, k0 + c))
+            if fresh > free:
+                raise NoPages("not enough free pages for the compacted tail")
+            free -= fresh
+            for page in rel:
+                refs[page] = refs.get(page, self.refcount[page]) - 1
+                free += refs[page] == 0
 
     # -- inspection --------------------------------------------------------
     def page_table(self, h):

@@ -247,20 +247,24 @@ def _state(model):
                            for h, s in model.seqs.items()}, model.peak_pages))
 
 
-def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False, deferred=False):
+def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False, deferred=False,
+                             inplace=False):
     """Random op sequences: the page model's logical views equal a naive list
     model's, for page sizes 1, 2, 4 and 16 (and each eviction chunk size).
     With ``remap`` half the marked spans are whole multiples of the page size,
     so that page-aligned remaps happen; returns the pages remapped.  With
-    ``deferred`` evictions are also deferred and compactions happen."""
+    ``deferred`` evictions are also deferred and compactions happen.  With
+    ``inplace`` evictions rewrite the sequence's own pages; returns the
+    evictions that moved tokens without taking a page."""
     rng = np.random.default_rng(seed)
     nl, hkv, d = 2, 2, 3
     remapped = 0
+    in_place = 0
     for page, chunk in itertools.product([1, 2, 4, 16], chunks):
         model = pg.PageModel(num_pages=400, page_size=page, max_seqs=6,
                              max_pages_per_seq=400, layers=nl, kv_heads=hkv,
                              head_dim=d, with_data=True, evict_chunk_pages=chunk,
-                             evict_remap=remap)
+                             evict_remap=remap, evict_inplace=inplace)
         ref = ListModel()
         next_cursor = 0
         h0 = model.seq_create()
@@ -298,7 +302,9 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False, deferr
             elif op == "evict":
                 cur = list(model.spans(h))
                 pick = [c for c in cur if rng.random() < 0.5]
-                remapped += model.evict(h, pick)["pages_remapped"]
+                st = model.evict(h, pick)
+                remapped += st["pages_remapped"]
+                in_place += st["tokens_moved"] > 0 and st["pages_allocated"] == 0
                 ref.evict(h, pick)
             elif op == "defer":
                 cur = list(model.spans(h))
@@ -335,7 +341,7 @@ def check_against_list_model(seed=10, n_ops=60, chunks=(0,), remap=False, deferr
         for h in list(model.seqs):
             model.release(h)
         assert model.live_pages() == 0
-    return remapped
+    return in_place if inplace else remapped
 
 
 def check_hand_worked_page_tables():
@@ -760,6 +766,152 @@ def check_remap_page_tables_by_hand():
 
 
 # --------------------------------------------------------------------------
+# in-place eviction (no transient pages)
+# --------------------------------------------------------------------------
+def check_inplace_against_list_model():
+    """In-place eviction, alone and with deferred evictions: every logical
+    view, span and position equals the naive list model's, refcounts match
+    the page lists (a branch's pages are never rewritten: its view is the
+    list model's too), and evictions that take no page do happen."""
+    assert check_against_list_model(seed=29, n_ops=60, inplace=True) > 0
+    assert check_against_list_model(seed=30, n_ops=60, deferred=True, inplace=True) > 0
+
+
+def check_inplace_page_tables_by_hand():
+    """P = 2, 8 tokens in pages [0, 1, 2, 3]; evicting tokens 1 and 2 keeps
+    0, 3, 4, 5, 6, 7.  In place: pages [0, 1, 2] hold (0, 3), (4, 5),
+    (6, 7); page 3 is freed; no page is taken.  With an auxiliary branch
+    forked at 4 (holding pages 0 and 1), those two pages stay as they are
+    for the branch and the sequence takes fresh pages 4 and 5 for them:
+    [4, 5, 2]."""
+    for fork, table, alloc in ((False, [0, 1, 2], 0), (True, [4, 5, 2], 2)):
+        m = pg.PageModel(num_pages=8, page_size=2, max_seqs=2, max_pages_per_seq=8,
+                         with_data=True, evict_inplace=True)
+        a = m.seq_create()
+        k = np.arange(8, dtype=np.float64).reshape(1, 8, 1, 1)
+        m.append(a, 8, k, -k)
+        if fork:
+            aux = m.fork(a, 4)
+        m.span_mark(a, 0, 1, 3)
+        st = m.evict(a, [0])
+        assert m.page_table(a) == table, (fork, m.page_table(a))
+        assert (st["pages_allocated"], st["pages_freed"], st["tokens_moved"]) == (alloc, 1, 6)
+        kv, vv, pos = m.view(a)
+        assert kv[:, 0, 0, 0].tolist() == [0, 3, 4, 5, 6, 7]
+        assert vv[:, 0, 0, 0].tolist() == [0, -3, -4, -5, -6, -7]
+        assert pos.tolist() == [0, 3, 4, 5, 6, 7]
+        assert m.peak_pages == 4 + alloc
+        if fork:
+            assert m.page_table(aux) == [0, 1]
+            assert m.view(aux)[0][:, 0, 0, 0].tolist() == [0, 1, 2, 3]
+            assert m.refcount.tolist()[:6] == [1, 1, 1, 0, 1, 1]
+
+
+def check_inplace_fits_a_full_pool():
+    """A pool whose every page holds the sequence: the one-shot and chunked
+    evictions need fresh pages and fail (changing nothing); in place needs
+    none and succeeds."""
+    for mode, ok in (({}, False), ({"evict_chunk_pages": 1}, False),
+                     ({"evict_inplace": True}, True)):
+        m = pg.PageModel(num_pages=4, page_size=2, max_seqs=2, max_pages_per_seq=8,
+                         with_data=True, **mode)
+        a = m.seq_create()
+        k = np.arange(8, dtype=np.float64).reshape(1, 8, 1, 1)
+        m.append(a, 8, k, k)
+        m.span_mark(a, 0, 1, 3)
+        assert m.free_pages() == 0
+        snap = _state(m)
+        try:
+            m.evict(a, [0])
+            assert ok, mode
+            assert m.page_table(a) == [0, 1, 2]
+            assert m.view(a)[0][:, 0, 0, 0].tolist() == [0, 3, 4, 5, 6, 7]
+            assert m.peak_pages == 4 and m.live_pages() == 3
+        except pg.NoPages:
+            assert not ok, mode
+            assert _state(m) == snap
+
+
+def _inplace_reads(length, spans, P, n_new, first):
+    """Old page-list indices each tail page's kept tokens come from (from
+    the eviction plan alone)."""
+    _keep, _dst, src_of, new_len, _f = ev.plan(length, spans)
+    fp = first // P
+    return [sorted({int(src_of[j]) // P
+                    for j in range((fp + k) * P, min((fp + k + 1) * P, new_len))})
+            for k in range(n_new)]
+
+
+def _inplace_rounds(reads, fp):
+    """Runs [a, b) of tail pages that one parallel launch may rewrite: taking
+    each page's read range whole, page b joins unless the range of pages
+    a .. b - 1 covers fp + b."""
+    rounds, a = [], 0
+    while a < len(reads):
+        lo, hi, b = reads[a][0], reads[a][-1], a + 1
+        while b < len(reads) and not (lo <= fp + b <= hi):
+            hi = max(hi, reads[b][-1])
+            b += 1
+        rounds.append((a, b))
+        a = b
+    return rounds
+
+
+def check_inplace_order_never_reads_a_rewritten_page(seed=31):
+    """Tail page k's tokens come from old list indices >= fp + k, so a pass
+    that rewrites the tail pages in order never reads a page it has already
+    rewritten; replaying such a pass on the physical pages (each page's
+    sources read, then the page written) gives the model's result.  Runs of
+    pages rewritten in parallel read no page of the run but their own, and
+    with a shift of s tokens a run spans about s / P pages."""
+    rng = np.random.default_rng(seed)
+    P = 4
+    for trial in range(60):
+        L = int(rng.integers(8, 120))
+        m = pg.PageModel(num_pages=64, page_size=P, max_seqs=2, max_pages_per_seq=64,
+                         head_dim=2, with_data=True, evict_inplace=True)
+        a = m.seq_create()
+        k = rng.standard_normal((1, L, 1, 2))
+        m.append(a, L, k, -k)
+        cuts = np.sort(rng.choice(np.arange(L + 1), size=2 * int(rng.integers(1, 4)),
+                                  replace=False))
+        spans = [(int(cuts[2 * i]), int(cuts[2 * i + 1])) for i in range(len(cuts) // 2)]
+        spans = [(s0, e0) for s0, e0 in spans if e0 > s0]
+        if not spans:
+            continue
+        for c, (s0, e0) in enumerate(spans):
+            m.span_mark(a, c, s0, e0)
+        old_pages = list(m.page_table(a))
+        phys_k = m.K.copy()
+        st = m.evict(a, list(range(len(spans))))
+        new_len, fp = m.info(a)["length"], st["first_evicted"] // P
+        n_new = math.ceil(new_len / P) - fp
+        reads = _inplace_reads(L, spans, P, n_new, st["first_evicted"])
+        assert m.page_table(a)[fp:] == old_pages[fp: fp + n_new]
+        _keep, _dst, src_of, _nl, _f = ev.plan(L, spans)
+        for kk in range(n_new):
+            assert reads[kk][0] >= fp + kk, (trial, kk, reads[kk])
+            # the pass: read page kk's sources from the current pages, write it
+            toks = range((fp + kk) * P, min((fp + kk + 1) * P, new_len))
+            vals = [phys_k[old_pages[int(src_of[j]) // P], int(src_of[j]) % P].copy() for j in toks]
+            for j, v in zip(toks, vals):
+                phys_k[old_pages[fp + kk], j % P] = v
+        for j in range(new_len):
+            pg_id = m.page_table(a)[j // P]
+            assert np.array_equal(phys_k[pg_id, j % P], m.K[pg_id, j % P])
+        rounds = _inplace_rounds(reads, fp)
+        for r0, r1 in rounds:
+            for kk in range(r0, r1):
+                others = {fp + x for x in range(r0, r1) if x != kk}
+                assert not (set(range(reads[kk][0], reads[kk][-1] + 1)) & others), (trial, kk)
+    # a shift of one token: every run is one page; a shift of 8 pages: runs of 8
+    for shift, want in ((1, 1), (8 * P, 8)):
+        reads = _inplace_reads(64 * P, [(0, shift)], P, math.ceil((64 * P - shift) / P), 0)
+        rounds = _inplace_rounds(reads, 0)
+        assert max(r1 - r0 for r0, r1 in rounds) == want, (shift, rounds[:3])
+
+
+# --------------------------------------------------------------------------
 # sinks and windows (model variants)
 # --------------------------------------------------------------------------
 def check_sinks_textbook(seed=22):
@@ -992,6 +1144,8 @@ ALL_CHECKS = [
     check_chunked_eviction_fits_where_one_shot_does_not,
     check_chunked_eviction_never_overwrites_unread_tokens,
     check_remap_against_list_model, check_remap_page_tables_by_hand,
+    check_inplace_against_list_model, check_inplace_page_tables_by_hand,
+    check_inplace_fits_a_full_pool, check_inplace_order_never_reads_a_rewritten_page,
     check_sinks_textbook, check_sink_closed_form, check_windows,
     check_deferred_against_list_model, check_deferred_by_hand,
     check_deferred_then_compact_equals_immediate,

@@ -265,6 +265,36 @@ def _extend_window_one_too_wide(q, k, v, scale, group, mask=None, window=0, sink
     return _orig_extend(q, k, v, scale, group, mask, window + 1 if window > 0 else 0, sinks)
 
 
+_ORIG_PLACE = pg.PageModel._place_tail
+
+
+def _inplace_ignores_sharing(self, seq, fp, n_new, src_of, new_len):
+    # rewrites the old tail page even when another branch still holds it
+    alias, kind = _ORIG_PLACE(self, seq, fp, n_new, src_of, new_len)
+    if self.evict_inplace:
+        for k in range(n_new):
+            alias[k], kind[k] = seq.pages[fp + k], "inplace"
+    return alias, kind
+
+
+def _inplace_next_page(self, seq, fp, n_new, src_of, new_len):
+    # takes the old page one list index further on (the last one stays fresh)
+    alias, kind = _ORIG_PLACE(self, seq, fp, n_new, src_of, new_len)
+    if self.evict_inplace:
+        for k in range(n_new):
+            ok = fp + k + 1 < len(seq.pages) and self.refcount[seq.pages[fp + k + 1]] == 1
+            alias[k], kind[k] = (seq.pages[fp + k + 1], "inplace") if ok else (None, "fresh")
+    return alias, kind
+
+
+def _inplace_counts_as_fresh(self, seq, fp, n_new, src_of, new_len):
+    # never reuses a page: the one-shot rule under the in-place flag
+    alias, kind = _ORIG_PLACE(self, seq, fp, n_new, src_of, new_len)
+    if self.evict_inplace:
+        alias, kind = [None] * n_new, ["fresh"] * n_new
+    return alias, kind
+
+
 MUTANTS = {
     "gqa_head_modulo": (att, "scores", _scores_gqa_modulo),
     "missing_scale": (att, "scores", _scores_no_scale),
@@ -287,6 +317,9 @@ MUTANTS = {
     "evict_chunk_releases_a_page_early": (pg.PageModel, "_released_after", _released_one_page_early),
     "remap_without_run_check": (pg.PageModel, "_remap_source", _remap_page_start_only),
     "remap_takes_the_next_page": (pg.PageModel, "_remap_source", _remap_next_page),
+    "inplace_rewrites_a_shared_page": (pg.PageModel, "_place_tail", _inplace_ignores_sharing),
+    "inplace_takes_the_next_page": (pg.PageModel, "_place_tail", _inplace_next_page),
+    "inplace_takes_fresh_pages": (pg.PageModel, "_place_tail", _inplace_counts_as_fresh),
     "sinks_ignored": (att, "attention", _sinks_ignored),
     "sink_carries_a_value": (att, "attention", _sink_carries_a_value),
     "window_one_key_too_wide": (att, "window_mask", _window_one_too_wide),
