@@ -60,7 +60,7 @@
 extern "C" {
 #endif
 
-#define SQ_ABI_VERSION 7
+#define SQ_ABI_VERSION 8
 
 typedef struct sq_store sq_store; /* opaque, library-owned host metadata */
 typedef int32_t sq_seq;           /* sequence handle: main thread or aux branch */
@@ -87,6 +87,18 @@ typedef enum {
                                      of a fresh page and a copy.  Logical
                                      views are the same; page tables and
                                      refcounts differ from the default. */
+#define SQ_STORE_EVICT_INPLACE 8u /* in-place eviction in sq_evict_spans: tail
+                                     page k of the compacted sequence is the
+                                     old page at the same list index (its
+                                     kept tokens rewritten there) whenever the
+                                     sequence alone holds that page; a fresh
+                                     page only replaces one another branch
+                                     still holds.  With no shared tail page
+                                     the eviction takes no page at all, so it
+                                     succeeds on a full pool.  Logical views
+                                     are the same; page tables differ from the
+                                     default.  Excludes SQ_STORE_EVICT_REMAP
+                                     and evict_chunk_pages > 0. */
 #define SQ_STORE_KV_FP8 4u        /* 8-bit KV cache (a model-serving option;
                                      the paper states no precision): the K and
                                      V pools hold E4M3 codes, one byte per
@@ -274,6 +286,11 @@ sq_status sq_release(sq_store *store, sq_seq seq);
  * from f/P on loses one reference.  Pages another live branch still holds
  * survive, so other branches keep attending to what they saw.  With
  * evict_chunk_pages > 0 the fresh pages come in chunks (see the config).
+ * With SQ_STORE_EVICT_INPLACE the tail is written into the sequence's own
+ * old pages instead (fresh pages only for pages another branch holds), one
+ * launch per run of tail pages that read no page the run writes except
+ * their own (each workgroup stages a page's sources before it writes it),
+ * or one pass in page order per (layer, KV head) where such runs are short.
  * With SQ_STORE_EVICT_REMAP a full tail page whose P kept tokens are one old
  * page's P tokens in order takes that old page by reference (no fresh page,
  * nothing copied): this happens behind every evicted run whose evicted

@@ -84,7 +84,26 @@ struct GatherArgs {
   NewIds ids;
 };
 
+// In-place eviction: tail pages [k0, k0 + n_pages) of the compacted
+// sequence, each filled from its kept tokens' old slots and written to
+// ids(k) (the old page at list index fp + k, or a fresh page).  Round mode
+// (sweep = 0): one workgroup per (page, layer * Hkv + head); no page of the
+// launch is read by another page of the launch.  Sweep mode (sweep = 1):
+// one workgroup per layer * Hkv + head takes the pages in order.
+struct InplaceArgs {
+  int32_t fp;
+  int32_t k0;
+  int32_t n_pages;
+  int32_t new_len;
+  int32_t sweep;
+  int32_t pad;
+  const int32_t *src_of;
+  const int32_t *pt_row;  // device page-table row, still holding the old ids
+  NewIds ids;             // destination id of tail page k (k counted from 0)
+};
+
 static_assert(sizeof(AppendArgs) < 4096, "append kernel arguments too large");
+static_assert(sizeof(InplaceArgs) + sizeof(Pools) < 4096, "in-place arguments too large");
 static_assert(sizeof(AppendBatchArgs) < 4096, "append-batch kernel arguments too large");
 static_assert(sizeof(EvictArgs) < 4096, "eviction index arguments too large");
 static_assert(sizeof(GatherArgs) + sizeof(Pools) < 4096, "gather arguments too large");
@@ -102,5 +121,6 @@ hipError_t launch_fill_i32(int32_t *dst, int32_t value, int32_t n, hipStream_t s
 hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s);
 hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStream_t s);
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s);
+hipError_t launch_evict_inplace(const Pools &p, const InplaceArgs &a, hipStream_t s);
 
 } // namespace sq

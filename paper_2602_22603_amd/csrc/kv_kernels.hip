@@ -436,6 +436,127 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
         p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
 }
 
+// ---------------------------------------------------------------------------
+// In-place eviction: tail page k of the compacted sequence is written to
+// ids(k), normally the old page at list index fp + k itself.  Its kept
+// tokens come from old list indices >= fp + k, so a page is never read after
+// a page before it in the tail has been rewritten, as long as the pages of
+// one launch read no page of the launch but their own: the host cuts the
+// tail into such runs (round mode, one workgroup per page and layer * Hkv +
+// head, like the gather), or hands a run of short ones to sweep mode, where
+// one workgroup per layer * Hkv + head takes the pages in order.  Either way
+// a workgroup stages everything a page needs (K rows, the V^T of its source
+// pages, positions) in LDS, waits at a barrier until every load of the page
+// has landed, and only then writes the page, which may be one of its own
+// sources.
+template <int D, class E>
+__global__ __launch_bounds__(256) void k_evict_inplace(Pools p, InplaceArgs a) {
+  constexpr int U = D * (int)sizeof(E) / 16;      // 16-byte units per K row
+  constexpr int VU = D * P * (int)sizeof(E) / 16; // 16-byte units of one page's V^T
+  constexpr int EPU = 16 / (int)sizeof(E);        // V^T elements per unit
+  constexpr int kMaxSrc = 4;                       // source pages staged whole
+  __shared__ int spage[P];
+  __shared__ int sslot[P];
+  __shared__ int sidx[P];
+  __shared__ int upage[P];
+  __shared__ int uidx[P];
+  __shared__ int nvalid;
+  __shared__ int n_up;
+  __shared__ uint4 kbuf[P * U];
+  __shared__ uint4 vbuf[kMaxSrc][VU]; // source pages, or the assembled page
+  __shared__ int32_t pbuf[P];
+  int pl0, pl1, lh;
+  if (a.sweep) {
+    pl0 = 0;
+    pl1 = a.n_pages;
+    lh = blockIdx.x;
+  } else {
+    // consecutive pages of one KV row to one XCD, as in the gather
+    const int n = gridDim.x;
+    const int total = n * gridDim.y;
+    const int lin = blockIdx.x + blockIdx.y * n;
+    const int x = lin % 8, q = total / 8, r = total % 8;
+    const int w = x * q + min(x, r) + lin / 8;
+    pl0 = w % n;
+    pl1 = pl0 + 1;
+    lh = w / n;
+  }
+  const int layer = lh / p.hkv;
+  const int head = lh % p.hkv;
+  for (int pl = pl0; pl < pl1; ++pl) {
+    const int k = a.k0 + pl;
+    const int t0 = (a.fp + k) * P;
+    const int dst_page = new_page_id(a.ids, k);
+    if (threadIdx.x < P) {
+      const int t = t0 + threadIdx.x;
+      if (t < a.new_len) {
+        const int src = a.src_of[t];
+        spage[threadIdx.x] = a.pt_row[src / P];
+        sslot[threadIdx.x] = src % P;
+        sidx[threadIdx.x] = src / P;
+      }
+    }
+    if (threadIdx.x == 0) nvalid = min(P, a.new_len - t0);
+    __syncthreads();
+    const int nv = nvalid;
+    if ((int)threadIdx.x < nv) {
+      int f = 0;
+      for (int i = 1; i <= (int)threadIdx.x; ++i) f += sidx[i] != sidx[i - 1];
+      uidx[threadIdx.x] = f;
+      upage[f] = spage[threadIdx.x];
+      if ((int)threadIdx.x == nv - 1) n_up = f + 1;
+    }
+    // ---- read: everything the page needs, into LDS ----
+    for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) {
+      const int j = idx / U, u = idx % U;
+      kbuf[idx] = reinterpret_cast<const uint4 *>(chunk_of<E>(p.k, p, layer, spage[j], head) +
+                                                  sslot[j] * D)[u];
+    }
+    if (lh == 0 && (int)threadIdx.x < nv)
+      pbuf[threadIdx.x] = p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
+    __syncthreads(); // n_up
+    const int nu = n_up;
+    if (nu <= kMaxSrc) {
+      for (int u = 0; u < nu; ++u) {
+        const uint4 *vs = reinterpret_cast<const uint4 *>(chunk_of<E>(p.v, p, layer, upage[u], head));
+        for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) vbuf[u][idx] = vs[idx];
+      }
+    } else {
+      E *vo = reinterpret_cast<E *>(&vbuf[0][0]);
+      for (int idx = threadIdx.x; idx < D * P; idx += blockDim.x) {
+        const int j = idx % P, d = idx / P;
+        vo[idx] = j < nv ? chunk_of<E>(p.v, p, layer, spage[j], head)[d * P + sslot[j]] : (E)0;
+      }
+    }
+    // every load of this page's sources has been written to LDS by now: the
+    // page itself may be overwritten
+    __syncthreads();
+    // ---- write ----
+    uint4 *kd = reinterpret_cast<uint4 *>(chunk_of<E>(p.k, p, layer, dst_page, head));
+    for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) kd[idx] = kbuf[idx];
+    E *vd = chunk_of<E>(p.v, p, layer, dst_page, head);
+    if (nu <= kMaxSrc) {
+      for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) {
+        const int d = idx / (P / EPU), c = idx % (P / EPU);
+        E out[EPU];
+#pragma unroll
+        for (int e = 0; e < EPU; ++e) {
+          const int j = c * EPU + e;
+          out[e] = j < nv ? reinterpret_cast<const E *>(vbuf[uidx[j]])[d * P + sslot[j]] : (E)0;
+        }
+        uint4 o;
+        __builtin_memcpy(&o, out, 16);
+        *reinterpret_cast<uint4 *>(vd + d * P + c * EPU) = o;
+      }
+    } else {
+      for (int idx = threadIdx.x; idx < VU; idx += blockDim.x)
+        reinterpret_cast<uint4 *>(vd)[idx] = vbuf[0][idx];
+    }
+    if (lh == 0 && (int)threadIdx.x < nv) p.pos[(int64_t)dst_page * P + threadIdx.x] = pbuf[threadIdx.x];
+    __syncthreads(); // the next page reuses the LDS
+  }
+}
+
 } // namespace
 
 // ---------------------------------------------------------------------------
@@ -519,6 +640,21 @@ hipError_t launch_evict_index(const EvictArgs &a, hipStream_t s) {
 hipError_t launch_write_ids(int32_t *dst, const NewIds &ids, int32_t n, hipStream_t s) {
   if (n == 0) return hipSuccess;
   hipLaunchKernelGGL(k_write_ids, dim3((n + 255) / 256), dim3(256), 0, s, dst, ids, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_evict_inplace(const Pools &p, const InplaceArgs &a, hipStream_t s) {
+  if (a.n_pages <= 0) return hipSuccess;
+  const dim3 grid = a.sweep ? dim3(p.nl * p.hkv) : dim3(a.n_pages, p.nl * p.hkv);
+  if (p.kv8) {
+    if (p.d == 128)
+      hipLaunchKernelGGL((k_evict_inplace<128, uint8_t>), grid, dim3(256), 0, s, p, a);
+    else
+      hipLaunchKernelGGL((k_evict_inplace<64, uint8_t>), grid, dim3(256), 0, s, p, a);
+  } else if (p.d == 128)
+    hipLaunchKernelGGL((k_evict_inplace<128, uint16_t>), grid, dim3(256), 0, s, p, a);
+  else
+    hipLaunchKernelGGL((k_evict_inplace<64, uint16_t>), grid, dim3(256), 0, s, p, a);
   return hipGetLastError();
 }
 

@@ -94,8 +94,12 @@ bool shape_ok(const sq_store_config *c, bool device, std::string *why) {
   if ((int64_t)c->max_pages_per_seq * c->page_size > (int64_t)INT32_MAX / 2)
     return bad("max_pages_per_seq * page_size too large");
   if (c->evict_chunk_pages < 0) return bad("evict_chunk_pages must be >= 0");
-  if (c->flags & ~(SQ_STORE_METADATA_ONLY | SQ_STORE_EVICT_REMAP | SQ_STORE_KV_FP8))
+  if (c->flags & ~(SQ_STORE_METADATA_ONLY | SQ_STORE_EVICT_REMAP | SQ_STORE_KV_FP8 |
+                   SQ_STORE_EVICT_INPLACE))
     return bad("unknown flags");
+  if ((c->flags & SQ_STORE_EVICT_INPLACE) &&
+      ((c->flags & SQ_STORE_EVICT_REMAP) || c->evict_chunk_pages > 0))
+    return bad("in-place eviction excludes remap and evict_chunk_pages");
   if (c->flags & SQ_STORE_KV_FP8) {
     if (!c->kv_scales) return bad("an 8-bit store needs kv_scales");
     for (int i = 0; i < 2 * c->num_layers; ++i)
@@ -282,7 +286,6 @@ struct sq_store {
   int64_t last_evict_L = 0, last_evict_Lp = 0;
 
   // tuning
-  int grid_rounds = 1;        // workgroups per launch = rounds * CUs * workgroups per CU
   int cus = 256;              // compute units (device query in device mode)
   int wg_per_cu[2] = {8, 3};  // resident workgroups per CU (VALU, MFMA), from occupancy
   int min_wg_pages_valu = 8;
@@ -290,8 +293,6 @@ struct sq_store {
   // flattened pages appended to every row of a launch (VALU, MFMA): a
   // piece's start-up cost in page equivalents, so the even split evens time
   int row_pad[2] = {2, 16};
-  bool auto_single_mfma = true;
-  int mfma_waves = 4; // waves per MFMA work item (1, 2 or 4)
 
   // every call that changes sequence metadata bumps gen; a begun decode
   // step is valid while gen is what sq_step_begin left
@@ -486,9 +487,8 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes();
   const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
-  // AUTO in an 8-bit store reads every sequence on the MFMA tile
-  const bool single_mfma = mode == SQ_ATTN_MFMA ||
-                           (mode == SQ_ATTN_AUTO && (s->auto_single_mfma || s->kv8));
+  // AUTO reads a sequence on its own on the MFMA tile too
+  const bool single_mfma = mode == SQ_ATTN_MFMA || mode == SQ_ATTN_AUTO;
 
   auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
                      const std::vector<int> &members, int32_t tok0 = 0) {
@@ -615,8 +615,8 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     return fail(SQ_ERR_INVALID, "decode batch needs %d segments (max %d)", (int)plan->segs.size(),
                 sq::kMaxSegs);
   // Each launch lays its segments' rows (segment, KV head) end to end in one
-  // flattened page range and splits it evenly over its workgroups: enough
-  // workgroups to fill the GPU `grid_rounds` times, at least `min_wg_pages`
+  // flattened page range and splits it evenly over its workgroups: at most
+  // one round of the GPU's resident workgroups, at least `min_wg_pages`
   // pages each, never more workgroups than pages.
   const int hkv = s->cfg.num_kv_heads;
   int count[2] = {0, 0};
@@ -636,7 +636,7 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   for (int L = 0; L < 2; ++L) {
     if (plan->total[L] == 0) continue;
     if (plan->total[L] > INT32_MAX) return fail(SQ_ERR_INVALID, "decode batch too large");
-    const int64_t fill = (int64_t)s->grid_rounds * s->cus * s->wg_per_cu[L];
+    const int64_t fill = (int64_t)s->cus * s->wg_per_cu[L];
     const int64_t min_pages = L == 1 ? s->min_wg_pages_mfma : s->min_wg_pages_valu;
     int64_t n = std::min<int64_t>(fill, (plan->total[L] + min_pages - 1) / min_pages);
     n = std::max<int64_t>(1, std::min<int64_t>(n, plan->total[L]));
@@ -779,20 +779,6 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
   for (int32_t i = 0; i < cfg->num_pages; ++i) s->freebits[i / 64] |= 1ull << (i % 64);
   s->n_free = cfg->num_pages;
   s->seqs.resize(cfg->max_seqs);
-  if (const char *e = std::getenv("SQ_GRID_ROUNDS")) {
-    const int v = std::atoi(e);
-    if (v >= 1 && v <= 64) s->grid_rounds = v;
-  }
-  for (int L = 0; L < 2; ++L)
-    if (const char *e = std::getenv(L ? "SQ_ROW_PAD_MFMA" : "SQ_ROW_PAD_VALU")) {
-      const int v = std::atoi(e);
-      if (v >= 0 && v <= 4096) s->row_pad[L] = v;
-    }
-  if (const char *e = std::getenv("SQ_AUTO_SINGLE")) s->auto_single_mfma = std::strcmp(e, "valu") != 0;
-  if (const char *e = std::getenv("SQ_MFMA_WAVES")) {
-    const int v = std::atoi(e);
-    if (v == 1 || v == 2 || v == 4) s->mfma_waves = v;
-  }
   if (device) {
     s->lay = lay;
     char *ws = static_cast<char *>(cfg->workspace);
@@ -841,10 +827,10 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
           hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
           cus > 0)
         s->cus = cus;
-      if (sq::decode_blocks_per_cu(s->kv8 ? 3 : 0, s->D, s->G, 1, &nb) == hipSuccess && nb > 0)
+      if (sq::decode_blocks_per_cu(s->kv8 ? 3 : 0, s->D, s->G, &nb) == hipSuccess && nb > 0)
         s->wg_per_cu[0] = nb;
       nb = 0;
-      if (sq::decode_blocks_per_cu(s->kv8 ? 2 : 1, s->D, s->G, s->mfma_waves, &nb) == hipSuccess && nb > 0)
+      if (sq::decode_blocks_per_cu(s->kv8 ? 2 : 1, s->D, s->G, &nb) == hipSuccess && nb > 0)
         s->wg_per_cu[1] = nb;
     }
     void *host = nullptr;
@@ -1233,6 +1219,59 @@ sq_status evict_deferred(sq_store *s, sq_seq h, const std::vector<int32_t> &ids,
   s->last_stream = strm;
   return upload_mask_row(s, h, strm);
 }
+// Launches of an in-place eviction.  Tail page k reads old list indices
+// lo(k) .. hi(k), all >= fp + k.  A round [a, b) of tail pages can run as
+// one parallel launch when no page of it reads the old page of another page
+// of it (each reads its own before writing it): with every page's read
+// range taken whole, adding page b is safe unless [lo(a), max hi] covers
+// fp + b.  Rounds grow with the evicted tokens before them; when the rounds
+// number more than kMaxInplaceRounds, the first ones run as one sweep (each
+// workgroup takes their pages in order).
+constexpr int64_t kMaxInplaceRounds = 64;
+
+sq_status evict_inplace_launches(sq_store *s, sq_seq h, int64_t fp, int64_t n_new, int64_t Lp,
+                                 const std::function<int64_t(int64_t)> &src_index,
+                                 const sq::NewIds &ids, hipStream_t strm) {
+  const int64_t P = s->P;
+  auto lo_of = [&](int64_t k) { return src_index((fp + k) * P) / P; };
+  auto hi_of = [&](int64_t k) { return src_index(std::min((fp + k + 1) * P, Lp) - 1) / P; };
+  std::vector<std::pair<int64_t, int64_t>> rounds;
+  for (int64_t a = 0; a < n_new;) {
+    const int64_t lo = lo_of(a);
+    int64_t hi = hi_of(a), b = a + 1;
+    while (b < n_new && !(lo <= fp + b && fp + b <= hi)) hi = std::max(hi, hi_of(b++));
+    rounds.push_back({a, b});
+    a = b;
+  }
+  size_t first = 0; // rounds before it go to one sweep
+  if ((int64_t)rounds.size() > kMaxInplaceRounds) first = rounds.size() - (kMaxInplaceRounds - 1);
+  auto launch = [&](int64_t k0, int64_t n, int sweep) {
+    sq::InplaceArgs ia{};
+    ia.fp = (int32_t)fp;
+    ia.k0 = (int32_t)k0;
+    ia.n_pages = (int32_t)n;
+    ia.new_len = (int32_t)Lp;
+    ia.sweep = sweep;
+    ia.src_of = s->ev_src;
+    ia.pt_row = s->pt_row(h);
+    ia.ids = ids;
+    ProfPair pp;
+    const bool on = s->prof_begin(strm, &pp, kProfGather);
+    hipError_t e = sq::launch_evict_inplace(s->pools, ia, strm);
+    s->prof_end(strm, &pp, on);
+    return e == hipSuccess ? SQ_OK : hip_fail(e, "in-place eviction");
+  };
+  if (first > 0) {
+    sq_status r = launch(0, rounds[first].first, 1);
+    if (r != SQ_OK) return r;
+  }
+  for (size_t i = first; i < rounds.size(); ++i) {
+    sq_status r = launch(rounds[i].first, rounds[i].second - rounds[i].first, 0);
+    if (r != SQ_OK) return r;
+  }
+  return SQ_OK;
+}
+
 } // namespace
 
 sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32_t n,
@@ -1317,6 +1356,17 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
         ++n_alias;
       }
     }
+  // In-place: tail page k is the old page at list index fp + k, rewritten,
+  // when this sequence alone holds it.
+  const bool inplace = (s->cfg.flags & SQ_STORE_EVICT_INPLACE) != 0;
+  int64_t n_inplace = 0;
+  if (inplace)
+    for (int64_t k = 0; k < n_new; ++k)
+      if (s->refcount[q->pages[fp + k]] == 1) {
+        alias[k] = q->pages[fp + k];
+        old_aliased[k] = 1;
+        ++n_inplace;
+      }
   auto fresh_in = [&](int64_t k0, int64_t c) {
     int64_t n = 0;
     for (int64_t k = k0; k < k0 + c; ++k) n += alias[k] < 0;
@@ -1430,7 +1480,12 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
     hipError_t e = sq::launch_evict_index(ea, strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "eviction index");
+    if (inplace) {
+      sq_status is = evict_inplace_launches(s, h, fp, n_new, Lp, src_index, all, strm);
+      if (is != SQ_OK) return is;
+    }
     for (const Step &st : steps) {
+      if (inplace) break;
       if (st.c == 0 || fresh_in(st.k0, st.c) == 0) continue; // nothing to copy
       sq::GatherArgs ga{};
       ga.fp = (int32_t)fp;
@@ -1501,13 +1556,13 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
   }
   q->kmask.clear(); // the masked slots are gone (their device row stays dirty)
   q->n_masked = 0;
-  const int64_t moved = Lp - fp * s->P - n_alias * s->P;
+  const int64_t moved = Lp - fp * s->P - n_alias * s->P; // in-place pages are rewritten
   const int64_t per_tok =
       (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes() + 4;
   es.tokens_removed = removed;
   es.tokens_moved = moved;
   es.bytes_moved = moved * per_tok;
-  es.pages_allocated = n_new - n_alias;
+  es.pages_allocated = n_new - n_alias - n_inplace;
   es.pages_remapped = n_alias;
   es.pages_freed = freed;
   es.first_evicted = f;
@@ -1590,7 +1645,7 @@ sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int3
     ProfPair pp;
     const bool on = s->prof_begin(strm, &pp, pass == 0 ? kProfValu : kProfMfma);
     hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, da[pass], strm)
-                             : sq::launch_decode_mfma(s->D, s->G, s->mfma_waves, da[pass], strm);
+                             : sq::launch_decode_mfma(s->D, s->G, da[pass], strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "decode kernel");
   }
@@ -1616,8 +1671,6 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   if (r != SQ_OK) return r;
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
   if (window < 0) return fail(SQ_ERR_INVALID, "window %d < 0", window);
-  if (s->device && mode != SQ_ATTN_STREAM && s->mfma_waves != 4)
-    return fail(SQ_ERR_INVALID, "decode steps need 4 waves per MFMA work item");
   // attention over the tokens before the step; the new ones join in the
   // merge (a window of W keys: the new token and the last W - 1 old ones)
   Plan plan, plan_w;
@@ -1631,8 +1684,7 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   }
   // which launches a layer makes depends on the mode only, so that a
   // captured step replays for every later step of the same batch and mode
-  const bool launch[2] = {mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX ||
-                              (mode == SQ_ATTN_AUTO && !s->auto_single_mfma && !s->kv8),
+  const bool launch[2] = {mode == SQ_ATTN_STREAM || mode == SQ_ATTN_SHARED_PREFIX,
                           mode != SQ_ATTN_STREAM};
   for (int L = 0; L < 2; ++L)
     if ((plan.n_wg[L] > 0 || plan_w.n_wg[L] > 0) && !launch[L])
@@ -1668,7 +1720,7 @@ sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32
   st.mode = mode;
   for (int L = 0; L < 2; ++L) {
     st.launch[L] = launch[L];
-    st.grid[L] = s->grid_rounds * s->cus * s->wg_per_cu[L]; // >= plan.n_wg[L]
+    st.grid[L] = s->cus * s->wg_per_cu[L]; // >= plan.n_wg[L]
   }
   st.kv_bytes = plan.kv_bytes + batch * tok_bytes;
   st.kv_bytes_logical = plan.kv_bytes_logical + batch * tok_bytes;
@@ -1739,7 +1791,7 @@ sq_status sq_step_attn_ex(sq_store *s, int32_t layer, const void *k_new, const v
     const bool on = prof && s->prof_begin(strm, &pp, L == 0 ? kProfValu : kProfMfma);
     const sq::DecodeDyn *dd = win ? s->step_dev->dec_w : s->step_dev->dec;
     hipError_t e = L == 0 ? sq::launch_step_valu(s->D, s->G, ds, &dd[0], st.grid[0], strm)
-                          : sq::launch_step_mfma(s->D, s->G, s->mfma_waves, ds, &dd[1], st.grid[1], strm);
+                          : sq::launch_step_mfma(s->D, s->G, ds, &dd[1], st.grid[1], strm);
     s->prof_end(strm, &pp, on);
     if (e != hipSuccess) return hip_fail(e, "decode step kernel");
   }

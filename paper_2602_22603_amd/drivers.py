@@ -58,7 +58,7 @@ def shared_task_inputs(w, t, device="cuda", layers=1, hkv=8, d=128):
 
 
 def build_compaction64k(device="cuda", extra_tokens=256, evict_chunk_pages=0, align=0,
-                        evict_remap=False):
+                        evict_remap=False, evict_inplace=False):
     """The 64K compaction workload: one sequence with its 40 tool spans
     marked (with ``align`` > 0 each span's ends rounded down to a multiple of
     it, as when every tool response starts on a page).  Returns (store,
@@ -67,7 +67,8 @@ def build_compaction64k(device="cuda", extra_tokens=256, evict_chunk_pages=0, al
     L = w.length
     store = _sq.Store(1, 32, 8, 128, num_pages=2 * (L // 16) + 2 * (extra_tokens // 16) + 64,
                       max_seqs=4, max_pages_per_seq=L // 16 + extra_tokens // 16 + 32,
-                      device=device, evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap)
+                      device=device, evict_chunk_pages=evict_chunk_pages, evict_remap=evict_remap,
+                      **({"evict_inplace": True} if evict_inplace else {}))
     k = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000, device)
     v = wl.device_normal_bf16((1, L, 8, 128), w.seed * 1000 + 1, device)
     base = store.seq_create()
@@ -132,7 +133,7 @@ def _extend_all_layers(store, seq, n, num_layers, seed, device):
 
 def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers=36,
                    device="cuda", decode=True, on_turn=None, store=None, evict_chunk_pages=0,
-                   extend=False):
+                   extend=False, evict_inplace=False):
     """Algorithm 1 over a synthetic task: a non-evictable prefix, then turns
     of reasoning plus one tool response each.  Phase 1 evicts the cursors the
     auxiliary thread named (when it has finished) and releases it; Phase 2
@@ -144,7 +145,8 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
     called after it.  Returns (store, main, aux, log, workload): aux is the
     auxiliary thread still alive after the last turn (or None); log has one
     record per turn.  evict_chunk_pages > 0 evicts in chunks of that many
-    fresh pages (bounded transient pages).  With ``extend`` every appended
+    fresh pages (bounded transient pages); ``evict_inplace`` rewrites the
+    sequence's own pages (no transient pages).  With ``extend`` every appended
     chunk (the auxiliary prompt, each turn) also runs its causal extend
     attention over every layer, timed in the record."""
     import torch
@@ -155,7 +157,7 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
     if store is None:
         store = _sq.Store(num_layers, 32, 8, 128, num_pages=pages + pages // 8 + 64, max_seqs=4,
                           max_pages_per_seq=max_tok // 16 + 64, device=device,
-                          evict_chunk_pages=evict_chunk_pages)
+                          evict_chunk_pages=evict_chunk_pages, evict_inplace=evict_inplace)
     main = store.seq_create()
     k, v = full_stack_inputs(w, -1, device)
     store.append(main, k, v)

@@ -19,6 +19,7 @@ OK, ERR_INVALID, ERR_NO_PAGES, ERR_UNKNOWN_SEQ, ERR_UNKNOWN_CURSOR, ERR_SPAN, ER
 STORE_METADATA_ONLY = 1
 STORE_EVICT_REMAP = 2
 STORE_KV_FP8 = 4
+STORE_EVICT_INPLACE = 8
 EVICT_DEFER = 1
 ATTN_AUTO, ATTN_STREAM, ATTN_SHARED_PREFIX, ATTN_MFMA = 0, 1, 2, 3
 MAX_BATCH = 64
@@ -200,7 +201,7 @@ class Store:
 
     def __init__(self, num_layers, num_q_heads, num_kv_heads, head_dim, num_pages, max_seqs,
                  max_pages_per_seq, page_size=16, device="cuda", metadata_only=False,
-                 evict_chunk_pages=0, evict_remap=False, kv_scales=None):
+                 evict_chunk_pages=0, evict_remap=False, kv_scales=None, evict_inplace=False):
         """kv_scales: [num_layers][2] K and V scales of an 8-bit (E4M3) store
         (None: bf16 pools)."""
         self.cfg = StoreConfig(num_layers, num_q_heads, num_kv_heads, head_dim, page_size,
@@ -208,13 +209,15 @@ class Store:
         self.cfg.evict_chunk_pages = evict_chunk_pages
         self.evict_chunk_pages = evict_chunk_pages
         self.evict_remap = bool(evict_remap)
+        self.evict_inplace = bool(evict_inplace)
         self.metadata_only = metadata_only
         self.num_layers, self.num_q_heads, self.num_kv_heads = num_layers, num_q_heads, num_kv_heads
         self.head_dim, self.page_size, self.num_pages = head_dim, page_size, num_pages
         self.max_seqs, self.max_pages_per_seq = max_seqs, max_pages_per_seq
         L = lib()
         self._handle = C.c_void_p()
-        self.cfg.flags = STORE_EVICT_REMAP if evict_remap else 0
+        self.cfg.flags = (STORE_EVICT_REMAP if evict_remap else 0) | \
+            (STORE_EVICT_INPLACE if evict_inplace else 0)
         self.kv_fp8 = kv_scales is not None
         self.kv_scales = None
         if self.kv_fp8:

@@ -44,11 +44,11 @@ def test_library_exports_every_declared_symbol(sq):
     assert lib.sq_abi_version() == version
 
 
-def _store(sq, num_pages, page, max_seqs, max_pages, chunk=0, remap=False):
+def _store(sq, num_pages, page, max_seqs, max_pages, chunk=0, remap=False, inplace=False):
     return sq.Store(num_layers=2, num_q_heads=4, num_kv_heads=2, head_dim=8,
                     num_pages=num_pages, max_seqs=max_seqs, max_pages_per_seq=max_pages,
                     page_size=page, metadata_only=True, evict_chunk_pages=chunk,
-                    evict_remap=remap)
+                    evict_remap=remap, evict_inplace=inplace)
 
 
 def _compare(store, model):
@@ -85,16 +85,19 @@ def _both(store, model, sq, fn_store, fn_model):
 
 
 @pytest.mark.parametrize("page", [1, 2, 4, 16])
-@pytest.mark.parametrize("seed,chunk,remap,deferred",
-                         [(0, 0, False, False), (1, 0, False, False), (2, 1, False, False),
-                          (3, 2, False, False), (4, 5, False, False), (5, 0, True, False),
-                          (6, 2, True, False), (7, 0, False, True), (8, 2, True, True)])
-def test_random_ops_match_oracle(sq, page, seed, chunk, remap, deferred):
+@pytest.mark.parametrize("seed,chunk,remap,deferred,inplace",
+                         [(0, 0, False, False, False), (1, 0, False, False, False),
+                          (2, 1, False, False, False), (3, 2, False, False, False),
+                          (4, 5, False, False, False), (5, 0, True, False, False),
+                          (6, 2, True, False, False), (7, 0, False, True, False),
+                          (8, 2, True, True, False), (9, 0, False, False, True),
+                          (10, 0, False, True, True)])
+def test_random_ops_match_oracle(sq, page, seed, chunk, remap, deferred, inplace):
     rng = np.random.default_rng(100 + seed * 7 + page)
     num_pages, max_seqs, max_pages = 300 // page + 40, 5, 400 // page + 8
-    store = _store(sq, num_pages, page, max_seqs, max_pages, chunk, remap)
+    store = _store(sq, num_pages, page, max_seqs, max_pages, chunk, remap, inplace)
     model = pg.PageModel(num_pages, page, max_seqs, max_pages, evict_chunk_pages=chunk,
-                         evict_remap=remap)
+                         evict_remap=remap, evict_inplace=inplace)
     cursor = 0
     h0, _ = _both(store, model, sq, store.seq_create, model.seq_create)
     for _ in range(250):
