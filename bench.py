@@ -47,9 +47,11 @@ def parse_args():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--tasks", type=int, default=8)
     ap.add_argument("--ctx", type=int, default=131072)
-    ap.add_argument("--legs", default="decode,modes,evict,extend,outlier,variants,fp8,fullstack,cpu",
-                    help="comma list of: decode, modes, evict, extend, outlier, fullstack, cpu, copy "
-                         "(a plain 1 GiB device copy used to calibrate HBM byte counters)")
+    ap.add_argument("--legs",
+                    default="decode,modes,evict,extend,outlier,variants,fp8,fullstack,postevict,cpu",
+                    help="comma list of: decode, modes, evict, extend, outlier, variants, fp8, "
+                         "fullstack, postevict, cpu, copy (a plain 1 GiB device copy used to "
+                         "calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     return ap.parse_args()
 
@@ -258,48 +260,98 @@ def time_events(torch, fn, reps, flush=None):
     return percentiles([a.elapsed_time(b) for a, b in ev])
 
 
-def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False):
+def evict_bytes(stats, length, kept):
+    """Algorithmic bytes of one eviction: the moved tokens' K, V (every layer
+    and head) and positions read and written, plus the index arrays (keep
+    u8 and dst i32 per old token, src_of i32 per kept token) and the fresh
+    page ids written to the page table."""
+    return 2 * stats["bytes_moved"] + 5 * length + 4 * kept + 4 * stats["pages_allocated"]
+
+
+def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False, inplace=False):
+    """The 64K compaction: sq_evict_spans of 40 tool spans (>= 65% of the
+    tokens) on a branch forked over the whole context, repeated.  Timed
+    warm (back to back: the ~180 MB read and written fit the 256 MB MALL)
+    and cold (a 1 GiB write flushes the MALL and L2 before each call).
+    GB/s divide the algorithmic bytes by the index kernel plus the gather
+    (HIP events around each kernel), and by the wall clock of the whole call."""
     from paper_2602_22603_amd import drivers
     store, base, w, k, v = drivers.build_compaction64k(evict_chunk_pages=chunk, align=align,
-                                                       evict_remap=remap)
+                                                       evict_remap=remap, evict_inplace=inplace)
     L = w.length
-    del k, v
+    if not inplace:
+        del k, v
     torch.cuda.synchronize()
-    walls, stats = [], None
-    store.profile_enable(True)
-    for r in range(reps + 2):
-        f = store.fork(base, L)  # aligned: aliases every page of the base
-        torch.cuda.synchronize()
-        if r == 2:
-            store.profile_read()
-        t0 = time.perf_counter()
-        stats = store.evict(f, w.evict_ids)
-        torch.cuda.synchronize()
-        if r >= 2:
-            walls.append(time.perf_counter() - t0)
-        if r < reps + 1:
+    flush = Flusher(torch)
+    med = lambda xs: sorted(xs)[len(xs) // 2]
+    runs = {}
+    stats = None
+
+    def victim():
+        """The sequence to evict from: a branch forked over the whole
+        context (aligned: it aliases every page of the base), or, in place,
+        a sequence that alone holds its pages (appended anew)."""
+        if not inplace:
+            return store.fork(base, L)
+        h = store.seq_create()
+        store.append(h, k, v)
+        for c, (s0, e0) in enumerate(w.spans):
+            store.span_mark(h, c, s0, e0)
+        return h
+    for temp in ("warm", "cold"):
+        walls = []
+        store.profile_enable(True)
+        for r in range(reps + 1):
+            f = victim()
+            if temp == "cold":
+                flush()
+            torch.cuda.synchronize()
+            if r == 1:
+                store.profile_read()  # the first call warms up
+            t0 = time.perf_counter()
+            stats = store.evict(f, w.evict_ids)
+            torch.cuda.synchronize()
+            if r >= 1:
+                walls.append(time.perf_counter() - t0)
             store.release(f)
-    prof = store.profile_read()
-    store.profile_enable(False)
-    gather_ms = prof["evict_gather_ms"] / max(1, prof["evict_gather_launches"])
-    scan_ms = prof["evict_scan_ms"] / max(1, prof["evict_scan_launches"])
-    moved = 2 * stats["bytes_moved"]  # read + write
+        prof = store.profile_read()
+        store.profile_enable(False)
+        kern = (prof["evict_scan_ms"] + prof["evict_gather_ms"]) / reps
+        runs[temp] = dict(walls=walls, kern=kern, prof=prof)
+    kept = L - stats["tokens_removed"]
+    alg = evict_bytes(stats, L, kept)
+    wall = {t: med(runs[t]["walls"]) for t in runs}
+    prof = runs["cold"]["prof"]
+    per = lambda key, n: prof[key] / max(1, prof[n])
+    info = dict(
+        workload=f"64K tokens, 40 tool + 40 reasoning spans, evict >= 65% (got "
+                 f"{stats['tokens_removed'] / L:.3f})",
+        evict_chunk_pages=chunk, remap=remap, inplace=inplace, span_align=align,
+        tokens_removed=stats["tokens_removed"], tokens_moved=stats["tokens_moved"],
+        pages_allocated=stats["pages_allocated"], pages_remapped=stats["pages_remapped"],
+        bytes_read_plus_written=2 * stats["bytes_moved"], algorithmic_bytes=alg,
+        gather_launches_per_call=prof["evict_gather_launches"] // reps,
+        index_ms_cold=round(per("evict_scan_ms", "evict_scan_launches"), 5),
+        gather_ms_per_call_cold=round(prof["evict_gather_ms"] / reps, 5),
+        kernel_ms_per_call={t: round(runs[t]["kern"], 5) for t in runs},
+        evict_gbps_cold=round(alg / (runs["cold"]["kern"] * 1e-3) / 1e9, 1) if runs["cold"]["kern"] else None,
+        evict_gbps_warm=round(alg / (runs["warm"]["kern"] * 1e-3) / 1e9, 1) if runs["warm"]["kern"] else None,
+        evict_wall_ms_median={t: round(wall[t] * 1e3, 4) for t in wall},
+        evict_gbps_wall={t: round(alg / wall[t] / 1e9, 1) for t in wall})
+    if info["evict_gbps_cold"]:
+        info["frac_of_hbm_peak_cold"] = round(info["evict_gbps_cold"] / HBM_PEAK_GBPS, 4)
     if not decode:
-        info = dict(evict_chunk_pages=chunk, remap=remap, span_align=align,
-                    tokens_removed=stats["tokens_removed"], tokens_moved=stats["tokens_moved"],
-                    pages_allocated=stats["pages_allocated"], pages_remapped=stats["pages_remapped"],
-                    bytes_read_plus_written=2 * stats["bytes_moved"],
-                    gather_launches_per_call=prof["evict_gather_launches"] // reps,
-                    gather_ms_per_call=prof["evict_gather_ms"] / reps,
-                    evict_wall_ms_median=sorted(walls)[len(walls) // 2] * 1e3,
-                    evict_gbps_wall=2 * stats["bytes_moved"] / (sorted(walls)[len(walls) // 2]) / 1e9)
+        del flush
+        if inplace:
+            del k, v
         store.close()
         return info
     # decode on the compacted cache vs the full cache (batch 1)
+    f = store.fork(base, L)
+    store.evict(f, w.evict_ids)
     q = wl.device_normal_bf16((1, 32, 128), 77, "cuda")
     out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
     res, pct = {}, {}
-    flush = Flusher(torch)
     for name, seq in (("compacted", f), ("full", base)):
         step = lambda: store.decode(0, [seq], q, out=out)
         for _ in range(3):
@@ -312,18 +364,83 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False)
         res[name] = (time.perf_counter() - t0) * 1e3 / 32
         pct[name] = dict(warm=time_events(torch, step, 32), cold=time_events(torch, step, 16, flush))
     del flush
-    info = dict(
-        workload=f"64K tokens, 40 tool + 40 reasoning spans, evict >= 65% (got "
-                 f"{stats['tokens_removed'] / L:.3f})",
-        tokens_removed=stats["tokens_removed"], tokens_moved=stats["tokens_moved"],
-        bytes_read_plus_written=moved, gather_ms=gather_ms, scan_ms=scan_ms,
-        evict_gbps=moved / (gather_ms * 1e-3) / 1e9,
-        evict_gbps_wall=moved / (sorted(walls)[len(walls) // 2]) / 1e9,
-        evict_wall_ms_median=sorted(walls)[len(walls) // 2] * 1e3,
-        decode_ms_compacted=res["compacted"], decode_ms_full=res["full"],
-        decode_step_ms=pct)
+    info.update(decode_ms_compacted=res["compacted"], decode_ms_full=res["full"],
+                decode_step_ms=pct)
     store.close()
     return info
+
+
+def _decode_split(torch, store, seqs, q, out, reps, flush=None, layers=(0,)):
+    """Median wall time of a decode call (every layer in ``layers``, batch
+    ``seqs``; synchronised after each), and the library's kernel times per
+    call: decode kernel(s), merge, and what the call costs beyond them."""
+    def call():
+        for layer in layers:
+            store.decode(layer, seqs, q, out=out)
+    for _ in range(3):
+        call()
+    torch.cuda.synchronize()
+    walls = []
+    store.profile_enable(True)
+    store.profile_read()
+    for _ in range(reps):
+        if flush is not None:
+            flush()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        call()
+        torch.cuda.synchronize()
+        walls.append((time.perf_counter() - t0) * 1e3)
+    prof = store.profile_read()
+    store.profile_enable(False)
+    kv = store.plan_info(seqs)["kv_bytes"] * len(layers)
+    med = sorted(walls)[len(walls) // 2]
+    dec = (prof["decode_mfma_ms"] + prof["decode_valu_ms"]) / reps
+    mrg = prof["decode_merge_ms"] / reps
+    plan = store.plan_info(seqs)
+    return dict(call_ms=round(med, 4), kv_bytes=kv, gbps_call=round(kv / (med * 1e-3) / 1e9, 1),
+                decode_kernel_ms=round(dec, 4), merge_ms=round(mrg, 4),
+                other_ms=round(med - dec - mrg, 4),
+                gbps_decode_kernel=round(kv / (dec * 1e-3) / 1e9, 1) if dec else None,
+                workgroups=plan["n_items_mfma"] + plan["n_items_valu"])
+
+
+def post_eviction_leg(sq, torch, wl, reps=20):
+    """Decode where eviction leaves it: the 64K context after its tool spans
+    were evicted (22.7K tokens, batch 1), warm and cold; and the final
+    36-layer step of the full-stack task after one-shot, chunked and
+    in-place eviction (every layer, batch 1).  Each call split into decode
+    kernel, merge and the rest (launch gaps, host)."""
+    from paper_2602_22603_amd import drivers
+    res = {}
+    store, base, w, k, v = drivers.build_compaction64k()
+    del k, v
+    store.evict(base, w.evict_ids)
+    q = wl.device_normal_bf16((1, 32, 128), 77, "cuda")
+    out = torch.empty((1, 32, 128), dtype=torch.float32, device="cuda")
+    flush = Flusher(torch)
+    res["compacted64k"] = dict(tokens=store.seq_info(base)["length"],
+                               warm=_decode_split(torch, store, [base], q, out, 50),
+                               cold=_decode_split(torch, store, [base], q, out, 20, flush))
+    store.close()
+    del flush
+    torch.cuda.empty_cache()
+    for name, chunk, inplace in (("one_shot", 0, False), ("chunked_64", 64, False),
+                                 ("in_place", 0, True)):
+        store, main, aux, log, w = drivers.run_full_stack(evict=True, evict_chunk_pages=chunk,
+                                                          evict_inplace=inplace, decode=False)
+        seqs = [main] + ([aux] if aux is not None else [])
+        qq = wl.device_normal_bf16((len(seqs), 32, 128), 79, "cuda")
+        oo = torch.empty((len(seqs), 32, 128), dtype=torch.float32, device="cuda")
+        pt = store.page_table(main)
+        runs = 1 + sum(1 for i in range(1, len(pt)) if pt[i] != pt[i - 1] + 1)
+        res["full_stack_final_" + name] = dict(
+            tokens=store.seq_info(main)["length"], batch=len(seqs), page_id_runs=runs,
+            peak_pages=store.stats()["peak_pages"],
+            step=_decode_split(torch, store, seqs, qq, oo, 10, layers=range(w.num_layers)))
+        store.close()
+        torch.cuda.empty_cache()
+    return res
 
 
 def deferred_leg(sq, torch, wl, reps=8):
@@ -586,19 +703,23 @@ def fp8_leg(sq, torch, wl, steps=20, warmup=3):
 def fullstack_leg(sq, torch, wl):
     """36 layers, 16K prefix + 30 turns of 8K tokens, auxiliary thread every 4
     turns; with one-shot eviction, with eviction in 64-page chunks (bounded
-    transient pages) and without eviction: peak KV bytes, the causal extend
+    transient pages), in place (no transient pages) and without eviction:
+    peak KV bytes, the causal extend
     attention of every appended chunk (one-shot and no eviction) and the
     decode step (all 36 layers) at each turn's end."""
     from paper_2602_22603_amd import drivers
     page_bytes = 36 * 8 * 16 * 128 * 2 * 2
     res = {}
-    for name, ev, chunk in (("with_eviction", True, 0), ("with_chunked_eviction", True, 64),
-                            ("without_eviction", False, 0)):
+    for name, ev, chunk, inplace in (("with_eviction", True, 0, False),
+                                     ("with_chunked_eviction", True, 64, False),
+                                     ("with_inplace_eviction", True, 0, True),
+                                     ("without_eviction", False, 0, False)):
+        full = chunk == 0 and not inplace
         store, main, aux, log, w = drivers.run_full_stack(evict=ev, evict_chunk_pages=chunk,
-                                                          extend=chunk == 0)
+                                                          extend=full, evict_inplace=inplace)
         st = store.stats()
         paths = decode_step_paths(torch, wl, store, [main] + ([aux] if aux is not None else [])) \
-            if chunk == 0 else None
+            if full else None
         final = log[-1]
         dec = [r["decode_ms"] for r in log]
         ev_ms = [r["evict_ms"] for r in log if "evict_ms" in r]
@@ -610,9 +731,9 @@ def fullstack_leg(sq, torch, wl):
             decode_ms_sum_over_turns=round(sum(dec), 2),
             kv_bytes_read_over_turns=sum(r["kv_bytes"] for r in log),
             evictions=len(ev_ms), evict_ms_total=round(sum(ev_ms), 3),
-            evict_gbps=round(2 * moved / (sum(ev_ms) * 1e-3) / 1e9, 1) if ev_ms else None,
+            evict_gbps_wall=round(2 * moved / (sum(ev_ms) * 1e-3) / 1e9, 1) if ev_ms else None,
             extend_ms_over_turns=round(sum(r.get("extend_ms", 0) + r.get("aux_extend_ms", 0)
-                                           for r in log), 1) if chunk == 0 else None,
+                                           for r in log), 1) if full else None,
             decode_step_paths_final=paths)
         store.close()
         torch.cuda.empty_cache()
@@ -621,6 +742,8 @@ def fullstack_leg(sq, torch, wl):
     res["extend_time_reduction"] = round(1 - a["extend_ms_over_turns"] / b["extend_ms_over_turns"], 4)
     res["peak_kv_reduction_chunked"] = round(
         1 - res["with_chunked_eviction"]["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
+    res["peak_kv_reduction_inplace"] = round(
+        1 - res["with_inplace_eviction"]["peak_kv_bytes"] / b["peak_kv_bytes"], 4)
     res["kv_read_reduction"] = round(1 - a["kv_bytes_read_over_turns"] / b["kv_bytes_read_over_turns"], 4)
     return res
 
@@ -756,10 +879,14 @@ def main():
                         ("shared_prefix", sq.ATTN_SHARED_PREFIX)):
             log(f"timing mode {name} ...")
             r = time_steps(sq, torch, store, seqs, m, args.steps, args.warmup, kb, vb, qs, out)
+            # requested: the bytes the mode's launches read (a per-sequence
+            # mode reads each shared prefix once per sequence, and the
+            # caches serve part of the repeats); unique: each page once
             modes[name] = dict(ms_per_step=round(r["ms_per_step"], 4),
-                               gbps_unique_bytes=round(r["gbps"], 1),
-                               gbps_logical_bytes=round(r["kv_bytes_logical_per_step"] /
-                                                        (r["ms_per_step"] * 1e-3) / 1e9, 1),
+                               kv_bytes_requested_per_step=r["kv_bytes_per_step"],
+                               gbps_requested_bytes=round(r["gbps"], 1),
+                               gbps_unique_bytes=round(main_res["kv_bytes_per_step"] /
+                                                       (r["ms_per_step"] * 1e-3) / 1e9, 1),
                                tokens_per_s=round(r["tokens_per_s"], 1))
         # the per-sequence kernels on unique pages: the 8 main threads alone
         mains = seqs[0::2]
@@ -788,6 +915,8 @@ def main():
         evict["page_aligned_spans_copy"] = evict_leg(sq, torch, wl, decode=False, align=16)
         evict["page_aligned_spans_remap"] = evict_leg(sq, torch, wl, decode=False, align=16,
                                                       remap=True)
+        # the tail rewritten in the sequence's own pages (no transient page)
+        evict["in_place"] = evict_leg(sq, torch, wl, decode=False, inplace=True)
         evict["deferred"] = deferred_leg(sq, torch, wl)
     if "copy" in legs:
         log("calibration copy: 1 GiB device-to-device ...")
@@ -820,6 +949,11 @@ def main():
     if "fullstack" in legs:
         log("full-stack leg (36 layers, 16K -> 256K) ...")
         fullstack = fullstack_leg(sq, torch, wl)
+    post = None
+    if "postevict" in legs:
+        log("post-eviction decode leg (compacted 64K; 36-layer final steps) ...")
+        post = post_eviction_leg(sq, torch, wl)
+        torch.cuda.empty_cache()
     cpu = None
     if "cpu" in legs:
         log("oracle CPU baseline ...")
@@ -858,6 +992,7 @@ def main():
         "attention_options": variants,
         "kv_fp8": fp8,
         "full_stack": fullstack,
+        "post_eviction_decode": post,
         "cpu_baseline": cpu,
         "kernel_sources_sha": kernel_sha(),
         "extend_kernel_sources_sha": kernel_sha(EXTEND_SOURCES),
