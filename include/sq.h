@@ -192,7 +192,7 @@ typedef struct {
   int32_t n_items_valu;     /* work items of the VALU split kernel */
   int32_t n_items_mfma;     /* work items of the MFMA tile kernel */
   int32_t chunk_pages;      /* pages per work item */
-  int32_t reserved;
+  int32_t n_slots;          /* partial slots (16 query rows each) the launches write */
   int64_t kv_bytes;         /* K/V bytes the call reads, shared pages once */
   int64_t kv_bytes_logical; /* K/V bytes with every sequence's pages counted */
   int64_t kv_bytes_valu;    /* part of kv_bytes read by the VALU kernel */
@@ -351,6 +351,27 @@ sq_status sq_keep_flags(sq_store *store, sq_seq seq, uint8_t *out, int64_t cap, 
  * metadata-only store. */
 sq_status sq_decode_attn(sq_store *store, int32_t layer, const sq_seq *seqs, int32_t batch,
                          const void *q, float *out, float scale, int32_t mode, void *stream);
+
+/* ---- decode attention without the workspace's partial buffers ----------
+ * For callers that cannot allocate device memory around a call (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * sq_decode_attn with the same arguments, kernels and result (bit for bit),
+ * whose split partials (m, l, acc of every workgroup's piece) live in a
+ * device array the library holds on each GPU it runs on, instead of the
+ * store's workspace.  The array holds SQ_NOALLOC_PARTIAL_SLOTS slots of 16
+ * query rows (34 MB) and stays allocated until the process ends; nothing in
+ * it needs clearing (every slot a call reads, the same call writes first).
+ * Every call on one GPU, from any store, uses the same array: calls that
+ * may overlap on one GPU (other streams, other host threads) race, so order
+ * them on one stream.  The call allocates nothing and records no profiling
+ * events.  SQ_ERR_INVALID as sq_decode_attn, and for a call whose work
+ * split needs more than SQ_NOALLOC_PARTIAL_SLOTS slots (with up to 8 KV
+ * heads every mode fits); SQ_ERR_HIP if the array's address could not be
+ * found when the store was created. */
+#define SQ_NOALLOC_PARTIAL_SLOTS 4096
+sq_status sq_decode_attn_noalloc(sq_store *store, int32_t layer, const sq_seq *seqs,
+                                 int32_t batch, const void *q, float *out, float scale,
+                                 int32_t mode, void *stream);
 
 /* ---- decode step with the append fused (graph-capturable) ----------------
  * The decode loop of §3.1 appends one token to every running thread and

@@ -169,6 +169,17 @@ hipError_t launch_step_valu(int d, int group, const DecodeStatic &st, const Deco
 hipError_t launch_step_mfma(int d, int group, const DecodeStatic &st, const DecodeDyn *dyn,
                             int n_wg, hipStream_t s);
 hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8, hipStream_t s);
+// Split-partial buffers of one decode call: m, l [slots][kRows] and acc
+// [slots][kRows][D].
+struct StaticPartials {
+  float *m = nullptr, *l = nullptr, *acc = nullptr;
+  int32_t slots = 0;
+};
+// Partial slots of the device array behind the allocation-free entry point.
+constexpr int kStaticSlots = 4096;
+// That array on the current device (its address looked up once per device).
+hipError_t static_partials(StaticPartials *out);
+
 // Workgroups of a decode kernel that fit on one CU.  kind: 0 VALU, 1 MFMA,
 // 2 the 8-bit MFMA kernel (four waves), 3 the 8-bit VALU kernel
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int *out);

@@ -40,6 +40,8 @@
 #include "decode_args.hpp"
 #include "fp8.hpp"
 
+#include <mutex>
+
 namespace sq {
 namespace {
 
@@ -1340,6 +1342,38 @@ hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8,
   else
     hipLaunchKernelGGL(k_step_merge<64>, grid, block, 0, s, a);
   return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Split partials of the allocation-free decode entry point: m [slots][kRows],
+// l [slots][kRows], acc [slots][kRows][128] (64-channel heads use the first
+// half of each acc slot's pitch-D rows), in a device array that every GPU the
+// library runs on holds until the process ends.  Host code never uses the
+// array's name as an address: the device address comes from
+// hipGetSymbolAddress, once per device, with that device current.
+static __device__ __align__(256) float scratch[kStaticSlots * kRows * (2 + 128)];
+
+hipError_t static_partials(StaticPartials *out) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void *addr[kMaxDevices] = {};
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void *p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    addr[dev] = p;
+  }
+  float *base = static_cast<float *>(addr[dev]);
+  out->m = base;
+  out->l = base + (int64_t)kStaticSlots * kRows;
+  out->acc = base + 2 * (int64_t)kStaticSlots * kRows;
+  out->slots = kStaticSlots;
+  return hipSuccess;
 }
 
 } // namespace sq

@@ -271,6 +271,10 @@ struct sq_store {
   uint8_t *ev_keep = nullptr;
   int32_t *ev_dst = nullptr, *ev_src = nullptr, *ev_upload = nullptr;
   float *part_m = nullptr, *part_l = nullptr, *part_acc = nullptr;
+  // the device array of the allocation-free decode entry point on this
+  // store's GPU (looked up at creation; spart_err if that failed)
+  sq::StaticPartials spart{};
+  hipError_t spart_err = hipErrorNotInitialized;
   int32_t *staging = nullptr;
   hipEvent_t staging_ev = nullptr;
   bool staging_pending = false;
@@ -466,6 +470,7 @@ struct Plan {
   int32_t seg_index[sq::kMaxSegs]; // index of each segment inside its launch
   bool pages_reread = false; // some page is read by more than one segment
   bool masked = false;       // some entry has slots masked by deferred evictions
+  int32_t n_slots = 0;       // partial slots the launches write
   int64_t kv_bytes = 0, kv_bytes_logical = 0, io_bytes = 0;
   int64_t kv_bytes_valu = 0, kv_bytes_mfma = 0;
 };
@@ -647,6 +652,7 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     plan->slot_base[L] = slots;
     slots += (int32_t)n + count[L] * hkv;
   }
+  plan->n_slots = slots;
   plan->io_bytes += (int64_t)batch * s->cfg.num_q_heads * s->cfg.head_dim * (2 + 4);
   return SQ_OK;
 }
@@ -657,17 +663,19 @@ uint16_t *layer_pool(sq_store *s, uint16_t *pool, int32_t layer) {
                                       layer * s->pools.layer_stride * (s->kv8 ? 1 : 2));
 }
 
-// The arguments of a layer's decode launches that no plan changes.
-sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float scale, bool nt) {
+// The arguments of a layer's decode launches that no plan changes (the
+// partials in the workspace, or in `pp`).
+sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float scale, bool nt,
+                               const sq::StaticPartials *pp = nullptr) {
   sq::DecodeStatic st{};
   st.q = static_cast<const uint16_t *>(q);
   st.k = layer_pool(s, s->pools.k, layer);
   st.v = layer_pool(s, s->pools.v, layer);
   st.pt = s->pt_dev;
   st.mask = s->mask_dev;
-  st.part_m = s->part_m;
-  st.part_l = s->part_l;
-  st.part_acc = s->part_acc;
+  st.part_m = pp ? pp->m : s->part_m;
+  st.part_l = pp ? pp->l : s->part_l;
+  st.part_acc = pp ? pp->acc : s->part_acc;
   st.page_stride = s->pools.page_stride;
   st.head_stride = s->pools.head_stride;
   st.max_pages = s->cfg.max_pages_per_seq;
@@ -680,15 +688,16 @@ sq::DecodeStatic decode_static(sq_store *s, int32_t layer, const void *q, float 
   return st;
 }
 
-sq::MergeStatic merge_static(sq_store *s, int32_t layer, float *out, const float *sinks) {
+sq::MergeStatic merge_static(sq_store *s, int32_t layer, float *out, const float *sinks,
+                             const sq::StaticPartials *pp = nullptr) {
   sq::MergeStatic st{};
   st.out = out;
   st.sinks = sinks;
   st.sink_scale = 1.4426950408889634f;
   st.out_scale = s->v_scale(layer); // 1 unless the store is 8-bit
-  st.part_m = s->part_m;
-  st.part_l = s->part_l;
-  st.part_acc = s->part_acc;
+  st.part_m = pp ? pp->m : s->part_m;
+  st.part_l = pp ? pp->l : s->part_l;
+  st.part_acc = pp ? pp->acc : s->part_acc;
   st.hq = s->cfg.num_q_heads;
   st.group = s->G;
   st.hkv = s->cfg.num_kv_heads;
@@ -833,6 +842,9 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
       if (sq::decode_blocks_per_cu(s->kv8 ? 2 : 1, s->D, s->G, &nb) == hipSuccess && nb > 0)
         s->wg_per_cu[1] = nb;
     }
+    // set-up of the allocation-free entry point: its device array's address
+    // on this GPU (a failure only disables that entry point)
+    s->spart_err = sq::static_partials(&s->spart);
     void *host = nullptr;
     hipError_t e = hipHostMalloc(&host, lay.upload_elems * 4, hipHostMallocDefault);
     if (e != hipSuccess) {
@@ -1029,6 +1041,69 @@ void take_one_token_each(sq_store *s, const sq_seq *seqs, int32_t batch, TokenSl
     q.next_pos += 1;
   }
   s->st.append_tokens += batch;
+}
+
+// One decode call: the partials in the store's workspace (pp null), or in
+// pp's buffers - the allocation-free entry point, which also records no
+// profiling events (creating one may allocate).
+sq_status decode_call(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch, const void *q,
+                      float *out, float scale, int32_t mode, const sq_attn_opts *opts,
+                      void *stream, const sq::StaticPartials *pp) {
+  sq_attn_opts o{};
+  sq_status r = take_opts(opts, &o);
+  if (r != SQ_OK) return r;
+  if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
+  if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
+  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
+  if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
+  if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
+  if (!q || !out || !aligned16(q) || !aligned16(out))
+    return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
+  if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
+  for (int b = 0; b < batch; ++b)
+    if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
+  Plan plan;
+  r = build_plan(s, seqs, batch, mode, &plan, o.window > 0 ? o.window : -1);
+  if (r != SQ_OK) return r;
+  if (plan.masked && o.window > 0)
+    return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
+  if (pp && plan.n_slots > pp->slots)
+    return fail(SQ_ERR_INVALID,
+                "this call needs %d partial slots; the allocation-free entry point holds %d",
+                plan.n_slots, pp->slots);
+
+  hipStream_t strm = static_cast<hipStream_t>(stream);
+  s->last_stream = strm;
+  if (plan.masked) {
+    r = clean_mask_rows(s, seqs, batch, strm);
+    if (r != SQ_OK) return r;
+  }
+  sq::DecodeArgs da[2]{};
+  sq::MergeArgs ma{};
+  da[0].st = decode_static(s, layer, q, scale, !plan.pages_reread, pp);
+  da[1].st = da[0].st;
+  ma.st = merge_static(s, layer, out, o.sinks, pp);
+  sq::DecodeDyn dyn[2]{};
+  fill_dyn(s, plan, dyn, &ma.dyn);
+  for (int pass = 0; pass < 2; ++pass) {
+    da[pass].dyn = dyn[pass];
+    if (da[pass].dyn.n_wg == 0) continue;
+    ProfPair pe;
+    const bool on = !pp && s->prof_begin(strm, &pe, pass == 0 ? kProfValu : kProfMfma);
+    hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, da[pass], strm)
+                             : sq::launch_decode_mfma(s->D, s->G, da[pass], strm);
+    s->prof_end(strm, &pe, on);
+    if (e != hipSuccess) return hip_fail(e, "decode kernel");
+  }
+  ProfPair pe;
+  const bool on = !pp && s->prof_begin(strm, &pe, kProfMerge);
+  hipError_t e = sq::launch_decode_merge(s->D, batch, ma, strm);
+  s->prof_end(strm, &pe, on);
+  if (e != hipSuccess) return hip_fail(e, "decode merge");
+  ++s->st.decode_calls;
+  s->st.decode_kv_bytes += plan.kv_bytes;
+  s->st.decode_kv_bytes_logical += plan.kv_bytes_logical;
+  return SQ_OK;
 }
 
 } // namespace
@@ -1591,6 +1666,7 @@ sq_status sq_decode_plan_info(sq_store *s, const sq_seq *seqs, int32_t batch, in
   out->n_items_mfma = plan.n_wg[1];
   out->chunk_pages = plan.n_wg[1] ? (int32_t)(plan.total[1] / plan.n_wg[1])
                                    : plan.n_wg[0] ? (int32_t)(plan.total[0] / plan.n_wg[0]) : 0;
+  out->n_slots = plan.n_slots;
   out->kv_bytes = plan.kv_bytes;
   out->kv_bytes_logical = plan.kv_bytes_logical;
   out->kv_bytes_valu = plan.kv_bytes_valu;
@@ -1607,57 +1683,16 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
 sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
                             const void *q, float *out, float scale, int32_t mode,
                             const sq_attn_opts *opts, void *stream) {
-  sq_attn_opts o{};
-  sq_status r = take_opts(opts, &o);
-  if (r != SQ_OK) return r;
-  if (!s || !seqs) return fail(SQ_ERR_INVALID, "null argument");
-  if (!s->device) return fail(SQ_ERR_INVALID, "metadata-only store cannot run attention");
-  if (batch < 1 || batch > SQ_MAX_BATCH) return fail(SQ_ERR_INVALID, "batch must be in [1, %d]", SQ_MAX_BATCH);
-  if (layer < 0 || layer >= s->cfg.num_layers) return fail(SQ_ERR_INVALID, "layer %d out of range", layer);
-  if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
-  if (!q || !out || !aligned16(q) || !aligned16(out))
-    return fail(SQ_ERR_INVALID, "q and out must be non-null and 16-byte aligned");
-  if (!std::isfinite(scale)) return fail(SQ_ERR_INVALID, "scale must be finite");
-  for (int b = 0; b < batch; ++b)
-    if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
-  Plan plan;
-  r = build_plan(s, seqs, batch, mode, &plan, o.window > 0 ? o.window : -1);
-  if (r != SQ_OK) return r;
-  if (plan.masked && o.window > 0)
-    return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
+  return decode_call(s, layer, seqs, batch, q, out, scale, mode, opts, stream, nullptr);
+}
 
-  hipStream_t strm = static_cast<hipStream_t>(stream);
-  s->last_stream = strm;
-  if (plan.masked) {
-    r = clean_mask_rows(s, seqs, batch, strm);
-    if (r != SQ_OK) return r;
-  }
-  sq::DecodeArgs da[2]{};
-  sq::MergeArgs ma{};
-  da[0].st = decode_static(s, layer, q, scale, !plan.pages_reread);
-  da[1].st = da[0].st;
-  ma.st = merge_static(s, layer, out, o.sinks);
-  sq::DecodeDyn dyn[2]{};
-  fill_dyn(s, plan, dyn, &ma.dyn);
-  for (int pass = 0; pass < 2; ++pass) {
-    da[pass].dyn = dyn[pass];
-    if (da[pass].dyn.n_wg == 0) continue;
-    ProfPair pp;
-    const bool on = s->prof_begin(strm, &pp, pass == 0 ? kProfValu : kProfMfma);
-    hipError_t e = pass == 0 ? sq::launch_decode_valu(s->D, s->G, da[pass], strm)
-                             : sq::launch_decode_mfma(s->D, s->G, da[pass], strm);
-    s->prof_end(strm, &pp, on);
-    if (e != hipSuccess) return hip_fail(e, "decode kernel");
-  }
-  ProfPair pp;
-  const bool on = s->prof_begin(strm, &pp, kProfMerge);
-  hipError_t e = sq::launch_decode_merge(s->D, batch, ma, strm);
-  s->prof_end(strm, &pp, on);
-  if (e != hipSuccess) return hip_fail(e, "decode merge");
-  ++s->st.decode_calls;
-  s->st.decode_kv_bytes += plan.kv_bytes;
-  s->st.decode_kv_bytes_logical += plan.kv_bytes_logical;
-  return SQ_OK;
+sq_status sq_decode_attn_noalloc(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
+                                 const void *q, float *out, float scale, int32_t mode,
+                                 void *stream) {
+  if (s && s->device && s->spart_err != hipSuccess)
+    return hip_fail(s->spart_err, "allocation-free partials (hipGetSymbolAddress at store creation)");
+  return decode_call(s, layer, seqs, batch, q, out, scale, mode, nullptr, stream,
+                     s ? &s->spart : nullptr);
 }
 
 sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,

@@ -20,6 +20,7 @@ STORE_METADATA_ONLY = 1
 STORE_EVICT_REMAP = 2
 STORE_KV_FP8 = 4
 STORE_EVICT_INPLACE = 8
+NOALLOC_PARTIAL_SLOTS = 4096  # SQ_NOALLOC_PARTIAL_SLOTS
 EVICT_DEFER = 1
 ATTN_AUTO, ATTN_STREAM, ATTN_SHARED_PREFIX, ATTN_MFMA = 0, 1, 2, 3
 MAX_BATCH = 64
@@ -71,7 +72,7 @@ class Stats(C.Structure):
 class PlanInfo(C.Structure):
     _fields_ = [("n_segments", C.c_int32), ("n_groups", C.c_int32),
                 ("n_items_valu", C.c_int32), ("n_items_mfma", C.c_int32),
-                ("chunk_pages", C.c_int32), ("reserved", C.c_int32),
+                ("chunk_pages", C.c_int32), ("n_slots", C.c_int32),
                 ("kv_bytes", C.c_int64), ("kv_bytes_logical", C.c_int64),
                 ("kv_bytes_valu", C.c_int64), ("kv_bytes_mfma", C.c_int64),
                 ("io_bytes", C.c_int64)]
@@ -111,6 +112,9 @@ _SIGS = {
                                  C.c_void_p, C.POINTER(EvictStats)]),
     "sq_decode_attn": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
                                  C.c_void_p, C.c_void_p, C.c_float, C.c_int32, C.c_void_p]),
+    "sq_decode_attn_noalloc": (C.c_int, [C.c_void_p, C.c_int32, C.POINTER(C.c_int32), C.c_int32,
+                                         C.c_void_p, C.c_void_p, C.c_float, C.c_int32,
+                                         C.c_void_p]),
     "sq_step_begin": (C.c_int, [C.c_void_p, C.POINTER(C.c_int32), C.c_int32, C.c_int32,
                                 C.c_void_p]),
     "sq_step_attn": (C.c_int, [C.c_void_p, C.c_int32, C.c_void_p, C.c_void_p, C.c_void_p,
@@ -394,6 +398,18 @@ class Store:
         else:
             _check(lib().sq_decode_attn_ex(self._handle, layer, _i32_array(seqs), len(seqs), qp,
                                            op, float(scale), mode, C.byref(o), _stream(stream)))
+        return out
+
+    def decode_noalloc(self, layer, seqs, q, out, scale=None, mode=ATTN_AUTO, stream=None):
+        """decode() through sq_decode_attn_noalloc: the split partials in the
+        library's per-GPU device array instead of the store's workspace; the
+        caller passes ``out`` (fp32 [B, Hq, D])."""
+        if scale is None:
+            scale = 1.0 / float(self.head_dim) ** 0.5
+        seqs = list(seqs)
+        qp, op = (_ptr(q), _ptr(out)) if self.metadata_only else self._qo_ptrs(q, out, len(seqs))
+        _check(lib().sq_decode_attn_noalloc(self._handle, layer, _i32_array(seqs), len(seqs), qp,
+                                            op, float(scale), mode, _stream(stream)))
         return out
 
     def step_begin(self, seqs, mode=ATTN_AUTO, stream=None, window=0):
