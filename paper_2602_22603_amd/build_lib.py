@@ -61,6 +61,52 @@ def build(verbose: bool = False) -> str:
     return LIB_PATH
 
 
+# Host-side checking build: the host library compiled by g++ with
+# AddressSanitizer and UndefinedBehaviorSanitizer (the HIP sources as in the
+# product build; no GPU code is sanitized).  Used by the CPU tests, which
+# preload the sanitizer runtimes and drive the metadata-only store.
+SAN_FLAGS = ["-fsanitize=address,undefined", "-fno-omit-frame-pointer", "-fno-sanitize-recover=all"]
+
+
+def sanitizer_runtimes():
+    """Paths of g++'s ASan and UBSan runtimes (for LD_PRELOAD)."""
+    out = []
+    for name in ("libasan.so", "libubsan.so"):
+        res = subprocess.run(["g++", f"-print-file-name={name}"], capture_output=True, text=True)
+        path = res.stdout.strip()
+        if res.returncode != 0 or not os.path.isabs(path) or not os.path.exists(path):
+            raise RuntimeError(f"g++ has no {name}")
+        out.append(path)
+    return out
+
+
+def build_sanitized(out_dir: str) -> str:
+    """Build libsq_san.so in out_dir: store.cpp by g++ with the sanitizers,
+    the kernel files by hipcc; returns its path."""
+    hipcc = _hipcc()
+    rocm = os.path.dirname(os.path.dirname(os.path.realpath(hipcc)))
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(out_dir, src + ".o")
+        if src.endswith(".hip"):
+            _compile(hipcc, src, obj)
+        else:
+            cmd = ["g++", "-std=c++17", "-O1", "-g", "-fPIC", "-D__HIP_PLATFORM_AMD__",
+                   "-I", os.path.join(rocm, "include"), "-I", INCLUDE, *SAN_FLAGS,
+                   "-c", os.path.join(CSRC, src), "-o", obj]
+            res = subprocess.run(cmd, capture_output=True, text=True)
+            if res.returncode != 0:
+                raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+        objs.append(obj)
+    out = os.path.join(out_dir, "libsq_san.so")
+    cmd = ["g++", "-shared", *SAN_FLAGS, *objs, "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           f"-Wl,-rpath,{os.path.join(rocm, 'lib')}", "-o", out]
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"link failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")
+    return out
+
+
 if __name__ == "__main__":
     build(verbose=True)
     sys.exit(0)
