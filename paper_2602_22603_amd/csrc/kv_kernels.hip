@@ -328,6 +328,79 @@ __global__ __launch_bounds__(256) void k_write_ids(int32_t *dst, NewIds ids, int
   if (i < n) dst[i] = new_page_id(ids, i);
 }
 
+// One destination page's sources, staged: each slot's source page id and
+// slot (LDS, written by the first P threads from src_of and the page-table
+// row, which still holds the old ids), and the distinct
+// source pages in order, which every thread finds itself from LDS (the kept
+// tokens are in old order, and a page list holds a page once, so the source
+// page changes exactly where the id does).
+constexpr int kMaxStaged = 4; // source pages of one destination page staged whole
+struct PageSources {
+  int nv;                  // valid slots
+  int nu;                  // distinct source pages (may exceed kMaxStaged)
+  int u0, u1, u2, u3;      // their ids, the first kMaxStaged of them (scalars,
+                           // so that nothing is indexed at run time)
+  __device__ int up(int u) const { return u == 0 ? u0 : u == 1 ? u1 : u == 2 ? u2 : u3; }
+};
+static_assert(kMaxStaged == 4, "PageSources holds four staged pages");
+
+__device__ inline void load_sources(const int32_t *src_of, const int32_t *pt_row, int t0, int nv,
+                                    int *spage, int *sslot) {
+  if ((int)threadIdx.x < nv) {
+    const int src = src_of[t0 + threadIdx.x];
+    spage[threadIdx.x] = pt_row[src / P];
+    sslot[threadIdx.x] = src % P;
+  }
+}
+
+__device__ inline PageSources distinct_sources(int nv, const int *spage) {
+  PageSources ps{};
+  ps.nv = nv;
+  for (int j = 0; j < nv; ++j)
+    if (j == 0 || spage[j] != spage[j - 1]) {
+      const int id = spage[j];
+      if (ps.nu == 0) ps.u0 = id;
+      else if (ps.nu == 1) ps.u1 = id;
+      else if (ps.nu == 2) ps.u2 = id;
+      else if (ps.nu == 3) ps.u3 = id;
+      ++ps.nu;
+    }
+  return ps;
+}
+
+// Staged source page of slot j: the page changes among slots 1..j.
+__device__ inline int staged_of(int j, const int *spage) {
+  int f = 0;
+  for (int i = 1; i <= j; ++i) f += spage[i] != spage[i - 1];
+  return f;
+}
+
+// The destination page's V^T units from the staged source pages (or, with
+// more than kMaxStaged of them, element by element from the pools).
+template <int D, class E>
+__device__ inline void assemble_v(const Pools &p, int layer, int head, E *vd, const PageSources &ps,
+                                  const uint4 (*vbuf)[D * P * sizeof(E) / 16], const int *spage,
+                                  const int *sslot) {
+  constexpr int VU = D * P * (int)sizeof(E) / 16;
+  constexpr int EPU = 16 / (int)sizeof(E);
+  for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) {
+    const int d = idx / (P / EPU), c = idx % (P / EPU);
+    E out[EPU];
+    int f = staged_of(c * EPU, spage);
+#pragma unroll
+    for (int e = 0; e < EPU; ++e) {
+      const int j = c * EPU + e;
+      if (e > 0 && j < ps.nv) f += spage[j] != spage[j - 1];
+      if (j >= ps.nv) out[e] = (E)0;
+      else if (ps.nu <= kMaxStaged) out[e] = reinterpret_cast<const E *>(vbuf[f])[d * P + sslot[j]];
+      else out[e] = chunk_of<E>(p.v, p, layer, spage[j], head)[d * P + sslot[j]];
+    }
+    uint4 o;
+    __builtin_memcpy(&o, out, 16);
+    *reinterpret_cast<uint4 *>(vd + d * P + c * EPU) = o;
+  }
+}
+
 // ---------------------------------------------------------------------------
 // Gather: a workgroup per (fresh page pi0 + b, layer * Hkv + head) fills
 // destination page fp + pi0 + b with the kept tokens (fp + pi0 + b) * P + j,
@@ -445,25 +518,18 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
 // tail into such runs (round mode, one workgroup per page and layer * Hkv +
 // head, like the gather), or hands a run of short ones to sweep mode, where
 // one workgroup per layer * Hkv + head takes the pages in order.  Either way
-// a workgroup stages everything a page needs (K rows, the V^T of its source
-// pages, positions) in LDS, waits at a barrier until every load of the page
-// has landed, and only then writes the page, which may be one of its own
-// sources.
+// a workgroup loads everything a page needs (K rows, the V^T of its source
+// pages, positions) in one round into LDS, waits at a barrier until every
+// load of the page has landed there, and only then writes the page, which
+// may be one of its own sources.
 template <int D, class E>
 __global__ __launch_bounds__(256) void k_evict_inplace(Pools p, InplaceArgs a) {
   constexpr int U = D * (int)sizeof(E) / 16;      // 16-byte units per K row
   constexpr int VU = D * P * (int)sizeof(E) / 16; // 16-byte units of one page's V^T
-  constexpr int EPU = 16 / (int)sizeof(E);        // V^T elements per unit
-  constexpr int kMaxSrc = 4;                       // source pages staged whole
   __shared__ int spage[P];
   __shared__ int sslot[P];
-  __shared__ int sidx[P];
-  __shared__ int upage[P];
-  __shared__ int uidx[P];
-  __shared__ int nvalid;
-  __shared__ int n_up;
   __shared__ uint4 kbuf[P * U];
-  __shared__ uint4 vbuf[kMaxSrc][VU]; // source pages, or the assembled page
+  __shared__ uint4 vbuf[kMaxStaged][VU];
   __shared__ int32_t pbuf[P];
   int pl0, pl1, lh;
   if (a.sweep) {
@@ -487,38 +553,21 @@ __global__ __launch_bounds__(256) void k_evict_inplace(Pools p, InplaceArgs a) {
     const int k = a.k0 + pl;
     const int t0 = (a.fp + k) * P;
     const int dst_page = new_page_id(a.ids, k);
-    if (threadIdx.x < P) {
-      const int t = t0 + threadIdx.x;
-      if (t < a.new_len) {
-        const int src = a.src_of[t];
-        spage[threadIdx.x] = a.pt_row[src / P];
-        sslot[threadIdx.x] = src % P;
-        sidx[threadIdx.x] = src / P;
-      }
-    }
-    if (threadIdx.x == 0) nvalid = min(P, a.new_len - t0);
+    const int nv = min(P, a.new_len - t0);
+    load_sources(a.src_of, a.pt_row, t0, nv, spage, sslot);
     __syncthreads();
-    const int nv = nvalid;
-    if ((int)threadIdx.x < nv) {
-      int f = 0;
-      for (int i = 1; i <= (int)threadIdx.x; ++i) f += sidx[i] != sidx[i - 1];
-      uidx[threadIdx.x] = f;
-      upage[f] = spage[threadIdx.x];
-      if ((int)threadIdx.x == nv - 1) n_up = f + 1;
-    }
-    // ---- read: everything the page needs, into LDS ----
+    const PageSources ps = distinct_sources(nv, spage);
+    // ---- read: everything the page needs, into LDS, in one round ----
     for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) {
       const int j = idx / U, u = idx % U;
       kbuf[idx] = reinterpret_cast<const uint4 *>(chunk_of<E>(p.k, p, layer, spage[j], head) +
                                                   sslot[j] * D)[u];
     }
-    if (lh == 0 && (int)threadIdx.x < nv)
-      pbuf[threadIdx.x] = p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
-    __syncthreads(); // n_up
-    const int nu = n_up;
-    if (nu <= kMaxSrc) {
-      for (int u = 0; u < nu; ++u) {
-        const uint4 *vs = reinterpret_cast<const uint4 *>(chunk_of<E>(p.v, p, layer, upage[u], head));
+    if (ps.nu <= kMaxStaged) {
+#pragma unroll
+      for (int u = 0; u < kMaxStaged; ++u) {
+        if (u >= ps.nu) break;
+        const uint4 *vs = reinterpret_cast<const uint4 *>(chunk_of<E>(p.v, p, layer, ps.up(u), head));
         for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) vbuf[u][idx] = vs[idx];
       }
     } else {
@@ -528,6 +577,8 @@ __global__ __launch_bounds__(256) void k_evict_inplace(Pools p, InplaceArgs a) {
         vo[idx] = j < nv ? chunk_of<E>(p.v, p, layer, spage[j], head)[d * P + sslot[j]] : (E)0;
       }
     }
+    if (lh == 0 && (int)threadIdx.x < nv)
+      pbuf[threadIdx.x] = p.pos[(int64_t)spage[threadIdx.x] * P + sslot[threadIdx.x]];
     // every load of this page's sources has been written to LDS by now: the
     // page itself may be overwritten
     __syncthreads();
@@ -535,19 +586,8 @@ __global__ __launch_bounds__(256) void k_evict_inplace(Pools p, InplaceArgs a) {
     uint4 *kd = reinterpret_cast<uint4 *>(chunk_of<E>(p.k, p, layer, dst_page, head));
     for (int idx = threadIdx.x; idx < nv * U; idx += blockDim.x) kd[idx] = kbuf[idx];
     E *vd = chunk_of<E>(p.v, p, layer, dst_page, head);
-    if (nu <= kMaxSrc) {
-      for (int idx = threadIdx.x; idx < VU; idx += blockDim.x) {
-        const int d = idx / (P / EPU), c = idx % (P / EPU);
-        E out[EPU];
-#pragma unroll
-        for (int e = 0; e < EPU; ++e) {
-          const int j = c * EPU + e;
-          out[e] = j < nv ? reinterpret_cast<const E *>(vbuf[uidx[j]])[d * P + sslot[j]] : (E)0;
-        }
-        uint4 o;
-        __builtin_memcpy(&o, out, 16);
-        *reinterpret_cast<uint4 *>(vd + d * P + c * EPU) = o;
-      }
+    if (ps.nu <= kMaxStaged) {
+      assemble_v<D, E>(p, layer, head, vd, ps, vbuf, spage, sslot);
     } else {
       for (int idx = threadIdx.x; idx < VU; idx += blockDim.x)
         reinterpret_cast<uint4 *>(vd)[idx] = vbuf[0][idx];
