@@ -293,7 +293,7 @@ struct sq_store {
   int cus = 256;              // compute units (device query in device mode)
   int wg_per_cu[2] = {8, 3};  // resident workgroups per CU (VALU, MFMA), from occupancy
   int min_wg_pages_valu = 8;
-  int min_wg_pages_mfma = 32;
+  int min_wg_pages_mfma = 8; // small launches still fill a round of resident workgroups
   // flattened pages appended to every row of a launch (VALU, MFMA): a
   // piece's start-up cost in page equivalents, so the even split evens time
   int row_pad[2] = {2, 16};
