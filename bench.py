@@ -371,36 +371,35 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False,
 
 
 def _decode_split(torch, store, seqs, q, out, reps, flush=None, layers=(0,)):
-    """Median wall time of a decode call (every layer in ``layers``, batch
-    ``seqs``; synchronised after each), and the library's kernel times per
-    call: decode kernel(s), merge, and what the call costs beyond them."""
+    """A decode call (every layer in ``layers``, batch ``seqs``): GPU time
+    per call from HIP events around it on the current stream (median over
+    ``reps``, each after a cache flush when ``flush`` is given), then, in a
+    second pass with the library's per-kernel events on (which add gaps of
+    their own), the decode kernel and merge times within a call."""
     def call():
         for layer in layers:
             store.decode(layer, seqs, q, out=out)
     for _ in range(3):
         call()
     torch.cuda.synchronize()
-    walls = []
+    gpu = time_events(torch, call, reps, flush)
     store.profile_enable(True)
     store.profile_read()
     for _ in range(reps):
         if flush is not None:
             flush()
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
         call()
-        torch.cuda.synchronize()
-        walls.append((time.perf_counter() - t0) * 1e3)
+    torch.cuda.synchronize()
     prof = store.profile_read()
     store.profile_enable(False)
     kv = store.plan_info(seqs)["kv_bytes"] * len(layers)
-    med = sorted(walls)[len(walls) // 2]
+    med = gpu["median"]
     dec = (prof["decode_mfma_ms"] + prof["decode_valu_ms"]) / reps
     mrg = prof["decode_merge_ms"] / reps
     plan = store.plan_info(seqs)
-    return dict(call_ms=round(med, 4), kv_bytes=kv, gbps_call=round(kv / (med * 1e-3) / 1e9, 1),
+    return dict(call_ms=gpu, kv_bytes=kv, gbps_call=round(kv / (med * 1e-3) / 1e9, 1),
                 decode_kernel_ms=round(dec, 4), merge_ms=round(mrg, 4),
-                other_ms=round(med - dec - mrg, 4),
+                launch_gaps_ms=round(med - dec - mrg, 4),
                 gbps_decode_kernel=round(kv / (dec * 1e-3) / 1e9, 1) if dec else None,
                 workgroups=plan["n_items_mfma"] + plan["n_items_valu"])
 
@@ -753,9 +752,10 @@ def _bf16_bits_to_f64(bits):
     return (bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
 
 
-def _oracle_head(args):
-    """One KV head of the sample through the oracle (runs in a worker)."""
-    import numpy as np
+def _oracle_part(args):
+    """The oracle's split partial (m, l, acc) of one KV head's query heads
+    over one token range of the sample (runs in a worker, BLAS on 1 thread);
+    returns (seconds, partial)."""
     from threadpoolctl import threadpool_limits
     from oracle import attention as oatt
     q, kbits, vbits = args
@@ -763,28 +763,46 @@ def _oracle_head(args):
         kf = _bf16_bits_to_f64(kbits)[:, None, :]
         vf = _bf16_bits_to_f64(vbits)[:, None, :]
         t0 = time.perf_counter()
-        oatt.attention(q, kf, vf, 1 / math.sqrt(128), 4)
-        return time.perf_counter() - t0
+        part = oatt.partial(q, kf, vf, 1 / math.sqrt(128), 4)
+        return time.perf_counter() - t0, part
+
+
+def _oracle_warm(_):
+    """Import what _oracle_part needs and wait a moment, so that every
+    worker of the pool is up before the timed map."""
+    from threadpoolctl import threadpool_limits  # noqa: F401
+    from oracle import attention  # noqa: F401
+    time.sleep(0.2)
+    return 0
 
 
 def _cpu_model():
+    """The host CPU as /proc/cpuinfo names it, with its family / model /
+    stepping (some virtual machines give only a short model name)."""
+    info = {}
     try:
         with open("/proc/cpuinfo") as fh:
             for line in fh:
-                if line.startswith("model name"):
-                    return line.split(":", 1)[1].strip()
+                if ":" in line:
+                    k, v = line.split(":", 1)
+                    info.setdefault(k.strip(), v.strip())
     except OSError:
         pass
-    return "unknown"
+    name = info.get("model name", "unknown")
+    ids = "/".join(info.get(k, "?") for k in ("cpu family", "model", "stepping"))
+    return f"{name} ({info.get('vendor_id', '?')}, family/model/stepping {ids})"
 
 
 def cpu_leg(sample, wl, budget_s):
-    """The float64 oracle on the host: KV heads of task 0's main thread, one
-    thread (BLAS pinned to 1), then one worker process per head in parallel."""
-    import concurrent.futures as cf
+    """The float64 oracle on the host, over KV heads of task 0's main thread:
+    first on one thread (BLAS pinned to 1), then split over every CPU the
+    process may use, each worker taking one token range of one head (the
+    oracle's split partials, combined by its merge and checked against the
+    single-thread outputs)."""
     import multiprocessing as mp
     import numpy as np
     import torch
+    from oracle import attention as oatt
     k, v = sample
     ctx = k.shape[1]
     rng = np.random.default_rng([2602, 2, 7])
@@ -792,26 +810,37 @@ def cpu_leg(sample, wl, budget_s):
     bits = lambda t, g: t[0, :, g].contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     heads = [(q[4 * g: 4 * g + 4], bits(k, g), bits(v, g)) for g in range(8)]
     bytes_per_head = ctx * 512
-    t_one, n_one = 0.0, 0
-    for h in heads:
-        t_one += _oracle_head(h)
-        n_one += 1
+    t_one, single = 0.0, {}
+    for g, h in enumerate(heads):
+        dt, part = _oracle_part(h)
+        t_one += dt
+        single[g] = oatt.merge([part])
         if t_one >= budget_s:
             break
-    one = bytes_per_head * n_one / t_one / 1e9
+    one = bytes_per_head * len(single) / t_one / 1e9
     avail = len(os.sched_getaffinity(0))
-    workers = max(1, min(len(heads), avail, 16))
-    with cf.ProcessPoolExecutor(max_workers=workers, mp_context=mp.get_context("spawn")) as ex:
-        list(ex.map(_oracle_head, [(h[0], h[1][:16], h[2][:16]) for h in heads[:workers]]))
+    workers = max(1, min(avail, 64))
+    chunks = max(1, -(-2 * workers // len(heads)))      # >= 2 units per worker
+    bounds = [ctx * c // chunks for c in range(chunks + 1)]
+    units = [(g, (h[0], h[1][a:b], h[2][a:b])) for g, h in enumerate(heads)
+             for a, b in zip(bounds[:-1], bounds[1:])]
+    # every worker is started and has imported the oracle before the clock runs
+    with mp.get_context("spawn").Pool(workers) as pool:
+        pool.map(_oracle_warm, range(workers), chunksize=1)
         t0 = time.perf_counter()
-        list(ex.map(_oracle_head, heads))
+        parts = pool.map(_oracle_part, [u[1] for u in units], chunksize=1)
         t_all = time.perf_counter() - t0
+    by_head = {}
+    for (g, _), (_, part) in zip(units, parts):
+        by_head.setdefault(g, []).append(part)
+    err = max(float(np.max(np.abs(oatt.merge(by_head[g]) - single[g]))) for g in single)
     par = bytes_per_head * len(heads) / t_all / 1e9
     return dict(value=par, unit="GB/s", cores=workers, kind="oracle",
                 sample=f"main thread of task 0: {ctx} tokens x 8 KV heads (4 query heads each), "
-                       f"float64 NumPy oracle, one worker process per KV head "
-                       f"({workers} processes, {t_all:.1f} s wall); single thread: {n_one} heads "
-                       f"in {t_one:.1f} s",
+                       f"float64 NumPy oracle split into {len(units)} (head, token range) "
+                       f"partials over {workers} worker processes ({t_all:.1f} s wall), merged "
+                       f"by the oracle (max diff {err:.1e} from the single-thread outputs); "
+                       f"single thread: {len(single)} heads in {t_one:.1f} s",
                 value_1_thread=one, cpu_model=_cpu_model(), affinity_cpus=avail,
                 blas_threads=1)
 
