@@ -16,15 +16,18 @@ namespace sq {
 // each row is followed by row_pad flattened pages that map to nothing.  They
 // stand for the fixed start-up cost of a piece (its query, page-id and
 // first page loads), so that the even split gives a workgroup that covers
-// many short rows fewer pages.
+// many short rows fewer pages.  row (< 256), nmem (<= kMaxMembers) and tok0
+// share one word.
 struct Seg {
-  int32_t row;
   int32_t page0;
   int32_t ntok;
   int32_t start;
-  int32_t nmem;
-  uint32_t mem; // byte j = batch index of member j
-  int32_t tok0;
+  uint32_t rmt;    // row | nmem << 8 | tok0 << 16
+  uint32_t mem[2]; // byte j of the pair = batch index of member j
+  __host__ __device__ int row() const { return (int)(rmt & 0xff); }
+  __host__ __device__ int nmem() const { return (int)((rmt >> 8) & 0xff); }
+  __host__ __device__ int tok0() const { return (int)(rmt >> 16); }
+  __host__ __device__ int member(int j) const { return (int)((mem[j >> 2] >> (8 * (j & 3))) & 0xff); }
 };
 
 // What a decode launch needs that does not change from call to call.
@@ -61,6 +64,9 @@ struct DecodeDyn {
   int32_t slot_base; // first partial slot of this launch
   int32_t row_pad;   // flattened pages after each row that map to nothing
   int32_t masked;    // 1: some segment's sequence has masked slots (read the masks)
+  int32_t rb;        // row blocks of 16 query rows per tile (MFMA launch: 1 or 2;
+                     // a piece then owns rb consecutive partial slots)
+  int32_t pad;
   Seg segs[kMaxSegs];
 };
 
@@ -77,7 +83,7 @@ __host__ __device__ inline int32_t wg_of(int64_t x, int64_t total, int64_t n_wg)
 
 // A batch entry attends to the segments on its path through the tree of
 // shared page runs: at most kMaxSrc (shared levels, then its own suffix).
-constexpr int kMaxSrc = 4;
+constexpr int kMaxSrc = 8;
 
 struct MergeStatic {
   float *out; // [B][Hq][D]
@@ -95,13 +101,19 @@ struct MergeStatic {
 
 struct MergeDyn {
   int32_t total[2], n_wg[2], slot_base[2], row_pad[2]; // per launch (0: VALU, 1: MFMA)
-  // per batch entry: the segments it attends; meta packs the launch (bit 0),
-  // the segment index inside that launch (bits 1-8) and the member index
-  // inside the segment (bits 9-10)
+  int32_t rb[2];                                       // row blocks per launch
+  // every segment of the call (both launches, plan order): flattened start
+  // of its rows, pages, and its launch (bit 0) and index inside that launch
+  // Every field is a whole 32-bit word: a kernel reads these tables with
+  // scalar loads, which address dwords.
+  int32_t seg_start[kMaxSegs];
+  int32_t seg_npages[kMaxSegs];
+  int32_t seg_meta[kMaxSegs];
+  // per batch entry: the segments it attends, each as the segment's plan
+  // index (bits 0-7) and the entry's member index inside it (bits 8-11),
+  // two to a word (source e in half e % 2 of word e / 2)
+  uint32_t src[kMaxBatch][kMaxSrc / 2];
   int32_t n_src[kMaxBatch];
-  int32_t src_meta[kMaxBatch][kMaxSrc];
-  int32_t src_start[kMaxBatch][kMaxSrc];  // flattened start of the segment's rows
-  int32_t src_npages[kMaxBatch][kMaxSrc];
 };
 
 struct MergeArgs {
@@ -181,7 +193,8 @@ constexpr int kStaticSlots = 4096;
 hipError_t static_partials(StaticPartials *out);
 
 // Workgroups of a decode kernel that fit on one CU.  kind: 0 VALU, 1 MFMA,
-// 2 the 8-bit MFMA kernel (four waves), 3 the 8-bit VALU kernel
+// 2 the 8-bit MFMA kernel (four waves), 3 the 8-bit VALU kernel, 4 the
+// two-row-block MFMA kernel
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int *out);
 
 } // namespace sq

@@ -169,13 +169,12 @@ struct DevPlan {
   __device__ Seg seg(int i) const {
     const SQ_CONST Seg &x = d->segs[i];
     Seg y;
-    y.row = x.row;
     y.page0 = x.page0;
     y.ntok = x.ntok;
     y.start = x.start;
-    y.nmem = x.nmem;
-    y.mem = x.mem;
-    y.tok0 = x.tok0;
+    y.rmt = x.rmt;
+    y.mem[0] = x.mem[0];
+    y.mem[1] = x.mem[1];
     return y;
   }
 };
@@ -242,10 +241,10 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
   int64_t x_pos = (int64_t)blockIdx.x * pl.total() / pl.n_wg();
   ItemPos ip;
   while (next_piece(pl, a.hkv, blockIdx.x, x_pos, x_end, ip)) {
-  const int b = ip.sg.mem & 0xff;
+  const int b = ip.sg.member(0);
   const int g = ip.g;
-  const int32_t *pt = a.pt + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
-  const int32_t *mrow = a.mask + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
+  const int32_t *pt = a.pt + (int64_t)ip.sg.row() * a.max_pages + ip.sg.page0;
+  const int32_t *mrow = a.mask + (int64_t)ip.sg.row() * a.max_pages + ip.sg.page0;
   const bool use_mask = pl.masked();
 
   const int t = lane >> 2, c = lane & 3; // score role
@@ -296,7 +295,7 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
 
   for (int pg = ip.pbeg; pg < ip.pend; ++pg) {
     const int valid = (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
-    const int lo = pg == 0 ? ip.sg.tok0 : 0; // tokens before lo: outside a window
+    const int lo = pg == 0 ? ip.sg.tok0() : 0; // tokens before lo: outside a window
     // slots attended: [lo, valid) less those a deferred eviction masked
     const int live = (use_mask ? mrow[pg] : 0xffff) & ((1 << valid) - 1) & ~((1 << lo) - 1);
     // stage the page in LDS
@@ -669,9 +668,14 @@ __device__ inline void mfma_values(VFrag<D> &f, int lo, int valid, int kg, s16x4
 }
 
 // MK: the plan may carry keep masks (decided at run time by the plan; false
-// compiles the mask path out).  KV8: the pools hold E4M3 codes.
-template <int D, int G, int kWaves, bool NT, bool MK, class PL, bool KV8 = false>
+// compiles the mask path out).  KV8: the pools hold E4M3 codes.  RB: row
+// blocks of 16 query rows per tile; with RB = 2 the second block (rows
+// 16..31: the members past 16 / G of a wide tile) takes the same K and V
+// fragments of each page through its own matrix-core instructions, and a
+// piece writes two consecutive partial slots.
+template <int D, int G, int kWaves, bool NT, bool MK, class PL, bool KV8 = false, int RB = 1>
 __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
+  static_assert(RB == 1 || (RB == 2 && !KV8), "two row blocks on bf16 stores only");
   constexpr int NS = D / 32;
   constexpr int NJ = D / 16;
   constexpr int APITCH = D + 4; // floats per row of a wave's accumulator in LDS
@@ -688,15 +692,18 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   ItemPos ip;
   while (next_piece(pl, a.hkv, blockIdx.x, x_pos, x_end, ip)) {
   const int g = ip.g;
-  const int nrows = ip.sg.nmem * G;
-  const bool qvalid = n < nrows;
-  const int jm = qvalid ? n / G : 0;
-  const int bq = (ip.sg.mem >> (8 * jm)) & 0xff;
-  const int32_t *pt = a.pt + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0;
+  const int nrows = ip.sg.nmem() * G;
+  const bool two = RB > 1 && nrows > kRows; // uniform: the piece uses block 1
+  const int32_t *pt = a.pt + (int64_t)ip.sg.row() * a.max_pages + ip.sg.page0;
 
-  bf16x8_t qb[NS];
-  {
-    const uint16_t *qp = a.q + ((int64_t)bq * a.hq + g * G + n % G) * D;
+  bf16x8_t qb[RB][NS];
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    const int row = n + kRows * rb;
+    const bool qvalid = row < nrows;
+    const int jm = qvalid ? row / G : 0;
+    const int bq = ip.sg.member(jm);
+    const uint16_t *qp = a.q + ((int64_t)bq * a.hq + g * G + row % G) * D;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
       // rows past nrows read member 0's row (in bounds) and are zeroed; an
@@ -704,14 +711,19 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
       const int c0 = KV8 ? 16 * kg + 64 * (s >> 1) + 8 * (s & 1) : 8 * kg + 32 * s;
       uint4 w = *reinterpret_cast<const uint4 *>(qp + c0);
       if (!qvalid) w = make_uint4(0, 0, 0, 0);
-      qb[s] = __builtin_bit_cast(bf16x8_t, w);
+      qb[rb][s] = __builtin_bit_cast(bf16x8_t, w);
     }
   }
 
-  f32x4_t acc[NJ];
+  f32x4_t acc[RB][NJ];
+  float m_run[RB], l_run[RB];
 #pragma unroll
-  for (int j = 0; j < NJ; ++j) acc[j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  float m_run = kNegInf, l_run = 0.f;
+  for (int rb = 0; rb < RB; ++rb) {
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) acc[rb][j] = f32x4_t{0.f, 0.f, 0.f, 0.f};
+    m_run[rb] = kNegInf;
+    l_run[rb] = 0.f;
+  }
 
   constexpr int ES = KV8 ? 1 : 2; // bytes per element
   const char *khead = reinterpret_cast<const char *>(a.k) + (int64_t)g * a.head_stride * ES;
@@ -740,12 +752,12 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     const int pg = wbeg + j;
     return j >= count ? 0 : (pg == ip.npages - 1) ? ip.sg.ntok - pg * P : P;
   };
-  auto lo_of = [&](int j) -> int { return wbeg + j == 0 ? ip.sg.tok0 : 0; };
+  auto lo_of = [&](int j) -> int { return wbeg + j == 0 ? ip.sg.tok0() : 0; };
   // keep masks of deferred evictions, scalar loads like the ids (all ones
   // when the plan has none)
   const bool use_mask = MK && pl.masked();
   const sptr_t mids =
-      (sptr_t)(a.mask + (int64_t)ip.sg.row * a.max_pages + ip.sg.page0 + wbeg);
+      (sptr_t)(a.mask + (int64_t)ip.sg.row() * a.max_pages + ip.sg.page0 + wbeg);
   auto smask = [&](int j) -> int { return use_mask ? mids[min(j, max(count - 1, 0))] : 0xffff; };
   if constexpr (KV8 && kStages8<D> > 2) {
   // An 8-bit page is half the bytes: more pages in flight, the same scheme
@@ -775,11 +787,11 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
     for (int st = 0; st < NST; ++st) {
       const int valid = valid_of(j + st), lo = lo_of(j + st);
       s16x4_t phi, plo;
-      mfma_scores<D, MK>(to_bf16(kf[st]), lo, valid, mkc[st], kg, a.scale_log2, qb, acc, m_run, l_run,
-                         phi, plo);
+      mfma_scores<D, MK>(to_bf16(kf[st]), lo, valid, mkc[st], kg, a.scale_log2, qb[0], acc[0],
+                         m_run[0], l_run[0], phi, plo);
       load_k<D, NT>(kf[st], rsrc(khead, nid[st], j + NST + st < count), koff);
       VFrag<D> vb = to_bf16(vf[st]);
-      mfma_values<D>(vb, lo, valid, kg, phi, plo, acc);
+      mfma_values<D>(vb, lo, valid, kg, phi, plo, acc[0]);
       load_v<D, NT>(vf[st], rsrc(vhead, nid[st], j + NST + st < count), voff);
       mkc[st] = mkn[st];
     }
@@ -811,11 +823,17 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   for (int j = 0; j < count; j += 2) {
     {
       const int valid = valid_of(j), lo = lo_of(j);
-      s16x4_t phi, plo;
-      mfma_scores<D, MK>(to_bf16(k0), lo, valid, mk0, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      s16x4_t phi[RB], plo[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb == 0 || two)
+          mfma_scores<D, MK>(to_bf16(k0), lo, valid, mk0, kg, a.scale_log2, qb[rb], acc[rb],
+                             m_run[rb], l_run[rb], phi[rb], plo[rb]);
       load_k<D, NT>(k0, rsrc(khead, n0, j + 2 < count), koff);
       VFrag<D> vb0 = to_bf16(v0);
-      mfma_values<D>(vb0, lo, valid, kg, phi, plo, acc);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb == 0 || two) mfma_values<D>(vb0, lo, valid, kg, phi[rb], plo[rb], acc[rb]);
       load_v<D, NT>(v0, rsrc(vhead, n0, j + 2 < count), voff);
       mk0 = q0;
     }
@@ -823,11 +841,17 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
       // page j + 1 may not exist (count odd): its fragments are then zeros
       // and with no valid token the update leaves (m, l, acc) as they are.
       const int valid = valid_of(j + 1), lo = lo_of(j + 1);
-      s16x4_t phi, plo;
-      mfma_scores<D, MK>(to_bf16(k1), lo, valid, mk1, kg, a.scale_log2, qb, acc, m_run, l_run, phi, plo);
+      s16x4_t phi[RB], plo[RB];
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb == 0 || two)
+          mfma_scores<D, MK>(to_bf16(k1), lo, valid, mk1, kg, a.scale_log2, qb[rb], acc[rb],
+                             m_run[rb], l_run[rb], phi[rb], plo[rb]);
       load_k<D, NT>(k1, rsrc(khead, n1, j + 3 < count), koff);
       VFrag<D> vb1 = to_bf16(v1);
-      mfma_values<D>(vb1, lo, valid, kg, phi, plo, acc);
+#pragma unroll
+      for (int rb = 0; rb < RB; ++rb)
+        if (rb == 0 || two) mfma_values<D>(vb1, lo, valid, kg, phi[rb], plo[rb], acc[rb]);
       load_v<D, NT>(v1, rsrc(vhead, n1, j + 3 < count), voff);
       mk1 = q1;
     }
@@ -839,25 +863,32 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
 
   }
 
-  float l_tot = sum_xrow16(l_run);
-  l_tot = sum_xrow32(l_tot);
   // combine the waves' states: M = max m_w, scale_w = 2^(m_w - M).  The
   // thread index is re-read here so that the LDS addresses below are
   // computed after the page loop instead of being held through it.
   int tx = threadIdx.x;
   __asm__ volatile("" : "+v"(tx));
   const int ew = tx >> 6, en = tx & 15, ekg = (tx >> 4) & 3;
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+  if (rb > 0 && !two) break;
+  if (rb > 0) __syncthreads(); // the previous block's combination has read the LDS
+  float l_tot = sum_xrow16(l_run[rb]);
+  l_tot = sum_xrow32(l_tot);
   if (ekg == 0) {
-    s_m[ew][en] = m_run;
+    s_m[ew][en] = m_run[rb];
     s_l[ew][en] = l_tot;
   }
 #pragma unroll
   for (int j = 0; j < NJ; ++j)
     *reinterpret_cast<float4 *>(&s_acc[ew][en * APITCH + 16 * j + 4 * ekg]) =
-        make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+        make_float4(acc[rb][j][0], acc[rb][j][1], acc[rb][j][2], acc[rb][j][3]);
   __syncthreads();
-  const int64_t prow = (int64_t)ip.slot * kRows;
-  if (tx < kRows && tx < nrows) {
+  // a piece's RB slots are consecutive: slot_base + RB * (its index) + rb
+  const int64_t prow =
+      ((int64_t)pl.slot_base() + (int64_t)RB * (ip.slot - pl.slot_base()) + rb) * kRows;
+  const int nr = nrows - kRows * rb; // rows of this block
+  if (tx < kRows && tx < nr) {
     const int r = tx;
     float mm = kNegInf;
 #pragma unroll
@@ -873,7 +904,7 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   constexpr int PER = kRows * D / (64 * kWaves); // output floats per thread
   const int e0 = tx * PER;
   const int r = e0 / D;
-  if (r < nrows) {
+  if (r < nr) {
     float mm = kNegInf;
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) mm = fmaxf(mm, s_m[w][r]);
@@ -895,6 +926,7 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
       *reinterpret_cast<float4 *>(a.part_acc + (prow + r) * D + d0 + e) = o;
     }
   }
+  } // row blocks
   __syncthreads(); // the next piece reuses the LDS
   } // pieces
 }
@@ -903,6 +935,13 @@ template <int D, int G, int kWaves, bool NT, bool MK>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kMfmaWavesPerEu, kMfmaWavesPerEu))) void
 k_decode_mfma(DecodeArgs a) {
   mfma_body<D, G, kWaves, NT, MK>(a.st, ArgPlan{a.dyn});
+}
+// Two row blocks (wide tiles of a tree's shared runs): twice the
+// accumulators, two waves per SIMD.
+template <int D, int G, int kWaves, bool NT, bool MK>
+__global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(2, 2))) void
+k_decode_mfma2(DecodeArgs a) {
+  mfma_body<D, G, kWaves, NT, MK, ArgPlan, false, 2>(a.st, ArgPlan{a.dyn});
 }
 template <int D, int G, int kWaves>
 __global__ __launch_bounds__(64 * kWaves) __attribute__((amdgpu_waves_per_eu(kMfmaWavesPerEu, kMfmaWavesPerEu))) void
@@ -941,9 +980,11 @@ struct ArgMerge {
   __device__ int slot_base(int L) const { return d.slot_base[L]; }
   __device__ int row_pad(int L) const { return d.row_pad[L]; }
   __device__ int n_src(int b) const { return d.n_src[b]; }
-  __device__ int src_meta(int b, int e) const { return d.src_meta[b][e]; }
-  __device__ int src_start(int b, int e) const { return d.src_start[b][e]; }
-  __device__ int src_npages(int b, int e) const { return d.src_npages[b][e]; }
+  __device__ int rb(int L) const { return d.rb[L]; }
+  __device__ int src(int b, int e) const { return (int)((d.src[b][e >> 1] >> (16 * (e & 1))) & 0xffff); }
+  __device__ int seg_start(int i) const { return d.seg_start[i]; }
+  __device__ int seg_npages(int i) const { return d.seg_npages[i]; }
+  __device__ int seg_meta(int i) const { return d.seg_meta[i]; }
 };
 struct DevMerge {
   const SQ_CONST MergeDyn *d;
@@ -952,9 +993,11 @@ struct DevMerge {
   __device__ int slot_base(int L) const { return d->slot_base[L]; }
   __device__ int row_pad(int L) const { return d->row_pad[L]; }
   __device__ int n_src(int b) const { return d->n_src[b]; }
-  __device__ int src_meta(int b, int e) const { return d->src_meta[b][e]; }
-  __device__ int src_start(int b, int e) const { return d->src_start[b][e]; }
-  __device__ int src_npages(int b, int e) const { return d->src_npages[b][e]; }
+  __device__ int rb(int L) const { return d->rb[L]; }
+  __device__ int src(int b, int e) const { return (int)((d->src[b][e >> 1] >> (16 * (e & 1))) & 0xffff); }
+  __device__ int seg_start(int i) const { return d->seg_start[i]; }
+  __device__ int seg_npages(int i) const { return d->seg_npages[i]; }
+  __device__ int seg_meta(int i) const { return d->seg_meta[i]; }
 };
 
 // With APPEND (a decode step), the last wave starts from the entry's new
@@ -980,21 +1023,27 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
   const int hr = h - g * a.group;
   const int ns = mp.n_src(b);
   int cum[kMaxSrc + 1];
-  int32_t base[kMaxSrc];
+  int32_t base[kMaxSrc], step[kMaxSrc];
   cum[0] = 0;
 #pragma unroll
   for (int e = 0; e < kMaxSrc; ++e) {
     int cnt = 0;
     base[e] = 0;
+    step[e] = kRows;
     if (e < ns) {
-      const int meta = mp.src_meta(b, e);
-      const int L = meta & 1, seg = (meta >> 1) & 0xff, member = (meta >> 9) & 3;
-      const int np = mp.src_npages(b, e);
-      const int64_t R = (int64_t)mp.src_start(b, e) + (int64_t)g * (np + mp.row_pad(L)); // row start
+      const int sr = mp.src(b, e);
+      const int si = sr & 0xff, member = (sr >> 8) & 0xf;
+      const int meta = mp.seg_meta(si);
+      const int L = meta & 1, seg = meta >> 1;
+      const int np = mp.seg_npages(si);
+      const int64_t R = (int64_t)mp.seg_start(si) + (int64_t)g * (np + mp.row_pad(L)); // row start
       const int w_lo = wg_of(R, mp.total(L), mp.n_wg(L));
       const int w_hi = wg_of(R + np - 1, mp.total(L), mp.n_wg(L));
       cnt = w_hi - w_lo + 1;
-      base[e] = (mp.slot_base(L) + w_lo + seg * a.hkv + g) * kRows + member * a.group + hr;
+      // a piece of an RB-block launch owns RB consecutive slots of 16 rows
+      step[e] = mp.rb(L) * kRows;
+      base[e] = (mp.slot_base(L) + mp.rb(L) * (w_lo + seg * a.hkv + g)) * kRows +
+                member * a.group + hr;
     }
     cum[e + 1] = cum[e] + cnt;
   }
@@ -1003,7 +1052,7 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
     int e = 0;
 #pragma unroll
     for (int k = 1; k < kMaxSrc; ++k) e += c >= cum[k];
-    return base[e] + (c - cum[e]) * kRows;
+    return base[e] + (c - cum[e]) * step[e];
   };
 
   // with APPEND the last wave takes the new token only, so its loads overlap
@@ -1193,12 +1242,34 @@ hipError_t mfma8_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
   return hipGetLastError();
 }
 
+template <int D, bool NT, bool MK>
+hipError_t mfma2_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
+  constexpr int W = kMfmaWaves;
+  const dim3 grid(a.dyn.n_wg), block(64 * W);
+  switch (group) { // G = 1 never needs a second block (at most 8 members)
+  case 2: hipLaunchKernelGGL((k_decode_mfma2<D, 2, W, NT, MK>), grid, block, 0, s, a); break;
+  case 4: hipLaunchKernelGGL((k_decode_mfma2<D, 4, W, NT, MK>), grid, block, 0, s, a); break;
+  case 8: hipLaunchKernelGGL((k_decode_mfma2<D, 8, W, NT, MK>), grid, block, 0, s, a); break;
+  default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 // a plan with keep masks takes the masked variant (ordinary loads); an
-// 8-bit store its own kernel (four waves)
+// 8-bit store its own kernel (four waves); tiles wider than 16 query rows
+// the two-block kernel
 template <int D>
 hipError_t mfma_dispatch(int group, const DecodeArgs &a, hipStream_t s) {
-  if (a.st.kv8)
+  if (a.st.kv8) {
+    if (a.dyn.rb != 1) return hipErrorInvalidValue;
     return a.dyn.masked ? mfma8_dispatch<D, true>(group, a, s) : mfma8_dispatch<D, false>(group, a, s);
+  }
+  if (a.dyn.rb == 2) {
+    if (a.dyn.masked) return mfma2_dispatch<D, false, true>(group, a, s);
+    return a.st.nontemporal ? mfma2_dispatch<D, true, false>(group, a, s)
+                            : mfma2_dispatch<D, false, false>(group, a, s);
+  }
+  if (a.dyn.rb != 1) return hipErrorInvalidValue;
   if (a.dyn.masked) return mfma_dispatch_w<D, kMfmaWaves, false, true>(group, a, s);
   return a.st.nontemporal ? mfma_dispatch_w<D, kMfmaWaves, true, false>(group, a, s)
                        : mfma_dispatch_w<D, kMfmaWaves, false, false>(group, a, s);
@@ -1235,12 +1306,21 @@ template <int D> const void *mfma8_fn(int group) {
   }
 }
 template <int D> const void *mfma_fn(int group) { return mfma_fn_w<D, kMfmaWaves>(group); }
+template <int D> const void *mfma2_fn(int group) {
+  switch (group) {
+  case 2: return reinterpret_cast<const void *>(&k_decode_mfma2<D, 2, kMfmaWaves, true, false>);
+  case 4: return reinterpret_cast<const void *>(&k_decode_mfma2<D, 4, kMfmaWaves, true, false>);
+  case 8: return reinterpret_cast<const void *>(&k_decode_mfma2<D, 8, kMfmaWaves, true, false>);
+  default: return nullptr;
+  }
+}
 } // namespace
 
 hipError_t decode_blocks_per_cu(int kind, int d, int group, int *out) {
   const void *fn = kind == 0   ? (d == 128 ? valu_fn<128, false>(group) : valu_fn<64, false>(group))
                    : kind == 3 ? (d == 128 ? valu_fn<128, true>(group) : valu_fn<64, true>(group))
                    : kind == 2 ? (d == 128 ? mfma8_fn<128>(group) : mfma8_fn<64>(group))
+                   : kind == 4 ? (d == 128 ? mfma2_fn<128>(group) : mfma2_fn<64>(group))
                                : (d == 128 ? mfma_fn<128>(group) : mfma_fn<64>(group));
   if (!fn) return hipErrorInvalidValue;
   const int block = kind == 0 || kind == 3 ? 64 : 64 * kMfmaWaves;

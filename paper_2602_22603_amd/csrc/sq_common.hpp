@@ -13,7 +13,7 @@ constexpr int kPage = 16;            // tokens per page in device mode
 constexpr int kMaxAppendPages = 240; // pages one append launch may touch
 constexpr int kMaxBatch = 64;        // queries per decode call
 constexpr int kMaxSegs = 128;        // (page range, query rows) units per decode
-constexpr int kMaxMembers = 4;       // sequences stacked in one MFMA tile
+constexpr int kMaxMembers = 8;       // sequences stacked in one MFMA tile
 constexpr int kRows = 16;            // query rows per partial slot (MFMA N)
 constexpr int kMaxItems = 8192;      // partial slots in the workspace
 

@@ -292,6 +292,7 @@ struct sq_store {
   // tuning
   int cus = 256;              // compute units (device query in device mode)
   int wg_per_cu[2] = {8, 3};  // resident workgroups per CU (VALU, MFMA), from occupancy
+  int wg_per_cu_rb2 = 2;      // the same for the two-row-block MFMA kernel
   int min_wg_pages_valu = 8;
   int min_wg_pages_mfma = 8; // small launches still fill a round of resident workgroups
   // flattened pages appended to every row of a launch (VALU, MFMA): a
@@ -466,6 +467,7 @@ struct Plan {
   int n_groups = 0;
   int64_t total[2] = {0, 0}; // flattened pages per launch (0: VALU, 1: MFMA)
   int32_t n_wg[2] = {0, 0};  // workgroups per launch
+  int32_t rb[2] = {1, 1};    // row blocks of 16 query rows per tile (MFMA launch: 1 or 2)
   int32_t slot_base[2] = {0, 0};
   int32_t seg_index[sq::kMaxSegs]; // index of each segment inside its launch
   bool pages_reread = false; // some page is read by more than one segment
@@ -486,11 +488,16 @@ template <class T> int64_t first_diff(const T *a, const T *b, int64_t n) {
 }
 
 // keep_last >= 0: each entry attends only to its last keep_last cached
-// tokens (a window), read on its own; < 0: every token.
+// tokens (a window), read on its own; < 0: every token.  max_rb: row blocks
+// of 16 query rows a tile may take (2 for a plain decode call on a bf16
+// store, whose wide tiles then run on the two-block kernel; 1 for the
+// fused step, whose launches are fixed per batch and mode, and for an
+// 8-bit store).
 sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode, Plan *plan,
-                     int64_t keep_last = -1) {
+                     int64_t keep_last = -1, int max_rb = 1) {
   const int64_t tok_bytes = (int64_t)s->cfg.num_kv_heads * s->cfg.head_dim * 2 * s->elem_bytes();
-  const int max_mem = std::min(sq::kMaxMembers, sq::kRows / s->G);
+  if (s->kv8) max_rb = 1;
+  const int max_mem = std::min(sq::kMaxMembers, max_rb * sq::kRows / s->G);
   const bool grouping = mode == SQ_ATTN_AUTO || mode == SQ_ATTN_SHARED_PREFIX;
   // AUTO reads a sequence on its own on the MFMA tile too
   const bool single_mfma = mode == SQ_ATTN_MFMA || mode == SQ_ATTN_AUTO;
@@ -498,14 +505,12 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   auto add_seg = [&](int32_t row, int32_t page0, int64_t ntok, bool mfma,
                      const std::vector<int> &members, int32_t tok0 = 0) {
     PlanSeg ps{};
-    ps.seg.row = row;
     ps.seg.page0 = page0;
     ps.seg.ntok = (int32_t)ntok;
-    ps.seg.tok0 = tok0;
-    ps.seg.nmem = (int32_t)members.size();
-    ps.seg.mem = 0;
+    ps.seg.rmt = (uint32_t)row | (uint32_t)members.size() << 8 | (uint32_t)tok0 << 16;
+    ps.seg.mem[0] = ps.seg.mem[1] = 0;
     for (size_t j = 0; j < members.size(); ++j) {
-      ps.seg.mem |= (uint32_t)members[j] << (8 * j);
+      ps.seg.mem[j >> 2] |= (uint32_t)members[j] << (8 * (j & 3));
       ps.members[j] = members[j];
     }
     ps.mfma = mfma;
@@ -624,6 +629,8 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   // one round of the GPU's resident workgroups, at least `min_wg_pages`
   // pages each, never more workgroups than pages.
   const int hkv = s->cfg.num_kv_heads;
+  for (const PlanSeg &ps : plan->segs)
+    if (ps.mfma && ps.seg.nmem() * s->G > sq::kRows) plan->rb[1] = 2;
   int count[2] = {0, 0};
   for (size_t i = 0; i < plan->segs.size(); ++i) {
     PlanSeg &ps = plan->segs[i];
@@ -632,7 +639,7 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
     ps.seg.start = (int32_t)plan->total[L];
     plan->seg_index[i] = count[L]++;
     plan->total[L] += (np + s->row_pad[L]) * hkv;
-    const int64_t seg_bytes = (int64_t)(ps.seg.ntok - ps.seg.tok0) * tok_bytes;
+    const int64_t seg_bytes = (int64_t)(ps.seg.ntok - ps.seg.tok0()) * tok_bytes;
     plan->kv_bytes += seg_bytes;
     (L == 0 ? plan->kv_bytes_valu : plan->kv_bytes_mfma) += seg_bytes;
     plan->io_bytes += np * 4;
@@ -641,16 +648,17 @@ sq_status build_plan(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mod
   for (int L = 0; L < 2; ++L) {
     if (plan->total[L] == 0) continue;
     if (plan->total[L] > INT32_MAX) return fail(SQ_ERR_INVALID, "decode batch too large");
-    const int64_t fill = (int64_t)s->cus * s->wg_per_cu[L];
+    const int64_t fill = (int64_t)s->cus * (plan->rb[L] == 2 ? s->wg_per_cu_rb2 : s->wg_per_cu[L]);
     const int64_t min_pages = L == 1 ? s->min_wg_pages_mfma : s->min_wg_pages_valu;
     int64_t n = std::min<int64_t>(fill, (plan->total[L] + min_pages - 1) / min_pages);
     n = std::max<int64_t>(1, std::min<int64_t>(n, plan->total[L]));
-    const int64_t room = sq::kMaxItems - slots - (int64_t)count[L] * hkv;
+    // each workgroup's piece of each row owns rb consecutive slots
+    const int64_t room = (sq::kMaxItems - slots) / plan->rb[L] - (int64_t)count[L] * hkv;
     if (room < 1) return fail(SQ_ERR_INVALID, "decode batch needs too many partial slots");
     n = std::min<int64_t>(n, room);
     plan->n_wg[L] = (int32_t)n;
     plan->slot_base[L] = slots;
-    slots += (int32_t)n + count[L] * hkv;
+    slots += ((int32_t)n + count[L] * hkv) * plan->rb[L];
   }
   plan->n_slots = slots;
   plan->io_bytes += (int64_t)batch * s->cfg.num_q_heads * s->cfg.head_dim * (2 + 4);
@@ -714,21 +722,24 @@ void fill_dyn(sq_store *s, const Plan &plan, sq::DecodeDyn dyn[2], sq::MergeDyn 
     d.total = (int32_t)plan.total[L];
     d.row_pad = s->row_pad[L];
     d.masked = plan.masked ? 1 : 0;
+    d.rb = plan.rb[L];
     d.n_wg = plan.n_wg[L];
     d.slot_base = plan.slot_base[L];
     md->total[L] = d.total;
     md->row_pad[L] = d.row_pad;
     md->n_wg[L] = d.n_wg;
     md->slot_base[L] = d.slot_base;
+    md->rb[L] = d.rb;
   }
   for (size_t i = 0; i < plan.segs.size(); ++i) {
     const PlanSeg &ps = plan.segs[i];
-    for (int j = 0; j < ps.seg.nmem; ++j) {
+    md->seg_start[i] = ps.seg.start;
+    md->seg_npages[i] = (ps.seg.ntok + s->P - 1) / s->P;
+    md->seg_meta[i] = (ps.mfma ? 1 : 0) | plan.seg_index[i] << 1;
+    for (int j = 0; j < ps.seg.nmem(); ++j) {
       const int b = ps.members[j];
       const int e = md->n_src[b]++;
-      md->src_meta[b][e] = (ps.mfma ? 1 : 0) | plan.seg_index[i] << 1 | j << 9;
-      md->src_start[b][e] = ps.seg.start;
-      md->src_npages[b][e] = (ps.seg.ntok + s->P - 1) / s->P;
+      md->src[b][e >> 1] |= (uint32_t)(i | j << 8) << (16 * (e & 1));
     }
   }
 }
@@ -841,6 +852,9 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
       nb = 0;
       if (sq::decode_blocks_per_cu(s->kv8 ? 2 : 1, s->D, s->G, &nb) == hipSuccess && nb > 0)
         s->wg_per_cu[1] = nb;
+      nb = 0;
+      if (s->G > 1 && sq::decode_blocks_per_cu(4, s->D, s->G, &nb) == hipSuccess && nb > 0)
+        s->wg_per_cu_rb2 = nb;
     }
     // set-up of the allocation-free entry point: its device array's address
     // on this GPU (a failure only disables that entry point)
@@ -1063,7 +1077,7 @@ sq_status decode_call(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t ba
   for (int b = 0; b < batch; ++b)
     if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
   Plan plan;
-  r = build_plan(s, seqs, batch, mode, &plan, o.window > 0 ? o.window : -1);
+  r = build_plan(s, seqs, batch, mode, &plan, o.window > 0 ? o.window : -1, 2);
   if (r != SQ_OK) return r;
   if (plan.masked && o.window > 0)
     return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
@@ -1657,7 +1671,7 @@ sq_status sq_decode_plan_info(sq_store *s, const sq_seq *seqs, int32_t batch, in
   for (int b = 0; b < batch; ++b)
     if (!s->get(seqs[b])) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", seqs[b]);
   Plan plan;
-  sq_status r = build_plan(s, seqs, batch, mode, &plan);
+  sq_status r = build_plan(s, seqs, batch, mode, &plan, -1, 2); // as sq_decode_attn plans
   if (r != SQ_OK) return r;
   *out = sq_plan_info{};
   out->n_segments = (int32_t)plan.segs.size();

@@ -425,10 +425,11 @@ def test_decode_step_metadata(sq):
 
 
 def test_decode_plan_worst_case_segments(sq):
-    """The most segments 64 entries can need: with at most 4 entries per MFMA
-    tile, a tile's run splits into two shared pairs and four private tails
-    (7 segments per 4 entries, 112 for 64), below the 128 one decode call
-    holds.  Eight trees of root -> 2 -> 4 -> 8 forks (P = 4) reach it."""
+    """Segments 64 entries can need: every shared run splits into at least
+    two parts, so n entries make at most 2n - 1 segments (127 for 64), below
+    the 128 one decode call holds.  Eight binary trees of root -> 2 -> 4 -> 8
+    forks (P = 4, G = 2: one tile takes all 8 leaves of a tree) make 15 per
+    tree: one run of 8, two of 4, four of 2 and 8 private tails."""
     s = _store(sq, 4000, 4, 255, 64)
     leaves = []
     for _ in range(8):
@@ -445,8 +446,51 @@ def test_decode_plan_worst_case_segments(sq):
                     s.append(y, n=1)
                     leaves.append(y)
     info = s.plan_info(leaves)
-    assert info["n_segments"] == 112 and info["n_groups"] == 48
+    assert info["n_segments"] == 120 and info["n_groups"] == 56
     assert info["kv_bytes"] < info["kv_bytes_logical"]
+
+
+@pytest.mark.parametrize("group,members,read_once", [(1, 8, True), (2, 8, True), (4, 8, True),
+                                                     (8, 8, False)])
+def test_deep_and_wide_trees(sq, group, members, read_once):
+    """A fork chain seven deep (each branch forked from the previous one,
+    page-aligned or mid-page) and a fan-out of eight branches at one point:
+    with 8 members per tile (16 / G rows per block, two blocks) each
+    distinct page is read once; with G = 8 a tile holds four members and
+    the wide runs are read once per tile."""
+    P, tok = 16, 2 * 128 * 2 * 2
+    s = sq.Store(1, 2 * group, 2, 128, num_pages=800, max_seqs=20, max_pages_per_seq=120,
+                 metadata_only=True)
+
+    def distinct(batch):
+        full, partial = set(), 0
+        for b in batch:
+            L = s.seq_info(b)["length"]
+            full.update(s.page_table(b)[: L // P])
+            partial += L % P
+        return (len(full) * P + partial) * tok
+
+    m = s.seq_create()
+    s.append(m, n=300)
+    chain = [m]
+    for d in range(members - 1):
+        nxt = s.fork(chain[-1], s.seq_info(chain[-1])["length"] - (7 if d % 2 else 0))
+        s.append(nxt, n=40)
+        chain.append(nxt)
+    a = s.seq_create()
+    s.append(a, n=700)
+    fan = [a]
+    for i in range(members - 1):
+        c = s.fork(a, 640 if i % 2 else 700)
+        s.append(c, n=5 + 7 * i)
+        fan.append(c)
+    for batch in (chain, fan):
+        info = s.plan_info(batch, sq.ATTN_AUTO)
+        assert (info["kv_bytes"] == distinct(batch)) == read_once, (batch, info)
+        assert info["kv_bytes"] < info["kv_bytes_logical"]
+    # the deepest entry of the chain attends to every level
+    info = s.plan_info(chain, sq.ATTN_AUTO)
+    assert info["n_groups"] >= (members - 1 if read_once else 1)
 
 
 def test_invalid_configurations(sq):
@@ -531,25 +575,27 @@ def test_decode_plan_reads_a_tree_of_shared_runs_once(sq):
         assert info["kv_bytes"] == 1320 * tok and info["kv_bytes_logical"] == 3720 * tok
     info = s.plan_info([m, a, b, c], sq.ATTN_STREAM)
     assert (info["n_segments"], info["n_groups"], info["kv_bytes"]) == (4, 0, 3720 * tok)
-    # a chain of six nested forks: more entries than one tile holds (4 for
-    # G = 4), so the root run is read once per tile: tile {m, c1, c2, c3}
-    # nests three runs, tile {c4, c5} one
+    # a chain of six nested forks: one tile holds all six entries (two
+    # 16-row blocks when G = 4), so the runs nest five deep and each page is
+    # read once: M's 1000 tokens, 40 private tokens per child, and the 8
+    # tokens each of the three mid-page forks (at 1000, 1080, 1160) copied
+    # into its own tail page
     chain = [m]
     for i in range(5):
         nxt = s.fork(chain[-1], s.seq_info(chain[-1])["length"])
         s.append(nxt, n=40)
         chain.append(nxt)
     info = s.plan_info(chain, sq.ATTN_AUTO)
-    assert info["n_groups"] == 4 and info["kv_bytes"] < info["kv_bytes_logical"]
+    assert info["n_groups"] == 5 and info["kv_bytes"] == (1000 + 5 * 40 + 3 * 8) * tok
 
 
 @pytest.mark.parametrize("seed", range(6))
 def test_tree_plan_reads_every_distinct_page_once(sq, seed):
     """Random forests of forks, appends and evictions (metadata only): for
-    any batch of at most four entries (one tile when G <= 4) the
-    shared-prefix plan reads each distinct page once; the count comes from
-    the page tables alone: P tokens per distinct full page plus each
-    entry's partial last page."""
+    any batch of at most eight entries (one tile of two 16-row blocks when
+    G = 4) the shared-prefix plan reads each distinct page once; the count
+    comes from the page tables alone: P tokens per distinct full page plus
+    each entry's partial last page."""
     rng = np.random.default_rng(1000 + seed)
     P, tok = 16, 2 * 128 * 2 * 2
     s = sq.Store(1, 8, 2, 128, num_pages=3000, max_seqs=16, max_pages_per_seq=400,
@@ -578,7 +624,7 @@ def test_tree_plan_reads_every_distinct_page_once(sq, seed):
             s.release(h)
             live.remove(h)
         for _ in range(3):
-            k = int(rng.integers(1, min(4, len(live)) + 1))
+            k = int(rng.integers(1, min(8, len(live)) + 1))
             batch = [live[i] for i in rng.choice(len(live), k, replace=False)]
             full = set()
             partial = 0

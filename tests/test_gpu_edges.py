@@ -174,6 +174,39 @@ def test_binding_rejects_bad_tensors(sq):
     s.close()
 
 
+@pytest.mark.parametrize("group", [1, 2, 4, 8])
+def test_deep_chain_and_wide_fanout(sq, group):
+    """A fork chain seven deep (page-aligned and mid-page fork points) and a
+    fan-out of eight branches at one point, alone and together: up to
+    eight members share one tile (two 16-row blocks when G = 4 or 8, the
+    two-block kernel), entries merge up to eight partial sources; every
+    mode against the oracle, page tables and views bit for bit."""
+    hkv = 2
+    t = sc.Twin(sq, 1, hkv * group, hkv, 128, 900, 20, 120, seed=90 + group)
+    m = t.create()
+    t.append(m, 300)
+    chain = [m]
+    for d in range(7):
+        nxt = t.fork(chain[-1], t.model.info(chain[-1])["length"] - (7 if d % 2 else 0))
+        t.append(nxt, 40)
+        chain.append(nxt)
+    a = t.create()
+    t.append(a, 700)
+    fan = [a]
+    for i in range(7):
+        c = t.fork(a, 640 if i % 2 else 700)
+        t.append(c, 5 + 7 * i)
+        fan.append(c)
+    t.check_state()
+    for seqs in (chain, fan, fan[:5], chain[3:] + fan[:4]):
+        info = t.store.plan_info(seqs, sq.ATTN_AUTO)
+        assert info["kv_bytes"] < info["kv_bytes_logical"]
+        _check(t, seqs)
+    # and a decode step (one-block tiles: the fused step keeps its launches)
+    err, _ = t.step(fan)
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("group", [1, 2, 4])
 def test_tree_of_forks(sq, group):
     """Forks of forks at page-aligned and mid-page points: the shared-prefix
