@@ -963,15 +963,18 @@ k_step_mfma8(DecodeStatic a, const DecodeDyn *dyn) {
 // ===========================================================================
 // Merge: one workgroup of kMergeWaves waves per (batch entry, query head).
 // Its partials are the pieces of at most kMaxSrc segments (the shared runs on
-// its path through the tree of forks, then its own suffix).  Wave w takes a
-// contiguous share of them, kMergeUnroll at a time: the acc rows (lanes over
-// channels) and the (m, l) pairs (lanes over partials) of a round are loaded
-// together, then folded into the wave's running (m_w, l_w, acc_w) with the
-// usual rescale.  The waves' states combine through LDS the same way.  One
-// round of global loads covers kMergeWaves * kMergeUnroll partials: latency,
-// not bandwidth, bounds this kernel.
+// its path through the tree of forks, then its own suffix).  Thread t takes
+// channel t % D of share t / D of each round of NSH * kMergeChunk pieces
+// (the round's partial rows listed in LDS first): it loads its share's
+// (m, l) pairs itself (the same addresses across the share's threads, one
+// request per wave) and its channel of each acc row, all in flight
+// together, and folds them into a running (m, l, acc) with the usual
+// rescale.  No cross-lane reduction; the shares (and the sink, and in a
+// step the new token) combine through LDS.  Latency, not bandwidth, bounds
+// this kernel: one round of loads covers a (batch entry, head)'s pieces
+// when there are at most NSH * kMergeChunk of them.
 constexpr int kMergeWaves = 8;
-constexpr int kMergeUnroll = 16;
+constexpr int kMergeChunk = 24;
 
 struct ArgMerge {
   const MergeDyn &d;
@@ -1000,23 +1003,25 @@ struct DevMerge {
   __device__ int seg_meta(int i) const { return d->seg_meta[i]; }
 };
 
-// With APPEND (a decode step), the last wave starts from the entry's new
-// token as a partial of its own - score q . k_new, weight 1, value v_new -
-// and the workgroup of the first query head of each KV head stores the new
-// token's K, V, position and page-table entry for later steps.
-// KV8 (with APPEND): the new token is stored as E4M3 codes and joins the
-// softmax as stored (its codes; the K scale is in scale_log2, the V scale in
-// out_scale).
+// With APPEND (a decode step), the entry's new token is one more term -
+// score q . k_new, weight 1, value v_new - and the workgroup of the first
+// query head of each KV head stores the new token's K, V and position for
+// later steps.  KV8 (with APPEND): the new token is stored as E4M3 codes and
+// joins the softmax as stored (its codes; the K scale is in scale_log2, the
+// V scale in out_scale).
 template <int D, bool APPEND, class MP, class SA, bool KV8 = false>
 __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &sa) {
-  constexpr int DPT = D / 64;
-  constexpr int U = kMergeUnroll;
-  __shared__ float s_m[kMergeWaves];
-  __shared__ float s_l[kMergeWaves];
-  __shared__ float s_num[kMergeWaves][D];
+  constexpr int NT = 64 * kMergeWaves;
+  constexpr int NSH = NT / D; // piece shares
+  constexpr int NX = NSH + 2; // the shares, then the sink, then the new token
+  constexpr int CH = kMergeChunk;
+  static_assert(NT % D == 0 && D % 64 == 0, "whole waves per share");
+  __shared__ float s_m[NX];
+  __shared__ float s_l[NX];
+  __shared__ float s_a[NX][D];
+  __shared__ float s_dot[D / 64];
   const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int c = tid % D, sh = tid / D;
   const int b = blockIdx.x / a.hq;
   const int h = blockIdx.x - b * a.hq;
   const int g = h / a.group;
@@ -1048,133 +1053,126 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
     cum[e + 1] = cum[e] + cnt;
   }
   const int total = cum[kMaxSrc];
-  auto row_of = [&](int c) -> int32_t {
+  auto row_of = [&](int i) -> int32_t {
     int e = 0;
 #pragma unroll
-    for (int k = 1; k < kMaxSrc; ++k) e += c >= cum[k];
-    return base[e] + (c - cum[e]) * step[e];
+    for (int k = 1; k < kMaxSrc; ++k) e += i >= cum[k];
+    return base[e] + (i - cum[e]) * step[e];
   };
 
-  // with APPEND the last wave takes the new token only, so its loads overlap
-  // the other waves' partials instead of adding to a share of its own
-  constexpr int NW = APPEND ? kMergeWaves - 1 : kMergeWaves;
-  const int per = (total + NW - 1) / NW;
-  const int cb = min(total, wave * per), ce = min(total, cb + per);
-  float m_w = kNegInf, l_w = 0.f;
-  float num[DPT];
+  // rounds of TILE pieces: the workgroup first lists the round's partial
+  // rows in LDS (one row_of per thread), then share sh folds pieces
+  // sh * CH .. + CH of the round, all of their loads in flight together
+  constexpr int TILE = NSH * CH;
+  static_assert(TILE <= NT, "one row per thread and round");
+  __shared__ int32_t s_rows[TILE];
+  float m_r = kNegInf, l_r = 0.f, a_r = 0.f;
+  for (int t0 = 0; t0 < total; t0 += TILE) {
+    const int nt = min(TILE, total - t0);
+    if (tid < nt) s_rows[tid] = row_of(t0 + tid);
+    __syncthreads();
+    const int kb = sh * CH, ke = min(nt, kb + CH);
+    if (kb < ke) {
+      float mv[CH], lv[CH], av[CH];
 #pragma unroll
-  for (int q = 0; q < DPT; ++q) num[q] = 0.f;
-  if (a.sinks && wave == 0) { // the sink: one more softmax term, with no value
-    m_w = a.sinks[h] * a.sink_scale;
-    l_w = 1.f;
-  }
-  if constexpr (APPEND) {
-    if (wave == kMergeWaves - 1) {
-      const int64_t kv = (int64_t)b * a.hkv + g;
-      const uint16_t *qr = sa.q + ((int64_t)b * a.hq + h) * D + lane * DPT;
-      const uint16_t *kr = sa.k_new + kv * D + lane * DPT;
-      const uint16_t *vr = sa.v_new + kv * D + lane * DPT;
-      float dot = 0.f;
-      uint16_t kb[DPT], vb[DPT];
-#pragma unroll
-      for (int q = 0; q < DPT; ++q) {
-        kb[q] = kr[q];
-        vb[q] = vr[q];
-        float kf = __uint_as_float((uint32_t)kb[q] << 16), vf = __uint_as_float((uint32_t)vb[q] << 16);
-        if constexpr (KV8) { // the codes, and their values as the store holds them
-          kb[q] = (uint16_t)e4m3_encode(kf * sa.inv_k);
-          vb[q] = (uint16_t)e4m3_encode(vf * sa.inv_v);
-          kf = __uint_as_float(e4m3x4_to_bf16(kb[q]).x << 16);
-          vf = __uint_as_float(e4m3x4_to_bf16(vb[q]).x << 16);
-        }
-        dot = fmaf(__uint_as_float((uint32_t)qr[q] << 16), kf, dot);
-        num[q] = vf;
+      for (int u = 0; u < CH; ++u) { // past ke: the share's last piece again, masked below
+        const int32_t row = s_rows[min(kb + u, ke - 1)];
+        mv[u] = a.part_m[row];
+        lv[u] = a.part_l[row];
+        av[u] = a.part_acc[(int64_t)row * D + c];
       }
+      float mx = m_r;
+#pragma unroll
+      for (int u = 0; u < CH; ++u)
+        if (kb + u < ke) mx = fmaxf(mx, mv[u]);
+      if (mx != kNegInf) { // else only empty pieces so far
+        const float sc = exp2_fast(m_r - mx); // 0 while m_r is -inf
+        l_r *= sc;
+        a_r *= sc;
+#pragma unroll
+        for (int u = 0; u < CH; ++u) {
+          const float w = kb + u < ke ? exp2_fast(mv[u] - mx) : 0.f; // 0 for empty pieces
+          l_r = fmaf(w, lv[u], l_r);
+          a_r = fmaf(w, av[u], a_r);
+        }
+        m_r = mx;
+      }
+    }
+    __syncthreads(); // s_rows is rewritten next round
+  }
+  if (c == 0) {
+    s_m[sh] = m_r;
+    s_l[sh] = l_r;
+  }
+  s_a[sh][c] = a_r;
+  if (sh == 0) { // the extra terms: the sink (no value), the new token
+    s_a[NSH][c] = 0.f;
+    float vnew = 0.f;
+    if constexpr (APPEND) {
+      const int64_t kv = (int64_t)b * a.hkv + g;
+      const uint16_t kraw = sa.k_new[kv * D + c], vraw = sa.v_new[kv * D + c];
+      float kf = __uint_as_float((uint32_t)kraw << 16), vf = __uint_as_float((uint32_t)vraw << 16);
+      uint16_t kb = kraw, vb = vraw;
+      if constexpr (KV8) { // the codes, and their values as the store holds them
+        kb = (uint16_t)e4m3_encode(kf * sa.inv_k);
+        vb = (uint16_t)e4m3_encode(vf * sa.inv_v);
+        kf = __uint_as_float(e4m3x4_to_bf16(kb).x << 16);
+        vf = __uint_as_float(e4m3x4_to_bf16(vb).x << 16);
+      }
+      float dot = __uint_as_float((uint32_t)sa.q[((int64_t)b * a.hq + h) * D + c] << 16) * kf;
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
-      m_w = dot * sa.scale_log2;
-      l_w = 1.f;
+      if ((tid & 63) == 0) s_dot[tid >> 6] = dot;
+      vnew = vf;
       if (hr == 0) { // store the new token of KV head g (the same in every head's workgroup)
         const SQ_CONST StepAppend &ap = ((const SQ_CONST StepPlan *)sa.plan)->app;
         const int page = ap.page[b], slot = ap.slot[b];
         const int64_t pb = (int64_t)g * sa.head_stride + (int64_t)page * sa.page_stride;
-#pragma unroll
-        for (int q = 0; q < DPT; ++q) {
-          const int c = lane * DPT + q;
-          if constexpr (KV8) {
-            uint8_t *k8 = reinterpret_cast<uint8_t *>(sa.k), *v8 = reinterpret_cast<uint8_t *>(sa.v);
-            k8[pb + (int64_t)slot * D + c] = (uint8_t)kb[q];
-            v8[pb + (int64_t)c * P + slot] = (uint8_t)vb[q];
-          } else {
-            sa.k[pb + (int64_t)slot * D + c] = kb[q];
-            sa.v[pb + (int64_t)c * P + slot] = vb[q];
-          }
+        if constexpr (KV8) {
+          uint8_t *k8 = reinterpret_cast<uint8_t *>(sa.k), *v8 = reinterpret_cast<uint8_t *>(sa.v);
+          k8[pb + (int64_t)slot * D + c] = (uint8_t)kb;
+          v8[pb + (int64_t)c * P + slot] = (uint8_t)vb;
+        } else {
+          sa.k[pb + (int64_t)slot * D + c] = kb;
+          sa.v[pb + (int64_t)c * P + slot] = vb;
         }
-        if (lane == 0 && g == 0) sa.pos[(int64_t)page * P + slot] = ap.pos[b];
+        if (c == 0 && g == 0) sa.pos[(int64_t)page * P + slot] = ap.pos[b];
       }
     }
+    s_a[NSH + 1][c] = vnew;
   }
-  for (int i = cb; i < ce; i += U) {
-    float x[U][DPT];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float *src = a.part_acc + (int64_t)row_of(min(i + u, ce - 1)) * D + lane * DPT;
-#pragma unroll
-      for (int q = 0; q < DPT; ++q) x[u][q] = src[q];
-    }
-    float mu = kNegInf, lu = 0.f;
-    if (lane < U && i + lane < ce) {
-      const int32_t row = row_of(i + lane);
-      mu = a.part_m[row];
-      lu = a.part_l[row];
-    }
-    float rmax = mu;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) rmax = fmaxf(rmax, __shfl_xor(rmax, o));
-    const float m_new = fmaxf(m_w, rmax);
-    if (m_new == kNegInf) continue; // only empty partials so far
-    const float sc = exp2_fast(m_w - m_new); // 0 while m_w is -inf
-    const float wu_lane = exp2_fast(mu - m_new); // 0 for empty partials and idle lanes
-    float lsum = wu_lane * lu;
-#pragma unroll
-    for (int o = 32; o > 0; o >>= 1) lsum += __shfl_xor(lsum, o);
-    l_w = l_w * sc + lsum;
-#pragma unroll
-    for (int q = 0; q < DPT; ++q) num[q] *= sc;
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const float wu = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wu_lane), u));
-#pragma unroll
-      for (int q = 0; q < DPT; ++q) num[q] = fmaf(wu, x[u][q], num[q]);
-    }
-    m_w = m_new;
-  }
-  if (lane == 0) {
-    s_m[wave] = m_w;
-    s_l[wave] = l_w;
-  }
-#pragma unroll
-  for (int q = 0; q < DPT; ++q) s_num[wave][lane * DPT + q] = num[q];
   __syncthreads();
-  if (wave == 0) {
+  if (tid < D) {
+    float xm[NX], xl[NX];
+#pragma unroll
+    for (int x = 0; x < NSH; ++x) {
+      xm[x] = s_m[x];
+      xl[x] = s_l[x];
+    }
+    xm[NSH] = a.sinks ? a.sinks[h] * a.sink_scale : kNegInf;
+    xl[NSH] = a.sinks ? 1.f : 0.f;
+    xm[NSH + 1] = kNegInf;
+    xl[NSH + 1] = 0.f;
+    if constexpr (APPEND) {
+      float dot = 0.f;
+#pragma unroll
+      for (int w = 0; w < D / 64; ++w) dot += s_dot[w];
+      xm[NSH + 1] = dot * sa.scale_log2;
+      xl[NSH + 1] = 1.f;
+    }
     float mm = kNegInf;
 #pragma unroll
-    for (int w = 0; w < kMergeWaves; ++w) mm = fmaxf(mm, s_m[w]);
-    float sc[kMergeWaves];
-    float dt = 0.f;
+    for (int x = 0; x < NX; ++x) mm = fmaxf(mm, xm[x]);
+    float num = 0.f, den = 0.f;
+    if (mm != kNegInf) {
 #pragma unroll
-    for (int w = 0; w < kMergeWaves; ++w) {
-      sc[w] = mm == kNegInf ? 0.f : exp2_fast(s_m[w] - mm);
-      dt = fmaf(sc[w], s_l[w], dt);
+      for (int x = 0; x < NX; ++x) {
+        const float w = exp2_fast(xm[x] - mm); // 0 for -inf terms
+        den = fmaf(w, xl[x], den);
+        num = fmaf(w, s_a[x][c], num);
+      }
     }
-    float *out = a.out + ((int64_t)b * a.hq + h) * D + lane * DPT;
-#pragma unroll
-    for (int q = 0; q < DPT; ++q) {
-      float nt = 0.f;
-#pragma unroll
-      for (int w = 0; w < kMergeWaves; ++w) nt = fmaf(sc[w], s_num[w][lane * DPT + q], nt);
-      out[q] = dt > 0.f ? nt / dt * a.out_scale : 0.f;
-    }
+    a.out[((int64_t)b * a.hq + h) * D + c] = den > 0.f ? num / den * a.out_scale : 0.f;
   }
 }
 
