@@ -53,7 +53,13 @@ def parse_args():
                          "fullstack, postevict, cpu, copy (a plain 1 GiB device copy used to "
                          "calibrate HBM byte counters)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-graph", action="store_true",
+                    help="leave out the graph-replay timings (for rocprofv3 counter runs, "
+                         "whose collection does not follow graph replays)")
     return ap.parse_args()
+
+
+GRAPH_TIMINGS = True
 
 
 DECODE_SOURCES = ("decode_kernels.hip", "decode_args.hpp", "sq_common.hpp", "fp8.hpp")
@@ -260,6 +266,33 @@ def time_events(torch, fn, reps, flush=None):
     return percentiles([a.elapsed_time(b) for a, b in ev])
 
 
+def graph_time(torch, fn, reps, flush=None):
+    """GPU time of fn() with the host out of the way: fn's launches captured
+    in a HIP graph and replayed.  Warm (flush None): 20 calls per graph, time
+    per call; cold: a one-call graph replayed after each cache flush.
+    Percentiles in ms; None with --no-graph."""
+    if not GRAPH_TIMINGS:
+        return None
+    n = 1 if flush is not None else 20
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(n):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for a, b in ev:
+        if flush is not None:
+            flush()
+        a.record()
+        g.replay()
+        b.record()
+    torch.cuda.synchronize()
+    del g
+    return percentiles([a.elapsed_time(b) / n for a, b in ev])
+
+
 def evict_bytes(stats, length, kept):
     """Algorithmic bytes of one eviction: the moved tokens' K, V (every layer
     and head) and positions read and written, plus the index arrays (keep
@@ -362,7 +395,9 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False,
             step()
         torch.cuda.synchronize()
         res[name] = (time.perf_counter() - t0) * 1e3 / 32
-        pct[name] = dict(warm=time_events(torch, step, 32), cold=time_events(torch, step, 16, flush))
+        pct[name] = dict(warm=time_events(torch, step, 32), cold=time_events(torch, step, 16, flush),
+                         graph_warm=graph_time(torch, step, 16),
+                         graph_cold=graph_time(torch, step, 16, flush))
     del flush
     info.update(decode_ms_compacted=res["compacted"], decode_ms_full=res["full"],
                 decode_step_ms=pct)
@@ -373,9 +408,12 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False,
 def _decode_split(torch, store, seqs, q, out, reps, flush=None, layers=(0,)):
     """A decode call (every layer in ``layers``, batch ``seqs``): GPU time
     per call from HIP events around it on the current stream (median over
-    ``reps``, each after a cache flush when ``flush`` is given), then, in a
-    second pass with the library's per-kernel events on (which add gaps of
-    their own), the decode kernel and merge times within a call."""
+    ``reps``, each after a cache flush when ``flush`` is given; the events
+    also see the host's submission of the call when the GPU waits for it),
+    the same from replays of the call captured in a HIP graph (no host
+    between the events), then, in a second pass with the library's
+    per-kernel events on (which add gaps of their own), the decode kernel
+    and merge times within a call."""
     def call():
         for layer in layers:
             store.decode(layer, seqs, q, out=out)
@@ -383,6 +421,7 @@ def _decode_split(torch, store, seqs, q, out, reps, flush=None, layers=(0,)):
         call()
     torch.cuda.synchronize()
     gpu = time_events(torch, call, reps, flush)
+    graph = graph_time(torch, call, reps, flush)
     store.profile_enable(True)
     store.profile_read()
     for _ in range(reps):
@@ -397,7 +436,9 @@ def _decode_split(torch, store, seqs, q, out, reps, flush=None, layers=(0,)):
     dec = (prof["decode_mfma_ms"] + prof["decode_valu_ms"]) / reps
     mrg = prof["decode_merge_ms"] / reps
     plan = store.plan_info(seqs)
-    return dict(call_ms=gpu, kv_bytes=kv, gbps_call=round(kv / (med * 1e-3) / 1e9, 1),
+    return dict(call_ms=gpu, graph_call_ms=graph, kv_bytes=kv,
+                gbps_call=round(kv / (med * 1e-3) / 1e9, 1),
+                gbps_graph=round(kv / (graph["median"] * 1e-3) / 1e9, 1) if graph else None,
                 decode_kernel_ms=round(dec, 4), merge_ms=round(mrg, 4),
                 launch_gaps_ms=round(med - dec - mrg, 4),
                 gbps_decode_kernel=round(kv / (dec * 1e-3) / 1e9, 1) if dec else None,
@@ -846,7 +887,9 @@ def cpu_leg(sample, wl, budget_s):
 
 
 def main():
+    global GRAPH_TIMINGS
     args = parse_args()
+    GRAPH_TIMINGS = not args.no_graph
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (got --gpus {args.gpus}); the library has no "
               "multi-GPU path", file=sys.stderr)

@@ -965,7 +965,8 @@ k_step_mfma8(DecodeStatic a, const DecodeDyn *dyn) {
 // Its partials are the pieces of at most kMaxSrc segments (the shared runs on
 // its path through the tree of forks, then its own suffix).  Thread t takes
 // channel t % D of share t / D of each round of NSH * kMergeChunk pieces
-// (the round's partial rows listed in LDS first): it loads its share's
+// (the round's partial rows listed in LDS first, pieces dealt to the shares
+// round-robin): it loads its share's
 // (m, l) pairs itself (the same addresses across the share's threads, one
 // request per wave) and its channel of each acc row, all in flight
 // together, and folds them into a running (m, l, acc) with the usual
@@ -1061,8 +1062,10 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
   };
 
   // rounds of TILE pieces: the workgroup first lists the round's partial
-  // rows in LDS (one row_of per thread), then share sh folds pieces
-  // sh * CH .. + CH of the round, all of their loads in flight together
+  // rows in LDS (one row lookup per thread), then share sh folds pieces
+  // sh, sh + NSH, ... of the round (pieces dealt round-robin, so that a few
+  // pieces still spread over every share), all of their loads in flight
+  // together
   constexpr int TILE = NSH * CH;
   static_assert(TILE <= NT, "one row per thread and round");
   __shared__ int32_t s_rows[TILE];
@@ -1071,32 +1074,34 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
     const int nt = min(TILE, total - t0);
     if (tid < nt) s_rows[tid] = row_of(t0 + tid);
     __syncthreads();
-    const int kb = sh * CH, ke = min(nt, kb + CH);
-    if (kb < ke) {
-      float mv[CH], lv[CH], av[CH];
+    const int cnt = sh < nt ? (nt - sh + NSH - 1) / NSH : 0; // this share's pieces (uniform)
+    float mv[CH], lv[CH], av[CH];
 #pragma unroll
-      for (int u = 0; u < CH; ++u) { // past ke: the share's last piece again, masked below
-        const int32_t row = s_rows[min(kb + u, ke - 1)];
+    for (int u = 0; u < CH; ++u) {
+      mv[u] = kNegInf;
+      lv[u] = 0.f;
+      av[u] = 0.f;
+      if (u < cnt) {
+        const int32_t row = s_rows[sh + NSH * u];
         mv[u] = a.part_m[row];
         lv[u] = a.part_l[row];
         av[u] = a.part_acc[(int64_t)row * D + c];
       }
-      float mx = m_r;
+    }
+    float mx = m_r;
 #pragma unroll
-      for (int u = 0; u < CH; ++u)
-        if (kb + u < ke) mx = fmaxf(mx, mv[u]);
-      if (mx != kNegInf) { // else only empty pieces so far
-        const float sc = exp2_fast(m_r - mx); // 0 while m_r is -inf
-        l_r *= sc;
-        a_r *= sc;
+    for (int u = 0; u < CH; ++u) mx = fmaxf(mx, mv[u]);
+    if (mx != kNegInf) { // else only empty pieces so far
+      const float sc = exp2_fast(m_r - mx); // 0 while m_r is -inf
+      l_r *= sc;
+      a_r *= sc;
 #pragma unroll
-        for (int u = 0; u < CH; ++u) {
-          const float w = kb + u < ke ? exp2_fast(mv[u] - mx) : 0.f; // 0 for empty pieces
-          l_r = fmaf(w, lv[u], l_r);
-          a_r = fmaf(w, av[u], a_r);
-        }
-        m_r = mx;
+      for (int u = 0; u < CH; ++u) {
+        const float w = exp2_fast(mv[u] - mx); // 0 for empty and absent pieces
+        l_r = fmaf(w, lv[u], l_r);
+        a_r = fmaf(w, av[u], a_r);
       }
+      m_r = mx;
     }
     __syncthreads(); // s_rows is rewritten next round
   }
@@ -1105,7 +1110,7 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
     s_l[sh] = l_r;
   }
   s_a[sh][c] = a_r;
-  if (sh == 0) { // the extra terms: the sink (no value), the new token
+  if (sh == NSH - 1) { // the extra terms: the sink (no value), the new token
     s_a[NSH][c] = 0.f;
     float vnew = 0.f;
     if constexpr (APPEND) {
@@ -1122,7 +1127,7 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
       float dot = __uint_as_float((uint32_t)sa.q[((int64_t)b * a.hq + h) * D + c] << 16) * kf;
 #pragma unroll
       for (int o = 32; o > 0; o >>= 1) dot += __shfl_xor(dot, o);
-      if ((tid & 63) == 0) s_dot[tid >> 6] = dot;
+      if ((tid & 63) == 0) s_dot[(tid >> 6) % (D / 64)] = dot;
       vnew = vf;
       if (hr == 0) { // store the new token of KV head g (the same in every head's workgroup)
         const SQ_CONST StepAppend &ap = ((const SQ_CONST StepPlan *)sa.plan)->app;

@@ -141,8 +141,9 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
     private tokens and names seeded-random live tool spans until at least
     60% of the live tool tokens are covered; Phase 3 appends the turn.
     With ``decode``, one decode step ([main] or [main, aux], every layer) is
-    run at the end of each turn and ``on_turn(t, store, seqs, q, out)`` is
-    called after it.  Returns (store, main, aux, log, workload): aux is the
+    timed at the end of each turn (median of three after an untimed one; the
+    steps read the cache and change nothing) and ``on_turn(t, store, seqs,
+    q, out)`` is called after it.  Returns (store, main, aux, log, workload): aux is the
     auxiliary thread still alive after the last turn (or None); log has one
     record per turn.  evict_chunk_pages > 0 evicts in chunks of that many
     fresh pages (bounded transient pages); ``evict_inplace`` rewrites the
@@ -212,12 +213,20 @@ def run_full_stack(evict=True, turns=30, turn_len=8192, prefix=16384, num_layers
         if decode:
             q = wl.device_normal_bf16((len(seqs), 32, 128), w.seed * 1000 + 7919 + t, device)
             out = torch.empty((len(seqs), 32, 128), dtype=torch.float32, device=device)
-            torch.cuda.synchronize()
-            t0 = time.perf_counter()
-            for layer in range(num_layers):
-                store.decode(layer, seqs, q, out=out)
-            torch.cuda.synchronize()
-            rec["decode_ms"] = (time.perf_counter() - t0) * 1e3
+            # the median of three timed steps after an untimed one: a single
+            # sample also carries one-time costs (the first reads of the
+            # turn's new pages, the clocks ramping up after host-only work),
+            # which differ between runs that do and do not extend each turn
+            walls = []
+            for rep in range(4):
+                torch.cuda.synchronize()
+                t0 = time.perf_counter()
+                for layer in range(num_layers):
+                    store.decode(layer, seqs, q, out=out)
+                torch.cuda.synchronize()
+                if rep:
+                    walls.append((time.perf_counter() - t0) * 1e3)
+            rec["decode_ms"] = sorted(walls)[1]
             rec["kv_bytes"] = store.plan_info(seqs)["kv_bytes"] * num_layers
             if on_turn is not None:
                 on_turn(t, store, seqs, q, out)
