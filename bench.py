@@ -268,29 +268,40 @@ def time_events(torch, fn, reps, flush=None):
 
 def graph_time(torch, fn, reps, flush=None):
     """GPU time of fn() with the host out of the way: fn's launches captured
-    in a HIP graph and replayed.  Warm (flush None): 20 calls per graph, time
-    per call; cold: a one-call graph replayed after each cache flush.
-    Percentiles in ms; None with --no-graph."""
+    in a HIP graph of 20 calls and replayed, time per call.  Cold (flush
+    given): the graph holds 20 (cache flush, call) pairs, and the time of a
+    graph of the 20 flushes alone is taken off.  Percentiles in ms over
+    reps replays; None with --no-graph."""
     if not GRAPH_TIMINGS:
         return None
-    n = 1 if flush is not None else 20
-    g = torch.cuda.CUDAGraph()
-    with torch.cuda.graph(g):
-        for _ in range(n):
-            fn()
-    g.replay()
-    torch.cuda.synchronize()
-    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-          for _ in range(reps)]
-    for a, b in ev:
-        if flush is not None:
-            flush()
-        a.record()
+    n = 20
+
+    def replay_ms(body):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            for _ in range(n):
+                body()
         g.replay()
-        b.record()
-    torch.cuda.synchronize()
-    del g
-    return percentiles([a.elapsed_time(b) / n for a, b in ev])
+        torch.cuda.synchronize()
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(reps)]
+        for a, b in ev:
+            a.record()
+            g.replay()
+            b.record()
+        torch.cuda.synchronize()
+        del g
+        return [a.elapsed_time(b) for a, b in ev]
+
+    if flush is None:
+        return percentiles([t / n for t in replay_ms(fn)])
+
+    def both():
+        flush()
+        fn()
+    with_call = replay_ms(both)
+    alone = sorted(replay_ms(flush))[len(with_call) // 2]
+    return percentiles([(t - alone) / n for t in with_call])
 
 
 def evict_bytes(stats, length, kept):
