@@ -526,6 +526,19 @@ const char *sq_last_error(void);
 /* SQ_ABI_VERSION of the loaded library. */
 int32_t sq_abi_version(void);
 
+/* Host call trace (off by default).  While open, every state-changing or
+ * compute call (store create/destroy, sequence create, appends, span marks,
+ * forks, releases, evictions, compaction, decode, decode steps, extend)
+ * writes one line: "sq <call>(<arguments>) host_us=<time> ok" or
+ * "... error: <message>", the time being the call's host time (device work
+ * is only enqueued).  path "-" traces to stderr, another path appends to
+ * that file, NULL closes the trace.  The environment variable SQ_TRACE,
+ * read once when the library loads, opens one the same way ("1" or "-":
+ * stderr; "0" or empty: none; otherwise a file path).  Lines are written
+ * whole by concurrent threads.  SQ_ERR_INVALID if the file cannot be
+ * opened (the previous trace stays open). */
+sq_status sq_trace_open(const char *path);
+
 #ifdef __cplusplus
 }
 #endif

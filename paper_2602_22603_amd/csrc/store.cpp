@@ -15,6 +15,8 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
+#include <chrono>
 #include <functional>
 #include <cmath>
 #include <cstdarg>
@@ -22,6 +24,7 @@
 #include <cstdlib>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -31,6 +34,7 @@
 namespace {
 
 thread_local std::string g_err;
+thread_local uint64_t g_fails = 0; // failures on this thread (the call trace reads it)
 
 sq_status fail(sq_status st, const char *fmt, ...) {
   char buf[512];
@@ -39,8 +43,75 @@ sq_status fail(sq_status st, const char *fmt, ...) {
   vsnprintf(buf, sizeof(buf), fmt, ap);
   va_end(ap);
   g_err = buf;
+  ++g_fails;
   return st;
 }
+
+// ---- host call trace -------------------------------------------------------
+// One line per state-changing or compute call while a trace is open: the
+// call, its arguments, its host time and its outcome.  Off by default; the
+// cost when off is one relaxed atomic load per call.
+std::mutex g_trace_mu;
+FILE *g_trace = nullptr;
+bool g_trace_owned = false;
+std::atomic<bool> g_trace_on{false};
+
+struct CallTrace {
+  const char *name;
+  bool on;
+  uint64_t fails0 = 0;
+  std::chrono::steady_clock::time_point t0;
+  char args[224];
+  CallTrace(const char *n, const char *fmt, ...) __attribute__((format(printf, 3, 4)))
+      : name(n), on(g_trace_on.load(std::memory_order_relaxed)) {
+    if (!on) return;
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(args, sizeof(args), fmt, ap);
+    va_end(ap);
+    fails0 = g_fails;
+    t0 = std::chrono::steady_clock::now();
+  }
+  ~CallTrace() {
+    if (!on) return;
+    const double us =
+        std::chrono::duration<double, std::micro>(std::chrono::steady_clock::now() - t0).count();
+    std::lock_guard<std::mutex> lk(g_trace_mu);
+    if (!g_trace) return;
+    if (g_fails != fails0) std::fprintf(g_trace, "sq %s(%s) host_us=%.1f error: %s\n", name, args, us, g_err.c_str());
+    else std::fprintf(g_trace, "sq %s(%s) host_us=%.1f ok\n", name, args, us);
+    std::fflush(g_trace);
+  }
+};
+#define SQ_TRACE_CALL(name, ...) CallTrace sq_call_trace_(name, __VA_ARGS__)
+
+sq_status trace_open(const char *path) {
+  std::lock_guard<std::mutex> lk(g_trace_mu);
+  FILE *f = nullptr;
+  bool owned = false;
+  if (path && std::strcmp(path, "-") == 0) {
+    f = stderr;
+  } else if (path) {
+    f = std::fopen(path, "a");
+    if (!f) return fail(SQ_ERR_INVALID, "cannot open trace file %s", path);
+    owned = true;
+  }
+  if (g_trace_owned && g_trace) std::fclose(g_trace);
+  g_trace = f;
+  g_trace_owned = owned;
+  g_trace_on.store(f != nullptr, std::memory_order_relaxed);
+  return SQ_OK;
+}
+
+// SQ_TRACE in the environment when the library loads: "1" or "-" logs to
+// stderr, any other value is a file to append to.
+struct TraceFromEnv {
+  TraceFromEnv() {
+    const char *e = std::getenv("SQ_TRACE");
+    if (!e || !*e || std::strcmp(e, "0") == 0) return;
+    (void)trace_open(std::strcmp(e, "1") == 0 ? "-" : e);
+  }
+} g_trace_from_env;
 
 sq_status hip_fail(hipError_t e, const char *what) {
   return fail(SQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -751,6 +822,8 @@ extern "C" {
 
 int32_t sq_abi_version(void) { return SQ_ABI_VERSION; }
 
+sq_status sq_trace_open(const char *path) { return trace_open(path); }
+
 const char *sq_last_error(void) { return g_err.c_str(); }
 
 uint64_t sq_workspace_bytes(const sq_store_config *cfg) {
@@ -769,6 +842,7 @@ uint64_t sq_pool_bytes(const sq_store_config *cfg, int32_t which) {
 }
 
 sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
+  SQ_TRACE_CALL("sq_store_create", "layers=%d q_heads=%d kv_heads=%d head_dim=%d pages=%d flags=%u", cfg ? cfg->num_layers : -1, cfg ? cfg->num_q_heads : -1, cfg ? cfg->num_kv_heads : -1, cfg ? cfg->head_dim : -1, cfg ? cfg->num_pages : -1, cfg ? cfg->flags : 0u);
   if (!out) return fail(SQ_ERR_INVALID, "null output pointer");
   const bool device = cfg && !(cfg->flags & SQ_STORE_METADATA_ONLY);
   std::string why;
@@ -896,6 +970,7 @@ sq_status sq_store_create(const sq_store_config *cfg, sq_store **out) {
 }
 
 sq_status sq_store_destroy(sq_store *s) {
+  SQ_TRACE_CALL("sq_store_destroy", "store=%p", (void *)s);
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   if (s->device) {
     if (s->staging_pending) (void)hipEventSynchronize(s->staging_ev);
@@ -918,6 +993,7 @@ sq_status sq_store_destroy(sq_store *s) {
 }
 
 sq_status sq_seq_create(sq_store *s, sq_seq *out) {
+  SQ_TRACE_CALL("sq_seq_create", "store=%p", (void *)s);
   if (!s || !out) return fail(SQ_ERR_INVALID, "null argument");
   for (int32_t h = 0; h < s->cfg.max_seqs; ++h) {
     if (!s->seqs[h].live) {
@@ -933,6 +1009,7 @@ sq_status sq_seq_create(sq_store *s, sq_seq *out) {
 
 sq_status sq_append(sq_store *s, sq_seq h, int32_t n, const void *k_new, const void *v_new,
                     void *stream) {
+  SQ_TRACE_CALL("sq_append", "store=%p seq=%d n=%d", (void *)s, h, n);
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
@@ -1124,6 +1201,7 @@ sq_status decode_call(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t ba
 
 sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const void *k_new,
                           const void *v_new, void *stream) {
+  SQ_TRACE_CALL("sq_append_batch", "store=%p batch=%d", (void *)s, batch);
   sq_status r = check_one_token_each(s, seqs, batch);
   if (r != SQ_OK) return r;
   if (s->device) {
@@ -1153,6 +1231,7 @@ sq_status sq_append_batch(sq_store *s, const sq_seq *seqs, int32_t batch, const 
 }
 
 sq_status sq_span_mark(sq_store *s, sq_seq h, int32_t cursor, int64_t start, int64_t end) {
+  SQ_TRACE_CALL("sq_span_mark", "store=%p seq=%d cursor=%d start=%lld end=%lld", (void *)s, h, cursor, (long long)start, (long long)end);
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
@@ -1177,6 +1256,7 @@ sq_status sq_span_mark(sq_store *s, sq_seq h, int32_t cursor, int64_t start, int
 }
 
 sq_status sq_fork(sq_store *s, sq_seq parent, int64_t fork_len, sq_seq *child, void *stream) {
+  SQ_TRACE_CALL("sq_fork", "store=%p parent=%d fork_len=%lld", (void *)s, parent, (long long)fork_len);
   if (!s || !child) return fail(SQ_ERR_INVALID, "null argument");
   Seq *par = s->get(parent);
   if (!par) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", parent);
@@ -1244,6 +1324,7 @@ sq_status sq_fork(sq_store *s, sq_seq parent, int64_t fork_len, sq_seq *child, v
 }
 
 sq_status sq_release(sq_store *s, sq_seq h) {
+  SQ_TRACE_CALL("sq_release", "store=%p seq=%d", (void *)s, h);
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
@@ -1260,6 +1341,7 @@ sq_status sq_evict_spans(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32
 }
 
 sq_status sq_compact(sq_store *s, sq_seq h, void *stream, sq_evict_stats *stats) {
+  SQ_TRACE_CALL("sq_compact", "store=%p seq=%d", (void *)s, h);
   return sq_evict_spans_ex(s, h, nullptr, 0, 0, stream, stats);
 }
 
@@ -1365,6 +1447,7 @@ sq_status evict_inplace_launches(sq_store *s, sq_seq h, int64_t fp, int64_t n_ne
 
 sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, int32_t n,
                             uint32_t flags, void *stream, sq_evict_stats *stats) {
+  SQ_TRACE_CALL("sq_evict_spans", "store=%p seq=%d n_cursors=%d flags=%u", (void *)s, h, n, flags);
   if (!s) return fail(SQ_ERR_INVALID, "null store");
   Seq *q = s->get(h);
   if (!q) return fail(SQ_ERR_UNKNOWN_SEQ, "unknown sequence %d", h);
@@ -1697,12 +1780,14 @@ sq_status sq_decode_attn(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t
 sq_status sq_decode_attn_ex(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
                             const void *q, float *out, float scale, int32_t mode,
                             const sq_attn_opts *opts, void *stream) {
+  SQ_TRACE_CALL("sq_decode_attn", "store=%p layer=%d batch=%d mode=%d window=%d sinks=%d", (void *)s, layer, batch, mode, opts ? opts->window : 0, opts && opts->sinks ? 1 : 0);
   return decode_call(s, layer, seqs, batch, q, out, scale, mode, opts, stream, nullptr);
 }
 
 sq_status sq_decode_attn_noalloc(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t batch,
                                  const void *q, float *out, float scale, int32_t mode,
                                  void *stream) {
+  SQ_TRACE_CALL("sq_decode_attn_noalloc", "store=%p layer=%d batch=%d mode=%d", (void *)s, layer, batch, mode);
   if (s && s->device && s->spart_err != hipSuccess)
     return hip_fail(s->spart_err, "allocation-free partials (hipGetSymbolAddress at store creation)");
   return decode_call(s, layer, seqs, batch, q, out, scale, mode, nullptr, stream,
@@ -1716,6 +1801,7 @@ sq_status sq_step_begin(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t 
 
 sq_status sq_step_begin_ex(sq_store *s, const sq_seq *seqs, int32_t batch, int32_t mode,
                            int32_t window, void *stream) {
+  SQ_TRACE_CALL("sq_step_begin", "store=%p batch=%d mode=%d window=%d", (void *)s, batch, mode, window);
   sq_status r = check_one_token_each(s, seqs, batch);
   if (r != SQ_OK) return r;
   if (mode < SQ_ATTN_AUTO || mode > SQ_ATTN_MFMA) return fail(SQ_ERR_INVALID, "unknown mode %d", mode);
@@ -1812,6 +1898,7 @@ sq_status sq_step_attn(sq_store *s, int32_t layer, const void *k_new, const void
 sq_status sq_step_attn_ex(sq_store *s, int32_t layer, const void *k_new, const void *v_new,
                           const void *q, float *out, float scale, const sq_attn_opts *opts,
                           void *stream) {
+  SQ_TRACE_CALL("sq_step_attn", "store=%p layer=%d window=%d sinks=%d", (void *)s, layer, opts ? opts->window : 0, opts && opts->sinks ? 1 : 0);
   sq_attn_opts o{};
   sq_status r = take_opts(opts, &o);
   if (r != SQ_OK) return r;
@@ -1877,6 +1964,7 @@ sq_status sq_extend_attn(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, 
 
 sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_new, const void *q,
                             float *out, float scale, const sq_attn_opts *opts, void *stream) {
+  SQ_TRACE_CALL("sq_extend_attn", "store=%p layer=%d seq=%d n_new=%d window=%d sinks=%d", (void *)s, layer, seq, n_new, opts ? opts->window : 0, opts && opts->sinks ? 1 : 0);
   sq_attn_opts o{};
   sq_status r = take_opts(opts, &o);
   if (r != SQ_OK) return r;

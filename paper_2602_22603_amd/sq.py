@@ -97,6 +97,7 @@ _LIB = None
 _SIGS = {
     "sq_abi_version": (C.c_int32, []),
     "sq_last_error": (C.c_char_p, []),
+    "sq_trace_open": (C.c_int, [C.c_char_p]),
     "sq_workspace_bytes": (C.c_uint64, [C.POINTER(StoreConfig)]),
     "sq_pool_bytes": (C.c_uint64, [C.POINTER(StoreConfig), C.c_int32]),
     "sq_store_create": (C.c_int, [C.POINTER(StoreConfig), C.POINTER(C.c_void_p)]),
@@ -176,6 +177,11 @@ def _check(status):
     if status != OK:
         msg = lib().sq_last_error().decode(errors="replace")
         raise SqError(status, msg)
+
+
+def trace_open(path):
+    """Host call trace: "-" to stderr, a path to append to, None to close."""
+    _check(lib().sq_trace_open(None if path is None else str(path).encode()))
 
 
 def _i32_array(values):

@@ -634,3 +634,52 @@ def test_tree_plan_reads_every_distinct_page_once(sq, seed):
                 partial += L % P
             info = s.plan_info(batch, sq.ATTN_AUTO)
             assert info["kv_bytes"] == (len(full) * P + partial) * tok, (batch, info)
+
+
+def test_host_call_trace(sq, tmp_path):
+    """sq_trace_open: one line per state-changing call, in call order, with
+    its arguments, host time and outcome; nothing once closed."""
+    path = tmp_path / "trace.log"
+    sq.trace_open(path)
+    try:
+        s = _store(sq, 40, 4, 4, 20)
+        a = s.seq_create()
+        s.append(a, n=30)
+        s.span_mark(a, 7, 4, 12)
+        b = s.fork(a, 16)
+        with pytest.raises(sq.SqError):
+            s.evict(a, [99])                     # unknown cursor: a failed call
+        s.evict(a, [7])
+        s.release(b)
+        s.page_table(a)                          # introspection is not traced
+    finally:
+        sq.trace_open(None)
+    s.append(a, n=1)                             # after the trace closed
+    lines = path.read_text().splitlines()
+    calls = [re.match(r"sq (\w+)\(", l).group(1) for l in lines]
+    assert calls == ["sq_store_create", "sq_seq_create", "sq_append", "sq_span_mark", "sq_fork",
+                     "sq_evict_spans", "sq_evict_spans", "sq_release"]
+    assert "seq=0 n=30" in lines[2] and "cursor=7 start=4 end=12" in lines[3]
+    assert "parent=0 fork_len=16" in lines[4]
+    assert lines[5].split("host_us=")[1].split()[1] == "error:" and "99" in lines[5]
+    for l in lines[:5] + lines[6:]:
+        assert l.endswith(" ok"), l
+        assert float(l.split("host_us=")[1].split()[0]) >= 0.0
+    with pytest.raises(sq.SqError):
+        sq.trace_open(tmp_path / "no_such_dir" / "trace.log")
+
+
+def test_host_call_trace_from_environment(tmp_path):
+    """SQ_TRACE names the trace file when the library loads."""
+    import subprocess
+    import sys
+    path = tmp_path / "env_trace.log"
+    code = ("import sys; sys.path.insert(0, %r)\n"
+            "from paper_2602_22603_amd import sq\n"
+            "s = sq.Store(1, 4, 2, 8, num_pages=8, max_seqs=2, max_pages_per_seq=8,"
+            " page_size=4, metadata_only=True)\n"
+            "s.append(s.seq_create(), n=5)\n") % ROOT
+    env = dict(os.environ, SQ_TRACE=str(path))
+    subprocess.run([sys.executable, "-c", code], check=True, env=env, timeout=120)
+    calls = [re.match(r"sq (\w+)\(", l).group(1) for l in path.read_text().splitlines()]
+    assert calls[:3] == ["sq_store_create", "sq_seq_create", "sq_append"]
