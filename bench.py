@@ -304,6 +304,37 @@ def graph_time(torch, fn, reps, flush=None):
     return percentiles([(t - alone) / n for t in with_call])
 
 
+def evict_gpu_time(torch, store, victim, ids, reps, flush):
+    """GPU time of one eviction call's device work (index, gather and the
+    page-table writes, with the gaps between them on the GPU), the host out
+    of the way: one event pair around the call, recorded while the GPU is
+    still busy with work queued before it - a spin kernel (warm: it touches
+    no memory) or the 1 GiB cache flush (cold) - so that the call's
+    launches are all queued before the GPU reaches the first event.
+    Percentiles in ms."""
+    res = {}
+    for temp in ("warm", "cold"):
+        times = []
+        for r in range(reps + 1):
+            f = victim()
+            torch.cuda.synchronize()
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            if temp == "cold":
+                flush()
+            else:
+                torch.cuda._sleep(1_000_000)
+            a.record()
+            store.evict(f, ids)
+            b.record()
+            torch.cuda.synchronize()
+            if r >= 1:
+                times.append(a.elapsed_time(b))
+            store.release(f)
+        res[temp] = percentiles(times)
+    return res
+
+
 def evict_bytes(stats, length, kept):
     """Algorithmic bytes of one eviction: the moved tokens' K, V (every layer
     and head) and positions read and written, plus the index arrays (keep
@@ -318,7 +349,10 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False,
     warm (back to back: the ~180 MB read and written fit the 256 MB MALL)
     and cold (a 1 GiB write flushes the MALL and L2 before each call).
     GB/s divide the algorithmic bytes by the index kernel plus the gather
-    (HIP events around each kernel), and by the wall clock of the whole call."""
+    (the library's HIP events around each launch, which also see the
+    host's submission of the launch when the GPU waits for it), by the
+    call's device work with the host out of the way (evict_gpu_time), and
+    by the wall clock of the whole call."""
     from paper_2602_22603_amd import drivers
     store, base, w, k, v = drivers.build_compaction64k(evict_chunk_pages=chunk, align=align,
                                                        evict_remap=remap, evict_inplace=inplace)
@@ -362,6 +396,7 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False,
         store.profile_enable(False)
         kern = (prof["evict_scan_ms"] + prof["evict_gather_ms"]) / reps
         runs[temp] = dict(walls=walls, kern=kern, prof=prof)
+    gpu = evict_gpu_time(torch, store, victim, w.evict_ids, reps, flush)
     kept = L - stats["tokens_removed"]
     alg = evict_bytes(stats, L, kept)
     wall = {t: med(runs[t]["walls"]) for t in runs}
@@ -381,7 +416,9 @@ def evict_leg(sq, torch, wl, reps=8, chunk=0, decode=True, align=0, remap=False,
         evict_gbps_cold=round(alg / (runs["cold"]["kern"] * 1e-3) / 1e9, 1) if runs["cold"]["kern"] else None,
         evict_gbps_warm=round(alg / (runs["warm"]["kern"] * 1e-3) / 1e9, 1) if runs["warm"]["kern"] else None,
         evict_wall_ms_median={t: round(wall[t] * 1e3, 4) for t in wall},
-        evict_gbps_wall={t: round(alg / wall[t] / 1e9, 1) for t in wall})
+        evict_gbps_wall={t: round(alg / wall[t] / 1e9, 1) for t in wall},
+        evict_gpu_ms=gpu,
+        evict_gbps_gpu={t: round(alg / (gpu[t]["median"] * 1e-3) / 1e9, 1) for t in gpu})
     if info["evict_gbps_cold"]:
         info["frac_of_hbm_peak_cold"] = round(info["evict_gbps_cold"] / HBM_PEAK_GBPS, 4)
     if not decode:

@@ -179,6 +179,16 @@ struct DevPlan {
   }
 };
 
+// floor(w * total / n) for 0 <= w <= n <= kMaxItems and total < 2^31, in
+// 32-bit arithmetic: with total = q n + r it is w q + floor(w r / n), and
+// w r < 2^26.  (A 64-bit division is a long instruction sequence that every
+// workgroup would run before its first load.)
+__device__ inline int64_t split_point(int w, int total, int n) {
+  const int q = total / n, r = total - q * n;
+  return (int64_t)w * q + (w * r) / n;
+}
+static_assert(kMaxItems <= (1 << 13), "w r must stay below 2^26");
+
 // The next piece of workgroup w's range [x, xe): the real pages of one row
 // from x on (skipping row padding); advances x past it.  False when the
 // range holds no more real pages.
@@ -194,7 +204,7 @@ __device__ inline bool next_piece(const PL &pl, int hkv, int w, int64_t &x, int6
     ip.sg = pl.seg(lo);
     ip.npages = (ip.sg.ntok + P - 1) / P;
     const int64_t rl = ip.npages + pl.row_pad();
-    ip.g = (int)((x - ip.sg.start) / rl);
+    ip.g = (int)(x - ip.sg.start) / (int)rl; // both below 2^31
     const int64_t rs = ip.sg.start + (int64_t)ip.g * rl;
     if (x - rs >= ip.npages) { // in the row's padding
       x = rs + rl;
@@ -237,8 +247,8 @@ __device__ inline void valu_body(const DecodeStatic &a, const PL &pl) {
 
   const int lane = threadIdx.x;
   if ((int)blockIdx.x >= pl.n_wg()) return;
-  const int64_t x_end = (int64_t)(blockIdx.x + 1) * pl.total() / pl.n_wg();
-  int64_t x_pos = (int64_t)blockIdx.x * pl.total() / pl.n_wg();
+  const int64_t x_end = split_point(blockIdx.x + 1, pl.total(), pl.n_wg());
+  int64_t x_pos = split_point(blockIdx.x, pl.total(), pl.n_wg());
   ItemPos ip;
   while (next_piece(pl, a.hkv, blockIdx.x, x_pos, x_end, ip)) {
   const int b = ip.sg.member(0);
@@ -687,8 +697,8 @@ __device__ inline void mfma_body(const DecodeStatic &a, const PL &pl) {
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6); // uniform in the wave
   const int n = lane & 15, kg = lane >> 4;
   if ((int)blockIdx.x >= pl.n_wg()) return;
-  const int64_t x_end = (int64_t)(blockIdx.x + 1) * pl.total() / pl.n_wg();
-  int64_t x_pos = (int64_t)blockIdx.x * pl.total() / pl.n_wg();
+  const int64_t x_end = split_point(blockIdx.x + 1, pl.total(), pl.n_wg());
+  int64_t x_pos = split_point(blockIdx.x, pl.total(), pl.n_wg());
   ItemPos ip;
   while (next_piece(pl, a.hkv, blockIdx.x, x_pos, x_end, ip)) {
   const int g = ip.g;
