@@ -36,8 +36,14 @@ def _hipcc():
     return path
 
 
+# Per-source additions.  The extend kernels' softmax takes maxima of MFMA
+# results, which are finite or -inf by construction: with NaN operands not
+# honoured, each v_max_f32 needs no canonicalising copy of its inputs.
+SOURCE_FLAGS = {"extend_kernels.hip": ["-fno-honor-nans"]}
+
+
 def _compile(hipcc, src, obj):
-    cmd = [hipcc, *HIP_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    cmd = [hipcc, *HIP_FLAGS, *SOURCE_FLAGS.get(src, []), "-c", os.path.join(CSRC, src), "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"compile failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

@@ -12,7 +12,7 @@
 //               of one KV head); each wave owns 32 rows as two MFMA column
 //               groups of 16.
 //   K/V       = blocks of 64 keys (4 pages), copied global -> LDS by the
-//               gfx950 direct-to-LDS loads (global_load_lds_dwordx4) into a
+//               gfx950 direct-to-LDS buffer loads (16 bytes a lane) into a
 //               double buffer: block b + 1 is in flight while block b is
 //               computed, and no registers hold staging data.  16-byte
 //               chunks are XOR-swizzled within their row so that the MFMA
@@ -90,23 +90,29 @@ template <int D> struct ExtLayout {
   static constexpr int NV = V_ELEMS * 2 / 1024 / 4; // V DMAs per wave per block
 };
 
-// Swizzles: the physical 16-byte chunk of logical chunk c in a row.  A
-// 16-byte LDS read (ds_read_b128) is served half a wave at a time from 128
-// four-byte banks (measured on gfx950 with the bank-conflict counter), so it
-// is conflict-free when the 32 chunks a half-wave reads are distinct modulo
-// 32.  An operand read has lane (n, kg) read logical chunk 4 kc + kg (K) or
-// 4 c2 + kg (V^T) of one of 16 rows picked by n.
-//   K: row = tile_key(t, n) = 32a + 8(n >> 2) + 4h + (n & 3).  With 256-byte
+// LDS layouts.  A 16-byte LDS read (ds_read_b128) is served half a wave at
+// a time from 128 four-byte banks (measured on gfx950 with the
+// bank-conflict counter), so it is conflict-free when the 32 chunks a
+// half-wave reads are distinct modulo 32.
+//   K: one row of D channels per key; an operand read has lane (n, kg) read
+//      logical chunk 4 kc + kg of row tile_key(t, n) = 32a + 8(n >> 2) + 4h
+//      + (n & 3), so chunks are XOR-swizzled within the row.  With 256-byte
 //      rows the key (n & 3) + 4 (n >> 2) = n spreads the 8 rows of each
 //      parity over all 16 slots; with 128-byte rows rows of equal n & 3
 //      share a bank quarter, and 2 (n >> 2) separates them.
-//   V^T: row d = 16 dt + n of 128 bytes; rows of equal n & 3 share a bank
-//      quarter, separated by 2 ((d >> 2) & 3).
+//   V^T: the block's four pages one after another, each as the pool holds
+//      it (D rows of 16 keys, 32 bytes), so a page is copied as it lies.  A
+//      P.V operand read has lane (n, kg) read keys 8 (4 c2 + kg) .. +7 of row
+//      d = 16 dt + n: page 2 c2 + kg / 2, chunk 2 d + kg % 2 of it, which
+//      makes 32 consecutive chunks per half-wave.
 template <int D> __device__ inline int k_phys(int row, int c) {
   if constexpr (D == 128) return c ^ ((row & 3) + 4 * ((row >> 3) & 3));
   else return c ^ (2 * ((row >> 3) & 3));
 }
-__device__ inline int v_phys(int d, int j) { return j ^ (2 * ((d >> 2) & 3)); }
+// Element offset, in a V^T block buffer, of keys 8 j .. 8 j + 7 of row d.
+template <int D> __device__ inline int v_off(int d, int j) {
+  return (j >> 1) * (D * kPage) + d * kPage + 8 * (j & 1);
+}
 
 // The block key held by A row r of S^T tile t (0..3): tiles 2c and 2c + 1
 // cover the 32-key chunk c, row 4 kg + i of tile 2c + h being key
@@ -134,31 +140,39 @@ __device__ inline int32_t pick4(const int32_t (&ids)[4], int q) {
   return (q & 2) ? hi : lo;
 }
 
+// A buffer resource over one page of a pool (the 16-byte loads below are
+// relative to it).
+__device__ inline __amdgpu_buffer_rsrc_t ext_page(const void *page, int bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(page), (short)0, bytes, 0x00020000);
+}
+
 // Global -> LDS (direct) for one block: this wave's share of the K rows and
-// V^T rows.
+// of the V^T pages.  Every copy instruction stays inside one page, whose
+// address the scalar unit forms from its id, so the lanes add only offsets
+// that do not change from block to block.
 template <int D>
 __device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
                                const uint16_t *kbase, const uint16_t *vbase,
                                const int32_t (&ids)[4], int wave, int lane) {
   using Lt = ExtLayout<D>;
+  constexpr int kPageBytes = kPage * D * 2;
+  constexpr int IPP = kPageBytes / 1024; // copy instructions per page
 #pragma unroll
   for (int u = 0; u < Lt::NK; ++u) {
     const int ins = wave * Lt::NK + u;
     const int row = ins * Lt::KROWS + lane / Lt::CH;
     const int c = k_phys<D>(row, lane % Lt::CH); // the swizzle is an involution
-    const int p = (ins * Lt::KROWS) / kPage;     // uniform: a DMA stays in one page
-    __builtin_amdgcn_global_load_lds(
-        kbase + (int64_t)pick4(ids, p) * a.page_stride + (row % kPage) * D + 8 * c,
-        (lds_void *)(sk + ins * 512), 16, 0, 0);
+    const int p = (ins * Lt::KROWS) / kPage;     // uniform: a copy stays in one page
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        ext_page(kbase + (int64_t)pick4(ids, p) * a.page_stride, kPageBytes),
+        (lds_void *)(sk + ins * 512), 16, ((row % kPage) * D + 8 * c) * 2, 0, 0, 0);
   }
 #pragma unroll
   for (int u = 0; u < Lt::NV; ++u) {
     const int ins = wave * Lt::NV + u;
-    const int d = ins * 8 + lane / 8;
-    const int j = v_phys(d, lane % 8);
-    __builtin_amdgcn_global_load_lds(
-        vbase + (int64_t)pick4(ids, j >> 1) * a.page_stride + d * kPage + 8 * (j & 1),
-        (lds_void *)(sv + ins * 512), 16, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(
+        ext_page(vbase + (int64_t)pick4(ids, ins / IPP) * a.page_stride, kPageBytes),
+        (lds_void *)(sv + ins * 512), 16, ((ins % IPP) * 512 + lane * 8) * 2, 0, 0, 0);
   }
 }
 
@@ -180,13 +194,12 @@ __device__ inline void ext_load8(uint2 (&kr)[ExtLayout<D>::NK], uint2 (&vr)[ExtL
     kr[u] = *reinterpret_cast<const uint2 *>(kbase + (int64_t)pick4(ids, p) * a.page_stride +
                                              (row % kPage) * D + 8 * c);
   }
+  constexpr int IPP = kPage * D * 2 / 1024; // bf16 copy instructions per page
 #pragma unroll
   for (int u = 0; u < Lt::NV; ++u) {
     const int ins = wave * Lt::NV + u;
-    const int d = ins * 8 + lane / 8;
-    const int j = v_phys(d, lane % 8);
-    vr[u] = *reinterpret_cast<const uint2 *>(vbase + (int64_t)pick4(ids, j >> 1) * a.page_stride +
-                                             d * kPage + 8 * (j & 1));
+    vr[u] = *reinterpret_cast<const uint2 *>(vbase + (int64_t)pick4(ids, ins / IPP) * a.page_stride +
+                                             (ins % IPP) * 512 + lane * 8);
   }
 }
 template <int D>
@@ -213,7 +226,7 @@ __device__ inline void ext_zero_tail(uint16_t *sv, int blk, int L, int tid) {
     const int d = q >> 3, j = q & 7;
     const int k0 = blk * BK + 8 * j;
     if (k0 + 8 <= L) continue;
-    uint4 *p = reinterpret_cast<uint4 *>(sv + d * BK + 8 * v_phys(d, j));
+    uint4 *p = reinterpret_cast<uint4 *>(sv + v_off<D>(d, j));
     uint4 x = *p;
     uint32_t m[4];
 #pragma unroll
@@ -323,7 +336,7 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
     for (int dt = 0; dt < NDT; ++dt) {
       const int d = 16 * dt + n;
       va[dt] = __builtin_bit_cast(
-          bf16x8_t, *reinterpret_cast<const uint4 *>(sv + d * BK + 8 * v_phys(d, 4 * c2 + kg)));
+          bf16x8_t, *reinterpret_cast<const uint4 *>(sv + v_off<D>(d, 4 * c2 + kg)));
     }
 #pragma unroll
     for (int dt = 0; dt < NDT; ++dt)
