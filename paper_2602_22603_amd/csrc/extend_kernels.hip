@@ -26,9 +26,11 @@
 //               page-transposed V pool, one contiguous 16-byte piece of V^T.
 //               P never moves between lanes.  P is split into bf16 hi + lo
 //               halves (two MFMAs) so the weights keep ~16 bits.
-//   softmax   online, per query row, in log2 units (one v_exp_f32 per score);
-//               row max across the four lane groups by permlane swaps; the
-//               reference max is raised lazily (see kLazy).
+//   softmax   online, per query row, in log2 units (one v_exp_f32 per score)
+//               against a running reference that is raised only when the
+//               weights of a half block could grow too large (see kBig); a
+//               raise takes the half block's row maximum across the four
+//               lane groups by permlane swaps.
 //
 // Work order: workgroup w takes KV head w % Hkv (consecutive workgroups land
 // on different XCDs, so each XCD's L2 serves one head's K/V) and query block
@@ -241,10 +243,13 @@ __device__ inline void ext_zero_tail(uint16_t *sv, int blk, int L, int tid) {
 }
 
 // Softmax state of one lane: two query columns (rows of the attention).  m
-// is the reference maximum in log2 units; it is only raised when a block's
-// maximum exceeds it by more than kLazy, so the O^T rescale is rare and the
-// weights stay below 2^kLazy (exact for the final out = acc / l either way).
-constexpr float kLazy = 8.f;
+// is the reference in log2 units: the weights of a half block (32 keys) are
+// taken as 2^(s - m) against the m in hand, and only when some lane's sum of
+// them reaches kBig (or the row has no reference yet) does the wave raise m
+// to the half block's maximum, rescale O^T and l, and take the weights
+// again.  A weight below 2^64 leaves fp32 room for l and acc over any key
+// count, and out = acc / l does not depend on m.
+constexpr float kBig = 0x1p64f;
 
 // One 64-key block against this wave's 32 query columns.  need_mask: the
 // block reaches past some column's last visible key (the chunk's diagonal,
@@ -288,47 +293,57 @@ __device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, 
           if (key > lim[cg] || key < first[cg] || !((lm >> (4 * tt + i)) & 1)) st[tt][cg][i] = kNegInf;
         }
   }
-  float alpha[2], nm[2];
+  float nm[2];
 #pragma unroll
-  for (int cg = 0; cg < 2; ++cg) {
-    float mx = kNegInf;
-#pragma unroll
-    for (int tt = 0; tt < 4; ++tt)
-      mx = fmaxf(mx, fmaxf(fmaxf(st[tt][cg][0], st[tt][cg][1]), fmaxf(st[tt][cg][2], st[tt][cg][3])));
-    mx = max_xrow16(mx);
-    mx = max_xrow32(mx) * c; // scale > 0: the max commutes with it
-    const float m_new = mx > m_run[cg] + kLazy ? mx : m_run[cg];
-    alpha[cg] = m_new == m_run[cg] ? 1.f : exp2_fast(m_run[cg] - m_new);
-    m_run[cg] = m_new;
-    nm[cg] = m_new == kNegInf ? 0.f : -m_new;
-    l_run[cg] *= alpha[cg];
-  }
-  if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
-#pragma unroll
-    for (int dt = 0; dt < NDT; ++dt)
-#pragma unroll
-      for (int cg = 0; cg < 2; ++cg) acc[dt][cg] *= alpha[cg];
-  }
+  for (int cg = 0; cg < 2; ++cg) nm[cg] = m_run[cg] == kNegInf ? 0.f : -m_run[cg];
 #pragma unroll
   for (int c2 = 0; c2 < 2; ++c2) {
     bf16x8_t phi[2], plo[2];
+    float psum[2];
+    auto weights = [&]() __attribute__((always_inline)) {
 #pragma unroll
-    for (int cg = 0; cg < 2; ++cg) {
-      uint32_t h[4], l[4];
-      float psum = 0.f;
+      for (int cg = 0; cg < 2; ++cg) {
+        uint32_t h[4], l[4];
+        psum[cg] = 0.f;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int tt = 2 * c2 + (e >> 1);
-        const float p0 = exp2_fast(fmaf(st[tt][cg][2 * (e & 1)], c, nm[cg]));
-        const float p1 = exp2_fast(fmaf(st[tt][cg][2 * (e & 1) + 1], c, nm[cg]));
-        h[e] = pack_bf16(p0, p1);
-        l[e] = pack_bf16(p0 - bf_lo(h[e]), p1 - bf_hi(h[e]));
-        psum += p0 + p1;
+        for (int e = 0; e < 4; ++e) {
+          const int tt = 2 * c2 + (e >> 1);
+          const float p0 = exp2_fast(fmaf(st[tt][cg][2 * (e & 1)], c, nm[cg]));
+          const float p1 = exp2_fast(fmaf(st[tt][cg][2 * (e & 1) + 1], c, nm[cg]));
+          h[e] = pack_bf16(p0, p1);
+          l[e] = pack_bf16(p0 - bf_lo(h[e]), p1 - bf_hi(h[e]));
+          psum[cg] += p0 + p1;
+        }
+        phi[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
+        plo[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
       }
-      l_run[cg] += psum;
-      phi[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(h[0], h[1], h[2], h[3]));
-      plo[cg] = __builtin_bit_cast(bf16x8_t, make_uint4(l[0], l[1], l[2], l[3]));
+    };
+    weights();
+    const bool ok = m_run[0] != kNegInf && m_run[1] != kNegInf && psum[0] < kBig && psum[1] < kBig;
+    if (!__all(ok)) { // (wave-uniform) raise the references to this half block's maxima
+      float alpha[2];
+#pragma unroll
+      for (int cg = 0; cg < 2; ++cg) {
+        float mx = kNegInf;
+#pragma unroll
+        for (int tt = 2 * c2; tt < 2 * c2 + 2; ++tt)
+          mx = fmaxf(mx, fmaxf(fmaxf(st[tt][cg][0], st[tt][cg][1]), fmaxf(st[tt][cg][2], st[tt][cg][3])));
+        mx = max_xrow16(mx);
+        mx = max_xrow32(mx) * c; // scale > 0: the max commutes with it
+        const float m_new = fmaxf(m_run[cg], mx);
+        alpha[cg] = m_new == m_run[cg] ? 1.f : exp2_fast(m_run[cg] - m_new); // 0 from -inf
+        m_run[cg] = m_new;
+        nm[cg] = m_new == kNegInf ? 0.f : -m_new;
+        l_run[cg] *= alpha[cg];
+      }
+#pragma unroll
+      for (int dt = 0; dt < NDT; ++dt)
+#pragma unroll
+        for (int cg = 0; cg < 2; ++cg) acc[dt][cg] *= alpha[cg];
+      weights();
     }
+#pragma unroll
+    for (int cg = 0; cg < 2; ++cg) l_run[cg] += psum[cg];
     // all hi products, then all lo: the two MFMAs into one accumulator are
     // 2 * NDT instructions apart
     bf16x8_t va[NDT];
