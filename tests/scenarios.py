@@ -168,11 +168,14 @@ class Twin:
         assert a == b
         return a
 
-    def append(self, h, n, const_v=None, outlier=False):
+    def append(self, h, n, const_v=None, outlier=False, k_scale=1):
         """n seeded tokens; ``outlier`` scales K channels 0-3 and V channels
-        5-8 by 8 (exact in bf16), the outlier-channel shape."""
+        5-8 by 8 (exact in bf16), the outlier-channel shape; ``k_scale`` (a
+        power of two, exact in bf16) scales every key."""
         kb = wl.normal_bf16(self.rng, (self.nl, n, self.hkv, self.d))
         vb = wl.normal_bf16(self.rng, (self.nl, n, self.hkv, self.d))
+        if k_scale != 1:
+            kb = wl.bf16_bits((wl.bf16_value(kb) * k_scale).astype(np.float32))
         if const_v is not None:
             vb[...] = wl.bf16_bits(np.full(vb.shape, const_v, np.float32))
         if outlier:

@@ -108,6 +108,27 @@ def test_extend_several_query_blocks(sq, hq, hkv, d, prefix, n):
     assert err <= TOL
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64)])
+def test_extend_scores_far_above_the_running_reference(sq, hq, hkv, d):
+    """Keys scaled by 16 and by 64 (exact in bf16) after ordinary ones: a
+    row's later scores exceed its running reference by tens and then
+    hundreds of log2 units, so the weights of those half blocks first sum
+    past the 2^64 guard and then overflow to infinity; the kernel must raise
+    the reference and take them again.  Ordinary keys after that carry
+    weights far below it.  Chunks of 256 and 200 tokens cover several query
+    blocks and the chunk's own diagonal."""
+    tw = _twin(sq, hq, hkv, d, 1500, seed=131)
+    a = tw.create()
+    tw.append(a, 400)
+    tw.append(a, 200, k_scale=16)
+    tw.append(a, 150, k_scale=64)
+    tw.append(a, 300)
+    tw.append(a, 256, k_scale=4)
+    err = _extend_error(tw, a, 256)
+    print(f"extend hq={hq} hkv={hkv} d={d} scaled keys: max abs err {err:.2e}")
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("hq,hkv,d,prefix,n", [(32, 8, 128, 20000, 1), (32, 8, 128, 20000, 7),
                                                 (32, 8, 128, 20000, 512), (16, 2, 64, 300, 1000),
                                                 (8, 8, 128, 5000, 130)])
