@@ -14,9 +14,10 @@
 //   K/V       = blocks of 64 keys (4 pages), copied global -> LDS by the
 //               gfx950 direct-to-LDS buffer loads (16 bytes a lane) into a
 //               double buffer: block b + 1 is in flight while block b is
-//               computed, and no registers hold staging data.  16-byte
-//               chunks are XOR-swizzled within their row so that the MFMA
-//               operand reads below are free of bank conflicts.
+//               computed, and no registers hold staging data.  K rows have
+//               their 16-byte chunks XOR-swizzled and V^T keeps the pool's
+//               page layout, so that the MFMA operand reads below are free
+//               of bank conflicts.
 //   S^T       = K . Q^T      v_mfma_f32_16x16x32_bf16 (A = K rows from LDS,
 //                            B = Q^T held in registers for the whole pass)
 //   O^T      += V^T . P^T    v_mfma_f32_16x16x32_bf16 over 32 keys at once.
