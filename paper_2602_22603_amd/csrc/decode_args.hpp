@@ -116,8 +116,27 @@ struct MergeDyn {
   int32_t n_src[kMaxBatch];
 };
 
+// The row lists of a small call's merge, one entry per (batch entry b, KV
+// head g) at index b * kInlineG + g: for each of the entry's sources e, the
+// partial row of its first piece for query head g * G (a workgroup adds its
+// head's offset within the group), and the piece count (bits 0-15) and row
+// step (bits 16-31).  A source past the entry's count has no pieces.  With
+// them, and the grid giving (head in group, KV head, entry), a merge
+// workgroup reads all it needs in one round: each dependent round of
+// argument reads costs a trip to HBM, since the arguments are written anew
+// for every launch.
+struct MergeRows {
+  int32_t base[kMaxSrc];
+  int32_t cnt_step[kMaxSrc];
+};
+constexpr int kInlineRows = 16;
+constexpr int kInlineG = 8; // entry stride: calls with Hkv <= 8 and at most 2 entries
+
 struct MergeArgs {
   MergeStatic st;
+  int32_t n_inline; // 1: rows[b * kInlineG + g] hold the row lists
+  int32_t pad[3];
+  MergeRows rows[kInlineRows];
   MergeDyn dyn;
 };
 

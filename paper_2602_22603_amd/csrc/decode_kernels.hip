@@ -1020,8 +1020,13 @@ struct DevMerge {
 // later steps.  KV8 (with APPEND): the new token is stored as E4M3 codes and
 // joins the softmax as stored (its codes; the K scale is in scale_log2, the
 // V scale in out_scale).
+// The grid is (G, Hkv, batch): workgroup (hr, g, b) merges query head
+// g * G + hr of batch entry b.  With has_inl, rows holds that (b, g)'s row
+// lists (the call carries them in its arguments); else they are derived
+// from the plan.
 template <int D, bool APPEND, class MP, class SA, bool KV8 = false>
-__device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &sa) {
+__device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &sa, bool has_inl,
+                                  const MergeRows &rows) {
   constexpr int NT = 64 * kMergeWaves;
   constexpr int NSH = NT / D; // piece shares
   constexpr int NX = NSH + 2; // the shares, then the sink, then the new token
@@ -1033,14 +1038,30 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
   __shared__ float s_dot[D / 64];
   const int tid = threadIdx.x;
   const int c = tid % D, sh = tid / D;
-  const int b = blockIdx.x / a.hq;
-  const int h = blockIdx.x - b * a.hq;
-  const int g = h / a.group;
-  const int hr = h - g * a.group;
-  const int ns = mp.n_src(b);
+  const int hr = blockIdx.x, g = blockIdx.y, b = blockIdx.z;
+  const int h = g * (int)gridDim.x + hr;
   int cum[kMaxSrc + 1];
   int32_t base[kMaxSrc], step[kMaxSrc];
   cum[0] = 0;
+  // (read before the test, so that they come in the first round of
+  // argument reads whichever way it goes)
+  int32_t ib[kMaxSrc], ics[kMaxSrc];
+#pragma unroll
+  for (int e = 0; e < kMaxSrc; ++e) {
+    ib[e] = rows.base[e];
+    ics[e] = rows.cnt_step[e];
+    __asm__ volatile("" ::"s"(ib[e]), "s"(ics[e]));
+  }
+  if (has_inl) {
+#pragma unroll
+    for (int e = 0; e < kMaxSrc; ++e) {
+      const uint32_t cs = (uint32_t)ics[e];
+      base[e] = ib[e] + hr;
+      step[e] = (int)(cs >> 16);
+      cum[e + 1] = cum[e] + (int)(cs & 0xffff);
+    }
+  } else {
+  const int ns = mp.n_src(b);
 #pragma unroll
   for (int e = 0; e < kMaxSrc; ++e) {
     int cnt = 0;
@@ -1063,6 +1084,7 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
     }
     cum[e + 1] = cum[e] + cnt;
   }
+  } // row lists from the plan
   const int total = cum[kMaxSrc];
   auto row_of = [&](int i) -> int32_t {
     int e = 0;
@@ -1191,20 +1213,25 @@ __device__ inline void merge_body(const MergeStatic &a, const MP &mp, const SA &
   }
 }
 
+__constant__ MergeRows kNoRows = {}; // step merges derive their row lists from the plan
+
 template <int D>
 __global__ __launch_bounds__(64 * kMergeWaves) void k_decode_merge(MergeArgs a) {
-  merge_body<D, false>(a.st, ArgMerge{a.dyn}, 0);
+  // (from the workgroup's own ids: no argument read before this one)
+  const int bg = min((int)(blockIdx.z * kInlineG + blockIdx.y), kInlineRows - 1);
+  merge_body<D, false>(a.st, ArgMerge{a.dyn}, 0, a.n_inline != 0, a.rows[bg]);
 }
 template <int D>
 __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge(StepMergeArgs a) {
   const SQ_CONST StepPlan *plan = (const SQ_CONST StepPlan *)a.plan;
-  if ((int)(blockIdx.x / a.st.hq) >= plan->batch) return; // a replay sized for a larger batch
-  merge_body<D, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a);
+  if ((int)blockIdx.z >= plan->batch) return; // a replay sized for a larger batch
+  merge_body<D, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a, false, kNoRows);
 }
 template <int D> __global__ __launch_bounds__(64 * kMergeWaves) void k_step_merge8(StepMergeArgs a) {
   const SQ_CONST StepPlan *plan = (const SQ_CONST StepPlan *)a.plan;
-  if ((int)blockIdx.x / a.st.hq >= plan->batch) return;
-  merge_body<D, true, DevMerge, StepMergeArgs, true>(a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a);
+  if ((int)blockIdx.z >= plan->batch) return;
+  merge_body<D, true, DevMerge, StepMergeArgs, true>(
+      a.st, DevMerge{a.windowed ? &plan->merge_w : &plan->merge}, a, false, kNoRows);
 }
 
 template <int D, bool NT, bool KV8>
@@ -1351,7 +1378,7 @@ hipError_t launch_decode_mfma(int d, int group, const DecodeArgs &a, hipStream_t
 }
 
 hipError_t launch_decode_merge(int d, int batch, const MergeArgs &a, hipStream_t s) {
-  const dim3 grid(batch * a.st.hq), block(64 * kMergeWaves);
+  const dim3 grid(a.st.group, a.st.hkv, batch), block(64 * kMergeWaves);
   if (d == 128)
     hipLaunchKernelGGL(k_decode_merge<128>, grid, block, 0, s, a);
   else
@@ -1424,7 +1451,7 @@ hipError_t launch_step_mfma(int d, int group, const DecodeStatic &st, const Deco
 }
 
 hipError_t launch_step_merge(int d, int batch, const StepMergeArgs &a, bool kv8, hipStream_t s) {
-  const dim3 grid(batch * a.st.hq), block(64 * kMergeWaves);
+  const dim3 grid(a.st.group, a.st.hkv, batch), block(64 * kMergeWaves);
   if (kv8) {
     if (d == 128)
       hipLaunchKernelGGL(k_step_merge8<128>, grid, block, 0, s, a);

@@ -815,6 +815,35 @@ void fill_dyn(sq_store *s, const Plan &plan, sq::DecodeDyn dyn[2], sq::MergeDyn 
   }
 }
 
+// A small call's merge row lists in the arguments (MergeRows): the same
+// arithmetic the merge kernel does from the plan's tables, done here once.
+void fill_inline_rows(const sq_store *s, int batch, sq::MergeArgs *ma) {
+  const sq::MergeDyn &md = ma->dyn;
+  const int hkv = s->cfg.num_kv_heads;
+  ma->n_inline = 0;
+  if (hkv > sq::kInlineG || (int64_t)batch * sq::kInlineG > sq::kInlineRows) return;
+  for (int b = 0; b < batch; ++b)
+    for (int g = 0; g < hkv; ++g) {
+      sq::MergeRows &r = ma->rows[b * sq::kInlineG + g];
+      for (int e = 0; e < sq::kMaxSrc; ++e) {
+        r.base[e] = 0;
+        r.cnt_step[e] = 0;
+        if (e >= md.n_src[b]) continue;
+        const int sr = (int)((md.src[b][e >> 1] >> (16 * (e & 1))) & 0xffff);
+        const int si = sr & 0xff, member = (sr >> 8) & 0xf;
+        const int L = md.seg_meta[si] & 1, seg = md.seg_meta[si] >> 1;
+        const int np = md.seg_npages[si];
+        const int64_t R = (int64_t)md.seg_start[si] + (int64_t)g * (np + md.row_pad[L]);
+        const int w_lo = sq::wg_of(R, md.total[L], md.n_wg[L]);
+        const int w_hi = sq::wg_of(R + np - 1, md.total[L], md.n_wg[L]);
+        const int rb = md.rb[L];
+        r.base[e] = (md.slot_base[L] + rb * (w_lo + seg * hkv + g)) * sq::kRows + member * s->G;
+        r.cnt_step[e] = (w_hi - w_lo + 1) | (rb * sq::kRows) << 16;
+      }
+    }
+  ma->n_inline = 1;
+}
+
 } // namespace
 
 // ===========================================================================
@@ -1176,6 +1205,7 @@ sq_status decode_call(sq_store *s, int32_t layer, const sq_seq *seqs, int32_t ba
   ma.st = merge_static(s, layer, out, o.sinks, pp);
   sq::DecodeDyn dyn[2]{};
   fill_dyn(s, plan, dyn, &ma.dyn);
+  fill_inline_rows(s, batch, &ma);
   for (int pass = 0; pass < 2; ++pass) {
     da[pass].dyn = dyn[pass];
     if (da[pass].dyn.n_wg == 0) continue;
