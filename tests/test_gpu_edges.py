@@ -234,3 +234,23 @@ def test_tree_of_forks(sq, group):
         info = t.store.plan_info(seqs, sq.ATTN_AUTO)
         assert info["kv_bytes"] < info["kv_bytes_logical"]
         _check(t, seqs)
+
+
+@pytest.mark.parametrize("hq,hkv", [(32, 8), (32, 16), (16, 16)])
+def test_merge_row_lists_in_arguments_and_from_the_plan(sq, hq, hkv):
+    """Calls of one or two entries with at most 8 KV heads carry each (entry,
+    KV head)'s merge row lists in the merge's arguments; three entries, or
+    16 KV heads, derive them from the plan's tables.  Both ways against the
+    oracle in every mode, on a shared prefix whose rows split over many
+    workgroups and private suffixes of a few tokens to a few hundred."""
+    t = sc.Twin(sq, 1, hq, hkv, 64, num_pages=2 * (3100 // 16) + 64, max_seqs=4,
+                max_pages_per_seq=3100 // 16 + 8, seed=173)
+    a = t.create()
+    t.append(a, 3000)
+    b = t.fork(a, 2000)
+    t.append(b, 300)
+    c = t.fork(a, 3000)
+    t.append(c, 17)
+    for seqs in ([a], [b], [a, b], [c, a], [a, b, c]):
+        errs, _ = _check(t, seqs)
+        print(f"hq={hq} hkv={hkv} batch {len(seqs)}:", {m: f"{e:.1e}" for m, e in errs.items()})
