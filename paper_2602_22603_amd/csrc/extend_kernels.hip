@@ -130,10 +130,14 @@ typedef __attribute__((address_space(3))) void lds_void;
 // last page: every key there is at or past L, so its score is masked and its
 // V zeroed before use).  The index is uniform, so these are scalar loads,
 // issued a block ahead of their use.
+// (Read through the constant address space: scalar loads, which the
+// scalar-load counter tracks.  As vector loads, each wait for them would
+// also wait for the block copies in flight, which count on the same
+// in-order vector counter.)
+typedef const int32_t __attribute__((address_space(4))) *ext_sptr_t;
 __device__ inline void block_ids(int32_t (&ids)[4], const ExtendArgs &a, int blk) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
-    ids[i] = __builtin_amdgcn_readfirstlane(a.pt[min(blk * (BK / kPage) + i, a.n_pages - 1)]);
+  for (int i = 0; i < 4; ++i) ids[i] = ((ext_sptr_t)a.pt)[min(blk * (BK / kPage) + i, a.n_pages - 1)];
 }
 
 // ids[q] for a q that may differ per lane, without branches.
@@ -258,7 +262,7 @@ constexpr float kBig = 0x1p64f;
 // slots a deferred eviction masked (lm: bit 4 tt + i = this lane's key
 // tile_key(tt, 4 kg + i) is kept); only then is the per-key test made.
 template <int D>
-__device__ inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, int n, int kg,
+__device__ __attribute__((always_inline)) inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, int n, int kg,
                                  float c, bool need_mask, const bf16x8_t (&qf)[2][D / 32],
                                  const int (&first)[2], const int (&lim)[2], uint32_t lm,
                                  f32x4_t (&acc)[D / 16][2], float (&m_run)[2], float (&l_run)[2]) {
@@ -374,8 +378,12 @@ k_extend(ExtendArgs a) {
   constexpr int NKC = D / 32; // k chunks of S^T = K . Q^T
   constexpr int NDT = D / 16; // 16-channel tiles of O^T
   constexpr int TQ = kExtRows / G;
-  __shared__ __attribute__((aligned(16))) uint16_t sk[2][Lt::K_ELEMS];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[2][Lt::V_ELEMS];
+  // The two buffers are separate LDS objects and the block loop below is
+  // unrolled by two, so every LDS read names its buffer at compile time:
+  // the compiler then knows that the copies in flight into the other
+  // buffer cannot alias it and does not wait for them before the read.
+  __shared__ __attribute__((aligned(16))) uint16_t sk0[Lt::K_ELEMS], sk1[Lt::K_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t sv0[Lt::V_ELEMS], sv1[Lt::V_ELEMS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -433,13 +441,16 @@ k_extend(ExtendArgs a) {
     block_ids(ids, a, b_lo);
     if constexpr (KV8) {
       ext_load8<D>(kr, vr, a, kbase8, vbase8, ids, wave, lane);
-      ext_store8<D>(sk[b_lo & 1], sv[b_lo & 1], kr, vr, wave, lane);
+      ext_store8<D>(sk0, sv0, kr, vr, wave, lane);
     } else {
-      ext_dma<D>(sk[b_lo & 1], sv[b_lo & 1], a, kbase, vbase, ids, wave, lane);
+      ext_dma<D>(sk0, sv0, a, kbase, vbase, ids, wave, lane);
     }
     block_ids(ids, a, b_lo + 1);
   }
-  for (int b = b_lo; b < b_hi; ++b) {
+  // block b (buffers 0 for b - b_lo even, 1 for odd), its copy already
+  // issued; the next block's copy goes to the other buffers
+  auto block = [&](int b, uint16_t *ck, uint16_t *cv, uint16_t *nk, uint16_t *nv)
+                   __attribute__((always_inline)) {
     // keep bits of this lane's 16 keys of the block (deferred evictions)
     uint32_t lm = 0xffffu;
     bool masked_here = false;
@@ -447,7 +458,7 @@ k_extend(ExtendArgs a) {
       int32_t mk[4];
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        mk[i] = __builtin_amdgcn_readfirstlane(a.mask_row[min(b * (BK / kPage) + i, a.n_pages - 1)]);
+        mk[i] = ((ext_sptr_t)a.mask_row)[min(b * (BK / kPage) + i, a.n_pages - 1)];
         masked_here = masked_here || mk[i] != 0xffff;
       }
       if (masked_here) {
@@ -466,23 +477,27 @@ k_extend(ExtendArgs a) {
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     if ((b + 1) * BK > a.L) {
-      ext_zero_tail<D>(sv[b & 1], b, a.L, tid);
+      ext_zero_tail<D>(cv, b, a.L, tid);
       __syncthreads();
     }
     if (b + 1 < b_hi) {
       if constexpr (KV8) {
         ext_load8<D>(kr, vr, a, kbase8, vbase8, ids, wave, lane); // stored after this block
       } else {
-        ext_dma<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], a, kbase, vbase, ids, wave, lane);
+        ext_dma<D>(nk, nv, a, kbase, vbase, ids, wave, lane);
       }
       block_ids(ids, a, b + 2);
     }
-    ext_block<D>(sk[b & 1], sv[b & 1], b, n, kg, a.scale_log2,
+    ext_block<D>(ck, cv, b, n, kg, a.scale_log2,
                  b * BK + BK - 1 > mask_from || b * BK < mask_below || masked_here, qf, first, lim,
                  lm, acc, m_run, l_run);
     if constexpr (KV8) { // the other buffer, which every wave left at the top of this block
-      if (b + 1 < b_hi) ext_store8<D>(sk[(b + 1) & 1], sv[(b + 1) & 1], kr, vr, wave, lane);
+      if (b + 1 < b_hi) ext_store8<D>(nk, nv, kr, vr, wave, lane);
     }
+  };
+  for (int b = b_lo; b < b_hi; b += 2) {
+    block(b, sk0, sv0, sk1, sv1);
+    if (b + 1 < b_hi) block(b + 1, sk1, sv1, sk0, sv0);
   }
 
   if (a.n_split > 1) {
