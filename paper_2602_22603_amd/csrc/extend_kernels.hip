@@ -273,19 +273,26 @@ __device__ __attribute__((always_inline)) inline void ext_block(const uint16_t *
   for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
     for (int cg = 0; cg < 2; ++cg) st[tt][cg] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-  // k chunks outermost: the 8 accumulators of a block are 8 independent
-  // chains, so consecutive MFMAs never wait on each other's result
+  // all the block's K fragments are read first (their LDS latency then
+  // overlaps), k chunks outermost: the 8 accumulators of a block are 8
+  // independent chains, so consecutive MFMAs never wait on each other's result
+  bf16x8_t ka[NKC][4];
 #pragma unroll
   for (int kc = 0; kc < NKC; ++kc)
 #pragma unroll
     for (int tt = 0; tt < 4; ++tt) {
       const int row = tile_key(tt, n);
-      const bf16x8_t ka = __builtin_bit_cast(
+      ka[kc][tt] = __builtin_bit_cast(
           bf16x8_t, *reinterpret_cast<const uint4 *>(sk + row * D + 8 * k_phys<D>(row, 4 * kc + kg)));
+    }
+  __builtin_amdgcn_sched_barrier(0); // (the compiler would move each read back next to its use)
+#pragma unroll
+  for (int kc = 0; kc < NKC; ++kc)
+#pragma unroll
+    for (int tt = 0; tt < 4; ++tt)
 #pragma unroll
       for (int cg = 0; cg < 2; ++cg)
-        st[tt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka, qf[cg][kc], st[tt][cg], 0, 0, 0);
-    }
+        st[tt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kc][tt], qf[cg][kc], st[tt][cg], 0, 0, 0);
   if (need_mask) {
 #pragma unroll
     for (int cg = 0; cg < 2; ++cg)
