@@ -153,34 +153,33 @@ __device__ inline __amdgpu_buffer_rsrc_t ext_page(const void *page, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(page), (short)0, bytes, 0x00020000);
 }
 
-// Global -> LDS (direct) for one block: this wave's share of the K rows and
-// of the V^T pages.  Every copy instruction stays inside one page, whose
-// address the scalar unit forms from its id, so the lanes add only offsets
-// that do not change from block to block.
+// Global -> LDS (direct) for one block: wave w copies page w of the block,
+// its K rows and its V^T, so one page address per wave serves all of its
+// copy instructions (formed by the scalar unit from the page id) and the
+// lanes add offsets that do not change from block to block.
 template <int D>
 __device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
                                const uint16_t *kbase, const uint16_t *vbase,
                                const int32_t (&ids)[4], int wave, int lane) {
   using Lt = ExtLayout<D>;
   constexpr int kPageBytes = kPage * D * 2;
-  constexpr int IPP = kPageBytes / 1024; // copy instructions per page
+  static_assert(Lt::NK * Lt::KROWS == kPage && Lt::NV * 1024 == kPageBytes,
+                "a wave's copies of a block are exactly one page");
+  const int64_t off = (int64_t)pick4(ids, wave) * a.page_stride;
+  const __amdgpu_buffer_rsrc_t kr = ext_page(kbase + off, kPageBytes);
+  const __amdgpu_buffer_rsrc_t vr = ext_page(vbase + off, kPageBytes);
 #pragma unroll
   for (int u = 0; u < Lt::NK; ++u) {
     const int ins = wave * Lt::NK + u;
     const int row = ins * Lt::KROWS + lane / Lt::CH;
     const int c = k_phys<D>(row, lane % Lt::CH); // the swizzle is an involution
-    const int p = (ins * Lt::KROWS) / kPage;     // uniform: a copy stays in one page
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        ext_page(kbase + (int64_t)pick4(ids, p) * a.page_stride, kPageBytes),
-        (lds_void *)(sk + ins * 512), 16, ((row % kPage) * D + 8 * c) * 2, 0, 0, 0);
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(kr, (lds_void *)(sk + ins * 512), 16,
+                                             ((row % kPage) * D + 8 * c) * 2, 0, 0, 0);
   }
 #pragma unroll
-  for (int u = 0; u < Lt::NV; ++u) {
-    const int ins = wave * Lt::NV + u;
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(
-        ext_page(vbase + (int64_t)pick4(ids, ins / IPP) * a.page_stride, kPageBytes),
-        (lds_void *)(sv + ins * 512), 16, ((ins % IPP) * 512 + lane * 8) * 2, 0, 0, 0);
-  }
+  for (int u = 0; u < Lt::NV; ++u)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void *)(sv + (wave * Lt::NV + u) * 512), 16,
+                                             (u * 512 + lane * 8) * 2, 0, 0, 0);
 }
 
 // An 8-bit store: the same block through registers.  ext_load8 loads the 8
