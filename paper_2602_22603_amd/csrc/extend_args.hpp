@@ -9,9 +9,11 @@ namespace sq {
 
 // ---- extend (causal attention of an appended chunk) ------------------------
 // The chunk is the last n of the sequence's L tokens; new token j attends to
-// logical keys 0 .. L - n + j.  A workgroup takes 128 query rows (128 / G
-// tokens x the G query heads of one KV head) against the whole key range.
-constexpr int kExtRows = 128;
+// logical keys 0 .. L - n + j.  A workgroup of kExtWaves waves takes 32
+// query rows per wave (kExtRows / G tokens x the G query heads of one KV
+// head) against the whole key range; one workgroup fits a CU.
+constexpr int kExtWaves = 8;
+constexpr int kExtRows = 32 * kExtWaves;
 constexpr int kExtKeys = 64; // keys per LDS block (4 pages)
 
 struct ExtendArgs {

@@ -5,19 +5,20 @@
 // turn's reasoning, then the tool output).  Each appended token attends to
 // every cached key up to and including itself: the compacted prefix left by
 // Phase 1's eviction and the chunk's earlier tokens.  Unlike decode this is a
-// dense contraction (128 query rows share every K/V tile), so it runs on the
+// dense contraction (256 query rows share every K/V tile), so it runs on the
 // matrix cores:
 //
-//   workgroup = 4 waves, 128 query rows = (128 / G tokens) x (G query heads
-//               of one KV head); each wave owns 32 rows as two MFMA column
-//               groups of 16.
+//   workgroup = 8 waves (one workgroup per CU, two waves per SIMD), 256
+//               query rows = (256 / G tokens) x (G query heads of one KV
+//               head); each wave owns 32 rows as two MFMA column groups of
+//               16.
 //   K/V       = blocks of 64 keys (4 pages), copied global -> LDS by the
-//               gfx950 direct-to-LDS buffer loads (16 bytes a lane) into a
-//               double buffer: block b + 1 is in flight while block b is
-//               computed, and no registers hold staging data.  K rows have
-//               their 16-byte chunks XOR-swizzled and V^T keeps the pool's
-//               page layout, so that the MFMA operand reads below are free
-//               of bank conflicts.
+//               gfx950 direct-to-LDS buffer loads (16 bytes a lane) into
+//               three buffers: blocks b + 1 and b + 2 are in flight while
+//               block b is computed, and no registers hold staging data.  K
+//               rows have their 16-byte chunks XOR-swizzled and V^T keeps
+//               the pool's page layout, so that the MFMA operand reads below
+//               are free of bank conflicts.
 //   S^T       = K . Q^T      v_mfma_f32_16x16x32_bf16 (A = K rows from LDS,
 //                            B = Q^T held in registers for the whole pass)
 //   O^T      += V^T . P^T    v_mfma_f32_16x16x32_bf16 over 32 keys at once.
@@ -45,10 +46,10 @@ namespace sq {
 namespace {
 
 constexpr int BK = kExtKeys;
-constexpr int kThreads = 256;
+constexpr int kThreads = 64 * kExtWaves;
 constexpr float kNegInf = -__builtin_huge_valf();
-// Two waves per SIMD: two workgroups per CU share the matrix cores, so one
-// workgroup's softmax and barriers overlap the other's MFMAs.
+// Two waves per SIMD: the eight waves of the one workgroup a CU holds (up
+// to 256 registers each).
 constexpr int kExtWavesPerEu = 2;
 
 typedef __bf16 bf16x8_t __attribute__((__vector_size__(8 * sizeof(__bf16))));
@@ -89,8 +90,11 @@ template <int D> struct ExtLayout {
   static constexpr int KROWS = 1024 / (2 * D); // K rows one wave-wide DMA writes
   static constexpr int K_ELEMS = BK * D;       // bf16 per K buffer
   static constexpr int V_ELEMS = D * BK;       // bf16 per V^T buffer
-  static constexpr int NK = K_ELEMS * 2 / 1024 / 4; // K DMAs per wave per block
-  static constexpr int NV = V_ELEMS * 2 / 1024 / 4; // V DMAs per wave per block
+  static constexpr int NK = K_ELEMS * 2 / 1024 / kExtWaves; // K DMAs per wave per block
+  static constexpr int NV = V_ELEMS * 2 / 1024 / kExtWaves; // V DMAs per wave per block
+  static constexpr int PW = NK * KROWS;  // a wave's copies cover keys of page (wave * PW) / kPage
+  static_assert(NK * kExtWaves * KROWS == BK && kPage % PW == 0, "a wave's copies stay in one page");
+  static_assert(NV * 1024 == kPage * D * 2 * 4 / kExtWaves, "V^T copies split evenly");
 };
 
 // LDS layouts.  A 16-byte LDS read (ds_read_b128) is served half a wave at
@@ -126,6 +130,18 @@ __device__ inline int tile_key(int t, int r) {
 
 typedef __attribute__((address_space(3))) void lds_void;
 
+// s_waitcnt immediate that waits until at most N vector memory operations
+// are outstanding and leaves the other counters alone (gfx9 encoding:
+// vmcnt in bits 3:0 and 15:14, expcnt 6:4, lgkmcnt 11:8).
+template <int N> constexpr int kVmcntKeep = (N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8);
+
+// A workgroup barrier for LDS written by ordinary stores: this wave's LDS
+// stores complete, then the barrier.  __syncthreads() (and a fence on LDS
+// alone) also waits for every vector memory operation in flight, the block
+// copies into the other buffers included, since they too write LDS.  The
+// memory clobber keeps the compiler from moving memory accesses across it.
+__device__ inline void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
 // Page ids of block blk (4 pages; ids past the sequence's list repeat its
 // last page: every key there is at or past L, so its score is masked and its
 // V zeroed before use).  The index is uniform, so these are scalar loads,
@@ -153,19 +169,18 @@ __device__ inline __amdgpu_buffer_rsrc_t ext_page(const void *page, int bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(page), (short)0, bytes, 0x00020000);
 }
 
-// Global -> LDS (direct) for one block: wave w copies page w of the block,
-// its K rows and its V^T, so one page address per wave serves all of its
-// copy instructions (formed by the scalar unit from the page id) and the
-// lanes add offsets that do not change from block to block.
+// Global -> LDS (direct) for one block: each wave copies a part of one page
+// of the block, K rows and V^T alike, so one page address per wave serves
+// all of its copy instructions (formed by the scalar unit from the page id)
+// and the lanes add offsets that do not change from block to block.
 template <int D>
 __device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
                                const uint16_t *kbase, const uint16_t *vbase,
                                const int32_t (&ids)[4], int wave, int lane) {
   using Lt = ExtLayout<D>;
   constexpr int kPageBytes = kPage * D * 2;
-  static_assert(Lt::NK * Lt::KROWS == kPage && Lt::NV * 1024 == kPageBytes,
-                "a wave's copies of a block are exactly one page");
-  const int64_t off = (int64_t)pick4(ids, wave) * a.page_stride;
+  constexpr int IPP = kPageBytes / 1024; // copy instructions per page
+  const int64_t off = (int64_t)pick4(ids, wave * Lt::PW / kPage) * a.page_stride;
   const __amdgpu_buffer_rsrc_t kr = ext_page(kbase + off, kPageBytes);
   const __amdgpu_buffer_rsrc_t vr = ext_page(vbase + off, kPageBytes);
 #pragma unroll
@@ -177,9 +192,11 @@ __device__ inline void ext_dma(uint16_t *sk, uint16_t *sv, const ExtendArgs &a,
                                              ((row % kPage) * D + 8 * c) * 2, 0, 0, 0);
   }
 #pragma unroll
-  for (int u = 0; u < Lt::NV; ++u)
-    __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void *)(sv + (wave * Lt::NV + u) * 512), 16,
-                                             (u * 512 + lane * 8) * 2, 0, 0, 0);
+  for (int u = 0; u < Lt::NV; ++u) {
+    const int ins = wave * Lt::NV + u;
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(vr, (lds_void *)(sv + ins * 512), 16,
+                                             ((ins % IPP) * 512 + lane * 8) * 2, 0, 0, 0);
+  }
 }
 
 // An 8-bit store: the same block through registers.  ext_load8 loads the 8
@@ -260,11 +277,16 @@ constexpr float kBig = 0x1p64f;
 // or the cache's end) or before some column's first one (a window), or holds
 // slots a deferred eviction masked (lm: bit 4 tt + i = this lane's key
 // tile_key(tt, 4 kg + i) is kept); only then is the per-key test made.
-template <int D>
+// after_scores() runs once the score MFMAs are issued: the caller's scalar
+// loads go there, since while one is in flight (scalar loads return out of
+// order on the counter they share with LDS reads) an MFMA could only wait
+// for all 16 K reads at once instead of for its own.
+template <int D, typename F>
 __device__ __attribute__((always_inline)) inline void ext_block(const uint16_t *sk, const uint16_t *sv, int b, int n, int kg,
                                  float c, bool need_mask, const bf16x8_t (&qf)[2][D / 32],
                                  const int (&first)[2], const int (&lim)[2], uint32_t lm,
-                                 f32x4_t (&acc)[D / 16][2], float (&m_run)[2], float (&l_run)[2]) {
+                                 f32x4_t (&acc)[D / 16][2], float (&m_run)[2], float (&l_run)[2],
+                                 F &&after_scores) {
   constexpr int NKC = D / 32;
   constexpr int NDT = D / 16;
   f32x4_t st[4][2];
@@ -292,6 +314,8 @@ __device__ __attribute__((always_inline)) inline void ext_block(const uint16_t *
 #pragma unroll
       for (int cg = 0; cg < 2; ++cg)
         st[tt][cg] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kc][tt], qf[cg][kc], st[tt][cg], 0, 0, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  after_scores();
   if (need_mask) {
 #pragma unroll
     for (int cg = 0; cg < 2; ++cg)
@@ -384,12 +408,13 @@ k_extend(ExtendArgs a) {
   constexpr int NKC = D / 32; // k chunks of S^T = K . Q^T
   constexpr int NDT = D / 16; // 16-channel tiles of O^T
   constexpr int TQ = kExtRows / G;
-  // The two buffers are separate LDS objects and the block loop below is
-  // unrolled by two, so every LDS read names its buffer at compile time:
-  // the compiler then knows that the copies in flight into the other
-  // buffer cannot alias it and does not wait for them before the read.
-  __shared__ __attribute__((aligned(16))) uint16_t sk0[Lt::K_ELEMS], sk1[Lt::K_ELEMS];
-  __shared__ __attribute__((aligned(16))) uint16_t sv0[Lt::V_ELEMS], sv1[Lt::V_ELEMS];
+  // Three block buffers: block b is read from buffer b % 3 while the copies
+  // of blocks b + 1 and b + 2 land in the other two.  They are separate LDS
+  // objects and the block loop below is unrolled by three, so every LDS
+  // read names its buffer at compile time: the compiler then knows that the
+  // copies in flight cannot alias it and does not wait for them.
+  __shared__ __attribute__((aligned(16))) uint16_t sk0[Lt::K_ELEMS], sk1[Lt::K_ELEMS], sk2[Lt::K_ELEMS];
+  __shared__ __attribute__((aligned(16))) uint16_t sv0[Lt::V_ELEMS], sv1[Lt::V_ELEMS], sv2[Lt::V_ELEMS];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
@@ -443,6 +468,13 @@ k_extend(ExtendArgs a) {
   const uint8_t *vbase8 = reinterpret_cast<const uint8_t *>(a.v) + (int64_t)g * a.head_stride;
   uint2 kr[Lt::NK], vr[Lt::NV]; // an 8-bit store's next block, in flight
   int32_t ids[4];
+  // Copies run two blocks ahead (one for an 8-bit store, whose next block
+  // passes through registers): ids holds the page ids of the next block to
+  // be fetched.  The copies of the two blocks past b_hi are issued too (of
+  // the last page, block_ids clamps) into buffers that no block reads: with
+  // a copy issued at the top of every block, the copies in flight at each
+  // block's top are the same on every path, which the compiler can follow,
+  // and it adds no wait of its own before the LDS reads.
   if (b_lo < b_hi) {
     block_ids(ids, a, b_lo);
     if constexpr (KV8) {
@@ -450,60 +482,81 @@ k_extend(ExtendArgs a) {
       ext_store8<D>(sk0, sv0, kr, vr, wave, lane);
     } else {
       ext_dma<D>(sk0, sv0, a, kbase, vbase, ids, wave, lane);
+      // the query loads, issued before this copy, have landed (said here, on
+      // the only way into the loop, so that the compiler knows it)
+      __builtin_amdgcn_s_waitcnt(kVmcntKeep<Lt::NK + Lt::NV>);
+      block_ids(ids, a, b_lo + 1);
+      ext_dma<D>(sk1, sv1, a, kbase, vbase, ids, wave, lane);
     }
-    block_ids(ids, a, b_lo + 1);
-  }
-  // block b (buffers 0 for b - b_lo even, 1 for odd), its copy already
-  // issued; the next block's copy goes to the other buffers
-  auto block = [&](int b, uint16_t *ck, uint16_t *cv, uint16_t *nk, uint16_t *nv)
-                   __attribute__((always_inline)) {
-    // keep bits of this lane's 16 keys of the block (deferred evictions)
-    uint32_t lm = 0xffffu;
-    bool masked_here = false;
-    if (a.masked) {
-      int32_t mk[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        mk[i] = ((ext_sptr_t)a.mask_row)[min(b * (BK / kPage) + i, a.n_pages - 1)];
-        masked_here = masked_here || mk[i] != 0xffff;
+    block_ids(ids, a, KV8 ? b_lo + 1 : b_lo + 2);
+    // block b from buffers c; buffers n1 and n2 are those of blocks b + 1 and
+    // b + 2 (an 8-bit store uses only two buffers)
+    auto block = [&](int b, uint16_t *ck, uint16_t *cv, uint16_t *n1k, uint16_t *n1v,
+                     uint16_t *n2k, uint16_t *n2v) __attribute__((always_inline)) {
+      // keep bits of this lane's 16 keys of the block (deferred evictions)
+      uint32_t lm = 0xffffu;
+      bool masked_here = false;
+      if (a.masked) {
+        const ext_sptr_t mr = (ext_sptr_t)a.mask_row;
+        const int p0 = b * (BK / kPage), last = a.n_pages - 1;
+        const uint32_t m0 = mr[min(p0, last)], m1 = mr[min(p0 + 1, last)];
+        const uint32_t m2 = mr[min(p0 + 2, last)], m3 = mr[min(p0 + 3, last)];
+        masked_here = (m0 & m1 & m2 & m3) != 0xffffu;
+        if (masked_here) {
+          // bit 4 tt + i is key tile_key(tt, 4 kg + i) = 32 (tt >> 1) + 8 kg
+          // + 4 (tt & 1) + i: page 2 (tt >> 1) + (kg >> 1), slot 8 (kg & 1)
+          // + 4 (tt & 1) + i, so tiles 0, 1 take 8 consecutive slots of page
+          // kg >> 1 and tiles 2, 3 the same slots of page 2 + (kg >> 1)
+          const int sh = 8 * (kg & 1);
+          const uint32_t lo = (kg >> 1) ? m1 : m0, hi = (kg >> 1) ? m3 : m2;
+          lm = ((lo >> sh) & 0xffu) | (((hi >> sh) & 0xffu) << 8);
+        }
       }
-      if (masked_here) {
-        lm = 0;
-#pragma unroll
-        for (int tt = 0; tt < 4; ++tt)
-#pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const int kk = tile_key(tt, 4 * kg + i);
-            lm |= (uint32_t)((pick4(mk, kk >> 4) >> (kk & 15)) & 1) << (4 * tt + i);
-          }
+      // block b has landed (every wave's copies; those of block b + 1, issued
+      // later, may still be in flight) and every wave is done with block
+      // b - 1, whose buffer the next copy overwrites
+      __builtin_amdgcn_s_waitcnt(KV8 ? 0 : kVmcntKeep<Lt::NK + Lt::NV>);
+      lds_barrier();
+      if ((b + 1) * BK > a.L) {
+        ext_zero_tail<D>(cv, b, a.L, tid);
+        lds_barrier();
       }
-    }
-    // block b has landed (every wave's copies) and every wave is done with
-    // block b - 1, whose buffer the next copy overwrites
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if ((b + 1) * BK > a.L) {
-      ext_zero_tail<D>(cv, b, a.L, tid);
-      __syncthreads();
-    }
-    if (b + 1 < b_hi) {
       if constexpr (KV8) {
-        ext_load8<D>(kr, vr, a, kbase8, vbase8, ids, wave, lane); // stored after this block
+        if (b + 1 < b_hi) ext_load8<D>(kr, vr, a, kbase8, vbase8, ids, wave, lane); // stored after this block
       } else {
-        ext_dma<D>(nk, nv, a, kbase, vbase, ids, wave, lane);
+        ext_dma<D>(n2k, n2v, a, kbase, vbase, ids, wave, lane);
       }
-      block_ids(ids, a, b + 2);
+      ext_block<D>(ck, cv, b, n, kg, a.scale_log2,
+                   b * BK + BK - 1 > mask_from || b * BK < mask_below || masked_here, qf, first, lim,
+                   lm, acc, m_run, l_run, [&]() __attribute__((always_inline)) {
+                     if constexpr (KV8) {
+                       if (b + 1 < b_hi) block_ids(ids, a, b + 2);
+                     } else {
+                       block_ids(ids, a, b + 3);
+                     }
+                   });
+      if constexpr (KV8) { // a buffer every wave left by the top of this block
+        if (b + 1 < b_hi) ext_store8<D>(n1k, n1v, kr, vr, wave, lane);
+      }
+    };
+    if constexpr (KV8) {
+      for (int b = b_lo; b < b_hi; b += 2) {
+        block(b, sk0, sv0, sk1, sv1, sk0, sv0);
+        if (b + 1 < b_hi) block(b + 1, sk1, sv1, sk0, sv0, sk1, sv1);
+      }
+    } else {
+      // whole turns of the three buffers, then the rest: the loop's back
+      // edge leaves every block of a turn behind it
+      int b = b_lo;
+      for (; b + 2 < b_hi; b += 3) {
+        block(b, sk0, sv0, sk1, sv1, sk2, sv2);
+        block(b + 1, sk1, sv1, sk2, sv2, sk0, sv0);
+        block(b + 2, sk2, sv2, sk0, sv0, sk1, sv1);
+      }
+      if (b < b_hi) block(b, sk0, sv0, sk1, sv1, sk2, sv2);
+      if (b + 1 < b_hi) block(b + 1, sk1, sv1, sk2, sv2, sk0, sv0);
+      __builtin_amdgcn_s_waitcnt(0); // no copy lands in LDS after the workgroup ends
     }
-    ext_block<D>(ck, cv, b, n, kg, a.scale_log2,
-                 b * BK + BK - 1 > mask_from || b * BK < mask_below || masked_here, qf, first, lim,
-                 lm, acc, m_run, l_run);
-    if constexpr (KV8) { // the other buffer, which every wave left at the top of this block
-      if (b + 1 < b_hi) ext_store8<D>(nk, nv, kr, vr, wave, lane);
-    }
-  };
-  for (int b = b_lo; b < b_hi; b += 2) {
-    block(b, sk0, sv0, sk1, sv1);
-    if (b + 1 < b_hi) block(b + 1, sk1, sv1, sk0, sv0);
   }
 
   if (a.n_split > 1) {

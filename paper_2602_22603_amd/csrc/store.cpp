@@ -2037,14 +2037,14 @@ sq_status sq_extend_attn_ex(sq_store *s, int32_t layer, sq_seq seq, int32_t n_ne
   a.masked = sqn->n_masked > 0 ? 1 : 0;
   if (a.masked && o.window > 0)
     return fail(SQ_ERR_INVALID, "a window over a sequence with masked slots (compact it first)");
-  // A chunk too short to give every CU two rounds of workgroups splits the
-  // key range of each query block (at least 4 blocks of 64 keys per split)
-  // and merges the partial rows in a second launch.
+  // A chunk too short to give every CU two rounds of workgroups (one fits a
+  // CU) splits the key range of each query block (at least 4 blocks of 64
+  // keys per split) and merges the partial rows in a second launch.
   int64_t key_blocks = (sqn->length + sq::kExtKeys - 1) / sq::kExtKeys; // the last query block's
   if (o.window > 0) // a query block's keys span at most W + TQ - 1 indices
     key_blocks = std::min<int64_t>(key_blocks, ((int64_t)o.window + tq - 2) / sq::kExtKeys + 2);
   const int64_t base_wg = (int64_t)a.n_qblocks * a.hkv;
-  const int64_t target = 4LL * s->cus;
+  const int64_t target = 2LL * s->cus;
   int64_t split = 1;
   if (base_wg < target) {
     split = (target + base_wg - 1) / base_wg;
