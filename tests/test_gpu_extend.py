@@ -108,6 +108,23 @@ def test_extend_several_query_blocks(sq, hq, hkv, d, prefix, n):
     assert err <= TOL
 
 
+@pytest.mark.parametrize("hq,hkv,d", [(8, 2, 128), (4, 1, 64)])
+@pytest.mark.parametrize("length", [64, 128, 192, 200, 256, 300, 384, 420])
+def test_extend_key_block_counts(sq, hq, hkv, d, length):
+    """One query block (a 16-token chunk) against 1 to 7 blocks of 64 keys,
+    full and ragged: the kernel cycles its three block buffers a whole turn
+    at a time and takes the last one or two blocks after the loop, so every
+    count of turns and of blocks left over is covered."""
+    n = 16
+    tw = _twin(sq, hq, hkv, d, length, seed=170 + length)
+    a = tw.create()
+    tw.append(a, length - n)
+    tw.append(a, n)
+    err = _extend_error(tw, a, n)
+    print(f"extend hq={hq} hkv={hkv} d={d} length={length}: max abs err {err:.2e}")
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("hq,hkv,d", [(32, 8, 128), (8, 2, 64)])
 def test_extend_scores_far_above_the_running_reference(sq, hq, hkv, d):
     """Keys scaled by 16 and by 64 (exact in bf16) after ordinary ones: a

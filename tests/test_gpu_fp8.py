@@ -178,6 +178,29 @@ def test_fp8_extend(sq, hq, hkv, d, prefix, n, window):
         assert err <= TOL
 
 
+@pytest.mark.parametrize("length", [128, 192, 256, 300])
+def test_fp8_extend_key_block_counts(sq, length):
+    """An 8-bit store's extend over 2 to 5 blocks of 64 keys (its converted
+    copies rotate through the kernel's block buffers like the bf16 ones)."""
+    import math
+    import torch
+    from oracle import extend as oex
+    hq, hkv, d, n = 8, 2, 128, 16
+    t = sc.Twin(sq, 1, hq, hkv, d, length // 16 + 24, 2, length // 16 + 8,
+                seed=780 + length, kv_scales=_scales(1))
+    a = t.create()
+    t.append(a, length - n)
+    t.append(a, n)
+    qb = wl.normal_bf16(t.rng, (n, hq, d))
+    out = t.store.extend(0, a, wl.to_torch_bf16(qb, "cuda"))
+    torch.cuda.synchronize()
+    k, v, _ = t.model.view(a)
+    ref = oex.extend_attention(wl.bf16_value(qb), k[:, 0], v[:, 0], 1 / math.sqrt(d), hq // hkv)
+    err = float(np.max(np.abs(out.cpu().numpy() - ref)))
+    print(f"fp8 extend length={length}: {err:.2e}")
+    assert err <= TOL
+
+
 @pytest.mark.parametrize("mi", [0, 1, 2, 3])
 def test_fp8_steps(sq, mi):
     """Fused decode steps on an 8-bit store: the new token is stored as its
