@@ -203,7 +203,10 @@ typedef struct {
 typedef struct {
   /* Sums of kernel durations (ms) measured with HIP events recorded on the
      store's stream around each launch, over the calls made since profiling
-     was enabled or last read. */
+     was enabled or last read.  evict_scan counts the eviction index kernel
+     where it runs on its own (in-place evictions, or when no page is
+     copied); otherwise the index is written inside the first gather launch
+     and counts in evict_gather. */
   double decode_valu_ms, decode_mfma_ms, decode_merge_ms;
   double evict_scan_ms, evict_gather_ms, append_ms;
   int64_t decode_valu_launches, decode_mfma_launches, decode_merge_launches;

@@ -286,14 +286,41 @@ __device__ inline int span_search(const int32_t *spans, int n_spans, int i) {
   return ans;
 }
 
-__global__ __launch_bounds__(kScanThreads) void k_evict_index(EvictArgs a) {
-  __shared__ int32_t lsp[3 * kInlineSpans];
+// The span list where a workgroup reads it: copied to LDS (lsp, 3 *
+// kInlineSpans ints) from the kernel arguments when it travels there, else
+// the device copy.  Every thread of the workgroup must call it.
+__device__ inline const int32_t *stage_spans(const EvictArgs &a, int32_t *lsp) {
   const bool inl = a.n_spans <= kInlineSpans;
   if (inl)
     for (int i = threadIdx.x; i < 3 * a.n_spans; i += blockDim.x) lsp[i] = a.inl[i];
   __syncthreads();
-  const int32_t *spans = inl ? lsp : a.spans;
-  const int base = blockIdx.x * kScanBlock + threadIdx.x * kPerThread;
+  return inl ? lsp : a.spans;
+}
+
+// The old index of the kept token that lands at new index d: the last span k
+// whose start lies at or before d once the tokens evicted before it are
+// taken out (start_k - before_k <= d; non-decreasing in k) has every span up
+// to it evicted before that token, so it is d + before_k + (end_k - start_k);
+// with no such span it is d.
+__device__ inline int source_of(const int32_t *spans, int n_spans, int d) {
+  int lo = 0, hi = n_spans - 1, k = -1;
+  while (lo <= hi) {
+    const int mid = (lo + hi) >> 1;
+    if (spans[3 * mid] - spans[3 * mid + 2] <= d) {
+      k = mid;
+      lo = mid + 1;
+    } else {
+      hi = mid - 1;
+    }
+  }
+  return k < 0 ? d : d + spans[3 * k + 2] + (spans[3 * k + 1] - spans[3 * k]);
+}
+
+// Block blk (kScanBlock tokens) of the eviction index, by a workgroup of
+// kScanThreads threads (the gather's too).
+static_assert(kScanThreads == 256, "gather workgroups also run index blocks");
+__device__ inline void evict_index_block(const EvictArgs &a, const int32_t *spans, int blk) {
+  const int base = blk * kScanBlock + threadIdx.x * kPerThread;
   if (base >= a.n_tokens) return;
   int s = span_search(spans, a.n_spans, base);
   for (int e = 0; e < kPerThread; ++e) {
@@ -312,6 +339,11 @@ __global__ __launch_bounds__(kScanThreads) void k_evict_index(EvictArgs a) {
     a.dst[i] = d;
     if (!inside) a.src_of[d] = i;
   }
+}
+
+__global__ __launch_bounds__(kScanThreads) void k_evict_index(EvictArgs a) {
+  __shared__ int32_t lsp[3 * kInlineSpans];
+  evict_index_block(a, stage_spans(a, lsp), blockIdx.x);
 }
 
 // Fresh page id number i of an eviction.
@@ -407,11 +439,16 @@ __device__ inline void assemble_v(const Pools &p, int layer, int head, E *vd, co
 // j < P, j below L'.  K rows move as 16-byte units; V^T rows are assembled
 // in LDS from the (at most four, usually one or two) source pages staged
 // whole with 16-byte loads, then written as 16-byte units (more source pages
-// fall back to element moves).  Each comes from token src_of[t] of the old pages, whose ids the
-// page-table row still holds (the new ids are written there after the last
-// gather).  A fresh page is never a page this or a later gather reads: it is
-// either a page nothing held or an old page whose tokens earlier gathers have
-// all moved, so nothing is read after being written.
+// fall back to element moves).  Kept token t comes from old token
+// source_of(t) of the old pages, whose ids the page-table row still holds
+// (the new ids are written there after the last gather).  The first launch
+// of an eviction also writes the eviction index (keep, dst, src_of) in its
+// first index_blocks workgroups, alongside the copies, and takes the
+// sources from the span list so that it does not wait for the index; later
+// launches of a chunked eviction read src_of.  A fresh page is never a page
+// this or a later gather reads: it is either a page nothing held or an old
+// page whose tokens earlier gathers have all moved, so nothing is read after
+// being written.
 template <int D, class E>
 __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   constexpr int U = D * (int)sizeof(E) / 16;      // 16-byte units per K row
@@ -426,30 +463,44 @@ __global__ __launch_bounds__(256) void k_evict_gather(Pools p, GatherArgs a) {
   __shared__ int uidx[P];  // slot j's source page in upage
   __shared__ int n_up;
   __shared__ uint4 vbuf[kMaxSrc][VU];
+  __shared__ int32_t lsp[3 * kInlineSpans];
+  const int n = a.n_new;
+  const int lin = blockIdx.x + blockIdx.y * gridDim.x;
+  // the launch that writes the index takes the sources from the spans; later
+  // launches of a chunked eviction read them from src_of (one round of loads)
+  const bool from_spans = a.index_blocks > 0;
+  const int32_t *spans = from_spans ? stage_spans(a.ev, lsp) : nullptr;
+  if (lin < a.index_blocks) {
+    evict_index_block(a.ev, spans, lin);
+    return;
+  }
   // Work item w = (KV row lh, tail page pl), page fastest.  Workgroups are
   // dealt to the 8 XCDs in turn, so each XCD takes a contiguous range of
   // w: neighbouring destination pages, which share source pages, then hit
-  // the same L2.
-  const int n = gridDim.x;
-  const int total = n * gridDim.y;
-  const int lin = blockIdx.x + blockIdx.y * n;
-  const int x = lin % 8, q = total / 8, r = total % 8;
-  const int w = x * q + min(x, r) + lin / 8;
+  // the same L2.  (Workgroups past the last item, which round the grid up
+  // to whole rows, have nothing to do.)
+  const int total = n * p.nl * p.hkv;
+  const int gl = lin - a.index_blocks;
+  if (gl >= total) return;
+  const int x = gl % 8, q = total / 8, r = total % 8;
+  const int w = x * q + min(x, r) + gl / 8;
   const int pl = w % n;
   const int lh = w / n;
   const int pi = a.pi0 + pl;
   const int layer = lh / p.hkv;
   const int head = lh % p.hkv;
   const int t0 = (a.fp + pi) * P;
+  const int ns = a.ev.n_spans;
+  auto src_of = [&](int t) { return from_spans ? source_of(spans, ns, t) : a.ev.src_of[t]; };
   if (a.remap && t0 + P <= a.new_len) {
-    const int s0 = a.src_of[t0];
-    if (s0 % P == 0 && a.src_of[t0 + P - 1] == s0 + P - 1) return; // remapped, not copied
+    const int s0 = src_of(t0);
+    if (s0 % P == 0 && src_of(t0 + P - 1) == s0 + P - 1) return; // remapped, not copied
   }
   const int dst_page = new_page_id(a.ids, pl);
   if (threadIdx.x < P) {
     const int t = t0 + threadIdx.x;
     if (t < a.new_len) {
-      const int src = a.src_of[t];
+      const int src = src_of(t);
       spage[threadIdx.x] = a.pt_row[src / P];
       sslot[threadIdx.x] = src % P;
       sidx[threadIdx.x] = src / P;
@@ -700,7 +751,10 @@ hipError_t launch_evict_inplace(const Pools &p, const InplaceArgs &a, hipStream_
 
 hipError_t launch_evict_gather(const Pools &p, const GatherArgs &a, hipStream_t s) {
   if (a.n_new == 0) return hipSuccess;
-  dim3 grid(a.n_new, p.nl * p.hkv);
+  // rows of n_new workgroups: the copies' (layer, head) rows, then enough
+  // for the index blocks
+  const int rows = p.nl * p.hkv + (a.index_blocks + a.n_new - 1) / a.n_new;
+  dim3 grid(a.n_new, rows);
   if (p.kv8) {
     if (p.d == 128)
       hipLaunchKernelGGL((k_evict_gather<128, uint8_t>), grid, dim3(256), 0, s, p, a);

@@ -1677,11 +1677,23 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
       if (us != SQ_OK) return us;
     }
     ea.spans = spans_inline ? nullptr : s->ev_upload;
+    // The gathers take each kept token's source from the spans, so the
+    // index (keep, dst, src_of: for the in-place kernel and the debug read)
+    // runs as extra workgroups of the first gather launch; on its own only
+    // when the in-place kernel reads it or no page is copied.
+    bool any_gather = false;
+    if (!inplace)
+      for (const Step &st : steps) any_gather = any_gather || (st.c != 0 && fresh_in(st.k0, st.c) != 0);
     ProfPair pp;
-    bool on = s->prof_begin(strm, &pp, kProfScan);
-    hipError_t e = sq::launch_evict_index(ea, strm);
-    s->prof_end(strm, &pp, on);
-    if (e != hipSuccess) return hip_fail(e, "eviction index");
+    bool on = false;
+    hipError_t e = hipSuccess;
+    if (!any_gather) {
+      on = s->prof_begin(strm, &pp, kProfScan);
+      e = sq::launch_evict_index(ea, strm);
+      s->prof_end(strm, &pp, on);
+      if (e != hipSuccess) return hip_fail(e, "eviction index");
+    }
+    int32_t index_blocks = any_gather ? (int32_t)((L + sq::kScanBlock - 1) / sq::kScanBlock) : 0;
     if (inplace) {
       sq_status is = evict_inplace_launches(s, h, fp, n_new, Lp, src_index, all, strm);
       if (is != SQ_OK) return is;
@@ -1694,7 +1706,9 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
       ga.pi0 = (int32_t)st.k0;
       ga.n_new = (int32_t)st.c;
       ga.new_len = (int32_t)Lp;
-      ga.src_of = s->ev_src;
+      ga.index_blocks = index_blocks;
+      index_blocks = 0; // the first launch writes the index
+      ga.ev = ea;
       ga.pt_row = s->pt_row(h);
       ga.remap = remap ? 1 : 0;
       if (all_inline) {
