@@ -76,8 +76,11 @@ struct GatherArgs {
   int32_t pi0;            // first fresh page (of the tail) this launch fills
   int32_t n_new;          // fresh pages this launch fills; ids[i] is tail page pi0 + i
   int32_t new_len;        // L'
-  int32_t index_blocks;   // > 0: the launch's first index_blocks workgroups write
-                          //      the eviction index (keep, dst, src_of) of ev
+  int32_t index_blocks;   // > 0 (spans in ev.inl only): the launch's first
+                          //      index_blocks workgroups write the eviction
+                          //      index (keep, dst, src_of) of ev, and the
+                          //      others take sources from the spans; 0: the
+                          //      sources are read from ev.src_of
   int32_t pad0;
   EvictArgs ev;           // the spans (each kept token's source comes from them)
   const int32_t *pt_row;  // device page-table row, still holding the old ids

@@ -441,11 +441,12 @@ __device__ inline void assemble_v(const Pools &p, int layer, int head, E *vd, co
 // whole with 16-byte loads, then written as 16-byte units (more source pages
 // fall back to element moves).  Kept token t comes from old token
 // source_of(t) of the old pages, whose ids the page-table row still holds
-// (the new ids are written there after the last gather).  The first launch
-// of an eviction also writes the eviction index (keep, dst, src_of) in its
-// first index_blocks workgroups, alongside the copies, and takes the
-// sources from the span list so that it does not wait for the index; later
-// launches of a chunked eviction read src_of.  A fresh page is never a page
+// (the new ids are written there after the last gather).  When the spans
+// travel in the kernel arguments, the first launch of an eviction also
+// writes the eviction index (keep, dst, src_of) in its first index_blocks
+// workgroups, alongside the copies, and takes the sources from the span
+// list so that it does not wait for the index; later launches of a chunked
+// eviction, and every launch after a separate index kernel, read src_of.  A fresh page is never a page
 // this or a later gather reads: it is either a page nothing held or an old
 // page whose tokens earlier gathers have all moved, so nothing is read after
 // being written.

@@ -1677,23 +1677,36 @@ sq_status sq_evict_spans_ex(sq_store *s, sq_seq h, const int32_t *cursor_ids, in
       if (us != SQ_OK) return us;
     }
     ea.spans = spans_inline ? nullptr : s->ev_upload;
-    // The gathers take each kept token's source from the spans, so the
-    // index (keep, dst, src_of: for the in-place kernel and the debug read)
-    // runs as extra workgroups of the first gather launch; on its own only
-    // when the in-place kernel reads it or no page is copied.
-    bool any_gather = false;
+    // A small first gather launch (one layer's pages, say) takes each kept
+    // token's source from the spans in its kernel arguments, and the index
+    // (keep, dst, src_of: for later gather launches, the in-place kernel and
+    // the debug read) runs as extra workgroups of that launch, which saves
+    // the index kernel and the gap after it (8-9 us).  Searching the spans
+    // lengthens each gather workgroup, though: on the 64K compaction (11K
+    // workgroups) the launch took 39.5 us against 33 us for the gather
+    // alone, a cost that grows with the launch.  So a launch of more than
+    // kFuseIndexMaxWgs workgroups keeps the index kernel, as do the
+    // in-place kernel, an eviction that copies no page, and spans too many
+    // to travel in the arguments; the gathers then read src_of.
+    constexpr int64_t kFuseIndexMaxWgs = 12288;
+    int64_t first_wgs = 0;
     if (!inplace)
-      for (const Step &st : steps) any_gather = any_gather || (st.c != 0 && fresh_in(st.k0, st.c) != 0);
+      for (const Step &st : steps)
+        if (st.c != 0 && fresh_in(st.k0, st.c) != 0) {
+          first_wgs = st.c * (int64_t)s->cfg.num_layers * s->cfg.num_kv_heads;
+          break;
+        }
+    const bool fuse_index = first_wgs > 0 && first_wgs <= kFuseIndexMaxWgs && spans_inline;
     ProfPair pp;
     bool on = false;
     hipError_t e = hipSuccess;
-    if (!any_gather) {
+    if (!fuse_index) {
       on = s->prof_begin(strm, &pp, kProfScan);
       e = sq::launch_evict_index(ea, strm);
       s->prof_end(strm, &pp, on);
       if (e != hipSuccess) return hip_fail(e, "eviction index");
     }
-    int32_t index_blocks = any_gather ? (int32_t)((L + sq::kScanBlock - 1) / sq::kScanBlock) : 0;
+    int32_t index_blocks = fuse_index ? (int32_t)((L + sq::kScanBlock - 1) / sq::kScanBlock) : 0;
     if (inplace) {
       sq_status is = evict_inplace_launches(s, h, fp, n_new, Lp, src_index, all, strm);
       if (is != SQ_OK) return is;
